@@ -1,0 +1,216 @@
+#!/usr/bin/env python3
+"""Benchmark of the FP8 attention hot path on one MI355X.
+
+One step = the whole hot path over one batch of the causal GQA d=128 8K
+workload (B=4, 16 query heads sharing 4 KV heads, N=8192, bf16 inputs with one
+outlier channel x20): quantize Q, K, V, dO (both MX copies) -> forward ->
+matched correction -> backward (dQ, dK, dV).  Inputs are resident in HBM
+before the timed region.
+
+Throughput uses the paper's accounting (App. C.2): credited FLOPs are
+B*Hq*N^2*(dqk+dv) for the forward and B*Hq*N^2*(3 dqk + 2 dv) for the
+backward; the correction pass and the quantizer earn no credit.
+
+Prints one JSON line (see the fields below).  `--gpus N` with N > 1 exits:
+this benchmark measures a single GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP8_TFLOPS = 5000.0      # MI355X dense FP8 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+class HipEvents:
+    """Raw HIP events (timing enabled) via the runtime's C API."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+
+    def create(self, n):
+        evs = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            rc = self.hip.hipEventCreate(ctypes.byref(e))
+            if rc != 0:
+                raise RuntimeError(f"hipEventCreate failed ({rc})")
+            evs.append(e)
+        return evs
+
+    def record(self, e, stream):
+        rc = self.hip.hipEventRecord(e, ctypes.c_void_p(stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+    def ms(self, a, b):
+        out = ctypes.c_float()
+        rc = self.hip.hipEventElapsedTime(ctypes.byref(out), a, b)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return float(out.value)
+
+
+def cpu_baseline(w, d, threads):
+    """The oracle (FP64 C, OpenMP) timed on the host cores on one query head
+    of batch 0 at the full sequence length."""
+    import oracle as orc
+    from paper_2609_37852_amd import synth
+    sl = dict(q=d["q"][:1, :, :1], k=d["k"][:1, :, :1], v=d["v"][:1, :, :1], do=d["do"][:1, :, :1])
+    ws = synth.with_shape(w, B=1, Hq=1, Hkv=1)
+    t = time.perf_counter()
+    orc.attention_from_inputs(sl["q"], sl["k"], sl["v"], sl["do"], float(np.float32(w.tau)), nthreads=threads)
+    dt = time.perf_counter() - t
+    f, b = ws.credited_flops()
+    return dict(value=round((f + b) / dt / 1e12, 6), unit="TFLOP/s", cores=threads, kind="oracle",
+                sample=f"batch 0, query head 0 (KV head 0), N={w.N}: quantize + fwd + matched "
+                       f"delta + bwd in FP64, {dt:.1f} s, credited {(f + b) / 1e9:.1f} GFLOP")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="gqa_d128_8k")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic", default=None, help="JSON file with measured HBM bytes of the bwd kernel")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the hot path runs on a "
+              f"single MI355X; see the sharding notes in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_37852_amd as pk
+    from paper_2609_37852_amd import synth
+
+    w = synth.WORKLOADS[args.workload]
+    d = synth.generate(w, seed=0)
+    dev = torch.device("cuda:0")
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    q, k, v, do = (torch.from_numpy(d[n]).to(tdt).to(dev) for n in ("q", "k", "v", "do"))
+    p = pk.Problem(w.B, w.N, w.Hq, w.Hkv, w.Dqk, w.Dv, float(np.float32(w.tau)))
+    mq, mk, mv, mdo = (pk.MX.empty(*t.shape, dev) for t in (q, k, v, do))
+    o = torch.empty((w.B, w.N, w.Hq, w.Dv), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((w.B, w.Hq, w.N), dtype=torch.float32, device=dev)
+    delta = torch.empty((w.B, w.Hq, w.N, 2), dtype=torch.float32, device=dev)
+    grads = (torch.empty((w.B, w.N, w.Hq, w.Dqk), dtype=torch.bfloat16, device=dev),
+             torch.empty((w.B, w.N, w.Hkv, w.Dqk), dtype=torch.bfloat16, device=dev),
+             torch.empty((w.B, w.N, w.Hkv, w.Dv), dtype=torch.bfloat16, device=dev))
+    ws = torch.empty(pk.attn_fp8_bwd_workspace_size(p), dtype=torch.uint8, device=dev)
+    L = pk.lib()
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    ev = HipEvents()
+
+    def quantize_into(x, m):
+        mc = m.c()
+        st = (ctypes.c_int64 * 3)(x.stride(0), x.stride(1), x.stride(2))
+        rc = L.attn_fp8_quantize(ctypes.c_void_p(x.data_ptr()), 1 if x.dtype == torch.bfloat16 else 0,
+                                 *x.shape, st, ctypes.byref(mc), 3, None, ctypes.c_void_p(stream))
+        if rc != 0:
+            raise RuntimeError(pk.last_error())
+
+    def step(marks=None, mode=pk.DELTA_MATCHING):
+        rec = (lambda i: ev.record(marks[i], stream)) if marks else (lambda i: None)
+        rec(0)
+        for x, m in ((q, mq), (k, mk), (v, mv), (do, mdo)):
+            quantize_into(x, m)
+        rec(1)
+        pk.attn_fp8_fwd(p, mq, mk, mv, o=o, lse=lse)
+        rec(2)
+        pk.attn_fp8_delta(p, mode, mq, mk, mv, mdo, lse, do, o, delta=delta)
+        rec(3)
+        pk.attn_fp8_bwd(p, mode, mq, mk, mv, mdo, lse, do, o, delta_in=delta, workspace=ws, out=grads,
+                        main_events=(marks[4].value, marks[5].value) if marks else None)
+        rec(6)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    marks = [ev.create(7) for _ in range(args.steps)]
+    t0, t1 = ev.create(2)
+    torch.cuda.synchronize()
+    ev.record(t0, stream)
+    for i in range(args.steps):
+        step(marks[i])
+    ev.record(t1, stream)
+    torch.cuda.synchronize()
+    total_ms = ev.ms(t0, t1)
+    ms_per_step = total_ms / args.steps
+
+    def avg(a, b):
+        return float(np.mean([ev.ms(m[a], m[b]) for m in marks]))
+
+    t_quant, t_fwd, t_delta = avg(0, 1), avg(1, 2), avg(2, 3)
+    t_bwd_main, t_bwd_call = avg(4, 5), avg(3, 6)
+
+    # the stale-rowsum correction, timed the same way, for the pre-pass ratio
+    smarks = [ev.create(7) for _ in range(3)]
+    for m in smarks:
+        step(m, mode=pk.DELTA_STALE_ROWSUM)
+    torch.cuda.synchronize()
+    t_delta_stale = float(np.mean([ev.ms(m[2], m[3]) for m in smarks]))
+
+    fwd_f, bwd_f = w.credited_flops()
+    credited = fwd_f + bwd_f
+    value = credited / (ms_per_step * 1e-3) / 1e12
+    paper_ms = t_fwd + t_delta + t_bwd_call
+    achieved = bwd_f / (t_bwd_main * 1e-3) / 1e12
+    traffic = None
+    if args.traffic and os.path.exists(args.traffic):
+        traffic = json.load(open(args.traffic)).get("bytes_per_launch")
+    quant_bytes = 4.0625 * sum(t.numel() for t in (q, k, v, do))   # bf16 in, two fp8 copies + scales out
+
+    line = {
+        "metric": "FP8 attention fwd+bwd TFLOP/s and % of FP8 MFMA peak (causal GQA d128, 8K)",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8_e4m3",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.B, "seqlen": w.N, "heads_q": w.Hq, "heads_kv": w.Hkv,
+                   "dim_qk": w.Dqk, "dim_v": w.Dv, "causal": True, "delta_mode": "matching",
+                   "inputs": "bf16, one outlier channel x20 in Q and K", "step": "quantize+fwd+delta+bwd"},
+        "pct_of_fp8_peak": round(100.0 * value / PEAK_FP8_TFLOPS, 2),
+        "breakdown_ms": {"quantize": round(t_quant, 4), "fwd": round(t_fwd, 4), "delta_matching": round(t_delta, 4),
+                         "delta_stale_rowsum": round(t_delta_stale, 4), "bwd_main_kernel": round(t_bwd_main, 4),
+                         "bwd_call": round(t_bwd_call, 4)},
+        "paper_accounting": {"fwd_tflops": round(fwd_f / (t_fwd * 1e-3) / 1e12, 2),
+                             "bwd_tflops_incl_delta": round(bwd_f / ((t_delta + t_bwd_call) * 1e-3) / 1e12, 2),
+                             "fwd_bwd_tflops_prequantized": round(credited / (paper_ms * 1e-3) / 1e12, 2),
+                             "pct_of_fp8_peak_prequantized": round(100 * credited / (paper_ms * 1e-3) / 1e12 /
+                                                                   PEAK_FP8_TFLOPS, 2),
+                             "delta_over_bwd_main": round(t_delta / t_bwd_main, 4),
+                             "delta_over_delta_plus_bwd": round(t_delta / (t_delta + t_bwd_call), 4)},
+        "quantize_hbm_gbs": round(quant_bytes / (t_quant * 1e-3) / 1e9, 1),
+        "roofline": {"kernel": "bwd_kernel<128,128>", "bound": "mfma", "achieved": round(achieved, 2),
+                     "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP8_TFLOPS, 4),
+                     "traffic": traffic},
+    }
+    if not args.no_cpu_baseline:
+        threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+        line["cpu_baseline"] = cpu_baseline(w, d, threads)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,174 @@
+/*
+ * attn_fp8.h -- C ABI of the gfx950 (MI355X) block-scaled FP8 attention
+ * library with Delta-Matching.
+ *
+ * Method: "Delta-Matching: Closing the Final Gap of Native 8-bit Training for
+ * LLMs".  Causal softmax attention (Sec. 2.3) whose seven matrix products all
+ * take FP8 (E4M3) operands with power-of-two (E8M0) block scales, and whose
+ * backward row correction is the matched correction
+ *     delta_i = sum_j P_ij dP_ij            (Sec. 3.4)
+ * computed from the unquantized probabilities and the FP32 products of the
+ * FP8 backward operands, in place of the saved-output shortcut
+ * sum_c dO_ic O_ic (Sec. 3.2, still available as DELTA_STALE_ROWSUM).
+ * Kernel numerics follow App. B.6, with power-of-two block scales:
+ *   - FP8 is OCP E4M3FN, round to nearest even; a block's scale is 2^e with e
+ *     the smallest integer such that max|x| <= 448 * 2^e (e in [-127, 127]).
+ *   - Every input X in {Q, K, V, dO} has two MX copies made from its source
+ *     values: a "row" copy in 1x32 blocks along head_dim (operand of the
+ *     products that contract head_dim: S = Q K^T, dP = dO V^T) and a "col"
+ *     copy in 32x1 blocks along the sequence (operand of the products that
+ *     contract the sequence: O = P V, dV = P^T dO, dK = dS^T Q, dQ = dS K).
+ *   - Forward probabilities are cast per query row and aligned 32-key group
+ *     with a power-of-two scale; the normalizer uses the values before the
+ *     cast.  Backward probabilities for dV use the fixed scale 2^-8; dS is
+ *     cast in aligned 32x32 (query x key) blocks shared by dQ and dK.
+ *
+ * Conventions (all entry points):
+ *   - Every pointer argument named as device memory is a device (HBM)
+ *     address owned by the caller; the library never allocates or frees
+ *     device memory and keeps no state between calls, apart from the
+ *     thread-local error text.
+ *   - Work is enqueued on `stream` and the call returns without
+ *     synchronizing; faults inside a kernel surface at the caller's next
+ *     synchronization.
+ *   - Return value 0 on success, else a negative attn_fp8_status; on error
+ *     nothing is launched and attn_fp8_last_error() describes the problem.
+ *   - Causal masking is top-left aligned: key j is visible to query i iff
+ *     j <= i (equal query and key lengths).  GQA: query head h reads KV head
+ *     floor(h / (heads_q / heads_kv)).  MLA-style problems use
+ *     dim_qk != dim_v with heads_q == heads_kv.
+ *   - Supported geometry: seqlen % 32 == 0 (seqlen may be 0), dim_qk in
+ *     {64, 128, 192, 256}, dim_v in {64, 128, 256} with (dim_qk, dim_v) in
+ *     {(64,64), (128,128), (256,256), (192,128)}, heads_q % heads_kv == 0.
+ *     Batch or head counts of 0 are valid empty problems.
+ *   - Strides are in elements; the last (channel) dimension is contiguous.
+ *     Device pointers must be 16-byte aligned, and every stride times the
+ *     element size must be a multiple of 16 bytes.
+ */
+#ifndef ATTN_FP8_H
+#define ATTN_FP8_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ATTN_FP8_OK = 0,
+  ATTN_FP8_EINVAL = -1,        /* NULL pointer, bad shape, stride or dtype */
+  ATTN_FP8_EUNSUPPORTED = -2,  /* valid request outside the supported geometry */
+  ATTN_FP8_EALIGN = -3,        /* pointer or stride not 16-byte aligned */
+  ATTN_FP8_EWORKSPACE = -4,    /* workspace missing or smaller than required */
+  ATTN_FP8_EHIP = -5           /* the HIP runtime rejected a launch */
+} attn_fp8_status;
+
+typedef enum { ATTN_FP8_DTYPE_F32 = 0, ATTN_FP8_DTYPE_BF16 = 1 } attn_fp8_dtype;
+
+typedef enum {
+  ATTN_FP8_DELTA_MATCHING = 0,      /* delta_i = sum_j P_ij dP_ij / sum_j P_ij (Sec. 3.4) */
+  ATTN_FP8_DELTA_STALE_ROWSUM = 1   /* delta_i = sum_c dO_ic O_ic (Sec. 3.2)            */
+} attn_fp8_delta_mode;
+
+enum { ATTN_FP8_QUANT_ROW = 1, ATTN_FP8_QUANT_COL = 2, ATTN_FP8_QUANT_BOTH = 3 };
+
+/* Problem geometry, read-only.  softmax_scale (tau, e.g. 1/sqrt(dim_qk))
+ * multiplies the FP32 score accumulator S = Q K^T. */
+typedef struct {
+  int64_t batch, seqlen, heads_q, heads_kv, dim_qk, dim_v;
+  int32_t causal;          /* must be 1 */
+  float softmax_scale;
+} attn_fp8_problem;
+
+/* One MX-quantized operand X of shape [B, N, H, D]; device memory, caller-owned.
+ *   code_row  [B, H, N, D]     E4M3FN codes, 1x32 blocks along D
+ *   scale_row [B, H, N, D/32]  E8M0 bytes (value 2^(byte-127))
+ *   code_col  [B, H, D, N]     E4M3FN codes, 32x1 blocks along N
+ *   scale_col [B, H, D, N/32]  E8M0 bytes
+ * A copy that an entry point does not read may be NULL. */
+typedef struct {
+  uint8_t* code_row;
+  uint8_t* scale_row;
+  uint8_t* code_col;
+  uint8_t* scale_col;
+} attn_fp8_mx;
+
+/* Input quantizer (App. B.6.1 with power-of-two 1x32 / 32x1 blocks).
+ *   x        device, [B, N, H, D] of x_dtype with element strides
+ *            strides = {stride_b, stride_n, stride_h}; channel stride 1.
+ *   out      receives the copies selected by `which` (ATTN_FP8_QUANT_*).
+ *   nonfinite_count  nullable device uint32: incremented by the number of
+ *            non-finite inputs seen (codes for them are NaN codes).  The
+ *            caller zeroes it.
+ * D must be one of 64, 128, 192, 256; N % 32 == 0. */
+int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, int64_t D,
+                      const int64_t strides[3], const attn_fp8_mx* out, int which,
+                      uint32_t* nonfinite_count, hipStream_t stream);
+
+/* Forward (Sec. 2.3; App. B.6.2): S = tau * Q K^T, online softmax with
+ * power-of-two rescaling, FP8 probabilities per 32-key group, O = P V / l.
+ *   q, k     row copies used;  v  col copy used.
+ *   o        device, [B, N, Hq, Dv] of o_dtype, strides o_strides {b, n, h}.
+ *   lse      device float [B, Hq, N]: natural-log LSE_i = m_i + ln l_i. */
+int attn_fp8_fwd(const attn_fp8_problem* p, const attn_fp8_mx* q, const attn_fp8_mx* k,
+                 const attn_fp8_mx* v, void* o, int o_dtype, const int64_t o_strides[3],
+                 float* lse, hipStream_t stream);
+
+/* Row correction (Sec. 3.4 / Sec. 3.2; App. B.6.3 "Matched correction").
+ *   MATCHING:     reads q, k, v, dout row copies and lse; recomputes
+ *                 P = 2^(S log2 e - LSE log2 e) and dP = dO_q V_q^T in FP32,
+ *                 reduces sum P dP and sum P in FP32 per 32-key group, then
+ *                 in FP64, and stores delta = num / den.
+ *   STALE_ROWSUM: reads dout_raw [B,N,Hq,Dv] (dout_dtype, strides
+ *                 dout_strides) and the stored output o (o_dtype,
+ *                 o_strides); delta = sum_c dO_ic O_ic in FP32.
+ * Pointers the mode does not read may be NULL.
+ *   delta    device float [B, Hq, N, 2]: (hi, lo) with delta ~= hi + lo
+ *            (lo = 0 for STALE_ROWSUM). */
+int attn_fp8_delta(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q,
+                   const attn_fp8_mx* k, const attn_fp8_mx* v, const attn_fp8_mx* dout,
+                   const float* lse, const void* dout_raw, int dout_dtype,
+                   const int64_t dout_strides[3], const void* o, int o_dtype,
+                   const int64_t o_strides[3], float* delta, hipStream_t stream);
+
+/* Workspace bytes attn_fp8_bwd needs for this problem (FP32 dQ accumulator
+ * plus the internal delta buffer).  Returns 0 / negative status. */
+int attn_fp8_bwd_workspace_size(const attn_fp8_problem* p, size_t* bytes);
+
+/* Backward (Sec. 2.3; App. B.6.3).  Key-major pass: recompute S, P, dP;
+ * dS = P ((dP - hi) - lo); P' = C8(256 P) 2^-8; dS' cast per 32x32 block;
+ * dV += P'^T dO_col, dK += dS'^T Q_col (summed over the KV group in FP32),
+ * dQ += dS' K_col (FP32 accumulation in the workspace); then dQ, dK are
+ * multiplied by tau and stored.
+ *   delta_in nullable device float [B, Hq, N, 2]: when given, used as the
+ *            correction (and delta_mode is ignored); else the correction is
+ *            computed first per delta_mode, exactly as attn_fp8_delta does.
+ *   dq [B,N,Hq,Dqk], dk [B,N,Hkv,Dqk], dv [B,N,Hkv,Dv]: device, grad_dtype,
+ *            element strides {b, n, h} in dq_strides / dk_strides / dv_strides.
+ *   workspace device, at least attn_fp8_bwd_workspace_size() bytes, 256-byte
+ *            aligned; contents on entry are ignored.
+ *   rowstats nullable device double [B, Hq, N, 4], zeroed by the caller:
+ *            accumulates, per query row and over all keys, sum dS, sum |dS|
+ *            and sum dS' (FP64 sums of the FP32 values before / after the
+ *            cast) and max |dS| (debug instrumentation of App. C.1; slower).
+ *   main_events nullable pointer to two events: recorded on `stream`
+ *            immediately before and after the main backward kernel, so a
+ *            caller can time that kernel alone. */
+int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q,
+                 const attn_fp8_mx* k, const attn_fp8_mx* v, const attn_fp8_mx* dout,
+                 const float* lse, const void* dout_raw, int dout_dtype,
+                 const int64_t dout_strides[3], const void* o, int o_dtype,
+                 const int64_t o_strides[3], const float* delta_in, void* dq, void* dk, void* dv,
+                 int grad_dtype, const int64_t dq_strides[3], const int64_t dk_strides[3],
+                 const int64_t dv_strides[3], void* workspace, size_t workspace_bytes,
+                 double* rowstats, const hipEvent_t* main_events, hipStream_t stream);
+
+/* Thread-local text describing the last error returned on this thread. */
+const char* attn_fp8_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ATTN_FP8_H */

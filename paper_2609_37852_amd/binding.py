@@ -1,0 +1,221 @@
+"""ctypes binding of libattn_fp8.so (include/attn_fp8.h).
+
+Argument marshalling only: torch supplies device memory and the current HIP
+stream; every step of the computation runs in the library's kernels.  There
+is no fallback: if the library is not built, or a call fails, an exception is
+raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libattn_fp8.so")
+
+DTYPE_F32, DTYPE_BF16 = 0, 1
+DELTA_MATCHING, DELTA_STALE_ROWSUM = 0, 1
+QUANT_ROW, QUANT_COL, QUANT_BOTH = 1, 2, 3
+STATUS = {0: "OK", -1: "EINVAL", -2: "EUNSUPPORTED", -3: "EALIGN", -4: "EWORKSPACE", -5: "EHIP"}
+EXPORTS = ("attn_fp8_quantize", "attn_fp8_fwd", "attn_fp8_delta", "attn_fp8_bwd_workspace_size",
+           "attn_fp8_bwd", "attn_fp8_last_error")
+
+
+class AttnFp8Error(RuntimeError):
+    def __init__(self, fn, code, msg):
+        super().__init__(f"{fn} failed: {STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int64), ("seqlen", ctypes.c_int64), ("heads_q", ctypes.c_int64),
+                ("heads_kv", ctypes.c_int64), ("dim_qk", ctypes.c_int64), ("dim_v", ctypes.c_int64),
+                ("causal", ctypes.c_int32), ("softmax_scale", ctypes.c_float)]
+
+
+class _MX(ctypes.Structure):
+    _fields_ = [("code_row", ctypes.c_void_p), ("scale_row", ctypes.c_void_p),
+                ("code_col", ctypes.c_void_p), ("scale_col", ctypes.c_void_p)]
+
+
+_I64x3 = ctypes.c_int64 * 3
+_LIB = None
+
+
+def lib():
+    """Load the library (built by paper_2609_37852_amd.build / __graft_entry__.build)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2609_37852_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
+        P = ctypes.POINTER
+        L.attn_fp8_quantize.argtypes = [vp, i32, i64, i64, i64, i64, P(ctypes.c_int64), P(_MX), i32, vp, vp]
+        L.attn_fp8_fwd.argtypes = [P(_Problem), P(_MX), P(_MX), P(_MX), vp, i32, P(ctypes.c_int64), vp, vp]
+        L.attn_fp8_delta.argtypes = [P(_Problem), i32, P(_MX), P(_MX), P(_MX), P(_MX), vp, vp, i32,
+                                     P(ctypes.c_int64), vp, i32, P(ctypes.c_int64), vp, vp]
+        L.attn_fp8_bwd_workspace_size.argtypes = [P(_Problem), P(sz)]
+        L.attn_fp8_bwd.argtypes = [P(_Problem), i32, P(_MX), P(_MX), P(_MX), P(_MX), vp, vp, i32,
+                                   P(ctypes.c_int64), vp, i32, P(ctypes.c_int64), vp, vp, vp, vp, i32,
+                                   P(ctypes.c_int64), P(ctypes.c_int64), P(ctypes.c_int64), vp, sz, vp, vp, vp]
+        L.attn_fp8_last_error.restype = ctypes.c_char_p
+        for name in EXPORTS[:-1]:
+            getattr(L, name).restype = ctypes.c_int
+        _LIB = L
+    return _LIB
+
+
+def last_error() -> str:
+    return lib().attn_fp8_last_error().decode()
+
+
+def _check(fn, rc):
+    if rc != 0:
+        raise AttnFp8Error(fn, rc, last_error())
+
+
+def _stream(device=None):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _dtype_code(dt):
+    if dt == torch.bfloat16:
+        return DTYPE_BF16
+    if dt == torch.float32:
+        return DTYPE_F32
+    raise ValueError(f"unsupported dtype {dt}")
+
+
+def _strides_bnh(t):
+    assert t.dim() == 4 and t.stride(3) == 1, "expected [B, N, H, D] with contiguous channels"
+    return _I64x3(t.stride(0), t.stride(1), t.stride(2))
+
+
+@dataclass
+class Problem:
+    batch: int
+    seqlen: int
+    heads_q: int
+    heads_kv: int
+    dim_qk: int
+    dim_v: int
+    softmax_scale: float
+    causal: int = 1
+
+    def c(self):
+        return _Problem(self.batch, self.seqlen, self.heads_q, self.heads_kv, self.dim_qk, self.dim_v,
+                        self.causal, self.softmax_scale)
+
+
+@dataclass
+class MX:
+    """MX copies of one operand X[B, N, H, D] (device uint8 tensors)."""
+    code_row: torch.Tensor | None
+    scale_row: torch.Tensor | None
+    code_col: torch.Tensor | None
+    scale_col: torch.Tensor | None
+
+    def c(self):
+        return _MX(*(t.data_ptr() if t is not None else None
+                     for t in (self.code_row, self.scale_row, self.code_col, self.scale_col)))
+
+    @staticmethod
+    def empty(B, N, H, D, device, which=QUANT_BOTH):
+        u8 = dict(dtype=torch.uint8, device=device)
+        row = which & QUANT_ROW
+        col = which & QUANT_COL
+        return MX(torch.empty((B, H, N, D), **u8) if row else None,
+                  torch.empty((B, H, N, D // 32), **u8) if row else None,
+                  torch.empty((B, H, D, N), **u8) if col else None,
+                  torch.empty((B, H, D, N // 32), **u8) if col else None)
+
+
+def attn_fp8_quantize(x: torch.Tensor, which: int = QUANT_BOTH, nonfinite: torch.Tensor | None = None) -> MX:
+    """x: [B, N, H, D] bf16/f32 on the GPU -> MX copies (App. B.6.1)."""
+    B, N, H, D = x.shape
+    out = MX.empty(B, N, H, D, x.device, which)
+    m = out.c()
+    _check("attn_fp8_quantize",
+           lib().attn_fp8_quantize(_ptr(x), _dtype_code(x.dtype), B, N, H, D, _strides_bnh(x), ctypes.byref(m),
+                                   which, _ptr(nonfinite), _stream(x.device)))
+    return out
+
+
+def attn_fp8_fwd(p: Problem, q: MX, k: MX, v: MX, o_dtype=torch.bfloat16, o: torch.Tensor | None = None,
+                 lse: torch.Tensor | None = None):
+    dev = q.code_row.device
+    if o is None:
+        o = torch.empty((p.batch, p.seqlen, p.heads_q, p.dim_v), dtype=o_dtype, device=dev)
+    if lse is None:
+        lse = torch.empty((p.batch, p.heads_q, p.seqlen), dtype=torch.float32, device=dev)
+    pc, qc, kc, vc = p.c(), q.c(), k.c(), v.c()
+    _check("attn_fp8_fwd", lib().attn_fp8_fwd(ctypes.byref(pc), ctypes.byref(qc), ctypes.byref(kc), ctypes.byref(vc),
+                                              _ptr(o), _dtype_code(o.dtype), _strides_bnh(o), _ptr(lse),
+                                              _stream(dev)))
+    return o, lse
+
+
+def _opt_mx(m):
+    return ctypes.byref(m.c()) if m is not None else None
+
+
+def attn_fp8_delta(p: Problem, mode: int, q: MX | None = None, k: MX | None = None, v: MX | None = None,
+                   dout: MX | None = None, lse=None, dout_raw=None, o=None, delta: torch.Tensor | None = None):
+    dev = (q.code_row if q is not None else dout_raw).device
+    if delta is None:
+        delta = torch.empty((p.batch, p.heads_q, p.seqlen, 2), dtype=torch.float32, device=dev)
+    pc = p.c()
+    mxs = [m.c() if m is not None else None for m in (q, k, v, dout)]
+    refs = [ctypes.byref(m) if m is not None else None for m in mxs]
+    ds = _strides_bnh(dout_raw) if dout_raw is not None else None
+    os_ = _strides_bnh(o) if o is not None else None
+    _check("attn_fp8_delta", lib().attn_fp8_delta(
+        ctypes.byref(pc), mode, *refs, _ptr(lse), _ptr(dout_raw),
+        _dtype_code(dout_raw.dtype) if dout_raw is not None else 0, ds, _ptr(o),
+        _dtype_code(o.dtype) if o is not None else 0, os_, _ptr(delta), _stream(dev)))
+    return delta
+
+
+def attn_fp8_bwd_workspace_size(p: Problem) -> int:
+    n = ctypes.c_size_t(0)
+    pc = p.c()
+    _check("attn_fp8_bwd_workspace_size", lib().attn_fp8_bwd_workspace_size(ctypes.byref(pc), ctypes.byref(n)))
+    return n.value
+
+
+def attn_fp8_bwd(p: Problem, mode: int, q: MX, k: MX, v: MX, dout: MX, lse, dout_raw=None, o=None,
+                 delta_in=None, grad_dtype=torch.bfloat16, rowstats: bool = False, workspace=None, out=None,
+                 main_events=None):
+    """Returns (dq, dk, dv, rowstats or None).  main_events: optional pair of
+    raw hipEvent_t handles recorded around the main backward kernel."""
+    dev = q.code_row.device
+    if out is None:
+        dq = torch.empty((p.batch, p.seqlen, p.heads_q, p.dim_qk), dtype=grad_dtype, device=dev)
+        dk = torch.empty((p.batch, p.seqlen, p.heads_kv, p.dim_qk), dtype=grad_dtype, device=dev)
+        dv = torch.empty((p.batch, p.seqlen, p.heads_kv, p.dim_v), dtype=grad_dtype, device=dev)
+    else:
+        dq, dk, dv = out
+    ws_bytes = attn_fp8_bwd_workspace_size(p)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    rs = torch.zeros((p.batch, p.heads_q, p.seqlen, 4), dtype=torch.float64, device=dev) if rowstats else None
+    pc = p.c()
+    mxs = [m.c() for m in (q, k, v, dout)]
+    ds = _strides_bnh(dout_raw) if dout_raw is not None else None
+    os_ = _strides_bnh(o) if o is not None else None
+    _check("attn_fp8_bwd", lib().attn_fp8_bwd(
+        ctypes.byref(pc), mode, *[ctypes.byref(m) for m in mxs], _ptr(lse), _ptr(dout_raw),
+        _dtype_code(dout_raw.dtype) if dout_raw is not None else 0, ds, _ptr(o),
+        _dtype_code(o.dtype) if o is not None else 0, os_, _ptr(delta_in), _ptr(dq), _ptr(dk), _ptr(dv),
+        _dtype_code(dq.dtype), _strides_bnh(dq), _strides_bnh(dk), _strides_bnh(dv), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(rs),
+        (ctypes.c_void_p * 2)(*main_events) if main_events is not None else None, _stream(dev)))
+    return dq, dk, dv, rs

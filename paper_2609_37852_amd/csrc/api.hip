@@ -1,0 +1,353 @@
+// Host implementation of the C ABI (include/attn_fp8.h): argument checks,
+// workspace layout and launch sequencing.  No device memory is allocated here.
+#include <cmath>
+#include <cstdio>
+#include <cstdarg>
+#include <string>
+
+#include "attn_fp8.h"
+#include "kernels.hpp"
+
+namespace {
+
+thread_local std::string g_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return code;
+}
+
+int ok() {
+  g_error.clear();
+  return ATTN_FP8_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int dtype_size(int dt) { return dt == ATTN_FP8_DTYPE_F32 ? 4 : dt == ATTN_FP8_DTYPE_BF16 ? 2 : 0; }
+
+bool head_dim_ok(int64_t d) { return d == 64 || d == 128 || d == 192 || d == 256; }
+
+bool pair_ok(int64_t dqk, int64_t dv) {
+  return (dqk == 64 && dv == 64) || (dqk == 128 && dv == 128) || (dqk == 256 && dv == 256) ||
+         (dqk == 192 && dv == 128);
+}
+
+// strides {b, n, h} of a [B, N, H, D] tensor with contiguous channels
+int check_strides(const char* name, const int64_t* s, int esize) {
+  if (!s) return fail(ATTN_FP8_EINVAL, "%s: strides pointer is NULL", name);
+  for (int i = 0; i < 3; i++) {
+    if (s[i] < 0) return fail(ATTN_FP8_EINVAL, "%s: negative stride %lld", name, (long long)s[i]);
+    if ((s[i] * esize) % 16 != 0)
+      return fail(ATTN_FP8_EALIGN, "%s: stride %lld elements is not a multiple of 16 bytes", name,
+                  (long long)s[i]);
+  }
+  return ATTN_FP8_OK;
+}
+
+int check_ptr(const char* name, const void* p) {
+  if (!p) return fail(ATTN_FP8_EINVAL, "%s is NULL", name);
+  if (!aligned16(p)) return fail(ATTN_FP8_EALIGN, "%s is not 16-byte aligned", name);
+  return ATTN_FP8_OK;
+}
+
+int check_mx(const char* name, const attn_fp8_mx* m, bool row, bool col) {
+  if (!m) return fail(ATTN_FP8_EINVAL, "%s: operand pointer is NULL", name);
+  std::string n(name);
+  int rc;
+  if (row) {
+    if ((rc = check_ptr((n + ".code_row").c_str(), m->code_row))) return rc;
+    if ((rc = check_ptr((n + ".scale_row").c_str(), m->scale_row))) return rc;
+  }
+  if (col) {
+    if ((rc = check_ptr((n + ".code_col").c_str(), m->code_col))) return rc;
+    if ((rc = check_ptr((n + ".scale_col").c_str(), m->scale_col))) return rc;
+  }
+  return ATTN_FP8_OK;
+}
+
+int check_problem(const attn_fp8_problem* p) {
+  if (!p) return fail(ATTN_FP8_EINVAL, "problem is NULL");
+  if (p->batch < 0 || p->seqlen < 0 || p->heads_q < 0 || p->heads_kv < 0)
+    return fail(ATTN_FP8_EINVAL, "negative problem size");
+  if (p->heads_kv == 0 && p->heads_q != 0) return fail(ATTN_FP8_EINVAL, "heads_kv is 0");
+  if (p->heads_kv > 0 && p->heads_q % p->heads_kv != 0)
+    return fail(ATTN_FP8_EUNSUPPORTED, "heads_q (%lld) is not a multiple of heads_kv (%lld)",
+                (long long)p->heads_q, (long long)p->heads_kv);
+  if (!pair_ok(p->dim_qk, p->dim_v))
+    return fail(ATTN_FP8_EUNSUPPORTED, "head dims (%lld, %lld) not instantiated", (long long)p->dim_qk,
+                (long long)p->dim_v);
+  if (p->causal != 1) return fail(ATTN_FP8_EUNSUPPORTED, "only causal attention is implemented");
+  if (p->seqlen % 32 != 0)
+    return fail(ATTN_FP8_EUNSUPPORTED, "seqlen %lld is not a multiple of 32", (long long)p->seqlen);
+  if (!(std::isfinite(p->softmax_scale) && p->softmax_scale > 0.f))
+    return fail(ATTN_FP8_EINVAL, "softmax_scale must be finite and positive");
+  if (p->batch > 65535 || p->heads_q > 65535 || p->seqlen > (int64_t(1) << 30))
+    return fail(ATTN_FP8_EUNSUPPORTED, "problem exceeds the launch grid limits");
+  return ATTN_FP8_OK;
+}
+
+bool empty(const attn_fp8_problem* p) { return p->batch == 0 || p->seqlen == 0 || p->heads_q == 0; }
+
+afp8::AttnArgs base_args(const attn_fp8_problem* p) {
+  afp8::AttnArgs a{};
+  a.B = p->batch;
+  a.N = p->seqlen;
+  a.Hq = p->heads_q;
+  a.Hkv = p->heads_kv;
+  a.G = p->heads_q / p->heads_kv;
+  a.tau = p->softmax_scale;
+  a.c = (float)((double)p->softmax_scale * 1.4426950408889634);
+  return a;
+}
+
+void set_row(const attn_fp8_mx* m, const uint8_t*& code, const uint8_t*& scale) {
+  code = m->code_row;
+  scale = m->scale_row;
+}
+void set_col(const attn_fp8_mx* m, const uint8_t*& code, const uint8_t*& scale) {
+  code = m->code_col;
+  scale = m->scale_col;
+}
+
+size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
+
+size_t ws_dq_bytes(const attn_fp8_problem* p) {
+  return round256((size_t)p->batch * p->seqlen * p->heads_q * p->dim_qk * sizeof(float));
+}
+size_t ws_delta_bytes(const attn_fp8_problem* p) {
+  return round256((size_t)p->batch * p->heads_q * p->seqlen * 2 * sizeof(float));
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(ATTN_FP8_EHIP, "%s: %s", what, hipGetErrorString(e));
+  return ATTN_FP8_OK;
+}
+
+int check_delta_inputs(const attn_fp8_problem* p, int mode, const attn_fp8_mx* q, const attn_fp8_mx* k,
+                       const attn_fp8_mx* v, const attn_fp8_mx* dout, const float* lse, const void* dout_raw,
+                       int dout_dtype, const int64_t* dout_strides, const void* o, int o_dtype,
+                       const int64_t* o_strides) {
+  int rc;
+  if (mode == ATTN_FP8_DELTA_MATCHING) {
+    if ((rc = check_mx("q", q, true, false)) || (rc = check_mx("k", k, true, false)) ||
+        (rc = check_mx("v", v, true, false)) || (rc = check_mx("dout", dout, true, false)) ||
+        (rc = check_ptr("lse", lse)))
+      return rc;
+  } else if (mode == ATTN_FP8_DELTA_STALE_ROWSUM) {
+    if (!dtype_size(dout_dtype) || !dtype_size(o_dtype)) return fail(ATTN_FP8_EINVAL, "bad dout/o dtype");
+    if ((rc = check_ptr("dout_raw", dout_raw)) || (rc = check_ptr("o", o)) ||
+        (rc = check_strides("dout_raw", dout_strides, dtype_size(dout_dtype))) ||
+        (rc = check_strides("o", o_strides, dtype_size(o_dtype))))
+      return rc;
+  } else {
+    return fail(ATTN_FP8_EINVAL, "unknown delta_mode %d", mode);
+  }
+  return ATTN_FP8_OK;
+}
+
+int launch_delta(const attn_fp8_problem* p, int mode, const attn_fp8_mx* q, const attn_fp8_mx* k,
+                 const attn_fp8_mx* v, const attn_fp8_mx* dout, const float* lse, const void* dout_raw,
+                 int dout_dtype, const int64_t* dout_strides, const void* o, int o_dtype,
+                 const int64_t* o_strides, float* delta, hipStream_t stream) {
+  if (mode == ATTN_FP8_DELTA_MATCHING) {
+    afp8::AttnArgs a = base_args(p);
+    set_row(q, a.q_code, a.q_scale);
+    set_row(k, a.k_code, a.k_scale);
+    set_row(v, a.v_code, a.v_scale);
+    set_row(dout, a.do_code, a.do_scale);
+    a.lse = lse;
+    a.delta_out = delta;
+    return hip_status(afp8::launch_delta_matching(a, (int)p->dim_qk, (int)p->dim_v, stream), "delta_matching");
+  }
+  afp8::StaleArgs s{};
+  s.dout = dout_raw;
+  s.o = o;
+  for (int i = 0; i < 3; i++) {
+    s.ds[i] = dout_strides[i];
+    s.os[i] = o_strides[i];
+  }
+  s.delta = delta;
+  s.B = p->batch;
+  s.N = p->seqlen;
+  s.Hq = p->heads_q;
+  s.Dv = (int)p->dim_v;
+  return hip_status(afp8::launch_stale_rowsum(s, dout_dtype == ATTN_FP8_DTYPE_BF16, o_dtype == ATTN_FP8_DTYPE_BF16,
+                                              stream),
+                    "stale_rowsum");
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* attn_fp8_last_error(void) { return g_error.c_str(); }
+
+int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, int64_t D,
+                      const int64_t strides[3], const attn_fp8_mx* out, int which, uint32_t* nonfinite_count,
+                      hipStream_t stream) {
+  int rc;
+  const int es = dtype_size(x_dtype);
+  if (!es) return fail(ATTN_FP8_EINVAL, "x_dtype %d is not F32 or BF16", x_dtype);
+  if (B < 0 || N < 0 || H < 0) return fail(ATTN_FP8_EINVAL, "negative size");
+  if (!head_dim_ok(D)) return fail(ATTN_FP8_EUNSUPPORTED, "D = %lld not in {64,128,192,256}", (long long)D);
+  if (N % 32 != 0) return fail(ATTN_FP8_EUNSUPPORTED, "N = %lld is not a multiple of 32", (long long)N);
+  if (which < 1 || which > 3) return fail(ATTN_FP8_EINVAL, "which = %d", which);
+  if (B > 65535 || H > 65535 || N > (int64_t(1) << 30)) return fail(ATTN_FP8_EUNSUPPORTED, "grid limits");
+  if (B == 0 || N == 0 || H == 0) return ok();  // empty: nothing is read or written
+  if ((rc = check_ptr("x", x)) || (rc = check_strides("x", strides, es)) ||
+      (rc = check_mx("out", out, which & 1, which & 2)))
+    return rc;
+  afp8::QuantArgs a{};
+  a.x = x;
+  a.sb = strides[0];
+  a.sn = strides[1];
+  a.sh = strides[2];
+  a.B = B;
+  a.N = N;
+  a.H = H;
+  a.code_row = out->code_row;
+  a.scale_row = out->scale_row;
+  a.code_col = out->code_col;
+  a.scale_col = out->scale_col;
+  a.which = which;
+  a.nonfinite = nonfinite_count;
+  if ((rc = hip_status(afp8::launch_quantize(a, (int)D, x_dtype == ATTN_FP8_DTYPE_BF16, stream), "quantize")))
+    return rc;
+  return ok();
+}
+
+int attn_fp8_fwd(const attn_fp8_problem* p, const attn_fp8_mx* q, const attn_fp8_mx* k, const attn_fp8_mx* v,
+                 void* o, int o_dtype, const int64_t o_strides[3], float* lse, hipStream_t stream) {
+  int rc;
+  if ((rc = check_problem(p))) return rc;
+  if (!dtype_size(o_dtype)) return fail(ATTN_FP8_EINVAL, "o_dtype %d", o_dtype);
+  if (empty(p)) return ok();
+  if ((rc = check_mx("q", q, true, false)) || (rc = check_mx("k", k, true, false)) ||
+      (rc = check_mx("v", v, false, true)) || (rc = check_ptr("o", o)) ||
+      (rc = check_strides("o", o_strides, dtype_size(o_dtype))) || (rc = check_ptr("lse", lse)))
+    return rc;
+  afp8::AttnArgs a = base_args(p);
+  set_row(q, a.q_code, a.q_scale);
+  set_row(k, a.k_code, a.k_scale);
+  set_col(v, a.vc_code, a.vc_scale);
+  a.o = o;
+  for (int i = 0; i < 3; i++) a.os[i] = o_strides[i];
+  a.o_bf16 = o_dtype == ATTN_FP8_DTYPE_BF16;
+  a.lse_out = lse;
+  if ((rc = hip_status(afp8::launch_fwd(a, (int)p->dim_qk, (int)p->dim_v, stream), "fwd"))) return rc;
+  return ok();
+}
+
+int attn_fp8_delta(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q, const attn_fp8_mx* k,
+                   const attn_fp8_mx* v, const attn_fp8_mx* dout, const float* lse, const void* dout_raw,
+                   int dout_dtype, const int64_t dout_strides[3], const void* o, int o_dtype,
+                   const int64_t o_strides[3], float* delta, hipStream_t stream) {
+  int rc;
+  if ((rc = check_problem(p))) return rc;
+  if (delta_mode != ATTN_FP8_DELTA_MATCHING && delta_mode != ATTN_FP8_DELTA_STALE_ROWSUM)
+    return fail(ATTN_FP8_EINVAL, "unknown delta_mode %d", delta_mode);
+  if (empty(p)) return ok();
+  if ((rc = check_delta_inputs(p, delta_mode, q, k, v, dout, lse, dout_raw, dout_dtype, dout_strides, o, o_dtype,
+                               o_strides)) ||
+      (rc = check_ptr("delta", delta)))
+    return rc;
+  if ((rc = launch_delta(p, delta_mode, q, k, v, dout, lse, dout_raw, dout_dtype, dout_strides, o, o_dtype,
+                         o_strides, delta, stream)))
+    return rc;
+  return ok();
+}
+
+int attn_fp8_bwd_workspace_size(const attn_fp8_problem* p, size_t* bytes) {
+  int rc;
+  if ((rc = check_problem(p))) return rc;
+  if (!bytes) return fail(ATTN_FP8_EINVAL, "bytes is NULL");
+  *bytes = ws_dq_bytes(p) + ws_delta_bytes(p);
+  return ok();
+}
+
+int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q, const attn_fp8_mx* k,
+                 const attn_fp8_mx* v, const attn_fp8_mx* dout, const float* lse, const void* dout_raw,
+                 int dout_dtype, const int64_t dout_strides[3], const void* o, int o_dtype,
+                 const int64_t o_strides[3], const float* delta_in, void* dq, void* dk, void* dv, int grad_dtype,
+                 const int64_t dq_strides[3], const int64_t dk_strides[3], const int64_t dv_strides[3],
+                 void* workspace, size_t workspace_bytes, double* rowstats, const hipEvent_t* main_events,
+                 hipStream_t stream) {
+  int rc;
+  if ((rc = check_problem(p))) return rc;
+  const int gs = dtype_size(grad_dtype);
+  if (!gs) return fail(ATTN_FP8_EINVAL, "grad_dtype %d", grad_dtype);
+  if (empty(p)) return ok();
+  if ((rc = check_mx("q", q, true, true)) || (rc = check_mx("k", k, true, true)) ||
+      (rc = check_mx("v", v, true, false)) || (rc = check_mx("dout", dout, true, true)) ||
+      (rc = check_ptr("lse", lse)) || (rc = check_ptr("dq", dq)) || (rc = check_ptr("dk", dk)) ||
+      (rc = check_ptr("dv", dv)) || (rc = check_strides("dq", dq_strides, gs)) ||
+      (rc = check_strides("dk", dk_strides, gs)) || (rc = check_strides("dv", dv_strides, gs)))
+    return rc;
+  if (delta_in) {
+    if ((rc = check_ptr("delta_in", delta_in))) return rc;
+  } else if ((rc = check_delta_inputs(p, delta_mode, q, k, v, dout, lse, dout_raw, dout_dtype, dout_strides, o,
+                                      o_dtype, o_strides))) {
+    return rc;
+  }
+  if (rowstats && !aligned16(rowstats)) return fail(ATTN_FP8_EALIGN, "rowstats is not 16-byte aligned");
+  const size_t need = ws_dq_bytes(p) + ws_delta_bytes(p);
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
+    return fail(ATTN_FP8_EWORKSPACE, "workspace is NULL or not 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(ATTN_FP8_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
+
+  float* dq_acc = reinterpret_cast<float*>(workspace);
+  float* delta = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + ws_dq_bytes(p));
+  if (delta_in) {
+    delta = const_cast<float*>(delta_in);
+  } else if ((rc = launch_delta(p, delta_mode, q, k, v, dout, lse, dout_raw, dout_dtype, dout_strides, o, o_dtype,
+                                o_strides, delta, stream))) {
+    return rc;
+  }
+  const int64_t ndq = p->batch * p->seqlen * p->heads_q * p->dim_qk;
+  if ((rc = hip_status(afp8::launch_fill_zero(dq_acc, ndq, stream), "fill_zero"))) return rc;
+
+  afp8::AttnArgs a = base_args(p);
+  set_row(q, a.q_code, a.q_scale);
+  set_row(k, a.k_code, a.k_scale);
+  set_row(v, a.v_code, a.v_scale);
+  set_row(dout, a.do_code, a.do_scale);
+  set_col(q, a.qc_code, a.qc_scale);
+  set_col(k, a.kc_code, a.kc_scale);
+  set_col(dout, a.doc_code, a.doc_scale);
+  a.lse = lse;
+  a.delta = delta;
+  a.dq_acc = dq_acc;
+  a.dk = dk;
+  a.dv = dv;
+  for (int i = 0; i < 3; i++) {
+    a.dks[i] = dk_strides[i];
+    a.dvs[i] = dv_strides[i];
+  }
+  a.grad_bf16 = grad_dtype == ATTN_FP8_DTYPE_BF16;
+  a.rowstats = rowstats;
+  if (main_events && (rc = hip_status(hipEventRecord(main_events[0], stream), "event record"))) return rc;
+  if ((rc = hip_status(afp8::launch_bwd(a, (int)p->dim_qk, (int)p->dim_v, stream), "bwd"))) return rc;
+  if (main_events && (rc = hip_status(hipEventRecord(main_events[1], stream), "event record"))) return rc;
+
+  afp8::DqFinalArgs f{};
+  f.acc = dq_acc;
+  f.dq = dq;
+  for (int i = 0; i < 3; i++) f.s[i] = dq_strides[i];
+  f.B = p->batch;
+  f.N = p->seqlen;
+  f.Hq = p->heads_q;
+  f.D = p->dim_qk;
+  f.tau = p->softmax_scale;
+  if ((rc = hip_status(afp8::launch_dq_finalize(f, grad_dtype == ATTN_FP8_DTYPE_BF16, stream), "dq_finalize")))
+    return rc;
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,110 @@
+// Device helpers shared by the gfx950 kernels: FP8/E8M0 arithmetic and the
+// MX-scaled 32x32x64 MFMA.
+//
+// Register layout of v_mfma_scale_f32_32x32x64_f8f6f4 with E4M3 operands
+// (measured on gfx950; lane l, half hf = l / 32):
+//   A (32 x 64):  lane l holds row l % 32; its bytes 0..15 are k = 16 hf + t,
+//                 bytes 16..31 are k = 32 + 16 hf + (t - 16).
+//   B (64 x 32):  lane l holds column l % 32 with the same k mapping.
+//   scales:       lane l's scale byte is the E8M0 scale of row (A) / column (B)
+//                 l % 32 for the 32-wide k block hf (k in [32 hf, 32 hf + 32)).
+//   C (32 x 32):  lane l, accumulator r holds row 8 (r / 4) + 4 hf + r % 4,
+//                 column l % 32.
+// Within one 32-wide k block the hardware sums products in chunks with an
+// aligned fixed-point adder (about 2^-13 of the largest product of a chunk);
+// chunk sums and the accumulator are FP32.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace afp8 {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef short v2s __attribute__((ext_vector_type(2)));
+typedef int v2i __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ v16f mfma_mx(const v8i& a, const v8i& b, const v16f& c, int scale_a,
+                                        int scale_b) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, scale_a, 0, scale_b);
+}
+
+// Smallest integer e with amax <= 448 * 2^e (448 = 1.75 * 2^8), clamped to the
+// E8M0 range [-127, 127]; zero and FP32-subnormal amax give -127.  Pure
+// integer arithmetic on the FP32 bit pattern.
+__device__ __forceinline__ int pow2_exponent(float amax) {
+  const uint32_t u = __float_as_uint(amax) & 0x7fffffffu;
+  const int be = (int)(u >> 23);
+  int e = be - 135 + ((u & 0x7fffffu) > 0x600000u ? 1 : 0);
+  e = be == 0 ? -127 : e;
+  e = be == 255 ? 127 : e;
+  return e < -127 ? -127 : (e > 127 ? 127 : e);
+}
+
+// 2^e as an FP32 value for e in [-126, 127].
+__device__ __forceinline__ float exp2i(int e) { return __uint_as_float((uint32_t)(e + 127) << 23); }
+
+// Four E4M3 codes of a/scale .. d/scale (scale a power of two, normal FP32),
+// round to nearest even, packed little-endian into one dword.
+__device__ __forceinline__ uint32_t cvt4_div(float a, float b, float c, float d, float scale) {
+  v2s r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32((v2s){0, 0}, a, b, scale, false);
+  r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(r, c, d, scale, true);
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+// Four E4M3 codes of already-scaled values (no saturation: |x| <= 448 by
+// construction at every call site).
+__device__ __forceinline__ uint32_t cvt4(float a, float b, float c, float d) {
+  uint32_t r = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0u, false);
+  return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, r, true);
+}
+
+// Decode byte `sel` (0..3) of a packed dword of E4M3 codes.
+__device__ __forceinline__ float fp8_value(uint32_t packed, int sel) {
+  switch (sel & 3) {
+    case 0: return __builtin_amdgcn_cvt_f32_fp8((int)packed, 0);
+    case 1: return __builtin_amdgcn_cvt_f32_fp8((int)packed, 1);
+    case 2: return __builtin_amdgcn_cvt_f32_fp8((int)packed, 2);
+    default: return __builtin_amdgcn_cvt_f32_fp8((int)packed, 3);
+  }
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// FP32 -> bfloat16 bits, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// v_permlane32_swap: for lanes < 32 returns {a[l], a[l + 32]}, for lanes >= 32
+// returns {b[l - 32], b[l]}.  With a = value of group 0, b = value of group 1,
+// each half of the wave receives both halves' values of "its" group.
+struct Pair { float lo, hi; };
+__device__ __forceinline__ Pair permlane32_swap(float a, float b) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+  return Pair{__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+
+// Value of `v` in the partner lane l ^ 32.
+__device__ __forceinline__ float partner(float v) {
+  Pair p = permlane32_swap(v, v);
+  return (threadIdx.x & 32) ? p.lo : p.hi;
+}
+
+}  // namespace afp8
+
+namespace afp8 {
+// Backward probability of one score (App. B.6.3): P = 2^(S tau log2e - L) with
+// L = LSE log2e, exponent clamped at 4 (256 P at 2^12).  Written with an
+// explicit FMA so that every kernel recomputing P gets the same FP32 value.
+__device__ __forceinline__ float bwd_prob(float s, float c, float L) {
+  return __builtin_amdgcn_exp2f(fminf(__builtin_fmaf(s, c, -L), 4.0f));
+}
+}  // namespace afp8

@@ -1,0 +1,71 @@
+// Kernel argument blocks and launchers (internal to the library; the public
+// interface is include/attn_fp8.h).  Host code validates every argument
+// before a launcher is called; kernels assume the geometry checked there.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace afp8 {
+
+struct QuantArgs {
+  const void* x;
+  int64_t sb, sn, sh;        // element strides of x (channel stride 1)
+  int64_t B, N, H;
+  uint8_t *code_row, *scale_row, *code_col, *scale_col;
+  int which;                 // bit 0 row copy, bit 1 col copy
+  uint32_t* nonfinite;       // nullable
+};
+
+struct StaleArgs {
+  const void* dout;
+  int64_t ds[3];
+  const void* o;
+  int64_t os[3];
+  float* delta;              // [B, Hq, N, 2]
+  int64_t B, N, Hq;
+  int Dv;
+};
+
+struct DqFinalArgs {
+  const float* acc;          // [B, N, Hq, D] FP32
+  void* dq;
+  int64_t s[3];
+  int64_t B, N, Hq, D;
+  float tau;
+};
+
+// Shared by the forward, the matched-correction pass and the backward.
+struct AttnArgs {
+  int64_t B, N, Hq, Hkv, G;  // G = Hq / Hkv
+  float c;                   // tau * log2(e), applied to the score accumulator
+  float tau;
+  const uint8_t *q_code, *q_scale;     // row copy of Q      [B,Hq,N,Dqk], [B,Hq,N,Dqk/32]
+  const uint8_t *k_code, *k_scale;     // row copy of K      [B,Hkv,N,Dqk]
+  const uint8_t *v_code, *v_scale;     // row copy of V      [B,Hkv,N,Dv]
+  const uint8_t *do_code, *do_scale;   // row copy of dO     [B,Hq,N,Dv]
+  const uint8_t *qc_code, *qc_scale;   // col copy of Q      [B,Hq,Dqk,N], [B,Hq,Dqk,N/32]
+  const uint8_t *kc_code, *kc_scale;   // col copy of K      [B,Hkv,Dqk,N]
+  const uint8_t *vc_code, *vc_scale;   // col copy of V      [B,Hkv,Dv,N]
+  const uint8_t *doc_code, *doc_scale; // col copy of dO     [B,Hq,Dv,N]
+  const float* lse;                    // [B,Hq,N]
+  float* lse_out;
+  const float* delta;                  // [B,Hq,N,2]
+  float* delta_out;
+  void* o;  int64_t os[3]; int o_bf16;
+  float* dq_acc;                       // [B,N,Hq,Dqk] FP32
+  void* dk; int64_t dks[3];
+  void* dv; int64_t dvs[3];
+  int grad_bf16;
+  double* rowstats;                    // nullable [B,Hq,N,4]
+};
+
+hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_t s);
+hipError_t launch_stale_rowsum(const StaleArgs& a, int dout_bf16, int o_bf16, hipStream_t s);
+hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
+hipError_t launch_dq_finalize(const DqFinalArgs& a, int grad_bf16, hipStream_t s);
+hipError_t launch_fwd(const AttnArgs& a, int dqk, int dv, hipStream_t s);
+hipError_t launch_delta_matching(const AttnArgs& a, int dqk, int dv, hipStream_t s);
+hipError_t launch_bwd(const AttnArgs& a, int dqk, int dv, hipStream_t s);
+
+}  // namespace afp8

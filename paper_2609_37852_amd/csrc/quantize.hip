@@ -1,0 +1,201 @@
+// Input quantizer: E4M3 codes with power-of-two (E8M0) scales, two copies
+// (App. B.6.1 with 1x32 / 32x1 blocks).  HBM-bound: one pass reads x once and
+// writes both copies.
+//
+// One workgroup = 32 tokens x D channels of one (batch, head), 2*D threads.
+//   row copy: thread t owns token t / (D/16) and 16 channels; a 1x32 block
+//             spans the thread and its neighbour t ^ 1.
+//   col copy: the tile is transposed through LDS; thread t owns channel t / 2
+//             and 16 tokens; a 32x1 block spans t and t ^ 1.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace afp8 {
+
+template <typename T>
+__device__ __forceinline__ void load16(const T* p, float (&v)[16]);
+
+template <>
+__device__ __forceinline__ void load16<float>(const float* p, float (&v)[16]) {
+  const float4* q = reinterpret_cast<const float4*>(p);
+#pragma unroll
+  for (int k = 0; k < 4; k++) {
+    float4 f = q[k];
+    v[4 * k] = f.x; v[4 * k + 1] = f.y; v[4 * k + 2] = f.z; v[4 * k + 3] = f.w;
+  }
+}
+
+template <>
+__device__ __forceinline__ void load16<uint16_t>(const uint16_t* p, float (&v)[16]) {
+  const uint4* q = reinterpret_cast<const uint4*>(p);
+#pragma unroll
+  for (int k = 0; k < 2; k++) {
+    uint4 u = q[k];
+    uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int m = 0; m < 4; m++) {
+      v[8 * k + 2 * m] = __uint_as_float(w[m] << 16);
+      v[8 * k + 2 * m + 1] = __uint_as_float(w[m] & 0xffff0000u);
+    }
+  }
+}
+
+// Codes of 16 values for one block exponent e: x * 2^-e is exact (power-of-two
+// scaling; |x * 2^-e| <= 448 by the choice of e), then rounded to E4M3.
+__device__ __forceinline__ uint4 encode16(const float (&v)[16], int e) {
+  uint32_t w[4];
+#pragma unroll
+  for (int k = 0; k < 4; k++)
+    w[k] = cvt4(__builtin_ldexpf(v[4 * k], -e), __builtin_ldexpf(v[4 * k + 1], -e),
+                __builtin_ldexpf(v[4 * k + 2], -e), __builtin_ldexpf(v[4 * k + 3], -e));
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+__device__ __forceinline__ float amax16(const float (&v)[16]) {
+  float m = 0.f;
+#pragma unroll
+  for (int k = 0; k < 16; k++) m = fmaxf(m, fabsf(v[k]));
+  return m;
+}
+
+template <int D, typename T>
+__global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
+  constexpr int CH = D / 16;  // 16-channel chunks per token
+  __shared__ float tile[32][D + 1];
+  const int t = threadIdx.x;
+  const int64_t n0 = (int64_t)blockIdx.x * 32, h = blockIdx.y, b = blockIdx.z;
+  const int64_t bh = b * a.H + h;
+  const int tok = t / CH, ch = (t % CH) * 16;
+  float v[16];
+  load16<T>(reinterpret_cast<const T*>(a.x) + b * a.sb + (n0 + tok) * a.sn + h * a.sh + ch, v);
+
+  if (a.nonfinite) {
+    uint32_t bad = 0;
+#pragma unroll
+    for (int k = 0; k < 16; k++) bad += __builtin_isfinite(v[k]) ? 0u : 1u;
+    if (bad) atomicAdd(a.nonfinite, bad);
+  }
+  if (a.which & 1) {
+    float am = amax16(v);
+    am = fmaxf(am, __shfl_xor(am, 1));
+    const int e = pow2_exponent(am);
+    *reinterpret_cast<uint4*>(a.code_row + (bh * a.N + n0 + tok) * D + ch) = encode16(v, e);
+    if ((t & 1) == 0) a.scale_row[(bh * a.N + n0 + tok) * (D / 32) + ch / 32] = (uint8_t)(e + 127);
+  }
+  if (a.which & 2) {
+#pragma unroll
+    for (int k = 0; k < 16; k++) tile[tok][ch + k] = v[k];
+    __syncthreads();
+    const int c = t >> 1, half = t & 1;
+    float w[16];
+#pragma unroll
+    for (int k = 0; k < 16; k++) w[k] = tile[half * 16 + k][c];
+    float am = amax16(w);
+    am = fmaxf(am, __shfl_xor(am, 1));
+    const int e = pow2_exponent(am);
+    *reinterpret_cast<uint4*>(a.code_col + (bh * D + c) * a.N + n0 + half * 16) = encode16(w, e);
+    if (half == 0) a.scale_col[(bh * D + c) * (a.N / 32) + n0 / 32] = (uint8_t)(e + 127);
+  }
+}
+
+hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_t s) {
+  dim3 grid((unsigned)(a.N / 32), (unsigned)a.H, (unsigned)a.B);
+#define AFP8_Q(DD)                                                                           \
+  if (D == DD) {                                                                             \
+    if (dtype_bf16) hipLaunchKernelGGL((quantize_kernel<DD, uint16_t>), grid, dim3(2 * DD), 0, s, a); \
+    else hipLaunchKernelGGL((quantize_kernel<DD, float>), grid, dim3(2 * DD), 0, s, a);       \
+    return hipGetLastError();                                                                \
+  }
+  AFP8_Q(64)
+  AFP8_Q(128)
+  AFP8_Q(192)
+  AFP8_Q(256)
+#undef AFP8_Q
+  return hipErrorInvalidValue;
+}
+
+// ---------------------------------------------------------------------------
+// Stale (saved-output) correction, Sec. 3.2: delta_i = sum_c dO_ic O_ic in
+// FP32 from the raw dO and the stored O.  One wave per (b, n, h) row.
+template <typename TD, typename TO>
+__global__ __launch_bounds__(256) void stale_rowsum_kernel(StaleArgs a) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int64_t nrows = a.B * a.N * a.Hq;
+  if (row >= nrows) return;
+  const int64_t h = row % a.Hq, n = (row / a.Hq) % a.N, b = row / (a.Hq * a.N);
+  const TD* d = reinterpret_cast<const TD*>(a.dout) + b * a.ds[0] + n * a.ds[1] + h * a.ds[2];
+  const TO* o = reinterpret_cast<const TO*>(a.o) + b * a.os[0] + n * a.os[1] + h * a.os[2];
+  float acc = 0.f;
+  for (int c = lane; c < a.Dv; c += 64) {
+    float dv, ov;
+    if constexpr (sizeof(TD) == 2) dv = bf16_to_f32(d[c]); else dv = (float)d[c];
+    if constexpr (sizeof(TO) == 2) ov = bf16_to_f32(o[c]); else ov = (float)o[c];
+    acc = __builtin_fmaf(dv, ov, acc);
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
+  if (lane == 0) {
+    float* dst = a.delta + ((b * a.Hq + h) * a.N + n) * 2;
+    dst[0] = acc;
+    dst[1] = 0.f;
+  }
+}
+
+hipError_t launch_stale_rowsum(const StaleArgs& a, int dout_bf16, int o_bf16, hipStream_t s) {
+  const int64_t nrows = a.B * a.N * a.Hq;
+  dim3 grid((unsigned)((nrows + 3) / 4));
+  if (dout_bf16 && o_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<uint16_t, uint16_t>), grid, dim3(256), 0, s, a);
+  else if (dout_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<uint16_t, float>), grid, dim3(256), 0, s, a);
+  else if (o_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<float, uint16_t>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((stale_rowsum_kernel<float, float>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Workspace clear (a fill kernel rather than a memset node, so callers may
+// capture the backward in a graph) and the final dQ = tau * dQ_acc store.
+__global__ __launch_bounds__(256) void fill_zero_kernel(float4* p, int64_t n4) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256)
+    p[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s) {
+  const int64_t n4 = n / 4;  // n is a multiple of 4 at every call site
+  if (n4 == 0) return hipSuccess;
+  int64_t blocks = (n4 + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, s, reinterpret_cast<float4*>(p), n4);
+  return hipGetLastError();
+}
+
+template <typename TG>
+__global__ __launch_bounds__(256) void dq_finalize_kernel(DqFinalArgs a) {
+  // one thread per 4 channels of one (b, n, h) row
+  const int64_t per_row = a.D / 4;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= a.B * a.N * a.Hq * per_row) return;
+  const int64_t c4 = idx % per_row, row = idx / per_row;
+  const int64_t h = row % a.Hq, n = (row / a.Hq) % a.N, b = row / (a.Hq * a.N);
+  const float4 v = reinterpret_cast<const float4*>(a.acc)[idx];
+  TG* dst = reinterpret_cast<TG*>(a.dq) + b * a.s[0] + n * a.s[1] + h * a.s[2] + c4 * 4;
+  if constexpr (sizeof(TG) == 2) {
+    uint2 o;
+    o.x = (uint32_t)f32_to_bf16(v.x * a.tau) | ((uint32_t)f32_to_bf16(v.y * a.tau) << 16);
+    o.y = (uint32_t)f32_to_bf16(v.z * a.tau) | ((uint32_t)f32_to_bf16(v.w * a.tau) << 16);
+    *reinterpret_cast<uint2*>(dst) = o;
+  } else {
+    *reinterpret_cast<float4*>(dst) = make_float4(v.x * a.tau, v.y * a.tau, v.z * a.tau, v.w * a.tau);
+  }
+}
+
+hipError_t launch_dq_finalize(const DqFinalArgs& a, int grad_bf16, hipStream_t s) {
+  const int64_t n = a.B * a.N * a.Hq * (a.D / 4);
+  if (n == 0) return hipSuccess;
+  dim3 grid((unsigned)((n + 255) / 256));
+  if (grad_bf16) hipLaunchKernelGGL(dq_finalize_kernel<uint16_t>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(dq_finalize_kernel<float>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace afp8

@@ -1,0 +1,88 @@
+// LDS staging of FP8 operand tiles shared by the forward, correction and
+// backward kernels.  All loads are 16-byte vector loads; rows past the end of
+// the sequence are zero-filled (zero codes, scale byte 0) so the MFMA sees
+// exact zeros there.
+#pragma once
+
+#include "common.hpp"
+
+namespace afp8 {
+
+// Rows [r0, r0 + ROWS) of a row-major [N, D] code matrix (one batch/head)
+// into LDS with row stride ST bytes; the block's E8M0 bytes [N, D/32] into
+// a dense [ROWS][D/32] LDS array.
+template <int ROWS, int D, int ST, int NT>
+__device__ __forceinline__ void stage_rows(uint8_t* lds, uint8_t* lds_scale, const uint8_t* code,
+                                           const uint8_t* scale, int64_t r0, int64_t N) {
+  constexpr int V = ROWS * D / 16;  // uint4 per tile
+  for (int u = threadIdx.x; u < V; u += NT) {
+    const int r = u / (D / 16), c = (u % (D / 16)) * 16;
+    uint4 val = make_uint4(0, 0, 0, 0);
+    if (r0 + r < N) val = *reinterpret_cast<const uint4*>(code + (r0 + r) * D + c);
+    *reinterpret_cast<uint4*>(lds + r * ST + c) = val;
+  }
+  constexpr int S = ROWS * D / 32;  // scale bytes
+  static_assert(S % 4 == 0, "scale tile is whole dwords");
+  for (int u = threadIdx.x; u < S / 4; u += NT) {
+    const int r = (u * 4) / (D / 32);
+    uint32_t val = 0;
+    if (r0 + r < N) val = *reinterpret_cast<const uint32_t*>(scale + r0 * (D / 32) + u * 4);
+    *reinterpret_cast<uint32_t*>(lds_scale + u * 4) = val;
+  }
+}
+
+// Columns [j0, j0 + 64) of a col-copy code matrix [D, N] (one batch/head)
+// into LDS as [D][64] with row stride ST, permuted inside each 32-wide group
+// so that the 16 sequence positions an MFMA lane of half hf holds in the
+// "C layout" (positions 8a + 4hf + b, a, b in 0..3) are contiguous:
+//   LDS position 16 hf + 4 a + b  <-  sequence position 8 a + 4 hf + b.
+// Scales [D, N/32] -> LDS [D][2].
+template <int D, int ST, int NT>
+__device__ __forceinline__ void stage_cols_perm(uint8_t* lds, uint8_t* lds_scale, const uint8_t* code,
+                                                const uint8_t* scale, int64_t j0, int64_t N) {
+  constexpr int V = D * 4;  // 4 uint4 per 64-wide row
+  for (int u = threadIdx.x; u < V; u += NT) {
+    const int c = u >> 2, q = u & 3;  // q: 16-position quarter of the 64-wide row
+    uint4 val = make_uint4(0, 0, 0, 0);
+    if (j0 + q * 16 < N) val = *reinterpret_cast<const uint4*>(code + (int64_t)c * N + j0 + q * 16);
+    uint8_t* base = lds + c * ST + (q >> 1) * 32 + (q & 1) * 8;
+    *reinterpret_cast<uint2*>(base) = make_uint2(val.x, val.z);
+    *reinterpret_cast<uint2*>(base + 16) = make_uint2(val.y, val.w);
+  }
+  for (int u = threadIdx.x; u < D; u += NT) {
+    const int64_t g = j0 / 32;
+    const uint8_t s0 = (j0 < N) ? scale[(int64_t)u * (N / 32) + g] : 0;
+    const uint8_t s1 = (j0 + 32 < N) ? scale[(int64_t)u * (N / 32) + g + 1] : 0;
+    lds_scale[u * 2] = s0;
+    lds_scale[u * 2 + 1] = s1;
+  }
+}
+
+// A/B fragment of a row-staged tile: lane (row li, half hf), k-step s.
+template <int ST>
+__device__ __forceinline__ v8i frag_rows(const uint8_t* lds, int row, int s, int hf) {
+  const uint8_t* p = lds + row * ST + 64 * s + 16 * hf;
+  const uint4 lo = *reinterpret_cast<const uint4*>(p);
+  const uint4 hi = *reinterpret_cast<const uint4*>(p + 32);
+  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
+
+// Same fragment straight from global memory (row-major [*, D] codes).
+__device__ __forceinline__ v8i frag_rows_global(const uint8_t* row_ptr, int s, int hf) {
+  const uint8_t* p = row_ptr + 64 * s + 16 * hf;
+  const uint4 lo = *reinterpret_cast<const uint4*>(p);
+  const uint4 hi = *reinterpret_cast<const uint4*>(p + 32);
+  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
+
+// Fragment of a permuted col-staged tile (stage_cols_perm): lane (row li of
+// the D dimension, half hf); bytes 0..15 cover group 0, 16..31 group 1.
+template <int ST>
+__device__ __forceinline__ v8i frag_cols(const uint8_t* lds, int row, int hf) {
+  const uint8_t* p = lds + row * ST + 16 * hf;
+  const uint4 lo = *reinterpret_cast<const uint4*>(p);
+  const uint4 hi = *reinterpret_cast<const uint4*>(p + 32);
+  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
+
+}  // namespace afp8

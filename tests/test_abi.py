@@ -1,0 +1,109 @@
+"""CPU checks of the C ABI: the library loads, exports every function that
+include/attn_fp8.h declares, and rejects invalid arguments on the host
+without launching anything (these calls never reach the GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_37852_amd as pk
+from paper_2609_37852_amd import binding as bd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    txt = open(os.path.join(ROOT, "include", "attn_fp8.h")).read()
+    return sorted(set(re.findall(r"^(?:int|const char\*|size_t)\s+(attn_fp8_\w+)\(", txt, re.M)))
+
+
+def test_exports_every_declared_symbol():
+    L = pk.lib()
+    names = _declared()
+    assert set(names) == set(bd.EXPORTS), names
+    for n in names:
+        assert hasattr(L, n)
+
+
+def _prob(**kw):
+    d = dict(batch=1, seqlen=128, heads_q=2, heads_kv=2, dim_qk=128, dim_v=128, softmax_scale=0.088)
+    d.update(kw)
+    return pk.Problem(**d)
+
+
+def _fake_mx(addr=4096):
+    return bd._MX(addr, addr, addr, addr)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dim_qk=96, dim_v=96), -2), (dict(dim_qk=128, dim_v=64), -2), (dict(seqlen=100), -2),
+    (dict(heads_q=3, heads_kv=2), -2), (dict(causal=0), -2), (dict(softmax_scale=float("nan")), -1),
+    (dict(seqlen=-32), -1), (dict(heads_kv=0), -1)])
+def test_fwd_rejects_bad_problem(kw, code):
+    L = pk.lib()
+    p = _prob(**kw).c()
+    m = _fake_mx()
+    st = bd._I64x3(128 * 2 * 128, 2 * 128, 128)
+    rc = L.attn_fp8_fwd(ctypes.byref(p), ctypes.byref(m), ctypes.byref(m), ctypes.byref(m), ctypes.c_void_p(4096),
+                        1, st, ctypes.c_void_p(4096), None)
+    assert rc == code, pk.last_error()
+    assert pk.last_error()
+
+
+def test_null_alignment_and_workspace_errors():
+    L = pk.lib()
+    p = _prob().c()
+    m = _fake_mx()
+    st = bd._I64x3(128 * 2 * 128, 2 * 128, 128)
+    # NULL output
+    assert L.attn_fp8_fwd(ctypes.byref(p), ctypes.byref(m), ctypes.byref(m), ctypes.byref(m), None, 1, st,
+                          ctypes.c_void_p(4096), None) == -1
+    # misaligned operand
+    bad = _fake_mx(4097)
+    assert L.attn_fp8_fwd(ctypes.byref(p), ctypes.byref(bad), ctypes.byref(m), ctypes.byref(m),
+                          ctypes.c_void_p(4096), 1, st, ctypes.c_void_p(4096), None) == -3
+    # stride not a multiple of 16 bytes
+    st_bad = bd._I64x3(128 * 2 * 128, 2 * 128 + 1, 128)
+    assert L.attn_fp8_fwd(ctypes.byref(p), ctypes.byref(m), ctypes.byref(m), ctypes.byref(m),
+                          ctypes.c_void_p(4096), 1, st_bad, ctypes.c_void_p(4096), None) == -3
+    # bad dtype, bad delta mode
+    assert L.attn_fp8_fwd(ctypes.byref(p), ctypes.byref(m), ctypes.byref(m), ctypes.byref(m),
+                          ctypes.c_void_p(4096), 7, st, ctypes.c_void_p(4096), None) == -1
+    assert L.attn_fp8_delta(ctypes.byref(p), 5, ctypes.byref(m), ctypes.byref(m), ctypes.byref(m),
+                            ctypes.byref(m), ctypes.c_void_p(4096), None, 1, None, None, 1, None,
+                            ctypes.c_void_p(4096), None) == -1
+    # workspace too small / misaligned
+    n = ctypes.c_size_t(0)
+    assert L.attn_fp8_bwd_workspace_size(ctypes.byref(p), ctypes.byref(n)) == 0
+    assert n.value == 128 * 2 * 128 * 4 + 2 * 128 * 2 * 4
+    args = [ctypes.byref(p), 0] + [ctypes.byref(m)] * 4 + [ctypes.c_void_p(4096), None, 1, None, None, 1, None,
+                                                           None] + [ctypes.c_void_p(4096)] * 3 + [1, st, st, st]
+    assert L.attn_fp8_bwd(*args, ctypes.c_void_p(4096), ctypes.c_size_t(n.value - 1), None, None, None) == -4
+    assert L.attn_fp8_bwd(*args, ctypes.c_void_p(4096 + 16), ctypes.c_size_t(n.value), None, None, None) == -4
+
+
+def test_quantize_rejects_bad_args():
+    L = pk.lib()
+    m = _fake_mx()
+    st = bd._I64x3(64 * 64, 64, 64)
+    q = lambda *a: L.attn_fp8_quantize(*a)
+    assert q(ctypes.c_void_p(4096), 1, 1, 64, 1, 96, st, ctypes.byref(m), 3, None, None) == -2   # D
+    assert q(ctypes.c_void_p(4096), 1, 1, 40, 1, 64, st, ctypes.byref(m), 3, None, None) == -2   # N % 32
+    assert q(ctypes.c_void_p(4096), 3, 1, 64, 1, 64, st, ctypes.byref(m), 3, None, None) == -1   # dtype
+    assert q(ctypes.c_void_p(4096), 1, 1, 64, 1, 64, st, ctypes.byref(m), 0, None, None) == -1   # which
+    assert q(None, 1, 1, 64, 1, 64, st, ctypes.byref(m), 3, None, None) == -1
+    st_bad = bd._I64x3(64 * 64, 63, 64)
+    assert q(ctypes.c_void_p(4096), 1, 1, 64, 1, 64, st_bad, ctypes.byref(m), 3, None, None) == -3
+    # empty problems are valid and launch nothing
+    assert q(ctypes.c_void_p(4096), 1, 0, 64, 1, 64, st, ctypes.byref(m), 3, None, None) == 0
+    assert q(ctypes.c_void_p(4096), 1, 1, 0, 1, 64, st, ctypes.byref(m), 3, None, None) == 0
+
+
+def test_empty_problem_is_a_noop():
+    L = pk.lib()
+    p = _prob(seqlen=0).c()
+    m = _fake_mx()
+    st = bd._I64x3(0, 256, 128)
+    assert L.attn_fp8_fwd(ctypes.byref(p), ctypes.byref(m), ctypes.byref(m), ctypes.byref(m), ctypes.c_void_p(4096),
+                          1, st, ctypes.c_void_p(4096), None) == 0

@@ -1,0 +1,55 @@
+"""Full-size workloads in the benchmark's launch configuration: the whole
+problem runs on the GPU; one (batch 0, KV head 0) group slice is recomputed
+by the oracle on that slice's inputs and compared element by element."""
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+import paper_2609_37852_amd as pk
+from paper_2609_37852_amd import synth
+from _helpers import REL_TOL, invariant_report, np64, problem, rel_err, say, to_dev
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def _slice_inputs(w, d, kvh=0):
+    G = w.Hq // w.Hkv
+    hs = slice(kvh * G, (kvh + 1) * G)
+    return dict(q=d["q"][:1, :, hs], k=d["k"][:1, :, kvh:kvh + 1], v=d["v"][:1, :, kvh:kvh + 1],
+                do=d["do"][:1, :, hs]), hs
+
+
+@pytest.mark.parametrize("name", ["gqa_d128_8k"])
+def test_full_size_slice(name):
+    w = synth.WORKLOADS[name]
+    say(f"full-size {name}: {w}")
+    d = synth.generate(w, seed=0)
+    q, k, v, do = (to_dev(d[n], w.dtype) for n in ("q", "k", "v", "do"))
+    p = problem(w)
+    mq, mk, mv, mdo = (pk.attn_fp8_quantize(t) for t in (q, k, v, do))
+    o, lse = pk.attn_fp8_fwd(p, mq, mk, mv)
+    delta = pk.attn_fp8_delta(p, pk.DELTA_MATCHING, mq, mk, mv, mdo, lse)
+    dq, dk, dv, rs = pk.attn_fp8_bwd(p, pk.DELTA_MATCHING, mq, mk, mv, mdo, lse, grad_dtype=torch.float32,
+                                     rowstats=True)
+    torch.cuda.synchronize()
+    say("  gpu done")
+    sl, hs = _slice_inputs(w, d)
+    ws = synth.with_shape(w, B=1, Hq=w.Hq // w.Hkv, Hkv=1)
+    t = time.time()
+    ref, _ = orc.attention_from_inputs(sl["q"], sl["k"], sl["v"], sl["do"], float(np.float32(w.tau)),
+                                       want_rowstats=True)
+    say(f"  oracle slice {time.time() - t:.1f}s")
+    g = dict(O=np64(o[:1, :, hs]), LSE=np64(lse[:1, hs]), dQ=np64(dq[:1, :, hs]), dK=np64(dk[:1, :, 0:1]),
+             dV=np64(dv[:1, :, 0:1]), delta=np64(delta[:1, hs]))
+    errs = {kk: rel_err(g[kk], ref[kk]) for kk in ("O", "dQ", "dK", "dV")}
+    errs["LSE_max_abs"] = float(np.max(np.abs(g["LSE"] - ref["LSE"])))
+    errs["delta"] = rel_err(g["delta"][..., 0] + g["delta"][..., 1], ref["delta"])
+    say("  errors", {kk: f"{vv:.3e}" for kk, vv in errs.items()})
+    rep = invariant_report(rs[:1, hs].cpu().numpy(), ref["rowstats"])
+    say("  invariant", rep)
+    assert rep["violations"] == 0
+    for kk in ("O", "dQ", "dK", "dV"):
+        assert errs[kk] <= REL_TOL, (kk, errs[kk])

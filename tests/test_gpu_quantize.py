@@ -1,0 +1,111 @@
+"""GPU input quantizer (App. B.6.1, power-of-two 1x32 / 32x1 blocks):
+codes and scales must be bit-exact with the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+import paper_2609_37852_amd as pk
+from _helpers import say
+
+pytestmark = pytest.mark.gpu
+
+
+def _cmp(x32: np.ndarray, dtype: str, tensor=None):
+    """x32: float32 array [B,N,H,D] of exactly representable values."""
+    t = tensor if tensor is not None else (
+        torch.from_numpy(x32).to(torch.bfloat16 if dtype == "bf16" else torch.float32).cuda())
+    m = pk.attn_fp8_quantize(t)
+    torch.cuda.synchronize()
+    ref = orc.quantize(x32.astype(np.float64))
+    for f in ("code_row", "scale_row", "code_col", "scale_col"):
+        got = getattr(m, f).cpu().numpy()
+        if not np.array_equal(got, ref[f]):
+            bad = np.argwhere(got != ref[f])
+            raise AssertionError(f"{f}: {len(bad)} mismatches, first at {bad[:3].tolist()}: "
+                                 f"gpu {got[tuple(bad[0])]:#x} oracle {ref[f][tuple(bad[0])]:#x}")
+
+
+@pytest.mark.parametrize("D", [64, 128, 192, 256])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_random_blocks(D, dtype):
+    say(f"quantize random D={D} {dtype}")
+    rng = np.random.default_rng(D)
+    B, N, H = 2, 96, 3
+    x = (rng.standard_normal((B, N, H, D)) * np.exp(rng.uniform(-20, 20, (B, N, H, 1)))).astype(np.float32)
+    if dtype == "bf16":
+        x = torch.from_numpy(x).to(torch.bfloat16).float().numpy()
+    _cmp(x, dtype)
+
+
+def test_every_bf16_value():
+    """All 65024 finite bfloat16 bit patterns, sorted (neighbouring magnitudes
+    share blocks, exercising every scale exponent) and shuffled."""
+    say("quantize exhaustive bf16")
+    bits = np.arange(65536, dtype=np.uint32)
+    finite = ((bits >> 7) & 0xFF) != 0xFF
+    vals = (bits[finite] << 16).view(np.float32)
+    for order in ("sorted", "shuffled"):
+        v = np.sort(vals) if order == "sorted" else np.random.default_rng(0).permutation(vals)
+        pad = (-len(v)) % (128 * 32)
+        v = np.concatenate([v, np.zeros(pad, np.float32)]).reshape(1, -1, 1, 128)
+        _cmp(v, "bf16")
+
+
+def test_edge_blocks_f32():
+    say("quantize edge blocks")
+    rng = np.random.default_rng(5)
+    D, N = 64, 64
+    x = np.zeros((1, N, 1, D), np.float32)
+    ks = np.arange(-140, 120, 4)
+    for r in range(N):
+        k = ks[r % len(ks)]
+        row = rng.standard_normal(D).astype(np.float32) * np.float32(2.0 ** k)
+        amax = np.float32(448.0 * 2.0 ** k) if k > -149 else np.float32(0)
+        kind = r % 4
+        if kind == 1:
+            amax = np.nextafter(amax, np.float32(np.inf))
+        elif kind == 2:
+            amax = np.nextafter(amax, np.float32(0))
+        row[::7] = 0.0
+        row[3] = amax
+        row[5] = -amax
+        if r % 9 == 0:
+            row[:] = 0.0
+        if r % 11 == 0:
+            row[:] = -0.0
+        x[0, r, 0] = row
+    # FP32 subnormal-only blocks
+    x[0, 60, 0, :32] = np.float32(1e-39) * np.arange(32, dtype=np.float32)
+    x[0, 61, 0, :] = -np.float32(1.1e-38)
+    _cmp(x, "f32")
+
+
+def test_strided_input_and_nonfinite_count():
+    say("quantize strided + nonfinite")
+    rng = np.random.default_rng(9)
+    big = rng.standard_normal((2, 64, 6, 128)).astype(np.float32)
+    tb = torch.from_numpy(big).cuda()
+    view = tb[:, :, ::2, :]                       # head stride 2*D
+    _cmp(np.ascontiguousarray(big[:, :, ::2, :]), "f32", tensor=view)
+    x = torch.zeros((1, 32, 1, 64), dtype=torch.float32, device="cuda")
+    x[0, 3, 0, 5] = float("inf")
+    x[0, 7, 0, 1] = float("nan")
+    cnt = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pk.attn_fp8_quantize(x, nonfinite=cnt)
+    torch.cuda.synchronize()
+    assert int(cnt.item()) == 2
+
+
+def test_empty_and_row_only():
+    say("quantize empty / row-only")
+    x = torch.zeros((1, 0, 2, 64), dtype=torch.bfloat16, device="cuda")
+    m = pk.attn_fp8_quantize(x)
+    assert m.code_row.numel() == 0
+    rng = np.random.default_rng(2)
+    xs = rng.standard_normal((1, 64, 2, 128)).astype(np.float32)
+    m = pk.attn_fp8_quantize(torch.from_numpy(xs).cuda(), which=pk.QUANT_ROW)
+    torch.cuda.synchronize()
+    assert m.code_col is None
+    ref = orc.quantize(xs.astype(np.float64))
+    assert np.array_equal(m.code_row.cpu().numpy(), ref["code_row"])
