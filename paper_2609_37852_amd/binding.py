@@ -38,7 +38,8 @@ class _Problem(ctypes.Structure):
 
 class _MX(ctypes.Structure):
     _fields_ = [("code_row", ctypes.c_void_p), ("scale_row", ctypes.c_void_p),
-                ("code_col", ctypes.c_void_p), ("scale_col", ctypes.c_void_p)]
+                ("code_col", ctypes.c_void_p), ("scale_col", ctypes.c_void_p),
+                ("channel_amax", ctypes.c_void_p)]
 
 
 _I64x3 = ctypes.c_int64 * 3
@@ -117,31 +118,36 @@ class Problem:
 
 @dataclass
 class MX:
-    """MX copies of one operand X[B, N, H, D] (device uint8 tensors)."""
+    """MX copies of one operand X[B, N, H, D] (device uint8 tensors) and its
+    optional per-channel maxima [B, H, D] (float32)."""
     code_row: torch.Tensor | None
     scale_row: torch.Tensor | None
     code_col: torch.Tensor | None
     scale_col: torch.Tensor | None
+    channel_amax: torch.Tensor | None = None
 
     def c(self):
         return _MX(*(t.data_ptr() if t is not None else None
-                     for t in (self.code_row, self.scale_row, self.code_col, self.scale_col)))
+                     for t in (self.code_row, self.scale_row, self.code_col, self.scale_col, self.channel_amax)))
 
     @staticmethod
-    def empty(B, N, H, D, device, which=QUANT_BOTH):
+    def empty(B, N, H, D, device, which=QUANT_BOTH, amax=True):
         u8 = dict(dtype=torch.uint8, device=device)
         row = which & QUANT_ROW
         col = which & QUANT_COL
         return MX(torch.empty((B, H, N, D), **u8) if row else None,
                   torch.empty((B, H, N, D // 32), **u8) if row else None,
                   torch.empty((B, H, D, N), **u8) if col else None,
-                  torch.empty((B, H, D, N // 32), **u8) if col else None)
+                  torch.empty((B, H, D, N // 32), **u8) if col else None,
+                  torch.empty((B, H, D), dtype=torch.float32, device=device) if (amax and col) else None)
 
 
-def attn_fp8_quantize(x: torch.Tensor, which: int = QUANT_BOTH, nonfinite: torch.Tensor | None = None) -> MX:
-    """x: [B, N, H, D] bf16/f32 on the GPU -> MX copies (App. B.6.1)."""
+def attn_fp8_quantize(x: torch.Tensor, which: int = QUANT_BOTH, nonfinite: torch.Tensor | None = None,
+                      amax: bool = True) -> MX:
+    """x: [B, N, H, D] bf16/f32 on the GPU -> MX copies (App. B.6.1), plus the
+    per-channel maxima that enable the isolated score channel (amax=True)."""
     B, N, H, D = x.shape
-    out = MX.empty(B, N, H, D, x.device, which)
+    out = MX.empty(B, N, H, D, x.device, which, amax=amax)
     m = out.c()
     _check("attn_fp8_quantize",
            lib().attn_fp8_quantize(_ptr(x), _dtype_code(x.dtype), B, N, H, D, _strides_bnh(x), ctypes.byref(m),

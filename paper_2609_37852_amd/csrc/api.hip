@@ -106,6 +106,13 @@ afp8::AttnArgs base_args(const attn_fp8_problem* p) {
   return a;
 }
 
+// Per-channel maxima of Q and K enable the isolated score channel.
+void set_amax(afp8::AttnArgs& a, const attn_fp8_mx* q, const attn_fp8_mx* k) {
+  const bool both = q && k && q->channel_amax && k->channel_amax;
+  a.q_amax = both ? q->channel_amax : nullptr;
+  a.k_amax = both ? k->channel_amax : nullptr;
+}
+
 void set_row(const attn_fp8_mx* m, const uint8_t*& code, const uint8_t*& scale) {
   code = m->code_row;
   scale = m->scale_row;
@@ -161,6 +168,7 @@ int launch_delta(const attn_fp8_problem* p, int mode, const attn_fp8_mx* q, cons
     set_row(k, a.k_code, a.k_scale);
     set_row(v, a.v_code, a.v_scale);
     set_row(dout, a.do_code, a.do_scale);
+    set_amax(a, q, k);
     a.lse = lse;
     a.delta_out = delta;
     return hip_status(afp8::launch_delta_matching(a, (int)p->dim_qk, (int)p->dim_v, stream), "delta_matching");
@@ -203,6 +211,10 @@ int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t 
   if ((rc = check_ptr("x", x)) || (rc = check_strides("x", strides, es)) ||
       (rc = check_mx("out", out, which & 1, which & 2)))
     return rc;
+  if (out->channel_amax) {
+    if (!(which & 2)) return fail(ATTN_FP8_EINVAL, "channel_amax needs the col copy (which & COL)");
+    if ((rc = check_ptr("out.channel_amax", out->channel_amax))) return rc;
+  }
   afp8::QuantArgs a{};
   a.x = x;
   a.sb = strides[0];
@@ -217,6 +229,7 @@ int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t 
   a.scale_col = out->scale_col;
   a.which = which;
   a.nonfinite = nonfinite_count;
+  a.chan_amax = out->channel_amax;
   if ((rc = hip_status(afp8::launch_quantize(a, (int)D, x_dtype == ATTN_FP8_DTYPE_BF16, stream), "quantize")))
     return rc;
   return ok();
@@ -236,6 +249,7 @@ int attn_fp8_fwd(const attn_fp8_problem* p, const attn_fp8_mx* q, const attn_fp8
   set_row(q, a.q_code, a.q_scale);
   set_row(k, a.k_code, a.k_scale);
   set_col(v, a.vc_code, a.vc_scale);
+  set_amax(a, q, k);
   a.o = o;
   for (int i = 0; i < 3; i++) a.os[i] = o_strides[i];
   a.o_bf16 = o_dtype == ATTN_FP8_DTYPE_BF16;
@@ -321,6 +335,7 @@ int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q
   set_col(q, a.qc_code, a.qc_scale);
   set_col(k, a.kc_code, a.kc_scale);
   set_col(dout, a.doc_code, a.doc_scale);
+  set_amax(a, q, k);
   a.lse = lse;
   a.delta = delta;
   a.dq_acc = dq_acc;

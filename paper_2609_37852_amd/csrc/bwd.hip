@@ -88,6 +88,8 @@ __global__ __launch_bounds__(64 * NWK) void bwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t sdSs[NWK * 2];
   __shared__ __attribute__((aligned(16))) float sL[BQ];
   __shared__ __attribute__((aligned(16))) float sD[BQ * 2];
+  __shared__ __attribute__((aligned(16))) float sQh[BQ];
+  __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
   const int64_t kb0 = (int64_t)blockIdx.x * BKB;  // key block (block 0 has the most work)
@@ -95,6 +97,7 @@ __global__ __launch_bounds__(64 * NWK) void bwd_kernel(AttnArgs a) {
   const int64_t kw0 = kb0 + 32 * w;                 // this wave's first key
   const bool live = kw0 < a.N;
   const int64_t kj = kw0 + li;                      // this lane's key
+  const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
 
   // K and V row codes of this lane's key (B operands of S and dP)
   v8i kf[KS], vf[VS];
@@ -108,6 +111,7 @@ __global__ __launch_bounds__(64 * NWK) void bwd_kernel(AttnArgs a) {
 #pragma unroll
     for (int s = 0; s < KS; s++) {
       kf[s] = frag_rows_global(a.k_code + row * DQK, s, hf);
+      clear_channel(kf[s], s, hf, hot);
       ksc[s] = a.k_scale[row * (DQK / 32) + 2 * s + hf];
     }
 #pragma unroll
@@ -116,6 +120,7 @@ __global__ __launch_bounds__(64 * NWK) void bwd_kernel(AttnArgs a) {
       vsc[s] = a.v_scale[row * (DV / 32) + 2 * s + hf];
     }
   }
+  const float khot = (live && hot >= 0) ? row_value<DQK>(a.k_code, a.k_scale, (b * a.Hkv + kh) * a.N + kj, hot) : 0.f;
   // K col codes of the workgroup's keys (B operand of dQ), once
   stage_col_slice<DQK, BKB, KCST, NT>(sKc, sKcs, a.kc_code + (b * a.Hkv + kh) * (int64_t)DQK * a.N,
                                       a.kc_scale + (b * a.Hkv + kh) * (int64_t)DQK * (a.N / 32), kb0, a.N);
@@ -138,7 +143,8 @@ __global__ __launch_bounds__(64 * NWK) void bwd_kernel(AttnArgs a) {
     for (int64_t qt = qt0; qt < nqt; qt++) {
       const int64_t i0 = qt * BQ;
       __syncthreads();
-      stage_rows<BQ, DQK, QST, NT>(sQ, sQs, a.q_code + bh * a.N * DQK, a.q_scale + bh * a.N * (DQK / 32), i0, a.N);
+      stage_rows<BQ, DQK, QST, NT>(sQ, sQs, a.q_code + bh * a.N * DQK, a.q_scale + bh * a.N * (DQK / 32), i0, a.N,
+                                   hot);
       stage_rows<BQ, DV, OST, NT>(sO, sOs, a.do_code + bh * a.N * DV, a.do_scale + bh * a.N * (DV / 32), i0, a.N);
       stage_cols_perm<DQK, CST, NT>(sQc, sQcs, a.qc_code + bh * (int64_t)DQK * a.N,
                                     a.qc_scale + bh * (int64_t)DQK * (a.N / 32), i0, a.N);
@@ -149,6 +155,7 @@ __global__ __launch_bounds__(64 * NWK) void bwd_kernel(AttnArgs a) {
         sL[u] = ok ? a.lse[bh * a.N + i0 + u] * kLog2e : 0.f;
         sD[2 * u] = ok ? a.delta[(bh * a.N + i0 + u) * 2] : 0.f;
         sD[2 * u + 1] = ok ? a.delta[(bh * a.N + i0 + u) * 2 + 1] : 0.f;
+        sQh[u] = (ok && hot >= 0) ? row_value<DQK>(a.q_code, a.q_scale, bh * a.N + i0 + u, hot) : 0.f;
       }
       __syncthreads();
 
@@ -181,13 +188,15 @@ __global__ __launch_bounds__(64 * NWK) void bwd_kernel(AttnArgs a) {
             const float4 Lg = *reinterpret_cast<const float4*>(&sL[qo]);
             const float4 d01 = *reinterpret_cast<const float4*>(&sD[2 * qo]);
             const float4 d23 = *reinterpret_cast<const float4*>(&sD[2 * qo + 4]);
+            const float4 qh = *reinterpret_cast<const float4*>(&sQh[qo]);
+            const float Qh[4] = {qh.x, qh.y, qh.z, qh.w};
             const float Lv[4] = {Lg.x, Lg.y, Lg.z, Lg.w};
             const float Hv[4] = {d01.x, d01.z, d23.x, d23.z};
             const float Lo[4] = {d01.y, d01.w, d23.y, d23.w};
 #pragma unroll
             for (int e = 0; e < 4; e++) {
               const int r = 4 * g + e;
-              float p = bwd_prob(s[r], a.c, Lv[e]);
+              float p = bwd_prob(__builtin_fmaf(Qh[e], khot, s[r]), a.c, Lv[e]);
               if (needmask) {
                 const int64_t qi = i0 + qo + e;
                 p = (kj > qi || qi >= a.N) ? 0.f : p;

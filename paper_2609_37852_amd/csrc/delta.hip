@@ -30,6 +30,8 @@ __global__ __launch_bounds__(64 * NW) void delta_matching_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t sKs[BK * DQK / 32];
   __shared__ __attribute__((aligned(16))) uint8_t sV[BK * VST];
   __shared__ __attribute__((aligned(16))) uint8_t sVs[BK * DV / 32];
+  __shared__ __attribute__((aligned(16))) float sKh[BK];
+  __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
   const int64_t nqb = (a.N + BQ - 1) / BQ;
@@ -38,6 +40,7 @@ __global__ __launch_bounds__(64 * NW) void delta_matching_kernel(AttnArgs a) {
   const int64_t q0 = qb * BQ + 32 * w;
   const bool live = q0 < a.N;
   const int64_t qi = q0 + li;
+  const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
 
   v8i qf[KS], df[VS];
   int qsc[KS], dsc[VS];
@@ -51,6 +54,7 @@ __global__ __launch_bounds__(64 * NW) void delta_matching_kernel(AttnArgs a) {
 #pragma unroll
     for (int s = 0; s < KS; s++) {
       qf[s] = frag_rows_global(a.q_code + row * DQK, s, hf);
+      clear_channel(qf[s], s, hf, hot);
       qsc[s] = a.q_scale[row * (DQK / 32) + 2 * s + hf];
     }
 #pragma unroll
@@ -60,6 +64,7 @@ __global__ __launch_bounds__(64 * NW) void delta_matching_kernel(AttnArgs a) {
     }
     L = a.lse[row] * kLog2e;
   }
+  const float qhot = (live && hot >= 0) ? row_value<DQK>(a.q_code, a.q_scale, (b * a.Hq + h) * a.N + qi, hot) : 0.f;
   double num = 0.0, den = 0.0;
 
   const int64_t qend = ((qb + 1) * BQ < a.N) ? (qb + 1) * BQ : a.N;
@@ -72,8 +77,10 @@ __global__ __launch_bounds__(64 * NW) void delta_matching_kernel(AttnArgs a) {
   for (int t = 0; t < ntiles; t++) {
     const int64_t j0 = (int64_t)t * BK;
     __syncthreads();
-    stage_rows<BK, DQK, KST, 64 * NW>(sK, sKs, kcode, kscale, j0, a.N);
+    stage_rows<BK, DQK, KST, 64 * NW>(sK, sKs, kcode, kscale, j0, a.N, hot);
     stage_rows<BK, DV, VST, 64 * NW>(sV, sVs, vcode, vscale, j0, a.N);
+    if (threadIdx.x < BK)
+      sKh[threadIdx.x] = (hot >= 0 && j0 + threadIdx.x < a.N) ? row_value<DQK>(kcode, kscale, j0 + threadIdx.x, hot) : 0.f;
     __syncthreads();
     if (!live || j0 > q0) continue;
 
@@ -95,9 +102,15 @@ __global__ __launch_bounds__(64 * NW) void delta_matching_kernel(AttnArgs a) {
         dp = mfma_mx(vf, df[st], dp, sVs[(32 * kb + li) * (DV / 32) + 2 * st + hf], dsc[st]);
       }
       float pn = 0.f, pd = 0.f;
+      float kh4[16];
+#pragma unroll
+      for (int g = 0; g < 4; g++) {
+        const float4 v4 = *reinterpret_cast<const float4*>(&sKh[32 * kb + 8 * g + 4 * hf]);
+        kh4[4 * g] = v4.x; kh4[4 * g + 1] = v4.y; kh4[4 * g + 2] = v4.z; kh4[4 * g + 3] = v4.w;
+      }
 #pragma unroll
       for (int r = 0; r < 16; r++) {
-        float p = bwd_prob(s[r], a.c, L);
+        float p = bwd_prob(__builtin_fmaf(qhot, kh4[r], s[r]), a.c, L);
         if (diag) {
           const int64_t key = j0 + 32 * kb + 8 * (r >> 2) + 4 * hf + (r & 3);
           p = key > qi ? 0.f : p;

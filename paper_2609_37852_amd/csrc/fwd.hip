@@ -33,6 +33,8 @@ __global__ __launch_bounds__(64 * NW) void fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t sKs[BK * DQK / 32];
   __shared__ __attribute__((aligned(16))) uint8_t sV[DV * VST];
   __shared__ __attribute__((aligned(16))) uint8_t sVs[DV * 2];
+  __shared__ __attribute__((aligned(16))) float sKh[BK];
+  __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
   const int64_t nqb = (a.N + BQ - 1) / BQ;
@@ -41,6 +43,7 @@ __global__ __launch_bounds__(64 * NW) void fwd_kernel(AttnArgs a) {
   const int64_t q0 = qb * BQ + 32 * w;
   const bool live = q0 < a.N;
   const int64_t qi = q0 + li;
+  const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
 
   v8i qf[KS];
   int qsc[KS];
@@ -54,9 +57,12 @@ __global__ __launch_bounds__(64 * NW) void fwd_kernel(AttnArgs a) {
 #pragma unroll
     for (int s = 0; s < KS; s++) {
       qf[s] = frag_rows_global(a.q_code + row * DQK, s, hf);
+      clear_channel(qf[s], s, hf, hot);
       qsc[s] = a.q_scale[row * (DQK / 32) + 2 * s + hf];
     }
   }
+  // the isolated channel's query value (0 without isolation)
+  const float qhot = (live && hot >= 0) ? row_value<DQK>(a.q_code, a.q_scale, (b * a.Hq + h) * a.N + qi, hot) : 0.f;
 
   v16f oacc[CB];
 #pragma unroll
@@ -76,8 +82,10 @@ __global__ __launch_bounds__(64 * NW) void fwd_kernel(AttnArgs a) {
   for (int t = ntiles - 1; t >= 0; t--) {
     const int64_t j0 = (int64_t)t * BK;
     __syncthreads();
-    stage_rows<BK, DQK, KST, 64 * NW>(sK, sKs, kcode, kscale, j0, a.N);
+    stage_rows<BK, DQK, KST, 64 * NW>(sK, sKs, kcode, kscale, j0, a.N, hot);
     stage_cols_perm<DV, VST, 64 * NW>(sV, sVs, vcode, vscale, j0, a.N);
+    if (threadIdx.x < BK)
+      sKh[threadIdx.x] = (hot >= 0 && j0 + threadIdx.x < a.N) ? row_value<DQK>(kcode, kscale, j0 + threadIdx.x, hot) : 0.f;
     __syncthreads();
     if (!live || j0 > q0) continue;  // every key of the tile is in this wave's future
 
@@ -98,9 +106,15 @@ __global__ __launch_bounds__(64 * NW) void fwd_kernel(AttnArgs a) {
 #pragma unroll
     for (int kb = 0; kb < 2; kb++) {
       float m = -__builtin_inff();
+      float kh4[16];
+#pragma unroll
+      for (int g = 0; g < 4; g++) {
+        const float4 v4 = *reinterpret_cast<const float4*>(&sKh[32 * kb + 8 * g + 4 * hf]);
+        kh4[4 * g] = v4.x; kh4[4 * g + 1] = v4.y; kh4[4 * g + 2] = v4.z; kh4[4 * g + 3] = v4.w;
+      }
 #pragma unroll
       for (int r = 0; r < 16; r++) {
-        float x = s[kb][r] * a.c;
+        float x = __builtin_fmaf(qhot, kh4[r], s[kb][r]) * a.c;
         if (diag) {
           const int64_t key = j0 + 32 * kb + 8 * (r >> 2) + 4 * hf + (r & 3);
           x = key > qi ? -__builtin_inff() : x;

@@ -15,6 +15,7 @@ struct QuantArgs {
   uint8_t *code_row, *scale_row, *code_col, *scale_col;
   int which;                 // bit 0 row copy, bit 1 col copy
   uint32_t* nonfinite;       // nullable
+  float* chan_amax;          // nullable [B, H, D]: max over tokens of |x| (zeroed before the launch)
 };
 
 struct StaleArgs {
@@ -48,6 +49,8 @@ struct AttnArgs {
   const uint8_t *kc_code, *kc_scale;   // col copy of K      [B,Hkv,Dqk,N]
   const uint8_t *vc_code, *vc_scale;   // col copy of V      [B,Hkv,Dv,N]
   const uint8_t *doc_code, *doc_scale; // col copy of dO     [B,Hq,Dv,N]
+  const float* q_amax;                 // nullable [B,Hq,Dqk] per-channel max |q|
+  const float* k_amax;                 // nullable [B,Hkv,Dqk] per-channel max |k|
   const float* lse;                    // [B,Hq,N]
   float* lse_out;
   const float* delta;                  // [B,Hq,N,2]

@@ -94,12 +94,22 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
     am = fmaxf(am, __shfl_xor(am, 1));
     const int e = pow2_exponent(am);
     *reinterpret_cast<uint4*>(a.code_col + (bh * D + c) * a.N + n0 + half * 16) = encode16(w, e);
-    if (half == 0) a.scale_col[(bh * D + c) * (a.N / 32) + n0 / 32] = (uint8_t)(e + 127);
+    if (half == 0) {
+      a.scale_col[(bh * D + c) * (a.N / 32) + n0 / 32] = (uint8_t)(e + 127);
+      // non-negative FP32 values order like their bit patterns
+      if (a.chan_amax) atomicMax(reinterpret_cast<unsigned int*>(a.chan_amax + bh * D + c), __float_as_uint(am));
+    }
   }
 }
 
+hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
+
 hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_t s) {
   dim3 grid((unsigned)(a.N / 32), (unsigned)a.H, (unsigned)a.B);
+  if (a.chan_amax) {
+    const hipError_t e = launch_fill_zero(a.chan_amax, a.B * a.H * D, s);
+    if (e != hipSuccess) return e;
+  }
 #define AFP8_Q(DD)                                                                           \
   if (D == DD) {                                                                             \
     if (dtype_bf16) hipLaunchKernelGGL((quantize_kernel<DD, uint16_t>), grid, dim3(2 * DD), 0, s, a); \

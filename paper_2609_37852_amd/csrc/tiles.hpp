@@ -8,17 +8,29 @@
 
 namespace afp8 {
 
+// Clears byte `pos` (0..15) of a 16-byte vector.
+__device__ __forceinline__ void clear_byte(uint4& v, int pos) {
+  const uint32_t m = ~(0xffu << (8 * (pos & 3)));
+  const int d = pos >> 2;
+  v.x &= d == 0 ? m : 0xffffffffu;
+  v.y &= d == 1 ? m : 0xffffffffu;
+  v.z &= d == 2 ? m : 0xffffffffu;
+  v.w &= d == 3 ? m : 0xffffffffu;
+}
+
 // Rows [r0, r0 + ROWS) of a row-major [N, D] code matrix (one batch/head)
 // into LDS with row stride ST bytes; the block's E8M0 bytes [N, D/32] into
-// a dense [ROWS][D/32] LDS array.
+// a dense [ROWS][D/32] LDS array.  zcol >= 0: that column's codes are stored
+// as zero (the isolated score channel).
 template <int ROWS, int D, int ST, int NT>
 __device__ __forceinline__ void stage_rows(uint8_t* lds, uint8_t* lds_scale, const uint8_t* code,
-                                           const uint8_t* scale, int64_t r0, int64_t N) {
+                                           const uint8_t* scale, int64_t r0, int64_t N, int zcol = -1) {
   constexpr int V = ROWS * D / 16;  // uint4 per tile
   for (int u = threadIdx.x; u < V; u += NT) {
     const int r = u / (D / 16), c = (u % (D / 16)) * 16;
     uint4 val = make_uint4(0, 0, 0, 0);
     if (r0 + r < N) val = *reinterpret_cast<const uint4*>(code + (r0 + r) * D + c);
+    if (zcol >= c && zcol < c + 16) clear_byte(val, zcol - c);
     *reinterpret_cast<uint4*>(lds + r * ST + c) = val;
   }
   constexpr int S = ROWS * D / 32;  // scale bytes
@@ -83,6 +95,53 @@ __device__ __forceinline__ v8i frag_cols(const uint8_t* lds, int row, int hf) {
   const uint4 lo = *reinterpret_cast<const uint4*>(p);
   const uint4 hi = *reinterpret_cast<const uint4*>(p + 32);
   return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
+
+// Same fragment with the isolated channel `hot` (if it falls in k-step s and
+// this lane's half) cleared.
+__device__ __forceinline__ void clear_channel(v8i& f, int s, int hf, int hot) {
+  const int cl = hot - 64 * s;
+  if (hot < 0 || cl < 0 || cl >= 64 || ((cl & 31) >> 4) != hf) return;
+  const int t = (cl < 32 ? 0 : 16) + (cl & 15);  // byte of the fragment holding channel `hot`
+  const uint32_t m = ~(0xffu << (8 * (t & 3)));
+#pragma unroll
+  for (int d = 0; d < 8; d++) f[d] = (int)((uint32_t)f[d] & (d == (t >> 2) ? m : 0xffffffffu));
+}
+
+// Decoded value of the element in column `col` of row `row` of a row copy.
+template <int D>
+__device__ __forceinline__ float row_value(const uint8_t* code, const uint8_t* scale, int64_t row, int col) {
+  const float v = fp8_value(code[row * D + col], 0);
+  return __builtin_ldexpf(v, (int)scale[row * (D / 32) + col / 32] - 127);
+}
+
+// The isolated score channel of KV head kh (see attn_fp8.h): argmax over c of
+// max_{h in group} q_amax[b,h,c] * k_amax[b,kh,c], lowest index on ties, or
+// -1 without the per-channel maxima.  Computed by wave 0; every thread of the
+// block returns the same value (contains a barrier).
+template <int D>
+__device__ __forceinline__ int select_hot_channel(const float* q_amax, const float* k_amax, int64_t b, int64_t kh,
+                                                  int64_t Hq, int64_t Hkv, int64_t G, int* slot) {
+  if (!q_amax || !k_amax) return -1;
+  if (threadIdx.x < 64) {
+    float best = -1.f;
+    int bi = D;
+    for (int c = threadIdx.x; c < D; c += 64) {
+      float qm = 0.f;
+      for (int64_t g = 0; g < G; g++) qm = fmaxf(qm, q_amax[(b * Hq + kh * G + g) * D + c]);
+      const float sc = qm * k_amax[(b * Hkv + kh) * D + c];
+      if (sc > best) { best = sc; bi = c; }
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      const float ob = __shfl_xor(best, m);
+      const int oi = __shfl_xor(bi, m);
+      if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
+    }
+    if (threadIdx.x == 0) *slot = bi < D ? bi : -1;
+  }
+  __syncthreads();
+  return *slot;
 }
 
 }  // namespace afp8

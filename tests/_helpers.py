@@ -35,10 +35,11 @@ def problem(w: synth.Workload) -> pk.Problem:
 
 
 def run_gpu(w, d, mode=pk.DELTA_MATCHING, grad_dtype=torch.float32, o_dtype=torch.bfloat16, rowstats=True,
-            delta_in=None):
-    """Quantize, forward, correction and backward on the GPU."""
+            delta_in=None, isolate=True):
+    """Quantize, forward, correction and backward on the GPU.  isolate=False
+    drops the per-channel maxima (no isolated score channel)."""
     q, k, v, do = (to_dev(d[n], w.dtype) for n in ("q", "k", "v", "do"))
-    mq, mk, mv, mdo = (pk.attn_fp8_quantize(t) for t in (q, k, v, do))
+    mq, mk, mv, mdo = (pk.attn_fp8_quantize(t, amax=isolate) for t in (q, k, v, do))
     p = problem(w)
     o, lse = pk.attn_fp8_fwd(p, mq, mk, mv, o_dtype=o_dtype)
     delta = pk.attn_fp8_delta(p, mode, mq, mk, mv, mdo, lse, do, o)

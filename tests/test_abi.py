@@ -33,7 +33,7 @@ def _prob(**kw):
 
 
 def _fake_mx(addr=4096):
-    return bd._MX(addr, addr, addr, addr)
+    return bd._MX(addr, addr, addr, addr, None)
 
 
 @pytest.mark.parametrize("kw,code", [

@@ -54,7 +54,26 @@ def test_parity(name, kw, mode):
         rep = invariant_report(g["rowstats"], o["rowstats"])
         say("  invariant", rep)
         assert rep["violations"] == 0, rep
-        assert rep["graded"] > 0.5 * (rep["graded"] + rep["excluded"])
+        # near-one-hot rows (outlier workload) are excluded by the cond filter and reported
+        assert rep["graded"] >= 0.25 * (rep["graded"] + rep["excluded"])
+
+
+def test_isolated_channel_on_outlier_workload():
+    """The outlier-channel workload: with the isolated score channel the
+    output errors fall far below the bound; without it the MFMA's grouped
+    accumulation costs an order of magnitude (reported, not asserted)."""
+    w = _workload("gqa_d128_8k", dict(B=1, N=512, Hq=4, Hkv=1))
+    d = synth.generate(w, seed=2)
+    o = run_oracle(w, d)
+    res = {}
+    for iso in (True, False):
+        g = run_gpu(w, d, isolate=iso, rowstats=False)
+        res[iso] = {k: rel_err(g[k], o[k]) for k in ("O", "dQ", "dK", "dV")}
+        res[iso]["LSE"] = float(np.max(np.abs(g["LSE"] - o["LSE"])))
+    say("  isolated", res[True], "\n  plain   ", res[False])
+    for k in ("O", "dQ", "dK", "dV"):
+        assert res[True][k] <= REL_TOL / 4, (k, res[True][k])
+    assert res[True]["LSE"] < 1e-3
 
 
 def test_delta_mode_changes_only_dq_dk():

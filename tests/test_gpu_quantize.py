@@ -18,6 +18,8 @@ def _cmp(x32: np.ndarray, dtype: str, tensor=None):
     m = pk.attn_fp8_quantize(t)
     torch.cuda.synchronize()
     ref = orc.quantize(x32.astype(np.float64))
+    # per-channel maxima over the sequence (exact: a max of float32 values)
+    assert np.array_equal(m.channel_amax.cpu().numpy(), np.abs(x32).max(axis=1).astype(np.float32))
     for f in ("code_row", "scale_row", "code_col", "scale_col"):
         got = getattr(m, f).cpu().numpy()
         if not np.array_equal(got, ref[f]):
