@@ -1,22 +1,26 @@
 // Forward pass (Sec. 2.3; App. B.6.2 with power-of-two probability scales).
 //
 // Workgroup: NW waves, 32 queries each, one (batch, query head).  Key tiles of
-// 64 are staged once in LDS and shared by the waves, visited from the causal
-// diagonal down to key 0.
+// BK = 128 are double-buffered in LDS (global loads for the next tile are in
+// flight while the current one is computed; one barrier per tile) and visited
+// from the causal diagonal down to key 0.
 //
-// Per wave and tile:
+// Per wave and tile (4 aligned 32-key groups):
 //   S^T = K Q^T       MX MFMA, A = K row tile (LDS), B = Q row codes (regs);
 //                     lane l owns query l % 32 and holds 16 keys of each
-//                     32-key half, so row reductions are in-lane plus one
-//                     exchange with lane l ^ 32.
-//   x = S * tau*log2e, masked keys -> -inf.
-//   M = integer running max (ceil of the row max).  When it grows, O and l
-//       are multiplied by 2^(M_old - M_new), an exact power of two.
+//                     group, so row reductions are in-lane plus one exchange
+//                     with lane l ^ 32.  The isolated score channel (if any)
+//                     is added with one FMA.
+//   M = integer running max of x = S tau log2e (ceil of the row max).  When it
+//       grows, O and l are multiplied by 2^(M_old - M_new), an exact power of
+//       two (decided per wave; at most a few times per row).
 //   p = 2^(x - M) (FP32, before any cast) feeds l.
-//   per aligned 32-key group g: E_g = smallest integer with max_g p <= 448 * 2^E_g,
-//       codes C8(p / 2^E_g) -- the group scale of the probability operand.
+//   group g: E_g = smallest integer with 2^(x_g - M) <= 448 * 2^E_g (x_g the
+//       group max), codes C8(p / 2^E_g) -- the group's probability scale.
 //   O^T += V^T P^T    MX MFMA, A = V col tile (LDS, permuted to the lane's
 //                     keys), B = probability codes straight from registers.
+// Only the group holding the diagonal needs a mask; groups wholly in a wave's
+// future skip their MFMA and exponentials.
 // Epilogue: O = O_acc / l (bf16 or fp32), LSE = (M + log2 l) ln 2.
 #include "common.hpp"
 #include "kernels.hpp"
@@ -24,45 +28,137 @@
 
 namespace afp8 {
 
+constexpr float kLog2_448 = 8.807354922057604f;
+
 template <int DQK, int DV, int NW>
-__global__ __launch_bounds__(64 * NW) void fwd_kernel(AttnArgs a) {
-  constexpr int BQ = 32 * NW, BK = 64;
+struct FwdTile {
+  static constexpr int BK = 128, NT = 64 * NW;
+  static constexpr int KST = DQK + 16, VST = BK + 16;
+  static constexpr int KU = BK * DQK / 16 / NT;   // uint4 of K codes per thread
+  static constexpr int VU = DV * BK / 16 / NT;    // uint4 of V codes per thread
+  static_assert(KU * NT * 16 == BK * DQK && VU * NT * 16 == DV * BK, "tile split");
+  static_assert(DQK <= NT && DV <= NT && BK <= NT, "one scale word / hot value per thread");
+};
+
+// Registers holding one tile in flight from global memory.
+template <int DQK, int DV, int NW>
+struct FwdPrefetch {
+  using T = FwdTile<DQK, DV, NW>;
+  uint4 k[T::KU];
+  uint4 v[T::VU];
+  uint32_t ks;     // 4 K scale bytes (thread < DQK)
+  uint32_t vs;     // 4 V scale bytes of one channel (thread < DV)
+  float kh;        // isolated-channel value of one key (thread < BK)
+};
+
+template <int DQK, int DV, int NW>
+__device__ __forceinline__ void fwd_load(FwdPrefetch<DQK, DV, NW>& f, const uint8_t* kcode, const uint8_t* kscale,
+                                         const uint8_t* vcode, const uint8_t* vscale, int j0, int N, int hot) {
+  using T = FwdTile<DQK, DV, NW>;
+  const int tid = threadIdx.x;
+  // K rows [j0, j0 + BK): contiguous; rows past N read the last valid bytes
+  // (finite codes whose scores the causal mask removes)
+  const int klim = (N - j0) * DQK - 16;
+#pragma unroll
+  for (int i = 0; i < T::KU; i++) {
+    const int off = (tid + i * T::NT) * 16;
+    f.k[i] = *reinterpret_cast<const uint4*>(kcode + (size_t)j0 * DQK + (off < klim ? off : klim));
+  }
+  // V col rows: channel c, keys [j0, j0 + BK) in 16-byte pieces
+#pragma unroll
+  for (int i = 0; i < T::VU; i++) {
+    const int u = tid + i * T::NT, c = u / (T::BK / 16), q = u % (T::BK / 16);
+    const int col = j0 + q * 16 < N - 16 ? j0 + q * 16 : N - 16;
+    f.v[i] = *reinterpret_cast<const uint4*>(vcode + (size_t)c * N + col);
+  }
+  if (tid < DQK) {  // K scales: BK rows x DQK/32 bytes = DQK dwords, clamped to the head's array
+    const int off = j0 * (DQK / 32) + tid * 4, lim = N * (DQK / 32) - 4;
+    f.ks = *reinterpret_cast<const uint32_t*>(kscale + (off < lim ? off : lim));
+  }
+  if (tid < DV) {   // V scales: 4 groups of channel tid
+    uint32_t w = 0;
+#pragma unroll
+    for (int g = 0; g < 4; g++) {
+      const int grp = (j0 + 32 * g < N ? j0 + 32 * g : N - 32) / 32;
+      w |= (uint32_t)vscale[(size_t)tid * (N / 32) + grp] << (8 * g);
+    }
+    f.vs = w;
+  }
+  if (tid < T::BK) {
+    const int r = j0 + tid < N ? j0 + tid : N - 1;
+    f.kh = hot >= 0 ? row_value<DQK>(kcode, kscale, r, hot) : 0.f;
+  }
+}
+
+template <int DQK, int DV, int NW>
+__device__ __forceinline__ void fwd_store(const FwdPrefetch<DQK, DV, NW>& f, uint8_t* sK, uint8_t* sKs, uint8_t* sV,
+                                          uint8_t* sVs, float* sKh, int hot) {
+  using T = FwdTile<DQK, DV, NW>;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < T::KU; i++) {
+    const int off = (tid + i * T::NT) * 16;
+    const int r = off / DQK, c = off % DQK;
+    uint4 val = f.k[i];
+    if (hot >= c && hot < c + 16) clear_byte(val, hot - c);
+    *reinterpret_cast<uint4*>(sK + r * T::KST + c) = val;
+  }
+#pragma unroll
+  for (int i = 0; i < T::VU; i++) {
+    const int u = tid + i * T::NT, c = u / (T::BK / 16), q = u % (T::BK / 16);
+    // 16 keys 16q..16q+15: group q/2; within the group, 4-key chunks go to
+    // position 16 * (chunk & 1) + 4 * (chunk >> 1) (see stage_cols_perm)
+    uint8_t* base = sV + c * T::VST + (q >> 1) * 32 + (q & 1) * 8;
+    *reinterpret_cast<uint2*>(base) = make_uint2(f.v[i].x, f.v[i].z);
+    *reinterpret_cast<uint2*>(base + 16) = make_uint2(f.v[i].y, f.v[i].w);
+  }
+  if (tid < DQK) *reinterpret_cast<uint32_t*>(sKs + tid * 4) = f.ks;
+  if (tid < DV) *reinterpret_cast<uint32_t*>(sVs + tid * 4) = f.vs;
+  if (tid < T::BK) sKh[tid] = f.kh;
+}
+
+template <int DQK, int DV, int NW>
+__global__ __launch_bounds__(64 * NW, 2) void fwd_kernel(AttnArgs a) {
+  using T = FwdTile<DQK, DV, NW>;
+  constexpr int BQ = 32 * NW, BK = T::BK;
   constexpr int KS = DQK / 64, CB = DV / 32;
-  constexpr int KST = DQK + 16, VST = BK + 16;
-  __shared__ __attribute__((aligned(16))) uint8_t sK[BK * KST];
-  __shared__ __attribute__((aligned(16))) uint8_t sKs[BK * DQK / 32];
-  __shared__ __attribute__((aligned(16))) uint8_t sV[DV * VST];
-  __shared__ __attribute__((aligned(16))) uint8_t sVs[DV * 2];
-  __shared__ __attribute__((aligned(16))) float sKh[BK];
+  __shared__ __attribute__((aligned(16))) uint8_t sK[2][BK * T::KST];
+  __shared__ __attribute__((aligned(16))) uint8_t sKs[2][BK * DQK / 32];
+  __shared__ __attribute__((aligned(16))) uint8_t sV[2][DV * T::VST];
+  __shared__ __attribute__((aligned(16))) uint8_t sVs[2][DV * 4];
+  __shared__ __attribute__((aligned(16))) float sKh[2][BK];
   __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
-  const int64_t nqb = (a.N + BQ - 1) / BQ;
-  const int64_t qb = nqb - 1 - (int64_t)blockIdx.x;  // longest causal rows first
-  const int64_t h = blockIdx.y, b = blockIdx.z, kh = h / a.G;
-  const int64_t q0 = qb * BQ + 32 * w;
-  const bool live = q0 < a.N;
-  const int64_t qi = q0 + li;
+  const int N = (int)a.N;
+  const int nqb = (N + BQ - 1) / BQ;
+  const int qb = nqb - 1 - (int)blockIdx.x;  // longest causal rows first
+  const int h = blockIdx.y, b = blockIdx.z, kh = h / (int)a.G;
+  const int q0 = qb * BQ + 32 * w;
+  const bool live = q0 < N;
+  const int qi = q0 + li;
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
+
+  const size_t bhq = (size_t)b * a.Hq + h, bhk = (size_t)b * a.Hkv + kh;
+  const uint8_t* kcode = a.k_code + bhk * N * DQK;
+  const uint8_t* kscale = a.k_scale + bhk * N * (DQK / 32);
+  const uint8_t* vcode = a.vc_code + bhk * DV * N;
+  const uint8_t* vscale = a.vc_scale + bhk * DV * (N / 32);
 
   v8i qf[KS];
   int qsc[KS];
-#pragma unroll
-  for (int s = 0; s < KS; s++) {
-    qf[s] = v8i{0, 0, 0, 0, 0, 0, 0, 0};
-    qsc[s] = 0;
-  }
-  if (live) {
-    const int64_t row = (b * a.Hq + h) * a.N + qi;
+  float qhot = 0.f;
+  {
+    const int row = live ? qi : 0;
+    const uint8_t* qrow = a.q_code + (bhq * N + row) * DQK;
 #pragma unroll
     for (int s = 0; s < KS; s++) {
-      qf[s] = frag_rows_global(a.q_code + row * DQK, s, hf);
+      qf[s] = frag_rows_global(qrow, s, hf);
       clear_channel(qf[s], s, hf, hot);
-      qsc[s] = a.q_scale[row * (DQK / 32) + 2 * s + hf];
+      qsc[s] = a.q_scale[(bhq * N + row) * (DQK / 32) + 2 * s + hf];
     }
+    if (hot >= 0) qhot = row_value<DQK>(a.q_code + bhq * N * DQK, a.q_scale + bhq * N * (DQK / 32), row, hot);
   }
-  // the isolated channel's query value (0 without isolation)
-  const float qhot = (live && hot >= 0) ? row_value<DQK>(a.q_code, a.q_scale, (b * a.Hq + h) * a.N + qi, hot) : 0.f;
 
   v16f oacc[CB];
 #pragma unroll
@@ -71,114 +167,132 @@ __global__ __launch_bounds__(64 * NW) void fwd_kernel(AttnArgs a) {
     for (int r = 0; r < 16; r++) oacc[cb][r] = 0.f;
   float M = -__builtin_inff();
   float lsum = 0.f;
+  const float c = a.c;
 
-  const int64_t qend = ((qb + 1) * BQ < a.N) ? (qb + 1) * BQ : a.N;
-  const int ntiles = (int)((qend + BK - 1) / BK);
-  const uint8_t* kcode = a.k_code + (b * a.Hkv + kh) * a.N * DQK;
-  const uint8_t* kscale = a.k_scale + (b * a.Hkv + kh) * a.N * (DQK / 32);
-  const uint8_t* vcode = a.vc_code + (b * a.Hkv + kh) * (int64_t)DV * a.N;
-  const uint8_t* vscale = a.vc_scale + (b * a.Hkv + kh) * (int64_t)DV * (a.N / 32);
+  const int qend = (qb + 1) * BQ < N ? (qb + 1) * BQ : N;
+  const int ntiles = (qend + BK - 1) / BK;
+  FwdPrefetch<DQK, DV, NW> pf;
+  fwd_load<DQK, DV, NW>(pf, kcode, kscale, vcode, vscale, (ntiles - 1) * BK, N, hot);
+  fwd_store<DQK, DV, NW>(pf, sK[0], sKs[0], sV[0], sVs[0], sKh[0], hot);
+  __syncthreads();
 
-  for (int t = ntiles - 1; t >= 0; t--) {
-    const int64_t j0 = (int64_t)t * BK;
-    __syncthreads();
-    stage_rows<BK, DQK, KST, 64 * NW>(sK, sKs, kcode, kscale, j0, a.N, hot);
-    stage_cols_perm<DV, VST, 64 * NW>(sV, sVs, vcode, vscale, j0, a.N);
-    if (threadIdx.x < BK)
-      sKh[threadIdx.x] = (hot >= 0 && j0 + threadIdx.x < a.N) ? row_value<DQK>(kcode, kscale, j0 + threadIdx.x, hot) : 0.f;
-    __syncthreads();
-    if (!live || j0 > q0) continue;  // every key of the tile is in this wave's future
+  for (int it = 0; it < ntiles; it++) {
+    const int cur = it & 1;
+    const int j0 = (ntiles - 1 - it) * BK;
+    if (it + 1 < ntiles) fwd_load<DQK, DV, NW>(pf, kcode, kscale, vcode, vscale, j0 - BK, N, hot);
 
-    v16f s[2];
+    if (live && j0 <= q0) {
+      const uint8_t* K = sK[cur];
+      const uint8_t* Ks = sKs[cur];
+      const float* Kh = sKh[cur];
+      const uint8_t* V = sV[cur];
+      const uint8_t* Vs = sVs[cur];
+      // two 64-key halves, each: scores -> max -> rescale -> exponentials -> P V
 #pragma unroll
-    for (int kb = 0; kb < 2; kb++) {
+      for (int hk = 0; hk < 2; hk++) {
+        if (j0 + 64 * hk > q0) break;          // both groups of this half are in the wave's future
+        v16f s[2];
+        float gm[2];
 #pragma unroll
-      for (int r = 0; r < 16; r++) s[kb][r] = 0.f;
+        for (int g2 = 0; g2 < 2; g2++) {
+          const int kb = 2 * hk + g2;
+          const int g0 = j0 + 32 * kb;         // first key of the group
+          if (g0 > q0) {                       // whole group in this wave's future
+            gm[g2] = -__builtin_inff();
+            continue;
+          }
 #pragma unroll
-      for (int st = 0; st < KS; st++) {
-        const v8i kf = frag_rows<KST>(sK, 32 * kb + li, st, hf);
-        const int ksc = sKs[(32 * kb + li) * (DQK / 32) + 2 * st + hf];
-        s[kb] = mfma_mx(kf, qf[st], s[kb], ksc, qsc[st]);
-      }
-    }
-    const bool diag = j0 + BK - 1 > q0;
-    float gmax[2];
+          for (int r = 0; r < 16; r++) s[g2][r] = 0.f;
 #pragma unroll
-    for (int kb = 0; kb < 2; kb++) {
-      float m = -__builtin_inff();
-      float kh4[16];
+          for (int st = 0; st < KS; st++)
+            s[g2] = mfma_mx(frag_rows<T::KST>(K, 32 * kb + li, st, hf), qf[st], s[g2],
+                            Ks[(32 * kb + li) * (DQK / 32) + 2 * st + hf], qsc[st]);
+          float kh16[16];
 #pragma unroll
-      for (int g = 0; g < 4; g++) {
-        const float4 v4 = *reinterpret_cast<const float4*>(&sKh[32 * kb + 8 * g + 4 * hf]);
-        kh4[4 * g] = v4.x; kh4[4 * g + 1] = v4.y; kh4[4 * g + 2] = v4.z; kh4[4 * g + 3] = v4.w;
-      }
+          for (int g = 0; g < 4; g++) {
+            const float4 v4 = *reinterpret_cast<const float4*>(&Kh[32 * kb + 8 * g + 4 * hf]);
+            kh16[4 * g] = v4.x; kh16[4 * g + 1] = v4.y; kh16[4 * g + 2] = v4.z; kh16[4 * g + 3] = v4.w;
+          }
+          float m = -__builtin_inff();
+          if (g0 == q0) {                      // the diagonal group: key offset > query offset is masked
 #pragma unroll
-      for (int r = 0; r < 16; r++) {
-        float x = __builtin_fmaf(qhot, kh4[r], s[kb][r]) * a.c;
-        if (diag) {
-          const int64_t key = j0 + 32 * kb + 8 * (r >> 2) + 4 * hf + (r & 3);
-          x = key > qi ? -__builtin_inff() : x;
+            for (int r = 0; r < 16; r++) {
+              const float t = __builtin_fmaf(qhot, kh16[r], s[g2][r]);
+              s[g2][r] = (8 * (r >> 2) + 4 * hf + (r & 3)) > li ? -__builtin_inff() : t;
+              m = fmaxf(m, s[g2][r]);
+            }
+          } else {
+#pragma unroll
+            for (int r = 0; r < 16; r++) {
+              s[g2][r] = __builtin_fmaf(qhot, kh16[r], s[g2][r]);
+              m = fmaxf(m, s[g2][r]);
+            }
+          }
+          gm[g2] = m;
         }
-        s[kb][r] = x;
-        m = fmaxf(m, x);
+        // full group maxima (raw score units) in every lane
+        gm[0] = fmaxf(gm[0], partner(gm[0]));
+        gm[1] = fmaxf(gm[1], partner(gm[1]));
+        const float mnew = fmaxf(M, __builtin_ceilf(fmaxf(gm[0], gm[1]) * c));
+        if (M == -__builtin_inff()) {
+          M = mnew;                            // first visible keys: nothing accumulated yet
+        } else if (__any(mnew > M)) {
+          const int d = (int)(M - mnew);       // 0 for lanes whose max did not move
+          const float alpha = d < -126 ? 0.f : exp2i(d);
+          lsum *= alpha;
+#pragma unroll
+          for (int cb = 0; cb < CB; cb++)
+#pragma unroll
+            for (int r = 0; r < 16; r++) oacc[cb][r] *= alpha;
+          M = mnew;
+        }
+        const float nM = -M;
+        uint32_t codes[2][4];
+        int eg[2];
+#pragma unroll
+        for (int g2 = 0; g2 < 2; g2++) {
+          if (j0 + 32 * (2 * hk + g2) > q0) {
+#pragma unroll
+            for (int k = 0; k < 4; k++) codes[g2][k] = 0u;
+            eg[g2] = -126;
+            continue;
+          }
+          // smallest E with 2^(x_g - M) <= 448 * 2^E, kept in the normal FP32 range
+          int e = (int)__builtin_ceilf(__builtin_fmaf(gm[g2], c, nM) - kLog2_448);
+          e = e < -126 ? -126 : e;
+          eg[g2] = e;
+          const float sc = exp2i(e);
+          float p[16];
+#pragma unroll
+          for (int r = 0; r < 16; r++) {
+            p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[g2][r], c, nM));
+            lsum += p[r];
+          }
+#pragma unroll
+          for (int k = 0; k < 4; k++) codes[g2][k] = cvt4_div(p[4 * k], p[4 * k + 1], p[4 * k + 2], p[4 * k + 3], sc);
+        }
+        const v8i pfr = v8i{(int)codes[0][0], (int)codes[0][1], (int)codes[0][2], (int)codes[0][3],
+                            (int)codes[1][0], (int)codes[1][1], (int)codes[1][2], (int)codes[1][3]};
+        const int psc = (hf ? eg[1] : eg[0]) + 127;
+#pragma unroll
+        for (int cb = 0; cb < CB; cb++) {
+          const uint8_t* vp = V + (32 * cb + li) * T::VST + 64 * hk + 16 * hf;
+          const uint4 lo = *reinterpret_cast<const uint4*>(vp);
+          const uint4 hi = *reinterpret_cast<const uint4*>(vp + 32);
+          const v8i vf = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+          oacc[cb] = mfma_mx(vf, pfr, oacc[cb], Vs[(32 * cb + li) * 4 + 2 * hk + hf], psc);
+        }
       }
-      gmax[kb] = m;
     }
-    // full group maxima in every lane (two exchanges with lane l ^ 32)
-    const Pair p1 = permlane32_swap(gmax[0], gmax[1]);
-    const float gown = fmaxf(p1.lo, p1.hi);
-    const Pair p2 = permlane32_swap(gown, gown);
-    const float g0 = p2.lo, g1 = p2.hi;
-
-    const float mnew = fmaxf(M, __builtin_ceilf(fmaxf(g0, g1)));
-    if (mnew > M) {
-      float alpha = 0.f;  // first visible tile: nothing accumulated yet
-      if (M != -__builtin_inff()) {
-        const int d = (int)(M - mnew);
-        alpha = d < -126 ? 0.f : exp2i(d);
-      }
-      lsum *= alpha;
-#pragma unroll
-      for (int cb = 0; cb < CB; cb++)
-#pragma unroll
-        for (int r = 0; r < 16; r++) oacc[cb][r] *= alpha;
-      M = mnew;
-    }
-    float ls = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < 2; kb++)
-#pragma unroll
-      for (int r = 0; r < 16; r++) {
-        const float p = __builtin_amdgcn_exp2f(s[kb][r] - M);
-        s[kb][r] = p;
-        ls += p;
-      }
-    lsum += ls;
-    int e0 = pow2_exponent(__builtin_amdgcn_exp2f(g0 - M));
-    int e1 = pow2_exponent(__builtin_amdgcn_exp2f(g1 - M));
-    e0 = e0 < -126 ? -126 : e0;
-    e1 = e1 < -126 ? -126 : e1;
-    const float sc0 = exp2i(e0), sc1 = exp2i(e1);
-    v8i pf;
-#pragma unroll
-    for (int k = 0; k < 4; k++) {
-      pf[k] = (int)cvt4_div(s[0][4 * k], s[0][4 * k + 1], s[0][4 * k + 2], s[0][4 * k + 3], sc0);
-      pf[4 + k] = (int)cvt4_div(s[1][4 * k], s[1][4 * k + 1], s[1][4 * k + 2], s[1][4 * k + 3], sc1);
-    }
-    const int psc = (hf ? e1 : e0) + 127;
-#pragma unroll
-    for (int cb = 0; cb < CB; cb++) {
-      const v8i vf = frag_cols<VST>(sV, 32 * cb + li, hf);
-      const int vsc = sVs[(32 * cb + li) * 2 + hf];
-      oacc[cb] = mfma_mx(vf, pf, oacc[cb], vsc, psc);
-    }
+    if (it + 1 < ntiles) fwd_store<DQK, DV, NW>(pf, sK[cur ^ 1], sKs[cur ^ 1], sV[cur ^ 1], sVs[cur ^ 1], sKh[cur ^ 1], hot);
+    __syncthreads();
   }
   if (!live) return;
   const float l = lsum + partner(lsum);
   const float inv = 1.0f / l;
   // lane (query qi, half hf) holds channels 32 cb + 8 (r/4) + 4 hf + r % 4
   if (a.o_bf16) {
-    uint16_t* orow = reinterpret_cast<uint16_t*>(a.o) + b * a.os[0] + qi * a.os[1] + h * a.os[2];
+    uint16_t* orow = reinterpret_cast<uint16_t*>(a.o) + b * a.os[0] + (int64_t)qi * a.os[1] + h * a.os[2];
 #pragma unroll
     for (int cb = 0; cb < CB; cb++)
 #pragma unroll
@@ -190,7 +304,7 @@ __global__ __launch_bounds__(64 * NW) void fwd_kernel(AttnArgs a) {
         *reinterpret_cast<uint2*>(orow + ch) = v;
       }
   } else {
-    float* orow = reinterpret_cast<float*>(a.o) + b * a.os[0] + qi * a.os[1] + h * a.os[2];
+    float* orow = reinterpret_cast<float*>(a.o) + b * a.os[0] + (int64_t)qi * a.os[1] + h * a.os[2];
 #pragma unroll
     for (int cb = 0; cb < CB; cb++)
 #pragma unroll
@@ -201,7 +315,7 @@ __global__ __launch_bounds__(64 * NW) void fwd_kernel(AttnArgs a) {
                         oacc[cb][4 * g + 3] * inv);
       }
   }
-  if (hf == 0) a.lse_out[(b * a.Hq + h) * a.N + qi] = (M + __builtin_amdgcn_logf(l)) * kLn2;
+  if (hf == 0) a.lse_out[bhq * N + qi] = (M + __builtin_amdgcn_logf(l)) * kLn2;
 }
 
 template <int DQK, int DV>
