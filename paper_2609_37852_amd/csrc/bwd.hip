@@ -4,22 +4,25 @@
 // w owns keys 32w..32w+31 of them.  The workgroup loops over the query heads
 // of the KV group and over 64-query tiles from the causal diagonal to the end
 // of the sequence.  dK and dV for its keys stay in registers (FP32) across
-// the whole loop, which is the GQA group sum.
+// the whole loop, which is the GQA group sum.  The next query tile's codes
+// are loaded into registers while the current one is computed (LDS
+// double-buffered where it fits).
 //
-// Per wave, tile and 32-query sub-block qs:
+// Per wave, tile and 32-query sub-block qs (skipped when it lies wholly
+// before the wave's keys or past the sequence; masked only on the diagonal):
 //   S  = Q K^T, dP = dO V^T   MX MFMA (A = Q / dO row tiles in LDS, B = the
 //                             wave's K / V row codes in registers); lane l
 //                             owns key l % 32 and holds 16 queries.
-//   P  = bwd_prob(S), zero for masked pairs;  dS = P ((dP - hi) - lo).
+//   P  = bwd_prob(S + q_c* k_c*), dS = P ((dP - hi) - lo).
 //   P' = C8(256 P) with scale 2^-8;  dS' = C8(dS / 2^e) with one exponent e
 //        per aligned 32x32 block (the wave's 32 keys x 32 queries).
 //   dV += P'^T dO_col,  dK += dS'^T Q_col   (A = codes straight from
 //                             registers, B = col tiles in LDS permuted to the
 //                             lane's queries).
-// dQ: every wave writes its dS' codes to LDS ([key][query]); after a barrier
-// the 64 x Dqk dQ tile = dS'(64 x BKB) K_col(BKB x Dqk) is split over the
-// waves, the dS' operand read with the 8-bit LDS transpose, and added to the
-// FP32 workspace with atomics (dQ = tau * workspace is stored by a second
+// dQ: every wave writes its dS' codes to LDS ([key][query]); after the tile's
+// barrier the 64 x Dqk dQ tile = dS'(64 x BKB) K_col(BKB x Dqk) is split over
+// the waves, the dS' operand read with the 8-bit LDS transpose, and added to
+// the FP32 workspace with atomics (dQ = tau * workspace is stored by a second
 // kernel).
 #include "common.hpp"
 #include "kernels.hpp"
@@ -27,21 +30,166 @@
 
 namespace afp8 {
 
+template <int DQK, int DV>
+struct BwdCfg {
+  // waves per workgroup and LDS buffers, sized to stay within 160 KB of LDS
+  static constexpr int NWK = (DQK + DV <= 256) ? 8 : 4;
+  static constexpr int NBUF = (DQK + DV <= 320) ? 2 : 1;   // staging buffers
+  static constexpr int NT = 64 * NWK, BKB = 32 * NWK, BQ = 64;
+  static constexpr int QST = DQK + 16, OST = DV + 16, CST = BQ + 16, KCST = BKB + 16, DST = BQ + 16;
+  static constexpr int NDS = (DQK == 128 && DV == 128) || (DQK == 64) ? 2 : 1;  // dS buffers
+  static constexpr int QU = BQ * DQK / 16, OU = BQ * DV / 16;   // uint4 per row tile
+  static constexpr int QCU = DQK * BQ / 16, OCU = DV * BQ / 16; // uint4 per col tile
+  static constexpr int PQ = (QU + NT - 1) / NT, PO = (OU + NT - 1) / NT;
+  static constexpr int PQC = (QCU + NT - 1) / NT, POC = (OCU + NT - 1) / NT;
+  static constexpr int QSD = BQ * DQK / 128, OSD = BQ * DV / 128;  // row-copy scale dwords per tile
+  static_assert(QSD <= NT && OSD <= NT && DQK <= NT && DV <= NT && BQ <= NT, "one element per thread");
+};
+
+// One query tile's operands: codes (row and col copies of Q and dO), their
+// scales, and the per-query values L = LSE log2e, delta (hi, lo) and the
+// isolated-channel query value.
+template <int DQK, int DV>
+struct BwdStage {
+  using C = BwdCfg<DQK, DV>;
+  uint4 q[C::PQ], o[C::PO], qc[C::PQC], oc[C::POC];
+  uint32_t qs, os;      // row-copy scale dwords (threads < 64 rows * D/32 / 4)
+  uint32_t qcs, ocs;    // col-copy scale pairs of one channel
+  float L, hi, lo, qh;  // per-query values (threads < BQ)
+};
+
+template <int DQK, int DV>
+__device__ __forceinline__ void bwd_load(BwdStage<DQK, DV>& st, const AttnArgs& a, size_t bh, int i0, int N,
+                                         int hot) {
+  using C = BwdCfg<DQK, DV>;
+  const int tid = threadIdx.x;
+  const uint8_t* qrow = a.q_code + bh * N * DQK;
+  const uint8_t* orow = a.do_code + bh * N * DV;
+  const uint8_t* qcol = a.qc_code + bh * DQK * N;
+  const uint8_t* ocol = a.doc_code + bh * DV * N;
+  // row tiles: contiguous; bytes past the sequence are read from its last
+  // valid 16 bytes (those queries are skipped)
+  const int qlim = (N - i0) * DQK - 16, olim = (N - i0) * DV - 16;
+#pragma unroll
+  for (int i = 0; i < C::PQ; i++) {
+    const int u = tid + i * C::NT;
+    const int off = (u < C::QU ? u : 0) * 16;
+    st.q[i] = *reinterpret_cast<const uint4*>(qrow + (size_t)i0 * DQK + (off < qlim ? off : qlim));
+  }
+#pragma unroll
+  for (int i = 0; i < C::PO; i++) {
+    const int u = tid + i * C::NT;
+    const int off = (u < C::OU ? u : 0) * 16;
+    st.o[i] = *reinterpret_cast<const uint4*>(orow + (size_t)i0 * DV + (off < olim ? off : olim));
+  }
+#pragma unroll
+  for (int i = 0; i < C::PQC; i++) {
+    const int u = (tid + i * C::NT) < C::QCU ? tid + i * C::NT : 0, c = u >> 2, q = u & 3;
+    const int col = i0 + q * 16 < N - 16 ? i0 + q * 16 : N - 16;
+    st.qc[i] = *reinterpret_cast<const uint4*>(qcol + (size_t)c * N + col);
+  }
+#pragma unroll
+  for (int i = 0; i < C::POC; i++) {
+    const int u = (tid + i * C::NT) < C::OCU ? tid + i * C::NT : 0, c = u >> 2, q = u & 3;
+    const int col = i0 + q * 16 < N - 16 ? i0 + q * 16 : N - 16;
+    st.oc[i] = *reinterpret_cast<const uint4*>(ocol + (size_t)c * N + col);
+  }
+  if (tid < C::QSD) {
+    const int off = i0 * (DQK / 32) + tid * 4, lim = N * (DQK / 32) - 4;
+    st.qs = *reinterpret_cast<const uint32_t*>(a.q_scale + bh * N * (DQK / 32) + (off < lim ? off : lim));
+  }
+  if (tid < C::OSD) {
+    const int off = i0 * (DV / 32) + tid * 4, lim = N * (DV / 32) - 4;
+    st.os = *reinterpret_cast<const uint32_t*>(a.do_scale + bh * N * (DV / 32) + (off < lim ? off : lim));
+  }
+  const int g0 = i0 / 32, g1 = (i0 + 32 < N ? i0 + 32 : i0) / 32;
+  if (tid < DQK) {
+    const uint8_t* sc = a.qc_scale + (bh * DQK + tid) * (N / 32);
+    st.qcs = (uint32_t)sc[g0] | ((uint32_t)sc[g1] << 8);
+  }
+  if (tid < DV) {
+    const uint8_t* sc = a.doc_scale + (bh * DV + tid) * (N / 32);
+    st.ocs = (uint32_t)sc[g0] | ((uint32_t)sc[g1] << 8);
+  }
+  if (tid < C::BQ) {
+    const int r = i0 + tid < N ? i0 + tid : N - 1;
+    st.L = a.lse[bh * N + r] * kLog2e;
+    const float2 d = *reinterpret_cast<const float2*>(a.delta + (bh * N + r) * 2);
+    st.hi = d.x;
+    st.lo = d.y;
+    st.qh = hot >= 0 ? row_value<DQK>(qrow, a.q_scale + bh * N * (DQK / 32), r, hot) : 0.f;
+  }
+}
+
+template <int DQK, int DV>
+__device__ __forceinline__ void bwd_store(const BwdStage<DQK, DV>& st, uint8_t* sQ, uint8_t* sQs, uint8_t* sO,
+                                          uint8_t* sOs, uint8_t* sQc, uint8_t* sQcs, uint8_t* sOc, uint8_t* sOcs,
+                                          float* sRow, int hot) {
+  using C = BwdCfg<DQK, DV>;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < C::PQ; i++) {
+    const int u = tid + i * C::NT;
+    if (C::QU % C::NT == 0 || u < C::QU) {
+      const int r = (u * 16) / DQK, c = (u * 16) % DQK;
+      uint4 v = st.q[i];
+      if (hot >= c && hot < c + 16) clear_byte(v, hot - c);
+      *reinterpret_cast<uint4*>(sQ + r * C::QST + c) = v;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < C::PO; i++) {
+    const int u = tid + i * C::NT;
+    if (C::OU % C::NT == 0 || u < C::OU)
+      *reinterpret_cast<uint4*>(sO + ((u * 16) / DV) * C::OST + (u * 16) % DV) = st.o[i];
+  }
+#pragma unroll
+  for (int i = 0; i < C::PQC; i++) {
+    const int u = tid + i * C::NT;
+    if (C::QCU % C::NT == 0 || u < C::QCU) {
+      const int c = u >> 2, q = u & 3;
+      uint8_t* base = sQc + c * C::CST + (q >> 1) * 32 + (q & 1) * 8;
+      *reinterpret_cast<uint2*>(base) = make_uint2(st.qc[i].x, st.qc[i].z);
+      *reinterpret_cast<uint2*>(base + 16) = make_uint2(st.qc[i].y, st.qc[i].w);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < C::POC; i++) {
+    const int u = tid + i * C::NT;
+    if (C::OCU % C::NT == 0 || u < C::OCU) {
+      const int c = u >> 2, q = u & 3;
+      uint8_t* base = sOc + c * C::CST + (q >> 1) * 32 + (q & 1) * 8;
+      *reinterpret_cast<uint2*>(base) = make_uint2(st.oc[i].x, st.oc[i].z);
+      *reinterpret_cast<uint2*>(base + 16) = make_uint2(st.oc[i].y, st.oc[i].w);
+    }
+  }
+  if (tid < C::QSD) *reinterpret_cast<uint32_t*>(sQs + tid * 4) = st.qs;
+  if (tid < C::OSD) *reinterpret_cast<uint32_t*>(sOs + tid * 4) = st.os;
+  if (tid < DQK) *reinterpret_cast<uint16_t*>(sQcs + tid * 2) = (uint16_t)st.qcs;
+  if (tid < DV) *reinterpret_cast<uint16_t*>(sOcs + tid * 2) = (uint16_t)st.ocs;
+  if (tid < C::BQ) {
+    sRow[tid] = st.L;
+    sRow[C::BQ + tid] = st.hi;
+    sRow[2 * C::BQ + tid] = st.lo;
+    sRow[3 * C::BQ + tid] = st.qh;
+  }
+}
+
 // Columns [k0, k0 + W) of a col-copy code matrix [D, N] into LDS [D][W]
 // (natural order, row stride ST) and their scales into [D][W/32].
 template <int D, int W, int ST, int NT>
 __device__ __forceinline__ void stage_col_slice(uint8_t* lds, uint8_t* lds_scale, const uint8_t* code,
-                                                const uint8_t* scale, int64_t k0, int64_t N) {
+                                                const uint8_t* scale, int k0, int N) {
   constexpr int PER = W / 16;
   for (int u = threadIdx.x; u < D * PER; u += NT) {
     const int c = u / PER, q = u % PER;
     uint4 v = make_uint4(0, 0, 0, 0);
-    if (k0 + q * 16 < N) v = *reinterpret_cast<const uint4*>(code + (int64_t)c * N + k0 + q * 16);
+    if (k0 + q * 16 < N) v = *reinterpret_cast<const uint4*>(code + (size_t)c * N + k0 + q * 16);
     *reinterpret_cast<uint4*>(lds + c * ST + q * 16) = v;
   }
   for (int u = threadIdx.x; u < D * (W / 32); u += NT) {
     const int c = u / (W / 32), g = u % (W / 32);
-    lds_scale[u] = (k0 + g * 32 < N) ? scale[(int64_t)c * (N / 32) + k0 / 32 + g] : (uint8_t)0;
+    lds_scale[u] = (k0 + g * 32 < N) ? scale[(size_t)c * (N / 32) + k0 / 32 + g] : (uint8_t)0;
   }
 }
 
@@ -50,12 +198,6 @@ __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int m = 1; m < 32; m <<= 1) v = fmaxf(v, __shfl_xor(v, m));
   return fmaxf(v, partner(v));
-}
-
-__device__ __forceinline__ float half_sum(float v) {
-#pragma unroll
-  for (int m = 1; m < 32; m <<= 1) v += __shfl_xor(v, m);
-  return v;
 }
 __device__ __forceinline__ double half_sum_d(double v) {
 #pragma unroll
@@ -68,62 +210,60 @@ __device__ __forceinline__ float half_max(float v) {
   return v;
 }
 
-template <int DQK, int DV, int NWK, bool STATS>
-__global__ __launch_bounds__(64 * NWK) void bwd_kernel(AttnArgs a) {
-  constexpr int BKB = 32 * NWK, BQ = 64;
+template <int DQK, int DV, bool STATS>
+__global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnArgs a) {
+  using C = BwdCfg<DQK, DV>;
+  constexpr int NWK = C::NWK, BKB = C::BKB, BQ = C::BQ, NT = C::NT;
   constexpr int KS = DQK / 64, VS = DV / 64, CK = DQK / 32, CV = DV / 32;
-  constexpr int QST = DQK + 16, OST = DV + 16, CST = BQ + 16, KCST = BKB + 16, DST = BQ + 16;
-  constexpr int NT = 64 * NWK;
-  __shared__ __attribute__((aligned(16))) uint8_t sQ[BQ * QST];
-  __shared__ __attribute__((aligned(16))) uint8_t sQs[BQ * DQK / 32];
-  __shared__ __attribute__((aligned(16))) uint8_t sO[BQ * OST];
-  __shared__ __attribute__((aligned(16))) uint8_t sOs[BQ * DV / 32];
-  __shared__ __attribute__((aligned(16))) uint8_t sQc[DQK * CST];
-  __shared__ __attribute__((aligned(16))) uint8_t sQcs[DQK * 2];
-  __shared__ __attribute__((aligned(16))) uint8_t sOc[DV * CST];
-  __shared__ __attribute__((aligned(16))) uint8_t sOcs[DV * 2];
-  __shared__ __attribute__((aligned(16))) uint8_t sKc[DQK * KCST];
+  __shared__ __attribute__((aligned(16))) uint8_t sQ[C::NBUF][BQ * C::QST];
+  __shared__ __attribute__((aligned(16))) uint8_t sQs[C::NBUF][BQ * DQK / 32];
+  __shared__ __attribute__((aligned(16))) uint8_t sO[C::NBUF][BQ * C::OST];
+  __shared__ __attribute__((aligned(16))) uint8_t sOs[C::NBUF][BQ * DV / 32];
+  __shared__ __attribute__((aligned(16))) uint8_t sQc[C::NBUF][DQK * C::CST];
+  __shared__ __attribute__((aligned(16))) uint8_t sQcs[C::NBUF][DQK * 2];
+  __shared__ __attribute__((aligned(16))) uint8_t sOc[C::NBUF][DV * C::CST];
+  __shared__ __attribute__((aligned(16))) uint8_t sOcs[C::NBUF][DV * 2];
+  __shared__ __attribute__((aligned(16))) float sRow[C::NBUF][4 * BQ];
+  __shared__ __attribute__((aligned(16))) uint8_t sKc[DQK * C::KCST];
   __shared__ __attribute__((aligned(16))) uint8_t sKcs[DQK * BKB / 32];
-  __shared__ __attribute__((aligned(16))) uint8_t sdS[BKB * DST];
-  __shared__ __attribute__((aligned(16))) uint8_t sdSs[NWK * 2];
-  __shared__ __attribute__((aligned(16))) float sL[BQ];
-  __shared__ __attribute__((aligned(16))) float sD[BQ * 2];
-  __shared__ __attribute__((aligned(16))) float sQh[BQ];
+  __shared__ __attribute__((aligned(16))) uint8_t sdS[C::NDS][BKB * C::DST];
+  __shared__ __attribute__((aligned(16))) uint8_t sdSs[C::NDS][NWK * 2];
   __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
-  const int64_t kb0 = (int64_t)blockIdx.x * BKB;  // key block (block 0 has the most work)
-  const int64_t kh = blockIdx.y, b = blockIdx.z;
-  const int64_t kw0 = kb0 + 32 * w;                 // this wave's first key
-  const bool live = kw0 < a.N;
-  const int64_t kj = kw0 + li;                      // this lane's key
+  const int N = (int)a.N;
+  const int kb0 = blockIdx.x * BKB;             // key block (block 0 has the most work)
+  const int kh = blockIdx.y, b = blockIdx.z;
+  const int kw0 = kb0 + 32 * w;                 // this wave's first key
+  const bool live = kw0 < N;
+  const int kj = kw0 + li;                      // this lane's key
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
+  const size_t bhk = (size_t)b * a.Hkv + kh;
 
   // K and V row codes of this lane's key (B operands of S and dP)
   v8i kf[KS], vf[VS];
   int ksc[KS], vsc[VS];
-#pragma unroll
-  for (int s = 0; s < KS; s++) { kf[s] = v8i{0, 0, 0, 0, 0, 0, 0, 0}; ksc[s] = 0; }
-#pragma unroll
-  for (int s = 0; s < VS; s++) { vf[s] = v8i{0, 0, 0, 0, 0, 0, 0, 0}; vsc[s] = 0; }
-  if (live) {
-    const int64_t row = (b * a.Hkv + kh) * a.N + kj;
+  float khot = 0.f;
+  {
+    const int row = live ? kj : 0;
+    const uint8_t* kr = a.k_code + (bhk * N + row) * DQK;
+    const uint8_t* vr = a.v_code + (bhk * N + row) * DV;
 #pragma unroll
     for (int s = 0; s < KS; s++) {
-      kf[s] = frag_rows_global(a.k_code + row * DQK, s, hf);
+      kf[s] = frag_rows_global(kr, s, hf);
       clear_channel(kf[s], s, hf, hot);
-      ksc[s] = a.k_scale[row * (DQK / 32) + 2 * s + hf];
+      ksc[s] = a.k_scale[(bhk * N + row) * (DQK / 32) + 2 * s + hf];
     }
 #pragma unroll
     for (int s = 0; s < VS; s++) {
-      vf[s] = frag_rows_global(a.v_code + row * DV, s, hf);
-      vsc[s] = a.v_scale[row * (DV / 32) + 2 * s + hf];
+      vf[s] = frag_rows_global(vr, s, hf);
+      vsc[s] = a.v_scale[(bhk * N + row) * (DV / 32) + 2 * s + hf];
     }
+    if (hot >= 0) khot = row_value<DQK>(a.k_code + bhk * N * DQK, a.k_scale + bhk * N * (DQK / 32), row, hot);
   }
-  const float khot = (live && hot >= 0) ? row_value<DQK>(a.k_code, a.k_scale, (b * a.Hkv + kh) * a.N + kj, hot) : 0.f;
   // K col codes of the workgroup's keys (B operand of dQ), once
-  stage_col_slice<DQK, BKB, KCST, NT>(sKc, sKcs, a.kc_code + (b * a.Hkv + kh) * (int64_t)DQK * a.N,
-                                      a.kc_scale + (b * a.Hkv + kh) * (int64_t)DQK * (a.N / 32), kb0, a.N);
+  stage_col_slice<DQK, BKB, C::KCST, NT>(sKc, sKcs, a.kc_code + bhk * DQK * N, a.kc_scale + bhk * DQK * (N / 32),
+                                         kb0, N);
 
   v16f dk[CK], dv[CV];
 #pragma unroll
@@ -135,171 +275,183 @@ __global__ __launch_bounds__(64 * NWK) void bwd_kernel(AttnArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; r++) dv[c][r] = 0.f;
 
-  const int64_t nqt = (a.N + BQ - 1) / BQ;
-  const int64_t qt0 = kb0 / BQ;
-  for (int64_t hh = 0; hh < a.G; hh++) {
-    const int64_t h = kh * a.G + hh;
-    const int64_t bh = b * a.Hq + h;
-    for (int64_t qt = qt0; qt < nqt; qt++) {
-      const int64_t i0 = qt * BQ;
-      __syncthreads();
-      stage_rows<BQ, DQK, QST, NT>(sQ, sQs, a.q_code + bh * a.N * DQK, a.q_scale + bh * a.N * (DQK / 32), i0, a.N,
-                                   hot);
-      stage_rows<BQ, DV, OST, NT>(sO, sOs, a.do_code + bh * a.N * DV, a.do_scale + bh * a.N * (DV / 32), i0, a.N);
-      stage_cols_perm<DQK, CST, NT>(sQc, sQcs, a.qc_code + bh * (int64_t)DQK * a.N,
-                                    a.qc_scale + bh * (int64_t)DQK * (a.N / 32), i0, a.N);
-      stage_cols_perm<DV, CST, NT>(sOc, sOcs, a.doc_code + bh * (int64_t)DV * a.N,
-                                   a.doc_scale + bh * (int64_t)DV * (a.N / 32), i0, a.N);
-      for (int u = threadIdx.x; u < BQ; u += NT) {
-        const bool ok = i0 + u < a.N;
-        sL[u] = ok ? a.lse[bh * a.N + i0 + u] * kLog2e : 0.f;
-        sD[2 * u] = ok ? a.delta[(bh * a.N + i0 + u) * 2] : 0.f;
-        sD[2 * u + 1] = ok ? a.delta[(bh * a.N + i0 + u) * 2 + 1] : 0.f;
-        sQh[u] = (ok && hot >= 0) ? row_value<DQK>(a.q_code, a.q_scale, bh * a.N + i0 + u, hot) : 0.f;
-      }
-      __syncthreads();
+  const int G = (int)a.G;
+  const int nqt = (N + BQ - 1) / BQ, qt0 = kb0 / BQ, nq = nqt - qt0;
+  const int total = G * nq;
+  BwdStage<DQK, DV> st;
+  bwd_load<DQK, DV>(st, a, (size_t)b * a.Hq + (size_t)kh * G, qt0 * BQ, N, hot);
+  bwd_store<DQK, DV>(st, sQ[0], sQs[0], sO[0], sOs[0], sQc[0], sQcs[0], sOc[0], sOcs[0], sRow[0], hot);
+  __syncthreads();
 
-      // this wave has work unless every query of the tile precedes its keys
-      const bool work = live && (i0 + BQ - 1 >= kw0);
-      const bool needmask = (i0 < kw0 + 31) || (i0 + BQ > a.N);
-      uint32_t dsc_codes[2][4];
-      int dse[2] = {-127, -127};
-      if (work) {
-        uint32_t pc[2][4];
+  for (int it = 0; it < total; it++) {
+    const int cur = C::NBUF == 2 ? (it & 1) : 0;  // staging buffer of this tile
+    const int dsb = C::NDS == 2 ? (it & 1) : 0;
+    const int hh = it / nq, qt = qt0 + it % nq;
+    const int h = kh * G + hh;
+    const size_t bh = (size_t)b * a.Hq + h;
+    const int i0 = qt * BQ;
+    if (it + 1 < total) {
+      const int hn = kh * G + (it + 1) / nq, qn = qt0 + (it + 1) % nq;
+      bwd_load<DQK, DV>(st, a, (size_t)b * a.Hq + hn, qn * BQ, N, hot);
+    }
+
+    const uint8_t* Q = sQ[cur];
+    const uint8_t* Qs = sQs[cur];
+    const uint8_t* O = sO[cur];
+    const uint8_t* Os = sOs[cur];
+    const float* Row = sRow[cur];
+    uint32_t pc[2][4], dc[2][4];
+    int dse[2] = {-127, -127};
+    bool any = false;
 #pragma unroll
-        for (int qs = 0; qs < 2; qs++) {
-          v16f s, dp;
+    for (int qs = 0; qs < 2; qs++) {
+      const int qb = i0 + 32 * qs;             // first query of the sub-block
+      // wave-uniform: skip sub-blocks wholly before this wave's keys or past the sequence
+      if (!live || qb < kw0 || qb >= N) {
 #pragma unroll
-          for (int r = 0; r < 16; r++) { s[r] = 0.f; dp[r] = 0.f; }
-#pragma unroll
-          for (int st = 0; st < KS; st++)
-            s = mfma_mx(frag_rows<QST>(sQ, 32 * qs + li, st, hf), kf[st], s,
-                        sQs[(32 * qs + li) * (DQK / 32) + 2 * st + hf], ksc[st]);
-#pragma unroll
-          for (int st = 0; st < VS; st++)
-            dp = mfma_mx(frag_rows<OST>(sO, 32 * qs + li, st, hf), vf[st], dp,
-                         sOs[(32 * qs + li) * (DV / 32) + 2 * st + hf], vsc[st]);
-          // lane holds queries 32 qs + 8 g + 4 hf + e (accumulator r = 4 g + e)
-          float P[16], dS[16];
-          float amax = 0.f;
-#pragma unroll
-          for (int g = 0; g < 4; g++) {
-            const int qo = 32 * qs + 8 * g + 4 * hf;
-            const float4 Lg = *reinterpret_cast<const float4*>(&sL[qo]);
-            const float4 d01 = *reinterpret_cast<const float4*>(&sD[2 * qo]);
-            const float4 d23 = *reinterpret_cast<const float4*>(&sD[2 * qo + 4]);
-            const float4 qh = *reinterpret_cast<const float4*>(&sQh[qo]);
-            const float Qh[4] = {qh.x, qh.y, qh.z, qh.w};
-            const float Lv[4] = {Lg.x, Lg.y, Lg.z, Lg.w};
-            const float Hv[4] = {d01.x, d01.z, d23.x, d23.z};
-            const float Lo[4] = {d01.y, d01.w, d23.y, d23.w};
-#pragma unroll
-            for (int e = 0; e < 4; e++) {
-              const int r = 4 * g + e;
-              float p = bwd_prob(__builtin_fmaf(Qh[e], khot, s[r]), a.c, Lv[e]);
-              if (needmask) {
-                const int64_t qi = i0 + qo + e;
-                p = (kj > qi || qi >= a.N) ? 0.f : p;
-              }
-              P[r] = p;
-              dS[r] = p * ((dp[r] - Hv[e]) - Lo[e]);
-              amax = fmaxf(amax, fabsf(dS[r]));
-            }
-          }
-#pragma unroll
-          for (int k = 0; k < 4; k++)
-            pc[qs][k] = cvt4_div(P[4 * k], P[4 * k + 1], P[4 * k + 2], P[4 * k + 3], 0.00390625f);
-          int e = pow2_exponent(wave_max(amax));
-          e = e < -126 ? -126 : e;
-          const float sc = exp2i(e);
-#pragma unroll
-          for (int k = 0; k < 4; k++)
-            dsc_codes[qs][k] = cvt4_div(dS[4 * k], dS[4 * k + 1], dS[4 * k + 2], dS[4 * k + 3], sc);
-          dse[qs] = e;
-          if constexpr (STATS) {
-            // per query row: FP64 sums over this wave's 32 keys, then atomics
-#pragma unroll
-            for (int r = 0; r < 16; r++) {
-              const float cast = fp8_value(dsc_codes[qs][r >> 2], r & 3) * sc;
-              const double s0 = half_sum_d((double)dS[r]);
-              const double s1 = half_sum_d((double)fabsf(dS[r]));
-              const double s2 = half_sum_d((double)cast);
-              const float mx = half_max(fabsf(dS[r]));
-              const int64_t qi = i0 + 32 * qs + 8 * (r >> 2) + 4 * hf + (r & 3);
-              if (li == 0 && qi < a.N) {
-                double* st = a.rowstats + (bh * a.N + qi) * 4;
-                atomicAdd(st + 0, s0);
-                atomicAdd(st + 1, s1);
-                atomicAdd(st + 2, s2);
-                atomicMax(reinterpret_cast<unsigned long long*>(st + 3),
-                          (unsigned long long)__double_as_longlong((double)mx));
-              }
-            }
-          }
-        }
-        // dV += P'^T dO_col ; dK += dS'^T Q_col   (k = the 64 queries of the tile)
-        const v8i pa = v8i{(int)pc[0][0], (int)pc[0][1], (int)pc[0][2], (int)pc[0][3],
-                           (int)pc[1][0], (int)pc[1][1], (int)pc[1][2], (int)pc[1][3]};
-        const v8i da = v8i{(int)dsc_codes[0][0], (int)dsc_codes[0][1], (int)dsc_codes[0][2], (int)dsc_codes[0][3],
-                           (int)dsc_codes[1][0], (int)dsc_codes[1][1], (int)dsc_codes[1][2], (int)dsc_codes[1][3]};
-        const int dascale = (hf ? dse[1] : dse[0]) + 127;
-#pragma unroll
-        for (int c = 0; c < CV; c++)
-          dv[c] = mfma_mx(pa, frag_cols<CST>(sOc, 32 * c + li, hf), dv[c], 127 - 8, sOcs[(32 * c + li) * 2 + hf]);
-#pragma unroll
-        for (int c = 0; c < CK; c++)
-          dk[c] = mfma_mx(da, frag_cols<CST>(sQc, 32 * c + li, hf), dk[c], dascale, sQcs[(32 * c + li) * 2 + hf]);
-      } else {
-#pragma unroll
-        for (int qs = 0; qs < 2; qs++)
-#pragma unroll
-          for (int k = 0; k < 4; k++) dsc_codes[qs][k] = 0u;
+        for (int k = 0; k < 4; k++) { pc[qs][k] = 0u; dc[qs][k] = 0u; }
+        continue;
       }
-      // dS' codes to LDS: row = key (32 w + li), columns = the lane's queries
+      any = true;
+      v16f s, dp;
 #pragma unroll
-      for (int qs = 0; qs < 2; qs++)
+      for (int r = 0; r < 16; r++) { s[r] = 0.f; dp[r] = 0.f; }
 #pragma unroll
-        for (int g = 0; g < 4; g++)
-          *reinterpret_cast<uint32_t*>(sdS + (32 * w + li) * DST + 32 * qs + 8 * g + 4 * hf) = dsc_codes[qs][g];
-      if (lane == 0) {
-        sdSs[w * 2] = (uint8_t)(dse[0] + 127);
-        sdSs[w * 2 + 1] = (uint8_t)(dse[1] + 127);
-      }
-      __syncthreads();
-      // dQ tile (64 queries x DQK) = dS'(64 x BKB) K_col(BKB x DQK): output
-      // blocks m = qs * CK + c, distributed round-robin over the waves
-      for (int m = w; m < 2 * CK; m += NWK) {
-        const int qs = m / CK, c = m % CK;
-        v16f acc;
+      for (int t = 0; t < KS; t++)
+        s = mfma_mx(frag_rows<C::QST>(Q, 32 * qs + li, t, hf), kf[t], s,
+                    Qs[(32 * qs + li) * (DQK / 32) + 2 * t + hf], ksc[t]);
 #pragma unroll
-        for (int r = 0; r < 16; r++) acc[r] = 0.f;
+      for (int t = 0; t < VS; t++)
+        dp = mfma_mx(frag_rows<C::OST>(O, 32 * qs + li, t, hf), vf[t], dp,
+                     Os[(32 * qs + li) * (DV / 32) + 2 * t + hf], vsc[t]);
+      // lane holds queries qb + 8 g + 4 hf + e (accumulator r = 4 g + e)
+      float P[16], dS[16];
+      float amax = 0.f;
 #pragma unroll
-        for (int ks = 0; ks < BKB / 64; ks++) {
-          // A: rows = queries of sub-block qs, k = keys 64 ks .. 64 ks + 63 (natural order)
-          const int i16 = lane & 15;
-          const int qbase = 32 * qs + 16 * ((lane >> 4) & 1);
-          int words[8];
+      for (int g = 0; g < 4; g++) {
+        const int qo = 32 * qs + 8 * g + 4 * hf;
+        const float4 Lg = *reinterpret_cast<const float4*>(&Row[qo]);
+        const float4 Hg = *reinterpret_cast<const float4*>(&Row[BQ + qo]);
+        const float4 Og = *reinterpret_cast<const float4*>(&Row[2 * BQ + qo]);
+        const float4 Qg = *reinterpret_cast<const float4*>(&Row[3 * BQ + qo]);
+        const float Lv[4] = {Lg.x, Lg.y, Lg.z, Lg.w}, Hv[4] = {Hg.x, Hg.y, Hg.z, Hg.w};
+        const float Ov[4] = {Og.x, Og.y, Og.z, Og.w}, Qh[4] = {Qg.x, Qg.y, Qg.z, Qg.w};
 #pragma unroll
-          for (int part = 0; part < 4; part++) {
-            const int kk = 64 * ks + 32 * (part >> 1) + 16 * hf + 8 * (part & 1);
-            const uint8_t* addr = sdS + (kk + (i16 >> 1)) * DST + qbase + 8 * (i16 & 1);
-            const v2i t = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
-                (__attribute__((address_space(3))) v2i*)(addr));
-            words[2 * part] = t[0];
-            words[2 * part + 1] = t[1];
-          }
-          const v8i af = v8i{words[0], words[1], words[2], words[3], words[4], words[5], words[6], words[7]};
-          const int as = sdSs[(2 * ks + hf) * 2 + qs];
-          acc = mfma_mx(af, frag_rows<KCST>(sKc, 32 * c + li, ks, hf), acc, as,
-                        sKcs[(32 * c + li) * (BKB / 32) + 2 * ks + hf]);
+        for (int e = 0; e < 4; e++) {
+          const int r = 4 * g + e;
+          float p = bwd_prob(__builtin_fmaf(Qh[e], khot, s[r]), a.c, Lv[e]);
+          if (qb == kw0) p = (li > 8 * g + 4 * hf + e) ? 0.f : p;   // diagonal block: key > query
+          P[r] = p;
+          dS[r] = p * ((dp[r] - Hv[e]) - Ov[e]);
+          amax = fmaxf(amax, fabsf(dS[r]));
         }
-        // lane holds channel 32 c + li, queries 32 qs + 8 (r/4) + 4 hf + r % 4
-        float* base = a.dq_acc + (b * a.N * a.Hq + h) * DQK + 32 * c + li;
+      }
+#pragma unroll
+      for (int k = 0; k < 4; k++)
+        pc[qs][k] = cvt4_div(P[4 * k], P[4 * k + 1], P[4 * k + 2], P[4 * k + 3], 0.00390625f);
+      int e = pow2_exponent(wave_max(amax));
+      e = e < -126 ? -126 : e;
+      const float sc = exp2i(e);
+#pragma unroll
+      for (int k = 0; k < 4; k++) dc[qs][k] = cvt4_div(dS[4 * k], dS[4 * k + 1], dS[4 * k + 2], dS[4 * k + 3], sc);
+      dse[qs] = e;
+      if constexpr (STATS) {
+        // per query row: FP64 sums over this wave's 32 keys, then atomics
 #pragma unroll
         for (int r = 0; r < 16; r++) {
-          const int64_t qi = i0 + 32 * qs + 8 * (r >> 2) + 4 * hf + (r & 3);
-          if (qi < a.N) atomicAdd(base + qi * a.Hq * DQK, acc[r]);
+          const float cast = fp8_value(dc[qs][r >> 2], r & 3) * sc;
+          const double s0 = half_sum_d((double)dS[r]);
+          const double s1 = half_sum_d((double)fabsf(dS[r]));
+          const double s2 = half_sum_d((double)cast);
+          const float mx = half_max(fabsf(dS[r]));
+          const int qi = qb + 8 * (r >> 2) + 4 * hf + (r & 3);
+          if (li == 0) {
+            double* sp = a.rowstats + (bh * N + qi) * 4;
+            atomicAdd(sp + 0, s0);
+            atomicAdd(sp + 1, s1);
+            atomicAdd(sp + 2, s2);
+            atomicMax(reinterpret_cast<unsigned long long*>(sp + 3),
+                      (unsigned long long)__double_as_longlong((double)mx));
+          }
         }
+      }
+    }
+    if (any) {
+      // dV += P'^T dO_col ; dK += dS'^T Q_col   (k = the 64 queries of the tile)
+      const v8i pa = v8i{(int)pc[0][0], (int)pc[0][1], (int)pc[0][2], (int)pc[0][3],
+                         (int)pc[1][0], (int)pc[1][1], (int)pc[1][2], (int)pc[1][3]};
+      const v8i da = v8i{(int)dc[0][0], (int)dc[0][1], (int)dc[0][2], (int)dc[0][3],
+                         (int)dc[1][0], (int)dc[1][1], (int)dc[1][2], (int)dc[1][3]};
+      const int dascale = (hf ? dse[1] : dse[0]) + 127;
+      const uint8_t* Oc = sOc[cur];
+      const uint8_t* Ocs = sOcs[cur];
+      const uint8_t* Qc = sQc[cur];
+      const uint8_t* Qcs = sQcs[cur];
+#pragma unroll
+      for (int c = 0; c < CV; c++)
+        dv[c] = mfma_mx(pa, frag_cols<C::CST>(Oc, 32 * c + li, hf), dv[c], 127 - 8, Ocs[(32 * c + li) * 2 + hf]);
+#pragma unroll
+      for (int c = 0; c < CK; c++)
+        dk[c] = mfma_mx(da, frag_cols<C::CST>(Qc, 32 * c + li, hf), dk[c], dascale, Qcs[(32 * c + li) * 2 + hf]);
+    }
+    // dS' codes to LDS: row = key (32 w + li), columns = the lane's queries
+    uint8_t* dS_l = sdS[dsb];
+#pragma unroll
+    for (int qs = 0; qs < 2; qs++)
+#pragma unroll
+      for (int g = 0; g < 4; g++)
+        *reinterpret_cast<uint32_t*>(dS_l + (32 * w + li) * C::DST + 32 * qs + 8 * g + 4 * hf) = dc[qs][g];
+    if (lane == 0) {
+      sdSs[dsb][w * 2] = (uint8_t)(dse[0] + 127);
+      sdSs[dsb][w * 2 + 1] = (uint8_t)(dse[1] + 127);
+    }
+    // the next tile into the other staging buffer (nobody reads it this tile)
+    if constexpr (C::NBUF == 2) {
+      const int nb = cur ^ 1;
+      if (it + 1 < total)
+        bwd_store<DQK, DV>(st, sQ[nb], sQs[nb], sO[nb], sOs[nb], sQc[nb], sQcs[nb], sOc[nb], sOcs[nb], sRow[nb], hot);
+    }
+    __syncthreads();
+    // dQ tile (64 queries x DQK) = dS'(64 x BKB) K_col(BKB x DQK): output blocks
+    // m = qs * CK + c, distributed round-robin over the waves
+    for (int m = w; m < 2 * CK; m += NWK) {
+      const int qs = m / CK, c = m % CK;
+      const int qb = i0 + 32 * qs;
+      if (qb >= N) continue;
+      v16f acc;
+#pragma unroll
+      for (int r = 0; r < 16; r++) acc[r] = 0.f;
+      const int i16 = lane & 15;
+      const int qbase = 32 * qs + 16 * ((lane >> 4) & 1);
+#pragma unroll
+      for (int ks = 0; ks < BKB / 64; ks++) {
+        if (kb0 + 64 * ks > qb + 31) break;    // these keys are all in the future of the sub-block
+        // A: rows = queries of sub-block qs, k = keys 64 ks .. 64 ks + 63 (natural order)
+        int words[8];
+#pragma unroll
+        for (int part = 0; part < 4; part++) {
+          const int kk = 64 * ks + 32 * (part >> 1) + 16 * hf + 8 * (part & 1);
+          const uint8_t* addr = dS_l + (kk + (i16 >> 1)) * C::DST + qbase + 8 * (i16 & 1);
+          const v2i t = __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i*)(addr));
+          words[2 * part] = t[0];
+          words[2 * part + 1] = t[1];
+        }
+        const v8i af = v8i{words[0], words[1], words[2], words[3], words[4], words[5], words[6], words[7]};
+        acc = mfma_mx(af, frag_rows<C::KCST>(sKc, 32 * c + li, ks, hf), acc, sdSs[dsb][(2 * ks + hf) * 2 + qs],
+                      sKcs[(32 * c + li) * (BKB / 32) + 2 * ks + hf]);
+      }
+      // lane holds channel 32 c + li, queries qb + 8 (r/4) + 4 hf + r % 4
+      float* base = a.dq_acc + ((size_t)b * N * a.Hq + h) * DQK + 32 * c + li;
+#pragma unroll
+      for (int r = 0; r < 16; r++)
+        atomicAdd(base + (size_t)(qb + 8 * (r >> 2) + 4 * hf + (r & 3)) * a.Hq * DQK, acc[r]);
+    }
+    if constexpr (C::NDS == 1) __syncthreads();   // single dS buffer: reads done before the next writes
+    if constexpr (C::NBUF == 1) {
+      if (it + 1 < total) {
+        if constexpr (C::NDS == 2) __syncthreads();
+        bwd_store<DQK, DV>(st, sQ[0], sQs[0], sO[0], sOs[0], sQc[0], sQcs[0], sOc[0], sOcs[0], sRow[0], hot);
+        __syncthreads();
       }
     }
   }
@@ -307,18 +459,17 @@ __global__ __launch_bounds__(64 * NWK) void bwd_kernel(AttnArgs a) {
   // dK (times tau) and dV: lane holds channel 32 c + li, keys kw0 + 8 (r/4) + 4 hf + r % 4
 #pragma unroll
   for (int r = 0; r < 16; r++) {
-    const int64_t key = kw0 + 8 * (r >> 2) + 4 * hf + (r & 3);
-    if (key >= a.N) continue;
+    const int key = kw0 + 8 * (r >> 2) + 4 * hf + (r & 3);
     if (a.grad_bf16) {
-      uint16_t* kd = reinterpret_cast<uint16_t*>(a.dk) + b * a.dks[0] + key * a.dks[1] + kh * a.dks[2];
-      uint16_t* vd = reinterpret_cast<uint16_t*>(a.dv) + b * a.dvs[0] + key * a.dvs[1] + kh * a.dvs[2];
+      uint16_t* kd = reinterpret_cast<uint16_t*>(a.dk) + b * a.dks[0] + (int64_t)key * a.dks[1] + kh * a.dks[2];
+      uint16_t* vd = reinterpret_cast<uint16_t*>(a.dv) + b * a.dvs[0] + (int64_t)key * a.dvs[1] + kh * a.dvs[2];
 #pragma unroll
       for (int c = 0; c < CK; c++) kd[32 * c + li] = f32_to_bf16(dk[c][r] * a.tau);
 #pragma unroll
       for (int c = 0; c < CV; c++) vd[32 * c + li] = f32_to_bf16(dv[c][r]);
     } else {
-      float* kd = reinterpret_cast<float*>(a.dk) + b * a.dks[0] + key * a.dks[1] + kh * a.dks[2];
-      float* vd = reinterpret_cast<float*>(a.dv) + b * a.dvs[0] + key * a.dvs[1] + kh * a.dvs[2];
+      float* kd = reinterpret_cast<float*>(a.dk) + b * a.dks[0] + (int64_t)key * a.dks[1] + kh * a.dks[2];
+      float* vd = reinterpret_cast<float*>(a.dv) + b * a.dvs[0] + (int64_t)key * a.dvs[1] + kh * a.dvs[2];
 #pragma unroll
       for (int c = 0; c < CK; c++) kd[32 * c + li] = dk[c][r] * a.tau;
 #pragma unroll
@@ -329,11 +480,11 @@ __global__ __launch_bounds__(64 * NWK) void bwd_kernel(AttnArgs a) {
 
 template <int DQK, int DV>
 static hipError_t bwd_dispatch(const AttnArgs& a, hipStream_t s) {
-  constexpr int NWK = 4;
-  const int64_t nkb = (a.N + 32 * NWK - 1) / (32 * NWK);
+  using C = BwdCfg<DQK, DV>;
+  const int64_t nkb = (a.N + C::BKB - 1) / C::BKB;
   dim3 grid((unsigned)nkb, (unsigned)a.Hkv, (unsigned)a.B);
-  if (a.rowstats) hipLaunchKernelGGL((bwd_kernel<DQK, DV, NWK, true>), grid, dim3(64 * NWK), 0, s, a);
-  else hipLaunchKernelGGL((bwd_kernel<DQK, DV, NWK, false>), grid, dim3(64 * NWK), 0, s, a);
+  if (a.rowstats) hipLaunchKernelGGL((bwd_kernel<DQK, DV, true>), grid, dim3(C::NT), 0, s, a);
+  else hipLaunchKernelGGL((bwd_kernel<DQK, DV, false>), grid, dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }
 
