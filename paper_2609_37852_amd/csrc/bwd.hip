@@ -8,8 +8,10 @@
 // are loaded into registers while the current one is computed (LDS
 // double-buffered where it fits).
 //
-// Per wave, tile and 32-query sub-block qs (skipped when it lies wholly
-// before the wave's keys or past the sequence; masked only on the diagonal):
+// Per wave, tile and 32-query sub-block qs (near the diagonal a sub-block is
+// skipped when it lies wholly before the wave's keys or past the sequence,
+// and masked when it holds them; tiles wholly after the workgroup's keys take
+// a path without either):
 //   S  = Q K^T, dP = dO V^T   MX MFMA (A = Q / dO row tiles in LDS, B = the
 //                             wave's K / V row codes in registers); lane l
 //                             owns key l % 32 and holds 16 queries.
@@ -24,6 +26,8 @@
 // the waves, the dS' operand read with the 8-bit LDS transpose, and added to
 // the FP32 workspace with atomics (dQ = tau * workspace is stored by a second
 // kernel).
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "tiles.hpp"
@@ -32,8 +36,9 @@ namespace afp8 {
 
 template <int DQK, int DV>
 struct BwdCfg {
-  // waves per workgroup and LDS buffers, sized to stay within 160 KB of LDS
-  static constexpr int NWK = (DQK + DV <= 256) ? 8 : 4;
+  // waves per workgroup (eight only where their dK/dV accumulators leave
+  // room for two waves per SIMD) and LDS buffers, within 160 KB of LDS
+  static constexpr int NWK = (DQK + DV <= 128) ? 8 : 4;
   static constexpr int NBUF = (DQK + DV <= 320) ? 2 : 1;   // staging buffers
   static constexpr int NT = 64 * NWK, BKB = 32 * NWK, BQ = 64;
   static constexpr int QST = DQK + 16, OST = DV + 16, CST = BQ + 16, KCST = BKB + 16, DST = BQ + 16;
@@ -46,78 +51,102 @@ struct BwdCfg {
   static_assert(QSD <= NT && OSD <= NT && DQK <= NT && DV <= NT && BQ <= NT, "one element per thread");
 };
 
-// One query tile's operands: codes (row and col copies of Q and dO), their
-// scales, and the per-query values L = LSE log2e, delta (hi, lo) and the
-// isolated-channel query value.
+// One query tile in flight from global memory: raw loaded words only.  Every
+// use of a loaded value waits for the load, so all decoding is left to
+// bwd_store, after the current tile has been computed.
 template <int DQK, int DV>
 struct BwdStage {
   using C = BwdCfg<DQK, DV>;
   uint4 q[C::PQ], o[C::PO], qc[C::PQC], oc[C::POC];
-  uint32_t qs, os;      // row-copy scale dwords (threads < 64 rows * D/32 / 4)
-  uint32_t qcs, ocs;    // col-copy scale pairs of one channel
-  float L, hi, lo, qh;  // per-query values (threads < BQ)
+  uint32_t qs, os;              // row-copy scale dwords
+  uint32_t qcs0, qcs1;          // col-copy scale bytes of one Q channel (query groups 0, 1)
+  uint32_t ocs0, ocs1;          // same for dO
+  float L, dhi, dlo;            // LSE and delta (hi, lo) of one query
+  uint32_t qhc, qhs;            // isolated-channel code and scale byte of one query
+};
+
+// Per-(batch, query head) base pointers of the query-side operands.
+struct BwdHead {
+  const uint8_t *qrow, *qsc, *orow, *osc, *qcol, *qcsc, *ocol, *ocsc;
+  const float *lse, *delta;
 };
 
 template <int DQK, int DV>
-__device__ __forceinline__ void bwd_load(BwdStage<DQK, DV>& st, const AttnArgs& a, size_t bh, int i0, int N,
-                                         int hot) {
+__device__ __forceinline__ BwdHead bwd_head(const AttnArgs& a, size_t bh, int N) {
+  BwdHead p;
+  p.qrow = a.q_code + bh * N * DQK;
+  p.qsc = a.q_scale + bh * N * (DQK / 32);
+  p.orow = a.do_code + bh * N * DV;
+  p.osc = a.do_scale + bh * N * (DV / 32);
+  p.qcol = a.qc_code + bh * DQK * N;
+  p.qcsc = a.qc_scale + bh * DQK * (N / 32);
+  p.ocol = a.doc_code + bh * DV * N;
+  p.ocsc = a.doc_scale + bh * DV * (N / 32);
+  p.lse = a.lse + bh * N;
+  p.delta = a.delta + bh * N * 2;
+  return p;
+}
+
+template <int DQK, int DV>
+__device__ __forceinline__ void bwd_load(BwdStage<DQK, DV>& st, const BwdHead& hp, int i0, int N, int hot) {
   using C = BwdCfg<DQK, DV>;
   const int tid = threadIdx.x;
-  const uint8_t* qrow = a.q_code + bh * N * DQK;
-  const uint8_t* orow = a.do_code + bh * N * DV;
-  const uint8_t* qcol = a.qc_code + bh * DQK * N;
-  const uint8_t* ocol = a.doc_code + bh * DV * N;
   // row tiles: contiguous; bytes past the sequence are read from its last
   // valid 16 bytes (those queries are skipped)
-  const int qlim = (N - i0) * DQK - 16, olim = (N - i0) * DV - 16;
+  const uint8_t* qrow = hp.qrow + i0 * DQK;
+  const uint8_t* orow = hp.orow + i0 * DV;
+  const uint32_t qlim = (N - i0) * DQK - 16, olim = (N - i0) * DV - 16;
 #pragma unroll
   for (int i = 0; i < C::PQ; i++) {
-    const int u = tid + i * C::NT;
-    const int off = (u < C::QU ? u : 0) * 16;
-    st.q[i] = *reinterpret_cast<const uint4*>(qrow + (size_t)i0 * DQK + (off < qlim ? off : qlim));
+    const uint32_t u = tid + i * C::NT;
+    const uint32_t off = (u < C::QU ? u : 0) * 16;
+    st.q[i] = *reinterpret_cast<const uint4*>(qrow + (off < qlim ? off : qlim));
   }
 #pragma unroll
   for (int i = 0; i < C::PO; i++) {
-    const int u = tid + i * C::NT;
-    const int off = (u < C::OU ? u : 0) * 16;
-    st.o[i] = *reinterpret_cast<const uint4*>(orow + (size_t)i0 * DV + (off < olim ? off : olim));
+    const uint32_t u = tid + i * C::NT;
+    const uint32_t off = (u < C::OU ? u : 0) * 16;
+    st.o[i] = *reinterpret_cast<const uint4*>(orow + (off < olim ? off : olim));
   }
+  const int cl = N - 16 - i0;   // last valid 16-byte column piece, relative to i0
 #pragma unroll
   for (int i = 0; i < C::PQC; i++) {
-    const int u = (tid + i * C::NT) < C::QCU ? tid + i * C::NT : 0, c = u >> 2, q = u & 3;
-    const int col = i0 + q * 16 < N - 16 ? i0 + q * 16 : N - 16;
-    st.qc[i] = *reinterpret_cast<const uint4*>(qcol + (size_t)c * N + col);
+    const uint32_t u = (tid + i * C::NT) < C::QCU ? tid + i * C::NT : 0, c = u >> 2, q = u & 3;
+    const int col = (int)q * 16 < cl ? (int)q * 16 : cl;
+    st.qc[i] = *reinterpret_cast<const uint4*>(hp.qcol + i0 + (c * N + col));
   }
 #pragma unroll
   for (int i = 0; i < C::POC; i++) {
-    const int u = (tid + i * C::NT) < C::OCU ? tid + i * C::NT : 0, c = u >> 2, q = u & 3;
-    const int col = i0 + q * 16 < N - 16 ? i0 + q * 16 : N - 16;
-    st.oc[i] = *reinterpret_cast<const uint4*>(ocol + (size_t)c * N + col);
+    const uint32_t u = (tid + i * C::NT) < C::OCU ? tid + i * C::NT : 0, c = u >> 2, q = u & 3;
+    const int col = (int)q * 16 < cl ? (int)q * 16 : cl;
+    st.oc[i] = *reinterpret_cast<const uint4*>(hp.ocol + i0 + (c * N + col));
   }
   if (tid < C::QSD) {
-    const int off = i0 * (DQK / 32) + tid * 4, lim = N * (DQK / 32) - 4;
-    st.qs = *reinterpret_cast<const uint32_t*>(a.q_scale + bh * N * (DQK / 32) + (off < lim ? off : lim));
+    const uint32_t off = i0 * (DQK / 32) + tid * 4, lim = N * (DQK / 32) - 4;
+    st.qs = *reinterpret_cast<const uint32_t*>(hp.qsc + (off < lim ? off : lim));
   }
   if (tid < C::OSD) {
-    const int off = i0 * (DV / 32) + tid * 4, lim = N * (DV / 32) - 4;
-    st.os = *reinterpret_cast<const uint32_t*>(a.do_scale + bh * N * (DV / 32) + (off < lim ? off : lim));
+    const uint32_t off = i0 * (DV / 32) + tid * 4, lim = N * (DV / 32) - 4;
+    st.os = *reinterpret_cast<const uint32_t*>(hp.osc + (off < lim ? off : lim));
   }
   const int g0 = i0 / 32, g1 = (i0 + 32 < N ? i0 + 32 : i0) / 32;
   if (tid < DQK) {
-    const uint8_t* sc = a.qc_scale + (bh * DQK + tid) * (N / 32);
-    st.qcs = (uint32_t)sc[g0] | ((uint32_t)sc[g1] << 8);
+    st.qcs0 = hp.qcsc[tid * (N / 32) + g0];
+    st.qcs1 = hp.qcsc[tid * (N / 32) + g1];
   }
   if (tid < DV) {
-    const uint8_t* sc = a.doc_scale + (bh * DV + tid) * (N / 32);
-    st.ocs = (uint32_t)sc[g0] | ((uint32_t)sc[g1] << 8);
+    st.ocs0 = hp.ocsc[tid * (N / 32) + g0];
+    st.ocs1 = hp.ocsc[tid * (N / 32) + g1];
   }
   if (tid < C::BQ) {
     const int r = i0 + tid < N ? i0 + tid : N - 1;
-    st.L = a.lse[bh * N + r] * kLog2e;
-    const float2 d = *reinterpret_cast<const float2*>(a.delta + (bh * N + r) * 2);
-    st.hi = d.x;
-    st.lo = d.y;
-    st.qh = hot >= 0 ? row_value<DQK>(qrow, a.q_scale + bh * N * (DQK / 32), r, hot) : 0.f;
+    st.L = hp.lse[r];
+    st.dhi = hp.delta[2 * r];
+    st.dlo = hp.delta[2 * r + 1];
+    if (hot >= 0) {
+      st.qhc = hp.qrow[r * DQK + hot];
+      st.qhs = hp.qsc[r * (DQK / 32) + hot / 32];
+    }
   }
 }
 
@@ -143,14 +172,18 @@ __device__ __forceinline__ void bwd_store(const BwdStage<DQK, DV>& st, uint8_t* 
     if (C::OU % C::NT == 0 || u < C::OU)
       *reinterpret_cast<uint4*>(sO + ((u * 16) / DV) * C::OST + (u * 16) % DV) = st.o[i];
   }
+  // col tiles, permuted within each 32-query group (stage_cols_perm); 32-bit
+  // stores keep the compiler from pairing the loaded registers early
 #pragma unroll
   for (int i = 0; i < C::PQC; i++) {
     const int u = tid + i * C::NT;
     if (C::QCU % C::NT == 0 || u < C::QCU) {
       const int c = u >> 2, q = u & 3;
-      uint8_t* base = sQc + c * C::CST + (q >> 1) * 32 + (q & 1) * 8;
-      *reinterpret_cast<uint2*>(base) = make_uint2(st.qc[i].x, st.qc[i].z);
-      *reinterpret_cast<uint2*>(base + 16) = make_uint2(st.qc[i].y, st.qc[i].w);
+      uint32_t* base = reinterpret_cast<uint32_t*>(sQc + c * C::CST + (q >> 1) * 32 + (q & 1) * 8);
+      base[0] = st.qc[i].x;
+      base[1] = st.qc[i].z;
+      base[4] = st.qc[i].y;
+      base[5] = st.qc[i].w;
     }
   }
 #pragma unroll
@@ -158,20 +191,22 @@ __device__ __forceinline__ void bwd_store(const BwdStage<DQK, DV>& st, uint8_t* 
     const int u = tid + i * C::NT;
     if (C::OCU % C::NT == 0 || u < C::OCU) {
       const int c = u >> 2, q = u & 3;
-      uint8_t* base = sOc + c * C::CST + (q >> 1) * 32 + (q & 1) * 8;
-      *reinterpret_cast<uint2*>(base) = make_uint2(st.oc[i].x, st.oc[i].z);
-      *reinterpret_cast<uint2*>(base + 16) = make_uint2(st.oc[i].y, st.oc[i].w);
+      uint32_t* base = reinterpret_cast<uint32_t*>(sOc + c * C::CST + (q >> 1) * 32 + (q & 1) * 8);
+      base[0] = st.oc[i].x;
+      base[1] = st.oc[i].z;
+      base[4] = st.oc[i].y;
+      base[5] = st.oc[i].w;
     }
   }
   if (tid < C::QSD) *reinterpret_cast<uint32_t*>(sQs + tid * 4) = st.qs;
   if (tid < C::OSD) *reinterpret_cast<uint32_t*>(sOs + tid * 4) = st.os;
-  if (tid < DQK) *reinterpret_cast<uint16_t*>(sQcs + tid * 2) = (uint16_t)st.qcs;
-  if (tid < DV) *reinterpret_cast<uint16_t*>(sOcs + tid * 2) = (uint16_t)st.ocs;
+  if (tid < DQK) *reinterpret_cast<uint16_t*>(sQcs + tid * 2) = (uint16_t)(st.qcs0 | (st.qcs1 << 8));
+  if (tid < DV) *reinterpret_cast<uint16_t*>(sOcs + tid * 2) = (uint16_t)(st.ocs0 | (st.ocs1 << 8));
   if (tid < C::BQ) {
-    sRow[tid] = st.L;
-    sRow[C::BQ + tid] = st.hi;
-    sRow[2 * C::BQ + tid] = st.lo;
-    sRow[3 * C::BQ + tid] = st.qh;
+    sRow[tid] = st.L * kLog2e;
+    sRow[C::BQ + tid] = st.dhi;
+    sRow[2 * C::BQ + tid] = st.dlo;
+    sRow[3 * C::BQ + tid] = hot >= 0 ? scaled_value(st.qhc, st.qhs) : 0.f;
   }
 }
 
@@ -193,12 +228,6 @@ __device__ __forceinline__ void stage_col_slice(uint8_t* lds, uint8_t* lds_scale
   }
 }
 
-// max over the 64 lanes of a wave
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int m = 1; m < 32; m <<= 1) v = fmaxf(v, __shfl_xor(v, m));
-  return fmaxf(v, partner(v));
-}
 __device__ __forceinline__ double half_sum_d(double v) {
 #pragma unroll
   for (int m = 1; m < 32; m <<= 1) v += __shfl_xor(v, m);
@@ -213,7 +242,7 @@ __device__ __forceinline__ float half_max(float v) {
 template <int DQK, int DV, bool STATS>
 __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnArgs a) {
   using C = BwdCfg<DQK, DV>;
-  constexpr int NWK = C::NWK, BKB = C::BKB, BQ = C::BQ, NT = C::NT;
+  constexpr int NWK = C::NWK, BKB = C::BKB, BQ = C::BQ;
   constexpr int KS = DQK / 64, VS = DV / 64, CK = DQK / 32, CV = DV / 32;
   __shared__ __attribute__((aligned(16))) uint8_t sQ[C::NBUF][BQ * C::QST];
   __shared__ __attribute__((aligned(16))) uint8_t sQs[C::NBUF][BQ * DQK / 32];
@@ -239,6 +268,8 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
   const int kj = kw0 + li;                      // this lane's key
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
   const size_t bhk = (size_t)b * a.Hkv + kh;
+  const int Hq = (int)a.Hq, G = (int)a.G;
+  const float c = a.c;
 
   // K and V row codes of this lane's key (B operands of S and dP)
   v8i kf[KS], vf[VS];
@@ -262,37 +293,42 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
     if (hot >= 0) khot = row_value<DQK>(a.k_code + bhk * N * DQK, a.k_scale + bhk * N * (DQK / 32), row, hot);
   }
   // K col codes of the workgroup's keys (B operand of dQ), once
-  stage_col_slice<DQK, BKB, C::KCST, NT>(sKc, sKcs, a.kc_code + bhk * DQK * N, a.kc_scale + bhk * DQK * (N / 32),
-                                         kb0, N);
+  stage_col_slice<DQK, BKB, C::KCST, C::NT>(sKc, sKcs, a.kc_code + bhk * DQK * N,
+                                           a.kc_scale + bhk * DQK * (N / 32), kb0, N);
 
   v16f dk[CK], dv[CV];
 #pragma unroll
-  for (int c = 0; c < CK; c++)
+  for (int i = 0; i < CK; i++)
 #pragma unroll
-    for (int r = 0; r < 16; r++) dk[c][r] = 0.f;
+    for (int r = 0; r < 16; r++) dk[i][r] = 0.f;
 #pragma unroll
-  for (int c = 0; c < CV; c++)
+  for (int i = 0; i < CV; i++)
 #pragma unroll
-    for (int r = 0; r < 16; r++) dv[c][r] = 0.f;
+    for (int r = 0; r < 16; r++) dv[i][r] = 0.f;
 
-  const int G = (int)a.G;
   const int nqt = (N + BQ - 1) / BQ, qt0 = kb0 / BQ, nq = nqt - qt0;
   const int total = G * nq;
   BwdStage<DQK, DV> st;
-  bwd_load<DQK, DV>(st, a, (size_t)b * a.Hq + (size_t)kh * G, qt0 * BQ, N, hot);
+  bwd_load<DQK, DV>(st, bwd_head<DQK, DV>(a, (size_t)b * Hq + kh * G, N), qt0 * BQ, N, hot);
   bwd_store<DQK, DV>(st, sQ[0], sQs[0], sO[0], sOs[0], sQc[0], sQcs[0], sOc[0], sOcs[0], sRow[0], hot);
   __syncthreads();
 
+  // dQ atomics: lane part of the offset into the [B, N, Hq, Dqk] workspace
+  const uint32_t HqD = (uint32_t)Hq * DQK;
+  const uint32_t dq_lane = (uint32_t)(4 * hf) * HqD + li;
+
   for (int it = 0; it < total; it++) {
-    const int cur = C::NBUF == 2 ? (it & 1) : 0;  // staging buffer of this tile
+    const int cur = C::NBUF == 2 ? (it & 1) : 0;   // staging buffer of this tile
     const int dsb = C::NDS == 2 ? (it & 1) : 0;
-    const int hh = it / nq, qt = qt0 + it % nq;
-    const int h = kh * G + hh;
-    const size_t bh = (size_t)b * a.Hq + h;
-    const int i0 = qt * BQ;
-    if (it + 1 < total) {
-      const int hn = kh * G + (it + 1) / nq, qn = qt0 + (it + 1) % nq;
-      bwd_load<DQK, DV>(st, a, (size_t)b * a.Hq + hn, qn * BQ, N, hot);
+    const int h = kh * G + it / nq;
+    const int i0 = (qt0 + it % nq) * BQ;
+    {
+      // next tile (the last iteration reloads the first one into the idle
+      // buffer): loads are issued unconditionally so that no merge of old and
+      // new register values forces a wait right here
+      const int itn = it + 1 < total ? it + 1 : 0;
+      bwd_load<DQK, DV>(st, bwd_head<DQK, DV>(a, (size_t)b * Hq + kh * G + itn / nq, N),
+                        (qt0 + itn % nq) * BQ, N, hot);
     }
 
     const uint8_t* Q = sQ[cur];
@@ -300,17 +336,20 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
     const uint8_t* O = sO[cur];
     const uint8_t* Os = sOs[cur];
     const float* Row = sRow[cur];
-    uint32_t pc[2][4], dc[2][4];
+    v8i pa, da;          // P' and dS' codes: A operands of dV and dK (k = the tile's 64 queries)
     int dse[2] = {-127, -127};
     bool any = false;
+    // tiles wholly after the workgroup's keys and inside the sequence: no
+    // mask, no skipped sub-block
+    const bool full = i0 >= kb0 + BKB && i0 + BQ <= N;
+
+    auto subblock = [&](const int qs, auto edge_tag) {
+      constexpr bool EDGE = decltype(edge_tag)::value;
+      const int qb = i0 + 32 * qs;               // first query of the sub-block
+      if (EDGE && (!live || qb < kw0 || qb >= N)) {
 #pragma unroll
-    for (int qs = 0; qs < 2; qs++) {
-      const int qb = i0 + 32 * qs;             // first query of the sub-block
-      // wave-uniform: skip sub-blocks wholly before this wave's keys or past the sequence
-      if (!live || qb < kw0 || qb >= N) {
-#pragma unroll
-        for (int k = 0; k < 4; k++) { pc[qs][k] = 0u; dc[qs][k] = 0u; }
-        continue;
+        for (int k = 0; k < 4; k++) { pa[4 * qs + k] = 0; da[4 * qs + k] = 0; }
+        return;
       }
       any = true;
       v16f s, dp;
@@ -325,7 +364,6 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
         dp = mfma_mx(frag_rows<C::OST>(O, 32 * qs + li, t, hf), vf[t], dp,
                      Os[(32 * qs + li) * (DV / 32) + 2 * t + hf], vsc[t]);
       // lane holds queries qb + 8 g + 4 hf + e (accumulator r = 4 g + e)
-      float P[16], dS[16];
       float amax = 0.f;
 #pragma unroll
       for (int g = 0; g < 4; g++) {
@@ -339,34 +377,35 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
 #pragma unroll
         for (int e = 0; e < 4; e++) {
           const int r = 4 * g + e;
-          float p = bwd_prob(__builtin_fmaf(Qh[e], khot, s[r]), a.c, Lv[e]);
-          if (qb == kw0) p = (li > 8 * g + 4 * hf + e) ? 0.f : p;   // diagonal block: key > query
-          P[r] = p;
-          dS[r] = p * ((dp[r] - Hv[e]) - Ov[e]);
-          amax = fmaxf(amax, fabsf(dS[r]));
+          float p = bwd_prob(__builtin_fmaf(Qh[e], khot, s[r]), c, Lv[e]);
+          if (EDGE && qb == kw0) p = (li > 8 * g + 4 * hf + e) ? 0.f : p;   // diagonal block: key > query
+          s[r] = p;
+          dp[r] = p * ((dp[r] - Hv[e]) - Ov[e]);
+          amax = fmaxf(amax, fabsf(dp[r]));
         }
       }
 #pragma unroll
       for (int k = 0; k < 4; k++)
-        pc[qs][k] = cvt4_div(P[4 * k], P[4 * k + 1], P[4 * k + 2], P[4 * k + 3], 0.00390625f);
-      int e = pow2_exponent(wave_max(amax));
+        pa[4 * qs + k] = (int)cvt4_div(s[4 * k], s[4 * k + 1], s[4 * k + 2], s[4 * k + 3], 0.00390625f);
+      int e = pow2_exponent(wave_max_nonneg(amax));
       e = e < -126 ? -126 : e;
       const float sc = exp2i(e);
 #pragma unroll
-      for (int k = 0; k < 4; k++) dc[qs][k] = cvt4_div(dS[4 * k], dS[4 * k + 1], dS[4 * k + 2], dS[4 * k + 3], sc);
+      for (int k = 0; k < 4; k++)
+        da[4 * qs + k] = (int)cvt4_div(dp[4 * k], dp[4 * k + 1], dp[4 * k + 2], dp[4 * k + 3], sc);
       dse[qs] = e;
       if constexpr (STATS) {
         // per query row: FP64 sums over this wave's 32 keys, then atomics
 #pragma unroll
         for (int r = 0; r < 16; r++) {
-          const float cast = fp8_value(dc[qs][r >> 2], r & 3) * sc;
-          const double s0 = half_sum_d((double)dS[r]);
-          const double s1 = half_sum_d((double)fabsf(dS[r]));
+          const float cast = fp8_value((uint32_t)da[4 * qs + (r >> 2)], r & 3) * sc;
+          const double s0 = half_sum_d((double)dp[r]);
+          const double s1 = half_sum_d((double)fabsf(dp[r]));
           const double s2 = half_sum_d((double)cast);
-          const float mx = half_max(fabsf(dS[r]));
+          const float mx = half_max(fabsf(dp[r]));
           const int qi = qb + 8 * (r >> 2) + 4 * hf + (r & 3);
           if (li == 0) {
-            double* sp = a.rowstats + (bh * N + qi) * 4;
+            double* sp = a.rowstats + (((size_t)b * Hq + h) * N + qi) * 4;
             atomicAdd(sp + 0, s0);
             atomicAdd(sp + 1, s1);
             atomicAdd(sp + 2, s2);
@@ -375,24 +414,27 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
           }
         }
       }
+    };
+    if (full) {
+      subblock(0, std::false_type{});
+      subblock(1, std::false_type{});
+    } else {
+      subblock(0, std::true_type{});
+      subblock(1, std::true_type{});
     }
     if (any) {
       // dV += P'^T dO_col ; dK += dS'^T Q_col   (k = the 64 queries of the tile)
-      const v8i pa = v8i{(int)pc[0][0], (int)pc[0][1], (int)pc[0][2], (int)pc[0][3],
-                         (int)pc[1][0], (int)pc[1][1], (int)pc[1][2], (int)pc[1][3]};
-      const v8i da = v8i{(int)dc[0][0], (int)dc[0][1], (int)dc[0][2], (int)dc[0][3],
-                         (int)dc[1][0], (int)dc[1][1], (int)dc[1][2], (int)dc[1][3]};
       const int dascale = (hf ? dse[1] : dse[0]) + 127;
       const uint8_t* Oc = sOc[cur];
       const uint8_t* Ocs = sOcs[cur];
       const uint8_t* Qc = sQc[cur];
       const uint8_t* Qcs = sQcs[cur];
 #pragma unroll
-      for (int c = 0; c < CV; c++)
-        dv[c] = mfma_mx(pa, frag_cols<C::CST>(Oc, 32 * c + li, hf), dv[c], 127 - 8, Ocs[(32 * c + li) * 2 + hf]);
+      for (int i = 0; i < CV; i++)
+        dv[i] = mfma_mx(pa, frag_cols<C::CST>(Oc, 32 * i + li, hf), dv[i], 127 - 8, Ocs[(32 * i + li) * 2 + hf]);
 #pragma unroll
-      for (int c = 0; c < CK; c++)
-        dk[c] = mfma_mx(da, frag_cols<C::CST>(Qc, 32 * c + li, hf), dk[c], dascale, Qcs[(32 * c + li) * 2 + hf]);
+      for (int i = 0; i < CK; i++)
+        dk[i] = mfma_mx(da, frag_cols<C::CST>(Qc, 32 * i + li, hf), dk[i], dascale, Qcs[(32 * i + li) * 2 + hf]);
     }
     // dS' codes to LDS: row = key (32 w + li), columns = the lane's queries
     uint8_t* dS_l = sdS[dsb];
@@ -400,7 +442,7 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
     for (int qs = 0; qs < 2; qs++)
 #pragma unroll
       for (int g = 0; g < 4; g++)
-        *reinterpret_cast<uint32_t*>(dS_l + (32 * w + li) * C::DST + 32 * qs + 8 * g + 4 * hf) = dc[qs][g];
+        *reinterpret_cast<int*>(dS_l + (32 * w + li) * C::DST + 32 * qs + 8 * g + 4 * hf) = da[4 * qs + g];
     if (lane == 0) {
       sdSs[dsb][w * 2] = (uint8_t)(dse[0] + 127);
       sdSs[dsb][w * 2 + 1] = (uint8_t)(dse[1] + 127);
@@ -408,14 +450,13 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
     // the next tile into the other staging buffer (nobody reads it this tile)
     if constexpr (C::NBUF == 2) {
       const int nb = cur ^ 1;
-      if (it + 1 < total)
-        bwd_store<DQK, DV>(st, sQ[nb], sQs[nb], sO[nb], sOs[nb], sQc[nb], sQcs[nb], sOc[nb], sOcs[nb], sRow[nb], hot);
+      bwd_store<DQK, DV>(st, sQ[nb], sQs[nb], sO[nb], sOs[nb], sQc[nb], sQcs[nb], sOc[nb], sOcs[nb], sRow[nb], hot);
     }
     __syncthreads();
     // dQ tile (64 queries x DQK) = dS'(64 x BKB) K_col(BKB x DQK): output blocks
-    // m = qs * CK + c, distributed round-robin over the waves
+    // m = qs * CK + i, distributed round-robin over the waves
     for (int m = w; m < 2 * CK; m += NWK) {
-      const int qs = m / CK, c = m % CK;
+      const int qs = m / CK, i = m % CK;
       const int qb = i0 + 32 * qs;
       if (qb >= N) continue;
       v16f acc;
@@ -427,24 +468,23 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
       for (int ks = 0; ks < BKB / 64; ks++) {
         if (kb0 + 64 * ks > qb + 31) break;    // these keys are all in the future of the sub-block
         // A: rows = queries of sub-block qs, k = keys 64 ks .. 64 ks + 63 (natural order)
-        int words[8];
+        v8i af;
 #pragma unroll
         for (int part = 0; part < 4; part++) {
           const int kk = 64 * ks + 32 * (part >> 1) + 16 * hf + 8 * (part & 1);
           const uint8_t* addr = dS_l + (kk + (i16 >> 1)) * C::DST + qbase + 8 * (i16 & 1);
           const v2i t = __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i*)(addr));
-          words[2 * part] = t[0];
-          words[2 * part + 1] = t[1];
+          af[2 * part] = t[0];
+          af[2 * part + 1] = t[1];
         }
-        const v8i af = v8i{words[0], words[1], words[2], words[3], words[4], words[5], words[6], words[7]};
-        acc = mfma_mx(af, frag_rows<C::KCST>(sKc, 32 * c + li, ks, hf), acc, sdSs[dsb][(2 * ks + hf) * 2 + qs],
-                      sKcs[(32 * c + li) * (BKB / 32) + 2 * ks + hf]);
+        acc = mfma_mx(af, frag_rows<C::KCST>(sKc, 32 * i + li, ks, hf), acc, sdSs[dsb][(2 * ks + hf) * 2 + qs],
+                      sKcs[(32 * i + li) * (BKB / 32) + 2 * ks + hf]);
       }
-      // lane holds channel 32 c + li, queries qb + 8 (r/4) + 4 hf + r % 4
-      float* base = a.dq_acc + ((size_t)b * N * a.Hq + h) * DQK + 32 * c + li;
+      // lane holds channel 32 i + li, queries qb + 8 (r/4) + 4 hf + r % 4
+      float* dqb = a.dq_acc + (((size_t)b * N + qb) * Hq + h) * DQK + 32 * i;
 #pragma unroll
       for (int r = 0; r < 16; r++)
-        atomicAdd(base + (size_t)(qb + 8 * (r >> 2) + 4 * hf + (r & 3)) * a.Hq * DQK, acc[r]);
+        atomicAdd(dqb + (uint32_t)(8 * (r >> 2) + (r & 3)) * HqD + dq_lane, acc[r]);
     }
     if constexpr (C::NDS == 1) __syncthreads();   // single dS buffer: reads done before the next writes
     if constexpr (C::NBUF == 1) {
@@ -456,7 +496,7 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
     }
   }
   if (!live) return;
-  // dK (times tau) and dV: lane holds channel 32 c + li, keys kw0 + 8 (r/4) + 4 hf + r % 4
+  // dK (times tau) and dV: lane holds channel 32 i + li, keys kw0 + 8 (r/4) + 4 hf + r % 4
 #pragma unroll
   for (int r = 0; r < 16; r++) {
     const int key = kw0 + 8 * (r >> 2) + 4 * hf + (r & 3);
@@ -464,16 +504,16 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
       uint16_t* kd = reinterpret_cast<uint16_t*>(a.dk) + b * a.dks[0] + (int64_t)key * a.dks[1] + kh * a.dks[2];
       uint16_t* vd = reinterpret_cast<uint16_t*>(a.dv) + b * a.dvs[0] + (int64_t)key * a.dvs[1] + kh * a.dvs[2];
 #pragma unroll
-      for (int c = 0; c < CK; c++) kd[32 * c + li] = f32_to_bf16(dk[c][r] * a.tau);
+      for (int i = 0; i < CK; i++) kd[32 * i + li] = f32_to_bf16(dk[i][r] * a.tau);
 #pragma unroll
-      for (int c = 0; c < CV; c++) vd[32 * c + li] = f32_to_bf16(dv[c][r]);
+      for (int i = 0; i < CV; i++) vd[32 * i + li] = f32_to_bf16(dv[i][r]);
     } else {
       float* kd = reinterpret_cast<float*>(a.dk) + b * a.dks[0] + (int64_t)key * a.dks[1] + kh * a.dks[2];
       float* vd = reinterpret_cast<float*>(a.dv) + b * a.dvs[0] + (int64_t)key * a.dvs[1] + kh * a.dvs[2];
 #pragma unroll
-      for (int c = 0; c < CK; c++) kd[32 * c + li] = dk[c][r] * a.tau;
+      for (int i = 0; i < CK; i++) kd[32 * i + li] = dk[i][r] * a.tau;
 #pragma unroll
-      for (int c = 0; c < CV; c++) vd[32 * c + li] = dv[c][r];
+      for (int i = 0; i < CV; i++) vd[32 * i + li] = dv[i][r];
     }
   }
 }

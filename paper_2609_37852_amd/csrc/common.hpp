@@ -92,6 +92,22 @@ __device__ __forceinline__ Pair permlane32_swap(float a, float b) {
   return Pair{__uint_as_float(r[0]), __uint_as_float(r[1])};
 }
 
+// Maximum over the 64 lanes of a wave of a non-negative value (FP32 order of
+// non-negative values is the integer order of their bit patterns): DPP within
+// rows of 16 lanes, then the row and half swaps of gfx950.
+__device__ __forceinline__ float wave_max_nonneg(float v) {
+  uint32_t u = __float_as_uint(v);
+  u = max(u, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0xB1, 0xf, 0xf, false));   // quad_perm 1,0,3,2
+  u = max(u, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x4E, 0xf, 0xf, false));   // quad_perm 2,3,0,1
+  u = max(u, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x124, 0xf, 0xf, false));  // row_ror 4
+  u = max(u, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x128, 0xf, 0xf, false));  // row_ror 8
+  auto r16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);                        // rows 2k <-> 2k+1
+  u = max((uint32_t)r16[0], (uint32_t)r16[1]);
+  auto r32 = __builtin_amdgcn_permlane32_swap(u, u, false, false);                        // halves
+  u = max((uint32_t)r32[0], (uint32_t)r32[1]);
+  return __uint_as_float(u);
+}
+
 // Value of `v` in the partner lane l ^ 32.
 __device__ __forceinline__ float partner(float v) {
   Pair p = permlane32_swap(v, v);

@@ -47,9 +47,11 @@ struct FwdPrefetch {
   uint4 k[T::KU];
   uint4 v[T::VU];
   uint32_t ks;     // 4 K scale bytes (thread < DQK)
-  uint32_t vs;     // 4 V scale bytes of one channel (thread < DV)
-  float kh;        // isolated-channel value of one key (thread < BK)
+  uint32_t vs[4];  // V scale bytes of one channel, one per 32-key group (thread < DV)
+  uint32_t khc, khs;  // isolated-channel code and scale byte of one key (thread < BK)
 };
+// Only loads are issued here; everything that needs the loaded values waits
+// for fwd_store, so the loads stay in flight while the current tile is computed.
 
 template <int DQK, int DV, int NW>
 __device__ __forceinline__ void fwd_load(FwdPrefetch<DQK, DV, NW>& f, const uint8_t* kcode, const uint8_t* kscale,
@@ -76,17 +78,16 @@ __device__ __forceinline__ void fwd_load(FwdPrefetch<DQK, DV, NW>& f, const uint
     f.ks = *reinterpret_cast<const uint32_t*>(kscale + (off < lim ? off : lim));
   }
   if (tid < DV) {   // V scales: 4 groups of channel tid
-    uint32_t w = 0;
 #pragma unroll
     for (int g = 0; g < 4; g++) {
       const int grp = (j0 + 32 * g < N ? j0 + 32 * g : N - 32) / 32;
-      w |= (uint32_t)vscale[(size_t)tid * (N / 32) + grp] << (8 * g);
+      f.vs[g] = vscale[tid * (N / 32) + grp];
     }
-    f.vs = w;
   }
-  if (tid < T::BK) {
+  if (tid < T::BK && hot >= 0) {
     const int r = j0 + tid < N ? j0 + tid : N - 1;
-    f.kh = hot >= 0 ? row_value<DQK>(kcode, kscale, r, hot) : 0.f;
+    f.khc = kcode[r * DQK + hot];
+    f.khs = kscale[r * (DQK / 32) + hot / 32];
   }
 }
 
@@ -108,13 +109,18 @@ __device__ __forceinline__ void fwd_store(const FwdPrefetch<DQK, DV, NW>& f, uin
     const int u = tid + i * T::NT, c = u / (T::BK / 16), q = u % (T::BK / 16);
     // 16 keys 16q..16q+15: group q/2; within the group, 4-key chunks go to
     // position 16 * (chunk & 1) + 4 * (chunk >> 1) (see stage_cols_perm)
-    uint8_t* base = sV + c * T::VST + (q >> 1) * 32 + (q & 1) * 8;
-    *reinterpret_cast<uint2*>(base) = make_uint2(f.v[i].x, f.v[i].z);
-    *reinterpret_cast<uint2*>(base + 16) = make_uint2(f.v[i].y, f.v[i].w);
+    // (32-bit stores: a 64-bit store of {x, z} would make the compiler pair
+    // the registers right after the load and wait for it there)
+    uint32_t* base = reinterpret_cast<uint32_t*>(sV + c * T::VST + (q >> 1) * 32 + (q & 1) * 8);
+    base[0] = f.v[i].x;
+    base[1] = f.v[i].z;
+    base[4] = f.v[i].y;
+    base[5] = f.v[i].w;
   }
   if (tid < DQK) *reinterpret_cast<uint32_t*>(sKs + tid * 4) = f.ks;
-  if (tid < DV) *reinterpret_cast<uint32_t*>(sVs + tid * 4) = f.vs;
-  if (tid < T::BK) sKh[tid] = f.kh;
+  if (tid < DV)
+    *reinterpret_cast<uint32_t*>(sVs + tid * 4) = f.vs[0] | (f.vs[1] << 8) | (f.vs[2] << 16) | (f.vs[3] << 24);
+  if (tid < T::BK) sKh[tid] = hot >= 0 ? scaled_value(f.khc, f.khs) : 0.f;
 }
 
 template <int DQK, int DV, int NW>
@@ -179,7 +185,10 @@ __global__ __launch_bounds__(64 * NW, 2) void fwd_kernel(AttnArgs a) {
   for (int it = 0; it < ntiles; it++) {
     const int cur = it & 1;
     const int j0 = (ntiles - 1 - it) * BK;
-    if (it + 1 < ntiles) fwd_load<DQK, DV, NW>(pf, kcode, kscale, vcode, vscale, j0 - BK, N, hot);
+    // always issue the next tile's loads (the last iteration reloads tile 0
+    // into the idle buffer): a conditional load would merge old and new
+    // register values after the branch and wait for the loads right there
+    fwd_load<DQK, DV, NW>(pf, kcode, kscale, vcode, vscale, j0 >= BK ? j0 - BK : 0, N, hot);
 
     if (live && j0 <= q0) {
       const uint8_t* K = sK[cur];
@@ -284,7 +293,7 @@ __global__ __launch_bounds__(64 * NW, 2) void fwd_kernel(AttnArgs a) {
         }
       }
     }
-    if (it + 1 < ntiles) fwd_store<DQK, DV, NW>(pf, sK[cur ^ 1], sKs[cur ^ 1], sV[cur ^ 1], sVs[cur ^ 1], sKh[cur ^ 1], hot);
+    fwd_store<DQK, DV, NW>(pf, sK[cur ^ 1], sKs[cur ^ 1], sV[cur ^ 1], sVs[cur ^ 1], sKh[cur ^ 1], hot);
     __syncthreads();
   }
   if (!live) return;

@@ -108,6 +108,11 @@ __device__ __forceinline__ void clear_channel(v8i& f, int s, int hf, int hot) {
   for (int d = 0; d < 8; d++) f[d] = (int)((uint32_t)f[d] & (d == (t >> 2) ? m : 0xffffffffu));
 }
 
+// Value of one E4M3 code (low byte of `code`) with its E8M0 scale byte.
+__device__ __forceinline__ float scaled_value(uint32_t code, uint32_t scale) {
+  return __builtin_ldexpf(fp8_value(code, 0), (int)(scale & 0xff) - 127);
+}
+
 // Decoded value of the element in column `col` of row `row` of a row copy.
 template <int D>
 __device__ __forceinline__ float row_value(const uint8_t* code, const uint8_t* scale, int64_t row, int col) {
