@@ -62,20 +62,22 @@ class HipEvents:
         return float(out.value)
 
 
-def cpu_baseline(w, d, threads):
-    """The oracle (FP64 C, OpenMP) timed on the host cores on one query head
-    of batch 0 at the full sequence length."""
+def cpu_baseline(w, d, threads, kv_heads=2):
+    """The oracle (FP64 C, OpenMP) timed on the host cores on the first
+    `kv_heads` KV groups of batch 0 at the full sequence length."""
     import oracle as orc
     from paper_2609_37852_amd import synth
-    sl = dict(q=d["q"][:1, :, :1], k=d["k"][:1, :, :1], v=d["v"][:1, :, :1], do=d["do"][:1, :, :1])
-    ws = synth.with_shape(w, B=1, Hq=1, Hkv=1)
+    hk = min(kv_heads, w.Hkv)
+    hq = hk * (w.Hq // w.Hkv)
+    sl = dict(q=d["q"][:1, :, :hq], k=d["k"][:1, :, :hk], v=d["v"][:1, :, :hk], do=d["do"][:1, :, :hq])
+    ws = synth.with_shape(w, B=1, Hq=hq, Hkv=hk)
     t = time.perf_counter()
     orc.attention_from_inputs(sl["q"], sl["k"], sl["v"], sl["do"], float(np.float32(w.tau)), nthreads=threads)
     dt = time.perf_counter() - t
     f, b = ws.credited_flops()
     return dict(value=round((f + b) / dt / 1e12, 6), unit="TFLOP/s", cores=threads, kind="oracle",
-                sample=f"batch 0, query head 0 (KV head 0), N={w.N}: quantize + fwd + matched "
-                       f"delta + bwd in FP64, {dt:.1f} s, credited {(f + b) / 1e9:.1f} GFLOP")
+                sample=f"batch 0, query heads 0..{hq - 1} (KV heads 0..{hk - 1}), N={w.N}: quantize + fwd + "
+                       f"matched delta + bwd in FP64, {dt:.1f} s, credited {(f + b) / 1e9:.1f} GFLOP")
 
 
 def main():
@@ -86,6 +88,9 @@ def main():
     ap.add_argument("--workload", default="gqa_d128_8k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic", default=None, help="JSON file with measured HBM bytes of the bwd kernel")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="after the timed steps, copy MIB MiB device-to-device once (a plain copy kernel whose "
+                         "FETCH_SIZE / WRITE_SIZE calibrate the HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the hot path runs on a "
@@ -206,6 +211,14 @@ def main():
                      "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP8_TFLOPS, 4),
                      "traffic": traffic},
     }
+    if args.copy_calibration > 0:
+        n = args.copy_calibration << 20
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        line["copy_calibration_bytes"] = n
     if not args.no_cpu_baseline:
         threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
         line["cpu_baseline"] = cpu_baseline(w, d, threads)
