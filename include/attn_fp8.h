@@ -146,8 +146,10 @@ int attn_fp8_delta(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx*
                    const int64_t dout_strides[3], const void* o, int o_dtype,
                    const int64_t o_strides[3], float* delta, hipStream_t stream);
 
-/* Workspace bytes attn_fp8_bwd needs for this problem (FP32 dQ accumulator
- * plus the internal delta buffer).  Returns 0 / negative status. */
+/* Workspace bytes attn_fp8_bwd needs for this problem: FP32 dQ accumulator
+ * [B,N,Hq,Dqk], the internal delta buffer [B,Hq,N,2] and 16-byte per-query
+ * records [B,Hq,N] (LSE log2 e, delta, isolated-channel value) that the main
+ * kernel streams with its query tiles.  Returns 0 / negative status. */
 int attn_fp8_bwd_workspace_size(const attn_fp8_problem* p, size_t* bytes);
 
 /* Backward (Sec. 2.3; App. B.6.3).  Key-major pass: recompute S, P, dP;

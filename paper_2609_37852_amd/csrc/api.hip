@@ -124,11 +124,28 @@ void set_col(const attn_fp8_mx* m, const uint8_t*& code, const uint8_t*& scale) 
 
 size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
 
-size_t ws_dq_bytes(const attn_fp8_problem* p) {
-  return round256((size_t)p->batch * p->seqlen * p->heads_q * p->dim_qk * sizeof(float));
+// stored dQ operand units (2048 B each) and their exponents (2 B each)
+size_t ws_units_bytes(const attn_fp8_problem* p) {
+  return round256((size_t)p->batch * p->heads_q * (size_t)afp8::dq_units_per_head(p->seqlen) * 2048);
+}
+size_t ws_exp_bytes(const attn_fp8_problem* p) {
+  return round256((size_t)p->batch * p->heads_q * (size_t)afp8::dq_units_per_head(p->seqlen) * 2);
 }
 size_t ws_delta_bytes(const attn_fp8_problem* p) {
   return round256((size_t)p->batch * p->heads_q * p->seqlen * 2 * sizeof(float));
+}
+size_t ws_rows_bytes(const attn_fp8_problem* p) {
+  return round256((size_t)p->batch * p->heads_q * p->seqlen * 4 * sizeof(float));
+}
+size_t ws_tile_cs_bytes(const attn_fp8_problem* p) {
+  return round256((size_t)p->batch * p->heads_q * ((p->seqlen + 63) / 64) * 2 * (p->dim_qk + p->dim_v));
+}
+size_t ws_tile_kcs_bytes(const attn_fp8_problem* p) {
+  return round256((size_t)p->batch * p->heads_kv * ((p->seqlen + 63) / 64) * 2 * p->dim_qk);
+}
+size_t ws_bwd_bytes(const attn_fp8_problem* p) {
+  return ws_units_bytes(p) + ws_exp_bytes(p) + ws_delta_bytes(p) + ws_rows_bytes(p) + ws_tile_cs_bytes(p) +
+         ws_tile_kcs_bytes(p);
 }
 
 int hip_status(hipError_t e, const char* what) {
@@ -281,7 +298,7 @@ int attn_fp8_bwd_workspace_size(const attn_fp8_problem* p, size_t* bytes) {
   int rc;
   if ((rc = check_problem(p))) return rc;
   if (!bytes) return fail(ATTN_FP8_EINVAL, "bytes is NULL");
-  *bytes = ws_dq_bytes(p) + ws_delta_bytes(p);
+  *bytes = ws_bwd_bytes(p);
   return ok();
 }
 
@@ -310,22 +327,25 @@ int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q
     return rc;
   }
   if (rowstats && !aligned16(rowstats)) return fail(ATTN_FP8_EALIGN, "rowstats is not 16-byte aligned");
-  const size_t need = ws_dq_bytes(p) + ws_delta_bytes(p);
+  const size_t need = ws_bwd_bytes(p);
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
     return fail(ATTN_FP8_EWORKSPACE, "workspace is NULL or not 256-byte aligned");
   if (workspace_bytes < need)
     return fail(ATTN_FP8_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
 
-  float* dq_acc = reinterpret_cast<float*>(workspace);
-  float* delta = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + ws_dq_bytes(p));
+  uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+  uint8_t* ds_units = ws;
+  uint8_t* ds_exp = ds_units + ws_units_bytes(p);
+  float* delta = reinterpret_cast<float*>(ds_exp + ws_exp_bytes(p));
+  float* rows = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(delta) + ws_delta_bytes(p));
+  uint8_t* tile_cs = reinterpret_cast<uint8_t*>(rows) + ws_rows_bytes(p);
+  uint8_t* tile_kcs = tile_cs + ws_tile_cs_bytes(p);
   if (delta_in) {
     delta = const_cast<float*>(delta_in);
   } else if ((rc = launch_delta(p, delta_mode, q, k, v, dout, lse, dout_raw, dout_dtype, dout_strides, o, o_dtype,
                                 o_strides, delta, stream))) {
     return rc;
   }
-  const int64_t ndq = p->batch * p->seqlen * p->heads_q * p->dim_qk;
-  if ((rc = hip_status(afp8::launch_fill_zero(dq_acc, ndq, stream), "fill_zero"))) return rc;
 
   afp8::AttnArgs a = base_args(p);
   set_row(q, a.q_code, a.q_scale);
@@ -338,30 +358,27 @@ int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q
   set_amax(a, q, k);
   a.lse = lse;
   a.delta = delta;
-  a.dq_acc = dq_acc;
+  a.ds_units = ds_units;
+  a.ds_exp = ds_exp;
+  a.dq = dq;
   a.dk = dk;
   a.dv = dv;
   for (int i = 0; i < 3; i++) {
     a.dks[i] = dk_strides[i];
     a.dvs[i] = dv_strides[i];
+    a.dqs[i] = dq_strides[i];
   }
   a.grad_bf16 = grad_dtype == ATTN_FP8_DTYPE_BF16;
   a.rowstats = rowstats;
+  a.rows = rows;
+  a.tile_cs = tile_cs;
+  a.tile_kcs = tile_kcs;
+  if ((rc = hip_status(afp8::launch_bwd_prep(a, (int)p->dim_qk, (int)p->dim_v, stream), "bwd_prep"))) return rc;
   if (main_events && (rc = hip_status(hipEventRecord(main_events[0], stream), "event record"))) return rc;
   if ((rc = hip_status(afp8::launch_bwd(a, (int)p->dim_qk, (int)p->dim_v, stream), "bwd"))) return rc;
   if (main_events && (rc = hip_status(hipEventRecord(main_events[1], stream), "event record"))) return rc;
 
-  afp8::DqFinalArgs f{};
-  f.acc = dq_acc;
-  f.dq = dq;
-  for (int i = 0; i < 3; i++) f.s[i] = dq_strides[i];
-  f.B = p->batch;
-  f.N = p->seqlen;
-  f.Hq = p->heads_q;
-  f.D = p->dim_qk;
-  f.tau = p->softmax_scale;
-  if ((rc = hip_status(afp8::launch_dq_finalize(f, grad_dtype == ATTN_FP8_DTYPE_BF16, stream), "dq_finalize")))
-    return rc;
+  if ((rc = hip_status(afp8::launch_dq(a, (int)p->dim_qk, stream), "dq"))) return rc;
   return ok();
 }
 

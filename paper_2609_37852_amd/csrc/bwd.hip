@@ -3,10 +3,13 @@
 // Key-major: a workgroup owns BKB = 32*NWK keys of one (batch, KV head); wave
 // w owns keys 32w..32w+31 of them.  The workgroup loops over the query heads
 // of the KV group and over 64-query tiles from the causal diagonal to the end
-// of the sequence.  dK and dV for its keys stay in registers (FP32) across
-// the whole loop, which is the GQA group sum.  The next query tile's codes
-// are loaded into registers while the current one is computed (LDS
-// double-buffered where it fits).
+// of the sequence.  dK and dV for its keys stay in MFMA accumulators (FP32)
+// across the whole loop, which is the GQA group sum.
+//
+// Query tiles reach LDS by direct global->LDS loads (no registers): while
+// tile t is computed, tile t+1 streams into the other stage buffer.  Tile
+// layouts are unpadded with an XOR swizzle of the 16-byte chunks, chosen so
+// that the 16-byte fragment reads of 16 consecutive lanes hit distinct banks.
 //
 // Per wave, tile and 32-query sub-block qs (near the diagonal a sub-block is
 // skipped when it lies wholly before the wave's keys or past the sequence,
@@ -18,14 +21,21 @@
 //   P  = bwd_prob(S + q_c* k_c*), dS = P ((dP - hi) - lo).
 //   P' = C8(256 P) with scale 2^-8;  dS' = C8(dS / 2^e) with one exponent e
 //        per aligned 32x32 block (the wave's 32 keys x 32 queries).
-//   dV += P'^T dO_col,  dK += dS'^T Q_col   (A = codes straight from
-//                             registers, B = col tiles in LDS permuted to the
-//                             lane's queries).
-// dQ: every wave writes its dS' codes to LDS ([key][query]); after the tile's
-// barrier the 64 x Dqk dQ tile = dS'(64 x BKB) K_col(BKB x Dqk) is split over
-// the waves, the dS' operand read with the 8-bit LDS transpose, and added to
-// the FP32 workspace with atomics (dQ = tau * workspace is stored by a second
-// kernel).
+//   dV += P'^T dO_col,  dK += dS'^T Q_col   (A = the codes after one
+//                             v_permlane32_swap per dword pair puts each
+//                             lane's 16 queries in natural order).
+// dQ: every wave writes its dS' codes to LDS ([key][query]); after the
+// tile's barrier, at the start of the next iteration, the waves read them
+// back with the 8-bit LDS transpose read as the A operands of dQ = dS' K_col
+// (32 queries x 64 keys each, the "units") and store those to HBM, in the
+// register order of the MFMA operand, with their two block exponents (the
+// paper also stores FP8 dS between passes).  dq_kernel then computes
+// dQ = tau dS' K_col query-major, without atomics.
+//
+// A preparation kernel packs what the tile loop needs besides the code tiles
+// into arrays it can stream with the same direct loads: one 16-byte record
+// per query (LSE log2 e, delta hi, delta lo, isolated-channel query value)
+// and, per 64-query tile, the col-copy scales of Q and dO.
 #include <type_traits>
 
 #include "common.hpp"
@@ -36,39 +46,77 @@ namespace afp8 {
 
 template <int DQK, int DV>
 struct BwdCfg {
-  // waves per workgroup (eight only where their dK/dV accumulators leave
-  // room for two waves per SIMD) and LDS buffers, within 160 KB of LDS
+  // waves per workgroup (eight where the dK/dV accumulators of two waves fit
+  // one SIMD's registers)
   static constexpr int NWK = (DQK + DV <= 128) ? 8 : 4;
-  static constexpr int NBUF = (DQK + DV <= 320) ? 2 : 1;   // staging buffers
-  static constexpr int NT = 64 * NWK, BKB = 32 * NWK, BQ = 64;
-  static constexpr int QST = DQK + 16, OST = DV + 16, CST = BQ + 16, KCST = BKB + 16, DST = BQ + 16;
-  static constexpr int NDS = (DQK == 128 && DV == 128) || (DQK == 64) ? 2 : 1;  // dS buffers
-  static constexpr int QU = BQ * DQK / 16, OU = BQ * DV / 16;   // uint4 per row tile
-  static constexpr int QCU = DQK * BQ / 16, OCU = DV * BQ / 16; // uint4 per col tile
-  static constexpr int PQ = (QU + NT - 1) / NT, PO = (OU + NT - 1) / NT;
-  static constexpr int PQC = (QCU + NT - 1) / NT, POC = (OCU + NT - 1) / NT;
-  static constexpr int QSD = BQ * DQK / 128, OSD = BQ * DV / 128;  // row-copy scale dwords per tile
-  static_assert(QSD <= NT && OSD <= NT && DQK <= NT && DV <= NT && BQ <= NT, "one element per thread");
+  // CSPLIT waves share one 32-key block, each accumulating dK/dV for 1/CSPLIT
+  // of the channels (S, P, dP and dS are computed by each of them): at
+  // dqk + dv >= 320 the accumulators of a whole key block exceed a wave
+  static constexpr int CSPLIT = (DQK + DV >= 320) ? 2 : 1;
+  // stage buffers: two (loads of the next tile overlap the current one)
+  // except at d = 256, where one buffer and the K col slice fill the LDS
+  static constexpr int NBUF = (DQK + DV <= 320) ? 2 : 1;
+  static constexpr int NT = 64 * NWK, BKB = 32 * NWK / CSPLIT, BQ = 64;
+  static constexpr int DST = BQ + 16;   // row stride of the dS' tile [key][query]
+  static constexpr int al16(int x) { return (x + 15) & ~15; }
+  // one stage buffer: the query tile's operands, 16-byte aligned parts
+  static constexpr int Q_OFF = 0;                                   // Q row codes [BQ][DQK], swizzled
+  static constexpr int O_OFF = Q_OFF + BQ * DQK;                    // dO row codes [BQ][DV], swizzled
+  static constexpr int QC_OFF = O_OFF + BQ * DV;                    // Q col codes [DQK][BQ], swizzled
+  static constexpr int OC_OFF = QC_OFF + DQK * BQ;                  // dO col codes [DV][BQ], swizzled
+  static constexpr int QS_OFF = OC_OFF + DV * BQ;                   // Q row scales [BQ][DQK/32]
+  static constexpr int OS_OFF = al16(QS_OFF + BQ * DQK / 32);       // dO row scales [BQ][DV/32]
+  static constexpr int QCS_OFF = al16(OS_OFF + BQ * DV / 32);       // Q col scales [DQK][2]
+  static constexpr int OCS_OFF = QCS_OFF + DQK * 2;                 // dO col scales [DV][2]
+  static constexpr int CS_BYTES = 2 * (DQK + DV);                   // both, as packed per tile by bwd_prep
+  static constexpr int ROW_OFF = al16(OCS_OFF + DV * 2);            // per-query records [BQ] x 16 B
+  static constexpr int STAGE = ROW_OFF + BQ * 16;
 };
 
-// One query tile in flight from global memory: raw loaded words only.  Every
-// use of a loaded value waits for the load, so all decoding is left to
-// bwd_store, after the current tile has been computed.
-template <int DQK, int DV>
-struct BwdStage {
-  using C = BwdCfg<DQK, DV>;
-  uint4 q[C::PQ], o[C::PO], qc[C::PQC], oc[C::POC];
-  uint32_t qs, os;              // row-copy scale dwords
-  uint32_t qcs0, qcs1;          // col-copy scale bytes of one Q channel (query groups 0, 1)
-  uint32_t ocs0, ocs1;          // same for dO
-  float L, dhi, dlo;            // LSE and delta (hi, lo) of one query
-  uint32_t qhc, qhs;            // isolated-channel code and scale byte of one query
-};
+// XOR swizzle of the 16-byte chunks of a row-major tile with D-byte rows
+// (16 consecutive rows read at one logical chunk land on distinct banks).
+template <int D>
+__device__ __forceinline__ int swz_row(int r) {
+  if constexpr (D == 64) return (r >> 2) & 3;
+  else if constexpr (D == 128) return (r >> 1) & 7;
+  else if constexpr (D == 192) return (r >> 2) & 3;
+  else return r & 15;
+}
+// col tiles have 64-byte rows (one channel, 64 queries)
+__device__ __forceinline__ int swz_col(int c) { return (c >> 2) & 3; }
+
+// dQ operand units of one head before query block q (block q has q/2 + 1
+// units of 64 keys up to the diagonal): sum_{i<q} (floor(i/2) + 1).
+__host__ __device__ __forceinline__ int64_t tri_units(int64_t q) {
+  const int64_t m = q >> 1;
+  return (q & 1) ? (m + 1) * (m + 1) : m * (m + 1);
+}
+
+// LDS byte pointer; direct-to-LDS loads take their destination in this form
+// (pointers derived from the __shared__ arrays themselves, never from a
+// generic pointer)
+typedef __attribute__((address_space(3))) uint8_t lds8;
+
+__device__ __forceinline__ void dma16(const void* src, lds8* lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+__device__ __forceinline__ void dma4(const void* src, lds8* lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 4, 0, 0);
+}
+
+// Waits for this wave's LDS writes and direct-to-LDS loads (and any other
+// vector memory operation), then a workgroup barrier ordered for LDS only.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0)
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 
 // Per-(batch, query head) base pointers of the query-side operands.
 struct BwdHead {
-  const uint8_t *qrow, *qsc, *orow, *osc, *qcol, *qcsc, *ocol, *ocsc;
-  const float *lse, *delta;
+  const uint8_t *qrow, *qsc, *orow, *osc, *qcol, *ocol, *tcs;
+  const float4* rows;
 };
 
 template <int DQK, int DV>
@@ -79,153 +127,93 @@ __device__ __forceinline__ BwdHead bwd_head(const AttnArgs& a, size_t bh, int N)
   p.orow = a.do_code + bh * N * DV;
   p.osc = a.do_scale + bh * N * (DV / 32);
   p.qcol = a.qc_code + bh * DQK * N;
-  p.qcsc = a.qc_scale + bh * DQK * (N / 32);
   p.ocol = a.doc_code + bh * DV * N;
-  p.ocsc = a.doc_scale + bh * DV * (N / 32);
-  p.lse = a.lse + bh * N;
-  p.delta = a.delta + bh * N * 2;
+  p.tcs = a.tile_cs + bh * ((N + 63) / 64) * (2 * (DQK + DV));
+  p.rows = reinterpret_cast<const float4*>(a.rows) + bh * N;
   return p;
 }
 
-template <int DQK, int DV>
-__device__ __forceinline__ void bwd_load(BwdStage<DQK, DV>& st, const BwdHead& hp, int i0, int N, int hot) {
-  using C = BwdCfg<DQK, DV>;
-  const int tid = threadIdx.x;
-  // row tiles: contiguous; bytes past the sequence are read from its last
-  // valid 16 bytes (those queries are skipped)
-  const uint8_t* qrow = hp.qrow + i0 * DQK;
-  const uint8_t* orow = hp.orow + i0 * DV;
-  const uint32_t qlim = (N - i0) * DQK - 16, olim = (N - i0) * DV - 16;
-#pragma unroll
-  for (int i = 0; i < C::PQ; i++) {
-    const uint32_t u = tid + i * C::NT;
-    const uint32_t off = (u < C::QU ? u : 0) * 16;
-    st.q[i] = *reinterpret_cast<const uint4*>(qrow + (off < qlim ? off : qlim));
+// Row-major code tile [BQ][D] (rows i0.., clamped to the sequence) into LDS,
+// swizzled; wave w issues instructions w, w + NWK, ...
+template <int D, int NWK>
+__device__ __forceinline__ void dma_rows(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) {
+  constexpr int NI = 64 * D / 1024;
+  for (int k = w; k < NI; k += NWK) {
+    const int off = 1024 * k + 16 * lane;
+    const int r = off / D, p = (off % D) / 16;
+    const int row = i0 + r < N ? i0 + r : N - 1;
+    dma16(code + row * D + 16 * (p ^ swz_row<D>(r)), lds + 1024 * k);
   }
-#pragma unroll
-  for (int i = 0; i < C::PO; i++) {
-    const uint32_t u = tid + i * C::NT;
-    const uint32_t off = (u < C::OU ? u : 0) * 16;
-    st.o[i] = *reinterpret_cast<const uint4*>(orow + (off < olim ? off : olim));
+}
+// Col-copy code tile: channels [0, D), queries [i0, i0 + 64) (clamped) -> [D][64].
+template <int D, int NWK>
+__device__ __forceinline__ void dma_cols(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) {
+  constexpr int NI = D * 64 / 1024;
+  for (int k = w; k < NI; k += NWK) {
+    const int off = 1024 * k + 16 * lane;
+    const int c = off / 64, p = (off % 64) / 16;
+    const int q = p ^ swz_col(c);
+    const int col = i0 + 16 * q < N - 16 ? i0 + 16 * q : N - 16;
+    dma16(code + c * N + col, lds + 1024 * k);
   }
-  const int cl = N - 16 - i0;   // last valid 16-byte column piece, relative to i0
-#pragma unroll
-  for (int i = 0; i < C::PQC; i++) {
-    const uint32_t u = (tid + i * C::NT) < C::QCU ? tid + i * C::NT : 0, c = u >> 2, q = u & 3;
-    const int col = (int)q * 16 < cl ? (int)q * 16 : cl;
-    st.qc[i] = *reinterpret_cast<const uint4*>(hp.qcol + i0 + (c * N + col));
-  }
-#pragma unroll
-  for (int i = 0; i < C::POC; i++) {
-    const uint32_t u = (tid + i * C::NT) < C::OCU ? tid + i * C::NT : 0, c = u >> 2, q = u & 3;
-    const int col = (int)q * 16 < cl ? (int)q * 16 : cl;
-    st.oc[i] = *reinterpret_cast<const uint4*>(hp.ocol + i0 + (c * N + col));
-  }
-  if (tid < C::QSD) {
-    const uint32_t off = i0 * (DQK / 32) + tid * 4, lim = N * (DQK / 32) - 4;
-    st.qs = *reinterpret_cast<const uint32_t*>(hp.qsc + (off < lim ? off : lim));
-  }
-  if (tid < C::OSD) {
-    const uint32_t off = i0 * (DV / 32) + tid * 4, lim = N * (DV / 32) - 4;
-    st.os = *reinterpret_cast<const uint32_t*>(hp.osc + (off < lim ? off : lim));
-  }
-  const int g0 = i0 / 32, g1 = (i0 + 32 < N ? i0 + 32 : i0) / 32;
-  if (tid < DQK) {
-    st.qcs0 = hp.qcsc[tid * (N / 32) + g0];
-    st.qcs1 = hp.qcsc[tid * (N / 32) + g1];
-  }
-  if (tid < DV) {
-    st.ocs0 = hp.ocsc[tid * (N / 32) + g0];
-    st.ocs1 = hp.ocsc[tid * (N / 32) + g1];
-  }
-  if (tid < C::BQ) {
-    const int r = i0 + tid < N ? i0 + tid : N - 1;
-    st.L = hp.lse[r];
-    st.dhi = hp.delta[2 * r];
-    st.dlo = hp.delta[2 * r + 1];
-    if (hot >= 0) {
-      st.qhc = hp.qrow[r * DQK + hot];
-      st.qhs = hp.qsc[r * (DQK / 32) + hot / 32];
+}
+// Row-copy scales of 64 rows: 64 * D / 32 contiguous bytes (clamped).
+template <int D, int NWK>
+__device__ __forceinline__ void dma_row_scales(lds8* lds, const uint8_t* scale, int i0, int N, int w, int lane,
+                                               int first_wave) {
+  constexpr int BYTES = 64 * D / 32, NI = (BYTES + 255) / 256;
+  for (int k = 0; k < NI; k++) {
+    if ((first_wave + k) % NWK != w) continue;
+    const int off = 256 * k + 4 * lane;
+    if (off < BYTES) {
+      const int g = i0 * (D / 32) + off, lim = N * (D / 32) - 4;
+      dma4(scale + (g < lim ? g : lim), lds + 256 * k);
     }
   }
 }
 
+// Issues every load of one query tile, all direct-to-LDS: codes, row scales,
+// the col scales packed per tile by bwd_prep and the per-query records.
 template <int DQK, int DV>
-__device__ __forceinline__ void bwd_store(const BwdStage<DQK, DV>& st, uint8_t* sQ, uint8_t* sQs, uint8_t* sO,
-                                          uint8_t* sOs, uint8_t* sQc, uint8_t* sQcs, uint8_t* sOc, uint8_t* sOcs,
-                                          float* sRow, int hot) {
+__device__ __forceinline__ void stage_issue(lds8* st, const BwdHead& hp, int i0, int N) {
   using C = BwdCfg<DQK, DV>;
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int i = 0; i < C::PQ; i++) {
-    const int u = tid + i * C::NT;
-    if (C::QU % C::NT == 0 || u < C::QU) {
-      const int r = (u * 16) / DQK, c = (u * 16) % DQK;
-      uint4 v = st.q[i];
-      if (hot >= c && hot < c + 16) clear_byte(v, hot - c);
-      *reinterpret_cast<uint4*>(sQ + r * C::QST + c) = v;
-    }
+  constexpr int NWK = C::NWK;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  dma_rows<DQK, NWK>(st + C::Q_OFF, hp.qrow, i0, N, w, lane);
+  dma_rows<DV, NWK>(st + C::O_OFF, hp.orow, i0, N, w, lane);
+  dma_cols<DQK, NWK>(st + C::QC_OFF, hp.qcol, i0, N, w, lane);
+  dma_cols<DV, NWK>(st + C::OC_OFF, hp.ocol, i0, N, w, lane);
+  dma_row_scales<DQK, NWK>(st + C::QS_OFF, hp.qsc, i0, N, w, lane, 0);
+  dma_row_scales<DV, NWK>(st + C::OS_OFF, hp.osc, i0, N, w, lane, 1);
+  constexpr int NCI = (C::CS_BYTES + 255) / 256;
+  const uint8_t* tcs = hp.tcs + (i0 / 64) * C::CS_BYTES;
+  for (int k = 0; k < NCI; k++) {
+    if ((2 + k) % NWK != w) continue;
+    const int off = 256 * k + 4 * lane;
+    if (off < C::CS_BYTES) dma4(tcs + off, st + C::QCS_OFF + 256 * k);
   }
-#pragma unroll
-  for (int i = 0; i < C::PO; i++) {
-    const int u = tid + i * C::NT;
-    if (C::OU % C::NT == 0 || u < C::OU)
-      *reinterpret_cast<uint4*>(sO + ((u * 16) / DV) * C::OST + (u * 16) % DV) = st.o[i];
-  }
-  // col tiles, permuted within each 32-query group (stage_cols_perm); 32-bit
-  // stores keep the compiler from pairing the loaded registers early
-#pragma unroll
-  for (int i = 0; i < C::PQC; i++) {
-    const int u = tid + i * C::NT;
-    if (C::QCU % C::NT == 0 || u < C::QCU) {
-      const int c = u >> 2, q = u & 3;
-      uint32_t* base = reinterpret_cast<uint32_t*>(sQc + c * C::CST + (q >> 1) * 32 + (q & 1) * 8);
-      base[0] = st.qc[i].x;
-      base[1] = st.qc[i].z;
-      base[4] = st.qc[i].y;
-      base[5] = st.qc[i].w;
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < C::POC; i++) {
-    const int u = tid + i * C::NT;
-    if (C::OCU % C::NT == 0 || u < C::OCU) {
-      const int c = u >> 2, q = u & 3;
-      uint32_t* base = reinterpret_cast<uint32_t*>(sOc + c * C::CST + (q >> 1) * 32 + (q & 1) * 8);
-      base[0] = st.oc[i].x;
-      base[1] = st.oc[i].z;
-      base[4] = st.oc[i].y;
-      base[5] = st.oc[i].w;
-    }
-  }
-  if (tid < C::QSD) *reinterpret_cast<uint32_t*>(sQs + tid * 4) = st.qs;
-  if (tid < C::OSD) *reinterpret_cast<uint32_t*>(sOs + tid * 4) = st.os;
-  if (tid < DQK) *reinterpret_cast<uint16_t*>(sQcs + tid * 2) = (uint16_t)(st.qcs0 | (st.qcs1 << 8));
-  if (tid < DV) *reinterpret_cast<uint16_t*>(sOcs + tid * 2) = (uint16_t)(st.ocs0 | (st.ocs1 << 8));
-  if (tid < C::BQ) {
-    sRow[tid] = st.L * kLog2e;
-    sRow[C::BQ + tid] = st.dhi;
-    sRow[2 * C::BQ + tid] = st.dlo;
-    sRow[3 * C::BQ + tid] = hot >= 0 ? scaled_value(st.qhc, st.qhs) : 0.f;
+  if (w == (3 % NWK)) {
+    const int r = i0 + lane < N ? i0 + lane : N - 1;
+    dma16(hp.rows + r, st + C::ROW_OFF);
   }
 }
 
-// Columns [k0, k0 + W) of a col-copy code matrix [D, N] into LDS [D][W]
-// (natural order, row stride ST) and their scales into [D][W/32].
-template <int D, int W, int ST, int NT>
-__device__ __forceinline__ void stage_col_slice(uint8_t* lds, uint8_t* lds_scale, const uint8_t* code,
-                                                const uint8_t* scale, int k0, int N) {
-  constexpr int PER = W / 16;
-  for (int u = threadIdx.x; u < D * PER; u += NT) {
-    const int c = u / PER, q = u % PER;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (k0 + q * 16 < N) v = *reinterpret_cast<const uint4*>(code + (size_t)c * N + k0 + q * 16);
-    *reinterpret_cast<uint4*>(lds + c * ST + q * 16) = v;
-  }
-  for (int u = threadIdx.x; u < D * (W / 32); u += NT) {
-    const int c = u / (W / 32), g = u % (W / 32);
-    lds_scale[u] = (k0 + g * 32 < N) ? scale[(size_t)c * (N / 32) + k0 / 32 + g] : (uint8_t)0;
-  }
+// A/B fragment (row `row`, k-step t, half hf) of a swizzled row-major tile.
+template <int D>
+__device__ __forceinline__ v8i frag_rows_swz(const uint8_t* tile, int row, int t, int hf) {
+  const int s = swz_row<D>(row), c = 4 * t + hf;
+  const uint8_t* base = tile + row * D;
+  const uint4 lo = *reinterpret_cast<const uint4*>(base + 16 * (c ^ s));
+  const uint4 hi = *reinterpret_cast<const uint4*>(base + 16 * ((c + 2) ^ s));
+  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
+// B fragment of a swizzled col tile: channel ch, queries 16 hf.. and 32 + 16 hf..
+__device__ __forceinline__ v8i frag_cols_swz(const uint8_t* tile, int ch, int hf) {
+  const int s = swz_col(ch);
+  const uint8_t* base = tile + ch * 64;
+  const uint4 lo = *reinterpret_cast<const uint4*>(base + 16 * (hf ^ s));
+  const uint4 hi = *reinterpret_cast<const uint4*>(base + 16 * ((hf + 2) ^ s));
+  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
 }
 
 __device__ __forceinline__ double half_sum_d(double v) {
@@ -239,31 +227,41 @@ __device__ __forceinline__ float half_max(float v) {
   return v;
 }
 
+// Dwords 4 qs .. 4 qs + 3 of `x` from the lane's query order (queries
+// 8 g + 4 hf + e of the sub-block in dword g) to natural order (queries
+// 16 hf + 4 d + e in dword d): lane l < 32 receives {x_g, partner's x_g} for
+// g = 0, 1; lane l >= 32 {partner's x_g, x_g} for g = 2, 3.
+__device__ __forceinline__ void to_natural(const v8i& x, v8i& y, int qs) {
+  const auto r0 = __builtin_amdgcn_permlane32_swap((uint32_t)x[4 * qs], (uint32_t)x[4 * qs + 2], false, false);
+  const auto r1 = __builtin_amdgcn_permlane32_swap((uint32_t)x[4 * qs + 1], (uint32_t)x[4 * qs + 3], false, false);
+  y[4 * qs] = (int)r0[0];
+  y[4 * qs + 1] = (int)r0[1];
+  y[4 * qs + 2] = (int)r1[0];
+  y[4 * qs + 3] = (int)r1[1];
+}
+
 template <int DQK, int DV, bool STATS>
 __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnArgs a) {
   using C = BwdCfg<DQK, DV>;
   constexpr int NWK = C::NWK, BKB = C::BKB, BQ = C::BQ;
-  constexpr int KS = DQK / 64, VS = DV / 64, CK = DQK / 32, CV = DV / 32;
-  __shared__ __attribute__((aligned(16))) uint8_t sQ[C::NBUF][BQ * C::QST];
-  __shared__ __attribute__((aligned(16))) uint8_t sQs[C::NBUF][BQ * DQK / 32];
-  __shared__ __attribute__((aligned(16))) uint8_t sO[C::NBUF][BQ * C::OST];
-  __shared__ __attribute__((aligned(16))) uint8_t sOs[C::NBUF][BQ * DV / 32];
-  __shared__ __attribute__((aligned(16))) uint8_t sQc[C::NBUF][DQK * C::CST];
-  __shared__ __attribute__((aligned(16))) uint8_t sQcs[C::NBUF][DQK * 2];
-  __shared__ __attribute__((aligned(16))) uint8_t sOc[C::NBUF][DV * C::CST];
-  __shared__ __attribute__((aligned(16))) uint8_t sOcs[C::NBUF][DV * 2];
-  __shared__ __attribute__((aligned(16))) float sRow[C::NBUF][4 * BQ];
-  __shared__ __attribute__((aligned(16))) uint8_t sKc[DQK * C::KCST];
-  __shared__ __attribute__((aligned(16))) uint8_t sKcs[DQK * BKB / 32];
-  __shared__ __attribute__((aligned(16))) uint8_t sdS[C::NDS][BKB * C::DST];
-  __shared__ __attribute__((aligned(16))) uint8_t sdSs[C::NDS][NWK * 2];
+  constexpr int KS = DQK / 64, VS = DV / 64, CK = DQK / 32 / C::CSPLIT, CV = DV / 32 / C::CSPLIT;
+  // two stage buffers and two dS buffers as distinct objects, so the
+  // compiler can tell loads into one from reads of the other
+  __shared__ __attribute__((aligned(16))) uint8_t stA[C::STAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t stB[C::NBUF == 2 ? C::STAGE : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t dsA[BKB * C::DST];
+  __shared__ __attribute__((aligned(16))) uint8_t dsB[BKB * C::DST];
+  __shared__ __attribute__((aligned(16))) uint8_t esA[NWK * 2];
+  __shared__ __attribute__((aligned(16))) uint8_t esB[NWK * 2];
   __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
   const int N = (int)a.N;
   const int kb0 = blockIdx.x * BKB;             // key block (block 0 has the most work)
   const int kh = blockIdx.y, b = blockIdx.z;
-  const int kw0 = kb0 + 32 * w;                 // this wave's first key
+  const int wk = w / C::CSPLIT;                 // this wave's 32-key block within the workgroup
+  const int chh = w % C::CSPLIT;                // and its share of the dK/dV channels
+  const int kw0 = kb0 + 32 * wk;                // this wave's first key
   const bool live = kw0 < N;
   const int kj = kw0 + li;                      // this lane's key
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
@@ -292,9 +290,6 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
     }
     if (hot >= 0) khot = row_value<DQK>(a.k_code + bhk * N * DQK, a.k_scale + bhk * N * (DQK / 32), row, hot);
   }
-  // K col codes of the workgroup's keys (B operand of dQ), once
-  stage_col_slice<DQK, BKB, C::KCST, C::NT>(sKc, sKcs, a.kc_code + bhk * DQK * N,
-                                           a.kc_scale + bhk * DQK * (N / 32), kb0, N);
 
   v16f dk[CK], dv[CV];
 #pragma unroll
@@ -308,42 +303,71 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
 
   const int nqt = (N + BQ - 1) / BQ, qt0 = kb0 / BQ, nq = nqt - qt0;
   const int total = G * nq;
-  BwdStage<DQK, DV> st;
-  bwd_load<DQK, DV>(st, bwd_head<DQK, DV>(a, (size_t)b * Hq + kh * G, N), qt0 * BQ, N, hot);
-  bwd_store<DQK, DV>(st, sQ[0], sQs[0], sO[0], sOs[0], sQc[0], sQcs[0], sOc[0], sOcs[0], sRow[0], hot);
-  __syncthreads();
+  const size_t bh0 = (size_t)b * Hq + (size_t)kh * G;   // first query head of the group
 
-  // dQ atomics: lane part of the offset into the [B, N, Hq, Dqk] workspace
-  const uint32_t HqD = (uint32_t)Hq * DQK;
-  const uint32_t dq_lane = (uint32_t)(4 * hf) * HqD + li;
+  // first tile and the K col slice of the workgroup's keys (B operand of dQ)
+  stage_issue<DQK, DV>((lds8*)stA, bwd_head<DQK, DV>(a, bh0, N), qt0 * BQ, N);
+  lds_barrier();
 
-  for (int it = 0; it < total; it++) {
-    const int cur = C::NBUF == 2 ? (it & 1) : 0;   // staging buffer of this tile
-    const int dsb = C::NDS == 2 ? (it & 1) : 0;
-    const int h = kh * G + it / nq;
-    const int i0 = (qt0 + it % nq) * BQ;
-    {
-      // next tile (the last iteration reloads the first one into the idle
-      // buffer): loads are issued unconditionally so that no merge of old and
-      // new register values forces a wait right here
-      const int itn = it + 1 < total ? it + 1 : 0;
-      bwd_load<DQK, DV>(st, bwd_head<DQK, DV>(a, (size_t)b * Hq + kh * G + itn / nq, N),
-                        (qt0 + itn % nq) * BQ, N, hot);
+  const int64_t units_per_head = tri_units(N / 32);
+
+  // dQ operand units of tile t (its dS' codes and exponents in ds / es): unit
+  // (query block qs, key step ks) holds 32 queries x 64 keys; units wholly in
+  // the future of their queries do not exist
+  auto ds_store = [&](const int t, const uint8_t* ds, const uint8_t* es) __attribute__((always_inline)) {
+    constexpr int KSN = BKB / 64;
+    const int h = kh * G + t / nq;
+    const int i0 = (qt0 + t % nq) * BQ;
+    for (int m = w; m < 2 * KSN; m += NWK) {
+      const int qs = m / KSN, ks = m % KSN;
+      const int qb = i0 + 32 * qs;
+      if (qb >= N || kb0 + 64 * ks > qb + 31) continue;
+      const int i16 = lane & 15;
+      const int qbase = 32 * qs + 16 * ((lane >> 4) & 1);
+      // A: rows = queries of sub-block qs, k = keys 64 ks .. 64 ks + 63 (natural order)
+      v8i af;
+#pragma unroll
+      for (int part = 0; part < 4; part++) {
+        const int kk = 64 * ks + 32 * (part >> 1) + 16 * hf + 8 * (part & 1);
+        const uint8_t* addr = ds + (kk + (i16 >> 1)) * C::DST + qbase + 8 * (i16 & 1);
+        const v2i tv = __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i*)(addr));
+        af[2 * part] = tv[0];
+        af[2 * part + 1] = tv[1];
+      }
+      const int64_t unit = ((int64_t)b * Hq + h) * units_per_head + tri_units(qb / 32) + (kb0 + 64 * ks) / 64;
+      uint4* dst = reinterpret_cast<uint4*>(a.ds_units + unit * 2048 + 32 * lane);
+      dst[0] = make_uint4((uint32_t)af[0], (uint32_t)af[1], (uint32_t)af[2], (uint32_t)af[3]);
+      dst[1] = make_uint4((uint32_t)af[4], (uint32_t)af[5], (uint32_t)af[6], (uint32_t)af[7]);
+      if (lane == 0) {
+        const uint32_t e2 = (uint32_t)es[(2 * ks) * 2 + qs] | ((uint32_t)es[(2 * ks + 1) * 2 + qs] << 8);
+        *reinterpret_cast<uint16_t*>(a.ds_exp + unit * 2) = (uint16_t)e2;
+      }
+    }
+  };
+
+  // one tile: dQ units of the previous tile, loads of the next, compute of this one
+  auto body = [&](const int t, const uint8_t* cur, uint8_t* nxt, lds8* nxt3, uint8_t* ds, uint8_t* es,
+                  const uint8_t* ds_prev, const uint8_t* es_prev) __attribute__((always_inline)) {
+    if (t > 0) ds_store(t - 1, ds_prev, es_prev);
+    const bool more = t + 1 < total;
+    if constexpr (C::NBUF == 2) {
+      if (more) stage_issue<DQK, DV>(nxt3, bwd_head<DQK, DV>(a, bh0 + (t + 1) / nq, N), (qt0 + (t + 1) % nq) * BQ, N);
     }
 
-    const uint8_t* Q = sQ[cur];
-    const uint8_t* Qs = sQs[cur];
-    const uint8_t* O = sO[cur];
-    const uint8_t* Os = sOs[cur];
-    const float* Row = sRow[cur];
-    v8i pa, da;          // P' and dS' codes: A operands of dV and dK (k = the tile's 64 queries)
+    const int h = kh * G + t / nq;
+    const int i0 = (qt0 + t % nq) * BQ;
+    const uint8_t* Q = cur + C::Q_OFF;
+    const uint8_t* Qs = cur + C::QS_OFF;
+    const uint8_t* O = cur + C::O_OFF;
+    const uint8_t* Os = cur + C::OS_OFF;
+    const float4* Row = reinterpret_cast<const float4*>(cur + C::ROW_OFF);
+    v8i pa, da;          // P' and dS' codes, the lane's query order
     int dse[2] = {-127, -127};
-    bool any = false;
     // tiles wholly after the workgroup's keys and inside the sequence: no
     // mask, no skipped sub-block
     const bool full = i0 >= kb0 + BKB && i0 + BQ <= N;
 
-    auto subblock = [&](const int qs, auto edge_tag) {
+    auto subblock = [&](const int qs, auto edge_tag) __attribute__((always_inline)) {
       constexpr bool EDGE = decltype(edge_tag)::value;
       const int qb = i0 + 32 * qs;               // first query of the sub-block
       if (EDGE && (!live || qb < kw0 || qb >= N)) {
@@ -351,36 +375,29 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
         for (int k = 0; k < 4; k++) { pa[4 * qs + k] = 0; da[4 * qs + k] = 0; }
         return;
       }
-      any = true;
       v16f s, dp;
 #pragma unroll
       for (int r = 0; r < 16; r++) { s[r] = 0.f; dp[r] = 0.f; }
 #pragma unroll
-      for (int t = 0; t < KS; t++)
-        s = mfma_mx(frag_rows<C::QST>(Q, 32 * qs + li, t, hf), kf[t], s,
-                    Qs[(32 * qs + li) * (DQK / 32) + 2 * t + hf], ksc[t]);
+      for (int t2 = 0; t2 < KS; t2++)
+        s = mfma_mx(frag_rows_swz<DQK>(Q, 32 * qs + li, t2, hf), kf[t2], s,
+                    Qs[(32 * qs + li) * (DQK / 32) + 2 * t2 + hf], ksc[t2]);
 #pragma unroll
-      for (int t = 0; t < VS; t++)
-        dp = mfma_mx(frag_rows<C::OST>(O, 32 * qs + li, t, hf), vf[t], dp,
-                     Os[(32 * qs + li) * (DV / 32) + 2 * t + hf], vsc[t]);
+      for (int t2 = 0; t2 < VS; t2++)
+        dp = mfma_mx(frag_rows_swz<DV>(O, 32 * qs + li, t2, hf), vf[t2], dp,
+                     Os[(32 * qs + li) * (DV / 32) + 2 * t2 + hf], vsc[t2]);
       // lane holds queries qb + 8 g + 4 hf + e (accumulator r = 4 g + e)
       float amax = 0.f;
 #pragma unroll
       for (int g = 0; g < 4; g++) {
-        const int qo = 32 * qs + 8 * g + 4 * hf;
-        const float4 Lg = *reinterpret_cast<const float4*>(&Row[qo]);
-        const float4 Hg = *reinterpret_cast<const float4*>(&Row[BQ + qo]);
-        const float4 Og = *reinterpret_cast<const float4*>(&Row[2 * BQ + qo]);
-        const float4 Qg = *reinterpret_cast<const float4*>(&Row[3 * BQ + qo]);
-        const float Lv[4] = {Lg.x, Lg.y, Lg.z, Lg.w}, Hv[4] = {Hg.x, Hg.y, Hg.z, Hg.w};
-        const float Ov[4] = {Og.x, Og.y, Og.z, Og.w}, Qh[4] = {Qg.x, Qg.y, Qg.z, Qg.w};
 #pragma unroll
         for (int e = 0; e < 4; e++) {
           const int r = 4 * g + e;
-          float p = bwd_prob(__builtin_fmaf(Qh[e], khot, s[r]), c, Lv[e]);
+          const float4 rv = Row[32 * qs + 8 * g + 4 * hf + e];   // L log2 e, delta hi, delta lo, q_c*
+          float p = bwd_prob(__builtin_fmaf(rv.w, khot, s[r]), c, rv.x);
           if (EDGE && qb == kw0) p = (li > 8 * g + 4 * hf + e) ? 0.f : p;   // diagonal block: key > query
           s[r] = p;
-          dp[r] = p * ((dp[r] - Hv[e]) - Ov[e]);
+          dp[r] = p * ((dp[r] - rv.y) - rv.z);
           amax = fmaxf(amax, fabsf(dp[r]));
         }
       }
@@ -394,7 +411,7 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
       for (int k = 0; k < 4; k++)
         da[4 * qs + k] = (int)cvt4_div(dp[4 * k], dp[4 * k + 1], dp[4 * k + 2], dp[4 * k + 3], sc);
       dse[qs] = e;
-      if constexpr (STATS) {
+      if (STATS && chh == 0) {
         // per query row: FP64 sums over this wave's 32 keys, then atomics
 #pragma unroll
         for (int r = 0; r < 16; r++) {
@@ -422,79 +439,66 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
       subblock(0, std::true_type{});
       subblock(1, std::true_type{});
     }
-    if (any) {
-      // dV += P'^T dO_col ; dK += dS'^T Q_col   (k = the 64 queries of the tile)
+    // natural query order: lane hf holds queries 16 hf .. 16 hf + 15 of each
+    // sub-block (dwords of the A operands of dV and dK)
+    v8i pn, dn;
+#pragma unroll
+    for (int qs = 0; qs < 2; qs++) {
+      to_natural(pa, pn, qs);
+      to_natural(da, dn, qs);
+    }
+    // dV += P'^T dO_col ; dK += dS'^T Q_col   (k = the 64 queries of the tile;
+    // skipped sub-blocks have zero codes)
+    {
       const int dascale = (hf ? dse[1] : dse[0]) + 127;
-      const uint8_t* Oc = sOc[cur];
-      const uint8_t* Ocs = sOcs[cur];
-      const uint8_t* Qc = sQc[cur];
-      const uint8_t* Qcs = sQcs[cur];
+      const uint8_t* Oc = cur + C::OC_OFF;
+      const uint8_t* Ocs = cur + C::OCS_OFF;
+      const uint8_t* Qc = cur + C::QC_OFF;
+      const uint8_t* Qcs = cur + C::QCS_OFF;
 #pragma unroll
-      for (int i = 0; i < CV; i++)
-        dv[i] = mfma_mx(pa, frag_cols<C::CST>(Oc, 32 * i + li, hf), dv[i], 127 - 8, Ocs[(32 * i + li) * 2 + hf]);
-#pragma unroll
-      for (int i = 0; i < CK; i++)
-        dk[i] = mfma_mx(da, frag_cols<C::CST>(Qc, 32 * i + li, hf), dk[i], dascale, Qcs[(32 * i + li) * 2 + hf]);
-    }
-    // dS' codes to LDS: row = key (32 w + li), columns = the lane's queries
-    uint8_t* dS_l = sdS[dsb];
-#pragma unroll
-    for (int qs = 0; qs < 2; qs++)
-#pragma unroll
-      for (int g = 0; g < 4; g++)
-        *reinterpret_cast<int*>(dS_l + (32 * w + li) * C::DST + 32 * qs + 8 * g + 4 * hf) = da[4 * qs + g];
-    if (lane == 0) {
-      sdSs[dsb][w * 2] = (uint8_t)(dse[0] + 127);
-      sdSs[dsb][w * 2 + 1] = (uint8_t)(dse[1] + 127);
-    }
-    // the next tile into the other staging buffer (nobody reads it this tile)
-    if constexpr (C::NBUF == 2) {
-      const int nb = cur ^ 1;
-      bwd_store<DQK, DV>(st, sQ[nb], sQs[nb], sO[nb], sOs[nb], sQc[nb], sQcs[nb], sOc[nb], sOcs[nb], sRow[nb], hot);
-    }
-    __syncthreads();
-    // dQ tile (64 queries x DQK) = dS'(64 x BKB) K_col(BKB x DQK): output blocks
-    // m = qs * CK + i, distributed round-robin over the waves
-    for (int m = w; m < 2 * CK; m += NWK) {
-      const int qs = m / CK, i = m % CK;
-      const int qb = i0 + 32 * qs;
-      if (qb >= N) continue;
-      v16f acc;
-#pragma unroll
-      for (int r = 0; r < 16; r++) acc[r] = 0.f;
-      const int i16 = lane & 15;
-      const int qbase = 32 * qs + 16 * ((lane >> 4) & 1);
-#pragma unroll
-      for (int ks = 0; ks < BKB / 64; ks++) {
-        if (kb0 + 64 * ks > qb + 31) break;    // these keys are all in the future of the sub-block
-        // A: rows = queries of sub-block qs, k = keys 64 ks .. 64 ks + 63 (natural order)
-        v8i af;
-#pragma unroll
-        for (int part = 0; part < 4; part++) {
-          const int kk = 64 * ks + 32 * (part >> 1) + 16 * hf + 8 * (part & 1);
-          const uint8_t* addr = dS_l + (kk + (i16 >> 1)) * C::DST + qbase + 8 * (i16 & 1);
-          const v2i t = __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i*)(addr));
-          af[2 * part] = t[0];
-          af[2 * part + 1] = t[1];
-        }
-        acc = mfma_mx(af, frag_rows<C::KCST>(sKc, 32 * i + li, ks, hf), acc, sdSs[dsb][(2 * ks + hf) * 2 + qs],
-                      sKcs[(32 * i + li) * (BKB / 32) + 2 * ks + hf]);
+      for (int i = 0; i < CV; i++) {
+        const int ch = 32 * (chh * CV + i) + li;
+        dv[i] = mfma_mx(pn, frag_cols_swz(Oc, ch, hf), dv[i], 127 - 8, Ocs[ch * 2 + hf]);
       }
-      // lane holds channel 32 i + li, queries qb + 8 (r/4) + 4 hf + r % 4
-      float* dqb = a.dq_acc + (((size_t)b * N + qb) * Hq + h) * DQK + 32 * i;
 #pragma unroll
-      for (int r = 0; r < 16; r++)
-        atomicAdd(dqb + (uint32_t)(8 * (r >> 2) + (r & 3)) * HqD + dq_lane, acc[r]);
+      for (int i = 0; i < CK; i++) {
+        const int ch = 32 * (chh * CK + i) + li;
+        dk[i] = mfma_mx(dn, frag_cols_swz(Qc, ch, hf), dk[i], dascale, Qcs[ch * 2 + hf]);
+      }
     }
-    if constexpr (C::NDS == 1) __syncthreads();   // single dS buffer: reads done before the next writes
+    // dS' codes to LDS: row = key (32 wk + li), 16 queries per lane and sub-block
+    if (chh == 0) {
+#pragma unroll
+      for (int qs = 0; qs < 2; qs++)
+        *reinterpret_cast<uint4*>(ds + (32 * wk + li) * C::DST + 32 * qs + 16 * hf) =
+            make_uint4((uint32_t)dn[4 * qs], (uint32_t)dn[4 * qs + 1], (uint32_t)dn[4 * qs + 2], (uint32_t)dn[4 * qs + 3]);
+      if (lane == 0) {
+        es[wk * 2] = (uint8_t)(dse[0] + 127);
+        es[wk * 2 + 1] = (uint8_t)(dse[1] + 127);
+      }
+    }
+    lds_barrier();
     if constexpr (C::NBUF == 1) {
-      if (it + 1 < total) {
-        if constexpr (C::NDS == 2) __syncthreads();
-        bwd_store<DQK, DV>(st, sQ[0], sQs[0], sO[0], sOs[0], sQc[0], sQcs[0], sOc[0], sOcs[0], sRow[0], hot);
-        __syncthreads();
+      // one buffer: the next tile is loaded once every wave is done with it
+      if (more) {
+        stage_issue<DQK, DV>(nxt3, bwd_head<DQK, DV>(a, bh0 + (t + 1) / nq, N), (qt0 + (t + 1) % nq) * BQ, N);
+        lds_barrier();
       }
+    }
+  };
+
+  for (int t = 0; t < total; t += 2) {
+    if constexpr (C::NBUF == 2) {
+      body(t, stA, stB, (lds8*)stB, dsA, esA, dsB, esB);
+      if (t + 1 < total) body(t + 1, stB, stA, (lds8*)stA, dsB, esB, dsA, esA);
+    } else {
+      body(t, stA, stA, (lds8*)stA, dsA, esA, dsB, esB);
+      if (t + 1 < total) body(t + 1, stA, stA, (lds8*)stA, dsB, esB, dsA, esA);
     }
   }
+  if (total & 1) ds_store(total - 1, dsA, esA);
+  else ds_store(total - 1, dsB, esB);
+
   if (!live) return;
   // dK (times tau) and dV: lane holds channel 32 i + li, keys kw0 + 8 (r/4) + 4 hf + r % 4
 #pragma unroll
@@ -504,19 +508,166 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
       uint16_t* kd = reinterpret_cast<uint16_t*>(a.dk) + b * a.dks[0] + (int64_t)key * a.dks[1] + kh * a.dks[2];
       uint16_t* vd = reinterpret_cast<uint16_t*>(a.dv) + b * a.dvs[0] + (int64_t)key * a.dvs[1] + kh * a.dvs[2];
 #pragma unroll
-      for (int i = 0; i < CK; i++) kd[32 * i + li] = f32_to_bf16(dk[i][r] * a.tau);
+      for (int i = 0; i < CK; i++) kd[32 * (chh * CK + i) + li] = f32_to_bf16(dk[i][r] * a.tau);
 #pragma unroll
-      for (int i = 0; i < CV; i++) vd[32 * i + li] = f32_to_bf16(dv[i][r]);
+      for (int i = 0; i < CV; i++) vd[32 * (chh * CV + i) + li] = f32_to_bf16(dv[i][r]);
     } else {
       float* kd = reinterpret_cast<float*>(a.dk) + b * a.dks[0] + (int64_t)key * a.dks[1] + kh * a.dks[2];
       float* vd = reinterpret_cast<float*>(a.dv) + b * a.dvs[0] + (int64_t)key * a.dvs[1] + kh * a.dvs[2];
 #pragma unroll
-      for (int i = 0; i < CK; i++) kd[32 * i + li] = dk[i][r] * a.tau;
+      for (int i = 0; i < CK; i++) kd[32 * (chh * CK + i) + li] = dk[i][r] * a.tau;
 #pragma unroll
-      for (int i = 0; i < CV; i++) vd[32 * i + li] = dv[i][r];
+      for (int i = 0; i < CV; i++) vd[32 * (chh * CV + i) + li] = dv[i][r];
     }
   }
 }
+
+// Query-side data the tile loop streams besides the code tiles:
+//   rows    [B, Hq, N] x 16 B: {LSE log2 e, delta hi, delta lo, isolated-channel
+//           query value};
+//   tile_cs [B, Hq, ceil(N/64)] x 2 (Dqk + Dv) B: for each 64-query tile, the
+//           col-copy scales of Q then dO for the tile's two 32-query groups
+//           ([channel][group]), the second clamped to the first past the end;
+//   tile_kcs [B, Hkv, ceil(N/64)] x 2 Dqk B: the same for K (dq_kernel).
+template <int DQK, int DV>
+__global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
+  __shared__ int hot_slot;
+  const int N = (int)a.N;
+  const int h = blockIdx.y, b = blockIdx.z, kh = h / (int)a.G;
+  const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
+  const size_t bh = (size_t)b * a.Hq + h;
+  const int i0 = blockIdx.x * 64;
+  if (threadIdx.x < 64 && i0 + (int)threadIdx.x < N) {
+    const size_t row = bh * N + i0 + threadIdx.x;
+    const float2 d = *reinterpret_cast<const float2*>(a.delta + row * 2);
+    const float qh = hot >= 0 ? row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot) : 0.f;
+    reinterpret_cast<float4*>(a.rows)[row] = make_float4(a.lse[row] * kLog2e, d.x, d.y, qh);
+  }
+  const int g0 = i0 / 32, g1 = (i0 + 32 < N ? i0 + 32 : i0) / 32;
+  uint8_t* dst = a.tile_cs + (bh * ((N + 63) / 64) + blockIdx.x) * (2 * (DQK + DV));
+  for (int u = threadIdx.x; u < DQK + DV; u += 256) {
+    const uint8_t* src = u < DQK ? a.qc_scale + (bh * DQK + u) * (N / 32)
+                                 : a.doc_scale + (bh * DV + (u - DQK)) * (N / 32);
+    dst[2 * u] = src[g0];
+    dst[2 * u + 1] = src[g1];
+  }
+  // the K col scales of the same 64 keys, once per KV head (for dq_kernel)
+  if (h < a.Hkv) {
+    const size_t bk = (size_t)b * a.Hkv + h;
+    uint8_t* dk = a.tile_kcs + (bk * ((N + 63) / 64) + blockIdx.x) * (2 * DQK);
+    for (int u = threadIdx.x; u < DQK; u += 256) {
+      const uint8_t* src = a.kc_scale + (bk * DQK + u) * (N / 32);
+      dk[2 * u] = src[g0];
+      dk[2 * u + 1] = src[g1];
+    }
+  }
+}
+
+// dQ = tau dS' K_col, query-major: a workgroup of 8 waves owns 256 queries
+// of one (batch, query head), wave w one 32-query block and all Dqk channels.
+// Per 64-key step up to the diagonal: the A operand is the stored unit (32
+// bytes per lane, already in operand order, prefetched into registers one
+// step ahead); the K col tile of the step [Dqk][64] and its scales reach LDS
+// by direct loads, double-buffered and shared by the 8 waves.  Keys past the
+// sequence meet zero dS' codes (their K loads are clamped into the array).
+template <int DQK>
+__global__ __launch_bounds__(512) void dq_kernel(AttnArgs a) {
+  constexpr int CQ = DQK / 32, NW = 8;
+  constexpr int KT = DQK * 64, KSB = 2 * DQK;       // K tile and scale bytes per step
+  __shared__ __attribute__((aligned(16))) uint8_t kA[KT + KSB];
+  __shared__ __attribute__((aligned(16))) uint8_t kB[KT + KSB];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
+  const int N = (int)a.N, nqb = N / 32;
+  const int ntile = (nqb + NW - 1) / NW;
+  const int tile = ntile - 1 - (int)blockIdx.x;      // longest rows first
+  const int h = blockIdx.y, b = blockIdx.z, kh = h / (int)a.G;
+  const int qb = NW * tile + w;                      // this wave's 32-query block
+  const int qlast = NW * tile + NW - 1 < nqb - 1 ? NW * tile + NW - 1 : nqb - 1;
+  const int nk = qb < nqb ? qb / 2 + 1 : 0;          // this wave's 64-key steps
+  const int nkw = qlast / 2 + 1;                     // the workgroup's
+  const int64_t bh = (int64_t)b * a.Hq + h;
+  const int64_t unit0 = bh * tri_units(nqb) + tri_units(qb < nqb ? qb : 0);
+  const uint8_t* units = a.ds_units + unit0 * 2048 + 32 * lane;
+  const uint8_t* ex = a.ds_exp + unit0 * 2;
+  const int64_t bk = (int64_t)b * a.Hkv + kh;
+  const uint8_t* kc = a.kc_code + bk * DQK * N;
+  const uint8_t* tk = a.tile_kcs + bk * ((N + 63) / 64) * KSB;
+
+  auto issue = [&](lds8* dst, int ks) __attribute__((always_inline)) {
+    dma_cols<DQK, NW>(dst, kc, 64 * ks, N, w, lane);
+    constexpr int NI = (KSB + 255) / 256;
+    for (int k = 0; k < NI; k++) {
+      if ((NW - 1 - k) != w) continue;
+      const int off = 256 * k + 4 * lane;
+      if (off < KSB) dma4(tk + ks * KSB + off, dst + KT + 256 * k);
+    }
+  };
+  struct Aop { uint4 lo, hi; uint32_t e; };
+  auto load_a = [&](Aop& op, int ks) __attribute__((always_inline)) {
+    ks = ks < nk ? ks : (nk > 0 ? nk - 1 : 0);     // past the wave's last step: reload it (unused)
+    op.lo = *reinterpret_cast<const uint4*>(units + ks * 2048);
+    op.hi = *reinterpret_cast<const uint4*>(units + ks * 2048 + 16);
+    op.e = ex[2 * ks + hf];
+  };
+  v16f acc[CQ];
+#pragma unroll
+  for (int i = 0; i < CQ; i++)
+#pragma unroll
+    for (int r = 0; r < 16; r++) acc[i][r] = 0.f;
+  auto compute = [&](const uint8_t* kt, const Aop& op) __attribute__((always_inline)) {
+    const v8i af = v8i{(int)op.lo.x, (int)op.lo.y, (int)op.lo.z, (int)op.lo.w,
+                       (int)op.hi.x, (int)op.hi.y, (int)op.hi.z, (int)op.hi.w};
+#pragma unroll
+    for (int i = 0; i < CQ; i++) {
+      const int ch = 32 * i + li;
+      acc[i] = mfma_mx(af, frag_cols_swz(kt, ch, hf), acc[i], (int)op.e, kt[KT + 2 * ch + hf]);
+    }
+  };
+  Aop a0, a1;
+  if (qb < nqb) load_a(a0, 0);
+  issue((lds8*)kA, 0);
+  lds_barrier();
+  for (int ks = 0; ks < nkw; ks += 2) {
+    if (ks + 1 < nkw) issue((lds8*)kB, ks + 1);
+    if (qb < nqb) load_a(a1, ks + 1);
+    if (ks < nk) compute(kA, a0);
+    lds_barrier();
+    if (ks + 1 >= nkw) break;
+    if (ks + 2 < nkw) issue((lds8*)kA, ks + 2);
+    if (qb < nqb) load_a(a0, ks + 2);
+    if (ks + 1 < nk) compute(kB, a1);
+    lds_barrier();
+  }
+  if (qb >= nqb) return;
+  // lane holds channel 32 i + li, queries 32 qb + 8 (r/4) + 4 hf + r % 4
+#pragma unroll
+  for (int r = 0; r < 16; r++) {
+    const int q = 32 * qb + 8 * (r >> 2) + 4 * hf + (r & 3);
+    if (a.grad_bf16) {
+      uint16_t* d = reinterpret_cast<uint16_t*>(a.dq) + b * a.dqs[0] + (int64_t)q * a.dqs[1] + h * a.dqs[2];
+#pragma unroll
+      for (int i = 0; i < CQ; i++) d[32 * i + li] = f32_to_bf16(acc[i][r] * a.tau);
+    } else {
+      float* d = reinterpret_cast<float*>(a.dq) + b * a.dqs[0] + (int64_t)q * a.dqs[1] + h * a.dqs[2];
+#pragma unroll
+      for (int i = 0; i < CQ; i++) d[32 * i + li] = acc[i][r] * a.tau;
+    }
+  }
+}
+
+hipError_t launch_dq(const AttnArgs& a, int dqk, hipStream_t s) {
+  const dim3 grid((unsigned)((a.N / 32 + 7) / 8), (unsigned)a.Hq, (unsigned)a.B);
+  switch (dqk) {
+    case 64: hipLaunchKernelGGL((dq_kernel<64>), grid, dim3(512), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((dq_kernel<128>), grid, dim3(512), 0, s, a); break;
+    case 192: hipLaunchKernelGGL((dq_kernel<192>), grid, dim3(512), 0, s, a); break;
+    case 256: hipLaunchKernelGGL((dq_kernel<256>), grid, dim3(512), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+int64_t dq_units_per_head(int64_t N) { return tri_units(N / 32); }
 
 template <int DQK, int DV>
 static hipError_t bwd_dispatch(const AttnArgs& a, hipStream_t s) {
@@ -525,6 +676,16 @@ static hipError_t bwd_dispatch(const AttnArgs& a, hipStream_t s) {
   dim3 grid((unsigned)nkb, (unsigned)a.Hkv, (unsigned)a.B);
   if (a.rowstats) hipLaunchKernelGGL((bwd_kernel<DQK, DV, true>), grid, dim3(C::NT), 0, s, a);
   else hipLaunchKernelGGL((bwd_kernel<DQK, DV, false>), grid, dim3(C::NT), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_prep(const AttnArgs& a, int dqk, int dv, hipStream_t s) {
+  const dim3 grid((unsigned)((a.N + 63) / 64), (unsigned)a.Hq, (unsigned)a.B);
+  if (dqk == 64 && dv == 64) hipLaunchKernelGGL((bwd_prep_kernel<64, 64>), grid, dim3(256), 0, s, a);
+  else if (dqk == 128 && dv == 128) hipLaunchKernelGGL((bwd_prep_kernel<128, 128>), grid, dim3(256), 0, s, a);
+  else if (dqk == 256 && dv == 256) hipLaunchKernelGGL((bwd_prep_kernel<256, 256>), grid, dim3(256), 0, s, a);
+  else if (dqk == 192 && dv == 128) hipLaunchKernelGGL((bwd_prep_kernel<192, 128>), grid, dim3(256), 0, s, a);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -28,14 +28,6 @@ struct StaleArgs {
   int Dv;
 };
 
-struct DqFinalArgs {
-  const float* acc;          // [B, N, Hq, D] FP32
-  void* dq;
-  int64_t s[3];
-  int64_t B, N, Hq, D;
-  float tau;
-};
-
 // Shared by the forward, the matched-correction pass and the backward.
 struct AttnArgs {
   int64_t B, N, Hq, Hkv, G;  // G = Hq / Hkv
@@ -55,8 +47,13 @@ struct AttnArgs {
   float* lse_out;
   const float* delta;                  // [B,Hq,N,2]
   float* delta_out;
+  float* rows;                         // [B,Hq,N,4] backward per-query records (workspace)
+  uint8_t* tile_cs;                    // [B,Hq,ceil(N/64),2(Dqk+Dv)] backward per-tile col scales (workspace)
+  uint8_t* tile_kcs;                   // [B,Hkv,ceil(N/64),2 Dqk] K col scales per 64-key step (workspace)
   void* o;  int64_t os[3]; int o_bf16;
-  float* dq_acc;                       // [B,N,Hq,Dqk] FP32
+  uint8_t* ds_units;                   // dQ operand units (workspace): 2048 B per (head, query block, 64 keys)
+  uint8_t* ds_exp;                     // their block exponents, 2 B per unit
+  void* dq; int64_t dqs[3];
   void* dk; int64_t dks[3];
   void* dv; int64_t dvs[3];
   int grad_bf16;
@@ -66,9 +63,11 @@ struct AttnArgs {
 hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_t s);
 hipError_t launch_stale_rowsum(const StaleArgs& a, int dout_bf16, int o_bf16, hipStream_t s);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
-hipError_t launch_dq_finalize(const DqFinalArgs& a, int grad_bf16, hipStream_t s);
 hipError_t launch_fwd(const AttnArgs& a, int dqk, int dv, hipStream_t s);
 hipError_t launch_delta_matching(const AttnArgs& a, int dqk, int dv, hipStream_t s);
+hipError_t launch_bwd_prep(const AttnArgs& a, int dqk, int dv, hipStream_t s);
 hipError_t launch_bwd(const AttnArgs& a, int dqk, int dv, hipStream_t s);
+hipError_t launch_dq(const AttnArgs& a, int dqk, hipStream_t s);
+int64_t dq_units_per_head(int64_t N);   // stored dQ operand units of one head
 
 }  // namespace afp8

@@ -163,8 +163,8 @@ hipError_t launch_stale_rowsum(const StaleArgs& a, int dout_bf16, int o_bf16, hi
 }
 
 // ---------------------------------------------------------------------------
-// Workspace clear (a fill kernel rather than a memset node, so callers may
-// capture the backward in a graph) and the final dQ = tau * dQ_acc store.
+// Buffer clear (a fill kernel rather than a memset node, so callers may
+// capture the calls in a graph).
 __global__ __launch_bounds__(256) void fill_zero_kernel(float4* p, int64_t n4) {
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256)
     p[i] = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -176,35 +176,6 @@ hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s) {
   int64_t blocks = (n4 + 255) / 256;
   if (blocks > 8192) blocks = 8192;
   hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, s, reinterpret_cast<float4*>(p), n4);
-  return hipGetLastError();
-}
-
-template <typename TG>
-__global__ __launch_bounds__(256) void dq_finalize_kernel(DqFinalArgs a) {
-  // one thread per 4 channels of one (b, n, h) row
-  const int64_t per_row = a.D / 4;
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= a.B * a.N * a.Hq * per_row) return;
-  const int64_t c4 = idx % per_row, row = idx / per_row;
-  const int64_t h = row % a.Hq, n = (row / a.Hq) % a.N, b = row / (a.Hq * a.N);
-  const float4 v = reinterpret_cast<const float4*>(a.acc)[idx];
-  TG* dst = reinterpret_cast<TG*>(a.dq) + b * a.s[0] + n * a.s[1] + h * a.s[2] + c4 * 4;
-  if constexpr (sizeof(TG) == 2) {
-    uint2 o;
-    o.x = (uint32_t)f32_to_bf16(v.x * a.tau) | ((uint32_t)f32_to_bf16(v.y * a.tau) << 16);
-    o.y = (uint32_t)f32_to_bf16(v.z * a.tau) | ((uint32_t)f32_to_bf16(v.w * a.tau) << 16);
-    *reinterpret_cast<uint2*>(dst) = o;
-  } else {
-    *reinterpret_cast<float4*>(dst) = make_float4(v.x * a.tau, v.y * a.tau, v.z * a.tau, v.w * a.tau);
-  }
-}
-
-hipError_t launch_dq_finalize(const DqFinalArgs& a, int grad_bf16, hipStream_t s) {
-  const int64_t n = a.B * a.N * a.Hq * (a.D / 4);
-  if (n == 0) return hipSuccess;
-  dim3 grid((unsigned)((n + 255) / 256));
-  if (grad_bf16) hipLaunchKernelGGL(dq_finalize_kernel<uint16_t>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(dq_finalize_kernel<float>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

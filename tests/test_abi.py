@@ -76,7 +76,10 @@ def test_null_alignment_and_workspace_errors():
     # workspace too small / misaligned
     n = ctypes.c_size_t(0)
     assert L.attn_fp8_bwd_workspace_size(ctypes.byref(p), ctypes.byref(n)) == 0
-    assert n.value == 128 * 2 * 128 * 4 + 2 * 128 * 2 * 4
+    # stored dQ operand units (2 KB) and exponents (2 B, padded to 256) for 4 query blocks per head
+    # (1 + 1 + 2 + 2 units), delta, per-query records, per-tile Q/dO col scales, per-tile K col scales
+    assert n.value == (2 * 6 * 2048 + 256 + 2 * 128 * 2 * 4 + 2 * 128 * 4 * 4 + 2 * 2 * 2 * (128 + 128)
+                       + 256 * ((p.heads_kv * 2 * 2 * 128 + 255) // 256))
     args = [ctypes.byref(p), 0] + [ctypes.byref(m)] * 4 + [ctypes.c_void_p(4096), None, 1, None, None, 1, None,
                                                            None] + [ctypes.c_void_p(4096)] * 3 + [1, st, st, st]
     assert L.attn_fp8_bwd(*args, ctypes.c_void_p(4096), ctypes.c_size_t(n.value - 1), None, None, None) == -4
