@@ -46,17 +46,15 @@ namespace afp8 {
 
 template <int DQK, int DV>
 struct BwdCfg {
-  // waves per workgroup (eight where the dK/dV accumulators of two waves fit
-  // one SIMD's registers)
-  static constexpr int NWK = (DQK + DV <= 128) ? 8 : 4;
-  // CSPLIT waves share one 32-key block, each accumulating dK/dV for 1/CSPLIT
-  // of the channels (S, P, dP and dS are computed by each of them): at
-  // dqk + dv >= 320 the accumulators of a whole key block exceed a wave
-  static constexpr int CSPLIT = (DQK + DV >= 320) ? 2 : 1;
+  // 8 waves: 4 blocks of 32 keys x 2 query sub-blocks.  The two waves of a
+  // key block (w and w + 4, on one SIMD) each compute S, dP, P and dS for one
+  // 32-query half of the tile; after exchanging codes through LDS the first
+  // accumulates dV and the second dK for all channels of their keys.
+  static constexpr int NWK = 8, KBW = 4;
   // stage buffers: two (loads of the next tile overlap the current one)
-  // except at d = 256, where one buffer and the K col slice fill the LDS
+  // except at d = 256, where one buffer fills the LDS
   static constexpr int NBUF = (DQK + DV <= 320) ? 2 : 1;
-  static constexpr int NT = 64 * NWK, BKB = 32 * NWK / CSPLIT, BQ = 64;
+  static constexpr int NT = 64 * NWK, BKB = 32 * KBW, BQ = 64;
   static constexpr int DST = BQ + 16;   // row stride of the dS' tile [key][query]
   static constexpr int al16(int x) { return (x + 15) & ~15; }
   // one stage buffer: the query tile's operands, 16-byte aligned parts
@@ -111,6 +109,17 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Workgroup barrier after this wave's LDS writes only: direct-to-LDS loads
+// in flight stay in flight (an LDS release fence would wait for them, since
+// they write LDS), so the ordering of the surrounding LDS accesses is kept
+// by compiler barriers instead.
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 // Per-(batch, query head) base pointers of the query-side operands.
@@ -227,41 +236,44 @@ __device__ __forceinline__ float half_max(float v) {
   return v;
 }
 
-// Dwords 4 qs .. 4 qs + 3 of `x` from the lane's query order (queries
-// 8 g + 4 hf + e of the sub-block in dword g) to natural order (queries
-// 16 hf + 4 d + e in dword d): lane l < 32 receives {x_g, partner's x_g} for
-// g = 0, 1; lane l >= 32 {partner's x_g, x_g} for g = 2, 3.
-__device__ __forceinline__ void to_natural(const v8i& x, v8i& y, int qs) {
-  const auto r0 = __builtin_amdgcn_permlane32_swap((uint32_t)x[4 * qs], (uint32_t)x[4 * qs + 2], false, false);
-  const auto r1 = __builtin_amdgcn_permlane32_swap((uint32_t)x[4 * qs + 1], (uint32_t)x[4 * qs + 3], false, false);
-  y[4 * qs] = (int)r0[0];
-  y[4 * qs + 1] = (int)r0[1];
-  y[4 * qs + 2] = (int)r1[0];
-  y[4 * qs + 3] = (int)r1[1];
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// The four code dwords of one 32-query half from the lane's query order
+// (queries 8 g + 4 hf + e in dword g) to natural order (queries 16 hf + 4 d + e
+// in dword d): lane l < 32 receives {x_g, partner's x_g} for g = 0, 1; lane
+// l >= 32 {partner's x_g, x_g} for g = 2, 3.
+__device__ __forceinline__ v4i to_natural4(const v4i& x) {
+  const auto r0 = __builtin_amdgcn_permlane32_swap((uint32_t)x[0], (uint32_t)x[2], false, false);
+  const auto r1 = __builtin_amdgcn_permlane32_swap((uint32_t)x[1], (uint32_t)x[3], false, false);
+  return v4i{(int)r0[0], (int)r0[1], (int)r1[0], (int)r1[1]};
 }
 
 template <int DQK, int DV, bool STATS>
-__global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnArgs a) {
+__global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   using C = BwdCfg<DQK, DV>;
-  constexpr int NWK = C::NWK, BKB = C::BKB, BQ = C::BQ;
-  constexpr int KS = DQK / 64, VS = DV / 64, CK = DQK / 32 / C::CSPLIT, CV = DV / 32 / C::CSPLIT;
+  constexpr int KBW = C::KBW, BKB = C::BKB, BQ = C::BQ;
+  constexpr int KS = DQK / 64, VS = DV / 64, CK = DQK / 32, CV = DV / 32;
+  constexpr int CMAX = CK > CV ? CK : CV;
   // two stage buffers and two dS buffers as distinct objects, so the
   // compiler can tell loads into one from reads of the other
   __shared__ __attribute__((aligned(16))) uint8_t stA[C::STAGE];
   __shared__ __attribute__((aligned(16))) uint8_t stB[C::NBUF == 2 ? C::STAGE : 16];
   __shared__ __attribute__((aligned(16))) uint8_t dsA[BKB * C::DST];
   __shared__ __attribute__((aligned(16))) uint8_t dsB[BKB * C::DST];
-  __shared__ __attribute__((aligned(16))) uint8_t esA[NWK * 2];
-  __shared__ __attribute__((aligned(16))) uint8_t esB[NWK * 2];
+  __shared__ __attribute__((aligned(16))) uint8_t esA[KBW * 2];
+  __shared__ __attribute__((aligned(16))) uint8_t esB[KBW * 2];
+  // code exchange within a key block, 16 bytes per lane in natural query
+  // order: [0] dS' of the first half (for dK), [1] P' of the second (for dV)
+  __shared__ __attribute__((aligned(16))) uint4 xch[2][KBW * 64];
   __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
+  const int kbw = w % KBW;                      // this wave's 32-key block within the workgroup
+  const int qs = w / KBW;                       // and its 32-query half of every tile
   const int N = (int)a.N;
   const int kb0 = blockIdx.x * BKB;             // key block (block 0 has the most work)
   const int kh = blockIdx.y, b = blockIdx.z;
-  const int wk = w / C::CSPLIT;                 // this wave's 32-key block within the workgroup
-  const int chh = w % C::CSPLIT;                // and its share of the dK/dV channels
-  const int kw0 = kb0 + 32 * wk;                // this wave's first key
+  const int kw0 = kb0 + 32 * kbw;               // this wave's first key
   const bool live = kw0 < N;
   const int kj = kw0 + li;                      // this lane's key
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
@@ -291,63 +303,58 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
     if (hot >= 0) khot = row_value<DQK>(a.k_code + bhk * N * DQK, a.k_scale + bhk * N * (DQK / 32), row, hot);
   }
 
-  v16f dk[CK], dv[CV];
+  // dV (first half, CV blocks) or dK (second half, CK blocks) of the wave's keys
+  v16f acc[CMAX];
 #pragma unroll
-  for (int i = 0; i < CK; i++)
+  for (int i = 0; i < CMAX; i++)
 #pragma unroll
-    for (int r = 0; r < 16; r++) dk[i][r] = 0.f;
-#pragma unroll
-  for (int i = 0; i < CV; i++)
-#pragma unroll
-    for (int r = 0; r < 16; r++) dv[i][r] = 0.f;
+    for (int r = 0; r < 16; r++) acc[i][r] = 0.f;
 
   const int nqt = (N + BQ - 1) / BQ, qt0 = kb0 / BQ, nq = nqt - qt0;
   const int total = G * nq;
   const size_t bh0 = (size_t)b * Hq + (size_t)kh * G;   // first query head of the group
 
-  // first tile and the K col slice of the workgroup's keys (B operand of dQ)
   stage_issue<DQK, DV>((lds8*)stA, bwd_head<DQK, DV>(a, bh0, N), qt0 * BQ, N);
   lds_barrier();
 
   const int64_t units_per_head = tri_units(N / 32);
 
   // dQ operand units of tile t (its dS' codes and exponents in ds / es): unit
-  // (query block qs, key step ks) holds 32 queries x 64 keys; units wholly in
+  // (query half uq, key step ks) holds 32 queries x 64 keys; units wholly in
   // the future of their queries do not exist
   auto ds_store = [&](const int t, const uint8_t* ds, const uint8_t* es) __attribute__((always_inline)) {
     constexpr int KSN = BKB / 64;
     const int h = kh * G + t / nq;
     const int i0 = (qt0 + t % nq) * BQ;
-    for (int m = w; m < 2 * KSN; m += NWK) {
-      const int qs = m / KSN, ks = m % KSN;
-      const int qb = i0 + 32 * qs;
-      if (qb >= N || kb0 + 64 * ks > qb + 31) continue;
-      const int i16 = lane & 15;
-      const int qbase = 32 * qs + 16 * ((lane >> 4) & 1);
-      // A: rows = queries of sub-block qs, k = keys 64 ks .. 64 ks + 63 (natural order)
-      v8i af;
+    if (w >= 2 * KSN) return;
+    const int uq = w / KSN, ks = w % KSN;
+    const int qb = i0 + 32 * uq;
+    if (qb >= N || kb0 + 64 * ks > qb + 31) return;
+    const int i16 = lane & 15;
+    const int qbase = 32 * uq + 16 * ((lane >> 4) & 1);
+    // A: rows = queries of half uq, k = keys 64 ks .. 64 ks + 63 (natural order)
+    v8i af;
 #pragma unroll
-      for (int part = 0; part < 4; part++) {
-        const int kk = 64 * ks + 32 * (part >> 1) + 16 * hf + 8 * (part & 1);
-        const uint8_t* addr = ds + (kk + (i16 >> 1)) * C::DST + qbase + 8 * (i16 & 1);
-        const v2i tv = __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i*)(addr));
-        af[2 * part] = tv[0];
-        af[2 * part + 1] = tv[1];
-      }
-      const int64_t unit = ((int64_t)b * Hq + h) * units_per_head + tri_units(qb / 32) + (kb0 + 64 * ks) / 64;
-      uint4* dst = reinterpret_cast<uint4*>(a.ds_units + unit * 2048 + 32 * lane);
-      dst[0] = make_uint4((uint32_t)af[0], (uint32_t)af[1], (uint32_t)af[2], (uint32_t)af[3]);
-      dst[1] = make_uint4((uint32_t)af[4], (uint32_t)af[5], (uint32_t)af[6], (uint32_t)af[7]);
-      if (lane == 0) {
-        const uint32_t e2 = (uint32_t)es[(2 * ks) * 2 + qs] | ((uint32_t)es[(2 * ks + 1) * 2 + qs] << 8);
-        *reinterpret_cast<uint16_t*>(a.ds_exp + unit * 2) = (uint16_t)e2;
-      }
+    for (int part = 0; part < 4; part++) {
+      const int kk = 64 * ks + 32 * (part >> 1) + 16 * hf + 8 * (part & 1);
+      const uint8_t* addr = ds + (kk + (i16 >> 1)) * C::DST + qbase + 8 * (i16 & 1);
+      const v2i tv = __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i*)(addr));
+      af[2 * part] = tv[0];
+      af[2 * part + 1] = tv[1];
+    }
+    const int64_t unit = ((int64_t)b * Hq + h) * units_per_head + tri_units(qb / 32) + (kb0 + 64 * ks) / 64;
+    uint4* dst = reinterpret_cast<uint4*>(a.ds_units + unit * 2048 + 32 * lane);
+    dst[0] = make_uint4((uint32_t)af[0], (uint32_t)af[1], (uint32_t)af[2], (uint32_t)af[3]);
+    dst[1] = make_uint4((uint32_t)af[4], (uint32_t)af[5], (uint32_t)af[6], (uint32_t)af[7]);
+    if (lane == 0) {
+      const uint32_t e2 = (uint32_t)es[(2 * ks) * 2 + uq] | ((uint32_t)es[(2 * ks + 1) * 2 + uq] << 8);
+      *reinterpret_cast<uint16_t*>(a.ds_exp + unit * 2) = (uint16_t)e2;
     }
   };
 
   // one tile: dQ units of the previous tile, loads of the next, compute of this one
-  auto body = [&](const int t, const uint8_t* cur, uint8_t* nxt, lds8* nxt3, uint8_t* ds, uint8_t* es,
-                  const uint8_t* ds_prev, const uint8_t* es_prev) __attribute__((always_inline)) {
+  auto body = [&](const int t, const uint8_t* cur, lds8* nxt3, uint8_t* ds, uint8_t* es, const uint8_t* ds_prev,
+                  const uint8_t* es_prev) __attribute__((always_inline)) {
     if (t > 0) ds_store(t - 1, ds_prev, es_prev);
     const bool more = t + 1 < total;
     if constexpr (C::NBUF == 2) {
@@ -356,23 +363,23 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
 
     const int h = kh * G + t / nq;
     const int i0 = (qt0 + t % nq) * BQ;
+    const int qb = i0 + 32 * qs;                 // first query of this wave's half
     const uint8_t* Q = cur + C::Q_OFF;
     const uint8_t* Qs = cur + C::QS_OFF;
     const uint8_t* O = cur + C::O_OFF;
     const uint8_t* Os = cur + C::OS_OFF;
     const float4* Row = reinterpret_cast<const float4*>(cur + C::ROW_OFF);
-    v8i pa, da;          // P' and dS' codes, the lane's query order
-    int dse[2] = {-127, -127};
+    v4i pc, dc;          // P' and dS' codes of the half, the lane's query order
+    int e = -127;
     // tiles wholly after the workgroup's keys and inside the sequence: no
-    // mask, no skipped sub-block
+    // mask, no skipped half
     const bool full = i0 >= kb0 + BKB && i0 + BQ <= N;
 
-    auto subblock = [&](const int qs, auto edge_tag) __attribute__((always_inline)) {
+    auto half = [&](auto edge_tag) __attribute__((always_inline)) {
       constexpr bool EDGE = decltype(edge_tag)::value;
-      const int qb = i0 + 32 * qs;               // first query of the sub-block
       if (EDGE && (!live || qb < kw0 || qb >= N)) {
-#pragma unroll
-        for (int k = 0; k < 4; k++) { pa[4 * qs + k] = 0; da[4 * qs + k] = 0; }
+        pc = v4i{0, 0, 0, 0};
+        dc = v4i{0, 0, 0, 0};
         return;
       }
       v16f s, dp;
@@ -386,16 +393,16 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
       for (int t2 = 0; t2 < VS; t2++)
         dp = mfma_mx(frag_rows_swz<DV>(O, 32 * qs + li, t2, hf), vf[t2], dp,
                      Os[(32 * qs + li) * (DV / 32) + 2 * t2 + hf], vsc[t2]);
-      // lane holds queries qb + 8 g + 4 hf + e (accumulator r = 4 g + e)
+      // lane holds queries qb + 8 g + 4 hf + e4 (accumulator r = 4 g + e4)
       float amax = 0.f;
 #pragma unroll
       for (int g = 0; g < 4; g++) {
 #pragma unroll
-        for (int e = 0; e < 4; e++) {
-          const int r = 4 * g + e;
-          const float4 rv = Row[32 * qs + 8 * g + 4 * hf + e];   // L log2 e, delta hi, delta lo, q_c*
+        for (int e4 = 0; e4 < 4; e4++) {
+          const int r = 4 * g + e4;
+          const float4 rv = Row[32 * qs + 8 * g + 4 * hf + e4];   // L log2 e, delta hi, delta lo, q_c*
           float p = bwd_prob(__builtin_fmaf(rv.w, khot, s[r]), c, rv.x);
-          if (EDGE && qb == kw0) p = (li > 8 * g + 4 * hf + e) ? 0.f : p;   // diagonal block: key > query
+          if (EDGE && qb == kw0) p = (li > 8 * g + 4 * hf + e4) ? 0.f : p;   // diagonal block: key > query
           s[r] = p;
           dp[r] = p * ((dp[r] - rv.y) - rv.z);
           amax = fmaxf(amax, fabsf(dp[r]));
@@ -403,19 +410,18 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
       }
 #pragma unroll
       for (int k = 0; k < 4; k++)
-        pa[4 * qs + k] = (int)cvt4_div(s[4 * k], s[4 * k + 1], s[4 * k + 2], s[4 * k + 3], 0.00390625f);
-      int e = pow2_exponent(wave_max_nonneg(amax));
+        pc[k] = (int)cvt4_div(s[4 * k], s[4 * k + 1], s[4 * k + 2], s[4 * k + 3], 0.00390625f);
+      e = pow2_exponent(wave_max_nonneg(amax));
       e = e < -126 ? -126 : e;
       const float sc = exp2i(e);
 #pragma unroll
       for (int k = 0; k < 4; k++)
-        da[4 * qs + k] = (int)cvt4_div(dp[4 * k], dp[4 * k + 1], dp[4 * k + 2], dp[4 * k + 3], sc);
-      dse[qs] = e;
-      if (STATS && chh == 0) {
+        dc[k] = (int)cvt4_div(dp[4 * k], dp[4 * k + 1], dp[4 * k + 2], dp[4 * k + 3], sc);
+      if constexpr (STATS) {
         // per query row: FP64 sums over this wave's 32 keys, then atomics
 #pragma unroll
         for (int r = 0; r < 16; r++) {
-          const float cast = fp8_value((uint32_t)da[4 * qs + (r >> 2)], r & 3) * sc;
+          const float cast = fp8_value((uint32_t)dc[r >> 2], r & 3) * sc;
           const double s0 = half_sum_d((double)dp[r]);
           const double s1 = half_sum_d((double)fabsf(dp[r]));
           const double s2 = half_sum_d((double)cast);
@@ -432,49 +438,43 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
         }
       }
     };
-    if (full) {
-      subblock(0, std::false_type{});
-      subblock(1, std::false_type{});
-    } else {
-      subblock(0, std::true_type{});
-      subblock(1, std::true_type{});
-    }
-    // natural query order: lane hf holds queries 16 hf .. 16 hf + 15 of each
-    // sub-block (dwords of the A operands of dV and dK)
-    v8i pn, dn;
-#pragma unroll
-    for (int qs = 0; qs < 2; qs++) {
-      to_natural(pa, pn, qs);
-      to_natural(da, dn, qs);
-    }
-    // dV += P'^T dO_col ; dK += dS'^T Q_col   (k = the 64 queries of the tile;
-    // skipped sub-blocks have zero codes)
+    if (full) half(std::false_type{});
+    else half(std::true_type{});
+
+    // natural query order: lane hf holds queries 16 hf .. 16 hf + 15 of the half
+    const v4i pn = to_natural4(pc), dn = to_natural4(dc);
+    // dS' codes for the dQ units and the exchange with the other half
+    *reinterpret_cast<uint4*>(ds + (32 * kbw + li) * C::DST + 32 * qs + 16 * hf) =
+        make_uint4((uint32_t)dn[0], (uint32_t)dn[1], (uint32_t)dn[2], (uint32_t)dn[3]);
+    if (lane == 0) es[kbw * 2 + qs] = (uint8_t)(e + 127);
     {
-      const int dascale = (hf ? dse[1] : dse[0]) + 127;
+      const v4i x = qs == 0 ? dn : pn;
+      xch[qs][kbw * 64 + lane] = make_uint4((uint32_t)x[0], (uint32_t)x[1], (uint32_t)x[2], (uint32_t)x[3]);
+    }
+    lds_sync();
+    // dV += P'^T dO_col (first half) or dK += dS'^T Q_col (second half); k =
+    // the tile's 64 queries, bytes 0..15 from the first half, 16..31 from the
+    // second (skipped halves have zero codes)
+    if (qs == 0) {
+      const uint4 o = xch[1][kbw * 64 + lane];
+      const v8i A = v8i{pn[0], pn[1], pn[2], pn[3], (int)o.x, (int)o.y, (int)o.z, (int)o.w};
       const uint8_t* Oc = cur + C::OC_OFF;
       const uint8_t* Ocs = cur + C::OCS_OFF;
+#pragma unroll
+      for (int i = 0; i < CV; i++) {
+        const int ch = 32 * i + li;
+        acc[i] = mfma_mx(A, frag_cols_swz(Oc, ch, hf), acc[i], 127 - 8, Ocs[ch * 2 + hf]);
+      }
+    } else {
+      const uint4 o = xch[0][kbw * 64 + lane];
+      const v8i A = v8i{(int)o.x, (int)o.y, (int)o.z, (int)o.w, dn[0], dn[1], dn[2], dn[3]};
+      const int dascale = hf ? e + 127 : (int)es[kbw * 2];
       const uint8_t* Qc = cur + C::QC_OFF;
       const uint8_t* Qcs = cur + C::QCS_OFF;
 #pragma unroll
-      for (int i = 0; i < CV; i++) {
-        const int ch = 32 * (chh * CV + i) + li;
-        dv[i] = mfma_mx(pn, frag_cols_swz(Oc, ch, hf), dv[i], 127 - 8, Ocs[ch * 2 + hf]);
-      }
-#pragma unroll
       for (int i = 0; i < CK; i++) {
-        const int ch = 32 * (chh * CK + i) + li;
-        dk[i] = mfma_mx(dn, frag_cols_swz(Qc, ch, hf), dk[i], dascale, Qcs[ch * 2 + hf]);
-      }
-    }
-    // dS' codes to LDS: row = key (32 wk + li), 16 queries per lane and sub-block
-    if (chh == 0) {
-#pragma unroll
-      for (int qs = 0; qs < 2; qs++)
-        *reinterpret_cast<uint4*>(ds + (32 * wk + li) * C::DST + 32 * qs + 16 * hf) =
-            make_uint4((uint32_t)dn[4 * qs], (uint32_t)dn[4 * qs + 1], (uint32_t)dn[4 * qs + 2], (uint32_t)dn[4 * qs + 3]);
-      if (lane == 0) {
-        es[wk * 2] = (uint8_t)(dse[0] + 127);
-        es[wk * 2 + 1] = (uint8_t)(dse[1] + 127);
+        const int ch = 32 * i + li;
+        acc[i] = mfma_mx(A, frag_cols_swz(Qc, ch, hf), acc[i], dascale, Qcs[ch * 2 + hf]);
       }
     }
     lds_barrier();
@@ -489,35 +489,42 @@ __global__ __launch_bounds__((64 * BwdCfg<DQK, DV>::NWK)) void bwd_kernel(AttnAr
 
   for (int t = 0; t < total; t += 2) {
     if constexpr (C::NBUF == 2) {
-      body(t, stA, stB, (lds8*)stB, dsA, esA, dsB, esB);
-      if (t + 1 < total) body(t + 1, stB, stA, (lds8*)stA, dsB, esB, dsA, esA);
+      body(t, stA, (lds8*)stB, dsA, esA, dsB, esB);
+      if (t + 1 < total) body(t + 1, stB, (lds8*)stA, dsB, esB, dsA, esA);
     } else {
-      body(t, stA, stA, (lds8*)stA, dsA, esA, dsB, esB);
-      if (t + 1 < total) body(t + 1, stA, stA, (lds8*)stA, dsB, esB, dsA, esA);
+      body(t, stA, (lds8*)stA, dsA, esA, dsB, esB);
+      if (t + 1 < total) body(t + 1, stA, (lds8*)stA, dsB, esB, dsA, esA);
     }
   }
   if (total & 1) ds_store(total - 1, dsA, esA);
   else ds_store(total - 1, dsB, esB);
 
   if (!live) return;
-  // dK (times tau) and dV: lane holds channel 32 i + li, keys kw0 + 8 (r/4) + 4 hf + r % 4
+  // dV (first half) or dK times tau (second half): lane holds channel
+  // 32 i + li, keys kw0 + 8 (r/4) + 4 hf + r % 4
 #pragma unroll
   for (int r = 0; r < 16; r++) {
     const int key = kw0 + 8 * (r >> 2) + 4 * hf + (r & 3);
-    if (a.grad_bf16) {
-      uint16_t* kd = reinterpret_cast<uint16_t*>(a.dk) + b * a.dks[0] + (int64_t)key * a.dks[1] + kh * a.dks[2];
-      uint16_t* vd = reinterpret_cast<uint16_t*>(a.dv) + b * a.dvs[0] + (int64_t)key * a.dvs[1] + kh * a.dvs[2];
+    if (qs == 0) {
+      if (a.grad_bf16) {
+        uint16_t* vd = reinterpret_cast<uint16_t*>(a.dv) + b * a.dvs[0] + (int64_t)key * a.dvs[1] + kh * a.dvs[2];
 #pragma unroll
-      for (int i = 0; i < CK; i++) kd[32 * (chh * CK + i) + li] = f32_to_bf16(dk[i][r] * a.tau);
+        for (int i = 0; i < CV; i++) vd[32 * i + li] = f32_to_bf16(acc[i][r]);
+      } else {
+        float* vd = reinterpret_cast<float*>(a.dv) + b * a.dvs[0] + (int64_t)key * a.dvs[1] + kh * a.dvs[2];
 #pragma unroll
-      for (int i = 0; i < CV; i++) vd[32 * (chh * CV + i) + li] = f32_to_bf16(dv[i][r]);
+        for (int i = 0; i < CV; i++) vd[32 * i + li] = acc[i][r];
+      }
     } else {
-      float* kd = reinterpret_cast<float*>(a.dk) + b * a.dks[0] + (int64_t)key * a.dks[1] + kh * a.dks[2];
-      float* vd = reinterpret_cast<float*>(a.dv) + b * a.dvs[0] + (int64_t)key * a.dvs[1] + kh * a.dvs[2];
+      if (a.grad_bf16) {
+        uint16_t* kd = reinterpret_cast<uint16_t*>(a.dk) + b * a.dks[0] + (int64_t)key * a.dks[1] + kh * a.dks[2];
 #pragma unroll
-      for (int i = 0; i < CK; i++) kd[32 * (chh * CK + i) + li] = dk[i][r] * a.tau;
+        for (int i = 0; i < CK; i++) kd[32 * i + li] = f32_to_bf16(acc[i][r] * a.tau);
+      } else {
+        float* kd = reinterpret_cast<float*>(a.dk) + b * a.dks[0] + (int64_t)key * a.dks[1] + kh * a.dks[2];
 #pragma unroll
-      for (int i = 0; i < CV; i++) vd[32 * (chh * CV + i) + li] = dv[i][r];
+        for (int i = 0; i < CK; i++) kd[32 * i + li] = acc[i][r] * a.tau;
+      }
     }
   }
 }
