@@ -39,6 +39,7 @@
 #include <type_traits>
 
 #include "common.hpp"
+#include "dma.hpp"
 #include "kernels.hpp"
 #include "tiles.hpp"
 
@@ -71,55 +72,11 @@ struct BwdCfg {
   static constexpr int STAGE = ROW_OFF + BQ * 16;
 };
 
-// XOR swizzle of the 16-byte chunks of a row-major tile with D-byte rows
-// (16 consecutive rows read at one logical chunk land on distinct banks).
-template <int D>
-__device__ __forceinline__ int swz_row(int r) {
-  if constexpr (D == 64) return (r >> 2) & 3;
-  else if constexpr (D == 128) return (r >> 1) & 7;
-  else if constexpr (D == 192) return (r >> 2) & 3;
-  else return r & 15;
-}
-// col tiles have 64-byte rows (one channel, 64 queries)
-__device__ __forceinline__ int swz_col(int c) { return (c >> 2) & 3; }
-
 // dQ operand units of one head before query block q (block q has q/2 + 1
 // units of 64 keys up to the diagonal): sum_{i<q} (floor(i/2) + 1).
 __host__ __device__ __forceinline__ int64_t tri_units(int64_t q) {
   const int64_t m = q >> 1;
   return (q & 1) ? (m + 1) * (m + 1) : m * (m + 1);
-}
-
-// LDS byte pointer; direct-to-LDS loads take their destination in this form
-// (pointers derived from the __shared__ arrays themselves, never from a
-// generic pointer)
-typedef __attribute__((address_space(3))) uint8_t lds8;
-
-__device__ __forceinline__ void dma16(const void* src, lds8* lds_base) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
-}
-__device__ __forceinline__ void dma4(const void* src, lds8* lds_base) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 4, 0, 0);
-}
-
-// Waits for this wave's LDS writes and direct-to-LDS loads (and any other
-// vector memory operation), then a workgroup barrier ordered for LDS only.
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0)
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
-// Workgroup barrier after this wave's LDS writes only: direct-to-LDS loads
-// in flight stay in flight (an LDS release fence would wait for them, since
-// they write LDS), so the ordering of the surrounding LDS accesses is kept
-// by compiler barriers instead.
-__device__ __forceinline__ void lds_sync() {
-  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
 }
 
 // Per-(batch, query head) base pointers of the query-side operands.
@@ -140,45 +97,6 @@ __device__ __forceinline__ BwdHead bwd_head(const AttnArgs& a, size_t bh, int N)
   p.tcs = a.tile_cs + bh * ((N + 63) / 64) * (2 * (DQK + DV));
   p.rows = reinterpret_cast<const float4*>(a.rows) + bh * N;
   return p;
-}
-
-// Row-major code tile [BQ][D] (rows i0.., clamped to the sequence) into LDS,
-// swizzled; wave w issues instructions w, w + NWK, ...
-template <int D, int NWK>
-__device__ __forceinline__ void dma_rows(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) {
-  constexpr int NI = 64 * D / 1024;
-  for (int k = w; k < NI; k += NWK) {
-    const int off = 1024 * k + 16 * lane;
-    const int r = off / D, p = (off % D) / 16;
-    const int row = i0 + r < N ? i0 + r : N - 1;
-    dma16(code + row * D + 16 * (p ^ swz_row<D>(r)), lds + 1024 * k);
-  }
-}
-// Col-copy code tile: channels [0, D), queries [i0, i0 + 64) (clamped) -> [D][64].
-template <int D, int NWK>
-__device__ __forceinline__ void dma_cols(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) {
-  constexpr int NI = D * 64 / 1024;
-  for (int k = w; k < NI; k += NWK) {
-    const int off = 1024 * k + 16 * lane;
-    const int c = off / 64, p = (off % 64) / 16;
-    const int q = p ^ swz_col(c);
-    const int col = i0 + 16 * q < N - 16 ? i0 + 16 * q : N - 16;
-    dma16(code + c * N + col, lds + 1024 * k);
-  }
-}
-// Row-copy scales of 64 rows: 64 * D / 32 contiguous bytes (clamped).
-template <int D, int NWK>
-__device__ __forceinline__ void dma_row_scales(lds8* lds, const uint8_t* scale, int i0, int N, int w, int lane,
-                                               int first_wave) {
-  constexpr int BYTES = 64 * D / 32, NI = (BYTES + 255) / 256;
-  for (int k = 0; k < NI; k++) {
-    if ((first_wave + k) % NWK != w) continue;
-    const int off = 256 * k + 4 * lane;
-    if (off < BYTES) {
-      const int g = i0 * (D / 32) + off, lim = N * (D / 32) - 4;
-      dma4(scale + (g < lim ? g : lim), lds + 256 * k);
-    }
-  }
 }
 
 // Issues every load of one query tile, all direct-to-LDS: codes, row scales,
@@ -205,24 +123,6 @@ __device__ __forceinline__ void stage_issue(lds8* st, const BwdHead& hp, int i0,
     const int r = i0 + lane < N ? i0 + lane : N - 1;
     dma16(hp.rows + r, st + C::ROW_OFF);
   }
-}
-
-// A/B fragment (row `row`, k-step t, half hf) of a swizzled row-major tile.
-template <int D>
-__device__ __forceinline__ v8i frag_rows_swz(const uint8_t* tile, int row, int t, int hf) {
-  const int s = swz_row<D>(row), c = 4 * t + hf;
-  const uint8_t* base = tile + row * D;
-  const uint4 lo = *reinterpret_cast<const uint4*>(base + 16 * (c ^ s));
-  const uint4 hi = *reinterpret_cast<const uint4*>(base + 16 * ((c + 2) ^ s));
-  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
-}
-// B fragment of a swizzled col tile: channel ch, queries 16 hf.. and 32 + 16 hf..
-__device__ __forceinline__ v8i frag_cols_swz(const uint8_t* tile, int ch, int hf) {
-  const int s = swz_col(ch);
-  const uint8_t* base = tile + ch * 64;
-  const uint4 lo = *reinterpret_cast<const uint4*>(base + 16 * (hf ^ s));
-  const uint4 hi = *reinterpret_cast<const uint4*>(base + 16 * ((hf + 2) ^ s));
-  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
 }
 
 __device__ __forceinline__ double half_sum_d(double v) {

@@ -2,55 +2,68 @@
 //
 // delta_i = (sum_j P_ij dP_ij) / (sum_j P_ij) with the FP32 probabilities
 // P = 2^(S tau log2e - LSE log2e) recomputed from the FP8 scores, and
-// dP = dO_row V_row^T (MX MFMA, FP32).  Keys are visited in ascending order;
-// sum P dP and sum P are reduced in FP32 over each aligned 32-key group, the
-// group sums are accumulated in FP64, and delta is stored as an FP32 pair
-// (hi, lo) with hi + lo the FP64 quotient to about 2^-48.  Dividing by sum P
-// makes the pair the exact centring constant of the P the backward
-// recomputes, even where the stored LSE leaves sum P a few ulp away from 1.
+// dP = dO_row V_row^T (MX MFMA, FP32).  Sums of P dP and of P are formed in
+// FP32 over each aligned 32-key group, the group sums are accumulated in
+// FP64, and delta is stored as an FP32 pair (hi, lo) with hi + lo the FP64
+// quotient to about 2^-48.  Dividing by sum P makes the pair the exact
+// centring constant of the P the backward recomputes, even where the stored
+// LSE leaves sum P a few ulp away from 1.
 //
-// Geometry as in the forward: NW waves x 32 queries per workgroup, 64-key
-// tiles of K and V (row copies) staged in LDS; S^T and dP^T are computed so
-// that each lane owns one query.  P and dP use exactly the operations of the
-// backward kernel (same MX MFMA operands and k order, bwd_prob()), so the
-// backward's dS = P (dP - delta) sums to zero over every row up to FP32
-// rounding of its own terms.
+// Workgroup: NW waves x 32 queries of one (batch, query head); 128-key tiles
+// of K and V (row copies) reach LDS by direct loads, double-buffered, so the
+// next tile streams in while the current one is computed.  S^T and dP^T put
+// one query in each lane (row reductions in-lane plus one exchange with lane
+// l ^ 32).  P and dP use exactly the operations of the backward kernel (same
+// MX MFMA operands and k order, bwd_prob()), so the backward's
+// dS = P (dP - delta) sums to zero over every row up to FP32 rounding of its
+// own terms.  Only the 32-key group holding the diagonal is masked; groups
+// in a wave's future are skipped.
 #include "common.hpp"
+#include "dma.hpp"
 #include "kernels.hpp"
 #include "tiles.hpp"
 
 namespace afp8 {
 
-template <int DQK, int DV, int NW>
-__global__ __launch_bounds__(64 * NW) void delta_matching_kernel(AttnArgs a) {
-  constexpr int BQ = 32 * NW, BK = 64;
+template <int DQK, int DV>
+struct DeltaCfg {
+  static constexpr int NW = 4, NT = 64 * NW, BQ = 32 * NW, BK = 128;
+  static constexpr int al16(int x) { return (x + 15) & ~15; }
+  static constexpr int K_OFF = 0;                               // K row codes [BK][DQK], swizzled
+  static constexpr int V_OFF = K_OFF + BK * DQK;                // V row codes [BK][DV], swizzled
+  static constexpr int KS_OFF = V_OFF + BK * DV;                // K row scales [BK][DQK/32]
+  static constexpr int VS_OFF = al16(KS_OFF + BK * DQK / 32);   // V row scales [BK][DV/32]
+  static constexpr int KH_OFF = al16(VS_OFF + BK * DV / 32);    // isolated-channel key values [BK] FP32
+  static constexpr int STAGE = KH_OFF + BK * 4;
+  // two workgroups per CU where both stage buffers fit 80 KB
+  static constexpr int WGS = 2 * STAGE <= 80 * 1024 ? 2 : 1;
+};
+
+template <int DQK, int DV>
+__global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_kernel(AttnArgs a) {
+  using C = DeltaCfg<DQK, DV>;
+  constexpr int NW = C::NW, BQ = C::BQ, BK = C::BK;
   constexpr int KS = DQK / 64, VS = DV / 64;
-  constexpr int KST = DQK + 16, VST = DV + 16;
-  __shared__ __attribute__((aligned(16))) uint8_t sK[BK * KST];
-  __shared__ __attribute__((aligned(16))) uint8_t sKs[BK * DQK / 32];
-  __shared__ __attribute__((aligned(16))) uint8_t sV[BK * VST];
-  __shared__ __attribute__((aligned(16))) uint8_t sVs[BK * DV / 32];
-  __shared__ __attribute__((aligned(16))) float sKh[BK];
+  __shared__ __attribute__((aligned(16))) uint8_t stA[C::STAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t stB[C::STAGE];
   __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
-  const int64_t nqb = (a.N + BQ - 1) / BQ;
-  const int64_t qb = nqb - 1 - (int64_t)blockIdx.x;
-  const int64_t h = blockIdx.y, b = blockIdx.z, kh = h / a.G;
-  const int64_t q0 = qb * BQ + 32 * w;
-  const bool live = q0 < a.N;
-  const int64_t qi = q0 + li;
+  const int N = (int)a.N;
+  const int nqb = (N + BQ - 1) / BQ;
+  const int qb = nqb - 1 - (int)blockIdx.x;    // longest causal rows first
+  const int h = blockIdx.y, b = blockIdx.z, kh = h / (int)a.G;
+  const int q0 = qb * BQ + 32 * w;
+  const bool live = q0 < N;
+  const int qi = q0 + li;
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
 
+  const size_t bhq = (size_t)b * a.Hq + h, bhk = (size_t)b * a.Hkv + kh;
   v8i qf[KS], df[VS];
   int qsc[KS], dsc[VS];
-  float L = 0.f;
-#pragma unroll
-  for (int s = 0; s < KS; s++) { qf[s] = v8i{0, 0, 0, 0, 0, 0, 0, 0}; qsc[s] = 0; }
-#pragma unroll
-  for (int s = 0; s < VS; s++) { df[s] = v8i{0, 0, 0, 0, 0, 0, 0, 0}; dsc[s] = 0; }
-  if (live) {
-    const int64_t row = (b * a.Hq + h) * a.N + qi;
+  float L = 0.f, qhot = 0.f;
+  {
+    const size_t row = bhq * N + (live ? qi : 0);
 #pragma unroll
     for (int s = 0; s < KS; s++) {
       qf[s] = frag_rows_global(a.q_code + row * DQK, s, hf);
@@ -63,87 +76,107 @@ __global__ __launch_bounds__(64 * NW) void delta_matching_kernel(AttnArgs a) {
       dsc[s] = a.do_scale[row * (DV / 32) + 2 * s + hf];
     }
     L = a.lse[row] * kLog2e;
+    if (hot >= 0) qhot = row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot);
   }
-  const float qhot = (live && hot >= 0) ? row_value<DQK>(a.q_code, a.q_scale, (b * a.Hq + h) * a.N + qi, hot) : 0.f;
   double num = 0.0, den = 0.0;
 
-  const int64_t qend = ((qb + 1) * BQ < a.N) ? (qb + 1) * BQ : a.N;
-  const int ntiles = (int)((qend + BK - 1) / BK);
-  const uint8_t* kcode = a.k_code + (b * a.Hkv + kh) * a.N * DQK;
-  const uint8_t* kscale = a.k_scale + (b * a.Hkv + kh) * a.N * (DQK / 32);
-  const uint8_t* vcode = a.v_code + (b * a.Hkv + kh) * a.N * DV;
-  const uint8_t* vscale = a.v_scale + (b * a.Hkv + kh) * a.N * (DV / 32);
+  const uint8_t* kcode = a.k_code + bhk * N * DQK;
+  const uint8_t* kscale = a.k_scale + bhk * N * (DQK / 32);
+  const uint8_t* vcode = a.v_code + bhk * N * DV;
+  const uint8_t* vscale = a.v_scale + bhk * N * (DV / 32);
+  const int qend = (qb + 1) * BQ < N ? (qb + 1) * BQ : N;
+  const int ntiles = (qend + BK - 1) / BK;
 
-  for (int t = 0; t < ntiles; t++) {
-    const int64_t j0 = (int64_t)t * BK;
-    __syncthreads();
-    stage_rows<BK, DQK, KST, 64 * NW>(sK, sKs, kcode, kscale, j0, a.N, hot);
-    stage_rows<BK, DV, VST, 64 * NW>(sV, sVs, vcode, vscale, j0, a.N);
+  // loads of tile j0 (raw isolated-channel bytes in registers, decoded when
+  // they are stored to LDS)
+  uint32_t khc = 0, khs = 0;
+  auto issue = [&](lds8* st, int j0) __attribute__((always_inline)) {
+    dma_rows<DQK, NW, BK>(st + C::K_OFF, kcode, j0, N, w, lane);
+    dma_rows<DV, NW, BK>(st + C::V_OFF, vcode, j0, N, w, lane);
+    dma_row_scales<DQK, NW, BK>(st + C::KS_OFF, kscale, j0, N, w, lane, 0);
+    dma_row_scales<DV, NW, BK>(st + C::VS_OFF, vscale, j0, N, w, lane, 1);
+    if (hot >= 0 && threadIdx.x < BK) {
+      const int r = j0 + (int)threadIdx.x < N ? j0 + (int)threadIdx.x : N - 1;
+      khc = kcode[r * DQK + hot];
+      khs = kscale[r * (DQK / 32) + hot / 32];
+    }
+    __builtin_amdgcn_sched_barrier(0);   // keep every load ahead of the tile's compute
+  };
+  auto finish = [&](uint8_t* st) __attribute__((always_inline)) {
     if (threadIdx.x < BK)
-      sKh[threadIdx.x] = (hot >= 0 && j0 + threadIdx.x < a.N) ? row_value<DQK>(kcode, kscale, j0 + threadIdx.x, hot) : 0.f;
-    __syncthreads();
-    if (!live || j0 > q0) continue;
+      reinterpret_cast<float*>(st + C::KH_OFF)[threadIdx.x] = hot >= 0 ? scaled_value(khc, khs) : 0.f;
+  };
 
-    const bool diag = j0 + BK - 1 > q0;
-    float gnum[2], gden[2];
+  auto tile = [&](const uint8_t* st, int j0) __attribute__((always_inline)) {
+    if (!live || j0 > q0) return;
+    const uint8_t* K = st + C::K_OFF;
+    const uint8_t* Ks = st + C::KS_OFF;
+    const uint8_t* V = st + C::V_OFF;
+    const uint8_t* Vs = st + C::VS_OFF;
+    const float* Kh = reinterpret_cast<const float*>(st + C::KH_OFF);
 #pragma unroll
-    for (int kb = 0; kb < 2; kb++) {
+    for (int g = 0; g < BK / 32; g++) {
+      const int g0 = j0 + 32 * g;              // first key of the group
+      if (g0 > q0) break;                      // this and later groups are in the wave's future
       v16f s, dp;
 #pragma unroll
       for (int r = 0; r < 16; r++) { s[r] = 0.f; dp[r] = 0.f; }
 #pragma unroll
-      for (int st = 0; st < KS; st++) {
-        const v8i kf = frag_rows<KST>(sK, 32 * kb + li, st, hf);
-        s = mfma_mx(kf, qf[st], s, sKs[(32 * kb + li) * (DQK / 32) + 2 * st + hf], qsc[st]);
-      }
+      for (int t = 0; t < KS; t++)
+        s = mfma_mx(frag_rows_swz<DQK>(K, 32 * g + li, t, hf), qf[t], s, Ks[(32 * g + li) * (DQK / 32) + 2 * t + hf],
+                    qsc[t]);
 #pragma unroll
-      for (int st = 0; st < VS; st++) {
-        const v8i vf = frag_rows<VST>(sV, 32 * kb + li, st, hf);
-        dp = mfma_mx(vf, df[st], dp, sVs[(32 * kb + li) * (DV / 32) + 2 * st + hf], dsc[st]);
-      }
+      for (int t = 0; t < VS; t++)
+        dp = mfma_mx(frag_rows_swz<DV>(V, 32 * g + li, t, hf), df[t], dp, Vs[(32 * g + li) * (DV / 32) + 2 * t + hf],
+                     dsc[t]);
+      // lane holds keys g0 + 8 (r/4) + 4 hf + r % 4 of query qi
       float pn = 0.f, pd = 0.f;
-      float kh4[16];
 #pragma unroll
-      for (int g = 0; g < 4; g++) {
-        const float4 v4 = *reinterpret_cast<const float4*>(&sKh[32 * kb + 8 * g + 4 * hf]);
-        kh4[4 * g] = v4.x; kh4[4 * g + 1] = v4.y; kh4[4 * g + 2] = v4.z; kh4[4 * g + 3] = v4.w;
-      }
+      for (int q4 = 0; q4 < 4; q4++) {
+        const float4 kh4 = *reinterpret_cast<const float4*>(&Kh[32 * g + 8 * q4 + 4 * hf]);
+        const float khv[4] = {kh4.x, kh4.y, kh4.z, kh4.w};
 #pragma unroll
-      for (int r = 0; r < 16; r++) {
-        float p = bwd_prob(__builtin_fmaf(qhot, kh4[r], s[r]), a.c, L);
-        if (diag) {
-          const int64_t key = j0 + 32 * kb + 8 * (r >> 2) + 4 * hf + (r & 3);
-          p = key > qi ? 0.f : p;
+        for (int e = 0; e < 4; e++) {
+          const int r = 4 * q4 + e;
+          float p = bwd_prob(__builtin_fmaf(qhot, khv[e], s[r]), a.c, L);
+          if (g0 == q0) p = (8 * q4 + 4 * hf + e) > li ? 0.f : p;   // diagonal group: key > query
+          pn = __builtin_fmaf(p, dp[r], pn);
+          pd += p;
         }
-        pn = __builtin_fmaf(p, dp[r], pn);
-        pd += p;
       }
-      gnum[kb] = pn;
-      gden[kb] = pd;
+      // 32-key group sums: this lane's 16 keys plus the partner's 16 (FP32)
+      num += (double)(pn + partner(pn));
+      den += (double)(pd + partner(pd));
     }
-    // 32-key group sums: this lane's 16 keys plus the partner's 16 (FP32)
-#pragma unroll
-    for (int kb = 0; kb < 2; kb++) {
-      const float n32 = gnum[kb] + partner(gnum[kb]);
-      const float d32 = gden[kb] + partner(gden[kb]);
-      num += (double)n32;
-      den += (double)d32;
-    }
+  };
+
+  issue((lds8*)stA, 0);
+  finish(stA);
+  lds_barrier();
+  for (int t = 0; t < ntiles; t += 2) {
+    if (t + 1 < ntiles) issue((lds8*)stB, (t + 1) * BK);
+    tile(stA, t * BK);
+    if (t + 1 < ntiles) finish(stB);
+    lds_barrier();
+    if (t + 1 >= ntiles) break;
+    if (t + 2 < ntiles) issue((lds8*)stA, (t + 2) * BK);
+    tile(stB, (t + 1) * BK);
+    if (t + 2 < ntiles) finish(stA);
+    lds_barrier();
   }
   if (!live || hf != 0) return;
   const double d = den > 0.0 ? num / den : 0.0;
   const float hi = (float)d;
   const float lo = (float)(d - (double)hi);
-  float* dst = a.delta_out + ((b * a.Hq + h) * a.N + qi) * 2;
-  *reinterpret_cast<float2*>(dst) = make_float2(hi, lo);
+  *reinterpret_cast<float2*>(a.delta_out + (bhq * N + qi) * 2) = make_float2(hi, lo);
 }
 
 template <int DQK, int DV>
 static hipError_t delta_dispatch(const AttnArgs& a, hipStream_t s) {
-  constexpr int NW = 4;
-  const int64_t nqb = (a.N + 32 * NW - 1) / (32 * NW);
+  using C = DeltaCfg<DQK, DV>;
+  const int64_t nqb = (a.N + C::BQ - 1) / C::BQ;
   dim3 grid((unsigned)nqb, (unsigned)a.Hq, (unsigned)a.B);
-  hipLaunchKernelGGL((delta_matching_kernel<DQK, DV, NW>), grid, dim3(64 * NW), 0, s, a);
+  hipLaunchKernelGGL((delta_matching_kernel<DQK, DV>), grid, dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }
 

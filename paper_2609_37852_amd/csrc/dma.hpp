@@ -1,0 +1,111 @@
+// Direct global -> LDS staging (global_load_lds, gfx950) shared by the
+// attention kernels: swizzled unpadded tile layouts, the loads that fill
+// them, the fragment reads, and the barriers that go with them.
+#pragma once
+
+#include "common.hpp"
+
+namespace afp8 {
+
+// XOR swizzle of the 16-byte chunks of a row-major tile with D-byte rows
+// (16 consecutive rows read at one logical chunk land on distinct banks).
+template <int D>
+__device__ __forceinline__ int swz_row(int r) {
+  if constexpr (D == 64) return (r >> 2) & 3;
+  else if constexpr (D == 128) return (r >> 1) & 7;
+  else if constexpr (D == 192) return (r >> 2) & 3;
+  else return r & 15;
+}
+// col tiles have 64-byte rows (one channel, 64 queries)
+__device__ __forceinline__ int swz_col(int c) { return (c >> 2) & 3; }
+
+// LDS byte pointer; direct-to-LDS loads take their destination in this form
+// (pointers derived from the __shared__ arrays themselves, never from a
+// generic pointer)
+typedef __attribute__((address_space(3))) uint8_t lds8;
+
+__device__ __forceinline__ void dma16(const void* src, lds8* lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+__device__ __forceinline__ void dma4(const void* src, lds8* lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 4, 0, 0);
+}
+
+// Waits for this wave's LDS writes and direct-to-LDS loads (and any other
+// vector memory operation), then a workgroup barrier ordered for LDS only.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0)
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Workgroup barrier after this wave's LDS writes only: direct-to-LDS loads
+// in flight stay in flight (an LDS release fence would wait for them, since
+// they write LDS), so the ordering of the surrounding LDS accesses is kept
+// by compiler barriers instead.
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Row-major code tile [ROWS][D] (rows i0.., clamped to the sequence) into
+// LDS, swizzled; wave w issues instructions w, w + NWK, ...
+template <int D, int NWK, int ROWS = 64>
+__device__ __forceinline__ void dma_rows(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) {
+  constexpr int NI = ROWS * D / 1024;
+  for (int k = w; k < NI; k += NWK) {
+    const int off = 1024 * k + 16 * lane;
+    const int r = off / D, p = (off % D) / 16;
+    const int row = i0 + r < N ? i0 + r : N - 1;
+    dma16(code + row * D + 16 * (p ^ swz_row<D>(r)), lds + 1024 * k);
+  }
+}
+// Col-copy code tile: channels [0, D), queries [i0, i0 + 64) (clamped) -> [D][64].
+template <int D, int NWK>
+__device__ __forceinline__ void dma_cols(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) {
+  constexpr int NI = D * 64 / 1024;
+  for (int k = w; k < NI; k += NWK) {
+    const int off = 1024 * k + 16 * lane;
+    const int c = off / 64, p = (off % 64) / 16;
+    const int q = p ^ swz_col(c);
+    const int col = i0 + 16 * q < N - 16 ? i0 + 16 * q : N - 16;
+    dma16(code + c * N + col, lds + 1024 * k);
+  }
+}
+// Row-copy scales of ROWS rows: ROWS * D / 32 contiguous bytes (clamped).
+template <int D, int NWK, int ROWS = 64>
+__device__ __forceinline__ void dma_row_scales(lds8* lds, const uint8_t* scale, int i0, int N, int w, int lane,
+                                               int first_wave) {
+  constexpr int BYTES = ROWS * D / 32, NI = (BYTES + 255) / 256;
+  for (int k = 0; k < NI; k++) {
+    if ((first_wave + k) % NWK != w) continue;
+    const int off = 256 * k + 4 * lane;
+    if (off < BYTES) {
+      const int g = i0 * (D / 32) + off, lim = N * (D / 32) - 4;
+      dma4(scale + (g < lim ? g : lim), lds + 256 * k);
+    }
+  }
+}
+
+// A/B fragment (row `row`, k-step t, half hf) of a swizzled row-major tile.
+template <int D>
+__device__ __forceinline__ v8i frag_rows_swz(const uint8_t* tile, int row, int t, int hf) {
+  const int s = swz_row<D>(row), c = 4 * t + hf;
+  const uint8_t* base = tile + row * D;
+  const uint4 lo = *reinterpret_cast<const uint4*>(base + 16 * (c ^ s));
+  const uint4 hi = *reinterpret_cast<const uint4*>(base + 16 * ((c + 2) ^ s));
+  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
+// B fragment of a swizzled col tile: channel ch, queries 16 hf.. and 32 + 16 hf..
+__device__ __forceinline__ v8i frag_cols_swz(const uint8_t* tile, int ch, int hf) {
+  const int s = swz_col(ch);
+  const uint8_t* base = tile + ch * 64;
+  const uint4 lo = *reinterpret_cast<const uint4*>(base + 16 * (hf ^ s));
+  const uint4 hi = *reinterpret_cast<const uint4*>(base + 16 * ((hf + 2) ^ s));
+  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
+
+}  // namespace afp8
