@@ -171,8 +171,12 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   const int kbw = w % KBW;                      // this wave's 32-key block within the workgroup
   const int qs = w / KBW;                       // and its 32-query half of every tile
   const int N = (int)a.N;
-  const int kb0 = blockIdx.x * BKB;             // key block (block 0 has the most work)
-  const int kh = blockIdx.y, b = blockIdx.z;
+  // workgroup id -> key block (slowest: block 0 has the most work and goes
+  // first) and (batch, KV head) (fastest: the key blocks of one KV head get
+  // ids equal mod 16, hence one XCD and its L2 when B * Hkv % 8 == 0)
+  const int GI = (int)(a.B * a.Hkv);
+  const int kb0 = ((int)blockIdx.x / GI) * BKB;
+  const int kh = ((int)blockIdx.x % GI) % (int)a.Hkv, b = ((int)blockIdx.x % GI) / (int)a.Hkv;
   const int kw0 = kb0 + 32 * kbw;               // this wave's first key
   const bool live = kw0 < N;
   const int kj = kw0 + li;                      // this lane's key
@@ -214,7 +218,12 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   const int total = G * nq;
   const size_t bh0 = (size_t)b * Hq + (size_t)kh * G;   // first query head of the group
 
-  stage_issue<DQK, DV>((lds8*)stA, bwd_head<DQK, DV>(a, bh0, N), qt0 * BQ, N);
+  // tile t: query head kh G + t / nq, 64 queries from tile_q0(t); within a
+  // head the tiles run from the end of the sequence down to the diagonal, so
+  // the workgroups of one KV head (which all start together) read the same
+  // query tiles at about the same time and share them in the caches
+  auto tile_q0 = [&](int t) __attribute__((always_inline)) { return (nqt - 1 - t % nq) * BQ; };
+  stage_issue<DQK, DV>((lds8*)stA, bwd_head<DQK, DV>(a, bh0, N), tile_q0(0), N);
   lds_barrier();
 
   const int64_t units_per_head = tri_units(N / 32);
@@ -225,7 +234,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   auto ds_store = [&](const int t, const uint8_t* ds, const uint8_t* es) __attribute__((always_inline)) {
     constexpr int KSN = BKB / 64;
     const int h = kh * G + t / nq;
-    const int i0 = (qt0 + t % nq) * BQ;
+    const int i0 = tile_q0(t);
     if (w >= 2 * KSN) return;
     const int uq = w / KSN, ks = w % KSN;
     const int qb = i0 + 32 * uq;
@@ -258,11 +267,11 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     if (t > 0) ds_store(t - 1, ds_prev, es_prev);
     const bool more = t + 1 < total;
     if constexpr (C::NBUF == 2) {
-      if (more) stage_issue<DQK, DV>(nxt3, bwd_head<DQK, DV>(a, bh0 + (t + 1) / nq, N), (qt0 + (t + 1) % nq) * BQ, N);
+      if (more) stage_issue<DQK, DV>(nxt3, bwd_head<DQK, DV>(a, bh0 + (t + 1) / nq, N), tile_q0(t + 1), N);
     }
 
     const int h = kh * G + t / nq;
-    const int i0 = (qt0 + t % nq) * BQ;
+    const int i0 = tile_q0(t);
     const int qb = i0 + 32 * qs;                 // first query of this wave's half
     const uint8_t* Q = cur + C::Q_OFF;
     const uint8_t* Qs = cur + C::QS_OFF;
@@ -381,7 +390,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     if constexpr (C::NBUF == 1) {
       // one buffer: the next tile is loaded once every wave is done with it
       if (more) {
-        stage_issue<DQK, DV>(nxt3, bwd_head<DQK, DV>(a, bh0 + (t + 1) / nq, N), (qt0 + (t + 1) % nq) * BQ, N);
+        stage_issue<DQK, DV>(nxt3, bwd_head<DQK, DV>(a, bh0 + (t + 1) / nq, N), tile_q0(t + 1), N);
         lds_barrier();
       }
     }
@@ -486,8 +495,9 @@ __global__ __launch_bounds__(512) void dq_kernel(AttnArgs a) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
   const int N = (int)a.N, nqb = N / 32;
   const int ntile = (nqb + NW - 1) / NW;
-  const int tile = ntile - 1 - (int)blockIdx.x;      // longest rows first
-  const int h = blockIdx.y, b = blockIdx.z, kh = h / (int)a.G;
+  const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);
+  const int tile = ntile - 1 - wc.r;                 // longest rows first
+  const int h = wc.h, b = wc.b, kh = h / (int)a.G;
   const int qb = NW * tile + w;                      // this wave's 32-query block
   const int qlast = NW * tile + NW - 1 < nqb - 1 ? NW * tile + NW - 1 : nqb - 1;
   const int nk = qb < nqb ? qb / 2 + 1 : 0;          // this wave's 64-key steps
@@ -563,7 +573,7 @@ __global__ __launch_bounds__(512) void dq_kernel(AttnArgs a) {
 }
 
 hipError_t launch_dq(const AttnArgs& a, int dqk, hipStream_t s) {
-  const dim3 grid((unsigned)((a.N / 32 + 7) / 8), (unsigned)a.Hq, (unsigned)a.B);
+  const dim3 grid((unsigned)((a.N / 32 + 7) / 8 * a.Hq * a.B));
   switch (dqk) {
     case 64: hipLaunchKernelGGL((dq_kernel<64>), grid, dim3(512), 0, s, a); break;
     case 128: hipLaunchKernelGGL((dq_kernel<128>), grid, dim3(512), 0, s, a); break;
@@ -580,7 +590,7 @@ template <int DQK, int DV>
 static hipError_t bwd_dispatch(const AttnArgs& a, hipStream_t s) {
   using C = BwdCfg<DQK, DV>;
   const int64_t nkb = (a.N + C::BKB - 1) / C::BKB;
-  dim3 grid((unsigned)nkb, (unsigned)a.Hkv, (unsigned)a.B);
+  const dim3 grid((unsigned)(nkb * a.Hkv * a.B));
   if (a.rowstats) hipLaunchKernelGGL((bwd_kernel<DQK, DV, true>), grid, dim3(C::NT), 0, s, a);
   else hipLaunchKernelGGL((bwd_kernel<DQK, DV, false>), grid, dim3(C::NT), 0, s, a);
   return hipGetLastError();

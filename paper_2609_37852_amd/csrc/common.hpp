@@ -108,6 +108,31 @@ __device__ __forceinline__ float wave_max_nonneg(float v) {
   return __uint_as_float(u);
 }
 
+// Workgroup order of the attention kernels (one-dimensional grids; the
+// hardware hands out workgroups in index order, round-robin over the 8 XCDs):
+// the heaviest work items come first (longest-processing-time order), and the
+// workgroups that share a KV head land on the same XCD, i.e. the same L2.
+//   query-major kernels: id -> (rank r of the query block, heaviest first,
+//   batch b, query head h); within a rank, the query heads of one KV group
+//   get ids that are equal mod 8 whenever B * Hkv is a multiple of 8.
+struct WgCoord { int r, b, h; };
+__device__ __forceinline__ WgCoord query_major_coord(int id, int B, int Hq, int Hkv) {
+  const int BH = B * Hq, G = Hq / Hkv, GI = B * Hkv;
+  WgCoord c;
+  c.r = id / BH;
+  const int u = id % BH;
+  if (GI % 8 == 0) {
+    const int xcd = u % 8, j = u / 8;
+    const int gi = (j / G) * 8 + xcd;           // (batch, KV head) group
+    c.b = gi / Hkv;
+    c.h = (gi % Hkv) * G + j % G;
+  } else {
+    c.b = u / Hq;
+    c.h = u % Hq;
+  }
+  return c;
+}
+
 // Value of `v` in the partner lane l ^ 32.
 __device__ __forceinline__ float partner(float v) {
   Pair p = permlane32_swap(v, v);

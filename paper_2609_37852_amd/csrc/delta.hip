@@ -51,8 +51,9 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
   const int N = (int)a.N;
   const int nqb = (N + BQ - 1) / BQ;
-  const int qb = nqb - 1 - (int)blockIdx.x;    // longest causal rows first
-  const int h = blockIdx.y, b = blockIdx.z, kh = h / (int)a.G;
+  const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);
+  const int qb = nqb - 1 - wc.r;              // longest causal rows first
+  const int h = wc.h, b = wc.b, kh = h / (int)a.G;
   const int q0 = qb * BQ + 32 * w;
   const bool live = q0 < N;
   const int qi = q0 + li;
@@ -175,7 +176,7 @@ template <int DQK, int DV>
 static hipError_t delta_dispatch(const AttnArgs& a, hipStream_t s) {
   using C = DeltaCfg<DQK, DV>;
   const int64_t nqb = (a.N + C::BQ - 1) / C::BQ;
-  dim3 grid((unsigned)nqb, (unsigned)a.Hq, (unsigned)a.B);
+  const dim3 grid((unsigned)(nqb * a.Hq * a.B));
   hipLaunchKernelGGL((delta_matching_kernel<DQK, DV>), grid, dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }

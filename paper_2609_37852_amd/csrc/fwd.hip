@@ -138,8 +138,9 @@ __global__ __launch_bounds__(64 * NW, 2) void fwd_kernel(AttnArgs a) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
   const int N = (int)a.N;
   const int nqb = (N + BQ - 1) / BQ;
-  const int qb = nqb - 1 - (int)blockIdx.x;  // longest causal rows first
-  const int h = blockIdx.y, b = blockIdx.z, kh = h / (int)a.G;
+  const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);
+  const int qb = nqb - 1 - wc.r;              // longest causal rows first
+  const int h = wc.h, b = wc.b, kh = h / (int)a.G;
   const int q0 = qb * BQ + 32 * w;
   const bool live = q0 < N;
   const int qi = q0 + li;
@@ -331,7 +332,7 @@ template <int DQK, int DV>
 static hipError_t fwd_dispatch(const AttnArgs& a, hipStream_t s) {
   constexpr int NW = 4;
   const int64_t nqb = (a.N + 32 * NW - 1) / (32 * NW);
-  dim3 grid((unsigned)nqb, (unsigned)a.Hq, (unsigned)a.B);
+  const dim3 grid((unsigned)(nqb * a.Hq * a.B));
   hipLaunchKernelGGL((fwd_kernel<DQK, DV, NW>), grid, dim3(64 * NW), 0, s, a);
   return hipGetLastError();
 }
