@@ -136,18 +136,6 @@ __device__ __forceinline__ float half_max(float v) {
   return v;
 }
 
-typedef int v4i __attribute__((ext_vector_type(4)));
-
-// The four code dwords of one 32-query half from the lane's query order
-// (queries 8 g + 4 hf + e in dword g) to natural order (queries 16 hf + 4 d + e
-// in dword d): lane l < 32 receives {x_g, partner's x_g} for g = 0, 1; lane
-// l >= 32 {partner's x_g, x_g} for g = 2, 3.
-__device__ __forceinline__ v4i to_natural4(const v4i& x) {
-  const auto r0 = __builtin_amdgcn_permlane32_swap((uint32_t)x[0], (uint32_t)x[2], false, false);
-  const auto r1 = __builtin_amdgcn_permlane32_swap((uint32_t)x[1], (uint32_t)x[3], false, false);
-  return v4i{(int)r0[0], (int)r0[1], (int)r1[0], (int)r1[1]};
-}
-
 template <int DQK, int DV, bool STATS>
 __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   using C = BwdCfg<DQK, DV>;

@@ -1,28 +1,36 @@
 // Forward pass (Sec. 2.3; App. B.6.2 with power-of-two probability scales).
 //
 // Workgroup: NW waves, 32 queries each, one (batch, query head).  Key tiles of
-// BK = 128 are double-buffered in LDS (global loads for the next tile are in
-// flight while the current one is computed; one barrier per tile) and visited
-// from the causal diagonal down to key 0.
+// BK = 128 keys (64 for wide heads; K row codes [BK][Dqk], V col codes
+// [Dv][BK], their scales) reach
+// LDS by direct loads, double-buffered: the next tile streams in while the
+// current one is computed, one barrier per tile.  Tiles run from key 0 up to
+// the causal diagonal, so the workgroups of one KV head that run together
+// read the same tiles.
 //
-// Per wave and tile (4 aligned 32-key groups):
+// Per wave and tile (aligned 32-key groups, taken in 64-key halves):
 //   S^T = K Q^T       MX MFMA, A = K row tile (LDS), B = Q row codes (regs);
 //                     lane l owns query l % 32 and holds 16 keys of each
 //                     group, so row reductions are in-lane plus one exchange
 //                     with lane l ^ 32.  The isolated score channel (if any)
-//                     is added with one FMA.
+//                     is cleared in Q and its product added by one more MFMA
+//                     whose Q operand holds that channel alone.
 //   M = integer running max of x = S tau log2e (ceil of the row max).  When it
 //       grows, O and l are multiplied by 2^(M_old - M_new), an exact power of
-//       two (decided per wave; at most a few times per row).
+//       two (decided per wave).
 //   p = 2^(x - M) (FP32, before any cast) feeds l.
 //   group g: E_g = smallest integer with 2^(x_g - M) <= 448 * 2^E_g (x_g the
 //       group max), codes C8(p / 2^E_g) -- the group's probability scale.
-//   O^T += V^T P^T    MX MFMA, A = V col tile (LDS, permuted to the lane's
-//                     keys), B = probability codes straight from registers.
+//       Since M is an integer the codes equal C8(2^(x - E)) with E the
+//       group's absolute exponent, whatever the running max was.
+//   O^T += V^T P^T    MX MFMA, A = V col tile (LDS), B = probability codes
+//                     from registers, put in natural key order by one
+//                     v_permlane32_swap per dword pair.
 // Only the group holding the diagonal needs a mask; groups wholly in a wave's
 // future skip their MFMA and exponentials.
 // Epilogue: O = O_acc / l (bf16 or fp32), LSE = (M + log2 l) ln 2.
 #include "common.hpp"
+#include "dma.hpp"
 #include "kernels.hpp"
 #include "tiles.hpp"
 
@@ -30,109 +38,46 @@ namespace afp8 {
 
 constexpr float kLog2_448 = 8.807354922057604f;
 
-template <int DQK, int DV, int NW>
-struct FwdTile {
-  static constexpr int BK = 128, NT = 64 * NW;
-  static constexpr int KST = DQK + 16, VST = BK + 16;
-  static constexpr int KU = BK * DQK / 16 / NT;   // uint4 of K codes per thread
-  static constexpr int VU = DV * BK / 16 / NT;    // uint4 of V codes per thread
-  static_assert(KU * NT * 16 == BK * DQK && VU * NT * 16 == DV * BK, "tile split");
-  static_assert(DQK <= NT && DV <= NT && BK <= NT, "one scale word / hot value per thread");
+template <int DQK, int DV>
+struct FwdCfg {
+  static constexpr int NW = 4, NT = 64 * NW, BQ = 32 * NW;
+  static constexpr int al16(int x) { return (x + 15) & ~15; }
+  static constexpr int stage_bytes(int bk) { return al16(al16(bk * (DQK + DV) + bk * DQK / 32) + DV * 4); }
+  // 128-key tiles where two double-buffered workgroups fit a CU's LDS,
+  // else 64-key tiles (wide heads)
+  static constexpr int BK = 2 * stage_bytes(128) <= 80 * 1024 ? 128 : 64;
+  static constexpr int K_OFF = 0;                               // K row codes [BK][DQK], swizzled
+  static constexpr int V_OFF = K_OFF + BK * DQK;                // V col codes [DV][BK], swizzled
+  static constexpr int KS_OFF = V_OFF + DV * BK;                // K row scales [BK][DQK/32]
+  static constexpr int VS_OFF = al16(KS_OFF + BK * DQK / 32);   // V col scales [DV][4] (BK/32 used)
+  static constexpr int STAGE = al16(VS_OFF + DV * 4);
+  static_assert(STAGE == stage_bytes(BK), "stage layout");
+  static_assert(DV <= NT, "one V scale word per thread");
+  static_assert(BQ % BK == 0, "a query block's diagonal starts a key tile");
 };
 
-// Registers holding one tile in flight from global memory.
-template <int DQK, int DV, int NW>
-struct FwdPrefetch {
-  using T = FwdTile<DQK, DV, NW>;
-  uint4 k[T::KU];
-  uint4 v[T::VU];
-  uint32_t ks;     // 4 K scale bytes (thread < DQK)
-  uint32_t vs[4];  // V scale bytes of one channel, one per 32-key group (thread < DV)
-  uint32_t khc, khs;  // isolated-channel code and scale byte of one key (thread < BK)
-};
-// Only loads are issued here; everything that needs the loaded values waits
-// for fwd_store, so the loads stay in flight while the current tile is computed.
-
-template <int DQK, int DV, int NW>
-__device__ __forceinline__ void fwd_load(FwdPrefetch<DQK, DV, NW>& f, const uint8_t* kcode, const uint8_t* kscale,
-                                         const uint8_t* vcode, const uint8_t* vscale, int j0, int N, int hot) {
-  using T = FwdTile<DQK, DV, NW>;
-  const int tid = threadIdx.x;
-  // K rows [j0, j0 + BK): contiguous; rows past N read the last valid bytes
-  // (finite codes whose scores the causal mask removes)
-  const int klim = (N - j0) * DQK - 16;
-#pragma unroll
-  for (int i = 0; i < T::KU; i++) {
-    const int off = (tid + i * T::NT) * 16;
-    f.k[i] = *reinterpret_cast<const uint4*>(kcode + (size_t)j0 * DQK + (off < klim ? off : klim));
-  }
-  // V col rows: channel c, keys [j0, j0 + BK) in 16-byte pieces
-#pragma unroll
-  for (int i = 0; i < T::VU; i++) {
-    const int u = tid + i * T::NT, c = u / (T::BK / 16), q = u % (T::BK / 16);
-    const int col = j0 + q * 16 < N - 16 ? j0 + q * 16 : N - 16;
-    f.v[i] = *reinterpret_cast<const uint4*>(vcode + (size_t)c * N + col);
-  }
-  if (tid < DQK) {  // K scales: BK rows x DQK/32 bytes = DQK dwords, clamped to the head's array
-    const int off = j0 * (DQK / 32) + tid * 4, lim = N * (DQK / 32) - 4;
-    f.ks = *reinterpret_cast<const uint32_t*>(kscale + (off < lim ? off : lim));
-  }
-  if (tid < DV) {   // V scales: 4 groups of channel tid
-#pragma unroll
-    for (int g = 0; g < 4; g++) {
-      const int grp = (j0 + 32 * g < N ? j0 + 32 * g : N - 32) / 32;
-      f.vs[g] = vscale[tid * (N / 32) + grp];
-    }
-  }
-  if (tid < T::BK && hot >= 0) {
-    const int r = j0 + tid < N ? j0 + tid : N - 1;
-    f.khc = kcode[r * DQK + hot];
-    f.khs = kscale[r * (DQK / 32) + hot / 32];
+// Col-copy code tile: channels [0, D), keys [j0, j0 + 128) (clamped to the
+// sequence) into LDS [D][128] with the 128-byte row swizzle; wave w issues
+// instructions w, w + NW, ...
+template <int D, int NW>
+__device__ __forceinline__ void dma_cols128(lds8* lds, const uint8_t* code, int j0, int N, int w, int lane) {
+  constexpr int NI = D * 128 / 1024;
+  for (int k = w; k < NI; k += NW) {
+    const int off = 1024 * k + 16 * lane;
+    const int c = off / 128, p = (off % 128) / 16;
+    const int q = p ^ swz_row<128>(c);
+    const int col = j0 + 16 * q < N - 16 ? j0 + 16 * q : N - 16;
+    dma16(code + c * N + col, lds + 1024 * k);
   }
 }
 
-template <int DQK, int DV, int NW>
-__device__ __forceinline__ void fwd_store(const FwdPrefetch<DQK, DV, NW>& f, uint8_t* sK, uint8_t* sKs, uint8_t* sV,
-                                          uint8_t* sVs, float* sKh, int hot) {
-  using T = FwdTile<DQK, DV, NW>;
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int i = 0; i < T::KU; i++) {
-    const int off = (tid + i * T::NT) * 16;
-    const int r = off / DQK, c = off % DQK;
-    uint4 val = f.k[i];
-    if (hot >= c && hot < c + 16) clear_byte(val, hot - c);
-    *reinterpret_cast<uint4*>(sK + r * T::KST + c) = val;
-  }
-#pragma unroll
-  for (int i = 0; i < T::VU; i++) {
-    const int u = tid + i * T::NT, c = u / (T::BK / 16), q = u % (T::BK / 16);
-    // 16 keys 16q..16q+15: group q/2; within the group, 4-key chunks go to
-    // position 16 * (chunk & 1) + 4 * (chunk >> 1) (see stage_cols_perm)
-    // (32-bit stores: a 64-bit store of {x, z} would make the compiler pair
-    // the registers right after the load and wait for it there)
-    uint32_t* base = reinterpret_cast<uint32_t*>(sV + c * T::VST + (q >> 1) * 32 + (q & 1) * 8);
-    base[0] = f.v[i].x;
-    base[1] = f.v[i].z;
-    base[4] = f.v[i].y;
-    base[5] = f.v[i].w;
-  }
-  if (tid < DQK) *reinterpret_cast<uint32_t*>(sKs + tid * 4) = f.ks;
-  if (tid < DV)
-    *reinterpret_cast<uint32_t*>(sVs + tid * 4) = f.vs[0] | (f.vs[1] << 8) | (f.vs[2] << 16) | (f.vs[3] << 24);
-  if (tid < T::BK) sKh[tid] = hot >= 0 ? scaled_value(f.khc, f.khs) : 0.f;
-}
-
-template <int DQK, int DV, int NW>
-__global__ __launch_bounds__(64 * NW, 2) void fwd_kernel(AttnArgs a) {
-  using T = FwdTile<DQK, DV, NW>;
-  constexpr int BQ = 32 * NW, BK = T::BK;
+template <int DQK, int DV>
+__global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
+  using C = FwdCfg<DQK, DV>;
+  constexpr int NW = C::NW, BQ = C::BQ, BK = C::BK;
   constexpr int KS = DQK / 64, CB = DV / 32;
-  __shared__ __attribute__((aligned(16))) uint8_t sK[2][BK * T::KST];
-  __shared__ __attribute__((aligned(16))) uint8_t sKs[2][BK * DQK / 32];
-  __shared__ __attribute__((aligned(16))) uint8_t sV[2][DV * T::VST];
-  __shared__ __attribute__((aligned(16))) uint8_t sVs[2][DV * 4];
-  __shared__ __attribute__((aligned(16))) float sKh[2][BK];
+  __shared__ __attribute__((aligned(16))) uint8_t stA[C::STAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t stB[C::STAGE];
   __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
@@ -152,19 +97,21 @@ __global__ __launch_bounds__(64 * NW, 2) void fwd_kernel(AttnArgs a) {
   const uint8_t* vcode = a.vc_code + bhk * DV * N;
   const uint8_t* vscale = a.vc_scale + bhk * DV * (N / 32);
 
-  v8i qf[KS];
-  int qsc[KS];
-  float qhot = 0.f;
+  v8i qf[KS], qf_hot = v8i{0, 0, 0, 0, 0, 0, 0, 0};
+  int qsc[KS], qsc_hot = 0;
+  const int shot = hot >= 0 ? hot / 64 : 0;    // k-step holding the isolated channel
   {
-    const int row = live ? qi : 0;
-    const uint8_t* qrow = a.q_code + (bhq * N + row) * DQK;
+    const size_t row = bhq * N + (live ? qi : 0);
 #pragma unroll
     for (int s = 0; s < KS; s++) {
-      qf[s] = frag_rows_global(qrow, s, hf);
+      qf[s] = frag_rows_global(a.q_code + row * DQK, s, hf);
+      qsc[s] = a.q_scale[row * (DQK / 32) + 2 * s + hf];
+      if (hot >= 0 && s == shot) {
+        qf_hot = keep_channel(qf[s], s, hf, hot);
+        qsc_hot = qsc[s];
+      }
       clear_channel(qf[s], s, hf, hot);
-      qsc[s] = a.q_scale[(bhq * N + row) * (DQK / 32) + 2 * s + hf];
     }
-    if (hot >= 0) qhot = row_value<DQK>(a.q_code + bhq * N * DQK, a.q_scale + bhq * N * (DQK / 32), row, hot);
   }
 
   v16f oacc[CB];
@@ -175,127 +122,144 @@ __global__ __launch_bounds__(64 * NW, 2) void fwd_kernel(AttnArgs a) {
   float M = -__builtin_inff();
   float lsum = 0.f;
   const float c = a.c;
+  const int ntiles = (qb + 1) * (BQ / BK);     // key tiles up to the block's diagonal
 
-  const int qend = (qb + 1) * BQ < N ? (qb + 1) * BQ : N;
-  const int ntiles = (qend + BK - 1) / BK;
-  FwdPrefetch<DQK, DV, NW> pf;
-  fwd_load<DQK, DV, NW>(pf, kcode, kscale, vcode, vscale, (ntiles - 1) * BK, N, hot);
-  fwd_store<DQK, DV, NW>(pf, sK[0], sKs[0], sV[0], sVs[0], sKh[0], hot);
-  __syncthreads();
-
-  for (int it = 0; it < ntiles; it++) {
-    const int cur = it & 1;
-    const int j0 = (ntiles - 1 - it) * BK;
-    // always issue the next tile's loads (the last iteration reloads tile 0
-    // into the idle buffer): a conditional load would merge old and new
-    // register values after the branch and wait for the loads right there
-    fwd_load<DQK, DV, NW>(pf, kcode, kscale, vcode, vscale, j0 >= BK ? j0 - BK : 0, N, hot);
-
-    if (live && j0 <= q0) {
-      const uint8_t* K = sK[cur];
-      const uint8_t* Ks = sKs[cur];
-      const float* Kh = sKh[cur];
-      const uint8_t* V = sV[cur];
-      const uint8_t* Vs = sVs[cur];
-      // two 64-key halves, each: scores -> max -> rescale -> exponentials -> P V
+  // Loads of tile j0: codes and K scales straight to LDS; the V col scales
+  // (4 strided bytes per channel) through registers, written by finish().
+  uint32_t vsr[BK / 32] = {};
+  auto issue = [&](lds8* st, int j0) __attribute__((always_inline)) {
+    dma_rows<DQK, NW, BK>(st + C::K_OFF, kcode, j0, N, w, lane);
+    if constexpr (BK == 128) dma_cols128<DV, NW>(st + C::V_OFF, vcode, j0, N, w, lane);
+    else dma_cols<DV, NW>(st + C::V_OFF, vcode, j0, N, w, lane);
+    dma_row_scales<DQK, NW, BK>(st + C::KS_OFF, kscale, j0, N, w, lane, 0);
+    if (threadIdx.x < DV) {
 #pragma unroll
-      for (int hk = 0; hk < 2; hk++) {
-        if (j0 + 64 * hk > q0) break;          // both groups of this half are in the wave's future
-        v16f s[2];
-        float gm[2];
-#pragma unroll
-        for (int g2 = 0; g2 < 2; g2++) {
-          const int kb = 2 * hk + g2;
-          const int g0 = j0 + 32 * kb;         // first key of the group
-          if (g0 > q0) {                       // whole group in this wave's future
-            gm[g2] = -__builtin_inff();
-            continue;
-          }
-#pragma unroll
-          for (int r = 0; r < 16; r++) s[g2][r] = 0.f;
-#pragma unroll
-          for (int st = 0; st < KS; st++)
-            s[g2] = mfma_mx(frag_rows<T::KST>(K, 32 * kb + li, st, hf), qf[st], s[g2],
-                            Ks[(32 * kb + li) * (DQK / 32) + 2 * st + hf], qsc[st]);
-          float kh16[16];
-#pragma unroll
-          for (int g = 0; g < 4; g++) {
-            const float4 v4 = *reinterpret_cast<const float4*>(&Kh[32 * kb + 8 * g + 4 * hf]);
-            kh16[4 * g] = v4.x; kh16[4 * g + 1] = v4.y; kh16[4 * g + 2] = v4.z; kh16[4 * g + 3] = v4.w;
-          }
-          float m = -__builtin_inff();
-          if (g0 == q0) {                      // the diagonal group: key offset > query offset is masked
-#pragma unroll
-            for (int r = 0; r < 16; r++) {
-              const float t = __builtin_fmaf(qhot, kh16[r], s[g2][r]);
-              s[g2][r] = (8 * (r >> 2) + 4 * hf + (r & 3)) > li ? -__builtin_inff() : t;
-              m = fmaxf(m, s[g2][r]);
-            }
-          } else {
-#pragma unroll
-            for (int r = 0; r < 16; r++) {
-              s[g2][r] = __builtin_fmaf(qhot, kh16[r], s[g2][r]);
-              m = fmaxf(m, s[g2][r]);
-            }
-          }
-          gm[g2] = m;
-        }
-        // full group maxima (raw score units) in every lane
-        gm[0] = fmaxf(gm[0], partner(gm[0]));
-        gm[1] = fmaxf(gm[1], partner(gm[1]));
-        const float mnew = fmaxf(M, __builtin_ceilf(fmaxf(gm[0], gm[1]) * c));
-        if (M == -__builtin_inff()) {
-          M = mnew;                            // first visible keys: nothing accumulated yet
-        } else if (__any(mnew > M)) {
-          const int d = (int)(M - mnew);       // 0 for lanes whose max did not move
-          const float alpha = d < -126 ? 0.f : exp2i(d);
-          lsum *= alpha;
-#pragma unroll
-          for (int cb = 0; cb < CB; cb++)
-#pragma unroll
-            for (int r = 0; r < 16; r++) oacc[cb][r] *= alpha;
-          M = mnew;
-        }
-        const float nM = -M;
-        uint32_t codes[2][4];
-        int eg[2];
-#pragma unroll
-        for (int g2 = 0; g2 < 2; g2++) {
-          if (j0 + 32 * (2 * hk + g2) > q0) {
-#pragma unroll
-            for (int k = 0; k < 4; k++) codes[g2][k] = 0u;
-            eg[g2] = -126;
-            continue;
-          }
-          // smallest E with 2^(x_g - M) <= 448 * 2^E, kept in the normal FP32 range
-          int e = (int)__builtin_ceilf(__builtin_fmaf(gm[g2], c, nM) - kLog2_448);
-          e = e < -126 ? -126 : e;
-          eg[g2] = e;
-          const float sc = exp2i(e);
-          float p[16];
-#pragma unroll
-          for (int r = 0; r < 16; r++) {
-            p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[g2][r], c, nM));
-            lsum += p[r];
-          }
-#pragma unroll
-          for (int k = 0; k < 4; k++) codes[g2][k] = cvt4_div(p[4 * k], p[4 * k + 1], p[4 * k + 2], p[4 * k + 3], sc);
-        }
-        const v8i pfr = v8i{(int)codes[0][0], (int)codes[0][1], (int)codes[0][2], (int)codes[0][3],
-                            (int)codes[1][0], (int)codes[1][1], (int)codes[1][2], (int)codes[1][3]};
-        const int psc = (hf ? eg[1] : eg[0]) + 127;
-#pragma unroll
-        for (int cb = 0; cb < CB; cb++) {
-          const uint8_t* vp = V + (32 * cb + li) * T::VST + 64 * hk + 16 * hf;
-          const uint4 lo = *reinterpret_cast<const uint4*>(vp);
-          const uint4 hi = *reinterpret_cast<const uint4*>(vp + 32);
-          const v8i vf = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
-          oacc[cb] = mfma_mx(vf, pfr, oacc[cb], Vs[(32 * cb + li) * 4 + 2 * hk + hf], psc);
-        }
+      for (int g = 0; g < BK / 32; g++) {
+        const int grp = (j0 + 32 * g < N ? j0 + 32 * g : N - 32) / 32;
+        vsr[g] = vscale[threadIdx.x * (N / 32) + grp];
       }
     }
-    fwd_store<DQK, DV, NW>(pf, sK[cur ^ 1], sKs[cur ^ 1], sV[cur ^ 1], sVs[cur ^ 1], sKh[cur ^ 1], hot);
-    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);   // keep every load ahead of the tile's compute
+  };
+  auto finish = [&](uint8_t* st) __attribute__((always_inline)) {
+    if (threadIdx.x < DV) {
+      if constexpr (BK == 128)
+        *reinterpret_cast<uint32_t*>(st + C::VS_OFF + 4 * threadIdx.x) =
+            vsr[0] | (vsr[1] << 8) | (vsr[2] << 16) | (vsr[3] << 24);
+      else
+        *reinterpret_cast<uint16_t*>(st + C::VS_OFF + 4 * threadIdx.x) = (uint16_t)(vsr[0] | (vsr[1] << 8));
+    }
+  };
+
+  auto tile = [&](const uint8_t* st, int j0) __attribute__((always_inline)) {
+    if (!live || j0 > q0) return;
+    const uint8_t* K = st + C::K_OFF;
+    const uint8_t* Ks = st + C::KS_OFF;
+    const uint8_t* V = st + C::V_OFF;
+    const uint8_t* Vs = st + C::VS_OFF;
+#pragma unroll
+    for (int hk = 0; hk < BK / 64; hk++) {
+      if (j0 + 64 * hk > q0) break;            // both groups of this half are in the wave's future
+      v16f s[2];
+      float gm[2];
+#pragma unroll
+      for (int g2 = 0; g2 < 2; g2++) {
+        const int kb = 2 * hk + g2;
+        const int g0 = j0 + 32 * kb;           // first key of the group
+        if (g0 > q0) {                         // whole group in this wave's future
+          gm[g2] = -__builtin_inff();
+          continue;
+        }
+#pragma unroll
+        for (int r = 0; r < 16; r++) s[g2][r] = 0.f;
+#pragma unroll
+        for (int t = 0; t < KS; t++)
+          s[g2] = mfma_mx(frag_rows_swz<DQK>(K, 32 * kb + li, t, hf), qf[t], s[g2],
+                          Ks[(32 * kb + li) * (DQK / 32) + 2 * t + hf], qsc[t]);
+        if (hot >= 0)
+          s[g2] = mfma_mx(frag_rows_swz<DQK>(K, 32 * kb + li, shot, hf), qf_hot, s[g2],
+                          Ks[(32 * kb + li) * (DQK / 32) + 2 * shot + hf], qsc_hot);
+        // lane holds keys g0 + 8 (r/4) + 4 hf + r % 4 of query qi
+        float m = -__builtin_inff();
+        if (g0 == q0) {                        // the diagonal group: keys after the query are masked
+#pragma unroll
+          for (int r = 0; r < 16; r++) {
+            s[g2][r] = (8 * (r >> 2) + 4 * hf + (r & 3)) > li ? -__builtin_inff() : s[g2][r];
+            m = fmaxf(m, s[g2][r]);
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; r++) m = fmaxf(m, s[g2][r]);
+        }
+        gm[g2] = m;
+      }
+      // full group maxima (raw score units) in every lane
+      gm[0] = fmaxf(gm[0], partner(gm[0]));
+      gm[1] = fmaxf(gm[1], partner(gm[1]));
+      const float mnew = fmaxf(M, __builtin_ceilf(fmaxf(gm[0], gm[1]) * c));
+      if (M == -__builtin_inff()) {
+        M = mnew;                              // first visible keys: nothing accumulated yet
+      } else if (__any(mnew > M)) {
+        const int d = (int)(M - mnew);         // 0 for lanes whose max did not move
+        const float alpha = d < -126 ? 0.f : exp2i(d);
+        lsum *= alpha;
+#pragma unroll
+        for (int cb = 0; cb < CB; cb++)
+#pragma unroll
+          for (int r = 0; r < 16; r++) oacc[cb][r] *= alpha;
+        M = mnew;
+      }
+      const float nM = -M;
+      v4i codes[2];
+      int eg[2];
+#pragma unroll
+      for (int g2 = 0; g2 < 2; g2++) {
+        if (j0 + 32 * (2 * hk + g2) > q0) {
+          codes[g2] = v4i{0, 0, 0, 0};
+          eg[g2] = -126;
+          continue;
+        }
+        // smallest E with 2^(x_g - M) <= 448 * 2^E, kept in the normal FP32 range
+        int e = (int)__builtin_ceilf(__builtin_fmaf(gm[g2], c, nM) - kLog2_448);
+        e = e < -126 ? -126 : e;
+        eg[g2] = e;
+        const float sc = exp2i(e);
+        float p[16];
+#pragma unroll
+        for (int r = 0; r < 16; r++) {
+          p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[g2][r], c, nM));
+          lsum += p[r];
+        }
+#pragma unroll
+        for (int k = 0; k < 4; k++)
+          codes[g2][k] = (int)cvt4_div(p[4 * k], p[4 * k + 1], p[4 * k + 2], p[4 * k + 3], sc);
+        codes[g2] = to_natural4(codes[g2]);    // lane half hf: keys 16 hf .. 16 hf + 15 of the group
+      }
+      // B operand of the 64-key step: group 2 hk in bytes 0-15, group 2 hk + 1
+      // in bytes 16-31; lane half hf carries the scale of group 2 hk + hf
+      const v8i pfr = v8i{codes[0][0], codes[0][1], codes[0][2], codes[0][3],
+                          codes[1][0], codes[1][1], codes[1][2], codes[1][3]};
+      const int psc = (hf ? eg[1] : eg[0]) + 127;
+#pragma unroll
+      for (int cb = 0; cb < CB; cb++)
+        oacc[cb] = mfma_mx(frag_rows_swz<BK>(V, 32 * cb + li, hk, hf), pfr, oacc[cb],
+                           Vs[(32 * cb + li) * 4 + 2 * hk + hf], psc);
+    }
+  };
+
+  issue((lds8*)stA, 0);
+  finish(stA);
+  lds_barrier();
+  for (int t = 0; t < ntiles; t += 2) {
+    if (t + 1 < ntiles) issue((lds8*)stB, (t + 1) * BK);
+    tile(stA, t * BK);
+    if (t + 1 < ntiles) finish(stB);
+    lds_barrier();
+    if (t + 1 >= ntiles) break;
+    if (t + 2 < ntiles) issue((lds8*)stA, (t + 2) * BK);
+    tile(stB, (t + 1) * BK);
+    if (t + 2 < ntiles) finish(stA);
+    lds_barrier();
   }
   if (!live) return;
   const float l = lsum + partner(lsum);
@@ -330,10 +294,10 @@ __global__ __launch_bounds__(64 * NW, 2) void fwd_kernel(AttnArgs a) {
 
 template <int DQK, int DV>
 static hipError_t fwd_dispatch(const AttnArgs& a, hipStream_t s) {
-  constexpr int NW = 4;
-  const int64_t nqb = (a.N + 32 * NW - 1) / (32 * NW);
+  using C = FwdCfg<DQK, DV>;
+  const int64_t nqb = (a.N + C::BQ - 1) / C::BQ;
   const dim3 grid((unsigned)(nqb * a.Hq * a.B));
-  hipLaunchKernelGGL((fwd_kernel<DQK, DV, NW>), grid, dim3(64 * NW), 0, s, a);
+  hipLaunchKernelGGL((fwd_kernel<DQK, DV>), grid, dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }
 

@@ -113,6 +113,22 @@ __device__ __forceinline__ float scaled_value(uint32_t code, uint32_t scale) {
   return __builtin_ldexpf(fp8_value(code, 0), (int)(scale & 0xff) - 127);
 }
 
+// The isolated channel `hot` alone: the lane's fragment of k-step s with
+// every byte but that channel's cleared (all zero when the channel is not in
+// this k-step or not in this lane's half).  An MFMA with this operand and the
+// other operand's fragment of the same k-step adds exactly the one product
+// of the channel to each score.
+__device__ __forceinline__ v8i keep_channel(const v8i& f, int s, int hf, int hot) {
+  const int cl = hot - 64 * s;
+  v8i z = v8i{0, 0, 0, 0, 0, 0, 0, 0};
+  if (hot < 0 || cl < 0 || cl >= 64 || ((cl & 31) >> 4) != hf) return z;
+  const int t = (cl < 32 ? 0 : 16) + (cl & 15);  // byte of the fragment holding channel `hot`
+  const uint32_t m = 0xffu << (8 * (t & 3));
+#pragma unroll
+  for (int d = 0; d < 8; d++) z[d] = d == (t >> 2) ? (int)((uint32_t)f[d] & m) : 0;
+  return z;
+}
+
 // Decoded value of the element in column `col` of row `row` of a row copy.
 template <int D>
 __device__ __forceinline__ float row_value(const uint8_t* code, const uint8_t* scale, int64_t row, int col) {
@@ -147,6 +163,19 @@ __device__ __forceinline__ int select_hot_channel(const float* q_amax, const flo
   }
   __syncthreads();
   return *slot;
+}
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// The four code dwords a lane holds for one 32-wide block of an MFMA result
+// (rows 8 g + 4 hf + e in dword g, e < 4) put in natural order (rows
+// 16 hf + 4 d + e in dword d), as an MFMA operand wants them: lane l < 32
+// receives {x_g, partner's x_g} for g = 0, 1; lane l >= 32 {partner's x_g, x_g}
+// for g = 2, 3.
+__device__ __forceinline__ v4i to_natural4(const v4i& x) {
+  const auto r0 = __builtin_amdgcn_permlane32_swap((uint32_t)x[0], (uint32_t)x[2], false, false);
+  const auto r1 = __builtin_amdgcn_permlane32_swap((uint32_t)x[1], (uint32_t)x[3], false, false);
+  return v4i{(int)r0[0], (int)r0[1], (int)r1[0], (int)r1[1]};
 }
 
 }  // namespace afp8
