@@ -18,7 +18,9 @@
 //   S  = Q K^T, dP = dO V^T   MX MFMA (A = Q / dO row tiles in LDS, B = the
 //                             wave's K / V row codes in registers); lane l
 //                             owns key l % 32 and holds 16 queries.
-//   P  = bwd_prob(S + q_c* k_c*), dS = P ((dP - hi) - lo).
+//   S' = S + q_c* k_c* - LSE / tau and dP' = (dP - hi) - lo by one FP32
+//        rank-2 MFMA each (the per-query values come from the records);
+//   P  = bwd_prob(S') = 2^(tau log2e S'), dS = P dP'.
 //   P' = C8(256 P) with scale 2^-8;  dS' = C8(dS / 2^e) with one exponent e
 //        per aligned 32x32 block (the wave's 32 keys x 32 queries).
 //   dV += P'^T dO_col,  dK += dS'^T Q_col   (A = the codes after one
@@ -34,8 +36,9 @@
 //
 // A preparation kernel packs what the tile loop needs besides the code tiles
 // into arrays it can stream with the same direct loads: one 16-byte record
-// per query (LSE log2 e, delta hi, delta lo, isolated-channel query value)
-// and, per 64-query tile, the col-copy scales of Q and dO.
+// per query (isolated-channel query value, -delta hi, -LSE / tau, -delta lo:
+// a lane of half hf reads the pair at 8 hf, the A operands of the two rank-2
+// updates) and, per 64-query tile, the col-copy scales of Q and dO.
 #include <type_traits>
 
 #include "common.hpp"
@@ -47,29 +50,32 @@ namespace afp8 {
 
 template <int DQK, int DV>
 struct BwdCfg {
-  // 8 waves: 4 blocks of 32 keys x 2 query sub-blocks.  The two waves of a
-  // key block (w and w + 4, on one SIMD) each compute S, dP, P and dS for one
+  // 8 waves: 4 blocks of 32 keys x 2 query halves.  The two waves of a key
+  // block (w and w + 4, on one SIMD) each compute S, dP, P and dS for one
   // 32-query half of the tile; after exchanging codes through LDS the first
   // accumulates dV and the second dK for all channels of their keys.
   static constexpr int NWK = 8, KBW = 4;
-  // stage buffers: two (loads of the next tile overlap the current one)
-  // except at d = 256, where one buffer fills the LDS
-  static constexpr int NBUF = (DQK + DV <= 320) ? 2 : 1;
   static constexpr int NT = 64 * NWK, BKB = 32 * KBW, BQ = 64;
   static constexpr int DST = BQ + 16;   // row stride of the dS' tile [key][query]
   static constexpr int al16(int x) { return (x + 15) & ~15; }
-  // one stage buffer: the query tile's operands, 16-byte aligned parts
+  // row part of a query tile (operands of S and dP, the per-query records)
   static constexpr int Q_OFF = 0;                                   // Q row codes [BQ][DQK], swizzled
   static constexpr int O_OFF = Q_OFF + BQ * DQK;                    // dO row codes [BQ][DV], swizzled
-  static constexpr int QC_OFF = O_OFF + BQ * DV;                    // Q col codes [DQK][BQ], swizzled
-  static constexpr int OC_OFF = QC_OFF + DQK * BQ;                  // dO col codes [DV][BQ], swizzled
-  static constexpr int QS_OFF = OC_OFF + DV * BQ;                   // Q row scales [BQ][DQK/32]
+  static constexpr int QS_OFF = O_OFF + BQ * DV;                    // Q row scales [BQ][DQK/32]
   static constexpr int OS_OFF = al16(QS_OFF + BQ * DQK / 32);       // dO row scales [BQ][DV/32]
-  static constexpr int QCS_OFF = al16(OS_OFF + BQ * DV / 32);       // Q col scales [DQK][2]
+  static constexpr int ROW_OFF = al16(OS_OFF + BQ * DV / 32);       // per-query records [BQ] x 16 B
+  static constexpr int RSTAGE = ROW_OFF + BQ * 16;
+  // col part (operands of dV and dK)
+  static constexpr int QC_OFF = 0;                                  // Q col codes [DQK][BQ], swizzled
+  static constexpr int OC_OFF = QC_OFF + DQK * BQ;                  // dO col codes [DV][BQ], swizzled
+  static constexpr int QCS_OFF = OC_OFF + DV * BQ;                  // Q col scales [DQK][2]
   static constexpr int OCS_OFF = QCS_OFF + DQK * 2;                 // dO col scales [DV][2]
   static constexpr int CS_BYTES = 2 * (DQK + DV);                   // both, as packed per tile by bwd_prep
-  static constexpr int ROW_OFF = al16(OCS_OFF + DV * 2);            // per-query records [BQ] x 16 B
-  static constexpr int STAGE = ROW_OFF + BQ * 16;
+  static constexpr int CSTAGE = al16(QCS_OFF + CS_BYTES);
+  // dS' tiles, exponents and code exchange, two of each
+  static constexpr int FIXED = 2 * (BKB * DST + KBW * 2 + 2 * KBW * 64 * 16);
+  // row parts are double-buffered; col parts too where the LDS allows
+  static constexpr int NCB = 2 * RSTAGE + 2 * CSTAGE + FIXED <= 156 * 1024 ? 2 : 1;
 };
 
 // dQ operand units of one head before query block q (block q has q/2 + 1
@@ -99,29 +105,37 @@ __device__ __forceinline__ BwdHead bwd_head(const AttnArgs& a, size_t bh, int N)
   return p;
 }
 
-// Issues every load of one query tile, all direct-to-LDS: codes, row scales,
-// the col scales packed per tile by bwd_prep and the per-query records.
+// Direct-to-LDS loads of the row part of one query tile: codes, row scales
+// and the per-query records.
 template <int DQK, int DV>
-__device__ __forceinline__ void stage_issue(lds8* st, const BwdHead& hp, int i0, int N) {
+__device__ __forceinline__ void stage_rows(lds8* st, const BwdHead& hp, int i0, int N) {
   using C = BwdCfg<DQK, DV>;
   constexpr int NWK = C::NWK;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   dma_rows<DQK, NWK>(st + C::Q_OFF, hp.qrow, i0, N, w, lane);
   dma_rows<DV, NWK>(st + C::O_OFF, hp.orow, i0, N, w, lane);
-  dma_cols<DQK, NWK>(st + C::QC_OFF, hp.qcol, i0, N, w, lane);
-  dma_cols<DV, NWK>(st + C::OC_OFF, hp.ocol, i0, N, w, lane);
   dma_row_scales<DQK, NWK>(st + C::QS_OFF, hp.qsc, i0, N, w, lane, 0);
   dma_row_scales<DV, NWK>(st + C::OS_OFF, hp.osc, i0, N, w, lane, 1);
-  constexpr int NCI = (C::CS_BYTES + 255) / 256;
-  const uint8_t* tcs = hp.tcs + (i0 / 64) * C::CS_BYTES;
-  for (int k = 0; k < NCI; k++) {
-    if ((2 + k) % NWK != w) continue;
-    const int off = 256 * k + 4 * lane;
-    if (off < C::CS_BYTES) dma4(tcs + off, st + C::QCS_OFF + 256 * k);
-  }
   if (w == (3 % NWK)) {
     const int r = i0 + lane < N ? i0 + lane : N - 1;
     dma16(hp.rows + r, st + C::ROW_OFF);
+  }
+}
+
+// ... and of its col part: codes and the col scales packed by bwd_prep.
+template <int DQK, int DV>
+__device__ __forceinline__ void stage_cols(lds8* st, const BwdHead& hp, int i0, int N) {
+  using C = BwdCfg<DQK, DV>;
+  constexpr int NWK = C::NWK;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  dma_cols<DQK, NWK>(st + C::QC_OFF, hp.qcol, i0, N, w, lane);
+  dma_cols<DV, NWK>(st + C::OC_OFF, hp.ocol, i0, N, w, lane);
+  constexpr int NCI = (C::CS_BYTES + 255) / 256;
+  const uint8_t* tcs = hp.tcs + (i0 / 64) * C::CS_BYTES;
+  for (int k = 0; k < NCI; k++) {
+    if ((4 + k) % NWK != w) continue;
+    const int off = 256 * k + 4 * lane;
+    if (off < C::CS_BYTES) dma4(tcs + off, st + C::QCS_OFF + 256 * k);
   }
 }
 
@@ -136,23 +150,39 @@ __device__ __forceinline__ float half_max(float v) {
   return v;
 }
 
+// Position of a query tile in the workgroup's loop: query head kh G + hi,
+// 64 queries from (nqt - 1 - r) * 64.  The loop runs r from the end of the
+// sequence down to the diagonal and, for each r, over the G query heads, so
+// every workgroup of one KV head (they start together) visits the same
+// (r, hi) sequence and stops at its own diagonal: the workgroups stay in
+// step and share each query tile in the L2.
+struct TilePos {
+  int hi, r;
+};
+__device__ __forceinline__ TilePos next_pos(TilePos p, int G) {
+  return p.hi + 1 < G ? TilePos{p.hi + 1, p.r} : TilePos{0, p.r + 1};
+}
+
 template <int DQK, int DV, bool STATS>
 __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   using C = BwdCfg<DQK, DV>;
-  constexpr int KBW = C::KBW, BKB = C::BKB, BQ = C::BQ;
+  constexpr int KBW = C::KBW, BKB = C::BKB, BQ = C::BQ, NCB = C::NCB;
   constexpr int KS = DQK / 64, VS = DV / 64, CK = DQK / 32, CV = DV / 32;
   constexpr int CMAX = CK > CV ? CK : CV;
-  // two stage buffers and two dS buffers as distinct objects, so the
-  // compiler can tell loads into one from reads of the other
-  __shared__ __attribute__((aligned(16))) uint8_t stA[C::STAGE];
-  __shared__ __attribute__((aligned(16))) uint8_t stB[C::NBUF == 2 ? C::STAGE : 16];
+  // every buffer that alternates between tiles is two distinct objects, so
+  // the compiler can tell loads into one from reads of the other
+  __shared__ __attribute__((aligned(16))) uint8_t rA[C::RSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t rB[C::RSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t cA[C::CSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t cB[NCB == 2 ? C::CSTAGE : 16];
   __shared__ __attribute__((aligned(16))) uint8_t dsA[BKB * C::DST];
   __shared__ __attribute__((aligned(16))) uint8_t dsB[BKB * C::DST];
   __shared__ __attribute__((aligned(16))) uint8_t esA[KBW * 2];
   __shared__ __attribute__((aligned(16))) uint8_t esB[KBW * 2];
   // code exchange within a key block, 16 bytes per lane in natural query
   // order: [0] dS' of the first half (for dK), [1] P' of the second (for dV)
-  __shared__ __attribute__((aligned(16))) uint4 xch[2][KBW * 64];
+  __shared__ __attribute__((aligned(16))) uint4 xA[2][KBW * 64];
+  __shared__ __attribute__((aligned(16))) uint4 xB[2][KBW * 64];
   __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
@@ -173,10 +203,12 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   const int Hq = (int)a.Hq, G = (int)a.G;
   const float c = a.c;
 
-  // K and V row codes of this lane's key (B operands of S and dP)
+  // K and V row codes of this lane's key (B operands of S and dP); kb: B
+  // operand of the score's rank-2 update (isolated-channel key value, or 1 in
+  // lanes >= 32)
   v8i kf[KS], vf[VS];
   int ksc[KS], vsc[VS];
-  float khot = 0.f;
+  float kb = 1.0f;
   {
     const int row = live ? kj : 0;
     const uint8_t* kr = a.k_code + (bhk * N + row) * DQK;
@@ -192,7 +224,8 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
       vf[s] = frag_rows_global(vr, s, hf);
       vsc[s] = a.v_scale[(bhk * N + row) * (DV / 32) + 2 * s + hf];
     }
-    if (hot >= 0) khot = row_value<DQK>(a.k_code + bhk * N * DQK, a.k_scale + bhk * N * (DQK / 32), row, hot);
+    if (hf == 0)
+      kb = hot >= 0 ? row_value<DQK>(a.k_code + bhk * N * DQK, a.k_scale + bhk * N * (DQK / 32), row, hot) : 0.f;
   }
 
   // dV (first half, CV blocks) or dK (second half, CK blocks) of the wave's keys
@@ -205,24 +238,161 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   const int nqt = (N + BQ - 1) / BQ, qt0 = kb0 / BQ, nq = nqt - qt0;
   const int total = G * nq;
   const size_t bh0 = (size_t)b * Hq + (size_t)kh * G;   // first query head of the group
-
-  // tile t: query head kh G + t / nq, 64 queries from tile_q0(t); within a
-  // head the tiles run from the end of the sequence down to the diagonal, so
-  // the workgroups of one KV head (which all start together) read the same
-  // query tiles at about the same time and share them in the caches
-  auto tile_q0 = [&](int t) __attribute__((always_inline)) { return (nqt - 1 - t % nq) * BQ; };
-  stage_issue<DQK, DV>((lds8*)stA, bwd_head<DQK, DV>(a, bh0, N), tile_q0(0), N);
-  lds_barrier();
-
   const int64_t units_per_head = tri_units(N / 32);
+  auto q0_of = [&](TilePos p) __attribute__((always_inline)) { return (nqt - 1 - p.r) * BQ; };
+  auto head_of = [&](TilePos p) __attribute__((always_inline)) { return bwd_head<DQK, DV>(a, bh0 + p.hi, N); };
 
-  // dQ operand units of tile t (its dS' codes and exponents in ds / es): unit
-  // (query half uq, key step ks) holds 32 queries x 64 keys; units wholly in
-  // the future of their queries do not exist
-  auto ds_store = [&](const int t, const uint8_t* ds, const uint8_t* es) __attribute__((always_inline)) {
+  // Pipeline, per tile i (each step a function of the buffers it touches):
+  //   barrier (codes of tile i exchanged, loads of rows i+1 and cols i landed)
+  //   loads: rows of tile i+2, cols of tile i+1
+  //   MFMA:  S, dP of tile i+1;  dV or dK of tile i
+  //   store: dQ units of tile i
+  //   VALU:  P, dS and codes of tile i+1 (overlapping the MFMAs above)
+  v16f s, dp;
+  v4i pn = v4i{0, 0, 0, 0}, dn = v4i{0, 0, 0, 0};   // this half's P' / dS' codes, natural query order
+  int e = -127;                                      // and the dS' block exponent
+
+  // S and dP of one tile's half (skipped halves: no MFMA, zero codes later)
+  auto sdp = [&](const uint8_t* R, bool skip) __attribute__((always_inline)) {
+    if (skip) return;
+    const uint8_t* Q = R + C::Q_OFF;
+    const uint8_t* Qs = R + C::QS_OFF;
+    const uint8_t* O = R + C::O_OFF;
+    const uint8_t* Os = R + C::OS_OFF;
+#pragma unroll
+    for (int r = 0; r < 16; r++) { s[r] = 0.f; dp[r] = 0.f; }
+#pragma unroll
+    for (int t2 = 0; t2 < KS; t2++)
+      s = mfma_mx(frag_rows_swz<DQK>(Q, 32 * qs + li, t2, hf), kf[t2], s,
+                  Qs[(32 * qs + li) * (DQK / 32) + 2 * t2 + hf], ksc[t2]);
+#pragma unroll
+    for (int t2 = 0; t2 < VS; t2++)
+      dp = mfma_mx(frag_rows_swz<DV>(O, 32 * qs + li, t2, hf), vf[t2], dp,
+                   Os[(32 * qs + li) * (DV / 32) + 2 * t2 + hf], vsc[t2]);
+    // per-query shifts: S += q_c* k_c*, then -LSE / tau; dP -= hi, then lo
+    const float2 rec = *reinterpret_cast<const float2*>(R + C::ROW_OFF + (32 * qs + li) * 16 + 8 * hf);
+    s = rank2_update(rec.x, kb, s);
+    dp = rank2_update(rec.y, 1.0f, dp);
+  };
+
+  // P, dS and their codes from the shifted s, dp; EDGE tiles may skip the
+  // half or hold the diagonal block (masked)
+  auto probs = [&](auto edge_tag, int qb, bool skip, int h) __attribute__((always_inline)) {
+    constexpr bool EDGE = decltype(edge_tag)::value;
+    v4i pc, dc;
+    e = -127;
+    if (EDGE && skip) {
+      pn = v4i{0, 0, 0, 0};
+      dn = v4i{0, 0, 0, 0};
+      return;
+    }
+    // lane holds queries qb + 8 g + 4 hf + e4 (accumulator r = 4 g + e4)
+    float amax = 0.f;
+#pragma unroll
+    for (int g = 0; g < 4; g++) {
+#pragma unroll
+      for (int e4 = 0; e4 < 4; e4++) {
+        const int r = 4 * g + e4;
+        float p = bwd_prob(s[r], c);
+        if (EDGE && qb == kw0) p = (li > 8 * g + 4 * hf + e4) ? 0.f : p;   // diagonal block: key > query
+        s[r] = p;
+        dp[r] = p * dp[r];
+        amax = fmaxf(amax, fabsf(dp[r]));
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 4; k++)
+      pc[k] = (int)cvt4_div(s[4 * k], s[4 * k + 1], s[4 * k + 2], s[4 * k + 3], 0.00390625f);
+    e = pow2_exponent(wave_max_nonneg(amax));
+    e = e < -126 ? -126 : e;
+    const float sc = exp2i(e);
+#pragma unroll
+    for (int k = 0; k < 4; k++)
+      dc[k] = (int)cvt4_div(dp[4 * k], dp[4 * k + 1], dp[4 * k + 2], dp[4 * k + 3], sc);
+    if constexpr (STATS) {
+      // per query row: FP64 sums over this wave's 32 keys, then atomics
+#pragma unroll
+      for (int r = 0; r < 16; r++) {
+        const float cast = fp8_value((uint32_t)dc[r >> 2], r & 3) * sc;
+        const double s0 = half_sum_d((double)dp[r]);
+        const double s1 = half_sum_d((double)fabsf(dp[r]));
+        const double s2 = half_sum_d((double)cast);
+        const float mx = half_max(fabsf(dp[r]));
+        const int qi = qb + 8 * (r >> 2) + 4 * hf + (r & 3);
+        if (li == 0) {
+          double* sp = a.rowstats + (((size_t)b * Hq + h) * N + qi) * 4;
+          atomicAdd(sp + 0, s0);
+          atomicAdd(sp + 1, s1);
+          atomicAdd(sp + 2, s2);
+          atomicMax(reinterpret_cast<unsigned long long*>(sp + 3),
+                    (unsigned long long)__double_as_longlong((double)mx));
+        }
+      }
+    }
+    // natural query order: lane hf holds queries 16 hf .. 16 hf + 15 of the half
+    pn = to_natural4(pc);
+    dn = to_natural4(dc);
+  };
+
+  // P, dS and codes of the tile at p for this wave's half, written to ds / es / x
+  auto front_vals = [&](TilePos p, uint8_t* ds, uint8_t* es, uint4 (*x)[KBW * 64])
+      __attribute__((always_inline)) {
+    const int i0 = q0_of(p);
+    const int qb = i0 + 32 * qs;
+    const bool full = i0 >= kb0 + BKB && i0 + BQ <= N;
+    const bool skip = !full && (!live || qb < kw0 || qb >= N);
+    const int h = kh * G + p.hi;
+    if (full) probs(std::false_type{}, qb, skip, h);
+    else probs(std::true_type{}, qb, skip, h);
+    // dS' codes for the dQ units and the exchange with the other half
+    *reinterpret_cast<uint4*>(ds + (32 * kbw + li) * C::DST + 32 * qs + 16 * hf) =
+        make_uint4((uint32_t)dn[0], (uint32_t)dn[1], (uint32_t)dn[2], (uint32_t)dn[3]);
+    if (lane == 0) es[kbw * 2 + qs] = (uint8_t)(e + 127);
+    const v4i xv = qs == 0 ? dn : pn;
+    x[qs][kbw * 64 + lane] = make_uint4((uint32_t)xv[0], (uint32_t)xv[1], (uint32_t)xv[2], (uint32_t)xv[3]);
+  };
+  auto front_skip = [&](TilePos p) __attribute__((always_inline)) {
+    const int i0 = q0_of(p);
+    const int qb = i0 + 32 * qs;
+    const bool full = i0 >= kb0 + BKB && i0 + BQ <= N;
+    return !full && (!live || qb < kw0 || qb >= N);
+  };
+
+  // dV += P'^T dO_col (first half) or dK += dS'^T Q_col (second half); k =
+  // the tile's 64 queries, bytes 0..15 from the first half, 16..31 from the
+  // second (skipped halves have zero codes)
+  auto back = [&](const uint8_t* Cc, const uint8_t* es, uint4 (*x)[KBW * 64]) __attribute__((always_inline)) {
+    if (qs == 0) {
+      const uint4 o = x[1][kbw * 64 + lane];
+      const v8i A = v8i{pn[0], pn[1], pn[2], pn[3], (int)o.x, (int)o.y, (int)o.z, (int)o.w};
+      const uint8_t* Oc = Cc + C::OC_OFF;
+      const uint8_t* Ocs = Cc + C::OCS_OFF;
+#pragma unroll
+      for (int i = 0; i < CV; i++) {
+        const int ch = 32 * i + li;
+        acc[i] = mfma_mx(A, frag_cols_swz(Oc, ch, hf), acc[i], 127 - 8, Ocs[ch * 2 + hf]);
+      }
+    } else {
+      const uint4 o = x[0][kbw * 64 + lane];
+      const v8i A = v8i{(int)o.x, (int)o.y, (int)o.z, (int)o.w, dn[0], dn[1], dn[2], dn[3]};
+      const int dascale = hf ? e + 127 : (int)es[kbw * 2];
+      const uint8_t* Qc = Cc + C::QC_OFF;
+      const uint8_t* Qcs = Cc + C::QCS_OFF;
+#pragma unroll
+      for (int i = 0; i < CK; i++) {
+        const int ch = 32 * i + li;
+        acc[i] = mfma_mx(A, frag_cols_swz(Qc, ch, hf), acc[i], dascale, Qcs[ch * 2 + hf]);
+      }
+    }
+  };
+
+  // dQ operand units of the tile at p (its dS' codes and exponents in ds /
+  // es): unit (query half uq, key step ks) holds 32 queries x 64 keys; units
+  // wholly in the future of their queries do not exist
+  auto ds_store = [&](TilePos p, const uint8_t* ds, const uint8_t* es) __attribute__((always_inline)) {
     constexpr int KSN = BKB / 64;
-    const int h = kh * G + t / nq;
-    const int i0 = tile_q0(t);
+    const int h = kh * G + p.hi;
+    const int i0 = q0_of(p);
     if (w >= 2 * KSN) return;
     const int uq = w / KSN, ks = w % KSN;
     const int qb = i0 + 32 * uq;
@@ -240,161 +410,69 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
       af[2 * part + 1] = tv[1];
     }
     const int64_t unit = ((int64_t)b * Hq + h) * units_per_head + tri_units(qb / 32) + (kb0 + 64 * ks) / 64;
-    uint4* dst = reinterpret_cast<uint4*>(a.ds_units + unit * 2048 + 32 * lane);
-    dst[0] = make_uint4((uint32_t)af[0], (uint32_t)af[1], (uint32_t)af[2], (uint32_t)af[3]);
-    dst[1] = make_uint4((uint32_t)af[4], (uint32_t)af[5], (uint32_t)af[6], (uint32_t)af[7]);
+    // streamed past the caches: the units are read once, by dq_kernel, and
+    // must not evict the query tiles the workgroups share
+    v4i* dst = reinterpret_cast<v4i*>(a.ds_units + unit * 2048 + 32 * lane);
+    __builtin_nontemporal_store(v4i{af[0], af[1], af[2], af[3]}, dst);
+    __builtin_nontemporal_store(v4i{af[4], af[5], af[6], af[7]}, dst + 1);
     if (lane == 0) {
       const uint32_t e2 = (uint32_t)es[(2 * ks) * 2 + uq] | ((uint32_t)es[(2 * ks + 1) * 2 + uq] << 8);
       *reinterpret_cast<uint16_t*>(a.ds_exp + unit * 2) = (uint16_t)e2;
     }
   };
 
-  // one tile: dQ units of the previous tile, loads of the next, compute of this one
-  auto body = [&](const int t, const uint8_t* cur, lds8* nxt3, uint8_t* ds, uint8_t* es, const uint8_t* ds_prev,
-                  const uint8_t* es_prev) __attribute__((always_inline)) {
-    if (t > 0) ds_store(t - 1, ds_prev, es_prev);
-    const bool more = t + 1 < total;
-    if constexpr (C::NBUF == 2) {
-      if (more) stage_issue<DQK, DV>(nxt3, bwd_head<DQK, DV>(a, bh0 + (t + 1) / nq, N), tile_q0(t + 1), N);
-    }
-
-    const int h = kh * G + t / nq;
-    const int i0 = tile_q0(t);
-    const int qb = i0 + 32 * qs;                 // first query of this wave's half
-    const uint8_t* Q = cur + C::Q_OFF;
-    const uint8_t* Qs = cur + C::QS_OFF;
-    const uint8_t* O = cur + C::O_OFF;
-    const uint8_t* Os = cur + C::OS_OFF;
-    const float4* Row = reinterpret_cast<const float4*>(cur + C::ROW_OFF);
-    v4i pc, dc;          // P' and dS' codes of the half, the lane's query order
-    int e = -127;
-    // tiles wholly after the workgroup's keys and inside the sequence: no
-    // mask, no skipped half
-    const bool full = i0 >= kb0 + BKB && i0 + BQ <= N;
-
-    auto half = [&](auto edge_tag) __attribute__((always_inline)) {
-      constexpr bool EDGE = decltype(edge_tag)::value;
-      if (EDGE && (!live || qb < kw0 || qb >= N)) {
-        pc = v4i{0, 0, 0, 0};
-        dc = v4i{0, 0, 0, 0};
-        return;
-      }
-      v16f s, dp;
-#pragma unroll
-      for (int r = 0; r < 16; r++) { s[r] = 0.f; dp[r] = 0.f; }
-#pragma unroll
-      for (int t2 = 0; t2 < KS; t2++)
-        s = mfma_mx(frag_rows_swz<DQK>(Q, 32 * qs + li, t2, hf), kf[t2], s,
-                    Qs[(32 * qs + li) * (DQK / 32) + 2 * t2 + hf], ksc[t2]);
-#pragma unroll
-      for (int t2 = 0; t2 < VS; t2++)
-        dp = mfma_mx(frag_rows_swz<DV>(O, 32 * qs + li, t2, hf), vf[t2], dp,
-                     Os[(32 * qs + li) * (DV / 32) + 2 * t2 + hf], vsc[t2]);
-      // lane holds queries qb + 8 g + 4 hf + e4 (accumulator r = 4 g + e4)
-      float amax = 0.f;
-#pragma unroll
-      for (int g = 0; g < 4; g++) {
-#pragma unroll
-        for (int e4 = 0; e4 < 4; e4++) {
-          const int r = 4 * g + e4;
-          const float4 rv = Row[32 * qs + 8 * g + 4 * hf + e4];   // L log2 e, delta hi, delta lo, q_c*
-          float p = bwd_prob(__builtin_fmaf(rv.w, khot, s[r]), c, rv.x);
-          if (EDGE && qb == kw0) p = (li > 8 * g + 4 * hf + e4) ? 0.f : p;   // diagonal block: key > query
-          s[r] = p;
-          dp[r] = p * ((dp[r] - rv.y) - rv.z);
-          amax = fmaxf(amax, fabsf(dp[r]));
-        }
-      }
-#pragma unroll
-      for (int k = 0; k < 4; k++)
-        pc[k] = (int)cvt4_div(s[4 * k], s[4 * k + 1], s[4 * k + 2], s[4 * k + 3], 0.00390625f);
-      e = pow2_exponent(wave_max_nonneg(amax));
-      e = e < -126 ? -126 : e;
-      const float sc = exp2i(e);
-#pragma unroll
-      for (int k = 0; k < 4; k++)
-        dc[k] = (int)cvt4_div(dp[4 * k], dp[4 * k + 1], dp[4 * k + 2], dp[4 * k + 3], sc);
-      if constexpr (STATS) {
-        // per query row: FP64 sums over this wave's 32 keys, then atomics
-#pragma unroll
-        for (int r = 0; r < 16; r++) {
-          const float cast = fp8_value((uint32_t)dc[r >> 2], r & 3) * sc;
-          const double s0 = half_sum_d((double)dp[r]);
-          const double s1 = half_sum_d((double)fabsf(dp[r]));
-          const double s2 = half_sum_d((double)cast);
-          const float mx = half_max(fabsf(dp[r]));
-          const int qi = qb + 8 * (r >> 2) + 4 * hf + (r & 3);
-          if (li == 0) {
-            double* sp = a.rowstats + (((size_t)b * Hq + h) * N + qi) * 4;
-            atomicAdd(sp + 0, s0);
-            atomicAdd(sp + 1, s1);
-            atomicAdd(sp + 2, s2);
-            atomicMax(reinterpret_cast<unsigned long long*>(sp + 3),
-                      (unsigned long long)__double_as_longlong((double)mx));
-          }
-        }
-      }
-    };
-    if (full) half(std::false_type{});
-    else half(std::true_type{});
-
-    // natural query order: lane hf holds queries 16 hf .. 16 hf + 15 of the half
-    const v4i pn = to_natural4(pc), dn = to_natural4(dc);
-    // dS' codes for the dQ units and the exchange with the other half
-    *reinterpret_cast<uint4*>(ds + (32 * kbw + li) * C::DST + 32 * qs + 16 * hf) =
-        make_uint4((uint32_t)dn[0], (uint32_t)dn[1], (uint32_t)dn[2], (uint32_t)dn[3]);
-    if (lane == 0) es[kbw * 2 + qs] = (uint8_t)(e + 127);
-    {
-      const v4i x = qs == 0 ? dn : pn;
-      xch[qs][kbw * 64 + lane] = make_uint4((uint32_t)x[0], (uint32_t)x[1], (uint32_t)x[2], (uint32_t)x[3]);
-    }
-    lds_sync();
-    // dV += P'^T dO_col (first half) or dK += dS'^T Q_col (second half); k =
-    // the tile's 64 queries, bytes 0..15 from the first half, 16..31 from the
-    // second (skipped halves have zero codes)
-    if (qs == 0) {
-      const uint4 o = xch[1][kbw * 64 + lane];
-      const v8i A = v8i{pn[0], pn[1], pn[2], pn[3], (int)o.x, (int)o.y, (int)o.z, (int)o.w};
-      const uint8_t* Oc = cur + C::OC_OFF;
-      const uint8_t* Ocs = cur + C::OCS_OFF;
-#pragma unroll
-      for (int i = 0; i < CV; i++) {
-        const int ch = 32 * i + li;
-        acc[i] = mfma_mx(A, frag_cols_swz(Oc, ch, hf), acc[i], 127 - 8, Ocs[ch * 2 + hf]);
-      }
-    } else {
-      const uint4 o = xch[0][kbw * 64 + lane];
-      const v8i A = v8i{(int)o.x, (int)o.y, (int)o.z, (int)o.w, dn[0], dn[1], dn[2], dn[3]};
-      const int dascale = hf ? e + 127 : (int)es[kbw * 2];
-      const uint8_t* Qc = cur + C::QC_OFF;
-      const uint8_t* Qcs = cur + C::QCS_OFF;
-#pragma unroll
-      for (int i = 0; i < CK; i++) {
-        const int ch = 32 * i + li;
-        acc[i] = mfma_mx(A, frag_cols_swz(Qc, ch, hf), acc[i], dascale, Qcs[ch * 2 + hf]);
-      }
-    }
+  // one step of the pipeline for tile i at position p (p1, p2: tiles i+1,
+  // i+2); R1: rows of tile i+1, Rl: buffer for the rows of tile i+2, Cc:
+  // cols of tile i, Cl: buffer for the cols of tile i+1 (Cc itself with one
+  // col buffer, after a barrier)
+  auto body = [&](int i, TilePos p, TilePos p1, TilePos p2, const uint8_t* R1, lds8* Rl, const uint8_t* Cc, lds8* Cl,
+                  const uint8_t* ds, const uint8_t* es, uint4 (*x)[KBW * 64], uint8_t* ds1, uint8_t* es1,
+                  uint4 (*x1)[KBW * 64]) __attribute__((always_inline)) {
     lds_barrier();
-    if constexpr (C::NBUF == 1) {
-      // one buffer: the next tile is loaded once every wave is done with it
-      if (more) {
-        stage_issue<DQK, DV>(nxt3, bwd_head<DQK, DV>(a, bh0 + (t + 1) / nq, N), tile_q0(t + 1), N);
-        lds_barrier();
-      }
+    const bool more = i + 1 < total;
+    if constexpr (NCB == 2) {
+      if (more) stage_cols<DQK, DV>(Cl, head_of(p1), q0_of(p1), N);
     }
+    if (i + 2 < total) stage_rows<DQK, DV>(Rl, head_of(p2), q0_of(p2), N);
+    const bool skip1 = front_skip(p1);
+    if (more) sdp(R1, skip1);
+    back(Cc, es, x);
+    __builtin_amdgcn_sched_barrier(0);   // both MFMA groups issue before the VALU work below
+    if constexpr (NCB == 1) {
+      lds_sync();                          // every wave has read the col operands of tile i
+      if (more) stage_cols<DQK, DV>(Cl, head_of(p1), q0_of(p1), N);
+    }
+    ds_store(p, ds, es);
+    if (more) front_vals(p1, ds1, es1, x1);
   };
 
-  for (int t = 0; t < total; t += 2) {
-    if constexpr (C::NBUF == 2) {
-      body(t, stA, (lds8*)stB, dsA, esA, dsB, esB);
-      if (t + 1 < total) body(t + 1, stB, (lds8*)stA, dsB, esB, dsA, esA);
+  // prologue: rows of tiles 0 and 1, cols of tile 0; S, dP, P, dS of tile 0
+  const TilePos p0 = TilePos{0, 0};
+  stage_rows<DQK, DV>((lds8*)rA, head_of(p0), q0_of(p0), N);
+  stage_cols<DQK, DV>((lds8*)cA, head_of(p0), q0_of(p0), N);
+  TilePos pa = next_pos(p0, G);
+  if (total > 1) stage_rows<DQK, DV>((lds8*)rB, head_of(pa), q0_of(pa), N);
+  lds_barrier();
+  sdp(rA, front_skip(p0));
+  front_vals(p0, dsA, esA, xA);
+
+  TilePos p = p0;
+  for (int i = 0; i < total; i += 2) {
+    const TilePos q1 = next_pos(p, G), q2 = next_pos(q1, G);
+    if constexpr (NCB == 2) {
+      body(i, p, q1, q2, rB, (lds8*)rA, cA, (lds8*)cB, dsA, esA, xA, dsB, esB, xB);
     } else {
-      body(t, stA, (lds8*)stA, dsA, esA, dsB, esB);
-      if (t + 1 < total) body(t + 1, stA, (lds8*)stA, dsB, esB, dsA, esA);
+      body(i, p, q1, q2, rB, (lds8*)rA, cA, (lds8*)cA, dsA, esA, xA, dsB, esB, xB);
     }
+    if (i + 1 >= total) break;
+    const TilePos q3 = next_pos(q2, G);
+    if constexpr (NCB == 2) {
+      body(i + 1, q1, q2, q3, rA, (lds8*)rB, cB, (lds8*)cA, dsB, esB, xB, dsA, esA, xA);
+    } else {
+      body(i + 1, q1, q2, q3, rA, (lds8*)rB, cA, (lds8*)cA, dsB, esB, xB, dsA, esA, xA);
+    }
+    p = q2;
   }
-  if (total & 1) ds_store(total - 1, dsA, esA);
-  else ds_store(total - 1, dsB, esB);
 
   if (!live) return;
   // dV (first half) or dK times tau (second half): lane holds channel
@@ -427,8 +505,8 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
 }
 
 // Query-side data the tile loop streams besides the code tiles:
-//   rows    [B, Hq, N] x 16 B: {LSE log2 e, delta hi, delta lo, isolated-channel
-//           query value};
+//   rows    [B, Hq, N] x 16 B: {isolated-channel query value, -delta hi,
+//           -LSE / tau, -delta lo};
 //   tile_cs [B, Hq, ceil(N/64)] x 2 (Dqk + Dv) B: for each 64-query tile, the
 //           col-copy scales of Q then dO for the tile's two 32-query groups
 //           ([channel][group]), the second clamped to the first past the end;
@@ -445,7 +523,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
     const size_t row = bh * N + i0 + threadIdx.x;
     const float2 d = *reinterpret_cast<const float2*>(a.delta + row * 2);
     const float qh = hot >= 0 ? row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot) : 0.f;
-    reinterpret_cast<float4*>(a.rows)[row] = make_float4(a.lse[row] * kLog2e, d.x, d.y, qh);
+    reinterpret_cast<float4*>(a.rows)[row] = make_float4(qh, -d.x, neg_lse_over_tau(a.lse[row], a.tau), -d.y);
   }
   const int g0 = i0 / 32, g1 = (i0 + 32 < N ? i0 + 32 : i0) / 32;
   uint8_t* dst = a.tile_cs + (bh * ((N + 63) / 64) + blockIdx.x) * (2 * (DQK + DV));

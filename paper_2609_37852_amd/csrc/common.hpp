@@ -50,8 +50,10 @@ __device__ __forceinline__ float exp2i(int e) { return __uint_as_float((uint32_t
 
 // Four E4M3 codes of a/scale .. d/scale (scale a power of two, normal FP32),
 // round to nearest even, packed little-endian into one dword.
+// (the first convert's unused high half comes from a's register, which the
+// second overwrites, so no zeroed destination is needed)
 __device__ __forceinline__ uint32_t cvt4_div(float a, float b, float c, float d, float scale) {
-  v2s r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32((v2s){0, 0}, a, b, scale, false);
+  v2s r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(__builtin_bit_cast(v2s, a), a, b, scale, false);
   r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(r, c, d, scale, true);
   return __builtin_bit_cast(uint32_t, r);
 }
@@ -59,7 +61,7 @@ __device__ __forceinline__ uint32_t cvt4_div(float a, float b, float c, float d,
 // Four E4M3 codes of already-scaled values (no saturation: |x| <= 448 by
 // construction at every call site).
 __device__ __forceinline__ uint32_t cvt4(float a, float b, float c, float d) {
-  uint32_t r = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0u, false);
+  uint32_t r = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, __builtin_bit_cast(uint32_t, a), false);
   return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, r, true);
 }
 
@@ -142,10 +144,26 @@ __device__ __forceinline__ float partner(float v) {
 }  // namespace afp8
 
 namespace afp8 {
-// Backward probability of one score (App. B.6.3): P = 2^(S tau log2e - L) with
-// L = LSE log2e, exponent clamped at 4 (256 P at 2^12).  Written with an
-// explicit FMA so that every kernel recomputing P gets the same FP32 value.
-__device__ __forceinline__ float bwd_prob(float s, float c, float L) {
-  return __builtin_amdgcn_exp2f(fminf(__builtin_fmaf(s, c, -L), 4.0f));
+// Two rank-1 updates of a 32x32 FP32 accumulator in one MFMA:
+// C[i][j] += a0_i b0_j, then += a1_i b1_j, where lane l < 32 supplies a0_l
+// (row l) and b0_l (column l) and lane l >= 32 supplies a1, b1 of row / column
+// l - 32.  Each addition is rounded to nearest even in that order (a property
+// of v_mfma_f32_32x32x2_f32 measured on the hardware), so with exact products
+// the result is exactly fl(fl(C + a0 b0) + a1 b1), whichever operand holds
+// the rows.
+__device__ __forceinline__ v16f rank2_update(float a, float b, const v16f& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+// Per-query shift of the raw score S (no tau) that makes P = 2^(c (S + shift))
+// with c = tau log2e equal exp(tau S - LSE) (App. B.6.3).  Every kernel that
+// recomputes P derives it from LSE with this one expression.
+__device__ __forceinline__ float neg_lse_over_tau(float lse, float tau) { return -(lse / tau); }
+
+// Backward probability from the shifted score: 2^(c s), clamped to [0, 1]
+// (the clamp is a free modifier of the exponential and keeps 256 P inside
+// the E4M3 range whatever LSE the caller passed).
+__device__ __forceinline__ float bwd_prob(float s, float c) {
+  return __builtin_amdgcn_fmed3f(__builtin_amdgcn_exp2f(s * c), 0.f, 1.f);
 }
 }  // namespace afp8

@@ -1,7 +1,7 @@
 // Matched correction pass (Sec. 3.4; App. B.6.3 "Matched correction").
 //
 // delta_i = (sum_j P_ij dP_ij) / (sum_j P_ij) with the FP32 probabilities
-// P = 2^(S tau log2e - LSE log2e) recomputed from the FP8 scores, and
+// P = 2^(tau log2e (S - LSE / tau)) recomputed from the FP8 scores, and
 // dP = dO_row V_row^T (MX MFMA, FP32).  Sums of P dP and of P are formed in
 // FP32 over each aligned 32-key group, the group sums are accumulated in
 // FP64, and delta is stored as an FP32 pair (hi, lo) with hi + lo the FP64
@@ -13,11 +13,13 @@
 // of K and V (row copies) reach LDS by direct loads, double-buffered, so the
 // next tile streams in while the current one is computed.  S^T and dP^T put
 // one query in each lane (row reductions in-lane plus one exchange with lane
-// l ^ 32).  P and dP use exactly the operations of the backward kernel (same
-// MX MFMA operands and k order, bwd_prob()), so the backward's
-// dS = P (dP - delta) sums to zero over every row up to FP32 rounding of its
-// own terms.  Only the 32-key group holding the diagonal is masked; groups
-// in a wave's future are skipped.
+// l ^ 32).  The isolated score channel (if any) is zeroed in the Q operand;
+// its product and the shift -LSE / tau are added to the scores by one FP32
+// rank-2 MFMA.  P and dP use exactly the operations of the backward kernel
+// (same MX MFMA products and k order, the same rank-2 update, bwd_prob()),
+// so the backward's dS = P (dP - delta) sums to zero over every row up to
+// FP32 rounding of its own terms.  Only the 32-key group holding the
+// diagonal is masked; groups in a wave's future are skipped.
 #include "common.hpp"
 #include "dma.hpp"
 #include "kernels.hpp"
@@ -62,7 +64,9 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   const size_t bhq = (size_t)b * a.Hq + h, bhk = (size_t)b * a.Hkv + kh;
   v8i qf[KS], df[VS];
   int qsc[KS], dsc[VS];
-  float L = 0.f, qhot = 0.f;
+  // B operand of the score's rank-2 update: isolated-channel value (lanes
+  // < 32), -LSE / tau (lanes >= 32) of the lane's query
+  float qv = 0.f;
   {
     const size_t row = bhq * N + (live ? qi : 0);
 #pragma unroll
@@ -76,8 +80,8 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
       df[s] = frag_rows_global(a.do_code + row * DV, s, hf);
       dsc[s] = a.do_scale[row * (DV / 32) + 2 * s + hf];
     }
-    L = a.lse[row] * kLog2e;
-    if (hot >= 0) qhot = row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot);
+    const float qhot = hot >= 0 ? row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot) : 0.f;
+    qv = hf ? neg_lse_over_tau(a.lse[row], a.tau) : qhot;
   }
   double num = 0.0, den = 0.0;
 
@@ -130,16 +134,17 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
       for (int t = 0; t < VS; t++)
         dp = mfma_mx(frag_rows_swz<DV>(V, 32 * g + li, t, hf), df[t], dp, Vs[(32 * g + li) * (DV / 32) + 2 * t + hf],
                      dsc[t]);
+      // S + k_c* q_c* - LSE / tau: A = isolated-channel key value (lanes
+      // < 32) or 1 (lanes >= 32), B = qv
+      s = rank2_update(hf ? 1.0f : Kh[32 * g + li], qv, s);
       // lane holds keys g0 + 8 (r/4) + 4 hf + r % 4 of query qi
       float pn = 0.f, pd = 0.f;
 #pragma unroll
       for (int q4 = 0; q4 < 4; q4++) {
-        const float4 kh4 = *reinterpret_cast<const float4*>(&Kh[32 * g + 8 * q4 + 4 * hf]);
-        const float khv[4] = {kh4.x, kh4.y, kh4.z, kh4.w};
 #pragma unroll
         for (int e = 0; e < 4; e++) {
           const int r = 4 * q4 + e;
-          float p = bwd_prob(__builtin_fmaf(qhot, khv[e], s[r]), a.c, L);
+          float p = bwd_prob(s[r], a.c);
           if (g0 == q0) p = (8 * q4 + 4 * hf + e) > li ? 0.f : p;   // diagonal group: key > query
           pn = __builtin_fmaf(p, dp[r], pn);
           pd += p;
