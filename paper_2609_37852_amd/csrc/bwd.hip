@@ -74,8 +74,14 @@ struct BwdCfg {
   static constexpr int CSTAGE = al16(QCS_OFF + CS_BYTES);
   // dS' tiles, exponents and code exchange, two of each
   static constexpr int FIXED = 2 * (BKB * DST + KBW * 2 + 2 * KBW * 64 * 16);
-  // row parts are double-buffered; col parts too where the LDS allows
-  static constexpr int NCB = 2 * RSTAGE + 2 * CSTAGE + FIXED <= 156 * 1024 ? 2 : 1;
+  // the workgroup's K and V row codes [BKB][DQK + DV] (swizzled), read as
+  // MFMA operands instead of being held in registers
+  static constexpr int KV = BKB * (DQK + DV);
+  static constexpr int LIM = 156 * 1024;
+  // row parts are double-buffered; col parts too and K / V are kept in LDS
+  // where the LDS allows, preferring K / V in LDS over a second col buffer
+  static constexpr bool KV_LDS = 2 * RSTAGE + CSTAGE + FIXED + KV <= LIM;
+  static constexpr int NCB = 2 * RSTAGE + 2 * CSTAGE + FIXED + (KV_LDS ? KV : 0) <= LIM ? 2 : 1;
 };
 
 // dQ operand units of one head before query block q (block q has q/2 + 1
@@ -105,15 +111,31 @@ __device__ __forceinline__ BwdHead bwd_head(const AttnArgs& a, size_t bh, int N)
   return p;
 }
 
+// Load plans of one wave for the code tiles of a query tile.
+template <int DQK, int DV>
+struct BwdLoads {
+  RowLoads<DQK, 8, 64> q;
+  RowLoads<DV, 8, 64> o;
+  ColLoads<DQK, 8> qc;
+  ColLoads<DV, 8> oc;
+  __device__ __forceinline__ void init(int w, int lane, int N) {
+    q.init(w, lane);
+    o.init(w, lane);
+    qc.init(w, lane, N);
+    oc.init(w, lane, N);
+  }
+};
+
 // Direct-to-LDS loads of the row part of one query tile: codes, row scales
 // and the per-query records.
 template <int DQK, int DV>
-__device__ __forceinline__ void stage_rows(lds8* st, const BwdHead& hp, int i0, int N) {
+__device__ __forceinline__ void stage_rows(lds8* st, const BwdLoads<DQK, DV>& L, const BwdHead& hp, int i0, int N) {
   using C = BwdCfg<DQK, DV>;
   constexpr int NWK = C::NWK;
+  static_assert(NWK == 8, "load plans assume 8 waves");
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  dma_rows<DQK, NWK>(st + C::Q_OFF, hp.qrow, i0, N, w, lane);
-  dma_rows<DV, NWK>(st + C::O_OFF, hp.orow, i0, N, w, lane);
+  L.q.issue(st + C::Q_OFF, hp.qrow, i0, N, w, lane);
+  L.o.issue(st + C::O_OFF, hp.orow, i0, N, w, lane);
   dma_row_scales<DQK, NWK>(st + C::QS_OFF, hp.qsc, i0, N, w, lane, 0);
   dma_row_scales<DV, NWK>(st + C::OS_OFF, hp.osc, i0, N, w, lane, 1);
   if (w == (3 % NWK)) {
@@ -124,12 +146,12 @@ __device__ __forceinline__ void stage_rows(lds8* st, const BwdHead& hp, int i0, 
 
 // ... and of its col part: codes and the col scales packed by bwd_prep.
 template <int DQK, int DV>
-__device__ __forceinline__ void stage_cols(lds8* st, const BwdHead& hp, int i0, int N) {
+__device__ __forceinline__ void stage_cols(lds8* st, const BwdLoads<DQK, DV>& L, const BwdHead& hp, int i0, int N) {
   using C = BwdCfg<DQK, DV>;
   constexpr int NWK = C::NWK;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  dma_cols<DQK, NWK>(st + C::QC_OFF, hp.qcol, i0, N, w, lane);
-  dma_cols<DV, NWK>(st + C::OC_OFF, hp.ocol, i0, N, w, lane);
+  L.qc.issue(st + C::QC_OFF, hp.qcol, i0, N, w, lane);
+  L.oc.issue(st + C::OC_OFF, hp.ocol, i0, N, w, lane);
   constexpr int NCI = (C::CS_BYTES + 255) / 256;
   const uint8_t* tcs = hp.tcs + (i0 / 64) * C::CS_BYTES;
   for (int k = 0; k < NCI; k++) {
@@ -209,6 +231,9 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   v8i kf[KS], vf[VS];
   int ksc[KS], vsc[VS];
   float kb = 1.0f;
+  constexpr bool KVL = C::KV_LDS;
+  __shared__ __attribute__((aligned(16))) uint8_t kL[KVL ? BKB * DQK : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t vL[KVL ? BKB * DV : 16];
   {
     const int row = live ? kj : 0;
     const uint8_t* kr = a.k_code + (bhk * N + row) * DQK;
@@ -226,7 +251,29 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     }
     if (hf == 0)
       kb = hot >= 0 ? row_value<DQK>(a.k_code + bhk * N * DQK, a.k_scale + bhk * N * (DQK / 32), row, hot) : 0.f;
+    if constexpr (KVL) {
+      // the first wave of each key block stores the K fragments, the second
+      // the V fragments, where frag_rows_swz reads them (visible after the
+      // prologue's barrier)
+      const int kr2 = 32 * kbw + li;
+      if (qs == 0) {
+#pragma unroll
+        for (int t = 0; t < KS; t++) kv_store<DQK>(kL, kr2, t, hf, kf[t]);
+      } else {
+#pragma unroll
+        for (int t = 0; t < VS; t++) kv_store<DV>(vL, kr2, t, hf, vf[t]);
+      }
+    }
   }
+  // operand fragments of k-step t of this lane's key
+  auto kfrag = [&](int t) __attribute__((always_inline)) {
+    if constexpr (KVL) return frag_rows_swz<DQK>(kL, 32 * kbw + li, t, hf);
+    else return kf[t];
+  };
+  auto vfrag = [&](int t) __attribute__((always_inline)) {
+    if constexpr (KVL) return frag_rows_swz<DV>(vL, 32 * kbw + li, t, hf);
+    else return vf[t];
+  };
 
   // dV (first half, CV blocks) or dK (second half, CK blocks) of the wave's keys
   v16f acc[CMAX];
@@ -240,6 +287,11 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   const size_t bh0 = (size_t)b * Hq + (size_t)kh * G;   // first query head of the group
   const int64_t units_per_head = tri_units(N / 32);
   auto q0_of = [&](TilePos p) __attribute__((always_inline)) { return (nqt - 1 - p.r) * BQ; };
+  BwdLoads<DQK, DV> ld;
+  ld.init(w, lane, N);
+  auto row_rec = [&](const uint8_t* R) __attribute__((always_inline)) {
+    return *reinterpret_cast<const float2*>(R + C::ROW_OFF + (32 * qs + li) * 16 + 8 * hf);
+  };
   auto head_of = [&](TilePos p) __attribute__((always_inline)) { return bwd_head<DQK, DV>(a, bh0 + p.hi, N); };
 
   // Pipeline, per tile i (each step a function of the buffers it touches):
@@ -253,7 +305,10 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   int e = -127;                                      // and the dS' block exponent
 
   // S and dP of one tile's half (skipped halves: no MFMA, zero codes later)
-  auto sdp = [&](const uint8_t* R, bool skip) __attribute__((always_inline)) {
+  // rec: the lane's pair of per-query record values (read before the loads
+  // of the next tiles are issued: the compiler cannot tell this read from
+  // the LDS those loads write and would wait for them)
+  auto sdp = [&](const uint8_t* R, bool skip, float2 rec) __attribute__((always_inline)) {
     if (skip) return;
     const uint8_t* Q = R + C::Q_OFF;
     const uint8_t* Qs = R + C::QS_OFF;
@@ -263,14 +318,13 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     for (int r = 0; r < 16; r++) { s[r] = 0.f; dp[r] = 0.f; }
 #pragma unroll
     for (int t2 = 0; t2 < KS; t2++)
-      s = mfma_mx(frag_rows_swz<DQK>(Q, 32 * qs + li, t2, hf), kf[t2], s,
+      s = mfma_mx(frag_rows_swz<DQK>(Q, 32 * qs + li, t2, hf), kfrag(t2), s,
                   Qs[(32 * qs + li) * (DQK / 32) + 2 * t2 + hf], ksc[t2]);
 #pragma unroll
     for (int t2 = 0; t2 < VS; t2++)
-      dp = mfma_mx(frag_rows_swz<DV>(O, 32 * qs + li, t2, hf), vf[t2], dp,
+      dp = mfma_mx(frag_rows_swz<DV>(O, 32 * qs + li, t2, hf), vfrag(t2), dp,
                    Os[(32 * qs + li) * (DV / 32) + 2 * t2 + hf], vsc[t2]);
     // per-query shifts: S += q_c* k_c*, then -LSE / tau; dP -= hi, then lo
-    const float2 rec = *reinterpret_cast<const float2*>(R + C::ROW_OFF + (32 * qs + li) * 16 + 8 * hf);
     s = rank2_update(rec.x, kb, s);
     dp = rank2_update(rec.y, 1.0f, dp);
   };
@@ -347,7 +401,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     // dS' codes for the dQ units and the exchange with the other half
     *reinterpret_cast<uint4*>(ds + (32 * kbw + li) * C::DST + 32 * qs + 16 * hf) =
         make_uint4((uint32_t)dn[0], (uint32_t)dn[1], (uint32_t)dn[2], (uint32_t)dn[3]);
-    if (lane == 0) es[kbw * 2 + qs] = (uint8_t)(e + 127);
+    if (lane == 0) es[qs * KBW + kbw] = (uint8_t)(e + 127);
     const v4i xv = qs == 0 ? dn : pn;
     x[qs][kbw * 64 + lane] = make_uint4((uint32_t)xv[0], (uint32_t)xv[1], (uint32_t)xv[2], (uint32_t)xv[3]);
   };
@@ -375,7 +429,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     } else {
       const uint4 o = x[0][kbw * 64 + lane];
       const v8i A = v8i{(int)o.x, (int)o.y, (int)o.z, (int)o.w, dn[0], dn[1], dn[2], dn[3]};
-      const int dascale = hf ? e + 127 : (int)es[kbw * 2];
+      const int dascale = hf ? e + 127 : (int)es[kbw];
       const uint8_t* Qc = Cc + C::QC_OFF;
       const uint8_t* Qcs = Cc + C::QCS_OFF;
 #pragma unroll
@@ -416,8 +470,8 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     __builtin_nontemporal_store(v4i{af[0], af[1], af[2], af[3]}, dst);
     __builtin_nontemporal_store(v4i{af[4], af[5], af[6], af[7]}, dst + 1);
     if (lane == 0) {
-      const uint32_t e2 = (uint32_t)es[(2 * ks) * 2 + uq] | ((uint32_t)es[(2 * ks + 1) * 2 + uq] << 8);
-      *reinterpret_cast<uint16_t*>(a.ds_exp + unit * 2) = (uint16_t)e2;
+      // the exponents of key blocks 2 ks and 2 ks + 1 of half uq, adjacent
+      *reinterpret_cast<uint16_t*>(a.ds_exp + unit * 2) = *reinterpret_cast<const uint16_t*>(es + uq * KBW + 2 * ks);
     }
   };
 
@@ -430,30 +484,34 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
                   uint4 (*x1)[KBW * 64]) __attribute__((always_inline)) {
     lds_barrier();
     const bool more = i + 1 < total;
+    // LDS reads the compiler cannot attribute to one buffer come first, before
+    // any load into LDS is in flight: the dQ units of tile i and the records
+    // of tile i+1
+    ds_store(p, ds, es);
+    const float2 rec = row_rec(R1);
     if constexpr (NCB == 2) {
-      if (more) stage_cols<DQK, DV>(Cl, head_of(p1), q0_of(p1), N);
+      if (more) stage_cols<DQK, DV>(Cl, ld, head_of(p1), q0_of(p1), N);
     }
-    if (i + 2 < total) stage_rows<DQK, DV>(Rl, head_of(p2), q0_of(p2), N);
+    if (i + 2 < total) stage_rows<DQK, DV>(Rl, ld, head_of(p2), q0_of(p2), N);
     const bool skip1 = front_skip(p1);
-    if (more) sdp(R1, skip1);
+    if (more) sdp(R1, skip1, rec);
     back(Cc, es, x);
     __builtin_amdgcn_sched_barrier(0);   // both MFMA groups issue before the VALU work below
     if constexpr (NCB == 1) {
       lds_sync();                          // every wave has read the col operands of tile i
-      if (more) stage_cols<DQK, DV>(Cl, head_of(p1), q0_of(p1), N);
+      if (more) stage_cols<DQK, DV>(Cl, ld, head_of(p1), q0_of(p1), N);
     }
-    ds_store(p, ds, es);
     if (more) front_vals(p1, ds1, es1, x1);
   };
 
   // prologue: rows of tiles 0 and 1, cols of tile 0; S, dP, P, dS of tile 0
   const TilePos p0 = TilePos{0, 0};
-  stage_rows<DQK, DV>((lds8*)rA, head_of(p0), q0_of(p0), N);
-  stage_cols<DQK, DV>((lds8*)cA, head_of(p0), q0_of(p0), N);
+  stage_rows<DQK, DV>((lds8*)rA, ld, head_of(p0), q0_of(p0), N);
+  stage_cols<DQK, DV>((lds8*)cA, ld, head_of(p0), q0_of(p0), N);
   TilePos pa = next_pos(p0, G);
-  if (total > 1) stage_rows<DQK, DV>((lds8*)rB, head_of(pa), q0_of(pa), N);
+  if (total > 1) stage_rows<DQK, DV>((lds8*)rB, ld, head_of(pa), q0_of(pa), N);
   lds_barrier();
-  sdp(rA, front_skip(p0));
+  sdp(rA, front_skip(p0), row_rec(rA));
   front_vals(p0, dsA, esA, xA);
 
   TilePos p = p0;

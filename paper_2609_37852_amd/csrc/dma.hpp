@@ -99,6 +99,14 @@ __device__ __forceinline__ v8i frag_rows_swz(const uint8_t* tile, int row, int t
   const uint4 hi = *reinterpret_cast<const uint4*>(base + 16 * ((c + 2) ^ s));
   return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
 }
+// Stores a fragment where frag_rows_swz<D>(tile, row, t, hf) reads it.
+template <int D>
+__device__ __forceinline__ void kv_store(uint8_t* tile, int row, int t, int hf, const v8i& f) {
+  const int s = swz_row<D>(row), c = 4 * t + hf;
+  uint8_t* base = tile + row * D;
+  *reinterpret_cast<uint4*>(base + 16 * (c ^ s)) = make_uint4((uint32_t)f[0], (uint32_t)f[1], (uint32_t)f[2], (uint32_t)f[3]);
+  *reinterpret_cast<uint4*>(base + 16 * ((c + 2) ^ s)) = make_uint4((uint32_t)f[4], (uint32_t)f[5], (uint32_t)f[6], (uint32_t)f[7]);
+}
 // B fragment of a swizzled col tile: channel ch, queries 16 hf.. and 32 + 16 hf..
 __device__ __forceinline__ v8i frag_cols_swz(const uint8_t* tile, int ch, int hf) {
   const int s = swz_col(ch);
@@ -107,5 +115,65 @@ __device__ __forceinline__ v8i frag_cols_swz(const uint8_t* tile, int ch, int hf
   const uint4 hi = *reinterpret_cast<const uint4*>(base + 16 * ((hf + 2) ^ s));
   return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
 }
+
+// Precomputed plans for the tile loads of one wave: the lane's byte offset in
+// the source matrix for each of its load instructions (k = w + NWK j), so a
+// whole tile costs one address add per load.  A tile that reaches past the
+// sequence end takes the clamping loaders above instead.
+//
+// Row tile: rows [i0, i0 + ROWS) of a [N][D] code matrix -> LDS [ROWS][D].
+template <int D, int NWK, int ROWS>
+struct RowLoads {
+  static constexpr int NI = ROWS * D / 1024, NS = (NI + NWK - 1) / NWK;
+  uint32_t off[NS];   // r D + 16 (swizzled chunk), r the lane's row in the tile
+  __device__ __forceinline__ void init(int w, int lane) {
+#pragma unroll
+    for (int j = 0; j < NS; j++) {
+      const int o = 1024 * (w + NWK * j) + 16 * lane;
+      const int r = o / D, p = (o % D) / 16;
+      off[j] = (uint32_t)(r * D + 16 * (p ^ swz_row<D>(r)));
+    }
+  }
+  __device__ __forceinline__ void issue(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) const {
+    if (i0 + ROWS > N) {
+      dma_rows<D, NWK, ROWS>(lds, code, i0, N, w, lane);
+      return;
+    }
+    const uint8_t* base = code + (size_t)i0 * D;
+#pragma unroll
+    for (int j = 0; j < NS; j++) {
+      const int k = w + NWK * j;
+      if (k < NI) dma16(base + off[j], lds + 1024 * k);
+    }
+  }
+};
+
+// Col tile: channels [0, D), sequence positions [i0, i0 + 64) of a [D][N]
+// code matrix -> LDS [D][64].
+template <int D, int NWK>
+struct ColLoads {
+  static constexpr int NI = D * 64 / 1024, NS = (NI + NWK - 1) / NWK;
+  uint32_t off[NS];   // c N + 16 q (q the swizzled chunk)
+  __device__ __forceinline__ void init(int w, int lane, int N) {
+#pragma unroll
+    for (int j = 0; j < NS; j++) {
+      const int o = 1024 * (w + NWK * j) + 16 * lane;
+      const int c = o / 64, p = (o % 64) / 16;
+      off[j] = (uint32_t)(c * N + 16 * (p ^ swz_col(c)));
+    }
+  }
+  __device__ __forceinline__ void issue(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) const {
+    if (i0 + 64 > N) {
+      dma_cols<D, NWK>(lds, code, i0, N, w, lane);
+      return;
+    }
+    const uint8_t* base = code + i0;
+#pragma unroll
+    for (int j = 0; j < NS; j++) {
+      const int k = w + NWK * j;
+      if (k < NI) dma16(base + off[j], lds + 1024 * k);
+    }
+  }
+};
 
 }  // namespace afp8
