@@ -25,7 +25,7 @@
  *      x_g the group max over visible keys); code = C8(2^{x - E_g}); the
  *      normalizer uses the exponentials before the cast.
  *   R6 backward probability codes for dV: C8(256 P) with fixed scale 2^-8;
- *      the exponent of 256 P is clamped at 12.
+ *      P is clamped to at most 1 (the range that fixed scale is meant for).
  *   R7 dS codes: aligned 32x32 blocks (query x key), one power-of-two scale
  *      per block, shared by dQ and dK.
  *   R8 matched correction: (sum_j P_ij dP_ij) / (sum_j P_ij) from the
@@ -227,11 +227,12 @@ static int group_exponent(double xg) {
   return E;
 }
 
-/* P_ij = exp(S_ij - LSE_i) with the score S_ij = tau <q_i, k_j> (App. B.6.3);
- * the exponent of 256 P is clamped at 12, i.e. P <= 16. */
+/* P_ij = exp(S_ij - LSE_i) with the score S_ij = tau <q_i, k_j> (App. B.6.3),
+ * clamped to at most 1 (R6): with the LSE of the same scores P <= 1 already;
+ * the clamp only matters for an inconsistent LSE. */
 static double probability(double tau, const double* q, const double* k, int64_t d, double lse) {
   double pij = exp(tau * dot(q, k, d) - lse);
-  return pij > 16.0 ? 16.0 : pij;
+  return pij > 1.0 ? 1.0 : pij;
 }
 
 typedef struct {
