@@ -173,7 +173,10 @@ def main():
     credited = fwd_f + bwd_f
     value = credited / (ms_per_step * 1e-3) / 1e12
     paper_ms = t_fwd + t_delta + t_bwd_call
-    achieved = bwd_f / (t_bwd_main * 1e-3) / 1e12
+    # the main backward kernel computes S, dP, dV and dK over the causal half
+    # (dQ is the separate dq pass): B*Hq*N^2*2*(dqk + dv) algorithmic FLOPs
+    main_f = w.B * w.Hq * w.N * w.N * 2 * (w.Dqk + w.Dv)
+    achieved = main_f / (t_bwd_main * 1e-3) / 1e12
     traffic = None
     if args.traffic and os.path.exists(args.traffic):
         traffic = json.load(open(args.traffic)).get("bytes_per_launch")
@@ -209,7 +212,7 @@ def main():
         "quantize_hbm_gbs": round(quant_bytes / (t_quant * 1e-3) / 1e9, 1),
         "roofline": {"kernel": "bwd_kernel<128,128>", "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP8_TFLOPS, 4),
-                     "traffic": traffic},
+                     "traffic": traffic, "flops_per_launch": main_f, "ms_per_launch": round(t_bwd_main, 4)},
     }
     if args.copy_calibration > 0:
         n = args.copy_calibration << 20
