@@ -146,17 +146,19 @@ int attn_fp8_delta(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx*
                    const int64_t dout_strides[3], const void* o, int o_dtype,
                    const int64_t o_strides[3], float* delta, hipStream_t stream);
 
-/* Workspace bytes attn_fp8_bwd needs for this problem: FP32 dQ accumulator
- * [B,N,Hq,Dqk], the internal delta buffer [B,Hq,N,2] and 16-byte per-query
- * records [B,Hq,N] (LSE log2 e, delta, isolated-channel value) that the main
- * kernel streams with its query tiles.  Returns 0 / negative status. */
+/* Workspace bytes attn_fp8_bwd needs for this problem: the FP8 dS' operand
+ * units (per query head, 2048 code bytes + 2 exponent bytes for every
+ * 32-query block x 64-key step at or before the diagonal), the internal delta
+ * buffer [B,Hq,N,2], 16-byte per-query records [B,Hq,N] that the main kernel
+ * streams with its query tiles, and per-tile packed col scales (Q and dO per
+ * 64-query tile, K per 64-key tile).  Returns 0 / negative status. */
 int attn_fp8_bwd_workspace_size(const attn_fp8_problem* p, size_t* bytes);
 
 /* Backward (Sec. 2.3; App. B.6.3).  Key-major pass: recompute S, P, dP;
- * dS = P ((dP - hi) - lo); P' = C8(256 P) 2^-8; dS' cast per 32x32 block;
- * dV += P'^T dO_col, dK += dS'^T Q_col (summed over the KV group in FP32),
- * dQ += dS' K_col (FP32 accumulation in the workspace); then dQ, dK are
- * multiplied by tau and stored.
+ * dS = P ((dP - hi) - lo); P' = C8(256 P) 2^-8 (P clamped to [0, 1]); dS'
+ * cast per 32x32 block; dV += P'^T dO_col, dK += dS'^T Q_col (summed over the
+ * KV group in FP32), dS' stored in the workspace; then a query-major pass
+ * computes dQ = dS' K_col.  dQ and dK are multiplied by tau and stored.
  *   delta_in nullable device float [B, Hq, N, 2]: when given, used as the
  *            correction (and delta_mode is ignored); else the correction is
  *            computed first per delta_mode, exactly as attn_fp8_delta does.
