@@ -20,6 +20,8 @@
 // so the backward's dS = P (dP - delta) sums to zero over every row up to
 // FP32 rounding of its own terms.  Only the 32-key group holding the
 // diagonal is masked; groups in a wave's future are skipped.
+#include <type_traits>
+
 #include "common.hpp"
 #include "dma.hpp"
 #include "kernels.hpp"
@@ -112,47 +114,62 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
       reinterpret_cast<float*>(st + C::KH_OFF)[threadIdx.x] = hot >= 0 ? scaled_value(khc, khs) : 0.f;
   };
 
-  auto tile = [&](const uint8_t* st, int j0) __attribute__((always_inline)) {
-    if (!live || j0 > q0) return;
+  // one 32-key group (keys j0 + 32 g ..) of the tile in st; DIAG: the group
+  // holding the wave's diagonal (keys after the query masked)
+  auto group = [&](const uint8_t* st, int g, auto diag_tag) __attribute__((always_inline)) {
+    constexpr bool DIAG = decltype(diag_tag)::value;
     const uint8_t* K = st + C::K_OFF;
     const uint8_t* Ks = st + C::KS_OFF;
     const uint8_t* V = st + C::V_OFF;
     const uint8_t* Vs = st + C::VS_OFF;
     const float* Kh = reinterpret_cast<const float*>(st + C::KH_OFF);
+    v16f s, dp;
+#pragma unroll
+    for (int r = 0; r < 16; r++) { s[r] = 0.f; dp[r] = 0.f; }
+#pragma unroll
+    for (int t = 0; t < KS; t++)
+      s = mfma_mx(frag_rows_swz<DQK>(K, 32 * g + li, t, hf), qf[t], s, Ks[(32 * g + li) * (DQK / 32) + 2 * t + hf],
+                  qsc[t]);
+#pragma unroll
+    for (int t = 0; t < VS; t++)
+      dp = mfma_mx(frag_rows_swz<DV>(V, 32 * g + li, t, hf), df[t], dp, Vs[(32 * g + li) * (DV / 32) + 2 * t + hf],
+                   dsc[t]);
+    // S + k_c* q_c* - LSE / tau: A = isolated-channel key value (lanes
+    // < 32) or 1 (lanes >= 32), B = qv
+    s = rank2_update(hf ? 1.0f : Kh[32 * g + li], qv, s);
+    // lane holds keys 32 g + 8 (r/4) + 4 hf + r % 4 of the tile, query qi
+    float pn = 0.f, pd = 0.f;
+#pragma unroll
+    for (int q4 = 0; q4 < 4; q4++) {
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        const int r = 4 * q4 + e;
+        float p = bwd_prob(s[r], a.c);
+        if (DIAG) p = (8 * q4 + 4 * hf + e) > li ? 0.f : p;
+        pn = __builtin_fmaf(p, dp[r], pn);
+        pd += p;
+      }
+    }
+    // 32-key group sums: this lane's 16 keys plus the partner's 16 (FP32)
+    num += (double)(pn + partner(pn));
+    den += (double)(pd + partner(pd));
+  };
+
+  auto tile = [&](const uint8_t* st, int j0) __attribute__((always_inline)) {
+    if (!live || j0 > q0) return;
+    if (j0 + BK <= q0) {
+      // wholly before the wave's queries: every group, no mask, no branch
+      // between groups (so one group's MFMAs can overlap another's VALU)
+#pragma unroll
+      for (int g = 0; g < BK / 32; g++) group(st, g, std::false_type{});
+      return;
+    }
 #pragma unroll
     for (int g = 0; g < BK / 32; g++) {
       const int g0 = j0 + 32 * g;              // first key of the group
       if (g0 > q0) break;                      // this and later groups are in the wave's future
-      v16f s, dp;
-#pragma unroll
-      for (int r = 0; r < 16; r++) { s[r] = 0.f; dp[r] = 0.f; }
-#pragma unroll
-      for (int t = 0; t < KS; t++)
-        s = mfma_mx(frag_rows_swz<DQK>(K, 32 * g + li, t, hf), qf[t], s, Ks[(32 * g + li) * (DQK / 32) + 2 * t + hf],
-                    qsc[t]);
-#pragma unroll
-      for (int t = 0; t < VS; t++)
-        dp = mfma_mx(frag_rows_swz<DV>(V, 32 * g + li, t, hf), df[t], dp, Vs[(32 * g + li) * (DV / 32) + 2 * t + hf],
-                     dsc[t]);
-      // S + k_c* q_c* - LSE / tau: A = isolated-channel key value (lanes
-      // < 32) or 1 (lanes >= 32), B = qv
-      s = rank2_update(hf ? 1.0f : Kh[32 * g + li], qv, s);
-      // lane holds keys g0 + 8 (r/4) + 4 hf + r % 4 of query qi
-      float pn = 0.f, pd = 0.f;
-#pragma unroll
-      for (int q4 = 0; q4 < 4; q4++) {
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-          const int r = 4 * q4 + e;
-          float p = bwd_prob(s[r], a.c);
-          if (g0 == q0) p = (8 * q4 + 4 * hf + e) > li ? 0.f : p;   // diagonal group: key > query
-          pn = __builtin_fmaf(p, dp[r], pn);
-          pd += p;
-        }
-      }
-      // 32-key group sums: this lane's 16 keys plus the partner's 16 (FP32)
-      num += (double)(pn + partner(pn));
-      den += (double)(pd + partner(pd));
+      if (g0 == q0) group(st, g, std::true_type{});
+      else group(st, g, std::false_type{});
     }
   };
 

@@ -13,11 +13,11 @@
 //                     lane l owns query l % 32 and holds 16 keys of each
 //                     group, so row reductions are in-lane plus one exchange
 //                     with lane l ^ 32.  The isolated score channel (if any)
-//                     is cleared in Q and its product added by one more MFMA
-//                     whose Q operand holds that channel alone.
-//   M = integer running max of x = S tau log2e (ceil of the row max).  When it
-//       grows, O and l are multiplied by 2^(M_old - M_new), an exact power of
-//       two (decided per wave).
+//                     is cleared in Q and its exact product added by one
+//                     FP32 rank-1 MFMA update.
+//   M = integer running reference for x = S tau log2e (ceil of the row max,
+//       raised lazily).  When it is raised, O and l are multiplied by
+//       2^(M_old - M_new), an exact power of two (decided per wave).
 //   p = 2^(x - M) (FP32, before any cast) feeds l.
 //   group g: E_g = smallest integer with 2^(x_g - M) <= 448 * 2^E_g (x_g the
 //       group max), codes C8(p / 2^E_g) -- the group's probability scale.
@@ -29,6 +29,8 @@
 // Only the group holding the diagonal needs a mask; groups wholly in a wave's
 // future skip their MFMA and exponentials.
 // Epilogue: O = O_acc / l (bf16 or fp32), LSE = (M + log2 l) ln 2.
+#include <type_traits>
+
 #include "common.hpp"
 #include "dma.hpp"
 #include "kernels.hpp"
@@ -37,12 +39,18 @@
 namespace afp8 {
 
 constexpr float kLog2_448 = 8.807354922057604f;
+// The reference M is raised only once some row's maximum exceeds it by more
+// than this many powers of two: until then p = 2^(x - M) <= 2^16 simply
+// accumulates larger, which FP32 holds exactly in range.  Rescales are exact
+// powers of two and the codes do not depend on M, so O and l come out the
+// same whenever the rescales happen.
+constexpr float kLazyRescale = 16.0f;
 
 template <int DQK, int DV>
 struct FwdCfg {
   static constexpr int NW = 4, NT = 64 * NW, BQ = 32 * NW;
   static constexpr int al16(int x) { return (x + 15) & ~15; }
-  static constexpr int stage_bytes(int bk) { return al16(al16(bk * (DQK + DV) + bk * DQK / 32) + DV * 4); }
+  static constexpr int stage_bytes(int bk) { return al16(al16(bk * (DQK + DV) + bk * DQK / 32) + DV * 4) + bk * 4; }
   // 128-key tiles where two double-buffered workgroups fit a CU's LDS,
   // else 64-key tiles (wide heads)
   static constexpr int BK = 2 * stage_bytes(128) <= 80 * 1024 ? 128 : 64;
@@ -50,7 +58,8 @@ struct FwdCfg {
   static constexpr int V_OFF = K_OFF + BK * DQK;                // V col codes [DV][BK], swizzled
   static constexpr int KS_OFF = V_OFF + DV * BK;                // K row scales [BK][DQK/32]
   static constexpr int VS_OFF = al16(KS_OFF + BK * DQK / 32);   // V col scales [DV][4] (BK/32 used)
-  static constexpr int STAGE = al16(VS_OFF + DV * 4);
+  static constexpr int KH_OFF = al16(VS_OFF + DV * 4);          // isolated-channel key values [BK] FP32
+  static constexpr int STAGE = KH_OFF + BK * 4;
   static_assert(STAGE == stage_bytes(BK), "stage layout");
   static_assert(DV <= NT, "one V scale word per thread");
   static_assert(BQ % BK == 0, "a query block's diagonal starts a key tile");
@@ -97,21 +106,18 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   const uint8_t* vcode = a.vc_code + bhk * DV * N;
   const uint8_t* vscale = a.vc_scale + bhk * DV * (N / 32);
 
-  v8i qf[KS], qf_hot = v8i{0, 0, 0, 0, 0, 0, 0, 0};
-  int qsc[KS], qsc_hot = 0;
-  const int shot = hot >= 0 ? hot / 64 : 0;    // k-step holding the isolated channel
+  v8i qf[KS];
+  int qsc[KS];
+  float qv = 0.f;     // B operand of the isolated channel's rank-1 update (lanes < 32)
   {
     const size_t row = bhq * N + (live ? qi : 0);
 #pragma unroll
     for (int s = 0; s < KS; s++) {
       qf[s] = frag_rows_global(a.q_code + row * DQK, s, hf);
       qsc[s] = a.q_scale[row * (DQK / 32) + 2 * s + hf];
-      if (hot >= 0 && s == shot) {
-        qf_hot = keep_channel(qf[s], s, hf, hot);
-        qsc_hot = qsc[s];
-      }
       clear_channel(qf[s], s, hf, hot);
     }
+    if (hot >= 0 && hf == 0) qv = row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot);
   }
 
   v16f oacc[CB];
@@ -125,8 +131,10 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   const int ntiles = (qb + 1) * (BQ / BK);     // key tiles up to the block's diagonal
 
   // Loads of tile j0: codes and K scales straight to LDS; the V col scales
-  // (4 strided bytes per channel) through registers, written by finish().
+  // (4 strided bytes per channel) and the isolated-channel bytes of each key
+  // through registers, written by finish().
   uint32_t vsr[BK / 32] = {};
+  uint32_t khc = 0, khs = 0;
   auto issue = [&](lds8* st, int j0) __attribute__((always_inline)) {
     dma_rows<DQK, NW, BK>(st + C::K_OFF, kcode, j0, N, w, lane);
     if constexpr (BK == 128) dma_cols128<DV, NW>(st + C::V_OFF, vcode, j0, N, w, lane);
@@ -139,6 +147,11 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
         vsr[g] = vscale[threadIdx.x * (N / 32) + grp];
       }
     }
+    if (hot >= 0 && threadIdx.x < BK) {
+      const int r = j0 + (int)threadIdx.x < N ? j0 + (int)threadIdx.x : N - 1;
+      khc = kcode[r * DQK + hot];
+      khs = kscale[r * (DQK / 32) + hot / 32];
+    }
     __builtin_amdgcn_sched_barrier(0);   // keep every load ahead of the tile's compute
   };
   auto finish = [&](uint8_t* st) __attribute__((always_inline)) {
@@ -149,24 +162,30 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
       else
         *reinterpret_cast<uint16_t*>(st + C::VS_OFF + 4 * threadIdx.x) = (uint16_t)(vsr[0] | (vsr[1] << 8));
     }
+    if (threadIdx.x < BK)
+      reinterpret_cast<float*>(st + C::KH_OFF)[threadIdx.x] = hot >= 0 ? scaled_value(khc, khs) : 0.f;
   };
 
-  auto tile = [&](const uint8_t* st, int j0) __attribute__((always_inline)) {
-    if (!live || j0 > q0) return;
+  // FULL: the tile lies wholly before the wave's queries (no mask, no skipped
+  // group, no branch between groups, so one half's MFMAs can overlap the
+  // other's vector work)
+  auto tile_body = [&](const uint8_t* st, int j0, auto full_tag) __attribute__((always_inline)) {
+    constexpr bool FULL = decltype(full_tag)::value;
     const uint8_t* K = st + C::K_OFF;
     const uint8_t* Ks = st + C::KS_OFF;
     const uint8_t* V = st + C::V_OFF;
     const uint8_t* Vs = st + C::VS_OFF;
+    const float* Kh = reinterpret_cast<const float*>(st + C::KH_OFF);
 #pragma unroll
     for (int hk = 0; hk < BK / 64; hk++) {
-      if (j0 + 64 * hk > q0) break;            // both groups of this half are in the wave's future
+      if (!FULL && j0 + 64 * hk > q0) break;   // both groups of this half are in the wave's future
       v16f s[2];
       float gm[2];
 #pragma unroll
       for (int g2 = 0; g2 < 2; g2++) {
         const int kb = 2 * hk + g2;
         const int g0 = j0 + 32 * kb;           // first key of the group
-        if (g0 > q0) {                         // whole group in this wave's future
+        if (!FULL && g0 > q0) {                // whole group in this wave's future
           gm[g2] = -__builtin_inff();
           continue;
         }
@@ -176,12 +195,12 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
         for (int t = 0; t < KS; t++)
           s[g2] = mfma_mx(frag_rows_swz<DQK>(K, 32 * kb + li, t, hf), qf[t], s[g2],
                           Ks[(32 * kb + li) * (DQK / 32) + 2 * t + hf], qsc[t]);
-        if (hot >= 0)
-          s[g2] = mfma_mx(frag_rows_swz<DQK>(K, 32 * kb + li, shot, hf), qf_hot, s[g2],
-                          Ks[(32 * kb + li) * (DQK / 32) + 2 * shot + hf], qsc_hot);
+        // + k_c* q_c*: rank-1 update, A = isolated-channel key value
+        // (lanes < 32), B = qv; lanes >= 32 contribute 0 * 0
+        if (hot >= 0) s[g2] = rank2_update(hf ? 0.f : Kh[32 * kb + li], qv, s[g2]);
         // lane holds keys g0 + 8 (r/4) + 4 hf + r % 4 of query qi
         float m = -__builtin_inff();
-        if (g0 == q0) {                        // the diagonal group: keys after the query are masked
+        if (!FULL && g0 == q0) {               // the diagonal group: keys after the query are masked
 #pragma unroll
           for (int r = 0; r < 16; r++) {
             s[g2][r] = (8 * (r >> 2) + 4 * hf + (r & 3)) > li ? -__builtin_inff() : s[g2][r];
@@ -199,7 +218,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
       const float mnew = fmaxf(M, __builtin_ceilf(fmaxf(gm[0], gm[1]) * c));
       if (M == -__builtin_inff()) {
         M = mnew;                              // first visible keys: nothing accumulated yet
-      } else if (__any(mnew > M)) {
+      } else if (__any(mnew > M + kLazyRescale)) {
         const int d = (int)(M - mnew);         // 0 for lanes whose max did not move
         const float alpha = d < -126 ? 0.f : exp2i(d);
         lsum *= alpha;
@@ -214,7 +233,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
       int eg[2];
 #pragma unroll
       for (int g2 = 0; g2 < 2; g2++) {
-        if (j0 + 32 * (2 * hk + g2) > q0) {
+        if (!FULL && j0 + 32 * (2 * hk + g2) > q0) {
           codes[g2] = v4i{0, 0, 0, 0};
           eg[g2] = -126;
           continue;
@@ -245,6 +264,11 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
         oacc[cb] = mfma_mx(frag_rows_swz<BK>(V, 32 * cb + li, hk, hf), pfr, oacc[cb],
                            Vs[(32 * cb + li) * 4 + 2 * hk + hf], psc);
     }
+  };
+  auto tile = [&](const uint8_t* st, int j0) __attribute__((always_inline)) {
+    if (!live || j0 > q0) return;
+    if (j0 + BK <= q0) tile_body(st, j0, std::true_type{});
+    else tile_body(st, j0, std::false_type{});
   };
 
   issue((lds8*)stA, 0);
