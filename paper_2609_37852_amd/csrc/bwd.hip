@@ -603,16 +603,17 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
   }
 }
 
-// dQ = tau dS' K_col, query-major: a workgroup of 8 waves owns 256 queries
-// of one (batch, query head), wave w one 32-query block and all Dqk channels.
+// dQ = tau dS' K_col, query-major: a workgroup of 4 waves owns 128 queries
+// of one (batch, query head), wave w one 32-query block and all Dqk channels
+// (small workgroups: several per CU keep more unit loads in flight).
 // Per 64-key step up to the diagonal: the A operand is the stored unit (32
 // bytes per lane, already in operand order, prefetched into registers one
 // step ahead); the K col tile of the step [Dqk][64] and its scales reach LDS
-// by direct loads, double-buffered and shared by the 8 waves.  Keys past the
+// by direct loads, double-buffered and shared by the 4 waves.  Keys past the
 // sequence meet zero dS' codes (their K loads are clamped into the array).
 template <int DQK>
-__global__ __launch_bounds__(512) void dq_kernel(AttnArgs a) {
-  constexpr int CQ = DQK / 32, NW = 8;
+__global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
+  constexpr int CQ = DQK / 32, NW = 4;
   constexpr int KT = DQK * 64, KSB = 2 * DQK;       // K tile and scale bytes per step
   __shared__ __attribute__((aligned(16))) uint8_t kA[KT + KSB];
   __shared__ __attribute__((aligned(16))) uint8_t kB[KT + KSB];
@@ -697,12 +698,12 @@ __global__ __launch_bounds__(512) void dq_kernel(AttnArgs a) {
 }
 
 hipError_t launch_dq(const AttnArgs& a, int dqk, hipStream_t s) {
-  const dim3 grid((unsigned)((a.N / 32 + 7) / 8 * a.Hq * a.B));
+  const dim3 grid((unsigned)((a.N / 32 + 3) / 4 * a.Hq * a.B));
   switch (dqk) {
-    case 64: hipLaunchKernelGGL((dq_kernel<64>), grid, dim3(512), 0, s, a); break;
-    case 128: hipLaunchKernelGGL((dq_kernel<128>), grid, dim3(512), 0, s, a); break;
-    case 192: hipLaunchKernelGGL((dq_kernel<192>), grid, dim3(512), 0, s, a); break;
-    case 256: hipLaunchKernelGGL((dq_kernel<256>), grid, dim3(512), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((dq_kernel<64>), grid, dim3(256), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((dq_kernel<128>), grid, dim3(256), 0, s, a); break;
+    case 192: hipLaunchKernelGGL((dq_kernel<192>), grid, dim3(256), 0, s, a); break;
+    case 256: hipLaunchKernelGGL((dq_kernel<256>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
