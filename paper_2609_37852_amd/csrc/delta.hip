@@ -114,16 +114,14 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
       reinterpret_cast<float*>(st + C::KH_OFF)[threadIdx.x] = hot >= 0 ? scaled_value(khc, khs) : 0.f;
   };
 
-  // one 32-key group (keys j0 + 32 g ..) of the tile in st; DIAG: the group
-  // holding the wave's diagonal (keys after the query masked)
-  auto group = [&](const uint8_t* st, int g, auto diag_tag) __attribute__((always_inline)) {
-    constexpr bool DIAG = decltype(diag_tag)::value;
+  // Scores (with the rank-2 update) and dP of one 32-key group (keys
+  // j0 + 32 g ..) of the tile in st.
+  auto group_mfma = [&](const uint8_t* st, int g, v16f& s, v16f& dp) __attribute__((always_inline)) {
     const uint8_t* K = st + C::K_OFF;
     const uint8_t* Ks = st + C::KS_OFF;
     const uint8_t* V = st + C::V_OFF;
     const uint8_t* Vs = st + C::VS_OFF;
     const float* Kh = reinterpret_cast<const float*>(st + C::KH_OFF);
-    v16f s, dp;
 #pragma unroll
     for (int r = 0; r < 16; r++) { s[r] = 0.f; dp[r] = 0.f; }
 #pragma unroll
@@ -137,7 +135,12 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
     // S + k_c* q_c* - LSE / tau: A = isolated-channel key value (lanes
     // < 32) or 1 (lanes >= 32), B = qv
     s = rank2_update(hf ? 1.0f : Kh[32 * g + li], qv, s);
-    // lane holds keys 32 g + 8 (r/4) + 4 hf + r % 4 of the tile, query qi
+  };
+  // P, then the group's sums of P dP and P; DIAG: the group holding the
+  // wave's diagonal (keys after the query masked).  The lane holds keys
+  // 32 g + 8 (r/4) + 4 hf + r % 4 of the tile, query qi.
+  auto group_sums = [&](const v16f& s, const v16f& dp, auto diag_tag) __attribute__((always_inline)) {
+    constexpr bool DIAG = decltype(diag_tag)::value;
     float pn = 0.f, pd = 0.f;
 #pragma unroll
     for (int q4 = 0; q4 < 4; q4++) {
@@ -157,19 +160,27 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
 
   auto tile = [&](const uint8_t* st, int j0) __attribute__((always_inline)) {
     if (!live || j0 > q0) return;
+    v16f s0, dp0, s1, dp1;
     if (j0 + BK <= q0) {
-      // wholly before the wave's queries: every group, no mask, no branch
-      // between groups (so one group's MFMAs can overlap another's VALU)
+      // wholly before the wave's queries: every group, no mask; the MFMAs of
+      // group g + 1 are issued before the vector work of group g
+      group_mfma(st, 0, s0, dp0);
 #pragma unroll
-      for (int g = 0; g < BK / 32; g++) group(st, g, std::false_type{});
+      for (int g = 0; g < BK / 32; g += 2) {
+        group_mfma(st, g + 1, s1, dp1);
+        group_sums(s0, dp0, std::false_type{});
+        if (g + 2 < BK / 32) group_mfma(st, g + 2, s0, dp0);
+        group_sums(s1, dp1, std::false_type{});
+      }
       return;
     }
 #pragma unroll
     for (int g = 0; g < BK / 32; g++) {
       const int g0 = j0 + 32 * g;              // first key of the group
       if (g0 > q0) break;                      // this and later groups are in the wave's future
-      if (g0 == q0) group(st, g, std::true_type{});
-      else group(st, g, std::false_type{});
+      group_mfma(st, g, s0, dp0);
+      if (g0 == q0) group_sums(s0, dp0, std::true_type{});
+      else group_sums(s0, dp0, std::false_type{});
     }
   };
 
