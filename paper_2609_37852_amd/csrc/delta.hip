@@ -97,9 +97,13 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   // loads of tile j0 (raw isolated-channel bytes in registers, decoded when
   // they are stored to LDS)
   uint32_t khc = 0, khs = 0;
+  RowLoads<DQK, NW, BK> kload;
+  RowLoads<DV, NW, BK> vload;
+  kload.init(w, lane);
+  vload.init(w, lane);
   auto issue = [&](lds8* st, int j0) __attribute__((always_inline)) {
-    dma_rows<DQK, NW, BK>(st + C::K_OFF, kcode, j0, N, w, lane);
-    dma_rows<DV, NW, BK>(st + C::V_OFF, vcode, j0, N, w, lane);
+    kload.issue(st + C::K_OFF, kcode, j0, N, w, lane);
+    vload.issue(st + C::V_OFF, vcode, j0, N, w, lane);
     dma_row_scales<DQK, NW, BK>(st + C::KS_OFF, kscale, j0, N, w, lane, 0);
     dma_row_scales<DV, NW, BK>(st + C::VS_OFF, vscale, j0, N, w, lane, 1);
     if (hot >= 0 && threadIdx.x < BK) {

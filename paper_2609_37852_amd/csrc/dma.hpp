@@ -117,18 +117,22 @@ __device__ __forceinline__ v8i frag_cols_swz(const uint8_t* tile, int ch, int hf
 }
 
 // Precomputed plans for the tile loads of one wave: the lane's byte offset in
-// the source matrix for each of its load instructions (k = w + NWK j), so a
-// whole tile costs one address add per load.  A tile that reaches past the
-// sequence end takes the clamping loaders above instead.
+// the source matrix for its first load instruction (k = w); the later ones
+// (k = w + NWK j) sit a fixed stride further wherever the swizzle repeats
+// with that stride, so a whole tile costs one address add per load.  A tile
+// that reaches past the sequence end takes the clamping loaders above.
 //
 // Row tile: rows [i0, i0 + ROWS) of a [N][D] code matrix -> LDS [ROWS][D].
 template <int D, int NWK, int ROWS>
 struct RowLoads {
   static constexpr int NI = ROWS * D / 1024, NS = (NI + NWK - 1) / NWK;
-  uint32_t off[NS];   // r D + 16 (swizzled chunk), r the lane's row in the tile
+  // the instructions of one wave are 1024 NWK / D rows apart; the swizzle
+  // repeats every 16 rows for every D but 192
+  static constexpr bool STRIDED = (1024 * NWK) % D == 0 && ((1024 * NWK) / D) % 16 == 0;
+  uint32_t off[STRIDED ? 1 : NS];   // r D + 16 (swizzled chunk), r the lane's row in the tile
   __device__ __forceinline__ void init(int w, int lane) {
 #pragma unroll
-    for (int j = 0; j < NS; j++) {
+    for (int j = 0; j < (STRIDED ? 1 : NS); j++) {
       const int o = 1024 * (w + NWK * j) + 16 * lane;
       const int r = o / D, p = (o % D) / 16;
       off[j] = (uint32_t)(r * D + 16 * (p ^ swz_row<D>(r)));
@@ -143,35 +147,50 @@ struct RowLoads {
 #pragma unroll
     for (int j = 0; j < NS; j++) {
       const int k = w + NWK * j;
-      if (k < NI) dma16(base + off[j], lds + 1024 * k);
+      if (k < NI) dma16(base + (STRIDED ? off[0] + 1024 * NWK * j : off[j]), lds + 1024 * k);
     }
   }
 };
 
-// Col tile: channels [0, D), sequence positions [i0, i0 + 64) of a [D][N]
-// code matrix -> LDS [D][64].
-template <int D, int NWK>
+// Col tile: channels [0, D), sequence positions [i0, i0 + COLS) of a [D][N]
+// code matrix -> LDS [D][COLS] (COLS = 64: the col-tile swizzle; 128: the
+// 128-byte row swizzle; both repeat with the channel step of one wave's
+// instructions).
+template <int D, int NWK, int COLS = 64>
 struct ColLoads {
-  static constexpr int NI = D * 64 / 1024, NS = (NI + NWK - 1) / NWK;
-  uint32_t off[NS];   // c N + 16 q (q the swizzled chunk)
+  static_assert(COLS == 64 || COLS == 128, "col tile width");
+  static constexpr int NI = D * COLS / 1024, NS = (NI + NWK - 1) / NWK;
+  static constexpr int CSTEP = 1024 * NWK / COLS;   // channels between a wave's instructions
+  static_assert(CSTEP % 16 == 0, "swizzle period");
+  uint32_t off;   // c N + 16 q of the first instruction (q the swizzled chunk)
+  int cstride;    // CSTEP N
   __device__ __forceinline__ void init(int w, int lane, int N) {
-#pragma unroll
-    for (int j = 0; j < NS; j++) {
-      const int o = 1024 * (w + NWK * j) + 16 * lane;
-      const int c = o / 64, p = (o % 64) / 16;
-      off[j] = (uint32_t)(c * N + 16 * (p ^ swz_col(c)));
-    }
+    const int o = 1024 * w + 16 * lane;
+    const int c = o / COLS, p = (o % COLS) / 16;
+    const int q = COLS == 64 ? (p ^ swz_col(c)) : (p ^ swz_row<128>(c));
+    off = (uint32_t)(c * N + 16 * q);
+    cstride = CSTEP * N;
   }
   __device__ __forceinline__ void issue(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) const {
-    if (i0 + 64 > N) {
-      dma_cols<D, NWK>(lds, code, i0, N, w, lane);
+    if (i0 + COLS > N) {
+      // ragged tile: clamp every 16-byte piece into its row
+#pragma unroll
+      for (int j = 0; j < NS; j++) {
+        const int k = w + NWK * j;
+        if (k >= NI) break;
+        const int o = 1024 * k + 16 * lane;
+        const int c = o / COLS, p = (o % COLS) / 16;
+        const int q = COLS == 64 ? (p ^ swz_col(c)) : (p ^ swz_row<128>(c));
+        const int col = i0 + 16 * q < N - 16 ? i0 + 16 * q : N - 16;
+        dma16(code + c * N + col, lds + 1024 * k);
+      }
       return;
     }
-    const uint8_t* base = code + i0;
+    const uint8_t* base = code + i0 + off;
 #pragma unroll
     for (int j = 0; j < NS; j++) {
       const int k = w + NWK * j;
-      if (k < NI) dma16(base + off[j], lds + 1024 * k);
+      if (k < NI) dma16(base + (size_t)j * cstride, lds + 1024 * k);
     }
   }
 };

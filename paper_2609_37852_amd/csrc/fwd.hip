@@ -65,21 +65,6 @@ struct FwdCfg {
   static_assert(BQ % BK == 0, "a query block's diagonal starts a key tile");
 };
 
-// Col-copy code tile: channels [0, D), keys [j0, j0 + 128) (clamped to the
-// sequence) into LDS [D][128] with the 128-byte row swizzle; wave w issues
-// instructions w, w + NW, ...
-template <int D, int NW>
-__device__ __forceinline__ void dma_cols128(lds8* lds, const uint8_t* code, int j0, int N, int w, int lane) {
-  constexpr int NI = D * 128 / 1024;
-  for (int k = w; k < NI; k += NW) {
-    const int off = 1024 * k + 16 * lane;
-    const int c = off / 128, p = (off % 128) / 16;
-    const int q = p ^ swz_row<128>(c);
-    const int col = j0 + 16 * q < N - 16 ? j0 + 16 * q : N - 16;
-    dma16(code + c * N + col, lds + 1024 * k);
-  }
-}
-
 template <int DQK, int DV>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   using C = FwdCfg<DQK, DV>;
@@ -135,10 +120,13 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   // through registers, written by finish().
   uint32_t vsr[BK / 32] = {};
   uint32_t khc = 0, khs = 0;
+  RowLoads<DQK, NW, BK> kload;
+  ColLoads<DV, NW, BK> vload;
+  kload.init(w, lane);
+  vload.init(w, lane, N);
   auto issue = [&](lds8* st, int j0) __attribute__((always_inline)) {
-    dma_rows<DQK, NW, BK>(st + C::K_OFF, kcode, j0, N, w, lane);
-    if constexpr (BK == 128) dma_cols128<DV, NW>(st + C::V_OFF, vcode, j0, N, w, lane);
-    else dma_cols<DV, NW>(st + C::V_OFF, vcode, j0, N, w, lane);
+    kload.issue(st + C::K_OFF, kcode, j0, N, w, lane);
+    vload.issue(st + C::V_OFF, vcode, j0, N, w, lane);
     dma_row_scales<DQK, NW, BK>(st + C::KS_OFF, kscale, j0, N, w, lane, 0);
     if (threadIdx.x < DV) {
 #pragma unroll
