@@ -2,11 +2,14 @@
 // (App. B.6.1 with 1x32 / 32x1 blocks).  HBM-bound: one pass reads x once and
 // writes both copies.
 //
-// One workgroup = 32 tokens x D channels of one (batch, head), 2*D threads.
-//   row copy: thread t owns token t / (D/16) and 16 channels; a 1x32 block
-//             spans the thread and its neighbour t ^ 1.
-//   col copy: the tile is transposed through LDS; thread t owns channel t / 2
-//             and 16 tokens; a 32x1 block spans t and t ^ 1.
+// One workgroup = 64 tokens x D channels of one (batch, head), 2*D threads
+// (two loads in flight per thread).
+//   row copy: thread t owns tokens t / (D/16) and 32 + t / (D/16), 16
+//             channels each; a 1x32 block spans the thread and its
+//             neighbour t ^ 1.
+//   col copy: the tile is transposed through LDS (BF16 inputs kept BF16);
+//             thread t owns channel t / 2 and the 32 tokens of block t % 2,
+//             one whole 32x1 block.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -58,46 +61,95 @@ __device__ __forceinline__ float amax16(const float (&v)[16]) {
   return m;
 }
 
+// Input values as kept in the transpose tile: BF16 inputs stay BF16 (exact).
+template <typename T> struct TileOf { typedef float type; };
+template <> struct TileOf<uint16_t> { typedef uint16_t type; };
+__device__ __forceinline__ float tile_get(float x) { return x; }
+__device__ __forceinline__ float tile_get(uint16_t x) { return __uint_as_float((uint32_t)x << 16); }
+__device__ __forceinline__ void tile_put(float& d, float x) { d = x; }
+__device__ __forceinline__ void tile_put(uint16_t& d, float x) { d = (uint16_t)(__float_as_uint(x) >> 16); }
+
+// Codes of 32 values for one block exponent e.
+__device__ __forceinline__ void encode32(const float (&v)[32], int e, uint4& lo, uint4& hi) {
+  uint32_t w[8];
+#pragma unroll
+  for (int k = 0; k < 8; k++)
+    w[k] = cvt4(__builtin_ldexpf(v[4 * k], -e), __builtin_ldexpf(v[4 * k + 1], -e),
+                __builtin_ldexpf(v[4 * k + 2], -e), __builtin_ldexpf(v[4 * k + 3], -e));
+  lo = make_uint4(w[0], w[1], w[2], w[3]);
+  hi = make_uint4(w[4], w[5], w[6], w[7]);
+}
+
+// One workgroup = 64 tokens (two 32-token blocks; the second may lie past the
+// end when N % 64 == 32) x D channels of one (batch, head), 2*D threads.
 template <int D, typename T>
 __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
   constexpr int CH = D / 16;  // 16-channel chunks per token
-  __shared__ float tile[32][D + 1];
+  typedef typename TileOf<T>::type TT;
+  __shared__ TT tile[64][D + (sizeof(TT) == 2 ? 2 : 1)];
   const int t = threadIdx.x;
-  const int64_t n0 = (int64_t)blockIdx.x * 32, h = blockIdx.y, b = blockIdx.z;
+  const int64_t n0 = (int64_t)blockIdx.x * 64, h = blockIdx.y, b = blockIdx.z;
   const int64_t bh = b * a.H + h;
+  const bool two = n0 + 64 <= a.N;            // both 32-token blocks inside the sequence
   const int tok = t / CH, ch = (t % CH) * 16;
-  float v[16];
-  load16<T>(reinterpret_cast<const T*>(a.x) + b * a.sb + (n0 + tok) * a.sn + h * a.sh + ch, v);
+  const T* src = reinterpret_cast<const T*>(a.x) + b * a.sb + h * a.sh + ch;
+  float v0[16], v1[16];
+  load16<T>(src + (n0 + tok) * a.sn, v0);
+  if (two) load16<T>(src + (n0 + 32 + tok) * a.sn, v1);
+  else {
+#pragma unroll
+    for (int k = 0; k < 16; k++) v1[k] = 0.f;
+  }
 
   if (a.nonfinite) {
     uint32_t bad = 0;
 #pragma unroll
-    for (int k = 0; k < 16; k++) bad += __builtin_isfinite(v[k]) ? 0u : 1u;
+    for (int k = 0; k < 16; k++) bad += (__builtin_isfinite(v0[k]) ? 0u : 1u) + (__builtin_isfinite(v1[k]) ? 0u : 1u);
     if (bad) atomicAdd(a.nonfinite, bad);
   }
   if (a.which & 1) {
-    float am = amax16(v);
-    am = fmaxf(am, __shfl_xor(am, 1));
-    const int e = pow2_exponent(am);
-    *reinterpret_cast<uint4*>(a.code_row + (bh * a.N + n0 + tok) * D + ch) = encode16(v, e);
-    if ((t & 1) == 0) a.scale_row[(bh * a.N + n0 + tok) * (D / 32) + ch / 32] = (uint8_t)(e + 127);
+#pragma unroll
+    for (int u = 0; u < 2; u++) {
+      if (u == 1 && !two) break;
+      const float (&v)[16] = u ? v1 : v0;
+      const int64_t n = n0 + 32 * u + tok;
+      float am = amax16(v);
+      am = fmaxf(am, __shfl_xor(am, 1));
+      const int e = pow2_exponent(am);
+      *reinterpret_cast<uint4*>(a.code_row + (bh * a.N + n) * D + ch) = encode16(v, e);
+      if ((t & 1) == 0) a.scale_row[(bh * a.N + n) * (D / 32) + ch / 32] = (uint8_t)(e + 127);
+    }
   }
   if (a.which & 2) {
 #pragma unroll
-    for (int k = 0; k < 16; k++) tile[tok][ch + k] = v[k];
+    for (int k = 0; k < 16; k++) {
+      tile_put(tile[tok][ch + k], v0[k]);
+      tile_put(tile[32 + tok][ch + k], v1[k]);
+    }
     __syncthreads();
-    const int c = t >> 1, half = t & 1;
-    float w[16];
+    // thread (channel c, block u): the 32 tokens of col block u
+    const int c = t >> 1, u = t & 1;
+    const bool valid = u == 0 || two;          // block u inside the sequence
+    float w[32];
 #pragma unroll
-    for (int k = 0; k < 16; k++) w[k] = tile[half * 16 + k][c];
-    float am = amax16(w);
-    am = fmaxf(am, __shfl_xor(am, 1));
-    const int e = pow2_exponent(am);
-    *reinterpret_cast<uint4*>(a.code_col + (bh * D + c) * a.N + n0 + half * 16) = encode16(w, e);
-    if (half == 0) {
-      a.scale_col[(bh * D + c) * (a.N / 32) + n0 / 32] = (uint8_t)(e + 127);
-      // non-negative FP32 values order like their bit patterns
-      if (a.chan_amax) atomicMax(reinterpret_cast<unsigned int*>(a.chan_amax + bh * D + c), __float_as_uint(am));
+    for (int k = 0; k < 32; k++) w[k] = tile_get(tile[32 * u + k][c]);
+    float am = 0.f;
+#pragma unroll
+    for (int k = 0; k < 32; k++) am = fmaxf(am, fabsf(w[k]));
+    am = valid ? am : 0.f;
+    if (valid) {
+      const int e = pow2_exponent(am);
+      uint4 lo, hi;
+      encode32(w, e, lo, hi);
+      uint4* dst = reinterpret_cast<uint4*>(a.code_col + (bh * D + c) * a.N + n0 + 32 * u);
+      dst[0] = lo;
+      dst[1] = hi;
+      a.scale_col[(bh * D + c) * (a.N / 32) + n0 / 32 + u] = (uint8_t)(e + 127);
+    }
+    // non-negative FP32 values order like their bit patterns
+    if (a.chan_amax) {
+      const float am2 = fmaxf(am, __shfl_xor(am, 1));   // both blocks of the channel
+      if (u == 0) atomicMax(reinterpret_cast<unsigned int*>(a.chan_amax + bh * D + c), __float_as_uint(am2));
     }
   }
 }
@@ -105,7 +157,7 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 
 hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_t s) {
-  dim3 grid((unsigned)(a.N / 32), (unsigned)a.H, (unsigned)a.B);
+  dim3 grid((unsigned)((a.N + 63) / 64), (unsigned)a.H, (unsigned)a.B);
   if (a.chan_amax) {
     const hipError_t e = launch_fill_zero(a.chan_amax, a.B * a.H * D, s);
     if (e != hipSuccess) return e;
