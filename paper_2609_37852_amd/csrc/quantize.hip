@@ -2,14 +2,14 @@
 // (App. B.6.1 with 1x32 / 32x1 blocks).  HBM-bound: one pass reads x once and
 // writes both copies.
 //
-// One workgroup = 64 tokens x D channels of one (batch, head), 2*D threads
-// (two loads in flight per thread).
-//   row copy: thread t owns tokens t / (D/16) and 32 + t / (D/16), 16
-//             channels each; a 1x32 block spans the thread and its
-//             neighbour t ^ 1.
+// One workgroup = 64 tokens (2 blocks of 32) x D channels of one (batch,
+// head), 2*D threads (two loads in flight per thread; 4 blocks measured
+// slower).
+//   row copy: thread t owns tokens 32 u + t / (D/16), 16 channels each; a
+//             1x32 block spans the thread and its neighbour t ^ 1.
 //   col copy: the tile is transposed through LDS (BF16 inputs kept BF16);
-//             thread t owns channel t / 2 and the 32 tokens of block t % 2,
-//             one whole 32x1 block.
+//             thread t owns channel t / 2 and the whole 32x1 block t % 2 of
+//             that channel.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -80,76 +80,83 @@ __device__ __forceinline__ void encode32(const float (&v)[32], int e, uint4& lo,
   hi = make_uint4(w[4], w[5], w[6], w[7]);
 }
 
-// One workgroup = 64 tokens (two 32-token blocks; the second may lie past the
-// end when N % 64 == 32) x D channels of one (batch, head), 2*D threads.
-template <int D, typename T>
+// One workgroup = 32 NB tokens (NB 32-token blocks; the last ones may lie
+// past the end of the sequence) x D channels of one (batch, head), 2*D threads.
+template <int D, typename T, int NB>
 __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
   constexpr int CH = D / 16;  // 16-channel chunks per token
   typedef typename TileOf<T>::type TT;
-  __shared__ TT tile[64][D + (sizeof(TT) == 2 ? 2 : 1)];
+  __shared__ TT tile[32 * NB][D + (sizeof(TT) == 2 ? 2 : 1)];
   const int t = threadIdx.x;
-  const int64_t n0 = (int64_t)blockIdx.x * 64, h = blockIdx.y, b = blockIdx.z;
+  const int64_t n0 = (int64_t)blockIdx.x * 32 * NB, h = blockIdx.y, b = blockIdx.z;
   const int64_t bh = b * a.H + h;
-  const bool two = n0 + 64 <= a.N;            // both 32-token blocks inside the sequence
+  const int nb = (int)((a.N - n0) / 32 < NB ? (a.N - n0) / 32 : NB);   // blocks inside the sequence
   const int tok = t / CH, ch = (t % CH) * 16;
   const T* src = reinterpret_cast<const T*>(a.x) + b * a.sb + h * a.sh + ch;
-  float v0[16], v1[16];
-  load16<T>(src + (n0 + tok) * a.sn, v0);
-  if (two) load16<T>(src + (n0 + 32 + tok) * a.sn, v1);
-  else {
+  float v[NB][16];
 #pragma unroll
-    for (int k = 0; k < 16; k++) v1[k] = 0.f;
+  for (int u = 0; u < NB; u++) {
+    if (u < nb) load16<T>(src + (n0 + 32 * u + tok) * a.sn, v[u]);
+    else {
+#pragma unroll
+      for (int k = 0; k < 16; k++) v[u][k] = 0.f;
+    }
   }
 
   if (a.nonfinite) {
     uint32_t bad = 0;
 #pragma unroll
-    for (int k = 0; k < 16; k++) bad += (__builtin_isfinite(v0[k]) ? 0u : 1u) + (__builtin_isfinite(v1[k]) ? 0u : 1u);
+    for (int u = 0; u < NB; u++)
+#pragma unroll
+      for (int k = 0; k < 16; k++) bad += __builtin_isfinite(v[u][k]) ? 0u : 1u;
     if (bad) atomicAdd(a.nonfinite, bad);
   }
   if (a.which & 1) {
 #pragma unroll
-    for (int u = 0; u < 2; u++) {
-      if (u == 1 && !two) break;
-      const float (&v)[16] = u ? v1 : v0;
+    for (int u = 0; u < NB; u++) {
+      if (u >= nb) break;
       const int64_t n = n0 + 32 * u + tok;
-      float am = amax16(v);
+      float am = amax16(v[u]);
       am = fmaxf(am, __shfl_xor(am, 1));
       const int e = pow2_exponent(am);
-      *reinterpret_cast<uint4*>(a.code_row + (bh * a.N + n) * D + ch) = encode16(v, e);
+      *reinterpret_cast<uint4*>(a.code_row + (bh * a.N + n) * D + ch) = encode16(v[u], e);
       if ((t & 1) == 0) a.scale_row[(bh * a.N + n) * (D / 32) + ch / 32] = (uint8_t)(e + 127);
     }
   }
   if (a.which & 2) {
 #pragma unroll
-    for (int k = 0; k < 16; k++) {
-      tile_put(tile[tok][ch + k], v0[k]);
-      tile_put(tile[32 + tok][ch + k], v1[k]);
-    }
+    for (int u = 0; u < NB; u++)
+#pragma unroll
+      for (int k = 0; k < 16; k++) tile_put(tile[32 * u + tok][ch + k], v[u][k]);
     __syncthreads();
-    // thread (channel c, block u): the 32 tokens of col block u
-    const int c = t >> 1, u = t & 1;
-    const bool valid = u == 0 || two;          // block u inside the sequence
-    float w[32];
+    // thread (channel c, parity u0): the 32 tokens of col blocks u0, u0 + 2, ..
+    const int c = t >> 1, u0 = t & 1;
+    float cam = 0.f;
 #pragma unroll
-    for (int k = 0; k < 32; k++) w[k] = tile_get(tile[32 * u + k][c]);
-    float am = 0.f;
+    for (int u = u0; u < NB; u += 2) {
+      const bool valid = u < nb;
+      float w[32];
 #pragma unroll
-    for (int k = 0; k < 32; k++) am = fmaxf(am, fabsf(w[k]));
-    am = valid ? am : 0.f;
-    if (valid) {
-      const int e = pow2_exponent(am);
-      uint4 lo, hi;
-      encode32(w, e, lo, hi);
-      uint4* dst = reinterpret_cast<uint4*>(a.code_col + (bh * D + c) * a.N + n0 + 32 * u);
-      dst[0] = lo;
-      dst[1] = hi;
-      a.scale_col[(bh * D + c) * (a.N / 32) + n0 / 32 + u] = (uint8_t)(e + 127);
+      for (int k = 0; k < 32; k++) w[k] = tile_get(tile[32 * u + k][c]);
+      float am = 0.f;
+#pragma unroll
+      for (int k = 0; k < 32; k++) am = fmaxf(am, fabsf(w[k]));
+      am = valid ? am : 0.f;
+      cam = fmaxf(cam, am);
+      if (valid) {
+        const int e = pow2_exponent(am);
+        uint4 lo, hi;
+        encode32(w, e, lo, hi);
+        uint4* dst = reinterpret_cast<uint4*>(a.code_col + (bh * D + c) * a.N + n0 + 32 * u);
+        dst[0] = lo;
+        dst[1] = hi;
+        a.scale_col[(bh * D + c) * (a.N / 32) + n0 / 32 + u] = (uint8_t)(e + 127);
+      }
     }
     // non-negative FP32 values order like their bit patterns
     if (a.chan_amax) {
-      const float am2 = fmaxf(am, __shfl_xor(am, 1));   // both blocks of the channel
-      if (u == 0) atomicMax(reinterpret_cast<unsigned int*>(a.chan_amax + bh * D + c), __float_as_uint(am2));
+      const float am2 = fmaxf(cam, __shfl_xor(cam, 1));   // every block of the channel
+      if (u0 == 0) atomicMax(reinterpret_cast<unsigned int*>(a.chan_amax + bh * D + c), __float_as_uint(am2));
     }
   }
 }
@@ -157,15 +164,16 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 
 hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_t s) {
-  dim3 grid((unsigned)((a.N + 63) / 64), (unsigned)a.H, (unsigned)a.B);
+  constexpr int NB = 2;
+  dim3 grid((unsigned)((a.N + 32 * NB - 1) / (32 * NB)), (unsigned)a.H, (unsigned)a.B);
   if (a.chan_amax) {
     const hipError_t e = launch_fill_zero(a.chan_amax, a.B * a.H * D, s);
     if (e != hipSuccess) return e;
   }
 #define AFP8_Q(DD)                                                                           \
   if (D == DD) {                                                                             \
-    if (dtype_bf16) hipLaunchKernelGGL((quantize_kernel<DD, uint16_t>), grid, dim3(2 * DD), 0, s, a); \
-    else hipLaunchKernelGGL((quantize_kernel<DD, float>), grid, dim3(2 * DD), 0, s, a);       \
+    if (dtype_bf16) hipLaunchKernelGGL((quantize_kernel<DD, uint16_t, NB>), grid, dim3(2 * DD), 0, s, a); \
+    else hipLaunchKernelGGL((quantize_kernel<DD, float, NB>), grid, dim3(2 * DD), 0, s, a);       \
     return hipGetLastError();                                                                \
   }
   AFP8_Q(64)
