@@ -55,6 +55,12 @@ struct BwdCfg {
   // 32-query half of the tile; after exchanging codes through LDS the first
   // accumulates dV and the second dK for all channels of their keys.
   static constexpr int NWK = 8, KBW = 4;
+  // the direct loads of the query tiles are issued by the first wave of each
+  // key block only (one wave per SIMD; these also store the dQ units), so the
+  // other four issue no vector memory instructions: spread over all eight,
+  // every wave stalls behind the burst of load instructions at the start of
+  // a tile
+  static constexpr int NLD = 4;
   static constexpr int NT = 64 * NWK, BKB = 32 * KBW, BQ = 64;
   static constexpr int DST = BQ + 16;   // row stride of the dS' tile [key][query]
   static constexpr int al16(int x) { return (x + 15) & ~15; }
@@ -111,13 +117,15 @@ __device__ __forceinline__ BwdHead bwd_head(const AttnArgs& a, size_t bh, int N)
   return p;
 }
 
-// Load plans of one wave for the code tiles of a query tile.
+// Load plans of one loading wave (index w among the NLD) for the code tiles
+// of a query tile.
 template <int DQK, int DV>
 struct BwdLoads {
-  RowLoads<DQK, 8, 64> q;
-  RowLoads<DV, 8, 64> o;
-  ColLoads<DQK, 8> qc;
-  ColLoads<DV, 8> oc;
+  static constexpr int NL = BwdCfg<DQK, DV>::NLD;
+  RowLoads<DQK, NL, 64> q;
+  RowLoads<DV, NL, 64> o;
+  ColLoads<DQK, NL> qc;
+  ColLoads<DV, NL> oc;
   __device__ __forceinline__ void init(int w, int lane, int N) {
     q.init(w, lane);
     o.init(w, lane);
@@ -126,14 +134,22 @@ struct BwdLoads {
   }
 };
 
+// Index of this wave among the loading waves (the first NLD), or -1.
+template <int DQK, int DV>
+__device__ __forceinline__ int loader_index() {
+  using C = BwdCfg<DQK, DV>;
+  const int w = (int)(threadIdx.x >> 6);
+  return w < C::NLD ? w : -1;
+}
+
 // Direct-to-LDS loads of the row part of one query tile: codes, row scales
 // and the per-query records.
 template <int DQK, int DV>
 __device__ __forceinline__ void stage_rows(lds8* st, const BwdLoads<DQK, DV>& L, const BwdHead& hp, int i0, int N) {
   using C = BwdCfg<DQK, DV>;
-  constexpr int NWK = C::NWK;
-  static_assert(NWK == 8, "load plans assume 8 waves");
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  constexpr int NWK = C::NLD;
+  const int lane = threadIdx.x & 63, w = loader_index<DQK, DV>();
+  if (w < 0) return;
   L.q.issue(st + C::Q_OFF, hp.qrow, i0, N, w, lane);
   L.o.issue(st + C::O_OFF, hp.orow, i0, N, w, lane);
   dma_row_scales<DQK, NWK>(st + C::QS_OFF, hp.qsc, i0, N, w, lane, 0);
@@ -148,14 +164,15 @@ __device__ __forceinline__ void stage_rows(lds8* st, const BwdLoads<DQK, DV>& L,
 template <int DQK, int DV>
 __device__ __forceinline__ void stage_cols(lds8* st, const BwdLoads<DQK, DV>& L, const BwdHead& hp, int i0, int N) {
   using C = BwdCfg<DQK, DV>;
-  constexpr int NWK = C::NWK;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  constexpr int NWK = C::NLD;
+  const int lane = threadIdx.x & 63, w = loader_index<DQK, DV>();
+  if (w < 0) return;
   L.qc.issue(st + C::QC_OFF, hp.qcol, i0, N, w, lane);
   L.oc.issue(st + C::OC_OFF, hp.ocol, i0, N, w, lane);
   constexpr int NCI = (C::CS_BYTES + 255) / 256;
   const uint8_t* tcs = hp.tcs + (i0 / 64) * C::CS_BYTES;
   for (int k = 0; k < NCI; k++) {
-    if ((4 + k) % NWK != w) continue;
+    if ((2 + k) % NWK != w) continue;   // loaders 2, 3, ...: 0 and 1 take the row scales
     const int off = 256 * k + 4 * lane;
     if (off < C::CS_BYTES) dma4(tcs + off, st + C::QCS_OFF + 256 * k);
   }
@@ -172,12 +189,45 @@ __device__ __forceinline__ float half_max(float v) {
   return v;
 }
 
+// Order of the key blocks in the grid (slot s = workgroup id / (B Hkv)).  The
+// blocks pair up as j and nkb - 1 - j (the pair's tile counts add to the same
+// total for every j).  In cohorts of P pairs, P the number of workgroups of
+// one KV head that run at once: first the long blocks j of the cohort, their
+// query tiles visited downwards from the end of the sequence, then the
+// partners, upwards from their diagonal, in the order the long blocks finish
+// (workgroups start in id order as earlier ones end, so each partner takes
+// the place of its own long block); a middle block (odd nkb) last.  With
+// nqt = 2 nkb query tiles, the workgroups of a cohort then stand at tile
+// nqt - 1 - t or t - 2 at step t, whichever block they hold: they read at
+// most two distinct tiles at a time and share them in the L2 (the workgroups
+// of one KV head run on one XCD).
+struct KeyBlock {
+  int kb;
+  bool up;
+};
+__device__ __forceinline__ KeyBlock key_block_of(int s, int nkb, int P) {
+  const int npair = nkb / 2, F = npair / P;
+  int cohort, o, m;
+  if (s < 2 * P * F) {
+    cohort = s / (2 * P);
+    o = s % (2 * P);
+    m = P;
+  } else {
+    cohort = F;
+    o = s - 2 * P * F;
+    m = npair - F * P;
+  }
+  const int j0 = cohort * P;
+  if (o < m) return KeyBlock{j0 + o, false};
+  if (o < 2 * m) return KeyBlock{nkb - 1 - (j0 + m - 1 - (o - m)), true};
+  return KeyBlock{npair, false};
+}
+
 // Position of a query tile in the workgroup's loop: query head kh G + hi,
-// 64 queries from (nqt - 1 - r) * 64.  The loop runs r from the end of the
-// sequence down to the diagonal and, for each r, over the G query heads, so
-// every workgroup of one KV head (they start together) visits the same
-// (r, hi) sequence and stops at its own diagonal: the workgroups stay in
-// step and share each query tile in the L2.
+// step r along the sequence (the G query heads of a step are consecutive);
+// its 64 queries start at (nqt - 1 - r) * 64 when the tiles are visited
+// downwards from the end of the sequence, at (qt0 + r) * 64 when upwards
+// from the key block's diagonal tile qt0.
 struct TilePos {
   int hi, r;
 };
@@ -211,11 +261,13 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   const int kbw = w % KBW;                      // this wave's 32-key block within the workgroup
   const int qs = w / KBW;                       // and its 32-query half of every tile
   const int N = (int)a.N;
-  // workgroup id -> key block (slowest: block 0 has the most work and goes
-  // first) and (batch, KV head) (fastest: the key blocks of one KV head get
-  // ids equal mod 16, hence one XCD and its L2 when B * Hkv % 8 == 0)
+  // workgroup id -> key block (slowest, in the order of key_block_of) and
+  // (batch, KV head) (fastest: the key blocks of one KV head get ids equal
+  // mod 16, hence one XCD and its L2 when B * Hkv % 8 == 0)
   const int GI = (int)(a.B * a.Hkv);
-  const int kb0 = ((int)blockIdx.x / GI) * BKB;
+  const KeyBlock kbk = key_block_of((int)blockIdx.x / GI, (N + BKB - 1) / BKB, a.bwd_cohort);
+  const int kb0 = kbk.kb * BKB;
+  const bool up = kbk.up;
   const int kh = ((int)blockIdx.x % GI) % (int)a.Hkv, b = ((int)blockIdx.x % GI) / (int)a.Hkv;
   const int kw0 = kb0 + 32 * kbw;               // this wave's first key
   const bool live = kw0 < N;
@@ -286,9 +338,9 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   const int total = G * nq;
   const size_t bh0 = (size_t)b * Hq + (size_t)kh * G;   // first query head of the group
   const int64_t units_per_head = tri_units(N / 32);
-  auto q0_of = [&](TilePos p) __attribute__((always_inline)) { return (nqt - 1 - p.r) * BQ; };
+  auto q0_of = [&](TilePos p) __attribute__((always_inline)) { return (up ? qt0 + p.r : nqt - 1 - p.r) * BQ; };
   BwdLoads<DQK, DV> ld;
-  ld.init(w, lane, N);
+  ld.init(loader_index<DQK, DV>() >= 0 ? loader_index<DQK, DV>() : 0, lane, N);
   auto row_rec = [&](const uint8_t* R) __attribute__((always_inline)) {
     return *reinterpret_cast<const float2*>(R + C::ROW_OFF + (32 * qs + li) * 16 + 8 * hf);
   };
@@ -712,10 +764,24 @@ hipError_t launch_dq(const AttnArgs& a, int dqk, hipStream_t s) {
 int64_t dq_units_per_head(int64_t N) { return tri_units(N / 32); }
 
 template <int DQK, int DV>
-static hipError_t bwd_dispatch(const AttnArgs& a, hipStream_t s) {
+static hipError_t bwd_dispatch(const AttnArgs& a0, hipStream_t s) {
   using C = BwdCfg<DQK, DV>;
-  const int64_t nkb = (a.N + C::BKB - 1) / C::BKB;
-  const dim3 grid((unsigned)(nkb * a.Hkv * a.B));
+  const int64_t nkb = (a0.N + C::BKB - 1) / C::BKB;
+  const dim3 grid((unsigned)(nkb * a0.Hkv * a0.B));
+  // workgroups of one KV head that run at once: one per compute unit (the
+  // kernel's LDS allows one), the units shared by the B Hkv heads
+  static int cu_count[64];   // per device, queried once
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  int cus = __atomic_load_n(&cu_count[dev], __ATOMIC_RELAXED);
+  if (cus <= 0) {
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+      return hipErrorInvalidDevice;
+    __atomic_store_n(&cu_count[dev], cus, __ATOMIC_RELAXED);
+  }
+  AttnArgs a = a0;
+  const int64_t per_head = cus / (a.B * a.Hkv);
+  a.bwd_cohort = (int)(per_head > 1 ? per_head : 1);
   if (a.rowstats) hipLaunchKernelGGL((bwd_kernel<DQK, DV, true>), grid, dim3(C::NT), 0, s, a);
   else hipLaunchKernelGGL((bwd_kernel<DQK, DV, false>), grid, dim3(C::NT), 0, s, a);
   return hipGetLastError();

@@ -57,6 +57,7 @@ struct AttnArgs {
   void* dk; int64_t dks[3];
   void* dv; int64_t dvs[3];
   int grad_bf16;
+  int bwd_cohort;                      // backward: workgroups of one KV head that run at once (set at launch)
   double* rowstats;                    // nullable [B,Hq,N,4]
 };
 
