@@ -31,6 +31,102 @@ sys.path.insert(0, ROOT)
 PEAK_FP8_TFLOPS = 5000.0      # MI355X dense FP8 MFMA
 PEAK_HBM_GBS = 8000.0
 
+# Measured HBM bytes of the main backward kernel (rocprofv3 FETCH_SIZE and
+# WRITE_SIZE, calibrated with a plain copy kernel), valid only for the kernel
+# sources it was taken on.
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "bwd_kernel_gqa_d128_8k_traffic.md")
+BWD_SOURCES = ("bwd.hip", "dma.hpp", "common.hpp", "tiles.hpp", "kernels.hpp")
+
+
+def bwd_sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for f in BWD_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_37852_amd", "csrc", f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def read_traffic(path):
+    """bytes_per_launch from a traffic summary, or None if it is absent or was
+    measured on other kernel sources."""
+    if not path or not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if line.startswith("- ") and ":" in line:
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    if fields.get("kernel_sources_sha256") != bwd_sources_sha256():
+        return None
+    return int(fields["bytes_per_launch"])
+
+
+def write_traffic_summary(fetch_csv, write_csv, out):
+    """Calibrated HBM bytes per launch of bwd_kernel<128,128> from two
+    rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE in KiB per dispatch) of
+    `bench.py --copy-calibration MIB`, whose negate kernel reads and writes
+    MIB MiB each."""
+    import csv
+
+    def per_kernel(path, counter):
+        vals = {"bwd": [], "copy": []}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            if "bwd_kernel<128, 128, false>" in name:
+                vals["bwd"].append(float(r["Counter_Value"]))
+            elif "neg" in name:
+                vals["copy"].append(float(r["Counter_Value"]))
+        if not vals["bwd"] or not vals["copy"]:
+            raise RuntimeError(f"{path}: no {counter} rows for the backward or the calibration kernel")
+        return float(np.mean(vals["bwd"])), float(np.mean(vals["copy"]))
+
+    calib = None
+    for line in open(os.path.join(os.path.dirname(fetch_csv), "..", "bench_traffic.log")):
+        if line.startswith("{"):
+            calib = json.loads(line)["copy_calibration_bytes"]
+    fb, fc = per_kernel(fetch_csv, "FETCH_SIZE")
+    wb, wc = per_kernel(write_csv, "WRITE_SIZE")
+    f_scale, w_scale = calib / (fc * 1024), calib / (wc * 1024)
+    fetch, write = fb * 1024 * f_scale, wb * 1024 * w_scale
+    total = int(round(fetch + write))
+    text = f"""# HBM traffic: bwd_kernel<128,128> on gqa_d128_8k (B=4, N=8192, Hq=16, Hkv=4, d=128, causal)
+
+Commands (MI355X, ROCm 7.2, repository root; `cd /tmp && export TMPDIR=/tmp` first):
+
+```
+python -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration 1024 > gpurun_out/bench_traffic.log
+rocprofv3 --kernel-include-regex "bwd_kernel|neg" --pmc FETCH_SIZE -d gpurun_out/tr_fetch -o run --output-format csv -- python -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration 1024
+rocprofv3 --kernel-include-regex "bwd_kernel|neg" --pmc WRITE_SIZE -d gpurun_out/tr_write -o run --output-format csv -- python -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration 1024
+python bench.py --traffic-summary gpurun_out/tr_fetch/run_counter_collection.csv gpurun_out/tr_write/run_counter_collection.csv
+```
+
+The calibration kernel is a float32 negate over {calib} bytes (it reads and writes
+{calib} bytes once each).
+
+| counter | bwd_kernel (KiB / dispatch) | calibration (KiB) | scale | bwd bytes / launch |
+|---|---:|---:|---:|---:|
+| FETCH_SIZE | {fb:.0f} | {fc:.0f} | {f_scale:.4f} | {fetch:.4e} |
+| WRITE_SIZE | {wb:.0f} | {wc:.0f} | {w_scale:.4f} | {write:.4e} |
+
+Algorithmic bytes per launch, for comparison: written, the dS' units for the dQ pass
+(one byte per causal score, B Hq N^2 / 2 = 2.15e9), their exponents (2 bytes per unit,
+2.1e6) and dK, dV (bf16, 6.7e7); read once, the row and col codes of Q and dO (B Hq N 2
+(dqk + dv) = 2.7e8), the K and V row codes (3.4e7), scales and per-query records (about
+3e7): 2.22e9 written and 3.3e8 read.  Reads above that are query tiles fetched again
+after leaving the L2; writes above it are partial-line writes of the exponents.
+
+Machine-read by bench.py (roofline.traffic; null when the kernel sources differ):
+
+- bytes_per_launch: {total}
+- kernel_sources_sha256: `{bwd_sources_sha256()}`
+"""
+    with open(out, "w") as fh:
+        fh.write(text)
+    print(text)
+
 
 class HipEvents:
     """Raw HIP events (timing enabled) via the runtime's C API."""
@@ -87,11 +183,17 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="gqa_d128_8k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--traffic", default=None, help="JSON file with measured HBM bytes of the bwd kernel")
+    ap.add_argument("--traffic", default=TRAFFIC_SUMMARY,
+                    help="summary with the measured HBM bytes of the bwd kernel (used while its sources match)")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the traffic summary from two rocprofv3 --pmc counter CSVs and exit")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the timed steps, copy MIB MiB device-to-device once (a plain copy kernel whose "
                          "FETCH_SIZE / WRITE_SIZE calibrate the HBM counters)")
     args = ap.parse_args()
+    if args.traffic_summary:
+        write_traffic_summary(*args.traffic_summary, TRAFFIC_SUMMARY)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the hot path runs on a "
               f"single MI355X; see the sharding notes in DESIGN.md)", file=sys.stderr)
@@ -177,9 +279,7 @@ def main():
     # (dQ is the separate dq pass): B*Hq*N^2*2*(dqk + dv) algorithmic FLOPs
     main_f = w.B * w.Hq * w.N * w.N * 2 * (w.Dqk + w.Dv)
     achieved = main_f / (t_bwd_main * 1e-3) / 1e12
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        traffic = json.load(open(args.traffic)).get("bytes_per_launch")
+    traffic = read_traffic(args.traffic)
     quant_bytes = 4.0625 * sum(t.numel() for t in (q, k, v, do))   # bf16 in, two fp8 copies + scales out
 
     line = {
@@ -215,11 +315,12 @@ def main():
                      "traffic": traffic, "flops_per_launch": main_f, "ms_per_launch": round(t_bwd_main, 4)},
     }
     if args.copy_calibration > 0:
+        # a plain streaming kernel of known size: n bytes read, n written
         n = args.copy_calibration << 20
-        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        src = torch.ones(n // 4, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
-        dst.copy_(src)
+        torch.neg(src, out=dst)
         torch.cuda.synchronize()
         line["copy_calibration_bytes"] = n
     if not args.no_cpu_baseline:
