@@ -518,9 +518,11 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     const int64_t unit = ((int64_t)b * Hq + h) * units_per_head + tri_units(qb / 32) + (kb0 + 64 * ks) / 64;
     // streamed past the caches: the units are read once, by dq_kernel, and
     // must not evict the query tiles the workgroups share
-    v4i* dst = reinterpret_cast<v4i*>(a.ds_units + unit * 2048 + 32 * lane);
-    __builtin_nontemporal_store(v4i{af[0], af[1], af[2], af[3]}, dst);
-    __builtin_nontemporal_store(v4i{af[4], af[5], af[6], af[7]}, dst + 1);
+    // (a unit is two 1 KB halves, operand bytes 0..15 then 16..31 of every
+    // lane, so each store covers 1 KB contiguously)
+    uint8_t* dst = a.ds_units + unit * 2048 + 16 * lane;
+    __builtin_nontemporal_store(v4i{af[0], af[1], af[2], af[3]}, reinterpret_cast<v4i*>(dst));
+    __builtin_nontemporal_store(v4i{af[4], af[5], af[6], af[7]}, reinterpret_cast<v4i*>(dst + 1024));
     if (lane == 0) {
       // the exponents of key blocks 2 ks and 2 ks + 1 of half uq, adjacent
       *reinterpret_cast<uint16_t*>(a.ds_exp + unit * 2) = *reinterpret_cast<const uint16_t*>(es + uq * KBW + 2 * ks);
@@ -659,10 +661,11 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
 // of one (batch, query head), wave w one 32-query block and all Dqk channels
 // (small workgroups: several per CU keep more unit loads in flight).
 // Per 64-key step up to the diagonal: the A operand is the stored unit (32
-// bytes per lane, already in operand order, prefetched into registers one
-// step ahead); the K col tile of the step [Dqk][64] and its scales reach LDS
-// by direct loads, double-buffered and shared by the 4 waves.  Keys past the
-// sequence meet zero dS' codes (their K loads are clamped into the array).
+// bytes per lane in operand order, as two 1 KB halves, prefetched into
+// registers one step ahead); the K col tile of the step [Dqk][64] and its
+// scales reach LDS by direct loads, double-buffered and shared by the 4
+// waves.  Keys past the sequence meet zero dS' codes (their K loads are
+// clamped into the array).
 template <int DQK>
 __global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
   constexpr int CQ = DQK / 32, NW = 4;
@@ -681,7 +684,7 @@ __global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
   const int nkw = qlast / 2 + 1;                     // the workgroup's
   const int64_t bh = (int64_t)b * a.Hq + h;
   const int64_t unit0 = bh * tri_units(nqb) + tri_units(qb < nqb ? qb : 0);
-  const uint8_t* units = a.ds_units + unit0 * 2048 + 32 * lane;
+  const uint8_t* units = a.ds_units + unit0 * 2048 + 16 * lane;
   const uint8_t* ex = a.ds_exp + unit0 * 2;
   const int64_t bk = (int64_t)b * a.Hkv + kh;
   const uint8_t* kc = a.kc_code + bk * DQK * N;
@@ -700,7 +703,7 @@ __global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
   auto load_a = [&](Aop& op, int ks) __attribute__((always_inline)) {
     ks = ks < nk ? ks : (nk > 0 ? nk - 1 : 0);     // past the wave's last step: reload it (unused)
     op.lo = *reinterpret_cast<const uint4*>(units + ks * 2048);
-    op.hi = *reinterpret_cast<const uint4*>(units + ks * 2048 + 16);
+    op.hi = *reinterpret_cast<const uint4*>(units + ks * 2048 + 1024);
     op.e = ex[2 * ks + hf];
   };
   v16f acc[CQ];
