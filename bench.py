@@ -115,8 +115,8 @@ Algorithmic bytes per launch, for comparison: written, the dS' units for the dQ 
 (one byte per causal score, B Hq N^2 / 2 = 2.15e9), their exponents (2 bytes per unit,
 2.1e6) and dK, dV (bf16, 6.7e7); read once, the row and col codes of Q and dO (B Hq N 2
 (dqk + dv) = 2.7e8), the K and V row codes (3.4e7), scales and per-query records (about
-3e7): 2.22e9 written and 3.3e8 read.  Reads above that are query tiles fetched again
-after leaving the L2; writes above it are partial-line writes of the exponents.
+3e7): 2.22e9 written and 3.3e8 read.  Measured / algorithmic: reads {fetch / 3.3e8:.2f}x (query
+tiles fetched again after leaving the L2), writes {write / 2.22e9:.2f}x.
 
 Machine-read by bench.py (roofline.traffic; null when the kernel sources differ):
 
