@@ -89,6 +89,12 @@ int check_problem(const attn_fp8_problem* p) {
     return fail(ATTN_FP8_EINVAL, "softmax_scale must be finite and positive");
   if (p->batch > 65535 || p->heads_q > 65535 || p->seqlen > (int64_t(1) << 30))
     return fail(ATTN_FP8_EUNSUPPORTED, "problem exceeds the launch grid limits");
+  // one launch dimension holds at most 2^32 - 1 work-items: the query-major
+  // kernels launch 2 B Hq N of them, the backward 4 B Hkv N
+  if (p->batch * p->heads_q * p->seqlen >= (int64_t(1) << 31) ||
+      p->batch * p->heads_kv * p->seqlen >= (int64_t(1) << 30))
+    return fail(ATTN_FP8_EUNSUPPORTED, "problem exceeds the launch grid limits (B Hq N = %lld)",
+                (long long)(p->batch * p->heads_q * p->seqlen));
   return ATTN_FP8_OK;
 }
 

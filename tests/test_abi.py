@@ -39,7 +39,10 @@ def _fake_mx(addr=4096):
 @pytest.mark.parametrize("kw,code", [
     (dict(dim_qk=96, dim_v=96), -2), (dict(dim_qk=128, dim_v=64), -2), (dict(seqlen=100), -2),
     (dict(heads_q=3, heads_kv=2), -2), (dict(causal=0), -2), (dict(softmax_scale=float("nan")), -1),
-    (dict(seqlen=-32), -1), (dict(heads_kv=0), -1)])
+    (dict(seqlen=-32), -1), (dict(heads_kv=0), -1),
+    # one launch dimension holds fewer than 2^32 work-items: B Hq N < 2^31, B Hkv N < 2^30
+    (dict(batch=1024, heads_q=64, heads_kv=64, seqlen=1 << 15), -2),
+    (dict(batch=512, heads_q=64, heads_kv=64, seqlen=1 << 15), -2)])
 def test_fwd_rejects_bad_problem(kw, code):
     L = pk.lib()
     p = _prob(**kw).c()
