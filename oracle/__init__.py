@@ -26,7 +26,7 @@ _i32p = ctypes.POINTER(ctypes.c_int32)
 
 EXACT_PFWD, EXACT_PBWD, EXACT_DS = 1, 2, 4
 EXACT_ALL = EXACT_PFWD | EXACT_PBWD | EXACT_DS
-DELTA_MATCHING, DELTA_STALE_ROWSUM = 0, 1
+DELTA_MATCHING, DELTA_STALE_ROWSUM, DELTA_CONSISTENT_DO = 0, 1, 2
 ROUND_NONE, ROUND_F32, ROUND_BF16 = 0, 1, 2
 ST_SUM_DS, ST_SUMABS_DS, ST_MAXABS_DS, ST_MAX_PDP, ST_SUM_DSCAST, ST_SUMABS_DSCAST, ST_SUM_P, \
     ST_SUM_PDP, NSTAT = range(9)

@@ -8,6 +8,7 @@
  *   - zero-row-sum invariant .......................... Sec. 3.1
  *   - matched correction delta = sum_j P_ij dP_ij ..... Sec. 3.4
  *   - stale (saved-output) correction ................. Sec. 3.2, App. A.3
+ *   - consistent-dO correction ........................ Sec. 3.4, App. B.6
  *   - kernel numerics (quantizer, probability codes,
  *     correction pass, dS cast, GQA sums) ............. App. B.6.1-B.6.3
  * adapted to power-of-two (E8M0) block scales as follows (readings of the
@@ -31,6 +32,9 @@
  *   R8 matched correction: (sum_j P_ij dP_ij) / (sum_j P_ij) from the
  *      unquantized P and the products of the FP8 backward operands.
  *   R9 stale correction: sum_c dO_ic O_ic from the raw dO and stored O.
+ *   R11 consistent-dO correction: the stale correction with the raw dO
+ *      replaced by its dequantized row copy (the operand of dP), the stored
+ *      O unchanged: sum_c dO^_ic O_ic.
  *   R10 causal mask is top-left aligned (key j visible to query i iff j <= i);
  *      query head h reads KV head floor(h / (Hq/Hkv)); dK and dV are summed
  *      over the query heads of a KV group before rounding.
@@ -371,7 +375,10 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
         double d;
         if (delta_in) d = delta_in[(b * Hq + h) * N + i];
         else if (delta_mode == ORC_DELTA_MATCHING) d = num / den;
-        else {
+        else if (delta_mode == ORC_DELTA_CONSISTENT_DO) {
+          d = 0.0;
+          for (int64_t c = 0; c < Dv; c++) d += go[c] * O[((b * N + i) * Hq + h) * Dv + c];
+        } else {
           d = 0.0;
           for (int64_t c = 0; c < Dv; c++)
             d += dO_raw[((b * N + i) * Hq + h) * Dv + c] * O[((b * N + i) * Hq + h) * Dv + c];

@@ -56,7 +56,7 @@ typedef struct {
 enum { ORC_EXACT_PFWD = 1,    /* forward probabilities are not cast to FP8 */
        ORC_EXACT_PBWD = 2,    /* backward (dV) probabilities are not cast */
        ORC_EXACT_DS   = 4 };  /* dS is not cast */
-enum { ORC_DELTA_MATCHING = 0, ORC_DELTA_STALE_ROWSUM = 1 };
+enum { ORC_DELTA_MATCHING = 0, ORC_DELTA_STALE_ROWSUM = 1, ORC_DELTA_CONSISTENT_DO = 2 };
 enum { ORC_ROUND_NONE = 0, ORC_ROUND_F32 = 1, ORC_ROUND_BF16 = 2 };
 
 /* per-row statistics written when rowstats != NULL, [B, Hq, N, ORC_NSTAT] */

@@ -141,6 +141,55 @@ def test_stale_residual_decomposition(orc):
     assert np.median(np.abs(t1) / scale) > 1e-5 and np.median(np.abs(t2) / scale) > 1e-5
 
 
+def test_consistent_do_residual_decomposition(orc):
+    """Consistent dO (the saved-output correction with dO replaced by its
+    dequantized row copy, Sec. 3.4 / App. B.6): the gradient-quantization
+    term of the stale decomposition vanishes and what remains is
+       eps_i = sum_k dOr_ik sum_j (P - Phat)_ij Vr_jk          (probability)
+             + sum_k dOr_ik sum_j Phat_ij (Vr - Vc)_jk          (two V copies)
+             + sum_k dOr_ik (O - O_stored)_ik                   (storage)
+    (the paper's residual with one V copy and exact O is the first term)."""
+    w, d = _quantized_case(orc, N=64)
+    outs = {}
+    for mode in (orc.DELTA_CONSISTENT_DO, orc.DELTA_STALE_ROWSUM):
+        outs[mode], quant = orc.attention_from_inputs(d["q"], d["k"], d["v"], d["do"], w.tau, delta_mode=mode,
+                                                      o_round=orc.ROUND_BF16, want_rowstats=True, want_phat=True)
+    out = outs[orc.DELTA_CONSISTENT_DO]
+    B, N, Hq, Hkv, D = w.B, w.N, w.Hq, w.Hkv, w.Dqk
+    Qr, _ = orc.dequantize(quant["Q"], B, N, Hq, D)
+    Kr, _ = orc.dequantize(quant["K"], B, N, Hkv, D)
+    Vr, Vc = orc.dequantize(quant["V"], B, N, Hkv, D)
+    dOr, _ = orc.dequantize(quant["dO"], B, N, Hq, D)
+    ref = torch_attention(Qr.transpose(0, 2, 1, 3), Kr.transpose(0, 2, 1, 3), Vr.transpose(0, 2, 1, 3),
+                          np.zeros((B, N, Hq, D)), w.tau)
+    P, Ph = ref["P"], out["phat"]
+    O = out["O_unrounded"].transpose(0, 2, 1, 3)
+    Ost = out["O"].transpose(0, 2, 1, 3)
+    G = Hq // Hkv
+    Vr_h, Vc_h = np.repeat(Vr, G, axis=1), np.repeat(Vc, G, axis=1)
+    # the correction itself: <dOr_i, O_stored_i>
+    assert np.allclose(out["delta"], np.einsum("bhik,bhik->bhi", dOr, Ost), rtol=1e-12, atol=1e-15)
+    t1 = np.einsum("bhik,bhik->bhi", dOr, (P - Ph) @ Vr_h)
+    t3 = np.einsum("bhik,bhik->bhi", dOr, Ph @ (Vr_h - Vc_h))
+    t4 = np.einsum("bhik,bhik->bhi", dOr, O - Ost)
+    eps = out["rowstats"][..., orc.ST_SUM_DS]
+    scale = out["rowstats"][..., orc.ST_SUMABS_DS]
+    assert np.max(np.abs(eps - (t1 + t3 + t4)) / np.maximum(scale, 1e-300)) < 1e-10
+    # a mismatch remains (the probability term), smaller than the stale one
+    eps_stale = outs[orc.DELTA_STALE_ROWSUM]["rowstats"][..., orc.ST_SUM_DS]
+    assert np.median(np.abs(t1) / scale) > 1e-5
+    assert np.median(np.abs(eps) / scale) < np.median(np.abs(eps_stale) / scale)
+
+
+def test_consistent_do_equals_stale_without_quantization(orc):
+    """With exact operands the dequantized dO is the raw dO, so the two
+    saved-output corrections coincide."""
+    q, k, v, do = inputs(1, 40, 2, 1, 32, 32, seed=4)
+    r = {m: orc.attention_from_inputs(q, k, v, do, 0.2, delta_mode=m, exact_inputs=True)[0]["delta"]
+         for m in (orc.DELTA_CONSISTENT_DO, orc.DELTA_STALE_ROWSUM)}
+    assert np.array_equal(r[orc.DELTA_CONSISTENT_DO], r[orc.DELTA_STALE_ROWSUM])
+
+
 def test_matched_delta_bilinearity(orc):
     """delta_matched_i = <dOr_i, (P Vr)_i> (the auxiliary-output identity of
     App. C.3.1), computed through a different contraction order."""
