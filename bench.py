@@ -264,12 +264,17 @@ def main():
     t_quant, t_fwd, t_delta = avg(0, 1), avg(1, 2), avg(2, 3)
     t_bwd_main, t_bwd_call = avg(4, 5), avg(3, 6)
 
-    # the stale-rowsum correction, timed the same way, for the pre-pass ratio
-    smarks = [ev.create(7) for _ in range(3)]
-    for m in smarks:
-        step(m, mode=pk.DELTA_STALE_ROWSUM)
-    torch.cuda.synchronize()
-    t_delta_stale = float(np.mean([ev.ms(m[2], m[3]) for m in smarks]))
+    # the saved-output corrections (stale and consistent dO), timed the same
+    # way, for the pre-pass ratios
+    def correction_ms(mode):
+        ms_ = [ev.create(7) for _ in range(3)]
+        for m in ms_:
+            step(m, mode=mode)
+        torch.cuda.synchronize()
+        return float(np.mean([ev.ms(m[2], m[3]) for m in ms_]))
+
+    t_delta_stale = correction_ms(pk.DELTA_STALE_ROWSUM)
+    t_delta_consistent = correction_ms(pk.DELTA_CONSISTENT_DO)
 
     fwd_f, bwd_f = w.credited_flops()
     credited = fwd_f + bwd_f
@@ -300,7 +305,8 @@ def main():
                    "inputs": "bf16, one outlier channel x20 in Q and K", "step": "quantize+fwd+delta+bwd"},
         "pct_of_fp8_peak": round(100.0 * value / PEAK_FP8_TFLOPS, 2),
         "breakdown_ms": {"quantize": round(t_quant, 4), "fwd": round(t_fwd, 4), "delta_matching": round(t_delta, 4),
-                         "delta_stale_rowsum": round(t_delta_stale, 4), "bwd_main_kernel": round(t_bwd_main, 4),
+                         "delta_stale_rowsum": round(t_delta_stale, 4),
+                         "delta_consistent_do": round(t_delta_consistent, 4), "bwd_main_kernel": round(t_bwd_main, 4),
                          "bwd_call": round(t_bwd_call, 4)},
         "paper_accounting": {"fwd_tflops": round(fwd_f / (t_fwd * 1e-3) / 1e12, 2),
                              "bwd_tflops_incl_delta": round(bwd_f / ((t_delta + t_bwd_call) * 1e-3) / 1e12, 2),

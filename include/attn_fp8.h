@@ -72,7 +72,9 @@ typedef enum { ATTN_FP8_DTYPE_F32 = 0, ATTN_FP8_DTYPE_BF16 = 1 } attn_fp8_dtype;
 
 typedef enum {
   ATTN_FP8_DELTA_MATCHING = 0,      /* delta_i = sum_j P_ij dP_ij / sum_j P_ij (Sec. 3.4) */
-  ATTN_FP8_DELTA_STALE_ROWSUM = 1   /* delta_i = sum_c dO_ic O_ic (Sec. 3.2)            */
+  ATTN_FP8_DELTA_STALE_ROWSUM = 1,  /* delta_i = sum_c dO_ic O_ic (Sec. 3.2)            */
+  ATTN_FP8_DELTA_CONSISTENT_DO = 2  /* delta_i = sum_c dO^_ic O_ic, dO^ the dequantized
+                                       row copy of dO (Sec. 3.4, App. B.6)           */
 } attn_fp8_delta_mode;
 
 enum { ATTN_FP8_QUANT_ROW = 1, ATTN_FP8_QUANT_COL = 2, ATTN_FP8_QUANT_BOTH = 3 };
@@ -140,9 +142,12 @@ int attn_fp8_fwd(const attn_fp8_problem* p, const attn_fp8_mx* q, const attn_fp8
  *   STALE_ROWSUM: reads dout_raw [B,N,Hq,Dv] (dout_dtype, strides
  *                 dout_strides) and the stored output o (o_dtype,
  *                 o_strides); delta = sum_c dO_ic O_ic in FP32.
+ *   CONSISTENT_DO: reads the row copy of dout (code_row, scale_row) and o;
+ *                 delta = sum_c dO^_ic O_ic in FP32 with dO^ = E4M3 code
+ *                 times the block's E8M0 scale (exact in FP32).
  * Pointers the mode does not read may be NULL.
  *   delta    device float [B, Hq, N, 2]: (hi, lo) with delta ~= hi + lo
- *            (lo = 0 for STALE_ROWSUM). */
+ *            (lo = 0 for STALE_ROWSUM and CONSISTENT_DO). */
 int attn_fp8_delta(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q,
                    const attn_fp8_mx* k, const attn_fp8_mx* v, const attn_fp8_mx* dout,
                    const float* lse, const void* dout_raw, int dout_dtype,

@@ -17,7 +17,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libattn_fp8.so")
 
 DTYPE_F32, DTYPE_BF16 = 0, 1
-DELTA_MATCHING, DELTA_STALE_ROWSUM = 0, 1
+DELTA_MATCHING, DELTA_STALE_ROWSUM, DELTA_CONSISTENT_DO = 0, 1, 2
 QUANT_ROW, QUANT_COL, QUANT_BOTH = 1, 2, 3
 STATUS = {0: "OK", -1: "EINVAL", -2: "EUNSUPPORTED", -3: "EALIGN", -4: "EWORKSPACE", -5: "EHIP"}
 EXPORTS = ("attn_fp8_quantize", "attn_fp8_fwd", "attn_fp8_delta", "attn_fp8_bwd_workspace_size",

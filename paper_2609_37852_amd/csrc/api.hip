@@ -175,6 +175,11 @@ int check_delta_inputs(const attn_fp8_problem* p, int mode, const attn_fp8_mx* q
         (rc = check_strides("dout_raw", dout_strides, dtype_size(dout_dtype))) ||
         (rc = check_strides("o", o_strides, dtype_size(o_dtype))))
       return rc;
+  } else if (mode == ATTN_FP8_DELTA_CONSISTENT_DO) {
+    if (!dtype_size(o_dtype)) return fail(ATTN_FP8_EINVAL, "bad o dtype");
+    if ((rc = check_mx("dout", dout, true, false)) || (rc = check_ptr("o", o)) ||
+        (rc = check_strides("o", o_strides, dtype_size(o_dtype))))
+      return rc;
   } else {
     return fail(ATTN_FP8_EINVAL, "unknown delta_mode %d", mode);
   }
@@ -197,17 +202,20 @@ int launch_delta(const attn_fp8_problem* p, int mode, const attn_fp8_mx* q, cons
     return hip_status(afp8::launch_delta_matching(a, (int)p->dim_qk, (int)p->dim_v, stream), "delta_matching");
   }
   afp8::StaleArgs s{};
-  s.dout = dout_raw;
   s.o = o;
-  for (int i = 0; i < 3; i++) {
-    s.ds[i] = dout_strides[i];
-    s.os[i] = o_strides[i];
-  }
+  for (int i = 0; i < 3; i++) s.os[i] = o_strides[i];
   s.delta = delta;
   s.B = p->batch;
   s.N = p->seqlen;
   s.Hq = p->heads_q;
   s.Dv = (int)p->dim_v;
+  if (mode == ATTN_FP8_DELTA_CONSISTENT_DO) {
+    s.do_code = dout->code_row;
+    s.do_scale = dout->scale_row;
+    return hip_status(afp8::launch_consistent_rowsum(s, o_dtype == ATTN_FP8_DTYPE_BF16, stream), "consistent_rowsum");
+  }
+  s.dout = dout_raw;
+  for (int i = 0; i < 3; i++) s.ds[i] = dout_strides[i];
   return hip_status(afp8::launch_stale_rowsum(s, dout_dtype == ATTN_FP8_DTYPE_BF16, o_dtype == ATTN_FP8_DTYPE_BF16,
                                               stream),
                     "stale_rowsum");
@@ -287,7 +295,8 @@ int attn_fp8_delta(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx*
                    const int64_t o_strides[3], float* delta, hipStream_t stream) {
   int rc;
   if ((rc = check_problem(p))) return rc;
-  if (delta_mode != ATTN_FP8_DELTA_MATCHING && delta_mode != ATTN_FP8_DELTA_STALE_ROWSUM)
+  if (delta_mode != ATTN_FP8_DELTA_MATCHING && delta_mode != ATTN_FP8_DELTA_STALE_ROWSUM &&
+      delta_mode != ATTN_FP8_DELTA_CONSISTENT_DO)
     return fail(ATTN_FP8_EINVAL, "unknown delta_mode %d", delta_mode);
   if (empty(p)) return ok();
   if ((rc = check_delta_inputs(p, delta_mode, q, k, v, dout, lse, dout_raw, dout_dtype, dout_strides, o, o_dtype,

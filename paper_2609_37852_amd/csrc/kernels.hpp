@@ -19,7 +19,9 @@ struct QuantArgs {
 };
 
 struct StaleArgs {
-  const void* dout;
+  const void* dout;                    // raw dO (stale), or NULL when the row copy below is read
+  const uint8_t* do_code;              // consistent dO: row codes [B,Hq,N,Dv]
+  const uint8_t* do_scale;             //                and scales [B,Hq,N,Dv/32]
   int64_t ds[3];
   const void* o;
   int64_t os[3];
@@ -63,6 +65,7 @@ struct AttnArgs {
 
 hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_t s);
 hipError_t launch_stale_rowsum(const StaleArgs& a, int dout_bf16, int o_bf16, hipStream_t s);
+hipError_t launch_consistent_rowsum(const StaleArgs& a, int o_bf16, hipStream_t s);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 hipError_t launch_fwd(const AttnArgs& a, int dqk, int dv, hipStream_t s);
 hipError_t launch_delta_matching(const AttnArgs& a, int dqk, int dv, hipStream_t s);

@@ -185,22 +185,31 @@ hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_
 }
 
 // ---------------------------------------------------------------------------
-// Stale (saved-output) correction, Sec. 3.2: delta_i = sum_c dO_ic O_ic in
-// FP32 from the raw dO and the stored O.  One wave per (b, n, h) row, rows
-// strided by the grid (whose size stays within the launch limits).
-template <typename TD, typename TO>
+// Saved-output corrections, delta_i = sum_c dO_ic O_ic in FP32 with the
+// stored O: stale (Sec. 3.2) from the raw dO; consistent dO (Sec. 3.4,
+// QDO) from the dequantized row copy of dO, the operand of dP (E4M3 code
+// times the block's power-of-two scale, both exact in FP32).  One wave per
+// (b, n, h) row, rows strided by the grid (whose size stays within the
+// launch limits).
+template <typename TD, typename TO, bool QDO>
 __global__ __launch_bounds__(256) void stale_rowsum_kernel(StaleArgs a) {
   const int lane = threadIdx.x & 63;
   const int64_t nrows = a.B * a.N * a.Hq;
   for (int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); row < nrows;
        row += (int64_t)gridDim.x * 4) {
     const int64_t h = row % a.Hq, n = (row / a.Hq) % a.N, b = row / (a.Hq * a.N);
-    const TD* d = reinterpret_cast<const TD*>(a.dout) + b * a.ds[0] + n * a.ds[1] + h * a.ds[2];
     const TO* o = reinterpret_cast<const TO*>(a.o) + b * a.os[0] + n * a.os[1] + h * a.os[2];
     float acc = 0.f;
     for (int c = lane; c < a.Dv; c += 64) {
       float dv, ov;
-      if constexpr (sizeof(TD) == 2) dv = bf16_to_f32(d[c]); else dv = (float)d[c];
+      if constexpr (QDO) {
+        const int64_t r = (b * a.Hq + h) * a.N + n;
+        const int e = (int)a.do_scale[r * (a.Dv / 32) + c / 32] - 127;
+        dv = ldexpf(fp8_value(a.do_code[r * a.Dv + c], 0), e);
+      } else {
+        const TD* d = reinterpret_cast<const TD*>(a.dout) + b * a.ds[0] + n * a.ds[1] + h * a.ds[2];
+        if constexpr (sizeof(TD) == 2) dv = bf16_to_f32(d[c]); else dv = (float)d[c];
+      }
       if constexpr (sizeof(TO) == 2) ov = bf16_to_f32(o[c]); else ov = (float)o[c];
       acc = __builtin_fmaf(dv, ov, acc);
     }
@@ -217,10 +226,18 @@ __global__ __launch_bounds__(256) void stale_rowsum_kernel(StaleArgs a) {
 hipError_t launch_stale_rowsum(const StaleArgs& a, int dout_bf16, int o_bf16, hipStream_t s) {
   const int64_t nrows = a.B * a.N * a.Hq, wgs = (nrows + 3) / 4;
   dim3 grid((unsigned)(wgs < (int64_t(1) << 20) ? wgs : (int64_t(1) << 20)));
-  if (dout_bf16 && o_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<uint16_t, uint16_t>), grid, dim3(256), 0, s, a);
-  else if (dout_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<uint16_t, float>), grid, dim3(256), 0, s, a);
-  else if (o_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<float, uint16_t>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((stale_rowsum_kernel<float, float>), grid, dim3(256), 0, s, a);
+  if (dout_bf16 && o_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<uint16_t, uint16_t, false>), grid, dim3(256), 0, s, a);
+  else if (dout_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<uint16_t, float, false>), grid, dim3(256), 0, s, a);
+  else if (o_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<float, uint16_t, false>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((stale_rowsum_kernel<float, float, false>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_consistent_rowsum(const StaleArgs& a, int o_bf16, hipStream_t s) {
+  const int64_t nrows = a.B * a.N * a.Hq, wgs = (nrows + 3) / 4;
+  dim3 grid((unsigned)(wgs < (int64_t(1) << 20) ? wgs : (int64_t(1) << 20)));
+  if (o_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<uint16_t, uint16_t, true>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((stale_rowsum_kernel<uint16_t, float, true>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

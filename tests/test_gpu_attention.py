@@ -30,7 +30,8 @@ def _workload(name, kw):
 
 @pytest.mark.parametrize("name,kw", CASES, ids=[f"{n}-{'-'.join(f'{k}{v}' for k, v in kw.items()) or 'full'}"
                                                  for n, kw in CASES])
-@pytest.mark.parametrize("mode", [pk.DELTA_MATCHING, pk.DELTA_STALE_ROWSUM], ids=["matching", "stale"])
+@pytest.mark.parametrize("mode", [pk.DELTA_MATCHING, pk.DELTA_STALE_ROWSUM, pk.DELTA_CONSISTENT_DO],
+                         ids=["matching", "stale", "consistent"])
 def test_parity(name, kw, mode):
     w = _workload(name, kw)
     say(f"parity {w} mode={mode}")
@@ -48,7 +49,7 @@ def test_parity(name, kw, mode):
     for k in ("O", "dQ", "dK", "dV"):
         assert errs[k] <= REL_TOL, (k, errs[k])
     assert errs["LSE"] < 1e-3
-    # the stale correction reads the bf16-rounded O, whose rounding flips move it
+    # the saved-output corrections read the bf16-rounded O, whose rounding flips move them
     assert errs["delta"] < (1e-3 if mode == pk.DELTA_MATCHING else 1e-2)
     if mode == pk.DELTA_MATCHING:
         rep = invariant_report(g["rowstats"], o["rowstats"])
@@ -107,10 +108,13 @@ def test_delta_mode_changes_only_dq_dk():
 
 
 def test_stale_residual_is_large_and_matching_small():
+    """Pre-cast row sums: the stale correction leaves the largest residual,
+    consistent dO (no gradient-quantization term, Sec. 3.4) a smaller but
+    still large one, the matched correction almost none."""
     w = _workload("tiny_mha_128", {})
     d = synth.generate(w, seed=0)
     res = {}
-    for mode in (pk.DELTA_MATCHING, pk.DELTA_STALE_ROWSUM):
+    for mode in (pk.DELTA_MATCHING, pk.DELTA_STALE_ROWSUM, pk.DELTA_CONSISTENT_DO):
         g = run_gpu(w, d, mode=mode)
         rs = g["rowstats"]
         live = rs[..., 1] > 0
@@ -118,6 +122,7 @@ def test_stale_residual_is_large_and_matching_small():
     say("  median r_pre", res)
     assert res[pk.DELTA_STALE_ROWSUM] > 1e-4
     assert res[pk.DELTA_STALE_ROWSUM] > 100 * res[pk.DELTA_MATCHING]
+    assert 100 * res[pk.DELTA_MATCHING] < res[pk.DELTA_CONSISTENT_DO] < res[pk.DELTA_STALE_ROWSUM]
 
 
 def test_delta_injection_affine():
