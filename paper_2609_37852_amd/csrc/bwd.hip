@@ -156,7 +156,7 @@ __device__ __forceinline__ void stage_rows(lds8* st, const BwdLoads<DQK, DV>& L,
   dma_row_scales<DV, NWK>(st + C::OS_OFF, hp.osc, i0, N, w, lane, 1);
   if (w == (3 % NWK)) {
     const int r = i0 + lane < N ? i0 + lane : N - 1;
-    dma16(hp.rows + r, st + C::ROW_OFF);
+    dma16(make_buf(hp.rows, (uint32_t)N * 16), (uint32_t)r * 16, st + C::ROW_OFF);
   }
 }
 
@@ -170,11 +170,11 @@ __device__ __forceinline__ void stage_cols(lds8* st, const BwdLoads<DQK, DV>& L,
   L.qc.issue(st + C::QC_OFF, hp.qcol, i0, N, w, lane);
   L.oc.issue(st + C::OC_OFF, hp.ocol, i0, N, w, lane);
   constexpr int NCI = (C::CS_BYTES + 255) / 256;
-  const uint8_t* tcs = hp.tcs + (i0 / 64) * C::CS_BYTES;
+  const Buf tcs = make_buf(hp.tcs, (uint32_t)((N + 63) / 64) * C::CS_BYTES);
   for (int k = 0; k < NCI; k++) {
     if ((2 + k) % NWK != w) continue;   // loaders 2, 3, ...: 0 and 1 take the row scales
     const int off = 256 * k + 4 * lane;
-    if (off < C::CS_BYTES) dma4(tcs + off, st + C::QCS_OFF + 256 * k);
+    if (off < C::CS_BYTES) dma4(tcs, (uint32_t)((i0 / 64) * C::CS_BYTES + off), st + C::QCS_OFF + 256 * k);
   }
 }
 
@@ -690,13 +690,14 @@ __global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
   const uint8_t* kc = a.kc_code + bk * DQK * N;
   const uint8_t* tk = a.tile_kcs + bk * ((N + 63) / 64) * KSB;
 
+  const Buf tkb = make_buf(tk, (uint32_t)((N + 63) / 64) * KSB);
   auto issue = [&](lds8* dst, int ks) __attribute__((always_inline)) {
     dma_cols<DQK, NW>(dst, kc, 64 * ks, N, w, lane);
     constexpr int NI = (KSB + 255) / 256;
     for (int k = 0; k < NI; k++) {
       if ((NW - 1 - k) != w) continue;
       const int off = 256 * k + 4 * lane;
-      if (off < KSB) dma4(tk + ks * KSB + off, dst + KT + 256 * k);
+      if (off < KSB) dma4(tkb, (uint32_t)(ks * KSB + off), dst + KT + 256 * k);
     }
   };
   struct Aop { uint4 lo, hi; uint32_t e; };

@@ -24,11 +24,25 @@ __device__ __forceinline__ int swz_col(int c) { return (c >> 2) & 3; }
 // generic pointer)
 typedef __attribute__((address_space(3))) uint8_t lds8;
 
-__device__ __forceinline__ void dma16(const void* src, lds8* lds_base) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+// Direct loads are MUBUF buffer loads with the LDS bit, over a buffer
+// resource of a wave-uniform base address: the FLAT-encoded global_load_lds
+// form makes the compiler treat every LDS access as completing out of order
+// while one is in flight, so each LDS wait would drain all outstanding reads
+// (lgkmcnt(0)); buffer loads count in vmcnt only, so operand reads for the
+// next MFMA can stay in flight while the current one waits.  `off` is the
+// lane's byte offset from the base; offsets at or past `bytes` read as zero.
+struct Buf {
+  __amdgpu_buffer_rsrc_t r;
+};
+__device__ __forceinline__ Buf make_buf(const void* base, uint32_t bytes) {
+  // 0x00020000: raw (untyped) buffer, 32-bit data format (gfx9 family)
+  return Buf{__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000)};
 }
-__device__ __forceinline__ void dma4(const void* src, lds8* lds_base) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 4, 0, 0);
+__device__ __forceinline__ void dma16(const Buf& b, uint32_t off, lds8* lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(b.r, (__attribute__((address_space(3))) void*)lds_base, 16, (int)off, 0, 0, 0);
+}
+__device__ __forceinline__ void dma4(const Buf& b, uint32_t off, lds8* lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(b.r, (__attribute__((address_space(3))) void*)lds_base, 4, (int)off, 0, 0, 0);
 }
 
 // Waits for this wave's LDS writes and direct-to-LDS loads (and any other
@@ -56,23 +70,25 @@ __device__ __forceinline__ void lds_sync() {
 template <int D, int NWK, int ROWS = 64>
 __device__ __forceinline__ void dma_rows(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) {
   constexpr int NI = ROWS * D / 1024;
+  const Buf b = make_buf(code, (uint32_t)N * D);
   for (int k = w; k < NI; k += NWK) {
     const int off = 1024 * k + 16 * lane;
     const int r = off / D, p = (off % D) / 16;
     const int row = i0 + r < N ? i0 + r : N - 1;
-    dma16(code + row * D + 16 * (p ^ swz_row<D>(r)), lds + 1024 * k);
+    dma16(b, (uint32_t)(row * D + 16 * (p ^ swz_row<D>(r))), lds + 1024 * k);
   }
 }
 // Col-copy code tile: channels [0, D), queries [i0, i0 + 64) (clamped) -> [D][64].
 template <int D, int NWK>
 __device__ __forceinline__ void dma_cols(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) {
   constexpr int NI = D * 64 / 1024;
+  const Buf b = make_buf(code, (uint32_t)D * N);
   for (int k = w; k < NI; k += NWK) {
     const int off = 1024 * k + 16 * lane;
     const int c = off / 64, p = (off % 64) / 16;
     const int q = p ^ swz_col(c);
     const int col = i0 + 16 * q < N - 16 ? i0 + 16 * q : N - 16;
-    dma16(code + c * N + col, lds + 1024 * k);
+    dma16(b, (uint32_t)(c * N + col), lds + 1024 * k);
   }
 }
 // Row-copy scales of ROWS rows: ROWS * D / 32 contiguous bytes (clamped).
@@ -80,12 +96,13 @@ template <int D, int NWK, int ROWS = 64>
 __device__ __forceinline__ void dma_row_scales(lds8* lds, const uint8_t* scale, int i0, int N, int w, int lane,
                                                int first_wave) {
   constexpr int BYTES = ROWS * D / 32, NI = (BYTES + 255) / 256;
+  const Buf b = make_buf(scale, (uint32_t)N * (D / 32));
   for (int k = 0; k < NI; k++) {
     if ((first_wave + k) % NWK != w) continue;
     const int off = 256 * k + 4 * lane;
     if (off < BYTES) {
       const int g = i0 * (D / 32) + off, lim = N * (D / 32) - 4;
-      dma4(scale + (g < lim ? g : lim), lds + 256 * k);
+      dma4(b, (uint32_t)(g < lim ? g : lim), lds + 256 * k);
     }
   }
 }
@@ -143,11 +160,12 @@ struct RowLoads {
       dma_rows<D, NWK, ROWS>(lds, code, i0, N, w, lane);
       return;
     }
-    const uint8_t* base = code + (size_t)i0 * D;
+    const Buf b = make_buf(code, (uint32_t)N * D);
+    const uint32_t base = (uint32_t)i0 * D;
 #pragma unroll
     for (int j = 0; j < NS; j++) {
       const int k = w + NWK * j;
-      if (k < NI) dma16(base + (STRIDED ? off[0] + 1024 * NWK * j : off[j]), lds + 1024 * k);
+      if (k < NI) dma16(b, base + (STRIDED ? off[0] + 1024 * NWK * j : off[j]), lds + 1024 * k);
     }
   }
 };
@@ -172,6 +190,7 @@ struct ColLoads {
     cstride = CSTEP * N;
   }
   __device__ __forceinline__ void issue(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) const {
+    const Buf b = make_buf(code, (uint32_t)D * N);
     if (i0 + COLS > N) {
       // ragged tile: clamp every 16-byte piece into its row
 #pragma unroll
@@ -182,15 +201,15 @@ struct ColLoads {
         const int c = o / COLS, p = (o % COLS) / 16;
         const int q = COLS == 64 ? (p ^ swz_col(c)) : (p ^ swz_row<128>(c));
         const int col = i0 + 16 * q < N - 16 ? i0 + 16 * q : N - 16;
-        dma16(code + c * N + col, lds + 1024 * k);
+        dma16(b, (uint32_t)(c * N + col), lds + 1024 * k);
       }
       return;
     }
-    const uint8_t* base = code + i0 + off;
+    const uint32_t base = (uint32_t)i0 + off;
 #pragma unroll
     for (int j = 0; j < NS; j++) {
       const int k = w + NWK * j;
-      if (k < NI) dma16(base + (size_t)j * cstride, lds + 1024 * k);
+      if (k < NI) dma16(b, base + (uint32_t)(j * cstride), lds + 1024 * k);
     }
   }
 };
