@@ -355,31 +355,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   v16f s, dp;
   v4i pn = v4i{0, 0, 0, 0}, dn = v4i{0, 0, 0, 0};   // this half's P' / dS' codes, natural query order
   int e = -127;                                      // and the dS' block exponent
-
-  // S and dP of one tile's half (skipped halves: no MFMA, zero codes later)
-  // rec: the lane's pair of per-query record values (read before the loads
-  // of the next tiles are issued: the compiler cannot tell this read from
-  // the LDS those loads write and would wait for them)
-  auto sdp = [&](const uint8_t* R, bool skip, float2 rec) __attribute__((always_inline)) {
-    if (skip) return;
-    const uint8_t* Q = R + C::Q_OFF;
-    const uint8_t* Qs = R + C::QS_OFF;
-    const uint8_t* O = R + C::O_OFF;
-    const uint8_t* Os = R + C::OS_OFF;
-#pragma unroll
-    for (int r = 0; r < 16; r++) { s[r] = 0.f; dp[r] = 0.f; }
-#pragma unroll
-    for (int t2 = 0; t2 < KS; t2++)
-      s = mfma_mx(frag_rows_swz<DQK>(Q, 32 * qs + li, t2, hf), kfrag(t2), s,
-                  Qs[(32 * qs + li) * (DQK / 32) + 2 * t2 + hf], ksc[t2]);
-#pragma unroll
-    for (int t2 = 0; t2 < VS; t2++)
-      dp = mfma_mx(frag_rows_swz<DV>(O, 32 * qs + li, t2, hf), vfrag(t2), dp,
-                   Os[(32 * qs + li) * (DV / 32) + 2 * t2 + hf], vsc[t2]);
-    // per-query shifts: S += q_c* k_c*, then -LSE / tau; dP -= hi, then lo
-    s = rank2_update(rec.x, kb, s);
-    dp = rank2_update(rec.y, 1.0f, dp);
-  };
+  v4i mine = v4i{0, 0, 0, 0};                        // this wave's operand codes for dV (P') or dK (dS')
 
   // P, dS and their codes from the shifted s, dp; EDGE tiles may skip the
   // half or hold the diagonal block (masked)
@@ -456,6 +432,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     if (lane == 0) es[qs * KBW + kbw] = (uint8_t)(e + 127);
     const v4i xv = qs == 0 ? dn : pn;
     x[qs][kbw * 64 + lane] = make_uint4((uint32_t)xv[0], (uint32_t)xv[1], (uint32_t)xv[2], (uint32_t)xv[3]);
+    mine = qs == 0 ? pn : dn;
   };
   auto front_skip = [&](TilePos p) __attribute__((always_inline)) {
     const int i0 = q0_of(p);
@@ -464,31 +441,112 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     return !full && (!live || qb < kw0 || qb >= N);
   };
 
-  // dV += P'^T dO_col (first half) or dK += dS'^T Q_col (second half); k =
-  // the tile's 64 queries, bytes 0..15 from the first half, 16..31 from the
-  // second (skipped halves have zero codes)
-  auto back = [&](const uint8_t* Cc, const uint8_t* es, uint4 (*x)[KBW * 64]) __attribute__((always_inline)) {
-    if (qs == 0) {
-      const uint4 o = x[1][kbw * 64 + lane];
-      const v8i A = v8i{pn[0], pn[1], pn[2], pn[3], (int)o.x, (int)o.y, (int)o.z, (int)o.w};
-      const uint8_t* Oc = Cc + C::OC_OFF;
-      const uint8_t* Ocs = Cc + C::OCS_OFF;
-#pragma unroll
-      for (int i = 0; i < CV; i++) {
-        const int ch = 32 * i + li;
-        acc[i] = mfma_mx(A, frag_cols_swz(Oc, ch, hf), acc[i], 127 - 8, Ocs[ch * 2 + hf]);
+  // The MFMAs of one pipeline step, as one straight sequence: S and dP of the
+  // next tile's half (skipped halves: none; zero codes later), the two
+  // rank-2 updates (per-query shifts: S += q_c* k_c*, then -LSE / tau; dP -=
+  // hi, then lo), and dV += P'^T dO_col (first wave of a key block) or dK +=
+  // dS'^T Q_col (second).  The LDS operands of each MFMA are read one MFMA
+  // ahead and a scheduling fence keeps them there, so each MFMA waits only
+  // for its own reads while the next ones are in flight.
+  // dV / dK: k = the tile's 64 queries.  The first wave's A holds its own P'
+  // codes (queries 0..31 of the tile) in bytes 0..15 and the second half's
+  // in bytes 16..31; the second wave's A holds its own dS' codes (queries
+  // 32..63) in bytes 0..15 and the first half's in bytes 16..31, so both
+  // build A from the same registers without a branch; the second wave's B
+  // fragments and the scale bytes of both operands swap the two 32-query
+  // blocks to match (the sum over k does not depend on the block order).
+  struct Opnd {
+    v8i a, b;
+    int sa, sb;
+  };
+  auto mfmas = [&](const uint8_t* R, bool skip, float2 rec, const uint8_t* Cc, const uint8_t* es,
+                   uint4 (*x)[KBW * 64], auto back_tag) __attribute__((always_inline)) {
+    const uint8_t* Q = R + C::Q_OFF;
+    const uint8_t* Qs = R + C::QS_OFF;
+    const uint8_t* O = R + C::O_OFF;
+    const uint8_t* Os = R + C::OS_OFF;
+    const int qrow = 32 * qs + li;
+    const uint4 o = x[1 - qs][kbw * 64 + lane];
+    const v8i A = v8i{mine[0], mine[1], mine[2], mine[3], (int)o.x, (int)o.y, (int)o.z, (int)o.w};
+    const int ascale = qs == 0 ? 127 - 8 : (hf ? (int)es[kbw] : e + 127);
+    const uint8_t* Bt = Cc + (qs ? C::QC_OFF : C::OC_OFF);
+    const uint8_t* Bs = Cc + (qs ? C::QCS_OFF : C::OCS_OFF);
+    const int nb = qs ? CK : CV;
+    const int clo = hf + 2 * qs, chi = hf + 2 - 2 * qs, sbk = hf ^ qs;
+    // S and dP operations interleaved while both last (independent chains)
+    constexpr int NSD = KS + VS, NI2 = KS < VS ? KS : VS;
+    auto sd_is_s = [](int m) { return m < 2 * NI2 ? (m & 1) == 0 : KS > VS; };
+    auto sd_t = [](int m) { return m < 2 * NI2 ? m >> 1 : m - NI2; };
+    auto load = [&](int m) __attribute__((always_inline)) {
+      Opnd r;
+      if (m < NSD) {
+        const int t = sd_t(m);
+        if (sd_is_s(m)) {
+          r.a = frag_rows_swz<DQK>(Q, qrow, t, hf);
+          r.b = kfrag(t);
+          r.sa = Qs[qrow * (DQK / 32) + 2 * t + hf];
+          r.sb = ksc[t];
+        } else {
+          r.a = frag_rows_swz<DV>(O, qrow, t, hf);
+          r.b = vfrag(t);
+          r.sa = Os[qrow * (DV / 32) + 2 * t + hf];
+          r.sb = vsc[t];
+        }
+      } else {
+        const int ch = 32 * (m - NSD) + li;
+        r.a = A;
+        r.b = frag_cols_chunks(Bt, ch, clo, chi);
+        r.sa = ascale;
+        r.sb = Bs[ch * 2 + sbk];
       }
+      return r;
+    };
+    auto exec = [&](int m, const Opnd& r) __attribute__((always_inline)) {
+      if (m < NSD) {
+        if (sd_is_s(m)) s = mfma_mx(r.a, r.b, s, r.sa, r.sb);
+        else dp = mfma_mx(r.a, r.b, dp, r.sa, r.sb);
+      } else {
+        const int i = m - NSD;
+        acc[i] = mfma_mx(r.a, r.b, acc[i], r.sa, r.sb);
+      }
+    };
+    // operations M0 .. M1 - 1 of the sequence; the rank-2 updates follow the
+    // second dV / dK MFMA (the S and dP chains have finished by then), or the
+    // last S / dP MFMA when there is no dV / dK work
+    auto run = [&](auto from_tag, auto with_back) __attribute__((always_inline)) {
+      constexpr int M0 = decltype(from_tag)::value;
+      constexpr int M1 = decltype(with_back)::value ? NSD + CMAX : NSD;
+      constexpr int R2 = M1 > NSD ? NSD + (CMAX > 1 ? 1 : 0) : NSD - 1;
+      if (M0 == 0) {
+#pragma unroll
+        for (int r = 0; r < 16; r++) { s[r] = 0.f; dp[r] = 0.f; }
+      }
+      Opnd cur = load(M0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int m = M0; m < M1; m++) {
+        // past the last dV MFMA of the first wave (dqk > dv): the second
+        // wave's remaining dK MFMAs only
+        const bool act = m < NSD || m - NSD < (CK < CV ? CK : CV) || m - NSD < nb;
+        Opnd nxt;
+        if (m + 1 < M1 && (m + 1 < NSD || m + 1 - NSD < (CK < CV ? CK : CV) || m + 1 - NSD < nb)) nxt = load(m + 1);
+        if (act) exec(m, cur);
+        if (M0 == 0 && m == R2) {
+          s = rank2_update(rec.x, kb, s);
+          dp = rank2_update(rec.y, 1.0f, dp);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);   // the reads of the next MFMA
+        __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);    // then this step's MFMAs
+        __builtin_amdgcn_sched_barrier(0);
+        cur = nxt;
+      }
+    };
+    if constexpr (decltype(back_tag)::value) {
+      if (skip) run(std::integral_constant<int, NSD>{}, std::true_type{});
+      else run(std::integral_constant<int, 0>{}, std::true_type{});
     } else {
-      const uint4 o = x[0][kbw * 64 + lane];
-      const v8i A = v8i{(int)o.x, (int)o.y, (int)o.z, (int)o.w, dn[0], dn[1], dn[2], dn[3]};
-      const int dascale = hf ? e + 127 : (int)es[kbw];
-      const uint8_t* Qc = Cc + C::QC_OFF;
-      const uint8_t* Qcs = Cc + C::QCS_OFF;
-#pragma unroll
-      for (int i = 0; i < CK; i++) {
-        const int ch = 32 * i + li;
-        acc[i] = mfma_mx(A, frag_cols_swz(Qc, ch, hf), acc[i], dascale, Qcs[ch * 2 + hf]);
-      }
+      // S and dP only (the first tile, before any dV / dK work)
+      if (!skip) run(std::integral_constant<int, 0>{}, std::false_type{});
     }
   };
 
@@ -547,10 +605,9 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
       if (more) stage_cols<DQK, DV>(Cl, ld, head_of(p1), q0_of(p1), N);
     }
     if (i + 2 < total) stage_rows<DQK, DV>(Rl, ld, head_of(p2), q0_of(p2), N);
-    const bool skip1 = front_skip(p1);
-    if (more) sdp(R1, skip1, rec);
-    back(Cc, es, x);
-    __builtin_amdgcn_sched_barrier(0);   // both MFMA groups issue before the VALU work below
+    const bool skip1 = !more || front_skip(p1);
+    mfmas(R1, skip1, rec, Cc, es, x, std::true_type{});
+    __builtin_amdgcn_sched_barrier(0);   // every MFMA issues before the VALU work below
     if constexpr (NCB == 1) {
       lds_sync();                          // every wave has read the col operands of tile i
       if (more) stage_cols<DQK, DV>(Cl, ld, head_of(p1), q0_of(p1), N);
@@ -565,7 +622,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   TilePos pa = next_pos(p0, G);
   if (total > 1) stage_rows<DQK, DV>((lds8*)rB, ld, head_of(pa), q0_of(pa), N);
   lds_barrier();
-  sdp(rA, front_skip(p0), row_rec(rA));
+  mfmas(rA, front_skip(p0), row_rec(rA), cA, esA, xA, std::false_type{});
   front_vals(p0, dsA, esA, xA);
 
   TilePos p = p0;

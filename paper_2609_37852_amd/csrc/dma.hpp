@@ -132,6 +132,15 @@ __device__ __forceinline__ v8i frag_cols_swz(const uint8_t* tile, int ch, int hf
   const uint4 hi = *reinterpret_cast<const uint4*>(base + 16 * ((hf + 2) ^ s));
   return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
 }
+// The same with explicit chunk indices (clo: bytes 0..15, chi: 16..31, each
+// before the swizzle).
+__device__ __forceinline__ v8i frag_cols_chunks(const uint8_t* tile, int ch, int clo, int chi) {
+  const int s = swz_col(ch);
+  const uint8_t* base = tile + ch * 64;
+  const uint4 lo = *reinterpret_cast<const uint4*>(base + 16 * (clo ^ s));
+  const uint4 hi = *reinterpret_cast<const uint4*>(base + 16 * (chi ^ s));
+  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
 
 // Precomputed plans for the tile loads of one wave: the lane's byte offset in
 // the source matrix for its first load instruction (k = w); the later ones
