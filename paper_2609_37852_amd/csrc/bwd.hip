@@ -81,12 +81,13 @@ struct BwdCfg {
   // dS' tiles, exponents and code exchange, two of each
   static constexpr int FIXED = 2 * (BKB * DST + KBW * 2 + 2 * KBW * 64 * 16);
   // the workgroup's K and V row codes [BKB][DQK + DV] (swizzled), read as
-  // MFMA operands instead of being held in registers
+  // MFMA operands from LDS at wide heads; up to d = 128 each lane keeps its
+  // key's fragments in registers (no LDS traffic for them)
   static constexpr int KV = BKB * (DQK + DV);
   static constexpr int LIM = 156 * 1024;
   // row parts are double-buffered; col parts too and K / V are kept in LDS
   // where the LDS allows, preferring K / V in LDS over a second col buffer
-  static constexpr bool KV_LDS = 2 * RSTAGE + CSTAGE + FIXED + KV <= LIM;
+  static constexpr bool KV_LDS = DQK + DV > 256 && 2 * RSTAGE + CSTAGE + FIXED + KV <= LIM;
   static constexpr int NCB = 2 * RSTAGE + 2 * CSTAGE + FIXED + (KV_LDS ? KV : 0) <= LIM ? 2 : 1;
 };
 
@@ -138,7 +139,7 @@ struct BwdLoads {
 template <int DQK, int DV>
 __device__ __forceinline__ int loader_index() {
   using C = BwdCfg<DQK, DV>;
-  const int w = (int)(threadIdx.x >> 6);
+  const int w = wave_id();
   return w < C::NLD ? w : -1;
 }
 
@@ -729,7 +730,7 @@ __global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
   constexpr int KT = DQK * 64, KSB = 2 * DQK;       // K tile and scale bytes per step
   __shared__ __attribute__((aligned(16))) uint8_t kA[KT + KSB];
   __shared__ __attribute__((aligned(16))) uint8_t kB[KT + KSB];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
+  const int lane = threadIdx.x & 63, w = wave_id(), hf = lane >> 5, li = lane & 31;
   const int N = (int)a.N, nqb = N / 32;
   const int ntile = (nqb + NW - 1) / NW;
   const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);

@@ -135,6 +135,12 @@ __device__ __forceinline__ WgCoord query_major_coord(int id, int B, int Hq, int 
   return c;
 }
 
+// Index of the calling wave in its workgroup, as a wave-uniform (scalar)
+// value: taken from threadIdx.x directly the compiler treats it as varying
+// per lane, so every branch on it (which waves load, store or skip) would be
+// compiled as a divergent branch with exec-mask bookkeeping.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
+
 // Value of `v` in the partner lane l ^ 32.
 __device__ __forceinline__ float partner(float v) {
   Pair p = permlane32_swap(v, v);
