@@ -98,24 +98,38 @@ __host__ __device__ __forceinline__ int64_t tri_units(int64_t q) {
   return (q & 1) ? (m + 1) * (m + 1) : m * (m + 1);
 }
 
-// Per-(batch, query head) base pointers of the query-side operands.
-struct BwdHead {
-  const uint8_t *qrow, *qsc, *orow, *osc, *qcol, *ocol, *tcs;
-  const float4* rows;
+// Query-side operands of one (batch, KV group): the bases of its first query
+// head (the G heads of a group are adjacent in every layout); a loading wave
+// builds a buffer over the group's heads at each load and adds the head and
+// tile offsets as scalar offsets to loop-invariant lane offsets.
+struct BwdGroup {
+  const uint8_t *qrow, *qsc, *orow, *osc, *qcol, *ocol, *tcs, *rows;
 };
 
 template <int DQK, int DV>
-__device__ __forceinline__ BwdHead bwd_head(const AttnArgs& a, size_t bh, int N) {
-  BwdHead p;
-  p.qrow = a.q_code + bh * N * DQK;
-  p.qsc = a.q_scale + bh * N * (DQK / 32);
-  p.orow = a.do_code + bh * N * DV;
-  p.osc = a.do_scale + bh * N * (DV / 32);
-  p.qcol = a.qc_code + bh * DQK * N;
-  p.ocol = a.doc_code + bh * DV * N;
-  p.tcs = a.tile_cs + bh * ((N + 63) / 64) * (2 * (DQK + DV));
-  p.rows = reinterpret_cast<const float4*>(a.rows) + bh * N;
-  return p;
+struct BwdStrides {   // bytes from one query head to the next
+  int N;
+  __device__ __forceinline__ uint32_t q() const { return (uint32_t)N * DQK; }
+  __device__ __forceinline__ uint32_t qs() const { return (uint32_t)N * (DQK / 32); }
+  __device__ __forceinline__ uint32_t o() const { return (uint32_t)N * DV; }
+  __device__ __forceinline__ uint32_t os() const { return (uint32_t)N * (DV / 32); }
+  __device__ __forceinline__ uint32_t tcs() const { return (uint32_t)((N + 63) / 64) * (2 * (DQK + DV)); }
+  __device__ __forceinline__ uint32_t rows() const { return (uint32_t)N * 16; }
+};
+
+template <int DQK, int DV>
+__device__ __forceinline__ BwdGroup bwd_group(const AttnArgs& a, size_t bh0, int N) {
+  const BwdStrides<DQK, DV> S{N};
+  BwdGroup g;
+  g.qrow = a.q_code + bh0 * S.q();
+  g.qsc = a.q_scale + bh0 * S.qs();
+  g.orow = a.do_code + bh0 * S.o();
+  g.osc = a.do_scale + bh0 * S.os();
+  g.qcol = a.qc_code + bh0 * S.q();
+  g.ocol = a.doc_code + bh0 * S.o();
+  g.tcs = a.tile_cs + bh0 * S.tcs();
+  g.rows = reinterpret_cast<const uint8_t*>(a.rows) + bh0 * S.rows();
+  return g;
 }
 
 // Load plans of one loading wave (index w among the NLD) for the code tiles
@@ -143,39 +157,44 @@ __device__ __forceinline__ int loader_index() {
   return w < C::NLD ? w : -1;
 }
 
-// Direct-to-LDS loads of the row part of one query tile: codes, row scales
-// and the per-query records.
+// Direct-to-LDS loads of the row part of one query tile (head hi of the
+// group, queries i0..): codes, row scales and the per-query records.
 template <int DQK, int DV>
-__device__ __forceinline__ void stage_rows(lds8* st, const BwdLoads<DQK, DV>& L, const BwdHead& hp, int i0, int N) {
+__device__ __forceinline__ void stage_rows(lds8* st, const BwdLoads<DQK, DV>& L, const BwdGroup& g, int G, int hi,
+                                           int i0, int N) {
   using C = BwdCfg<DQK, DV>;
   constexpr int NWK = C::NLD;
   const int lane = threadIdx.x & 63, w = loader_index<DQK, DV>();
   if (w < 0) return;
-  L.q.issue(st + C::Q_OFF, hp.qrow, i0, N, w, lane);
-  L.o.issue(st + C::O_OFF, hp.orow, i0, N, w, lane);
-  dma_row_scales<DQK, NWK>(st + C::QS_OFF, hp.qsc, i0, N, w, lane, 0);
-  dma_row_scales<DV, NWK>(st + C::OS_OFF, hp.osc, i0, N, w, lane, 1);
+  const BwdStrides<DQK, DV> S{N};
+  L.q.issue_s(st + C::Q_OFF, make_buf(g.qrow, G * S.q()), hi * S.q(), i0, N, w, lane);
+  L.o.issue_s(st + C::O_OFF, make_buf(g.orow, G * S.o()), hi * S.o(), i0, N, w, lane);
+  dma_row_scales_s<DQK, NWK>(st + C::QS_OFF, make_buf(g.qsc, G * S.qs()), hi * S.qs(), i0, N, w, lane, 0);
+  dma_row_scales_s<DV, NWK>(st + C::OS_OFF, make_buf(g.osc, G * S.os()), hi * S.os(), i0, N, w, lane, 1);
   if (w == (3 % NWK)) {
-    const int r = i0 + lane < N ? i0 + lane : N - 1;
-    dma16(make_buf(hp.rows, (uint32_t)N * 16), (uint32_t)r * 16, st + C::ROW_OFF);
+    const int r = i0 + lane < N ? lane : N - 1 - i0;
+    dma16s(make_buf(g.rows, G * S.rows()), (uint32_t)r * 16, hi * S.rows() + (uint32_t)i0 * 16, st + C::ROW_OFF);
   }
 }
 
 // ... and of its col part: codes and the col scales packed by bwd_prep.
 template <int DQK, int DV>
-__device__ __forceinline__ void stage_cols(lds8* st, const BwdLoads<DQK, DV>& L, const BwdHead& hp, int i0, int N) {
+__device__ __forceinline__ void stage_cols(lds8* st, const BwdLoads<DQK, DV>& L, const BwdGroup& g, int G, int hi,
+                                           int i0, int N) {
   using C = BwdCfg<DQK, DV>;
   constexpr int NWK = C::NLD;
   const int lane = threadIdx.x & 63, w = loader_index<DQK, DV>();
   if (w < 0) return;
-  L.qc.issue(st + C::QC_OFF, hp.qcol, i0, N, w, lane);
-  L.oc.issue(st + C::OC_OFF, hp.ocol, i0, N, w, lane);
+  const BwdStrides<DQK, DV> S{N};
+  L.qc.issue_s(st + C::QC_OFF, make_buf(g.qcol, G * S.q()), hi * S.q(), i0, N, w, lane);
+  L.oc.issue_s(st + C::OC_OFF, make_buf(g.ocol, G * S.o()), hi * S.o(), i0, N, w, lane);
   constexpr int NCI = (C::CS_BYTES + 255) / 256;
-  const Buf tcs = make_buf(hp.tcs, (uint32_t)((N + 63) / 64) * C::CS_BYTES);
   for (int k = 0; k < NCI; k++) {
     if ((2 + k) % NWK != w) continue;   // loaders 2, 3, ...: 0 and 1 take the row scales
     const int off = 256 * k + 4 * lane;
-    if (off < C::CS_BYTES) dma4(tcs, (uint32_t)((i0 / 64) * C::CS_BYTES + off), st + C::QCS_OFF + 256 * k);
+    if (off < C::CS_BYTES)
+      dma4s(make_buf(g.tcs, G * S.tcs()), (uint32_t)off, hi * S.tcs() + (uint32_t)(i0 / 64) * C::CS_BYTES,
+            st + C::QCS_OFF + 256 * k);
   }
 }
 
@@ -345,7 +364,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   auto row_rec = [&](const uint8_t* R) __attribute__((always_inline)) {
     return *reinterpret_cast<const float2*>(R + C::ROW_OFF + (32 * qs + li) * 16 + 8 * hf);
   };
-  auto head_of = [&](TilePos p) __attribute__((always_inline)) { return bwd_head<DQK, DV>(a, bh0 + p.hi, N); };
+  const BwdGroup grp = bwd_group<DQK, DV>(a, bh0, N);
 
   // Pipeline, per tile i (each step a function of the buffers it touches):
   //   barrier (codes of tile i exchanged, loads of rows i+1 and cols i landed)
@@ -603,25 +622,25 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     ds_store(p, ds, es);
     const float2 rec = row_rec(R1);
     if constexpr (NCB == 2) {
-      if (more) stage_cols<DQK, DV>(Cl, ld, head_of(p1), q0_of(p1), N);
+      if (more) stage_cols<DQK, DV>(Cl, ld, grp, G, p1.hi, q0_of(p1), N);
     }
-    if (i + 2 < total) stage_rows<DQK, DV>(Rl, ld, head_of(p2), q0_of(p2), N);
+    if (i + 2 < total) stage_rows<DQK, DV>(Rl, ld, grp, G, p2.hi, q0_of(p2), N);
     const bool skip1 = !more || front_skip(p1);
     mfmas(R1, skip1, rec, Cc, es, x, std::true_type{});
     __builtin_amdgcn_sched_barrier(0);   // every MFMA issues before the VALU work below
     if constexpr (NCB == 1) {
       lds_sync();                          // every wave has read the col operands of tile i
-      if (more) stage_cols<DQK, DV>(Cl, ld, head_of(p1), q0_of(p1), N);
+      if (more) stage_cols<DQK, DV>(Cl, ld, grp, G, p1.hi, q0_of(p1), N);
     }
     if (more) front_vals(p1, ds1, es1, x1);
   };
 
   // prologue: rows of tiles 0 and 1, cols of tile 0; S, dP, P, dS of tile 0
   const TilePos p0 = TilePos{0, 0};
-  stage_rows<DQK, DV>((lds8*)rA, ld, head_of(p0), q0_of(p0), N);
-  stage_cols<DQK, DV>((lds8*)cA, ld, head_of(p0), q0_of(p0), N);
+  stage_rows<DQK, DV>((lds8*)rA, ld, grp, G, p0.hi, q0_of(p0), N);
+  stage_cols<DQK, DV>((lds8*)cA, ld, grp, G, p0.hi, q0_of(p0), N);
   TilePos pa = next_pos(p0, G);
-  if (total > 1) stage_rows<DQK, DV>((lds8*)rB, ld, head_of(pa), q0_of(pa), N);
+  if (total > 1) stage_rows<DQK, DV>((lds8*)rB, ld, grp, G, pa.hi, q0_of(pa), N);
   lds_barrier();
   mfmas(rA, front_skip(p0), row_rec(rA), cA, esA, xA, std::false_type{});
   front_vals(p0, dsA, esA, xA);

@@ -44,6 +44,17 @@ __device__ __forceinline__ void dma16(const Buf& b, uint32_t off, lds8* lds_base
 __device__ __forceinline__ void dma4(const Buf& b, uint32_t off, lds8* lds_base) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(b.r, (__attribute__((address_space(3))) void*)lds_base, 4, (int)off, 0, 0, 0);
 }
+// The same with a wave-uniform part of the offset in a scalar register
+// (address = base + soff + voff): the per-lane part can stay in a long-lived
+// register while the head and tile offsets change.
+__device__ __forceinline__ void dma16s(const Buf& b, uint32_t voff, uint32_t soff, lds8* lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(b.r, (__attribute__((address_space(3))) void*)lds_base, 16, (int)voff,
+                                           (int)soff, 0, 0);
+}
+__device__ __forceinline__ void dma4s(const Buf& b, uint32_t voff, uint32_t soff, lds8* lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(b.r, (__attribute__((address_space(3))) void*)lds_base, 4, (int)voff,
+                                           (int)soff, 0, 0);
+}
 
 // Waits for this wave's LDS writes and direct-to-LDS loads (and any other
 // vector memory operation), then a workgroup barrier ordered for LDS only.
@@ -103,6 +114,21 @@ __device__ __forceinline__ void dma_row_scales(lds8* lds, const uint8_t* scale, 
     if (off < BYTES) {
       const int g = i0 * (D / 32) + off, lim = N * (D / 32) - 4;
       dma4(b, (uint32_t)(g < lim ? g : lim), lds + 256 * k);
+    }
+  }
+}
+
+// dma_row_scales for a scale matrix at byte offset `head` inside buffer b.
+template <int D, int NWK, int ROWS = 64>
+__device__ __forceinline__ void dma_row_scales_s(lds8* lds, const Buf& b, uint32_t head, int i0, int N, int w,
+                                                 int lane, int first_wave) {
+  constexpr int BYTES = ROWS * D / 32, NI = (BYTES + 255) / 256;
+  for (int k = 0; k < NI; k++) {
+    if ((first_wave + k) % NWK != w) continue;
+    const int off = 256 * k + 4 * lane;
+    if (off < BYTES) {
+      const int g = i0 * (D / 32) + off, lim = N * (D / 32) - 4;
+      dma4s(b, (uint32_t)(g < lim ? g : lim), head, lds + 256 * k);
     }
   }
 }
@@ -177,6 +203,25 @@ struct RowLoads {
       if (k < NI) dma16(b, base + (STRIDED ? off[0] + 1024 * NWK * j : off[j]), lds + 1024 * k);
     }
   }
+  // Rows of a matrix at byte offset `head` inside buffer b (head: wave-uniform).
+  __device__ __forceinline__ void issue_s(lds8* lds, const Buf& b, uint32_t head, int i0, int N, int w,
+                                          int lane) const {
+    if (i0 + ROWS > N) {
+      for (int k = w; k < NI; k += NWK) {
+        const int o = 1024 * k + 16 * lane;
+        const int r = o / D, p = (o % D) / 16;
+        const int row = i0 + r < N ? i0 + r : N - 1;
+        dma16s(b, (uint32_t)(row * D + 16 * (p ^ swz_row<D>(r))), head, lds + 1024 * k);
+      }
+      return;
+    }
+    const uint32_t sb = head + (uint32_t)i0 * D;
+#pragma unroll
+    for (int j = 0; j < NS; j++) {
+      const int k = w + NWK * j;
+      if (k < NI) dma16s(b, STRIDED ? off[0] + 1024 * NWK * j : off[j], sb, lds + 1024 * k);
+    }
+  }
 };
 
 // Col tile: channels [0, D), sequence positions [i0, i0 + COLS) of a [D][N]
@@ -219,6 +264,29 @@ struct ColLoads {
     for (int j = 0; j < NS; j++) {
       const int k = w + NWK * j;
       if (k < NI) dma16(b, base + (uint32_t)(j * cstride), lds + 1024 * k);
+    }
+  }
+  // The same for a matrix at byte offset `head` inside buffer b.
+  __device__ __forceinline__ void issue_s(lds8* lds, const Buf& b, uint32_t head, int i0, int N, int w,
+                                          int lane) const {
+    if (i0 + COLS > N) {
+#pragma unroll
+      for (int j = 0; j < NS; j++) {
+        const int k = w + NWK * j;
+        if (k >= NI) break;
+        const int o = 1024 * k + 16 * lane;
+        const int c = o / COLS, p = (o % COLS) / 16;
+        const int q = COLS == 64 ? (p ^ swz_col(c)) : (p ^ swz_row<128>(c));
+        const int col = i0 + 16 * q < N - 16 ? i0 + 16 * q : N - 16;
+        dma16s(b, (uint32_t)(c * N + col), head, lds + 1024 * k);
+      }
+      return;
+    }
+    const uint32_t sb = head + (uint32_t)i0;
+#pragma unroll
+    for (int j = 0; j < NS; j++) {
+      const int k = w + NWK * j;
+      if (k < NI) dma16s(b, off + (uint32_t)(j * cstride), sb, lds + 1024 * k);
     }
   }
 };
