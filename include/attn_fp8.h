@@ -42,8 +42,10 @@
  *     {(64,64), (128,128), (256,256), (192,128)}, heads_q % heads_kv == 0.
  *     Batch or head counts of 0 are valid empty problems.  Launch limits
  *     (ATTN_FP8_EUNSUPPORTED beyond them): batch and heads <= 65535,
- *     seqlen <= 2^30, batch * heads_q * seqlen < 2^31 and
- *     batch * heads_kv * seqlen < 2^30.
+ *     seqlen <= 2^30, batch * heads_q * seqlen < 2^31,
+ *     batch * heads_kv * seqlen < 2^30 and (heads_q / heads_kv) * seqlen *
+ *     max(dim_qk, dim_v) < 2^32 (one GQA group's operands are addressed
+ *     with 32-bit offsets).
  *   - Strides are in elements; the last (channel) dimension is contiguous.
  *     Device pointers must be 16-byte aligned, and every stride times the
  *     element size must be a multiple of 16 bytes.

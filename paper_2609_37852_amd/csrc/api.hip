@@ -95,8 +95,17 @@ int check_problem(const attn_fp8_problem* p) {
       p->batch * p->heads_kv * p->seqlen >= (int64_t(1) << 30))
     return fail(ATTN_FP8_EUNSUPPORTED, "problem exceeds the launch grid limits (B Hq N = %lld)",
                 (long long)(p->batch * p->heads_q * p->seqlen));
+  // the kernels address the operands of one GQA group (G = Hq / Hkv adjacent
+  // heads) with 32-bit buffer offsets
+  if (p->heads_kv > 0) {
+    const int64_t G = p->heads_q / p->heads_kv, D = p->dim_qk > p->dim_v ? p->dim_qk : p->dim_v;
+    if (G * p->seqlen * D >= (int64_t(1) << 32))
+      return fail(ATTN_FP8_EUNSUPPORTED, "problem exceeds the 32-bit buffer offsets (G N D = %lld)",
+                  (long long)(G * p->seqlen * D));
+  }
   return ATTN_FP8_OK;
 }
+
 
 bool empty(const attn_fp8_problem* p) { return p->batch == 0 || p->seqlen == 0 || p->heads_q == 0; }
 

@@ -42,7 +42,9 @@ def _fake_mx(addr=4096):
     (dict(seqlen=-32), -1), (dict(heads_kv=0), -1),
     # one launch dimension holds fewer than 2^32 work-items: B Hq N < 2^31, B Hkv N < 2^30
     (dict(batch=1024, heads_q=64, heads_kv=64, seqlen=1 << 15), -2),
-    (dict(batch=512, heads_q=64, heads_kv=64, seqlen=1 << 15), -2)])
+    (dict(batch=512, heads_q=64, heads_kv=64, seqlen=1 << 15), -2),
+    # one GQA group's operands within 32-bit buffer offsets: (Hq / Hkv) N D < 2^32
+    (dict(heads_q=64, heads_kv=1, seqlen=1 << 20), -2)])
 def test_fwd_rejects_bad_problem(kw, code):
     L = pk.lib()
     p = _prob(**kw).c()
