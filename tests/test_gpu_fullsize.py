@@ -22,7 +22,7 @@ def _slice_inputs(w, d, kvh=0):
                 do=d["do"][:1, :, hs]), hs
 
 
-@pytest.mark.parametrize("name", ["gqa_d128_8k"])
+@pytest.mark.parametrize("name", ["gqa_d128_8k", "gqa_d256_8k_qknorm", "mla_d192_4k"])
 def test_full_size_slice(name):
     w = synth.WORKLOADS[name]
     say(f"full-size {name}: {w}")
