@@ -150,7 +150,7 @@ size_t ws_delta_bytes(const attn_fp8_problem* p) {
   return round256((size_t)p->batch * p->heads_q * p->seqlen * 2 * sizeof(float));
 }
 size_t ws_rows_bytes(const attn_fp8_problem* p) {
-  return round256((size_t)p->batch * p->heads_q * p->seqlen * 4 * sizeof(float));
+  return round256((size_t)p->batch * p->heads_q * ((p->seqlen + 63) / 64) * 1024);
 }
 size_t ws_tile_cs_bytes(const attn_fp8_problem* p) {
   return round256((size_t)p->batch * p->heads_q * ((p->seqlen + 63) / 64) * 2 * (p->dim_qk + p->dim_v));

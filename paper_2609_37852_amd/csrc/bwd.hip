@@ -18,9 +18,14 @@
 //   S  = Q K^T, dP = dO V^T   MX MFMA (A = Q / dO row tiles in LDS, B = the
 //                             wave's K / V row codes in registers); lane l
 //                             owns key l % 32 and holds 16 queries.
-//   S' = S + q_c* k_c* - LSE / tau and dP' = (dP - hi) - lo by one FP32
-//        rank-2 MFMA each (the per-query values come from the records);
-//   P  = bwd_prob(S') = 2^(tau log2e S'), dS = P dP'.
+//   S' = S + q_c* k_c* - LSE / tau by one FP32 rank-2 MFMA (the per-query
+//        values come from the records);
+//   P  = bwd_prob(S') = 2^(tau log2e S'), dS = fma(P, dP, fl(P (-delta))):
+//        P dP enters exactly and every rounding is of its own element.  (The
+//        shift dP - delta taken first, as the definition reads, rounds every
+//        dP of one binade by the same amount, since they share one FP32
+//        grid; on long flat rows those equal errors add up, weighted by P,
+//        to more than the row's whole zero-sum budget.)
 //   P' = C8(256 P) with scale 2^-8;  dS' = C8(dS / 2^e) with one exponent e
 //        per aligned 32x32 block (the wave's 32 keys x 32 queries).
 //   dV += P'^T dO_col,  dK += dS'^T Q_col   (A = the codes after one
@@ -35,10 +40,11 @@
 // dQ = tau dS' K_col query-major, without atomics.
 //
 // A preparation kernel packs what the tile loop needs besides the code tiles
-// into arrays it can stream with the same direct loads: one 16-byte record
-// per query (isolated-channel query value, -delta hi, -LSE / tau, -delta lo:
-// a lane of half hf reads the pair at 8 hf, the A operands of the two rank-2
-// updates) and, per 64-query tile, the col-copy scales of Q and dO.
+// into arrays it can stream with the same direct loads: per 64-query tile a
+// 1 KB block of per-query values (the pair {isolated-channel query value,
+// -LSE / tau} at 8 q, the A operands of the score's rank-2 update, a lane of
+// half hf reading the value at 8 q + 4 hf; -delta at 512 + 4 q) and the
+// col-copy scales of Q and dO.
 #include <type_traits>
 
 #include "common.hpp"
@@ -69,7 +75,7 @@ struct BwdCfg {
   static constexpr int O_OFF = Q_OFF + BQ * DQK;                    // dO row codes [BQ][DV], swizzled
   static constexpr int QS_OFF = O_OFF + BQ * DV;                    // Q row scales [BQ][DQK/32]
   static constexpr int OS_OFF = al16(QS_OFF + BQ * DQK / 32);       // dO row scales [BQ][DV/32]
-  static constexpr int ROW_OFF = al16(OS_OFF + BQ * DV / 32);       // per-query records [BQ] x 16 B
+  static constexpr int ROW_OFF = al16(OS_OFF + BQ * DV / 32);       // the tile's 1 KB block of per-query values
   static constexpr int RSTAGE = ROW_OFF + BQ * 16;
   // col part (operands of dV and dK)
   static constexpr int QC_OFF = 0;                                  // Q col codes [DQK][BQ], swizzled
@@ -114,7 +120,7 @@ struct BwdStrides {   // bytes from one query head to the next
   __device__ __forceinline__ uint32_t o() const { return (uint32_t)N * DV; }
   __device__ __forceinline__ uint32_t os() const { return (uint32_t)N * (DV / 32); }
   __device__ __forceinline__ uint32_t tcs() const { return (uint32_t)((N + 63) / 64) * (2 * (DQK + DV)); }
-  __device__ __forceinline__ uint32_t rows() const { return (uint32_t)N * 16; }
+  __device__ __forceinline__ uint32_t rows() const { return (uint32_t)((N + 63) / 64) * 1024; }
 };
 
 template <int DQK, int DV>
@@ -172,8 +178,8 @@ __device__ __forceinline__ void stage_rows(lds8* st, const BwdLoads<DQK, DV>& L,
   dma_row_scales_s<DQK, NWK>(st + C::QS_OFF, make_buf(g.qsc, G * S.qs()), hi * S.qs(), i0, N, w, lane, 0);
   dma_row_scales_s<DV, NWK>(st + C::OS_OFF, make_buf(g.osc, G * S.os()), hi * S.os(), i0, N, w, lane, 1);
   if (w == (3 % NWK)) {
-    const int r = i0 + lane < N ? lane : N - 1 - i0;
-    dma16s(make_buf(g.rows, G * S.rows()), (uint32_t)r * 16, hi * S.rows() + (uint32_t)i0 * 16, st + C::ROW_OFF);
+    dma16s(make_buf(g.rows, G * S.rows()), (uint32_t)lane * 16, hi * S.rows() + (uint32_t)(i0 / 64) * 1024,
+           st + C::ROW_OFF);
   }
 }
 
@@ -362,7 +368,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   BwdLoads<DQK, DV> ld;
   ld.init(loader_index<DQK, DV>() >= 0 ? loader_index<DQK, DV>() : 0, lane, N);
   auto row_rec = [&](const uint8_t* R) __attribute__((always_inline)) {
-    return *reinterpret_cast<const float2*>(R + C::ROW_OFF + (32 * qs + li) * 16 + 8 * hf);
+    return *reinterpret_cast<const float*>(R + C::ROW_OFF + (32 * qs + li) * 8 + 4 * hf);
   };
   const BwdGroup grp = bwd_group<DQK, DV>(a, bh0, N);
 
@@ -379,7 +385,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
 
   // P, dS and their codes from the shifted s, dp; EDGE tiles may skip the
   // half or hold the diagonal block (masked)
-  auto probs = [&](auto edge_tag, int qb, bool skip, int h) __attribute__((always_inline)) {
+  auto probs = [&](auto edge_tag, int qb, bool skip, int h, const uint8_t* R) __attribute__((always_inline)) {
     constexpr bool EDGE = decltype(edge_tag)::value;
     v4i pc, dc;
     e = -127;
@@ -392,13 +398,16 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     float amax = 0.f;
 #pragma unroll
     for (int g = 0; g < 4; g++) {
+      // -delta of the lane's four queries 8 g + 4 hf .. + 3 of the half
+      const float4 nd = *reinterpret_cast<const float4*>(R + C::ROW_OFF + 512 + 4 * (32 * qs + 8 * g + 4 * hf));
+      const float ndv[4] = {nd.x, nd.y, nd.z, nd.w};
 #pragma unroll
       for (int e4 = 0; e4 < 4; e4++) {
         const int r = 4 * g + e4;
         float p = bwd_prob(s[r], c);
         if (EDGE && qb == kw0) p = (li > 8 * g + 4 * hf + e4) ? 0.f : p;   // diagonal block: key > query
         s[r] = p;
-        dp[r] = p * dp[r];
+        dp[r] = __builtin_fmaf(p, dp[r], p * ndv[e4]);
         amax = fmaxf(amax, fabsf(dp[r]));
       }
     }
@@ -437,15 +446,15 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   };
 
   // P, dS and codes of the tile at p for this wave's half, written to ds / es / x
-  auto front_vals = [&](TilePos p, uint8_t* ds, uint8_t* es, uint4 (*x)[KBW * 64])
+  auto front_vals = [&](TilePos p, const uint8_t* R, uint8_t* ds, uint8_t* es, uint4 (*x)[KBW * 64])
       __attribute__((always_inline)) {
     const int i0 = q0_of(p);
     const int qb = i0 + 32 * qs;
     const bool full = i0 >= kb0 + BKB && i0 + BQ <= N;
     const bool skip = !full && (!live || qb < kw0 || qb >= N);
     const int h = kh * G + p.hi;
-    if (full) probs(std::false_type{}, qb, skip, h);
-    else probs(std::true_type{}, qb, skip, h);
+    if (full) probs(std::false_type{}, qb, skip, h, R);
+    else probs(std::true_type{}, qb, skip, h, R);
     // dS' codes for the dQ units and the exchange with the other half
     *reinterpret_cast<uint4*>(ds + (32 * kbw + li) * C::DST + 32 * qs + 16 * hf) =
         make_uint4((uint32_t)dn[0], (uint32_t)dn[1], (uint32_t)dn[2], (uint32_t)dn[3]);
@@ -462,9 +471,9 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   };
 
   // The MFMAs of one pipeline step, as one straight sequence: S and dP of the
-  // next tile's half (skipped halves: none; zero codes later), the two
-  // rank-2 updates (per-query shifts: S += q_c* k_c*, then -LSE / tau; dP -=
-  // hi, then lo), and dV += P'^T dO_col (first wave of a key block) or dK +=
+  // next tile's half (skipped halves: none; zero codes later), the rank-2
+  // update of S (per-query shifts: S += q_c* k_c*, then -LSE / tau), and
+  // dV += P'^T dO_col (first wave of a key block) or dK +=
   // dS'^T Q_col (second).  The LDS operands of each MFMA are read one MFMA
   // ahead and a scheduling fence keeps them there, so each MFMA waits only
   // for its own reads while the next ones are in flight.
@@ -479,7 +488,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     v8i a, b;
     int sa, sb;
   };
-  auto mfmas = [&](const uint8_t* R, bool skip, float2 rec, const uint8_t* Cc, const uint8_t* es,
+  auto mfmas = [&](const uint8_t* R, bool skip, float rec, const uint8_t* Cc, const uint8_t* es,
                    uint4 (*x)[KBW * 64], auto back_tag) __attribute__((always_inline)) {
     const uint8_t* Q = R + C::Q_OFF;
     const uint8_t* Qs = R + C::QS_OFF;
@@ -530,9 +539,9 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
         acc[i] = mfma_mx(r.a, r.b, acc[i], r.sa, r.sb);
       }
     };
-    // operations M0 .. M1 - 1 of the sequence; the rank-2 updates follow the
-    // second dV / dK MFMA (the S and dP chains have finished by then), or the
-    // last S / dP MFMA when there is no dV / dK work
+    // operations M0 .. M1 - 1 of the sequence; the rank-2 update follows the
+    // second dV / dK MFMA (the S chain has finished by then), or the last
+    // S / dP MFMA when there is no dV / dK work
     auto run = [&](auto from_tag, auto with_back) __attribute__((always_inline)) {
       constexpr int M0 = decltype(from_tag)::value;
       constexpr int M1 = decltype(with_back)::value ? NSD + CMAX : NSD;
@@ -552,8 +561,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
         if (m + 1 < M1 && (m + 1 < NSD || m + 1 - NSD < (CK < CV ? CK : CV) || m + 1 - NSD < nb)) nxt = load(m + 1);
         if (act) exec(m, cur);
         if (M0 == 0 && m == R2) {
-          s = rank2_update(rec.x, kb, s);
-          dp = rank2_update(rec.y, 1.0f, dp);
+          s = rank2_update(rec, kb, s);
         }
         __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);   // the reads of the next MFMA
         __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);    // then this step's MFMAs
@@ -620,7 +628,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     // any load into LDS is in flight: the dQ units of tile i and the records
     // of tile i+1
     ds_store(p, ds, es);
-    const float2 rec = row_rec(R1);
+    const float rec = row_rec(R1);
     if constexpr (NCB == 2) {
       if (more) stage_cols<DQK, DV>(Cl, ld, grp, G, p1.hi, q0_of(p1), N);
     }
@@ -632,7 +640,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
       lds_sync();                          // every wave has read the col operands of tile i
       if (more) stage_cols<DQK, DV>(Cl, ld, grp, G, p1.hi, q0_of(p1), N);
     }
-    if (more) front_vals(p1, ds1, es1, x1);
+    if (more) front_vals(p1, R1, ds1, es1, x1);
   };
 
   // prologue: rows of tiles 0 and 1, cols of tile 0; S, dP, P, dS of tile 0
@@ -643,7 +651,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
   if (total > 1) stage_rows<DQK, DV>((lds8*)rB, ld, grp, G, pa.hi, q0_of(pa), N);
   lds_barrier();
   mfmas(rA, front_skip(p0), row_rec(rA), cA, esA, xA, std::false_type{});
-  front_vals(p0, dsA, esA, xA);
+  front_vals(p0, rA, dsA, esA, xA);
 
   TilePos p = p0;
   for (int i = 0; i < total; i += 2) {
@@ -694,8 +702,10 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
 }
 
 // Query-side data the tile loop streams besides the code tiles:
-//   rows    [B, Hq, N] x 16 B: {isolated-channel query value, -delta hi,
-//           -LSE / tau, -delta lo};
+//   rows    [B, Hq, ceil(N/64)] x 1 KB: per 64-query tile, the pairs
+//           {isolated-channel query value, -LSE / tau} of its queries (8 B
+//           each), then -delta of each (4 B; delta rounded to FP32, i.e. its
+//           hi part), zero past the end of the sequence;
 //   tile_cs [B, Hq, ceil(N/64)] x 2 (Dqk + Dv) B: for each 64-query tile, the
 //           col-copy scales of Q then dO for the tile's two 32-query groups
 //           ([channel][group]), the second clamped to the first past the end;
@@ -708,11 +718,19 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
   const size_t bh = (size_t)b * a.Hq + h;
   const int i0 = blockIdx.x * 64;
-  if (threadIdx.x < 64 && i0 + (int)threadIdx.x < N) {
-    const size_t row = bh * N + i0 + threadIdx.x;
-    const float2 d = *reinterpret_cast<const float2*>(a.delta + row * 2);
-    const float qh = hot >= 0 ? row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot) : 0.f;
-    reinterpret_cast<float4*>(a.rows)[row] = make_float4(qh, -d.x, neg_lse_over_tau(a.lse[row], a.tau), -d.y);
+  if (threadIdx.x < 64) {
+    uint8_t* blk = reinterpret_cast<uint8_t*>(a.rows) + (bh * ((N + 63) / 64) + blockIdx.x) * 1024;
+    float2 pr = make_float2(0.f, 0.f);
+    float nd = 0.f;
+    if (i0 + (int)threadIdx.x < N) {
+      const size_t row = bh * N + i0 + threadIdx.x;
+      const float2 d = *reinterpret_cast<const float2*>(a.delta + row * 2);
+      const float qh = hot >= 0 ? row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot) : 0.f;
+      pr = make_float2(qh, neg_lse_over_tau(a.lse[row], a.tau));
+      nd = -d.x;
+    }
+    reinterpret_cast<float2*>(blk)[threadIdx.x] = pr;
+    reinterpret_cast<float*>(blk + 512)[threadIdx.x] = nd;
   }
   const int g0 = i0 / 32, g1 = (i0 + 32 < N ? i0 + 32 : i0) / 32;
   uint8_t* dst = a.tile_cs + (bh * ((N + 63) / 64) + blockIdx.x) * (2 * (DQK + DV));

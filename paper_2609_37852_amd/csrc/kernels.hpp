@@ -49,7 +49,7 @@ struct AttnArgs {
   float* lse_out;
   const float* delta;                  // [B,Hq,N,2]
   float* delta_out;
-  float* rows;                         // [B,Hq,N,4] backward per-query records (workspace)
+  float* rows;                         // [B,Hq,ceil(N/64)] x 1 KB backward per-query values (workspace)
   uint8_t* tile_cs;                    // [B,Hq,ceil(N/64),2(Dqk+Dv)] backward per-tile col scales (workspace)
   uint8_t* tile_kcs;                   // [B,Hkv,ceil(N/64),2 Dqk] K col scales per 64-key step (workspace)
   void* o;  int64_t os[3]; int o_bf16;

@@ -53,3 +53,43 @@ def test_full_size_slice(name):
     assert rep["violations"] == 0
     for kk in ("O", "dQ", "dK", "dV"):
         assert errs[kk] <= REL_TOL, (kk, errs[kk])
+
+
+def test_long_context_prefix():
+    """C5 (N = 65536) at full size: causal attention is closed under
+    prefixes (query i sees keys 0..i only, and every quantization block lies
+    inside 32 consecutive tokens), so O, LSE, the matched delta and dQ of the
+    first M queries equal those of the problem cut at M.  The oracle runs on
+    the (batch 0, KV head 0) group cut at M = 8192; dK and dV depend on later
+    queries and are not compared here."""
+    w = synth.WORKLOADS["gqa_d128_64k_nope"]
+    M = 8192
+    say(f"full-size {w.name}: {w}, prefix {M}")
+    d = synth.generate(w, seed=0)
+    q, k, v, do = (to_dev(d[n], w.dtype) for n in ("q", "k", "v", "do"))
+    p = problem(w)
+    mq, mk, mv, mdo = (pk.attn_fp8_quantize(t) for t in (q, k, v, do))
+    o, lse = pk.attn_fp8_fwd(p, mq, mk, mv)
+    delta = pk.attn_fp8_delta(p, pk.DELTA_MATCHING, mq, mk, mv, mdo, lse)
+    dq, dk, dv, rs = pk.attn_fp8_bwd(p, pk.DELTA_MATCHING, mq, mk, mv, mdo, lse, grad_dtype=torch.float32,
+                                     rowstats=True)
+    torch.cuda.synchronize()
+    say("  gpu done")
+    sl, hs = _slice_inputs(w, d)
+    sl = {n: t[:, :M] for n, t in sl.items()}
+    t = time.time()
+    ref, _ = orc.attention_from_inputs(sl["q"], sl["k"], sl["v"], sl["do"], float(np.float32(w.tau)),
+                                       want_rowstats=True)
+    say(f"  oracle prefix {time.time() - t:.1f}s")
+    g = dict(O=np64(o[:1, :M, hs]), LSE=np64(lse[:1, hs, :M]), dQ=np64(dq[:1, :M, hs]),
+             delta=np64(delta[:1, hs, :M]))
+    errs = {kk: rel_err(g[kk], ref[kk]) for kk in ("O", "dQ")}
+    errs["LSE_max_abs"] = float(np.max(np.abs(g["LSE"] - ref["LSE"])))
+    errs["delta"] = rel_err(g["delta"][..., 0] + g["delta"][..., 1], ref["delta"])
+    say("  errors", {kk: f"{vv:.3e}" for kk, vv in errs.items()})
+    rep = invariant_report(rs[:1, hs, :M].cpu().numpy(), ref["rowstats"])
+    say("  invariant", rep)
+    assert rep["violations"] == 0
+    for kk in ("O", "dQ"):
+        assert errs[kk] <= REL_TOL, (kk, errs[kk])
+    assert errs["LSE_max_abs"] <= 1e-3 and errs["delta"] <= 1e-3, errs
