@@ -183,6 +183,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="gqa_d128_8k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--diagnostics", action="store_true",
+                    help="also report the row-sum and key-gradient diagnostics of the three corrections "
+                         "(untimed; five extra backward runs)")
     ap.add_argument("--traffic", default=TRAFFIC_SUMMARY,
                     help="summary with the measured HBM bytes of the bwd kernel (used while its sources match)")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -329,6 +332,9 @@ def main():
         torch.neg(src, out=dst)
         torch.cuda.synchronize()
         line["copy_calibration_bytes"] = n
+    if args.diagnostics:
+        from paper_2609_37852_amd import diagnostics
+        line["diagnostics"] = diagnostics.run(p, mq, mk, mv, mdo, lse, do, o)
     if not args.no_cpu_baseline:
         threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
         line["cpu_baseline"] = cpu_baseline(w, d, threads)

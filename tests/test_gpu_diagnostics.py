@@ -1,0 +1,32 @@
+"""Diagnostics of the three corrections on the GPU (App. C.1 on synthetic
+data): the matched correction's pre-cast row sums are at FP32 rounding level
+and far below the saved-output corrections'; its correction pass agrees with
+the backward's own sums (e_i); the stale correction leaves the larger
+key-gradient common mode."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_37852_amd as pk
+from paper_2609_37852_amd import diagnostics, synth
+from _helpers import problem, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def test_three_corrections_ordering():
+    w = synth.with_shape(synth.WORKLOADS["gqa_d128_8k"], B=1, N=2048)
+    d = synth.generate(w, seed=0)
+    q, k, v, do = (to_dev(d[n], w.dtype) for n in ("q", "k", "v", "do"))
+    p = problem(w)
+    mq, mk, mv, mdo = (pk.attn_fp8_quantize(t) for t in (q, k, v, do))
+    o, lse = pk.attn_fp8_fwd(p, mq, mk, mv)
+    torch.cuda.synchronize()
+    r = diagnostics.run(p, mq, mk, mv, mdo, lse, do, o)
+    say("diagnostics", r)
+    st, co, ma = r["stale_rowsum"], r["consistent_do"], r["matching"]
+    assert st["r_pre_median"] > co["r_pre_median"] > 100 * ma["r_pre_median"]
+    assert ma["r_pre_median"] < 1e-5
+    assert ma["e_median"] < 1e-5
+    assert st["c_K_median"] > ma["c_K_median"]
+    assert np.isfinite([st["kappa_mean"], co["kappa_mean"], ma["kappa_mean"]]).all()
