@@ -176,10 +176,11 @@ int attn_fp8_bwd_workspace_size(const attn_fp8_problem* p, size_t* bytes);
  *            element strides {b, n, h} in dq_strides / dk_strides / dv_strides.
  *   workspace device, at least attn_fp8_bwd_workspace_size() bytes, 256-byte
  *            aligned; contents on entry are ignored.
- *   rowstats nullable device double [B, Hq, N, 4], zeroed by the caller:
- *            accumulates, per query row and over all keys, sum dS, sum |dS|
- *            and sum dS' (FP64 sums of the FP32 values before / after the
- *            cast) and max |dS| (debug instrumentation of App. C.1; slower).
+ *   rowstats nullable device double [B, Hq, N, 5], zeroed by the caller:
+ *            accumulates, per query row and over all keys, sum dS, sum |dS|,
+ *            sum dS', max |dS| and sum |dS'| (FP64 sums of the FP32 values
+ *            before / after the cast; debug instrumentation of App. C.1;
+ *            slower).
  *   main_events nullable pointer to two events: recorded on `stream`
  *            immediately before and after the main backward kernel, so a
  *            caller can time that kernel alone. */

@@ -212,7 +212,7 @@ def attn_fp8_bwd(p: Problem, mode: int, q: MX, k: MX, v: MX, dout: MX, lse, dout
     ws_bytes = attn_fp8_bwd_workspace_size(p)
     if workspace is None:
         workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
-    rs = torch.zeros((p.batch, p.heads_q, p.seqlen, 4), dtype=torch.float64, device=dev) if rowstats else None
+    rs = torch.zeros((p.batch, p.heads_q, p.seqlen, 5), dtype=torch.float64, device=dev) if rowstats else None
     pc = p.c()
     mxs = [m.c() for m in (q, k, v, dout)]
     ds = _strides_bnh(dout_raw) if dout_raw is not None else None

@@ -428,15 +428,17 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
         const double s0 = half_sum_d((double)dp[r]);
         const double s1 = half_sum_d((double)fabsf(dp[r]));
         const double s2 = half_sum_d((double)cast);
+        const double s3 = half_sum_d((double)fabsf(cast));
         const float mx = half_max(fabsf(dp[r]));
         const int qi = qb + 8 * (r >> 2) + 4 * hf + (r & 3);
         if (li == 0) {
-          double* sp = a.rowstats + (((size_t)b * Hq + h) * N + qi) * 4;
+          double* sp = a.rowstats + (((size_t)b * Hq + h) * N + qi) * 5;
           atomicAdd(sp + 0, s0);
           atomicAdd(sp + 1, s1);
           atomicAdd(sp + 2, s2);
           atomicMax(reinterpret_cast<unsigned long long*>(sp + 3),
                     (unsigned long long)__double_as_longlong((double)mx));
+          atomicAdd(sp + 4, s3);
         }
       }
     }

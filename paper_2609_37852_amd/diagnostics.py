@@ -1,9 +1,11 @@
 """Row-sum and key-gradient diagnostics of the backward (App. C.1, on synthetic
 data), from the per-row statistics the backward records with `rowstats`:
-[B, Hq, N, 4] FP64 = (sum_j dS_ij, sum_j |dS_ij|, sum_j dS'_ij, max_j |dS_ij|)
-with dS the FP32 score gradient before the FP8 cast and dS' the decoded cast.
+[B, Hq, N, 5] FP64 = (sum_j dS_ij, sum_j |dS_ij|, sum_j dS'_ij, max_j |dS_ij|,
+sum_j |dS'_ij|) with dS the FP32 score gradient before the FP8 cast and dS'
+the decoded cast.
 
   r_pre_i  = |sum_j dS_ij| / l_i,   r_post_i = |sum_j dS'_ij| / l_i,
+  r_post,own_i = |sum_j dS'_ij| / l'_i,  l'_i = sum_j |dS'_ij| (rows with l'_i > 0),
   kappa_i  = (sum_j dS'_ij - sum_j dS_ij) / l_i,     l_i = sum_j |dS_ij|,
   c_K      = || sum_j dK_j ||_2 / (sum_j ||dK_j||_2^2)^(1/2)   per (batch, KV head),
   e_i      = |delta_i - delta*_i| |S^P_i| / l_i,  with S^PdP_i = R_i(0),
@@ -11,8 +13,7 @@ with dS the FP32 score gradient before the FP8 cast and dS' the decoded cast.
              pre-cast row sum of a backward run with the correction injected as c.
 
 Rows: query positions i >= 64 whose l_i is nonzero under every correction
-compared (the common row set).  r^post,own (own cast denominator) needs
-sum_j |dS'_ij|, which the recorded statistics do not hold.
+compared (the common row set).
 The numpy functions here run anywhere; run() drives the library on a GPU.
 """
 import numpy as np
@@ -33,7 +34,9 @@ def common_rows(stats_by_mode, min_row=MIN_ROW):
 
 def row_residuals(stats_by_mode, min_row=MIN_ROW):
     """Per correction: median r_pre and r_post, and mean kappa, over the
-    common row set (rows whose cast gradient vanishes count with r_post 0)."""
+    common row set (rows whose cast gradient vanishes count with r_post 0);
+    median r_post,own over those of its rows whose cast gradient does not
+    vanish."""
     keep = common_rows(stats_by_mode, min_row)
     out = {}
     for name, st in stats_by_mode.items():
@@ -41,6 +44,10 @@ def row_residuals(stats_by_mode, min_row=MIN_ROW):
         out[name] = dict(r_pre_median=float(np.median(np.abs(s) / ell)),
                          r_post_median=float(np.median(np.abs(cast) / ell)),
                          kappa_mean=float(np.mean((cast - s) / ell)))
+        if st.shape[-1] > 4:
+            own = st[..., 4][keep]
+            nz = own > 0
+            out[name]["r_post_own_median"] = float(np.median(np.abs(cast[nz]) / own[nz])) if nz.any() else 0.0
     out["rows"] = int(keep.sum())
     return out
 

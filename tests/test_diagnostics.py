@@ -7,7 +7,7 @@ from paper_2609_37852_amd import diagnostics as dg
 def _stats(B=1, H=2, N=128, seed=0):
     rng = np.random.default_rng(seed)
     ell = rng.uniform(1.0, 2.0, (B, H, N))
-    st = np.zeros((B, H, N, 4))
+    st = np.zeros((B, H, N, 5))
     st[..., 1] = ell
     return st, ell
 
@@ -31,6 +31,13 @@ def test_row_residuals_known_values():
     assert np.isclose(r["m"]["r_pre_median"], 0.25)
     assert np.isclose(r["m"]["kappa_mean"], 0.125)
     # r_post: |+-l/4 + l/8| / l is 3/8 or 1/8 in equal numbers; the median of the 128 values
+    assert np.isclose(r["m"]["r_post_median"], 0.25)
+    # own denominator: with sum |dS'| = l / 2 the same rows give 3/4 and 1/4; rows with a
+    # vanishing cast (sum |dS'| = 0) are left out of it only
+    st[..., 4] = 0.5 * ell
+    st[0, 0, 64:80, 4] = 0.0
+    r = dg.row_residuals({"m": st})
+    assert np.isclose(r["m"]["r_post_own_median"], 0.5)
     assert np.isclose(r["m"]["r_post_median"], 0.25)
 
 
