@@ -46,7 +46,8 @@ __device__ __forceinline__ void dma4(const Buf& b, uint32_t off, lds8* lds_base)
 }
 // The same with a wave-uniform part of the offset in a scalar register
 // (address = base + soff + voff): the per-lane part can stay in a long-lived
-// register while the head and tile offsets change.
+// register while the head and tile offsets change.  The buffer's range check
+// covers voff only, so callers keep soff + voff inside the buffer themselves.
 __device__ __forceinline__ void dma16s(const Buf& b, uint32_t voff, uint32_t soff, lds8* lds_base) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(b.r, (__attribute__((address_space(3))) void*)lds_base, 16, (int)voff,
                                            (int)soff, 0, 0);
