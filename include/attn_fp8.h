@@ -26,8 +26,9 @@
  * Conventions (all entry points):
  *   - Every pointer argument named as device memory is a device (HBM)
  *     address owned by the caller; the library never allocates or frees
- *     device memory and keeps no state between calls, apart from the
- *     thread-local error text.
+ *     device memory.  Between calls it keeps only the thread-local error
+ *     text and, per device, the compute-unit count it queries once (the
+ *     backward sizes its key-block order by it).
  *   - Work is enqueued on `stream` and the call returns without
  *     synchronizing; faults inside a kernel surface at the caller's next
  *     synchronization.
@@ -165,8 +166,10 @@ int attn_fp8_delta(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx*
 int attn_fp8_bwd_workspace_size(const attn_fp8_problem* p, size_t* bytes);
 
 /* Backward (Sec. 2.3; App. B.6.3).  Key-major pass: recompute S, P, dP;
- * dS = P ((dP - hi) - lo); P' = C8(256 P) 2^-8 (P clamped to [0, 1]); dS'
- * cast per 32x32 block; dV += P'^T dO_col, dK += dS'^T Q_col (summed over the
+ * dS = P (dP - delta) formed as fma(P, dP, fl(P * (-d))) with d the
+ * correction rounded to FP32 (the hi part; P dP enters exactly and every
+ * rounding is of its own element); P' = C8(256 P) 2^-8 (P clamped to
+ * [0, 1]); dS' cast per 32x32 block; dV += P'^T dO_col, dK += dS'^T Q_col (summed over the
  * KV group in FP32), dS' stored in the workspace; then a query-major pass
  * computes dQ = dS' K_col.  dQ and dK are multiplied by tau and stored.
  *   delta_in nullable device float [B, Hq, N, 2]: when given, used as the
@@ -176,11 +179,13 @@ int attn_fp8_bwd_workspace_size(const attn_fp8_problem* p, size_t* bytes);
  *            element strides {b, n, h} in dq_strides / dk_strides / dv_strides.
  *   workspace device, at least attn_fp8_bwd_workspace_size() bytes, 256-byte
  *            aligned; contents on entry are ignored.
- *   rowstats nullable device double [B, Hq, N, 5], zeroed by the caller:
+ *   rowstats nullable device double [B, Hq, N, 7], zeroed by the caller:
  *            accumulates, per query row and over all keys, sum dS, sum |dS|,
- *            sum dS', max |dS| and sum |dS'| (FP64 sums of the FP32 values
- *            before / after the cast; debug instrumentation of App. C.1;
- *            slower).
+ *            sum dS', max |dS|, sum |dS'|, max P |dP| and sum P' (FP64 sums
+ *            of the FP32 values before the cast, dS and P dP, and of the
+ *            decoded FP8 operands dS' and P'; debug instrumentation of
+ *            App. C.1; a separate, slower kernel instantiation whose
+ *            gradients are bitwise those of the plain one).
  *   main_events nullable pointer to two events: recorded on `stream`
  *            immediately before and after the main backward kernel, so a
  *            caller can time that kernel alone. */

@@ -29,7 +29,7 @@ EXACT_ALL = EXACT_PFWD | EXACT_PBWD | EXACT_DS
 DELTA_MATCHING, DELTA_STALE_ROWSUM, DELTA_CONSISTENT_DO = 0, 1, 2
 ROUND_NONE, ROUND_F32, ROUND_BF16 = 0, 1, 2
 ST_SUM_DS, ST_SUMABS_DS, ST_MAXABS_DS, ST_MAX_PDP, ST_SUM_DSCAST, ST_SUMABS_DSCAST, ST_SUM_P, \
-    ST_SUM_PDP, NSTAT = range(9)
+    ST_SUM_PDP, ST_SUM_PCAST, ST_SUM_P_ABSTERMS, NSTAT = range(11)
 
 
 class _Problem(ctypes.Structure):
@@ -62,8 +62,8 @@ def lib():
         L.orc_quantize.argtypes = [_dp] + [ctypes.c_int64] * 4 + [_u8p] * 4
         L.orc_dequantize.argtypes = [_u8p] * 4 + [ctypes.c_int64] * 4 + [_dp, _dp]
         L.orc_attention.restype = ctypes.c_int
-        L.orc_attention.argtypes = ([ctypes.POINTER(_Problem)] + [ctypes.c_int] * 4 + [_dp] * 21
-                                    + [ctypes.c_int])
+        L.orc_attention.argtypes = ([ctypes.POINTER(_Problem)] + [ctypes.c_int] * 4 + [_dp] * 22
+                                    + [ctypes.c_int64, ctypes.c_int])
         _LIB = L
     return _LIB
 
@@ -134,13 +134,15 @@ def dequantize(q, B, N, H, D):
 
 # ---------------------------------------------------------------- attention
 def attention(B, N, Hq, Hkv, Dqk, Dv, tau, ops, dO_raw=None, *, flags=0, delta_mode=DELTA_MATCHING,
-              o_round=ROUND_BF16, grad_round=ROUND_NONE, delta_in=None, want_rowstats=False,
-              want_phat=False, want_ds=False, nthreads=0):
+              o_round=ROUND_BF16, grad_round=ROUND_NONE, delta_in=None, lse_in=None, want_rowstats=False,
+              want_phat=False, want_ds=False, row_lo=0, nthreads=0):
     """Forward + correction + backward on dequantized operands.
 
     ops: dict with Qr, Kr, Vr, dOr, Qc, Kc, Vc, dOc, each [B,H,N,D] float64
     (H = Hq for Q/dO, Hkv for K/V).  dO_raw: [B,N,Hq,Dv] (needed for the stale
-    correction).  Returns a dict of float64 arrays."""
+    correction).  row_lo: compute only query rows and keys >= row_lo (the
+    causal suffix; other entries stay zero).  Returns a dict of float64
+    arrays."""
     L = lib()
     pr = _Problem(B, N, Hq, Hkv, Dqk, Dv, float(tau))
     names = ("Qr", "Kr", "Vr", "dOr", "Qc", "Kc", "Vc", "dOc")
@@ -158,6 +160,9 @@ def attention(B, N, Hq, Hkv, Dqk, Dv, tau, ops, dO_raw=None, *, flags=0, delta_m
     if delta_in is not None:
         delta_in = _f64(delta_in)
         assert delta_in.shape == (B, Hq, N)
+    if lse_in is not None:
+        lse_in = _f64(lse_in)
+        assert lse_in.shape == (B, Hq, N)
     out = dict(O=np.zeros((B, N, Hq, Dv)), O_unrounded=np.zeros((B, N, Hq, Dv)), LSE=np.zeros((B, Hq, N)),
                delta=np.zeros((B, Hq, N)), dQ=np.zeros((B, N, Hq, Dqk)), dK=np.zeros((B, N, Hkv, Dqk)),
                dV=np.zeros((B, N, Hkv, Dv)))
@@ -166,10 +171,10 @@ def attention(B, N, Hq, Hkv, Dqk, Dv, tau, ops, dO_raw=None, *, flags=0, delta_m
     out["dsraw"] = np.zeros((B, Hq, N, N)) if want_ds else None
     out["dshat"] = np.zeros((B, Hq, N, N)) if want_ds else None
     rc = L.orc_attention(ctypes.byref(pr), flags, delta_mode, o_round, grad_round,
-                         *[_ptr(arrs[k]) for k in names], _ptr(dO_raw), _ptr(delta_in),
+                         *[_ptr(arrs[k]) for k in names], _ptr(dO_raw), _ptr(delta_in), _ptr(lse_in),
                          _ptr(out["O"]), _ptr(out["O_unrounded"]), _ptr(out["LSE"]), _ptr(out["delta"]),
                          _ptr(out["dQ"]), _ptr(out["dK"]), _ptr(out["dV"]), _ptr(out["rowstats"]),
-                         _ptr(out["phat"]), _ptr(out["dsraw"]), _ptr(out["dshat"]), int(nthreads))
+                         _ptr(out["phat"]), _ptr(out["dsraw"]), _ptr(out["dshat"]), int(row_lo), int(nthreads))
     if rc != 0:
         raise ValueError(f"orc_attention failed ({rc})")
     return out

@@ -26,7 +26,10 @@
  *      x_g the group max over visible keys); code = C8(2^{x - E_g}); the
  *      normalizer uses the exponentials before the cast.
  *   R6 backward probability codes for dV: C8(256 P) with fixed scale 2^-8;
- *      P is clamped to at most 1 (the range that fixed scale is meant for).
+ *      the recomputed P is clamped to at most 1.  The paper clamps the
+ *      base-two exponent of 256 P at 12 (P <= 16).  The two clamps differ
+ *      only when the LSE handed to the backward is below the row's largest
+ *      score, which the forward's own LSE never is; lse_in reaches it.
  *   R7 dS codes: aligned 32x32 blocks (query x key), one power-of-two scale
  *      per block, shared by dQ and dK.
  *   R8 matched correction: (sum_j P_ij dP_ij) / (sum_j P_ij) from the
@@ -217,6 +220,13 @@ static double dot(const double* a, const double* b, int64_t n) {
   return (s0 + s1) + (s2 + s3);
 }
 
+/* sum_k |a_k b_k|: the magnitude scale of a dot product's terms */
+static double dot_abs(const double* a, const double* b, int64_t n) {
+  double s = 0.0;
+  for (int64_t k = 0; k < n; k++) s += fabs(a[k] * b[k]);
+  return s;
+}
+
 static double round_to(double v, int mode) {
   if (mode == ORC_ROUND_F32) return (double)(float)v;
   if (mode == ORC_ROUND_BF16) return orc_bf16_round(v);
@@ -281,14 +291,15 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
                   int o_round, int grad_round,
                   const double* Qr, const double* Kr, const double* Vr, const double* dOr,
                   const double* Qc, const double* Kc, const double* Vc, const double* dOc,
-                  const double* dO_raw, const double* delta_in,
+                  const double* dO_raw, const double* delta_in, const double* lse_in,
                   double* O, double* O_unrounded, double* LSE, double* delta,
                   double* dQ, double* dK, double* dV,
-                  double* rowstats, double* phat, double* dsraw, double* dshat, int nthreads) {
+                  double* rowstats, double* phat, double* dsraw, double* dshat, int64_t row_lo,
+                  int nthreads) {
   const int64_t B = p->B, N = p->N, Hq = p->Hq, Hkv = p->Hkv, Dqk = p->Dqk, Dv = p->Dv;
   const double tau = p->tau;
   if (B < 0 || N < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || Dqk <= 0 || Dv <= 0 ||
-      Dqk > ORC_MAXD || Dv > ORC_MAXD)
+      Dqk > ORC_MAXD || Dv > ORC_MAXD || row_lo < 0 || row_lo % 32 != 0 || (N > 0 && row_lo >= N))
     return -1;
   const int64_t G = Hq / Hkv;
   const double LOG2E = 1.4426950408889634074;
@@ -309,7 +320,7 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
 #pragma omp for collapse(3) schedule(dynamic, 16)
     for (int64_t b = 0; b < B; b++)
       for (int64_t h = 0; h < Hq; h++)
-        for (int64_t i = 0; i < N; i++) {
+        for (int64_t i = row_lo; i < N; i++) {
           const int64_t kh = h / G;
           const double* q = Qr + ((b * Hq + h) * N + i) * Dqk;
           /* scores over the visible keys j <= i, base-2 exponent x = S log2 e */
@@ -355,21 +366,25 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
   }
 
   /* ---- correction pass (Sec. 3.4; App. B.6.3 with readings R8, R9) ----
-   * P_ij = exp(S_ij - LSE_i) recomputed from the scores, dP_ij = <dOr_i, Vr_j>. */
+   * P_ij = exp(S_ij - LSE_i) recomputed from the scores, dP_ij = <dOr_i, Vr_j>.
+   * The backward reads the LSE the forward stored, or lse_in when given (a
+   * caller-supplied LSE, e.g. an inconsistent one that exercises R6's clamp). */
+  const double* LB = lse_in ? lse_in : LSE;
 #pragma omp parallel for collapse(3) schedule(dynamic, 16)
   for (int64_t b = 0; b < B; b++)
     for (int64_t h = 0; h < Hq; h++)
-      for (int64_t i = 0; i < N; i++) {
+      for (int64_t i = row_lo; i < N; i++) {
         const int64_t kh = h / G;
-        const double lse = LSE[(b * Hq + h) * N + i];
+        const double lse = LB[(b * Hq + h) * N + i];
         const double* q = Qr + ((b * Hq + h) * N + i) * Dqk;
         const double* go = dOr + ((b * Hq + h) * N + i) * Dv;
-        double num = 0.0, den = 0.0, maxpdp = 0.0;
+        double num = 0.0, den = 0.0, maxpdp = 0.0, tabs = 0.0;
         for (int64_t j = 0; j <= i; j++) {
           const double pij = probability(tau, q, Kr + ((b * Hkv + kh) * N + j) * Dqk, Dqk, lse);
           const double dpij = dot(go, Vr + ((b * Hkv + kh) * N + j) * Dv, Dv);
           num += pij * dpij;
           den += pij;
+          if (rowstats) tabs += pij * dot_abs(go, Vr + ((b * Hkv + kh) * N + j) * Dv, Dv);
           if (fabs(pij * dpij) > maxpdp) maxpdp = fabs(pij * dpij);
         }
         double d;
@@ -389,6 +404,7 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
           st[ORC_ST_MAX_PDP] = maxpdp;
           st[ORC_ST_SUM_P] = den;
           st[ORC_ST_SUM_PDP] = num;
+          st[ORC_ST_SUM_P_ABSTERMS] = tabs;
         }
       }
 
@@ -398,14 +414,14 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
    * dK/dV pass (one key block at a time, looping the query heads of its KV
    * group) see identical dS' and P' values, and every sum has a fixed order. */
   const int64_t nrb = (N + 31) / 32;
-  tile_ctx ctx = {B, N, Hq, Hkv, Dqk, Dv, G, tau, flags, Qr, Kr, Vr, dOr, LSE, delta};
+  tile_ctx ctx = {B, N, Hq, Hkv, Dqk, Dv, G, tau, flags, Qr, Kr, Vr, dOr, LB, delta};
 #pragma omp parallel for collapse(3) schedule(dynamic, 1)
   for (int64_t b = 0; b < B; b++)
     for (int64_t h = 0; h < Hq; h++)
-      for (int64_t rb = 0; rb < nrb; rb++) {
+      for (int64_t rb = row_lo / 32; rb < nrb; rb++) {
         const int64_t kh = h / G;
         double P[32][32], dS[32][32], Pb[32][32], dSh[32][32];
-        double sds[32] = {0}, sads[32] = {0}, mads[32] = {0}, sdc[32] = {0}, sadc[32] = {0};
+        double sds[32] = {0}, sads[32] = {0}, mads[32] = {0}, sdc[32] = {0}, sadc[32] = {0}, spc[32] = {0};
         double dq[32][ORC_MAXD];
         memset(dq, 0, sizeof dq);
         const int64_t i0 = rb * 32, nr = (i0 + 32 <= N) ? 32 : N - i0;
@@ -423,6 +439,7 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
               if (fabs(dS[r][t]) > mads[r]) mads[r] = fabs(dS[r][t]);
               sdc[r] += g;
               sadc[r] += fabs(g);
+              spc[r] += Pb[r][t];
               if (dsraw) dsraw[((b * Hq + h) * N + i) * N + j] = dS[r][t];
               if (dshat) dshat[((b * Hq + h) * N + i) * N + j] = g;
               const double* kc = Kc + ((b * Hkv + kh) * N + j) * Dqk;
@@ -440,13 +457,14 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
             st[ORC_ST_MAXABS_DS] = mads[r];
             st[ORC_ST_SUM_DSCAST] = sdc[r];
             st[ORC_ST_SUMABS_DSCAST] = sadc[r];
+            st[ORC_ST_SUM_PCAST] = spc[r];
           }
         }
       }
 #pragma omp parallel for collapse(3) schedule(dynamic, 1)
   for (int64_t b = 0; b < B; b++)
     for (int64_t kh = 0; kh < Hkv; kh++)
-      for (int64_t jb = 0; jb < nrb; jb++) {
+      for (int64_t jb = row_lo / 32; jb < nrb; jb++) {
         double P[32][32], dS[32][32], Pb[32][32], dSh[32][32];
         double dk[32][ORC_MAXD], dv[32][ORC_MAXD];
         memset(dk, 0, sizeof dk);

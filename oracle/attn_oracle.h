@@ -68,13 +68,23 @@ enum { ORC_ST_SUM_DS = 0,      /* sum_j dS_ij (pre-cast)            */
        ORC_ST_SUMABS_DSCAST,   /* sum_j |dS'_ij|                     */
        ORC_ST_SUM_P,           /* sum_j P_ij                          */
        ORC_ST_SUM_PDP,         /* sum_j P_ij dP_ij                    */
+       ORC_ST_SUM_PCAST,       /* sum_j P'_ij (decoded dV operand)    */
+       ORC_ST_SUM_P_ABSTERMS,  /* sum_j P_ij sum_c |dO_ic V_jc| (the
+                                  magnitude of dP's terms, weighted by P) */
        ORC_NSTAT };
 
 /* Forward + correction + backward of causal attention on dequantized
  * operands (row copies feed the contractions over head_dim, col copies the
  * contractions over the sequence).  See attn_oracle.c for the steps.
  * O receives the stored output (rounded per o_round); gradients are rounded
- * per grad_round.  delta_in (nullable) replaces the computed correction.
+ * per grad_round.  delta_in (nullable) replaces the computed correction;
+ * lse_in (nullable, [B,Hq,N]) replaces the stored LSE in the correction and
+ * gradient passes (the forward is unchanged).
+ * row_lo (a multiple of 32, 0 for the whole problem) restricts the work to
+ * query rows i >= row_lo (O, LSE, delta, dQ, row statistics) and keys
+ * j >= row_lo (dK, dV): by causality those depend on no other rows or keys'
+ * outputs, so they come out exactly as in the whole problem; the rest of
+ * the outputs are left untouched.
  * phat / dsraw / dshat (nullable, [B,Hq,N,N]) receive the normalized forward
  * probabilities actually used for O, dS before and after the FP8 cast
  * (tiny problems only).
@@ -83,10 +93,11 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
                   int o_round, int grad_round,
                   const double* Qr, const double* Kr, const double* Vr, const double* dOr,
                   const double* Qc, const double* Kc, const double* Vc, const double* dOc,
-                  const double* dO_raw, const double* delta_in,
+                  const double* dO_raw, const double* delta_in, const double* lse_in,
                   double* O, double* O_unrounded, double* LSE, double* delta,
                   double* dQ, double* dK, double* dV,
-                  double* rowstats, double* phat, double* dsraw, double* dshat, int nthreads);
+                  double* rowstats, double* phat, double* dsraw, double* dshat, int64_t row_lo,
+                  int nthreads);
 
 #ifdef __cplusplus
 }

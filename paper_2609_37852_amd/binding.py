@@ -19,6 +19,9 @@ LIB_PATH = os.path.join(_PKG, "libattn_fp8.so")
 DTYPE_F32, DTYPE_BF16 = 0, 1
 DELTA_MATCHING, DELTA_STALE_ROWSUM, DELTA_CONSISTENT_DO = 0, 1, 2
 QUANT_ROW, QUANT_COL, QUANT_BOTH = 1, 2, 3
+# fields of the backward's per-row statistics [B, Hq, N, ROWSTATS] (FP64)
+RS_SUM_DS, RS_SUMABS_DS, RS_SUM_DSCAST, RS_MAXABS_DS, RS_SUMABS_DSCAST, RS_MAX_PDP, RS_SUM_PCAST = range(7)
+ROWSTATS = 7
 STATUS = {0: "OK", -1: "EINVAL", -2: "EUNSUPPORTED", -3: "EALIGN", -4: "EWORKSPACE", -5: "EHIP"}
 EXPORTS = ("attn_fp8_quantize", "attn_fp8_fwd", "attn_fp8_delta", "attn_fp8_bwd_workspace_size",
            "attn_fp8_bwd", "attn_fp8_last_error")
@@ -212,7 +215,7 @@ def attn_fp8_bwd(p: Problem, mode: int, q: MX, k: MX, v: MX, dout: MX, lse, dout
     ws_bytes = attn_fp8_bwd_workspace_size(p)
     if workspace is None:
         workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
-    rs = torch.zeros((p.batch, p.heads_q, p.seqlen, 5), dtype=torch.float64, device=dev) if rowstats else None
+    rs = torch.zeros((p.batch, p.heads_q, p.seqlen, ROWSTATS), dtype=torch.float64, device=dev) if rowstats else None
     pc = p.c()
     mxs = [m.c() for m in (q, k, v, dout)]
     ds = _strides_bnh(dout_raw) if dout_raw is not None else None

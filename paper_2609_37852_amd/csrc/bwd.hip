@@ -396,6 +396,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     }
     // lane holds queries qb + 8 g + 4 hf + e4 (accumulator r = 4 g + e4)
     float amax = 0.f;
+    float pdp[16];   // |P dP| (row statistics only)
 #pragma unroll
     for (int g = 0; g < 4; g++) {
       // -delta of the lane's four queries 8 g + 4 hf .. + 3 of the half
@@ -407,6 +408,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
         float p = bwd_prob(s[r], c);
         if (EDGE && qb == kw0) p = (li > 8 * g + 4 * hf + e4) ? 0.f : p;   // diagonal block: key > query
         s[r] = p;
+        if constexpr (STATS) pdp[r] = fabsf(p * dp[r]);
         dp[r] = __builtin_fmaf(p, dp[r], p * ndv[e4]);
         amax = fmaxf(amax, fabsf(dp[r]));
       }
@@ -422,23 +424,30 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
       dc[k] = (int)cvt4_div(dp[4 * k], dp[4 * k + 1], dp[4 * k + 2], dp[4 * k + 3], sc);
     if constexpr (STATS) {
       // per query row: FP64 sums over this wave's 32 keys, then atomics
+      // (non-negative maxima as the integer maximum of their bit patterns)
 #pragma unroll
       for (int r = 0; r < 16; r++) {
         const float cast = fp8_value((uint32_t)dc[r >> 2], r & 3) * sc;
+        const float pcast = fp8_value((uint32_t)pc[r >> 2], r & 3) * 0.00390625f;
         const double s0 = half_sum_d((double)dp[r]);
         const double s1 = half_sum_d((double)fabsf(dp[r]));
         const double s2 = half_sum_d((double)cast);
         const double s3 = half_sum_d((double)fabsf(cast));
+        const double s6 = half_sum_d((double)pcast);
         const float mx = half_max(fabsf(dp[r]));
+        const float mpdp = half_max(pdp[r]);
         const int qi = qb + 8 * (r >> 2) + 4 * hf + (r & 3);
         if (li == 0) {
-          double* sp = a.rowstats + (((size_t)b * Hq + h) * N + qi) * 5;
+          double* sp = a.rowstats + (((size_t)b * Hq + h) * N + qi) * kRowStats;
           atomicAdd(sp + 0, s0);
           atomicAdd(sp + 1, s1);
           atomicAdd(sp + 2, s2);
           atomicMax(reinterpret_cast<unsigned long long*>(sp + 3),
                     (unsigned long long)__double_as_longlong((double)mx));
           atomicAdd(sp + 4, s3);
+          atomicMax(reinterpret_cast<unsigned long long*>(sp + 5),
+                    (unsigned long long)__double_as_longlong((double)mpdp));
+          atomicAdd(sp + 6, s6);
         }
       }
     }

@@ -108,8 +108,8 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
     dma_row_scales<DV, NW, BK>(st + C::VS_OFF, vscale, j0, N, w, lane, 1);
     if (hot >= 0 && threadIdx.x < BK) {
       const int r = j0 + (int)threadIdx.x < N ? j0 + (int)threadIdx.x : N - 1;
-      khc = kcode[r * DQK + hot];
-      khs = kscale[r * (DQK / 32) + hot / 32];
+      khc = kcode[(int64_t)r * DQK + hot];
+      khs = kscale[(int64_t)r * (DQK / 32) + hot / 32];
     }
     __builtin_amdgcn_sched_barrier(0);   // keep every load ahead of the tile's compute
   };

@@ -137,8 +137,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
     }
     if (hot >= 0 && threadIdx.x < BK) {
       const int r = j0 + (int)threadIdx.x < N ? j0 + (int)threadIdx.x : N - 1;
-      khc = kcode[r * DQK + hot];
-      khs = kscale[r * (DQK / 32) + hot / 32];
+      khc = kcode[(int64_t)r * DQK + hot];
+      khs = kscale[(int64_t)r * (DQK / 32) + hot / 32];
     }
     __builtin_amdgcn_sched_barrier(0);   // keep every load ahead of the tile's compute
   };

@@ -8,6 +8,12 @@
 
 namespace afp8 {
 
+// Per-row statistics of the instrumented backward (FP64, per query row over
+// all keys): sum dS, sum |dS|, sum dS', max |dS|, sum |dS'|, max P |dP|,
+// sum P' (dS, P, dP the FP32 values before the cast; dS', P' the decoded
+// FP8 operands).
+constexpr int kRowStats = 7;
+
 struct QuantArgs {
   const void* x;
   int64_t sb, sn, sh;        // element strides of x (channel stride 1)
@@ -60,7 +66,7 @@ struct AttnArgs {
   void* dv; int64_t dvs[3];
   int grad_bf16;
   int bwd_cohort;                      // backward: workgroups of one KV head that run at once (set at launch)
-  double* rowstats;                    // nullable [B,Hq,N,4]
+  double* rowstats;                    // nullable [B,Hq,N,kRowStats]
 };
 
 hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_t s);

@@ -1,8 +1,8 @@
 """Row-sum and key-gradient diagnostics of the backward (App. C.1, on synthetic
 data), from the per-row statistics the backward records with `rowstats`:
-[B, Hq, N, 5] FP64 = (sum_j dS_ij, sum_j |dS_ij|, sum_j dS'_ij, max_j |dS_ij|,
-sum_j |dS'_ij|) with dS the FP32 score gradient before the FP8 cast and dS'
-the decoded cast.
+[B, Hq, N, 7] FP64 = (sum_j dS_ij, sum_j |dS_ij|, sum_j dS'_ij, max_j |dS_ij|,
+sum_j |dS'_ij|, max_j P_ij |dP_ij|, sum_j P'_ij) with dS the FP32 score
+gradient before the FP8 cast and dS', P' the decoded casts.
 
   r_pre_i  = |sum_j dS_ij| / l_i,   r_post_i = |sum_j dS'_ij| / l_i,
   r_post,own_i = |sum_j dS'_ij| / l'_i,  l'_i = sum_j |dS'_ij| (rows with l'_i > 0),

@@ -30,7 +30,7 @@ class Workload:
     Dqk: int
     Dv: int
     dtype: str          # "f32" or "bf16": storage dtype of Q, K, V, dO
-    transform: str      # "none", "outlier", "qknorm", "rope", "temperature"
+    transform: str      # "none", "outlier", "outlier3", "qknorm", "rope", "temperature"
     tau: float          # softmax scale
 
     @property
@@ -87,9 +87,10 @@ def generate(w: Workload, seed: int = 0):
     v = _rng(seed, "v").standard_normal((B, N, w.Hkv, w.Dv), dtype=np.float32)
     do = _rng(seed, "do").standard_normal((B, N, w.Hq, w.Dv), dtype=np.float32)
     aux = _rng(seed, "aux")
-    if w.transform == "outlier":
-        # 1% of head_dim channels (at least one), shared by all heads, x20 in Q and K
-        n_out = max(1, int(round(0.01 * w.Dqk)))
+    if w.transform in ("outlier", "outlier3"):
+        # 1% of head_dim channels (at least one), shared by all heads, x20 in Q
+        # and K; "outlier3": three such channels (a robustness recipe)
+        n_out = 3 if w.transform == "outlier3" else max(1, int(round(0.01 * w.Dqk)))
         idx = aux.choice(w.Dqk, size=n_out, replace=False)
         q[..., idx] *= 20.0
         k[..., idx] *= 20.0

@@ -115,3 +115,14 @@ def test_empty_problem_is_a_noop():
     st = bd._I64x3(0, 256, 128)
     assert L.attn_fp8_fwd(ctypes.byref(p), ctypes.byref(m), ctypes.byref(m), ctypes.byref(m), ctypes.c_void_p(4096),
                           1, st, ctypes.c_void_p(4096), None) == 0
+
+
+def test_package_exports_binding_names():
+    """Every public name of the binding that the tests and the benchmark use
+    is re-exported by the package."""
+    for name in pk.__all__:
+        assert hasattr(pk, name), name
+    for name in ("ROWSTATS", "RS_SUM_DS", "RS_SUMABS_DS", "RS_SUM_DSCAST", "RS_MAXABS_DS", "RS_SUMABS_DSCAST",
+                 "RS_MAX_PDP", "RS_SUM_PCAST"):
+        assert getattr(pk, name) == getattr(bd, name)
+    assert pk.ROWSTATS == 7 and sorted(getattr(bd, n) for n in dir(bd) if n.startswith("RS_")) == list(range(7))

@@ -1,6 +1,10 @@
 """GPU forward, correction and backward against the same-quantization oracle
-(relative Frobenius error <= 2e-2), the zero-row-sum invariant on the GPU's own
-pre-cast dS, and the structural identities of App. C.1 / C.3.1."""
+(relative Frobenius error <= 2e-2 per tensor and for the median 32-row
+block, <= 2^-3 for every block: one E4M3 step of a dominant element), the
+zero-row-sum invariant on the GPU's own pre-cast dS, and the structural
+identities of App. C.1 / App. C.4.1.  Every backward case runs the plain
+kernel (the one the benchmark times) against the oracle and the
+instrumented kernel, which must return bitwise the same gradients."""
 import numpy as np
 import pytest
 import torch
@@ -8,7 +12,8 @@ import torch
 import oracle as orc
 import paper_2609_37852_amd as pk
 from paper_2609_37852_amd import synth
-from _helpers import REL_TOL, INV_TOL, invariant_report, rel_err, run_gpu, run_oracle, say
+from _helpers import (REL_TOL, block_errors, check_blocks, check_row_stat_fields, invariant_report, rel_err, run_gpu,
+                      run_oracle, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -22,10 +27,24 @@ CASES = [
     ("gqa_d128_64k_nope", dict(B=1, N=256, Hq=4, Hkv=2)),
 ]
 
+# Share of rows the invariant must grade (reading R12).  With the x20
+# outlier channel in Q and K the score of that channel alone has a standard
+# deviation near 35 (400 tau), so most rows are near one-hot: their dS is
+# below FP32 resolution of their largest P dP and they fall under the cond
+# filter by construction (about 60 % of rows at N = 320).  Elsewhere at least
+# half the rows are graded.
+MIN_GRADED = {"outlier": 0.25}
+
 
 def _workload(name, kw):
     w = synth.WORKLOADS[name]
     return synth.with_shape(w, **kw) if kw else w
+
+
+def _compare(g, o, kinds=("O", "dQ", "dK", "dV")):
+    errs = {k: rel_err(g[k], o[k]) for k in kinds}
+    blk = {k: block_errors(g[k], o[k]) for k in kinds}
+    return errs, blk
 
 
 @pytest.mark.parametrize("name,kw", CASES, ids=[f"{n}-{'-'.join(f'{k}{v}' for k, v in kw.items()) or 'full'}"
@@ -42,21 +61,72 @@ def test_parity(name, kw, mode):
     for n in ("Q", "K", "V", "dO"):
         for f in ("code_row", "scale_row", "code_col", "scale_col"):
             assert np.array_equal(g["mx"][n][f], o["quant"][n][f]), (n, f)
-    errs = {k: rel_err(g[k], o[k]) for k in ("O", "dQ", "dK", "dV")}
+    errs, blk = _compare(g, o)
     errs["LSE"] = float(np.max(np.abs(g["LSE"] - o["LSE"])))
     errs["delta"] = rel_err(g["delta"][..., 0] + g["delta"][..., 1], o["delta"])
     say("  errors", {k: f"{v:.2e}" for k, v in errs.items()})
+    say("  32-row blocks (worst, at, median)", {k: (f"{v[0]:.2e}", v[1], f"{v[2]:.1e}") for k, v in blk.items()})
     for k in ("O", "dQ", "dK", "dV"):
         assert errs[k] <= REL_TOL, (k, errs[k])
+    check_blocks(blk)
     assert errs["LSE"] < 1e-3
     # the saved-output corrections read the bf16-rounded O, whose rounding flips move them
     assert errs["delta"] < (1e-3 if mode == pk.DELTA_MATCHING else 1e-2)
+    fields = check_row_stat_fields(g["rowstats"], o["rowstats"])
+    say("  row-stat fields vs oracle (median rel. diff)", fields)
+    assert fields["max_pdp"] < 1e-3 and fields["sum_pcast"] < 1e-3, fields
     if mode == pk.DELTA_MATCHING:
-        rep = invariant_report(g["rowstats"], o["rowstats"])
+        rep = invariant_report(g["rowstats"])
         say("  invariant", rep)
         assert rep["violations"] == 0, rep
-        # near-one-hot rows (outlier workload) are excluded by the cond filter and reported
-        assert rep["graded"] >= 0.25 * (rep["graded"] + rep["excluded"])
+        need = MIN_GRADED.get(w.transform, 0.5)
+        assert rep["share"] >= need, (rep["share"], need)
+
+
+def test_injected_lse_reaches_the_probability_clamp():
+    """Reading R6: the backward clamps the recomputed P at 1.  With an LSE
+    0.5 below the forward's, P reaches e^0.5 before the clamp; the GPU and
+    the oracle (given the same shift of its own LSE) clamp alike, so the
+    correction, gradients and sum_j P'_ij still agree."""
+    w = _workload("tiny_mha_128", dict(N=160))
+    d = synth.generate(w, seed=9)
+    g = run_gpu(w, d, lse_shift=-0.5)
+    base = run_oracle(w, d)
+    o = run_oracle(w, d, lse_in=base["LSE"] - 0.5)
+    errs, blk = _compare(g, o, ("dQ", "dK", "dV"))
+    errs["delta"] = rel_err(g["delta"][..., 0] + g["delta"][..., 1], o["delta"])
+    fields = check_row_stat_fields(g["rowstats"], o["rowstats"])
+    say("  errors", errs, "fields", fields)
+    # the shift inflates every row's probabilities by e^0.5 (sum_j P'_ij
+    # above 1); rows with a dominant key (row 0 at least) reach the clamp
+    sp = o["rowstats"][..., orc.ST_SUM_PCAST]
+    assert np.max(sp) > 1.0
+    for k in ("dQ", "dK", "dV"):
+        assert errs[k] <= REL_TOL, (k, errs[k])
+    check_blocks(blk)
+    assert errs["delta"] < 1e-3 and fields["sum_pcast"] < 1e-3
+
+
+@pytest.mark.xfail(strict=True, reason="one isolated score channel: with three x20 channels the other two stay in "
+                                       "the MFMA's grouped accumulation (measured O 2.1e-2, LSE 6.1e-2)")
+def test_three_outlier_channels():
+    """Robustness of the isolated score channel: three x20 channels in Q and K
+    (the kernels take one channel out of the MFMA; the other two stay in its
+    grouped accumulation)."""
+    w = _workload("gqa_d128_8k", dict(B=1, N=320, Hq=4, Hkv=1, transform="outlier3"))
+    d = synth.generate(w, seed=1)
+    g = run_gpu(w, d)
+    o = run_oracle(w, d)
+    errs, blk = _compare(g, o)
+    errs["LSE"] = float(np.max(np.abs(g["LSE"] - o["LSE"])))
+    say("  errors", {k: f"{v:.2e}" for k, v in errs.items()})
+    say("  32-row blocks (worst, at, median)", {k: (f"{v[0]:.2e}", v[1], f"{v[2]:.1e}") for k, v in blk.items()})
+    rep = invariant_report(g["rowstats"])
+    say("  invariant", rep)
+    for k in ("O", "dQ", "dK", "dV"):
+        assert errs[k] <= REL_TOL, (k, errs[k])
+    check_blocks(blk)
+    assert rep["violations"] == 0
 
 
 def test_key_block_order_with_partial_cohort():
@@ -97,7 +167,7 @@ def test_isolated_channel_on_outlier_workload():
 
 
 def test_delta_mode_changes_only_dq_dk():
-    """App. C.3.1: changing only the correction leaves O and dV bitwise
+    """App. C.4.1: changing only the correction leaves O and dV bitwise
     unchanged and changes dQ and dK."""
     w = _workload("gqa_d128_8k", dict(B=1, N=256, Hq=2, Hkv=1))
     d = synth.generate(w, seed=3)
@@ -132,7 +202,6 @@ def test_delta_injection_affine():
     w = _workload("tiny_mha_128", dict(N=192, Hq=2, Hkv=1))
     d = synth.generate(w, seed=4)
     base = run_gpu(w, d)
-    orc_rs = run_oracle(w, d)["rowstats"]
     z = torch.zeros((w.B, w.Hq, w.N, 2), dtype=torch.float32, device="cuda")
     r0 = run_gpu(w, d, delta_in=z)
     one = z.clone()
@@ -140,11 +209,12 @@ def test_delta_injection_affine():
     r1 = run_gpu(w, d, delta_in=one)
     R0, R1 = r0["rowstats"][..., 0], r1["rowstats"][..., 0]
     SP = R0 - R1                                    # = sum_j P_ij of the backward's own P
-    cond = base["rowstats"][..., 3] / np.maximum(orc_rs[..., orc.ST_MAX_PDP], 1e-300)
+    st = base["rowstats"]
+    cond = st[..., pk.RS_MAXABS_DS] / np.maximum(st[..., pk.RS_MAX_PDP], 1e-300)
     ok = (np.abs(SP) > 0.5) & (cond >= 2.0 ** -5)
     dstar = R0[ok] / SP[ok]
     dl = (base["delta"][..., 0] + base["delta"][..., 1])[ok]
-    e = np.abs(dstar - dl) * np.abs(SP[ok]) / np.maximum(base["rowstats"][..., 1][ok], 1e-30)
+    e = np.abs(dstar - dl) * np.abs(SP[ok]) / np.maximum(st[..., 1][ok], 1e-30)
     say("  rows", int(ok.sum()), "median e", float(np.median(e)), "max", float(e.max()))
     assert ok.sum() > 0.5 * ok.size
     assert np.median(e) < 1e-6 and e.max() < 1e-4
@@ -163,7 +233,7 @@ def test_determinism():
 def test_bf16_gradients_and_empty():
     w = _workload("tiny_mha_128", dict(N=64))
     d = synth.generate(w, seed=6)
-    g = run_gpu(w, d, grad_dtype=torch.bfloat16, rowstats=False)
+    g = run_gpu(w, d, grad_dtype=torch.bfloat16)
     o = run_oracle(w, d, grad_round=orc.ROUND_BF16)
     for k in ("dQ", "dK", "dV"):
         assert rel_err(g[k], o[k]) <= REL_TOL

@@ -192,7 +192,7 @@ def test_consistent_do_equals_stale_without_quantization(orc):
 
 def test_matched_delta_bilinearity(orc):
     """delta_matched_i = <dOr_i, (P Vr)_i> (the auxiliary-output identity of
-    App. C.3.1), computed through a different contraction order."""
+    App. C.4.1), computed through a different contraction order."""
     w, d = _quantized_case(orc, N=96)
     out, quant = orc.attention_from_inputs(d["q"], d["k"], d["v"], d["do"], w.tau, want_rowstats=True)
     B, N, Hq, Hkv, D = w.B, w.N, w.Hq, w.Hkv, w.Dqk
@@ -355,6 +355,74 @@ def test_delta_injection_is_affine(orc):
     R0 = r0["rowstats"][..., orc.ST_SUM_DS]; R1 = r1["rowstats"][..., orc.ST_SUM_DS]
     dstar = R0 / (R0 - R1)
     assert np.max(np.abs(dstar - base["delta"]) / np.maximum(np.abs(base["delta"]), 1e-3)) < 1e-10
-    # changing only delta leaves O and dV unchanged (App. C.3.1)
+    # changing only delta leaves O and dV unchanged (App. C.4.1)
     assert np.array_equal(r0["O"], base["O"]) and np.array_equal(r0["dV"], base["dV"])
     assert not np.array_equal(r0["dQ"], base["dQ"])
+
+
+def test_probability_clamp_with_injected_lse(orc):
+    """Reading R6 (App. B.6.3): the backward's recomputed P is clamped at 1
+    and P' = C8(256 P) 2^-8.  An LSE 0.5 below the forward's inflates every
+    P by e^0.5, so rows whose largest P exceeds e^-0.5 reach the clamp.
+    Pinned against P recomputed here from the dequantized operands (numpy
+    matmul) and torch's E4M3 cast: sum_j P_ij and sum_j P'_ij per row, with
+    a dropped clamp failing both."""
+    w, d = _quantized_case(orc, N=64)
+    base, quant = orc.attention_from_inputs(d["q"], d["k"], d["v"], d["do"], w.tau)
+    lse_in = base["LSE"] - 0.5
+    out, _ = orc.attention_from_inputs(d["q"], d["k"], d["v"], d["do"], w.tau, lse_in=lse_in,
+                                       want_rowstats=True)
+    B, N, Hq, Hkv, D = w.B, w.N, w.Hq, w.Hkv, w.Dqk
+    Qr, _ = orc.dequantize(quant["Q"], B, N, Hq, D)
+    Kr, _ = orc.dequantize(quant["K"], B, N, Hkv, D)
+    S = w.tau * (Qr @ np.repeat(Kr, Hq // Hkv, axis=1).transpose(0, 1, 3, 2))
+    vis = np.tril(np.ones((N, N), dtype=bool))
+    P_raw = np.where(vis, np.exp(np.where(vis, S, 0.0) - lse_in[..., None]), 0.0)
+    P = np.minimum(P_raw, 1.0)
+    assert (P_raw > 1.0).sum() >= B * Hq          # the clamp is reached (row 0 of every head at least)
+    st = out["rowstats"]
+    assert np.allclose(st[..., orc.ST_SUM_P], P.sum(-1), rtol=1e-12, atol=0)
+    assert not np.allclose(st[..., orc.ST_SUM_P], P_raw.sum(-1), rtol=1e-6, atol=0)
+    pc = torch.tensor(256.0 * P).to(torch.float8_e4m3fn).to(torch.float64).numpy() / 256.0
+    assert np.allclose(st[..., orc.ST_SUM_PCAST], pc.sum(-1), rtol=1e-12, atol=0)
+    # the forward does not read the injected LSE
+    assert np.array_equal(out["O"], base["O"]) and np.array_equal(out["LSE"], base["LSE"])
+
+
+def test_row_window_equals_whole_problem(orc):
+    """row_lo restricts the oracle to the causal suffix (query rows and keys
+    >= row_lo); by causality those outputs do not depend on anything left
+    out, so they equal the whole problem's bit for bit (same arithmetic in
+    the same order), and everything before row_lo stays zero."""
+    w, d = _quantized_case(orc, "gqa_d128_8k", seed=2, B=1, N=160, Hq=4, Hkv=2)
+    full, _ = orc.attention_from_inputs(d["q"], d["k"], d["v"], d["do"], w.tau, want_rowstats=True)
+    win, _ = orc.attention_from_inputs(d["q"], d["k"], d["v"], d["do"], w.tau, want_rowstats=True, row_lo=96)
+    for name in ("O", "dQ", "dK", "dV"):
+        assert np.array_equal(win[name][:, 96:], full[name][:, 96:]), name
+        assert not np.any(win[name][:, :96]), name
+    for name in ("LSE", "delta"):
+        assert np.array_equal(win[name][..., 96:], full[name][..., 96:]), name
+    assert np.array_equal(win["rowstats"][:, :, 96:], full["rowstats"][:, :, 96:])
+    with pytest.raises(ValueError):
+        orc.attention_from_inputs(d["q"], d["k"], d["v"], d["do"], w.tau, row_lo=40)
+
+
+def test_term_magnitude_statistic(orc):
+    """ST_SUM_P_ABSTERMS = sum_j P_ij sum_c |dOr_ic Vr_jc| (the scale the FP32
+    accumulation of dP works on), against numpy on the dequantized operands;
+    it bounds |sum_j P_ij dP_ij| from above."""
+    w, d = _quantized_case(orc, N=64)
+    out, quant = orc.attention_from_inputs(d["q"], d["k"], d["v"], d["do"], w.tau, want_rowstats=True)
+    B, N, Hq, Hkv, D = w.B, w.N, w.Hq, w.Hkv, w.Dqk
+    Qr, _ = orc.dequantize(quant["Q"], B, N, Hq, D)
+    Kr, _ = orc.dequantize(quant["K"], B, N, Hkv, D)
+    Vr, _ = orc.dequantize(quant["V"], B, N, Hkv, D)
+    dOr, _ = orc.dequantize(quant["dO"], B, N, Hq, D)
+    G = Hq // Hkv
+    S = w.tau * (Qr @ np.repeat(Kr, G, axis=1).transpose(0, 1, 3, 2))
+    vis = np.tril(np.ones((N, N), dtype=bool))
+    P = np.where(vis, np.exp(np.where(vis, S, 0.0) - out["LSE"][..., None]), 0.0)
+    T = np.einsum("bhij,bhijk->bhi", P, np.abs(dOr[:, :, :, None, :] * np.repeat(Vr, G, axis=1)[:, :, None, :, :]))
+    st = out["rowstats"]
+    assert np.allclose(st[..., orc.ST_SUM_P_ABSTERMS], T, rtol=1e-12, atol=0)
+    assert np.all(np.abs(st[..., orc.ST_SUM_PDP]) <= st[..., orc.ST_SUM_P_ABSTERMS] * (1 + 1e-12))
