@@ -188,57 +188,114 @@ hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_
 // Saved-output corrections, delta_i = sum_c dO_ic O_ic in FP32 with the
 // stored O: stale (Sec. 3.2) from the raw dO; consistent dO (Sec. 3.4,
 // QDO) from the dequantized row copy of dO, the operand of dP (E4M3 code
-// times the block's power-of-two scale, both exact in FP32).  One wave per
-// (b, n, h) row, rows strided by the grid (whose size stays within the
-// launch limits).
-template <typename TD, typename TO, bool QDO>
+// times the block's power-of-two scale, both exact in FP32).
+//
+// HBM-bound (4 bytes per channel read for BF16 dO and O, 8 bytes per row
+// written).  A lane owns 8 consecutive channels of a row: one 16-byte load
+// of each BF16 operand (two for FP32), 8 FMAs in channel order, then a
+// butterfly sum over the DV / 8 lanes of the row.  A workgroup of 256 lanes
+// holds 2048 / DV rows at a time and each lane takes RPT rows (the rows of
+// one workgroup are consecutive (b, n, h) positions, so with the usual
+// [B, N, H, D] layout its loads cover one contiguous range); the grid
+// strides over the rows beyond that.
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, float (&v)[8]);
+template <>
+__device__ __forceinline__ void load8<uint16_t>(const uint16_t* p, float (&v)[8]) {
+  const uint4 u = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int m = 0; m < 4; m++) {
+    v[2 * m] = __uint_as_float(w[m] << 16);
+    v[2 * m + 1] = __uint_as_float(w[m] & 0xffff0000u);
+  }
+}
+template <>
+__device__ __forceinline__ void load8<float>(const float* p, float (&v)[8]) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
+template <int DV, typename TD, typename TO, bool QDO>
 __global__ __launch_bounds__(256) void stale_rowsum_kernel(StaleArgs a) {
-  const int lane = threadIdx.x & 63;
+  constexpr int LPR = DV / 8;            // lanes per row
+  constexpr int RPW = 256 / LPR;         // rows per workgroup pass
+  constexpr int RPT = 2;                 // rows per lane (loads in flight)
+  const int t = threadIdx.x, sub = t % LPR, c0 = 8 * sub;
   const int64_t nrows = a.B * a.N * a.Hq;
-  for (int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); row < nrows;
-       row += (int64_t)gridDim.x * 4) {
-    const int64_t h = row % a.Hq, n = (row / a.Hq) % a.N, b = row / (a.Hq * a.N);
-    const TO* o = reinterpret_cast<const TO*>(a.o) + b * a.os[0] + n * a.os[1] + h * a.os[2];
-    float acc = 0.f;
-    for (int c = lane; c < a.Dv; c += 64) {
-      float dv, ov;
+  for (int64_t base = (int64_t)blockIdx.x * RPW * RPT; base < nrows; base += (int64_t)gridDim.x * RPW * RPT) {
+    float acc[RPT];
+    int64_t rr[RPT];
+#pragma unroll
+    for (int u = 0; u < RPT; u++) {
+      const int64_t row = base + u * RPW + t / LPR;   // (b, n, h) position
+      rr[u] = row;
+      acc[u] = 0.f;
+      if (row >= nrows) continue;
+      const int64_t h = row % a.Hq, n = (row / a.Hq) % a.N, b = row / (a.Hq * a.N);
+      float dv[8], ov[8];
       if constexpr (QDO) {
         const int64_t r = (b * a.Hq + h) * a.N + n;
-        const int e = (int)a.do_scale[r * (a.Dv / 32) + c / 32] - 127;
-        dv = ldexpf(fp8_value(a.do_code[r * a.Dv + c], 0), e);
+        const uint2 cw = *reinterpret_cast<const uint2*>(a.do_code + r * DV + c0);
+        const int e = (int)a.do_scale[r * (DV / 32) + c0 / 32] - 127;
+#pragma unroll
+        for (int k = 0; k < 8; k++) dv[k] = __builtin_ldexpf(fp8_value(k < 4 ? cw.x : cw.y, k & 3), e);
       } else {
-        const TD* d = reinterpret_cast<const TD*>(a.dout) + b * a.ds[0] + n * a.ds[1] + h * a.ds[2];
-        if constexpr (sizeof(TD) == 2) dv = bf16_to_f32(d[c]); else dv = (float)d[c];
+        load8<TD>(reinterpret_cast<const TD*>(a.dout) + b * a.ds[0] + n * a.ds[1] + h * a.ds[2] + c0, dv);
       }
-      if constexpr (sizeof(TO) == 2) ov = bf16_to_f32(o[c]); else ov = (float)o[c];
-      acc = __builtin_fmaf(dv, ov, acc);
+      load8<TO>(reinterpret_cast<const TO*>(a.o) + b * a.os[0] + n * a.os[1] + h * a.os[2] + c0, ov);
+#pragma unroll
+      for (int k = 0; k < 8; k++) acc[u] = __builtin_fmaf(dv[k], ov[k], acc[u]);
     }
 #pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
-    if (lane == 0) {
-      float* dst = a.delta + ((b * a.Hq + h) * a.N + n) * 2;
-      dst[0] = acc;
-      dst[1] = 0.f;
+    for (int u = 0; u < RPT; u++) {
+#pragma unroll
+      for (int m = LPR / 2; m >= 1; m >>= 1) acc[u] += __shfl_xor(acc[u], m);
+      const int64_t row = rr[u];
+      if (sub == 0 && row < nrows) {
+        const int64_t h = row % a.Hq, n = (row / a.Hq) % a.N, b = row / (a.Hq * a.N);
+        *reinterpret_cast<float2*>(a.delta + ((b * a.Hq + h) * a.N + n) * 2) = make_float2(acc[u], 0.f);
+      }
     }
   }
 }
 
-hipError_t launch_stale_rowsum(const StaleArgs& a, int dout_bf16, int o_bf16, hipStream_t s) {
-  const int64_t nrows = a.B * a.N * a.Hq, wgs = (nrows + 3) / 4;
-  dim3 grid((unsigned)(wgs < (int64_t(1) << 20) ? wgs : (int64_t(1) << 20)));
-  if (dout_bf16 && o_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<uint16_t, uint16_t, false>), grid, dim3(256), 0, s, a);
-  else if (dout_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<uint16_t, float, false>), grid, dim3(256), 0, s, a);
-  else if (o_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<float, uint16_t, false>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((stale_rowsum_kernel<float, float, false>), grid, dim3(256), 0, s, a);
+template <int DV>
+static void launch_rowsum_dv(const StaleArgs& a, dim3 grid, int dout_bf16, int o_bf16, bool qdo, hipStream_t s) {
+  if (qdo) {
+    if (o_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<DV, uint16_t, uint16_t, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((stale_rowsum_kernel<DV, uint16_t, float, true>), grid, dim3(256), 0, s, a);
+  } else if (dout_bf16 && o_bf16) {
+    hipLaunchKernelGGL((stale_rowsum_kernel<DV, uint16_t, uint16_t, false>), grid, dim3(256), 0, s, a);
+  } else if (dout_bf16) {
+    hipLaunchKernelGGL((stale_rowsum_kernel<DV, uint16_t, float, false>), grid, dim3(256), 0, s, a);
+  } else if (o_bf16) {
+    hipLaunchKernelGGL((stale_rowsum_kernel<DV, float, uint16_t, false>), grid, dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((stale_rowsum_kernel<DV, float, float, false>), grid, dim3(256), 0, s, a);
+  }
+}
+
+static hipError_t launch_rowsum(const StaleArgs& a, int dout_bf16, int o_bf16, bool qdo, hipStream_t s) {
+  const int64_t nrows = a.B * a.N * a.Hq;
+  const int64_t per_wg = 2 * (2048 / a.Dv), wgs = (nrows + per_wg - 1) / per_wg;
+  const dim3 grid((unsigned)(wgs < (int64_t(1) << 20) ? wgs : (int64_t(1) << 20)));
+  switch (a.Dv) {
+    case 64: launch_rowsum_dv<64>(a, grid, dout_bf16, o_bf16, qdo, s); break;
+    case 128: launch_rowsum_dv<128>(a, grid, dout_bf16, o_bf16, qdo, s); break;
+    case 256: launch_rowsum_dv<256>(a, grid, dout_bf16, o_bf16, qdo, s); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
+hipError_t launch_stale_rowsum(const StaleArgs& a, int dout_bf16, int o_bf16, hipStream_t s) {
+  return launch_rowsum(a, dout_bf16, o_bf16, false, s);
+}
+
 hipError_t launch_consistent_rowsum(const StaleArgs& a, int o_bf16, hipStream_t s) {
-  const int64_t nrows = a.B * a.N * a.Hq, wgs = (nrows + 3) / 4;
-  dim3 grid((unsigned)(wgs < (int64_t(1) << 20) ? wgs : (int64_t(1) << 20)));
-  if (o_bf16) hipLaunchKernelGGL((stale_rowsum_kernel<uint16_t, uint16_t, true>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((stale_rowsum_kernel<uint16_t, float, true>), grid, dim3(256), 0, s, a);
-  return hipGetLastError();
+  return launch_rowsum(a, 1, o_bf16, true, s);
 }
 
 // ---------------------------------------------------------------------------
