@@ -28,7 +28,8 @@
  *     address owned by the caller; the library never allocates or frees
  *     device memory.  Between calls it keeps only the thread-local error
  *     text and, per device, the compute-unit count it queries once (the
- *     backward sizes its key-block order by it).
+ *     backward sizes its key-block order by it); attn_fp8_bwd_noalloc
+ *     alone uses device memory of the library's own (see there).
  *   - Work is enqueued on `stream` and the call returns without
  *     synchronizing; faults inside a kernel surface at the caller's next
  *     synchronization.
@@ -197,6 +198,30 @@ int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q
                  int grad_dtype, const int64_t dq_strides[3], const int64_t dk_strides[3],
                  const int64_t dv_strides[3], void* workspace, size_t workspace_bytes,
                  double* rowstats, const hipEvent_t* main_events, hipStream_t stream);
+
+/* Backward without any device allocation, for callers that cannot allocate
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation).  Same arguments, checks and results as attn_fp8_bwd, whose
+ * kernels it runs, except that the workspace is the library's own scratch:
+ * ATTN_FP8_NOALLOC_SCRATCH_BYTES of device memory per device, held from the
+ * call that first uses a device until the process ends (its device address
+ * is looked up once per device with that device current).
+ *   - Problems whose attn_fp8_bwd_workspace_size exceeds the scratch are
+ *     rejected with ATTN_FP8_EUNSUPPORTED before anything is launched.
+ *   - The call allocates and frees nothing (no hipMalloc/hipFree, no
+ *     allocating library routine).
+ *   - All calls on one device share its scratch and leave their contents
+ *     there; nothing in it needs to start at zero.  Calls that overlap on one
+ *     device (other streams, other threads) race on it: serialize them. */
+#define ATTN_FP8_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int attn_fp8_bwd_noalloc(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q,
+                         const attn_fp8_mx* k, const attn_fp8_mx* v, const attn_fp8_mx* dout,
+                         const float* lse, const void* dout_raw, int dout_dtype,
+                         const int64_t dout_strides[3], const void* o, int o_dtype,
+                         const int64_t o_strides[3], const float* delta_in, void* dq, void* dk,
+                         void* dv, int grad_dtype, const int64_t dq_strides[3],
+                         const int64_t dk_strides[3], const int64_t dv_strides[3], double* rowstats,
+                         const hipEvent_t* main_events, hipStream_t stream);
 
 /* Thread-local text describing the last error returned on this thread. */
 const char* attn_fp8_last_error(void);

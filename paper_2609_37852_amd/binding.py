@@ -24,7 +24,8 @@ RS_SUM_DS, RS_SUMABS_DS, RS_SUM_DSCAST, RS_MAXABS_DS, RS_SUMABS_DSCAST, RS_MAX_P
 ROWSTATS = 7
 STATUS = {0: "OK", -1: "EINVAL", -2: "EUNSUPPORTED", -3: "EALIGN", -4: "EWORKSPACE", -5: "EHIP"}
 EXPORTS = ("attn_fp8_quantize", "attn_fp8_fwd", "attn_fp8_delta", "attn_fp8_bwd_workspace_size",
-           "attn_fp8_bwd", "attn_fp8_last_error")
+           "attn_fp8_bwd", "attn_fp8_bwd_noalloc", "attn_fp8_last_error")
+NOALLOC_SCRATCH_BYTES = 64 << 20   # ATTN_FP8_NOALLOC_SCRATCH_BYTES
 
 
 class AttnFp8Error(RuntimeError):
@@ -66,6 +67,9 @@ def lib():
         L.attn_fp8_bwd.argtypes = [P(_Problem), i32, P(_MX), P(_MX), P(_MX), P(_MX), vp, vp, i32,
                                    P(ctypes.c_int64), vp, i32, P(ctypes.c_int64), vp, vp, vp, vp, i32,
                                    P(ctypes.c_int64), P(ctypes.c_int64), P(ctypes.c_int64), vp, sz, vp, vp, vp]
+        L.attn_fp8_bwd_noalloc.argtypes = [P(_Problem), i32, P(_MX), P(_MX), P(_MX), P(_MX), vp, vp, i32,
+                                           P(ctypes.c_int64), vp, i32, P(ctypes.c_int64), vp, vp, vp, vp, i32,
+                                           P(ctypes.c_int64), P(ctypes.c_int64), P(ctypes.c_int64), vp, vp, vp]
         L.attn_fp8_last_error.restype = ctypes.c_char_p
         for name in EXPORTS[:-1]:
             getattr(L, name).restype = ctypes.c_int
@@ -227,4 +231,30 @@ def attn_fp8_bwd(p: Problem, mode: int, q: MX, k: MX, v: MX, dout: MX, lse, dout
         _dtype_code(dq.dtype), _strides_bnh(dq), _strides_bnh(dk), _strides_bnh(dv), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _ptr(rs),
         (ctypes.c_void_p * 2)(*main_events) if main_events is not None else None, _stream(dev)))
+    return dq, dk, dv, rs
+
+
+def attn_fp8_bwd_noalloc(p: Problem, mode: int, q: MX, k: MX, v: MX, dout: MX, lse, dout_raw=None, o=None,
+                         delta_in=None, grad_dtype=torch.bfloat16, rowstats: bool = False, out=None):
+    """attn_fp8_bwd on the library's own scratch (no workspace argument; the
+    library allocates nothing for it).  Returns (dq, dk, dv, rowstats or None);
+    the output tensors are allocated here unless given in `out`."""
+    dev = q.code_row.device
+    if out is None:
+        dq = torch.empty((p.batch, p.seqlen, p.heads_q, p.dim_qk), dtype=grad_dtype, device=dev)
+        dk = torch.empty((p.batch, p.seqlen, p.heads_kv, p.dim_qk), dtype=grad_dtype, device=dev)
+        dv = torch.empty((p.batch, p.seqlen, p.heads_kv, p.dim_v), dtype=grad_dtype, device=dev)
+    else:
+        dq, dk, dv = out
+    rs = torch.zeros((p.batch, p.heads_q, p.seqlen, ROWSTATS), dtype=torch.float64, device=dev) if rowstats else None
+    pc = p.c()
+    mxs = [m.c() for m in (q, k, v, dout)]
+    ds = _strides_bnh(dout_raw) if dout_raw is not None else None
+    os_ = _strides_bnh(o) if o is not None else None
+    _check("attn_fp8_bwd_noalloc", lib().attn_fp8_bwd_noalloc(
+        ctypes.byref(pc), mode, *[ctypes.byref(m) for m in mxs], _ptr(lse), _ptr(dout_raw),
+        _dtype_code(dout_raw.dtype) if dout_raw is not None else 0, ds, _ptr(o),
+        _dtype_code(o.dtype) if o is not None else 0, os_, _ptr(delta_in), _ptr(dq), _ptr(dk), _ptr(dv),
+        _dtype_code(dq.dtype), _strides_bnh(dq), _strides_bnh(dk), _strides_bnh(dv), _ptr(rs), None,
+        _stream(dev)))
     return dq, dk, dv, rs

@@ -3,10 +3,19 @@
 #include <cmath>
 #include <cstdio>
 #include <cstdarg>
+#include <mutex>
 #include <string>
 
 #include "attn_fp8.h"
 #include "kernels.hpp"
+
+// Scratch of attn_fp8_bwd_noalloc: device memory the library holds for the
+// whole process on every device it runs on (one copy per device, each at its
+// own address).  Host code never uses the array's name as an address: the
+// device address of each device's copy is looked up once, with that device
+// current, and kept in g_scratch_ptr below.
+constexpr size_t kNoAllocScratchBytes = ATTN_FP8_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
 
 namespace {
 
@@ -230,6 +239,27 @@ int launch_delta(const attn_fp8_problem* p, int mode, const attn_fp8_mx* q, cons
                     "stale_rowsum");
 }
 
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+int scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(ATTN_FP8_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(ATTN_FP8_EUNSUPPORTED, "device %d out of range", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(ATTN_FP8_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return ATTN_FP8_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -404,6 +434,29 @@ int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q
 
   if ((rc = hip_status(afp8::launch_dq(a, (int)p->dim_qk, stream), "dq"))) return rc;
   return ok();
+}
+
+int attn_fp8_bwd_noalloc(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q, const attn_fp8_mx* k,
+                         const attn_fp8_mx* v, const attn_fp8_mx* dout, const float* lse, const void* dout_raw,
+                         int dout_dtype, const int64_t dout_strides[3], const void* o, int o_dtype,
+                         const int64_t o_strides[3], const float* delta_in, void* dq, void* dk, void* dv,
+                         int grad_dtype, const int64_t dq_strides[3], const int64_t dk_strides[3],
+                         const int64_t dv_strides[3], double* rowstats, const hipEvent_t* main_events,
+                         hipStream_t stream) {
+  int rc;
+  if ((rc = check_problem(p))) return rc;
+  if (empty(p)) return ok();
+  const size_t need = ws_bwd_bytes(p);
+  if (need > kNoAllocScratchBytes)
+    return fail(ATTN_FP8_EUNSUPPORTED,
+                "attn_fp8_bwd_noalloc: this problem needs %zu bytes of scratch; the library's scratch holds %zu "
+                "(use attn_fp8_bwd with a caller workspace)",
+                need, kNoAllocScratchBytes);
+  void* ws = nullptr;
+  if ((rc = scratch_address(&ws))) return rc;
+  return attn_fp8_bwd(p, delta_mode, q, k, v, dout, lse, dout_raw, dout_dtype, dout_strides, o, o_dtype, o_strides,
+                      delta_in, dq, dk, dv, grad_dtype, dq_strides, dk_strides, dv_strides, ws, kNoAllocScratchBytes,
+                      rowstats, main_events, stream);
 }
 
 }  // extern "C"

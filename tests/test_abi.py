@@ -126,3 +126,15 @@ def test_package_exports_binding_names():
                  "RS_MAX_PDP", "RS_SUM_PCAST"):
         assert getattr(pk, name) == getattr(bd, name)
     assert pk.ROWSTATS == 7 and sorted(getattr(bd, n) for n in dir(bd) if n.startswith("RS_")) == list(range(7))
+
+
+def test_noalloc_rejects_oversized_problem_on_the_host():
+    """attn_fp8_bwd_noalloc checks the scratch need before touching the
+    device: an oversized problem fails with EUNSUPPORTED and a message."""
+    L = pk.lib()
+    p = _prob(batch=4, seqlen=8192, heads_q=16, heads_kv=4).c()
+    m = _fake_mx()
+    st = bd._I64x3(128 * 2 * 128, 2 * 128, 128)
+    rc = L.attn_fp8_bwd_noalloc(ctypes.byref(p), 0, *[ctypes.byref(m)] * 4, ctypes.c_void_p(4096), None, 1, None,
+                                None, 1, None, None, *[ctypes.c_void_p(4096)] * 3, 1, st, st, st, None, None, None)
+    assert rc == -2 and "scratch" in pk.last_error()
