@@ -197,10 +197,10 @@ __device__ __forceinline__ void stage_cols(lds8* st, const BwdLoads<DQK, DV>& L,
   constexpr int NCI = (C::CS_BYTES + 255) / 256;
   for (int k = 0; k < NCI; k++) {
     if ((2 + k) % NWK != w) continue;   // loaders 2, 3, ...: 0 and 1 take the row scales
-    const int off = 256 * k + 4 * lane;
-    if (off < C::CS_BYTES)
-      dma4s(make_buf(g.tcs, G * S.tcs()), (uint32_t)off, hi * S.tcs() + (uint32_t)(i0 / 64) * C::CS_BYTES,
-            st + C::QCS_OFF + 256 * k);
+    // the piece's offset in the scalar part, the lane's 4 bytes in the vector part
+    if (4 * lane < C::CS_BYTES - 256 * k)
+      dma4s(make_buf(g.tcs, G * S.tcs()), (uint32_t)(4 * lane),
+            hi * S.tcs() + (uint32_t)(i0 / 64) * C::CS_BYTES + 256 * k, st + C::QCS_OFF + 256 * k);
   }
 }
 
@@ -600,6 +600,8 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     const int uq = w / KSN, ks = w % KSN;
     const int qb = i0 + 32 * uq;
     if (qb >= N || kb0 + 64 * ks > qb + 31) return;
+    uint32_t ex2 = *reinterpret_cast<const uint16_t*>(es + uq * KBW + 2 * ks);
+    asm volatile("" : "+v"(ex2));
     const int i16 = lane & 15;
     const int qbase = 32 * uq + 16 * ((lane >> 4) & 1);
     // A: rows = queries of half uq, k = keys 64 ks .. 64 ks + 63 (natural order)
@@ -620,10 +622,7 @@ __global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
     uint8_t* dst = a.ds_units + unit * 2048 + 16 * lane;
     __builtin_nontemporal_store(v4i{af[0], af[1], af[2], af[3]}, reinterpret_cast<v4i*>(dst));
     __builtin_nontemporal_store(v4i{af[4], af[5], af[6], af[7]}, reinterpret_cast<v4i*>(dst + 1024));
-    if (lane == 0) {
-      // the exponents of key blocks 2 ks and 2 ks + 1 of half uq, adjacent
-      *reinterpret_cast<uint16_t*>(a.ds_exp + unit * 2) = *reinterpret_cast<const uint16_t*>(es + uq * KBW + 2 * ks);
-    }
+    if (lane == 0) *reinterpret_cast<uint16_t*>(a.ds_exp + unit * 2) = (uint16_t)ex2;
   };
 
   // one step of the pipeline for tile i at position p (p1, p2: tiles i+1,
