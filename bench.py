@@ -11,8 +11,15 @@ Throughput uses the paper's accounting (App. C.2): credited FLOPs are
 B*Hq*N^2*(dqk+dv) for the forward and B*Hq*N^2*(3 dqk + 2 dv) for the
 backward; the correction pass and the quantizer earn no credit.
 
-Prints one JSON line (see the fields below).  `--gpus N` with N > 1 exits:
-this benchmark measures a single GPU.
+Prints one JSON line.  Besides the contract's fields (value = credited
+TFLOP/s of the timed steps), it carries per-kernel times, the HBM rates of
+the quantizer and the saved-output corrections, the main backward kernel's
+roofline, the paper's own timing protocol (App. C.2: clock warm-up, five
+interleaved rounds of the median of 20 timings after 5 warm-up calls, mean
+and standard error, pre-quantized inputs) for the matched and the stale
+backward, a whole step with the stale correction, the same on the d = 256
+workload, and the oracle's CPU rate.  `--gpus N` with N > 1 exits: this
+benchmark measures a single GPU.
 """
 from __future__ import annotations
 
@@ -158,6 +165,137 @@ class HipEvents:
         return float(out.value)
 
 
+class Runner:
+    """One workload resident on the GPU: inputs, MX copies, outputs and the
+    backward workspace allocated once; step() runs the whole hot path
+    (quantize Q, K, V, dO -> forward -> correction -> backward) on the
+    current stream."""
+
+    def __init__(self, w, ev):
+        import torch
+        import paper_2609_37852_amd as pk
+        from paper_2609_37852_amd import synth
+        self.pk, self.torch, self.w, self.ev = pk, torch, w, ev
+        d = synth.generate(w, seed=0)
+        dev = torch.device("cuda:0")
+        tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        self.q, self.k, self.v, self.do = (torch.from_numpy(d[n]).to(tdt).to(dev) for n in ("q", "k", "v", "do"))
+        del d
+        self.p = pk.Problem(w.B, w.N, w.Hq, w.Hkv, w.Dqk, w.Dv, float(np.float32(w.tau)))
+        self.mq, self.mk, self.mv, self.mdo = (pk.MX.empty(*t.shape, dev) for t in (self.q, self.k, self.v, self.do))
+        self.o = torch.empty((w.B, w.N, w.Hq, w.Dv), dtype=torch.bfloat16, device=dev)
+        self.lse = torch.empty((w.B, w.Hq, w.N), dtype=torch.float32, device=dev)
+        self.delta = torch.empty((w.B, w.Hq, w.N, 2), dtype=torch.float32, device=dev)
+        self.grads = (torch.empty((w.B, w.N, w.Hq, w.Dqk), dtype=torch.bfloat16, device=dev),
+                      torch.empty((w.B, w.N, w.Hkv, w.Dqk), dtype=torch.bfloat16, device=dev),
+                      torch.empty((w.B, w.N, w.Hkv, w.Dv), dtype=torch.bfloat16, device=dev))
+        self.ws = torch.empty(pk.attn_fp8_bwd_workspace_size(self.p), dtype=torch.uint8, device=dev)
+        self.L = pk.lib()
+        self.stream = torch.cuda.current_stream(dev).cuda_stream
+
+    def quantize(self):
+        for x, m in ((self.q, self.mq), (self.k, self.mk), (self.v, self.mv), (self.do, self.mdo)):
+            mc = m.c()
+            st = (ctypes.c_int64 * 3)(x.stride(0), x.stride(1), x.stride(2))
+            rc = self.L.attn_fp8_quantize(ctypes.c_void_p(x.data_ptr()), 1 if x.dtype == self.torch.bfloat16 else 0,
+                                          *x.shape, st, ctypes.byref(mc), 3, None, ctypes.c_void_p(self.stream))
+            if rc != 0:
+                raise RuntimeError(self.pk.last_error())
+
+    def fwd(self):
+        self.pk.attn_fp8_fwd(self.p, self.mq, self.mk, self.mv, o=self.o, lse=self.lse)
+
+    def correction(self, mode):
+        self.pk.attn_fp8_delta(self.p, mode, self.mq, self.mk, self.mv, self.mdo, self.lse, self.do, self.o,
+                               delta=self.delta)
+
+    def bwd(self, mode, main_events=None):
+        self.pk.attn_fp8_bwd(self.p, mode, self.mq, self.mk, self.mv, self.mdo, self.lse, self.do, self.o,
+                             delta_in=self.delta, workspace=self.ws, out=self.grads, main_events=main_events)
+
+    def step(self, marks=None, mode=None):
+        """marks: 7 events recorded around quantize / fwd / correction / the
+        backward call, and (4, 5) around the main backward kernel."""
+        mode = self.pk.DELTA_MATCHING if mode is None else mode
+        rec = (lambda i: self.ev.record(marks[i], self.stream)) if marks else (lambda i: None)
+        rec(0)
+        self.quantize()
+        rec(1)
+        self.fwd()
+        rec(2)
+        self.correction(mode)
+        rec(3)
+        self.bwd(mode, main_events=(marks[4].value, marks[5].value) if marks else None)
+        rec(6)
+
+    def correction_ms(self, mode, n=3):
+        """Correction pass of the given mode, timed within n whole steps."""
+        ms_ = [self.ev.create(7) for _ in range(n)]
+        for m in ms_:
+            self.step(m, mode=mode)
+        self.torch.cuda.synchronize()
+        return float(np.mean([self.ev.ms(m[2], m[3]) for m in ms_]))
+
+    def timed(self, fn, warm=5, reps=20):
+        """Median of `reps` event timings of fn() after `warm` calls."""
+        for _ in range(warm):
+            fn()
+        evs = [self.ev.create(2) for _ in range(reps)]
+        for a, b in evs:
+            self.ev.record(a, self.stream)
+            fn()
+            self.ev.record(b, self.stream)
+        self.torch.cuda.synchronize()
+        return float(np.median([self.ev.ms(a, b) for a, b in evs]))
+
+    def full_step(self, mode):
+        """Whole step (quantize + fwd + correction + bwd) in the given mode:
+        median of 20 timings after 5 warm-up steps."""
+        ms = self.timed(lambda: self.step(mode=mode))
+        f, b = self.w.credited_flops()
+        return {"ms": round(ms, 4), "tflops": round((f + b) / (ms * 1e-3) / 1e12, 2),
+                "pct_of_fp8_peak": round(100 * (f + b) / (ms * 1e-3) / 1e12 / PEAK_FP8_TFLOPS, 2)}
+
+    def protocol(self, clock_warmup_s, rounds=5):
+        """The paper's timing protocol (App. C.2, Timing and accounting): a
+        clock warm-up of back-to-back steps, then `rounds` interleaved rounds;
+        in each, the forward, forward + matched backward and forward + stale
+        backward are each the median of 20 timings after 5 warm-up calls, with
+        pre-quantized inputs.  Backward = (forward + backward) - forward.
+        Reported as mean and standard error over the rounds."""
+        pk = self.pk
+        self.quantize()
+        t_end = time.perf_counter() + clock_warmup_s
+        while time.perf_counter() < t_end:
+            self.step()
+            self.torch.cuda.synchronize()
+        res = {"fwd": [], "fwd_bwd_matched": [], "fwd_bwd_stale": []}
+        for _ in range(rounds):
+            res["fwd"].append(self.timed(self.fwd))
+            for key, mode in (("fwd_bwd_matched", pk.DELTA_MATCHING), ("fwd_bwd_stale", pk.DELTA_STALE_ROWSUM)):
+                res[key].append(self.timed(lambda m=mode: (self.fwd(), self.correction(m), self.bwd(m))))
+        f, b = self.w.credited_flops()
+        fwd = np.array(res["fwd"])
+        out = {"rounds": rounds, "timings_per_round": 20, "warmup_calls": 5, "clock_warmup_s": clock_warmup_s}
+
+        def ms_tflops(name, t_ms, flops):
+            t_ms = np.asarray(t_ms)
+            tf = flops / (t_ms * 1e-3) / 1e12
+            se = lambda x: float(np.std(x, ddof=1) / np.sqrt(len(x))) if len(x) > 1 else 0.0
+            out[name] = {"ms_mean": round(float(t_ms.mean()), 4), "ms_se": round(se(t_ms), 4),
+                         "tflops_mean": round(float(tf.mean()), 2), "tflops_se": round(se(tf), 2)}
+        ms_tflops("fwd", fwd, f)
+        for mode in ("matched", "stale"):
+            fb = np.array(res[f"fwd_bwd_{mode}"])
+            ms_tflops(f"bwd_{mode}", fb - fwd, b)
+            ms_tflops(f"fwd_bwd_{mode}", fb, f + b)
+        ratio = (np.array(res["fwd_bwd_matched"]) - fwd) / (np.array(res["fwd_bwd_stale"]) - fwd) - 1
+        out["matched_over_stale_bwd"] = {"mean": round(float(ratio.mean()), 4),
+                                         "se": round(float(np.std(ratio, ddof=1) / np.sqrt(rounds)), 4)}
+        out["pct_of_fp8_peak_matched"] = round(100 * out["fwd_bwd_matched"]["tflops_mean"] / PEAK_FP8_TFLOPS, 2)
+        return out
+
+
 def cpu_baseline(w, d, threads, kv_heads=2):
     """The oracle (FP64 C, OpenMP) timed on the host cores on the first
     `kv_heads` KV groups of batch 0 at the full sequence length."""
@@ -171,9 +309,21 @@ def cpu_baseline(w, d, threads, kv_heads=2):
     orc.attention_from_inputs(sl["q"], sl["k"], sl["v"], sl["do"], float(np.float32(w.tau)), nthreads=threads)
     dt = time.perf_counter() - t
     f, b = ws.credited_flops()
+    fw, bw = w.credited_flops()
+    model = "unknown"
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return dict(value=round((f + b) / dt / 1e12, 6), unit="TFLOP/s", cores=threads, kind="oracle",
+                cpu_model=model, host_threads=os.cpu_count(),
                 sample=f"batch 0, query heads 0..{hq - 1} (KV heads 0..{hk - 1}), N={w.N}: quantize + fwd + "
-                       f"matched delta + bwd in FP64, {dt:.1f} s, credited {(f + b) / 1e9:.1f} GFLOP")
+                       f"matched delta + bwd in FP64, {dt:.1f} s, credited {(f + b) / 1e9:.1f} GFLOP",
+                extrapolated_full_workload_s=round(dt * (fw + bw) / (f + b), 1),
+                extrapolation="linear in credited FLOP from the sample to the whole workload (not measured)")
 
 
 def main():
@@ -183,6 +333,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="gqa_d128_8k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-protocol", action="store_true",
+                    help="skip the paper's timing protocol, the stale-mode step and the d = 256 line")
+    ap.add_argument("--clock-warmup", type=float, default=3.0,
+                    help="seconds of back-to-back steps before the paper's protocol (clock warm-up)")
     ap.add_argument("--diagnostics", action="store_true",
                     help="also report the row-sum and key-gradient diagnostics of the three corrections "
                          "(untimed; five extra backward runs)")
@@ -206,57 +360,22 @@ def main():
     import paper_2609_37852_amd as pk
     from paper_2609_37852_amd import synth
 
-    w = synth.WORKLOADS[args.workload]
-    d = synth.generate(w, seed=0)
-    dev = torch.device("cuda:0")
-    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
-    q, k, v, do = (torch.from_numpy(d[n]).to(tdt).to(dev) for n in ("q", "k", "v", "do"))
-    p = pk.Problem(w.B, w.N, w.Hq, w.Hkv, w.Dqk, w.Dv, float(np.float32(w.tau)))
-    mq, mk, mv, mdo = (pk.MX.empty(*t.shape, dev) for t in (q, k, v, do))
-    o = torch.empty((w.B, w.N, w.Hq, w.Dv), dtype=torch.bfloat16, device=dev)
-    lse = torch.empty((w.B, w.Hq, w.N), dtype=torch.float32, device=dev)
-    delta = torch.empty((w.B, w.Hq, w.N, 2), dtype=torch.float32, device=dev)
-    grads = (torch.empty((w.B, w.N, w.Hq, w.Dqk), dtype=torch.bfloat16, device=dev),
-             torch.empty((w.B, w.N, w.Hkv, w.Dqk), dtype=torch.bfloat16, device=dev),
-             torch.empty((w.B, w.N, w.Hkv, w.Dv), dtype=torch.bfloat16, device=dev))
-    ws = torch.empty(pk.attn_fp8_bwd_workspace_size(p), dtype=torch.uint8, device=dev)
-    L = pk.lib()
-    stream = torch.cuda.current_stream(dev).cuda_stream
     ev = HipEvents()
-
-    def quantize_into(x, m):
-        mc = m.c()
-        st = (ctypes.c_int64 * 3)(x.stride(0), x.stride(1), x.stride(2))
-        rc = L.attn_fp8_quantize(ctypes.c_void_p(x.data_ptr()), 1 if x.dtype == torch.bfloat16 else 0,
-                                 *x.shape, st, ctypes.byref(mc), 3, None, ctypes.c_void_p(stream))
-        if rc != 0:
-            raise RuntimeError(pk.last_error())
-
-    def step(marks=None, mode=pk.DELTA_MATCHING):
-        rec = (lambda i: ev.record(marks[i], stream)) if marks else (lambda i: None)
-        rec(0)
-        for x, m in ((q, mq), (k, mk), (v, mv), (do, mdo)):
-            quantize_into(x, m)
-        rec(1)
-        pk.attn_fp8_fwd(p, mq, mk, mv, o=o, lse=lse)
-        rec(2)
-        pk.attn_fp8_delta(p, mode, mq, mk, mv, mdo, lse, do, o, delta=delta)
-        rec(3)
-        pk.attn_fp8_bwd(p, mode, mq, mk, mv, mdo, lse, do, o, delta_in=delta, workspace=ws, out=grads,
-                        main_events=(marks[4].value, marks[5].value) if marks else None)
-        rec(6)
+    w = synth.WORKLOADS[args.workload]
+    run = Runner(w, ev)
 
     for _ in range(args.warmup):
-        step()
+        run.step()
     torch.cuda.synchronize()
 
+    # the contract's timed region: exactly `steps` steps between two events
     marks = [ev.create(7) for _ in range(args.steps)]
     t0, t1 = ev.create(2)
     torch.cuda.synchronize()
-    ev.record(t0, stream)
+    ev.record(t0, run.stream)
     for i in range(args.steps):
-        step(marks[i])
-    ev.record(t1, stream)
+        run.step(marks[i])
+    ev.record(t1, run.stream)
     torch.cuda.synchronize()
     total_ms = ev.ms(t0, t1)
     ms_per_step = total_ms / args.steps
@@ -266,18 +385,8 @@ def main():
 
     t_quant, t_fwd, t_delta = avg(0, 1), avg(1, 2), avg(2, 3)
     t_bwd_main, t_bwd_call = avg(4, 5), avg(3, 6)
-
-    # the saved-output corrections (stale and consistent dO), timed the same
-    # way, for the pre-pass ratios
-    def correction_ms(mode):
-        ms_ = [ev.create(7) for _ in range(3)]
-        for m in ms_:
-            step(m, mode=mode)
-        torch.cuda.synchronize()
-        return float(np.mean([ev.ms(m[2], m[3]) for m in ms_]))
-
-    t_delta_stale = correction_ms(pk.DELTA_STALE_ROWSUM)
-    t_delta_consistent = correction_ms(pk.DELTA_CONSISTENT_DO)
+    t_delta_stale = run.correction_ms(pk.DELTA_STALE_ROWSUM)
+    t_delta_consistent = run.correction_ms(pk.DELTA_CONSISTENT_DO)
 
     fwd_f, bwd_f = w.credited_flops()
     credited = fwd_f + bwd_f
@@ -288,7 +397,11 @@ def main():
     main_f = w.B * w.Hq * w.N * w.N * 2 * (w.Dqk + w.Dv)
     achieved = main_f / (t_bwd_main * 1e-3) / 1e12
     traffic = read_traffic(args.traffic)
-    quant_bytes = 4.0625 * sum(t.numel() for t in (q, k, v, do))   # bf16 in, two fp8 copies + scales out
+    n_in = sum(t.numel() for t in (run.q, run.k, run.v, run.do))
+    quant_bytes = 4.0625 * n_in                     # bf16 in, two fp8 copies + scales out
+    rows = w.B * w.N * w.Hq
+    stale_bytes = 4.0 * rows * w.Dv + 8.0 * rows    # bf16 dO and O in, (hi, lo) out
+    consistent_bytes = (1 + 1 / 32 + 2) * rows * w.Dv + 8.0 * rows
 
     line = {
         "metric": "FP8 attention fwd+bwd TFLOP/s and % of FP8 MFMA peak (causal GQA d128, 8K)",
@@ -317,27 +430,49 @@ def main():
                              "pct_of_fp8_peak_prequantized": round(100 * credited / (paper_ms * 1e-3) / 1e12 /
                                                                    PEAK_FP8_TFLOPS, 2),
                              "delta_over_bwd_main": round(t_delta / t_bwd_main, 4),
-                             "delta_over_delta_plus_bwd": round(t_delta / (t_delta + t_bwd_call), 4)},
-        "quantize_hbm_gbs": round(quant_bytes / (t_quant * 1e-3) / 1e9, 1),
+                             "delta_over_delta_plus_bwd": round(t_delta / (t_delta + t_bwd_call), 4),
+                             # the paper's reading: the matched backward's added time over the stale one
+                             "matched_over_stale_bwd": round((t_delta + t_bwd_call) / (t_delta_stale + t_bwd_call) - 1,
+                                                             4)},
+        "hbm_gbs": {"quantize": round(quant_bytes / (t_quant * 1e-3) / 1e9, 1),
+                    "delta_stale_rowsum": round(stale_bytes / (t_delta_stale * 1e-3) / 1e9, 1),
+                    "delta_consistent_do": round(consistent_bytes / (t_delta_consistent * 1e-3) / 1e9, 1),
+                    "peak": PEAK_HBM_GBS},
         "roofline": {"kernel": "bwd_kernel<128,128>", "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP8_TFLOPS, 4),
                      "traffic": traffic, "flops_per_launch": main_f, "ms_per_launch": round(t_bwd_main, 4)},
     }
+    if args.diagnostics:
+        from paper_2609_37852_amd import diagnostics
+        line["diagnostics"] = diagnostics.run(run.p, run.mq, run.mk, run.mv, run.mdo, run.lse, run.do, run.o)
+    if not args.no_protocol:
+        line["paper_protocol"] = run.protocol(args.clock_warmup)
+        line["stale_step"] = run.full_step(pk.DELTA_STALE_ROWSUM)
+        if args.workload == "gqa_d128_8k":
+            # the paper's other throughput shape: d = 256 (QK-norm workload), matched and stale
+            del run
+            torch.cuda.empty_cache()
+            w3 = synth.WORKLOADS["gqa_d256_8k_qknorm"]
+            r3 = Runner(w3, ev)
+            for _ in range(3):
+                r3.step()
+            torch.cuda.synchronize()
+            line["secondary"] = {"workload": w3.name, "matched_step": r3.full_step(pk.DELTA_MATCHING),
+                                 "stale_step": r3.full_step(pk.DELTA_STALE_ROWSUM),
+                                 "paper_protocol": r3.protocol(0.0)}
+            run = r3
     if args.copy_calibration > 0:
         # a plain streaming kernel of known size: n bytes read, n written
         n = args.copy_calibration << 20
-        src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda:0")
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
         torch.neg(src, out=dst)
         torch.cuda.synchronize()
         line["copy_calibration_bytes"] = n
-    if args.diagnostics:
-        from paper_2609_37852_amd import diagnostics
-        line["diagnostics"] = diagnostics.run(p, mq, mk, mv, mdo, lse, do, o)
     if not args.no_cpu_baseline:
         threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
-        line["cpu_baseline"] = cpu_baseline(w, d, threads)
+        line["cpu_baseline"] = cpu_baseline(w, synth.generate(w, seed=0), threads)
     print(json.dumps(line), flush=True)
 
 

@@ -57,16 +57,18 @@ namespace afp8 {
 template <int DQK, int DV>
 struct BwdCfg {
   // 8 waves: 4 blocks of 32 keys x 2 query halves.  The two waves of a key
-  // block (w and w + 4, on one SIMD) each compute S, dP, P and dS for one
-  // 32-query half of the tile; after exchanging codes through LDS the first
-  // accumulates dV and the second dK for all channels of their keys.
-  static constexpr int NWK = 8, KBW = 4;
+  // block (w and w + KBW) each compute S, dP, P and dS for one 32-query half
+  // of the tile; after exchanging codes through LDS the first accumulates dV
+  // and the second dK for all channels of their keys.  Wide heads (dqk + dv
+  // > 256) take 2 key blocks (4 waves): with 4 the accumulators and the K / V
+  // fragments of 8 waves do not fit the registers and the LDS together.
+  static constexpr int KBW = DQK + DV > 256 ? 2 : 4, NWK = 2 * KBW;
   // the direct loads of the query tiles are issued by the first wave of each
   // key block only (one wave per SIMD; these also store the dQ units), so the
   // other four issue no vector memory instructions: spread over all eight,
   // every wave stalls behind the burst of load instructions at the start of
   // a tile
-  static constexpr int NLD = 4;
+  static constexpr int NLD = KBW;
   static constexpr int NT = 64 * NWK, BKB = 32 * KBW, BQ = 64;
   static constexpr int DST = BQ + 16;   // row stride of the dS' tile [key][query]
   static constexpr int al16(int x) { return (x + 15) & ~15; }
@@ -262,7 +264,7 @@ __device__ __forceinline__ TilePos next_pos(TilePos p, int G) {
 }
 
 template <int DQK, int DV, bool STATS>
-__global__ __launch_bounds__(512) void bwd_kernel(AttnArgs a) {
+__global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) {
   using C = BwdCfg<DQK, DV>;
   constexpr int KBW = C::KBW, BKB = C::BKB, BQ = C::BQ, NCB = C::NCB;
   constexpr int KS = DQK / 64, VS = DV / 64, CK = DQK / 32, CV = DV / 32;
