@@ -61,6 +61,7 @@ def lib():
         L.orc_quantize.restype = ctypes.c_int64
         L.orc_quantize.argtypes = [_dp] + [ctypes.c_int64] * 4 + [_u8p] * 4
         L.orc_dequantize.argtypes = [_u8p] * 4 + [ctypes.c_int64] * 4 + [_dp, _dp]
+        L.orc_producer.argtypes = [_dp] + [ctypes.c_int64] * 4 + [ctypes.c_double, ctypes.c_int, _dp, _dp]
         L.orc_attention.restype = ctypes.c_int
         L.orc_attention.argtypes = ([ctypes.POINTER(_Problem)] + [ctypes.c_int] * 4 + [_dp] * 22
                                     + [ctypes.c_int64, ctypes.c_int])
@@ -121,6 +122,20 @@ def quantize(x):
                                                     ("code_row", "scale_row", "code_col", "scale_col")])
     out["nonfinite"] = int(nf)
     return out
+
+
+def producer(x, prescale=1.0, center=False):
+    """Input producer (App. B.6.1, reading R13): x [B, N, H, D] (exact
+    values) -> (y, mean): y = fl32(fl32(x * prescale) - mean), mean [B, H, D]
+    the FP32 mean over tokens (zero unless center).  prescale is taken as
+    the FP32 value it rounds to."""
+    x = _f64(x)
+    B, N, H, D = x.shape
+    assert N % 32 == 0
+    y = np.empty_like(x)
+    mean = np.empty((B, H, D))
+    lib().orc_producer(_ptr(x), B, N, H, D, float(np.float32(prescale)), int(bool(center)), _ptr(y), _ptr(mean))
+    return y, mean
 
 
 def dequantize(q, B, N, H, D):

@@ -183,6 +183,40 @@ int64_t orc_quantize(const double* x, int64_t B, int64_t N, int64_t H, int64_t D
   return nonfinite;
 }
 
+/* Input producer (App. B.6.1, Operands, Scaling, and Accumulation): before
+ * quantization the query is multiplied by the attention scale in FP32, and
+ * the key has its FP32 mean over sequence positions subtracted, separately
+ * for each channel and KV head.  Reading R13 (the paper does not fix the
+ * mean's summation): x' = fl32(x * prescale); the mean is the FP64 sum of
+ * the FP64 sums of aligned 32-token blocks (tokens ascending within a
+ * block, blocks ascending), divided by N in FP64 and rounded once to FP32;
+ * y = fl32(x' - mean) (center != 0) or y = x' (center == 0).  x, y
+ * [B,N,H,D]; mean [B,H,D] (zero without centering).  N % 32 == 0. */
+static double fl32(double v) { return (double)(float)v; }
+
+void orc_producer(const double* x, int64_t B, int64_t N, int64_t H, int64_t D, double prescale, int center,
+                  double* y, double* mean) {
+  for (int64_t b = 0; b < B; b++)
+    for (int64_t h = 0; h < H; h++)
+      for (int64_t c = 0; c < D; c++) {
+        double m = 0.0;
+        if (center) {
+          double total = 0.0;
+          for (int64_t n0 = 0; n0 < N; n0 += 32) {
+            double part = 0.0;
+            for (int64_t n = n0; n < n0 + 32; n++) part += fl32(x[((b * N + n) * H + h) * D + c] * prescale);
+            total += part;
+          }
+          m = fl32(total / (double)N);
+        }
+        mean[(b * H + h) * D + c] = m;
+        for (int64_t n = 0; n < N; n++) {
+          const int64_t o = ((b * N + n) * H + h) * D + c;
+          y[o] = fl32(fl32(x[o] * prescale) - m);
+        }
+      }
+}
+
 void orc_dequantize(const uint8_t* code_row, const uint8_t* scale_row,
                     const uint8_t* code_col, const uint8_t* scale_col,
                     int64_t B, int64_t N, int64_t H, int64_t D,

@@ -42,6 +42,12 @@ int64_t orc_quantize(const double* x, int64_t B, int64_t N, int64_t H, int64_t D
                      uint8_t* code_row, uint8_t* scale_row,
                      uint8_t* code_col, uint8_t* scale_col);
 
+/* Input producer (App. B.6.1): y = fl32(fl32(x * prescale) - mean), the
+ * mean over tokens per (b, h, c) as reading R13 defines it when center != 0
+ * (else 0).  x, y [B,N,H,D]; mean [B,H,D].  N % 32 == 0. */
+void orc_producer(const double* x, int64_t B, int64_t N, int64_t H, int64_t D, double prescale, int center,
+                  double* y, double* mean);
+
 /* Decode both copies into [B,H,N,D] doubles (either output may be NULL). */
 void orc_dequantize(const uint8_t* code_row, const uint8_t* scale_row,
                     const uint8_t* code_col, const uint8_t* scale_col,
