@@ -129,6 +129,30 @@ int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t 
                       const int64_t strides[3], const attn_fp8_mx* out, int which,
                       uint32_t* nonfinite_count, hipStream_t stream);
 
+/* Input producer + quantizer (App. B.6.1, Operands, Scaling, and
+ * Accumulation): the quantizer above applied to the transformed values
+ *   x' = fl32(x * prescale)                     (e.g. the query times tau,
+ *                                                 with softmax_scale 1 later)
+ *   y  = fl32(x' - mean[b, h, c])   if center   (e.g. the key minus its mean
+ *                                                 over sequence positions,
+ *                                                 per channel and KV head)
+ * each rounded once to FP32 (no fused multiply-add).  The mean is the FP64
+ * sum of FP64 sums over aligned 32-token blocks (tokens ascending, blocks
+ * ascending), divided by N in FP64 and rounded to FP32, so it does not depend
+ * on scheduling.  The backward takes the resulting codes as given: gradients
+ * are those of the transformed operands (straight-through, App. B.6.3; the
+ * key gradient is not re-centered).
+ *   prescale      finite, nonzero (1 for none)
+ *   center        0 or 1
+ *   channel_mean  device float [B, H, D], written when center (else unused)
+ *   partials      device double [B, H, D, N/32] workspace, when center
+ * Other arguments, checks and outputs as attn_fp8_quantize (channel_amax,
+ * when requested, is of the transformed values). */
+int attn_fp8_quantize_producer(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H,
+                               int64_t D, const int64_t strides[3], float prescale, int center,
+                               float* channel_mean, double* partials, const attn_fp8_mx* out,
+                               int which, uint32_t* nonfinite_count, hipStream_t stream);
+
 /* Forward (Sec. 2.3; App. B.6.2): S = tau * Q K^T, online softmax with
  * power-of-two rescaling, FP8 probabilities per 32-key group, O = P V / l.
  *   q, k     row copies used;  v  col copy used.

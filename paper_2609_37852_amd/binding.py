@@ -24,7 +24,7 @@ RS_SUM_DS, RS_SUMABS_DS, RS_SUM_DSCAST, RS_MAXABS_DS, RS_SUMABS_DSCAST, RS_MAX_P
 ROWSTATS = 7
 STATUS = {0: "OK", -1: "EINVAL", -2: "EUNSUPPORTED", -3: "EALIGN", -4: "EWORKSPACE", -5: "EHIP"}
 EXPORTS = ("attn_fp8_quantize", "attn_fp8_fwd", "attn_fp8_delta", "attn_fp8_bwd_workspace_size",
-           "attn_fp8_bwd", "attn_fp8_bwd_noalloc", "attn_fp8_last_error")
+           "attn_fp8_bwd", "attn_fp8_bwd_noalloc", "attn_fp8_quantize_producer", "attn_fp8_last_error")
 NOALLOC_SCRATCH_BYTES = 64 << 20   # ATTN_FP8_NOALLOC_SCRATCH_BYTES
 
 
@@ -60,6 +60,8 @@ def lib():
         vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
         P = ctypes.POINTER
         L.attn_fp8_quantize.argtypes = [vp, i32, i64, i64, i64, i64, P(ctypes.c_int64), P(_MX), i32, vp, vp]
+        L.attn_fp8_quantize_producer.argtypes = [vp, i32, i64, i64, i64, i64, P(ctypes.c_int64), ctypes.c_float, i32,
+                                                 vp, vp, P(_MX), i32, vp, vp]
         L.attn_fp8_fwd.argtypes = [P(_Problem), P(_MX), P(_MX), P(_MX), vp, i32, P(ctypes.c_int64), vp, vp]
         L.attn_fp8_delta.argtypes = [P(_Problem), i32, P(_MX), P(_MX), P(_MX), P(_MX), vp, vp, i32,
                                      P(ctypes.c_int64), vp, i32, P(ctypes.c_int64), vp, vp]
@@ -160,6 +162,22 @@ def attn_fp8_quantize(x: torch.Tensor, which: int = QUANT_BOTH, nonfinite: torch
            lib().attn_fp8_quantize(_ptr(x), _dtype_code(x.dtype), B, N, H, D, _strides_bnh(x), ctypes.byref(m),
                                    which, _ptr(nonfinite), _stream(x.device)))
     return out
+
+
+def attn_fp8_quantize_producer(x: torch.Tensor, prescale: float = 1.0, center: bool = False,
+                               which: int = QUANT_BOTH, nonfinite: torch.Tensor | None = None, amax: bool = True):
+    """The input producer (App. B.6.1) then the quantizer: x [B, N, H, D] ->
+    (MX copies of fl32(fl32(x prescale) - mean), mean [B, H, D] or None)."""
+    B, N, H, D = x.shape
+    out = MX.empty(B, N, H, D, x.device, which, amax=amax)
+    mean = torch.empty((B, H, D), dtype=torch.float32, device=x.device) if center else None
+    parts = torch.empty((B, H, D, max(N // 32, 1)), dtype=torch.float64, device=x.device) if center else None
+    m = out.c()
+    _check("attn_fp8_quantize_producer",
+           lib().attn_fp8_quantize_producer(_ptr(x), _dtype_code(x.dtype), B, N, H, D, _strides_bnh(x),
+                                            float(prescale), int(bool(center)), _ptr(mean), _ptr(parts),
+                                            ctypes.byref(m), which, _ptr(nonfinite), _stream(x.device)))
+    return out, mean
 
 
 def attn_fp8_fwd(p: Problem, q: MX, k: MX, v: MX, o_dtype=torch.bfloat16, o: torch.Tensor | None = None,

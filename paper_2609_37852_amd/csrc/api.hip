@@ -260,15 +260,9 @@ int scratch_address(void** out) {
   return ATTN_FP8_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-const char* attn_fp8_last_error(void) { return g_error.c_str(); }
-
-int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, int64_t D,
-                      const int64_t strides[3], const attn_fp8_mx* out, int which, uint32_t* nonfinite_count,
-                      hipStream_t stream) {
+int quantize_impl(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, int64_t D, const int64_t strides[3],
+                  float prescale, float* mean, double* partials, const attn_fp8_mx* out, int which,
+                  uint32_t* nonfinite_count, hipStream_t stream) {
   int rc;
   const int es = dtype_size(x_dtype);
   if (!es) return fail(ATTN_FP8_EINVAL, "x_dtype %d is not F32 or BF16", x_dtype);
@@ -300,9 +294,38 @@ int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t 
   a.which = which;
   a.nonfinite = nonfinite_count;
   a.chan_amax = out->channel_amax;
+  a.prescale = prescale;
+  a.mean = mean;
+  a.partials = partials;
   if ((rc = hip_status(afp8::launch_quantize(a, (int)D, x_dtype == ATTN_FP8_DTYPE_BF16, stream), "quantize")))
     return rc;
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* attn_fp8_last_error(void) { return g_error.c_str(); }
+
+int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, int64_t D,
+                      const int64_t strides[3], const attn_fp8_mx* out, int which, uint32_t* nonfinite_count,
+                      hipStream_t stream) {
+  return quantize_impl(x, x_dtype, B, N, H, D, strides, 1.0f, nullptr, nullptr, out, which, nonfinite_count, stream);
+}
+
+int attn_fp8_quantize_producer(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, int64_t D,
+                               const int64_t strides[3], float prescale, int center, float* channel_mean,
+                               double* partials, const attn_fp8_mx* out, int which, uint32_t* nonfinite_count,
+                               hipStream_t stream) {
+  int rc;
+  if (!(std::isfinite(prescale) && prescale != 0.f))
+    return fail(ATTN_FP8_EINVAL, "prescale must be finite and nonzero");
+  if (center) {
+    if ((rc = check_ptr("channel_mean", channel_mean)) || (rc = check_ptr("partials", partials))) return rc;
+  }
+  return quantize_impl(x, x_dtype, B, N, H, D, strides, prescale, center ? channel_mean : nullptr,
+                       center ? partials : nullptr, out, which, nonfinite_count, stream);
 }
 
 int attn_fp8_fwd(const attn_fp8_problem* p, const attn_fp8_mx* q, const attn_fp8_mx* k, const attn_fp8_mx* v,

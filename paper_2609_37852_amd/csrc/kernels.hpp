@@ -22,6 +22,12 @@ struct QuantArgs {
   int which;                 // bit 0 row copy, bit 1 col copy
   uint32_t* nonfinite;       // nullable
   float* chan_amax;          // nullable [B, H, D]: max over tokens of |x| (zeroed before the launch)
+  // input producer (all optional): x' = fl32(x * prescale), then
+  // fl32(x' - mean[b, h, c]) when mean is given; partials: [B, H, D, N/32]
+  // FP64 block sums of x' the mean is formed from
+  float prescale;            // 1 for none
+  float* mean;               // nullable [B, H, D]
+  double* partials;          // required with mean
 };
 
 struct StaleArgs {

@@ -10,6 +10,8 @@
 //   col copy: the tile is transposed through LDS (BF16 inputs kept BF16);
 //             thread t owns channel t / 2 and the whole 32x1 block t % 2 of
 //             that channel.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -80,12 +82,28 @@ __device__ __forceinline__ void encode32(const float (&v)[32], int e, uint4& lo,
   hi = make_uint4(w[4], w[5], w[6], w[7]);
 }
 
+// FP32 multiply and subtract, each rounded once: the pragma keeps the
+// compiler from contracting a product and a following subtraction into one
+// FMA (HIP compiles with contraction on).
+__device__ __forceinline__ float mul_rn(float x, float y) {
+#pragma clang fp contract(off)
+  return x * y;
+}
+__device__ __forceinline__ float sub_rn(float x, float y) {
+#pragma clang fp contract(off)
+  return x - y;
+}
+
 // One workgroup = 32 NB tokens (NB 32-token blocks; the last ones may lie
 // past the end of the sequence) x D channels of one (batch, head), 2*D threads.
-template <int D, typename T, int NB>
+// PROD: the input producer's transform is applied to every value first
+// (FP32 multiply by the prescale, then FP32 subtraction of the channel mean,
+// each rounded once: no contraction into an FMA); the transposed tile then
+// holds FP32 values.
+template <int D, typename T, int NB, bool PROD>
 __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
   constexpr int CH = D / 16;  // 16-channel chunks per token
-  typedef typename TileOf<T>::type TT;
+  typedef typename std::conditional<PROD, float, typename TileOf<T>::type>::type TT;
   __shared__ TT tile[32 * NB][D + (sizeof(TT) == 2 ? 2 : 1)];
   const int t = threadIdx.x;
   const int64_t n0 = (int64_t)blockIdx.x * 32 * NB, h = blockIdx.y, b = blockIdx.z;
@@ -110,6 +128,18 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
 #pragma unroll
       for (int k = 0; k < 16; k++) bad += __builtin_isfinite(v[u][k]) ? 0u : 1u;
     if (bad) atomicAdd(a.nonfinite, bad);
+  }
+  if constexpr (PROD) {
+    float mu[16];
+#pragma unroll
+    for (int k = 0; k < 16; k++) mu[k] = a.mean ? a.mean[bh * D + ch + k] : 0.f;
+#pragma unroll
+    for (int u = 0; u < NB; u++)
+#pragma unroll
+      for (int k = 0; k < 16; k++) {
+        const float xs = mul_rn(v[u][k], a.prescale);
+        v[u][k] = a.mean ? sub_rn(xs, mu[k]) : xs;
+      }
   }
   if (a.which & 1) {
 #pragma unroll
@@ -163,6 +193,38 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
 
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 
+// Key mean of the input producer (reading R13): FP64 sums of the prescaled
+// values over aligned 32-token blocks, tokens ascending (one thread per
+// channel: grid (N/32, H, B)), then the block sums ascending (grid (H, B)),
+// divided by N in FP64 and rounded once to FP32.  The fixed order makes the
+// mean independent of scheduling.
+template <typename T>
+__global__ __launch_bounds__(256) void producer_partials_kernel(QuantArgs a, int D) {
+  const int c = threadIdx.x;
+  if (c >= D) return;
+  const int64_t t = blockIdx.x, h = blockIdx.y, b = blockIdx.z, nblk = a.N / 32;
+  const T* src = reinterpret_cast<const T*>(a.x) + b * a.sb + h * a.sh + c;
+  double part = 0.0;
+#pragma unroll 8
+  for (int k = 0; k < 32; k++) {
+    const T x = src[(32 * t + k) * a.sn];
+    float f;
+    if constexpr (sizeof(T) == 2) f = bf16_to_f32(x); else f = (float)x;
+    part += (double)mul_rn(f, a.prescale);
+  }
+  a.partials[((b * a.H + h) * D + c) * nblk + t] = part;
+}
+
+__global__ __launch_bounds__(256) void producer_mean_kernel(QuantArgs a, int D) {
+  const int c = threadIdx.x;
+  if (c >= D) return;
+  const int64_t h = blockIdx.x, b = blockIdx.y, nblk = a.N / 32;
+  const double* p = a.partials + ((b * a.H + h) * D + c) * nblk;
+  double total = 0.0;
+  for (int64_t t = 0; t < nblk; t++) total += p[t];
+  a.mean[(b * a.H + h) * D + c] = (float)(total / (double)a.N);
+}
+
 hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_t s) {
   constexpr int NB = 2;
   dim3 grid((unsigned)((a.N + 32 * NB - 1) / (32 * NB)), (unsigned)a.H, (unsigned)a.B);
@@ -170,11 +232,23 @@ hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_
     const hipError_t e = launch_fill_zero(a.chan_amax, a.B * a.H * D, s);
     if (e != hipSuccess) return e;
   }
-#define AFP8_Q(DD)                                                                           \
-  if (D == DD) {                                                                             \
-    if (dtype_bf16) hipLaunchKernelGGL((quantize_kernel<DD, uint16_t, NB>), grid, dim3(2 * DD), 0, s, a); \
-    else hipLaunchKernelGGL((quantize_kernel<DD, float, NB>), grid, dim3(2 * DD), 0, s, a);       \
-    return hipGetLastError();                                                                \
+  const bool prod = a.prescale != 1.0f || a.mean;
+  if (a.mean) {
+    const dim3 g1((unsigned)(a.N / 32), (unsigned)a.H, (unsigned)a.B), g2((unsigned)a.H, (unsigned)a.B);
+    if (dtype_bf16) hipLaunchKernelGGL(producer_partials_kernel<uint16_t>, g1, dim3(256), 0, s, a, D);
+    else hipLaunchKernelGGL(producer_partials_kernel<float>, g1, dim3(256), 0, s, a, D);
+    hipLaunchKernelGGL(producer_mean_kernel, g2, dim3(256), 0, s, a, D);
+  }
+#define AFP8_Q(DD)                                                                                      \
+  if (D == DD) {                                                                                        \
+    if (prod) {                                                                                         \
+      if (dtype_bf16) hipLaunchKernelGGL((quantize_kernel<DD, uint16_t, NB, true>), grid, dim3(2 * DD), 0, s, a); \
+      else hipLaunchKernelGGL((quantize_kernel<DD, float, NB, true>), grid, dim3(2 * DD), 0, s, a);     \
+    } else {                                                                                            \
+      if (dtype_bf16) hipLaunchKernelGGL((quantize_kernel<DD, uint16_t, NB, false>), grid, dim3(2 * DD), 0, s, a); \
+      else hipLaunchKernelGGL((quantize_kernel<DD, float, NB, false>), grid, dim3(2 * DD), 0, s, a);    \
+    }                                                                                                   \
+    return hipGetLastError();                                                                           \
   }
   AFP8_Q(64)
   AFP8_Q(128)

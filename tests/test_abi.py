@@ -138,3 +138,17 @@ def test_noalloc_rejects_oversized_problem_on_the_host():
     rc = L.attn_fp8_bwd_noalloc(ctypes.byref(p), 0, *[ctypes.byref(m)] * 4, ctypes.c_void_p(4096), None, 1, None,
                                 None, 1, None, None, *[ctypes.c_void_p(4096)] * 3, 1, st, st, st, None, None, None)
     assert rc == -2 and "scratch" in pk.last_error()
+
+
+def test_producer_rejects_bad_arguments():
+    L = pk.lib()
+    m = _fake_mx()
+    st = bd._I64x3(64 * 64, 64, 64)
+    args = (ctypes.c_void_p(4096), 1, 1, 64, 1, 64, st)
+    assert L.attn_fp8_quantize_producer(*args, float("nan"), 0, None, None, ctypes.byref(m), 3, None, None) == -1
+    assert L.attn_fp8_quantize_producer(*args, 0.0, 0, None, None, ctypes.byref(m), 3, None, None) == -1
+    # centering needs the mean output and the partial-sum workspace
+    assert L.attn_fp8_quantize_producer(*args, 1.0, 1, None, ctypes.c_void_p(4096), ctypes.byref(m), 3, None,
+                                        None) == -1
+    assert L.attn_fp8_quantize_producer(*args, 1.0, 1, ctypes.c_void_p(4096), None, ctypes.byref(m), 3, None,
+                                        None) == -1

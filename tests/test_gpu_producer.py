@@ -1,0 +1,81 @@
+"""The input producer (App. B.6.1; reading R13) on the GPU: FP32 query
+prescale and per-(channel, KV head) key centering before quantization.
+Codes, scales and the key mean are bit-exact with the oracle's producer and
+quantizer; the whole path on the transformed operands (queries prescaled by
+tau, softmax scale 1, keys centred; straight-through key gradient) agrees
+with the oracle within the parity bounds and keeps the invariant."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+import paper_2609_37852_amd as pk
+from paper_2609_37852_amd import synth
+from _helpers import REL_TOL, block_errors, bwd_plain_and_stats, check_blocks, invariant_report, np64, rel_err, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _keys(B, N, H, D, seed, dtype):
+    rng = np.random.default_rng(seed)
+    # a per-channel bias, as trained keys carry, so that the mean matters
+    x = rng.standard_normal((B, N, H, D)).astype(np.float32) + rng.uniform(-2, 2, (1, 1, H, D)).astype(np.float32)
+    return synth.round_bf16(x) if dtype == "bf16" else x
+
+
+@pytest.mark.parametrize("D", [64, 128, 192, 256])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("prescale,center", [(1 / math.sqrt(128), False), (1.0, True), (0.3, True)])
+def test_producer_codes_bit_exact(D, dtype, prescale, center):
+    B, N, H = 2, 96, 3
+    x = _keys(B, N, H, D, seed=D, dtype=dtype)
+    # a strided view: every other head of a wider tensor
+    wide = np.zeros((B, N, 2 * H, D), np.float32)
+    wide[:, :, ::2] = x
+    t = torch.from_numpy(wide).cuda()
+    t = (t.to(torch.bfloat16) if dtype == "bf16" else t)[:, :, ::2]
+    g, mean = pk.attn_fp8_quantize_producer(t, prescale, center)
+    torch.cuda.synchronize()
+    y, m = orc.producer(x, prescale, center)
+    ref = orc.quantize(y)
+    for f in ("code_row", "scale_row", "code_col", "scale_col"):
+        assert np.array_equal(getattr(g, f).cpu().numpy(), ref[f]), f
+    if center:
+        assert np.array_equal(mean.cpu().numpy().astype(np.float64), m)
+    # channel maxima of the transformed values
+    assert np.array_equal(g.channel_amax.cpu().numpy(), np.abs(y).max(axis=1).astype(np.float32))
+
+
+def test_producer_path_matches_oracle():
+    """Queries prescaled by tau (softmax scale 1), keys centred, outlier
+    recipe (C2) at a reduced size: forward, matched correction and backward
+    against the oracle run on the oracle producer's operands."""
+    w = synth.with_shape(synth.WORKLOADS["gqa_d128_8k"], B=1, N=384, Hq=4, Hkv=2)
+    d = synth.generate(w, seed=4)
+    tau = float(np.float32(w.tau))
+    k = (d["k"] + np.float32(0.7)).astype(np.float32)           # keys with a common offset
+    k = synth.round_bf16(k)
+    qt, kt, vt, dot = (torch.from_numpy(a).to(torch.bfloat16).cuda() for a in (d["q"], k, d["v"], d["do"]))
+    mq, _ = pk.attn_fp8_quantize_producer(qt, tau, False)
+    mk, kmean = pk.attn_fp8_quantize_producer(kt, 1.0, True)
+    mv, mdo = pk.attn_fp8_quantize(vt), pk.attn_fp8_quantize(dot)
+    p = pk.Problem(w.B, w.N, w.Hq, w.Hkv, w.Dqk, w.Dv, 1.0)
+    o, lse = pk.attn_fp8_fwd(p, mq, mk, mv)
+    dq, dk, dv, rs = bwd_plain_and_stats(p, pk.DELTA_MATCHING, mq, mk, mv, mdo, lse)
+    torch.cuda.synchronize()
+    qy, _ = orc.producer(d["q"], tau, False)
+    ky, km = orc.producer(k, 1.0, True)
+    assert np.array_equal(kmean.cpu().numpy().astype(np.float64), km)
+    ref, _ = orc.attention_from_inputs(qy, ky, d["v"], d["do"], 1.0, want_rowstats=True)
+    g = dict(O=np64(o), dQ=np64(dq), dK=np64(dk), dV=np64(dv))
+    errs = {n: rel_err(g[n], ref[n]) for n in g}
+    blk = {n: block_errors(g[n], ref[n]) for n in g}
+    errs["LSE"] = float(np.max(np.abs(np64(lse) - ref["LSE"])))
+    rep = invariant_report(rs.cpu().numpy())
+    say("  errors", {n: f"{e:.2e}" for n, e in errs.items()}, "invariant", rep)
+    for n in ("O", "dQ", "dK", "dV"):
+        assert errs[n] <= REL_TOL, (n, errs[n])
+    check_blocks(blk)
+    assert errs["LSE"] < 1e-3 and rep["violations"] == 0
