@@ -35,7 +35,7 @@ ST_SUM_DS, ST_SUMABS_DS, ST_MAXABS_DS, ST_MAX_PDP, ST_SUM_DSCAST, ST_SUMABS_DSCA
 class _Problem(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int64), ("N", ctypes.c_int64), ("Hq", ctypes.c_int64),
                 ("Hkv", ctypes.c_int64), ("Dqk", ctypes.c_int64), ("Dv", ctypes.c_int64),
-                ("tau", ctypes.c_double)]
+                ("tau", ctypes.c_double), ("Nk", ctypes.c_int64), ("causal", ctypes.c_int32)]
 
 
 def lib():
@@ -150,19 +150,21 @@ def dequantize(q, B, N, H, D):
 # ---------------------------------------------------------------- attention
 def attention(B, N, Hq, Hkv, Dqk, Dv, tau, ops, dO_raw=None, *, flags=0, delta_mode=DELTA_MATCHING,
               o_round=ROUND_BF16, grad_round=ROUND_NONE, delta_in=None, lse_in=None, want_rowstats=False,
-              want_phat=False, want_ds=False, row_lo=0, nthreads=0):
+              want_phat=False, want_ds=False, row_lo=0, nthreads=0, causal=True, Nk=None):
     """Forward + correction + backward on dequantized operands.
 
-    ops: dict with Qr, Kr, Vr, dOr, Qc, Kc, Vc, dOc, each [B,H,N,D] float64
-    (H = Hq for Q/dO, Hkv for K/V).  dO_raw: [B,N,Hq,Dv] (needed for the stale
-    correction).  row_lo: compute only query rows and keys >= row_lo (the
-    causal suffix; other entries stay zero).  Returns a dict of float64
-    arrays."""
+    ops: dict with Qr, Kr, Vr, dOr, Qc, Kc, Vc, dOc, each [B,H,L,D] float64
+    (H = Hq, L = N for Q/dO; H = Hkv, L = Nk for K/V).  dO_raw: [B,N,Hq,Dv]
+    (needed for the stale correction).  causal: top-left mask (Nk must equal
+    N); without it every query sees all Nk keys (Nk defaults to N).
+    row_lo: compute only query rows and keys >= row_lo (the causal suffix;
+    other entries stay zero).  Returns a dict of float64 arrays."""
     L = lib()
-    pr = _Problem(B, N, Hq, Hkv, Dqk, Dv, float(tau))
+    Nk = N if Nk is None else int(Nk)
+    pr = _Problem(B, N, Hq, Hkv, Dqk, Dv, float(tau), Nk, int(bool(causal)))
     names = ("Qr", "Kr", "Vr", "dOr", "Qc", "Kc", "Vc", "dOc")
-    shapes = dict(Qr=(B, Hq, N, Dqk), Kr=(B, Hkv, N, Dqk), Vr=(B, Hkv, N, Dv), dOr=(B, Hq, N, Dv),
-                  Qc=(B, Hq, N, Dqk), Kc=(B, Hkv, N, Dqk), Vc=(B, Hkv, N, Dv), dOc=(B, Hq, N, Dv))
+    shapes = dict(Qr=(B, Hq, N, Dqk), Kr=(B, Hkv, Nk, Dqk), Vr=(B, Hkv, Nk, Dv), dOr=(B, Hq, N, Dv),
+                  Qc=(B, Hq, N, Dqk), Kc=(B, Hkv, Nk, Dqk), Vc=(B, Hkv, Nk, Dv), dOc=(B, Hq, N, Dv))
     arrs = {}
     for k in names:
         a = _f64(ops[k])
@@ -179,12 +181,12 @@ def attention(B, N, Hq, Hkv, Dqk, Dv, tau, ops, dO_raw=None, *, flags=0, delta_m
         lse_in = _f64(lse_in)
         assert lse_in.shape == (B, Hq, N)
     out = dict(O=np.zeros((B, N, Hq, Dv)), O_unrounded=np.zeros((B, N, Hq, Dv)), LSE=np.zeros((B, Hq, N)),
-               delta=np.zeros((B, Hq, N)), dQ=np.zeros((B, N, Hq, Dqk)), dK=np.zeros((B, N, Hkv, Dqk)),
-               dV=np.zeros((B, N, Hkv, Dv)))
+               delta=np.zeros((B, Hq, N)), dQ=np.zeros((B, N, Hq, Dqk)), dK=np.zeros((B, Nk, Hkv, Dqk)),
+               dV=np.zeros((B, Nk, Hkv, Dv)))
     out["rowstats"] = np.zeros((B, Hq, N, NSTAT)) if want_rowstats else None
-    out["phat"] = np.zeros((B, Hq, N, N)) if want_phat else None
-    out["dsraw"] = np.zeros((B, Hq, N, N)) if want_ds else None
-    out["dshat"] = np.zeros((B, Hq, N, N)) if want_ds else None
+    out["phat"] = np.zeros((B, Hq, N, Nk)) if want_phat else None
+    out["dsraw"] = np.zeros((B, Hq, N, Nk)) if want_ds else None
+    out["dshat"] = np.zeros((B, Hq, N, Nk)) if want_ds else None
     rc = L.orc_attention(ctypes.byref(pr), flags, delta_mode, o_round, grad_round,
                          *[_ptr(arrs[k]) for k in names], _ptr(dO_raw), _ptr(delta_in), _ptr(lse_in),
                          _ptr(out["O"]), _ptr(out["O_unrounded"]), _ptr(out["LSE"]), _ptr(out["delta"]),
@@ -197,12 +199,12 @@ def attention(B, N, Hq, Hkv, Dqk, Dv, tau, ops, dO_raw=None, *, flags=0, delta_m
 
 def attention_from_inputs(q, k, v, do, tau, *, flags=0, delta_mode=DELTA_MATCHING, o_round=ROUND_BF16,
                           grad_round=ROUND_NONE, exact_inputs=False, **kw):
-    """Convenience: raw inputs q,do [B,N,Hq,D], k,v [B,N,Hkv,D] (exact values)
-    -> quantize each (or, with exact_inputs, use the raw values for both
-    copies) -> attention().  Returns (outputs, quantized dict)."""
+    """Convenience: raw inputs q,do [B,N,Hq,D], k,v [B,Nk,Hkv,D] (exact
+    values) -> quantize each (or, with exact_inputs, use the raw values for
+    both copies) -> attention().  Returns (outputs, quantized dict)."""
     q, k, v, do = (_f64(t) for t in (q, k, v, do))
     B, N, Hq, Dqk = q.shape
-    Hkv, Dv = k.shape[2], v.shape[3]
+    Nk, Hkv, Dv = k.shape[1], k.shape[2], v.shape[3]
     quant = {}
     ops = {}
     for name, t in (("Q", q), ("K", k), ("V", v), ("dO", do)):
@@ -215,5 +217,5 @@ def attention_from_inputs(q, k, v, do, tau, *, flags=0, delta_mode=DELTA_MATCHIN
             quant[name] = qd
             ops[name + "r"], ops[name + "c"] = dequantize(qd, Bt, Nt, Ht, Dt)
     out = attention(B, N, Hq, Hkv, Dqk, Dv, tau, ops, do, flags=flags, delta_mode=delta_mode,
-                    o_round=o_round, grad_round=grad_round, **kw)
+                    o_round=o_round, grad_round=grad_round, Nk=Nk, **kw)
     return out, quant

@@ -38,9 +38,11 @@
  *   R11 consistent-dO correction: the stale correction with the raw dO
  *      replaced by its dequantized row copy (the operand of dP), the stored
  *      O unchanged: sum_c dO^_ic O_ic.
- *   R10 causal mask is top-left aligned (key j visible to query i iff j <= i);
- *      query head h reads KV head floor(h / (Hq/Hkv)); dK and dV are summed
- *      over the query heads of a KV group before rounding.
+ *   R10 causal mask is top-left aligned (key j visible to query i iff j <= i,
+ *      equal query and key lengths); without the mask (causal == 0) every
+ *      query sees all Nk keys and the key length may differ from the query
+ *      length; query head h reads KV head floor(h / (Hq/Hkv)); dK and dV are
+ *      summed over the query heads of a KV group before rounding.
  */
 #include "attn_oracle.h"
 
@@ -284,14 +286,16 @@ static double probability(double tau, const double* q, const double* k, int64_t 
 }
 
 typedef struct {
-  int64_t B, N, Hq, Hkv, Dqk, Dv, G;
+  int64_t B, N, Nk, Hq, Hkv, Dqk, Dv, G;
+  int causal;
   double tau;
   int flags;
   const double *Qr, *Kr, *Vr, *dOr, *LSE, *delta;
 } tile_ctx;
 
 /* One aligned 32x32 tile of the backward (query rows i0.., keys j0..):
- * P and dS = P (dP - delta) before any cast (zero for masked j > i), the
+ * P and dS = P (dP - delta) before any cast (zero for masked j > i when
+ * causal), the
  * backward probability operand P' = C8(256 P) 2^-8 (R6) and the dS operand
  * dS' cast with one power-of-two scale for the whole tile (R7). */
 static void tile(const tile_ctx* c, int64_t b, int64_t h, int64_t i0, int64_t nr, int64_t j0,
@@ -301,12 +305,12 @@ static void tile(const tile_ctx* c, int64_t b, int64_t h, int64_t i0, int64_t nr
   for (int64_t r = 0; r < 32; r++)
     for (int64_t t = 0; t < 32; t++) {
       const int64_t i = i0 + r, j = j0 + t;
-      if (r >= nr || t >= nc || j > i) { P[r][t] = 0.0; dS[r][t] = 0.0; continue; }
+      if (r >= nr || t >= nc || (c->causal && j > i)) { P[r][t] = 0.0; dS[r][t] = 0.0; continue; }
       const double lse = c->LSE[(b * c->Hq + h) * c->N + i];
       const double pij = probability(c->tau, c->Qr + ((b * c->Hq + h) * c->N + i) * c->Dqk,
-                                     c->Kr + ((b * c->Hkv + kh) * c->N + j) * c->Dqk, c->Dqk, lse);
+                                     c->Kr + ((b * c->Hkv + kh) * c->Nk + j) * c->Dqk, c->Dqk, lse);
       const double dpij = dot(c->dOr + ((b * c->Hq + h) * c->N + i) * c->Dv,
-                              c->Vr + ((b * c->Hkv + kh) * c->N + j) * c->Dv, c->Dv);
+                              c->Vr + ((b * c->Hkv + kh) * c->Nk + j) * c->Dv, c->Dv);
       P[r][t] = pij;
       dS[r][t] = pij * (dpij - c->delta[(b * c->Hq + h) * c->N + i]);
       if (fabs(dS[r][t]) > amax) amax = fabs(dS[r][t]);
@@ -330,10 +334,15 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
                   double* dQ, double* dK, double* dV,
                   double* rowstats, double* phat, double* dsraw, double* dshat, int64_t row_lo,
                   int nthreads) {
-  const int64_t B = p->B, N = p->N, Hq = p->Hq, Hkv = p->Hkv, Dqk = p->Dqk, Dv = p->Dv;
+  const int64_t B = p->B, N = p->N, Nk = p->Nk, Hq = p->Hq, Hkv = p->Hkv, Dqk = p->Dqk, Dv = p->Dv;
+  const int causal = p->causal;
   const double tau = p->tau;
-  if (B < 0 || N < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || Dqk <= 0 || Dv <= 0 ||
+  if (B < 0 || N < 0 || Nk < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || Dqk <= 0 || Dv <= 0 ||
       Dqk > ORC_MAXD || Dv > ORC_MAXD || row_lo < 0 || row_lo % 32 != 0 || (N > 0 && row_lo >= N))
+    return -1;
+  /* causal: equal lengths (R10); row_lo restricts a causal problem only; a
+   * query needs at least one key */
+  if ((causal != 0 && causal != 1) || (causal && Nk != N) || (!causal && row_lo != 0) || (N > 0 && Nk == 0))
     return -1;
   const int64_t G = Hq / Hkv;
   const double LOG2E = 1.4426950408889634074;
@@ -342,38 +351,40 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
 #else
   (void)nthreads;
 #endif
-  if (phat) memset(phat, 0, sizeof(double) * (size_t)(B * Hq * N * N));
-  if (dshat) memset(dshat, 0, sizeof(double) * (size_t)(B * Hq * N * N));
-  if (dsraw) memset(dsraw, 0, sizeof(double) * (size_t)(B * Hq * N * N));
+  if (phat) memset(phat, 0, sizeof(double) * (size_t)(B * Hq * N * Nk));
+  if (dshat) memset(dshat, 0, sizeof(double) * (size_t)(B * Hq * N * Nk));
+  if (dsraw) memset(dsraw, 0, sizeof(double) * (size_t)(B * Hq * N * Nk));
 
   /* ---- forward (Sec. 2.3; App. B.6.2 with reading R5) ---- */
 #pragma omp parallel
   {
-    double* x = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
-    double* w = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
+    double* x = (double*)malloc(sizeof(double) * (size_t)(Nk > 0 ? Nk : 1));
+    double* w = (double*)malloc(sizeof(double) * (size_t)(Nk > 0 ? Nk : 1));
 #pragma omp for collapse(3) schedule(dynamic, 16)
     for (int64_t b = 0; b < B; b++)
       for (int64_t h = 0; h < Hq; h++)
         for (int64_t i = row_lo; i < N; i++) {
           const int64_t kh = h / G;
           const double* q = Qr + ((b * Hq + h) * N + i) * Dqk;
-          /* scores over the visible keys j <= i, base-2 exponent x = S log2 e */
+          /* scores over the visible keys j < je (j <= i when causal), base-2
+           * exponent x = S log2 e */
+          const int64_t je = causal ? i + 1 : Nk;
           double smax = -INFINITY;
-          for (int64_t j = 0; j <= i; j++) {
-            double s = tau * dot(q, Kr + ((b * Hkv + kh) * N + j) * Dqk, Dqk);
+          for (int64_t j = 0; j < je; j++) {
+            double s = tau * dot(q, Kr + ((b * Hkv + kh) * Nk + j) * Dqk, Dqk);
             x[j] = s;
             if (s > smax) smax = s;
           }
           double se = 0.0;
-          for (int64_t j = 0; j <= i; j++) se += exp(x[j] - smax);
+          for (int64_t j = 0; j < je; j++) se += exp(x[j] - smax);
           LSE[(b * Hq + h) * N + i] = smax + log(se);
-          for (int64_t j = 0; j <= i; j++) x[j] *= LOG2E;
+          for (int64_t j = 0; j < je; j++) x[j] *= LOG2E;
           /* integer reference Mi: every weight below is relative to 2^Mi */
           const double Mi = ceil(smax * LOG2E);
           double ell = 0.0;                      /* normalizer from pre-cast exponentials */
-          for (int64_t j = 0; j <= i; j++) ell += exp2(x[j] - Mi);
-          for (int64_t g0 = 0; g0 <= i; g0 += 32) {
-            const int64_t g1 = (g0 + 32 < i + 1) ? g0 + 32 : i + 1;
+          for (int64_t j = 0; j < je; j++) ell += exp2(x[j] - Mi);
+          for (int64_t g0 = 0; g0 < je; g0 += 32) {
+            const int64_t g1 = (g0 + 32 < je) ? g0 + 32 : je;
             if (flags & ORC_EXACT_PFWD) {
               for (int64_t j = g0; j < g1; j++) w[j] = exp2(x[j] - Mi);
             } else {
@@ -386,14 +397,14 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
           }
           for (int64_t c = 0; c < Dv; c++) {
             double acc = 0.0;
-            for (int64_t j = 0; j <= i; j++) acc += w[j] * Vc[((b * Hkv + kh) * N + j) * Dv + c];
+            for (int64_t j = 0; j < je; j++) acc += w[j] * Vc[((b * Hkv + kh) * Nk + j) * Dv + c];
             const double o = acc / ell;
             const int64_t oi = ((b * N + i) * Hq + h) * Dv + c;
             if (O_unrounded) O_unrounded[oi] = o;
             O[oi] = round_to(o, o_round);
           }
           if (phat)
-            for (int64_t j = 0; j <= i; j++) phat[((b * Hq + h) * N + i) * N + j] = w[j] / ell;
+            for (int64_t j = 0; j < je; j++) phat[((b * Hq + h) * N + i) * Nk + j] = w[j] / ell;
         }
     free(x);
     free(w);
@@ -413,12 +424,13 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
         const double* q = Qr + ((b * Hq + h) * N + i) * Dqk;
         const double* go = dOr + ((b * Hq + h) * N + i) * Dv;
         double num = 0.0, den = 0.0, maxpdp = 0.0, tabs = 0.0;
-        for (int64_t j = 0; j <= i; j++) {
-          const double pij = probability(tau, q, Kr + ((b * Hkv + kh) * N + j) * Dqk, Dqk, lse);
-          const double dpij = dot(go, Vr + ((b * Hkv + kh) * N + j) * Dv, Dv);
+        const int64_t je = causal ? i + 1 : Nk;
+        for (int64_t j = 0; j < je; j++) {
+          const double pij = probability(tau, q, Kr + ((b * Hkv + kh) * Nk + j) * Dqk, Dqk, lse);
+          const double dpij = dot(go, Vr + ((b * Hkv + kh) * Nk + j) * Dv, Dv);
           num += pij * dpij;
           den += pij;
-          if (rowstats) tabs += pij * dot_abs(go, Vr + ((b * Hkv + kh) * N + j) * Dv, Dv);
+          if (rowstats) tabs += pij * dot_abs(go, Vr + ((b * Hkv + kh) * Nk + j) * Dv, Dv);
           if (fabs(pij * dpij) > maxpdp) maxpdp = fabs(pij * dpij);
         }
         double d;
@@ -447,8 +459,8 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
    * block jb) with tile(), so the dQ pass (one query block at a time) and the
    * dK/dV pass (one key block at a time, looping the query heads of its KV
    * group) see identical dS' and P' values, and every sum has a fixed order. */
-  const int64_t nrb = (N + 31) / 32;
-  tile_ctx ctx = {B, N, Hq, Hkv, Dqk, Dv, G, tau, flags, Qr, Kr, Vr, dOr, LB, delta};
+  const int64_t nrb = (N + 31) / 32, nkb = (Nk + 31) / 32;
+  tile_ctx ctx = {B, N, Nk, Hq, Hkv, Dqk, Dv, G, causal, tau, flags, Qr, Kr, Vr, dOr, LB, delta};
 #pragma omp parallel for collapse(3) schedule(dynamic, 1)
   for (int64_t b = 0; b < B; b++)
     for (int64_t h = 0; h < Hq; h++)
@@ -459,14 +471,15 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
         double dq[32][ORC_MAXD];
         memset(dq, 0, sizeof dq);
         const int64_t i0 = rb * 32, nr = (i0 + 32 <= N) ? 32 : N - i0;
-        for (int64_t jb = 0; jb <= rb; jb++) {
-          const int64_t j0 = jb * 32, nc = (j0 + 32 <= N) ? 32 : N - j0;
+        const int64_t jb_end = causal ? rb + 1 : nkb;
+        for (int64_t jb = 0; jb < jb_end; jb++) {
+          const int64_t j0 = jb * 32, nc = (j0 + 32 <= Nk) ? 32 : Nk - j0;
           tile(&ctx, b, h, i0, nr, j0, nc, P, dS, Pb, dSh);
           for (int64_t r = 0; r < nr; r++) {
             const int64_t i = i0 + r;
             for (int64_t t = 0; t < nc; t++) {
               const int64_t j = j0 + t;
-              if (j > i) break;
+              if (causal && j > i) break;
               const double g = dSh[r][t];
               sds[r] += dS[r][t];
               sads[r] += fabs(dS[r][t]);
@@ -474,9 +487,9 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
               sdc[r] += g;
               sadc[r] += fabs(g);
               spc[r] += Pb[r][t];
-              if (dsraw) dsraw[((b * Hq + h) * N + i) * N + j] = dS[r][t];
-              if (dshat) dshat[((b * Hq + h) * N + i) * N + j] = g;
-              const double* kc = Kc + ((b * Hkv + kh) * N + j) * Dqk;
+              if (dsraw) dsraw[((b * Hq + h) * N + i) * Nk + j] = dS[r][t];
+              if (dshat) dshat[((b * Hq + h) * N + i) * Nk + j] = g;
+              const double* kc = Kc + ((b * Hkv + kh) * Nk + j) * Dqk;
               for (int64_t c = 0; c < Dqk; c++) dq[r][c] += g * kc[c];
             }
           }
@@ -498,14 +511,14 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
 #pragma omp parallel for collapse(3) schedule(dynamic, 1)
   for (int64_t b = 0; b < B; b++)
     for (int64_t kh = 0; kh < Hkv; kh++)
-      for (int64_t jb = row_lo / 32; jb < nrb; jb++) {
+      for (int64_t jb = row_lo / 32; jb < nkb; jb++) {
         double P[32][32], dS[32][32], Pb[32][32], dSh[32][32];
         double dk[32][ORC_MAXD], dv[32][ORC_MAXD];
         memset(dk, 0, sizeof dk);
         memset(dv, 0, sizeof dv);
-        const int64_t j0 = jb * 32, nc = (j0 + 32 <= N) ? 32 : N - j0;
+        const int64_t j0 = jb * 32, nc = (j0 + 32 <= Nk) ? 32 : Nk - j0;
         for (int64_t h = kh * G; h < (kh + 1) * G; h++)
-          for (int64_t rb = jb; rb < nrb; rb++) {
+          for (int64_t rb = causal ? jb : 0; rb < nrb; rb++) {
             const int64_t i0 = rb * 32, nr = (i0 + 32 <= N) ? 32 : N - i0;
             tile(&ctx, b, h, i0, nr, j0, nc, P, dS, Pb, dSh);
             for (int64_t r = 0; r < nr; r++) {
@@ -513,7 +526,7 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
               const double* qc = Qc + ((b * Hq + h) * N + i) * Dqk;
               const double* gc = dOc + ((b * Hq + h) * N + i) * Dv;
               for (int64_t t = 0; t < nc; t++) {
-                if (j0 + t > i) break;
+                if (causal && j0 + t > i) break;
                 const double g = dSh[r][t], pb = Pb[r][t];
                 for (int64_t c = 0; c < Dqk; c++) dk[t][c] += g * qc[c];
                 for (int64_t c = 0; c < Dv; c++) dv[t][c] += pb * gc[c];
@@ -522,12 +535,12 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
           }
         for (int64_t t = 0; t < nc; t++) {
           const int64_t j = j0 + t;
-          for (int64_t c = 0; c < Dqk; c++) dK[((b * N + j) * Hkv + kh) * Dqk + c] = tau * dk[t][c];
-          for (int64_t c = 0; c < Dv; c++) dV[((b * N + j) * Hkv + kh) * Dv + c] = dv[t][c];
+          for (int64_t c = 0; c < Dqk; c++) dK[((b * Nk + j) * Hkv + kh) * Dqk + c] = tau * dk[t][c];
+          for (int64_t c = 0; c < Dv; c++) dV[((b * Nk + j) * Hkv + kh) * Dv + c] = dv[t][c];
         }
       }
   for (int64_t k = 0; k < B * N * Hq * Dqk; k++) dQ[k] = round_to(dQ[k], grad_round);
-  for (int64_t k = 0; k < B * N * Hkv * Dqk; k++) dK[k] = round_to(dK[k], grad_round);
-  for (int64_t k = 0; k < B * N * Hkv * Dv; k++) dV[k] = round_to(dV[k], grad_round);
+  for (int64_t k = 0; k < B * Nk * Hkv * Dqk; k++) dK[k] = round_to(dK[k], grad_round);
+  for (int64_t k = 0; k < B * Nk * Hkv * Dv; k++) dV[k] = round_to(dV[k], grad_round);
   return 0;
 }

@@ -15,7 +15,8 @@
  *   col copy  codes     [B, H, D, N]      scales [B, H, D, N/32]   (32x1 blocks along N)
  *   dequantized operand [B, H, N, D]      (both copies are returned in this layout)
  *   O, dQ               [B, N, Hq, D]     LSE, delta [B, Hq, N]
- *   dK, dV              [B, N, Hkv, D]
+ *   dK, dV              [B, Nk, Hkv, D]
+ * (K and V have the key length Nk, equal to N for causal problems.)
  */
 #ifndef ATTN_ORACLE_H
 #define ATTN_ORACLE_H
@@ -57,6 +58,8 @@ void orc_dequantize(const uint8_t* code_row, const uint8_t* scale_row,
 typedef struct {
   int64_t B, N, Hq, Hkv, Dqk, Dv;
   double tau;                 /* softmax scale, applied to the score accumulator */
+  int64_t Nk;                 /* key / value length (== N when causal) */
+  int32_t causal;             /* 1: top-left causal mask; 0: every query sees all Nk keys */
 } orc_problem;
 
 enum { ORC_EXACT_PFWD = 1,    /* forward probabilities are not cast to FP8 */
@@ -79,19 +82,20 @@ enum { ORC_ST_SUM_DS = 0,      /* sum_j dS_ij (pre-cast)            */
                                   magnitude of dP's terms, weighted by P) */
        ORC_NSTAT };
 
-/* Forward + correction + backward of causal attention on dequantized
+/* Forward + correction + backward of softmax attention on dequantized
  * operands (row copies feed the contractions over head_dim, col copies the
  * contractions over the sequence).  See attn_oracle.c for the steps.
  * O receives the stored output (rounded per o_round); gradients are rounded
  * per grad_round.  delta_in (nullable) replaces the computed correction;
  * lse_in (nullable, [B,Hq,N]) replaces the stored LSE in the correction and
  * gradient passes (the forward is unchanged).
- * row_lo (a multiple of 32, 0 for the whole problem) restricts the work to
+ * row_lo (a multiple of 32, 0 for the whole problem; causal problems only)
+ * restricts the work to
  * query rows i >= row_lo (O, LSE, delta, dQ, row statistics) and keys
  * j >= row_lo (dK, dV): by causality those depend on no other rows or keys'
  * outputs, so they come out exactly as in the whole problem; the rest of
  * the outputs are left untouched.
- * phat / dsraw / dshat (nullable, [B,Hq,N,N]) receive the normalized forward
+ * phat / dsraw / dshat (nullable, [B,Hq,N,Nk]) receive the normalized forward
  * probabilities actually used for O, dS before and after the FP8 cast
  * (tiny problems only).
  * Returns 0, or -1 on invalid geometry. */
