@@ -3,7 +3,7 @@
  * library with Delta-Matching.
  *
  * Method: "Delta-Matching: Closing the Final Gap of Native 8-bit Training for
- * LLMs".  Causal softmax attention (Sec. 2.3) whose seven matrix products all
+ * LLMs".  Softmax attention (Sec. 2.3), causal or not, whose seven matrix products all
  * take FP8 (E4M3) operands with power-of-two (E8M0) block scales, and whose
  * backward row correction is the matched correction
  *     delta_i = sum_j P_ij dP_ij            (Sec. 3.4)
@@ -36,18 +36,21 @@
  *   - Return value 0 on success, else a negative attn_fp8_status; on error
  *     nothing is launched and attn_fp8_last_error() describes the problem.
  *   - Causal masking is top-left aligned: key j is visible to query i iff
- *     j <= i (equal query and key lengths).  GQA: query head h reads KV head
- *     floor(h / (heads_q / heads_kv)).  MLA-style problems use
+ *     j <= i (equal query and key lengths).  Without the mask (causal = 0)
+ *     every query sees all seqlen_kv keys, which may differ from seqlen:
+ *     K, V, dK and dV then have length seqlen_kv.  GQA: query head h reads
+ *     KV head floor(h / (heads_q / heads_kv)).  MLA-style problems use
  *     dim_qk != dim_v with heads_q == heads_kv.
- *   - Supported geometry: seqlen % 32 == 0 (seqlen may be 0), dim_qk in
+ *   - Supported geometry: seqlen % 32 == 0 and seqlen_kv % 32 == 0 (seqlen
+ *     may be 0; then seqlen_kv must be too), dim_qk in
  *     {64, 128, 192, 256}, dim_v in {64, 128, 256} with (dim_qk, dim_v) in
  *     {(64,64), (128,128), (256,256), (192,128)}, heads_q % heads_kv == 0.
  *     Batch or head counts of 0 are valid empty problems.  Launch limits
  *     (ATTN_FP8_EUNSUPPORTED beyond them): batch and heads <= 65535,
- *     seqlen <= 2^30, batch * heads_q * seqlen < 2^31,
- *     batch * heads_kv * seqlen < 2^30 and (heads_q / heads_kv) * seqlen *
- *     max(dim_qk, dim_v) < 2^32 (one GQA group's operands are addressed
- *     with 32-bit offsets).
+ *     seqlen, seqlen_kv <= 2^30, batch * heads_q * seqlen < 2^31,
+ *     batch * heads_kv * seqlen_kv < 2^30 and max((heads_q / heads_kv) *
+ *     seqlen, seqlen_kv) * max(dim_qk, dim_v) < 2^32 (one GQA group's
+ *     operands are addressed with 32-bit offsets).
  *   - Strides are in elements; the last (channel) dimension is contiguous.
  *     Device pointers must be 16-byte aligned, and every stride times the
  *     element size must be a multiple of 16 bytes.
@@ -87,8 +90,9 @@ enum { ATTN_FP8_QUANT_ROW = 1, ATTN_FP8_QUANT_COL = 2, ATTN_FP8_QUANT_BOTH = 3 }
  * multiplies the FP32 score accumulator S = Q K^T. */
 typedef struct {
   int64_t batch, seqlen, heads_q, heads_kv, dim_qk, dim_v;
-  int32_t causal;          /* must be 1 */
+  int32_t causal;          /* 1: top-left causal mask (seqlen_kv == seqlen); 0: no mask */
   float softmax_scale;
+  int64_t seqlen_kv;       /* key / value length; 0 stands for seqlen */
 } attn_fp8_problem;
 
 /* One MX-quantized operand X of shape [B, N, H, D]; device memory, caller-owned.

@@ -37,7 +37,7 @@ class AttnFp8Error(RuntimeError):
 class _Problem(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int64), ("seqlen", ctypes.c_int64), ("heads_q", ctypes.c_int64),
                 ("heads_kv", ctypes.c_int64), ("dim_qk", ctypes.c_int64), ("dim_v", ctypes.c_int64),
-                ("causal", ctypes.c_int32), ("softmax_scale", ctypes.c_float)]
+                ("causal", ctypes.c_int32), ("softmax_scale", ctypes.c_float), ("seqlen_kv", ctypes.c_int64)]
 
 
 class _MX(ctypes.Structure):
@@ -119,10 +119,15 @@ class Problem:
     dim_v: int
     softmax_scale: float
     causal: int = 1
+    seqlen_kv: int = 0          # key / value length; 0 stands for seqlen
+
+    @property
+    def nk(self) -> int:
+        return self.seqlen_kv if self.seqlen_kv else self.seqlen
 
     def c(self):
         return _Problem(self.batch, self.seqlen, self.heads_q, self.heads_kv, self.dim_qk, self.dim_v,
-                        self.causal, self.softmax_scale)
+                        self.causal, self.softmax_scale, self.seqlen_kv)
 
 
 @dataclass
@@ -230,8 +235,8 @@ def attn_fp8_bwd(p: Problem, mode: int, q: MX, k: MX, v: MX, dout: MX, lse, dout
     dev = q.code_row.device
     if out is None:
         dq = torch.empty((p.batch, p.seqlen, p.heads_q, p.dim_qk), dtype=grad_dtype, device=dev)
-        dk = torch.empty((p.batch, p.seqlen, p.heads_kv, p.dim_qk), dtype=grad_dtype, device=dev)
-        dv = torch.empty((p.batch, p.seqlen, p.heads_kv, p.dim_v), dtype=grad_dtype, device=dev)
+        dk = torch.empty((p.batch, p.nk, p.heads_kv, p.dim_qk), dtype=grad_dtype, device=dev)
+        dv = torch.empty((p.batch, p.nk, p.heads_kv, p.dim_v), dtype=grad_dtype, device=dev)
     else:
         dq, dk, dv = out
     ws_bytes = attn_fp8_bwd_workspace_size(p)
@@ -260,8 +265,8 @@ def attn_fp8_bwd_noalloc(p: Problem, mode: int, q: MX, k: MX, v: MX, dout: MX, l
     dev = q.code_row.device
     if out is None:
         dq = torch.empty((p.batch, p.seqlen, p.heads_q, p.dim_qk), dtype=grad_dtype, device=dev)
-        dk = torch.empty((p.batch, p.seqlen, p.heads_kv, p.dim_qk), dtype=grad_dtype, device=dev)
-        dv = torch.empty((p.batch, p.seqlen, p.heads_kv, p.dim_v), dtype=grad_dtype, device=dev)
+        dk = torch.empty((p.batch, p.nk, p.heads_kv, p.dim_qk), dtype=grad_dtype, device=dev)
+        dv = torch.empty((p.batch, p.nk, p.heads_kv, p.dim_v), dtype=grad_dtype, device=dev)
     else:
         dq, dk, dv = out
     rs = torch.zeros((p.batch, p.heads_q, p.seqlen, ROWSTATS), dtype=torch.float64, device=dev) if rowstats else None

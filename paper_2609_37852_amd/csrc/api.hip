@@ -80,6 +80,8 @@ int check_mx(const char* name, const attn_fp8_mx* m, bool row, bool col) {
   return ATTN_FP8_OK;
 }
 
+int64_t kv_len(const attn_fp8_problem* p) { return p->seqlen_kv ? p->seqlen_kv : p->seqlen; }
+
 int check_problem(const attn_fp8_problem* p) {
   if (!p) return fail(ATTN_FP8_EINVAL, "problem is NULL");
   if (p->batch < 0 || p->seqlen < 0 || p->heads_q < 0 || p->heads_kv < 0)
@@ -91,26 +93,35 @@ int check_problem(const attn_fp8_problem* p) {
   if (!pair_ok(p->dim_qk, p->dim_v))
     return fail(ATTN_FP8_EUNSUPPORTED, "head dims (%lld, %lld) not instantiated", (long long)p->dim_qk,
                 (long long)p->dim_v);
-  if (p->causal != 1) return fail(ATTN_FP8_EUNSUPPORTED, "only causal attention is implemented");
-  if (p->seqlen % 32 != 0)
-    return fail(ATTN_FP8_EUNSUPPORTED, "seqlen %lld is not a multiple of 32", (long long)p->seqlen);
+  if (p->causal != 0 && p->causal != 1) return fail(ATTN_FP8_EINVAL, "causal must be 0 or 1");
+  if (p->seqlen_kv < 0) return fail(ATTN_FP8_EINVAL, "negative seqlen_kv");
+  const int64_t nk = kv_len(p);
+  if (p->causal && nk != p->seqlen)
+    return fail(ATTN_FP8_EUNSUPPORTED, "causal attention needs seqlen_kv == seqlen (%lld != %lld)", (long long)nk,
+                (long long)p->seqlen);
+  if (p->seqlen == 0 && nk != 0)
+    return fail(ATTN_FP8_EUNSUPPORTED, "seqlen 0 with seqlen_kv %lld (no queries, keys without gradient)",
+                (long long)nk);
+  if (p->seqlen % 32 != 0 || nk % 32 != 0)
+    return fail(ATTN_FP8_EUNSUPPORTED, "seqlen %lld / seqlen_kv %lld is not a multiple of 32", (long long)p->seqlen,
+                (long long)nk);
   if (!(std::isfinite(p->softmax_scale) && p->softmax_scale > 0.f))
     return fail(ATTN_FP8_EINVAL, "softmax_scale must be finite and positive");
-  if (p->batch > 65535 || p->heads_q > 65535 || p->seqlen > (int64_t(1) << 30))
+  if (p->batch > 65535 || p->heads_q > 65535 || p->seqlen > (int64_t(1) << 30) || nk > (int64_t(1) << 30))
     return fail(ATTN_FP8_EUNSUPPORTED, "problem exceeds the launch grid limits");
   // one launch dimension holds at most 2^32 - 1 work-items: the query-major
-  // kernels launch 2 B Hq N of them, the backward 4 B Hkv N
-  if (p->batch * p->heads_q * p->seqlen >= (int64_t(1) << 31) ||
-      p->batch * p->heads_kv * p->seqlen >= (int64_t(1) << 30))
-    return fail(ATTN_FP8_EUNSUPPORTED, "problem exceeds the launch grid limits (B Hq N = %lld)",
-                (long long)(p->batch * p->heads_q * p->seqlen));
+  // kernels launch 2 B Hq N of them, the backward 4 B Hkv Nk
+  if (p->batch * p->heads_q * p->seqlen >= (int64_t(1) << 31) || p->batch * p->heads_kv * nk >= (int64_t(1) << 30))
+    return fail(ATTN_FP8_EUNSUPPORTED, "problem exceeds the launch grid limits (B Hq N = %lld, B Hkv Nk = %lld)",
+                (long long)(p->batch * p->heads_q * p->seqlen), (long long)(p->batch * p->heads_kv * nk));
   // the kernels address the operands of one GQA group (G = Hq / Hkv adjacent
-  // heads) with 32-bit buffer offsets
+  // heads) and one KV head with 32-bit buffer offsets
   if (p->heads_kv > 0) {
     const int64_t G = p->heads_q / p->heads_kv, D = p->dim_qk > p->dim_v ? p->dim_qk : p->dim_v;
-    if (G * p->seqlen * D >= (int64_t(1) << 32))
-      return fail(ATTN_FP8_EUNSUPPORTED, "problem exceeds the 32-bit buffer offsets (G N D = %lld)",
-                  (long long)(G * p->seqlen * D));
+    const int64_t L = G * p->seqlen > nk ? G * p->seqlen : nk;
+    if (L * D >= (int64_t(1) << 32))
+      return fail(ATTN_FP8_EUNSUPPORTED, "problem exceeds the 32-bit buffer offsets (max(G N, Nk) D = %lld)",
+                  (long long)(L * D));
   }
   return ATTN_FP8_OK;
 }
@@ -125,6 +136,8 @@ afp8::AttnArgs base_args(const attn_fp8_problem* p) {
   a.Hq = p->heads_q;
   a.Hkv = p->heads_kv;
   a.G = p->heads_q / p->heads_kv;
+  a.Nk = kv_len(p);
+  a.causal = p->causal;
   a.tau = p->softmax_scale;
   a.c = (float)((double)p->softmax_scale * 1.4426950408889634);
   return a;
@@ -149,11 +162,14 @@ void set_col(const attn_fp8_mx* m, const uint8_t*& code, const uint8_t*& scale) 
 size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // stored dQ operand units (2048 B each) and their exponents (2 B each)
+size_t units_per_head(const attn_fp8_problem* p) {
+  return (size_t)afp8::dq_units_per_head(p->seqlen, kv_len(p), p->causal != 0);
+}
 size_t ws_units_bytes(const attn_fp8_problem* p) {
-  return round256((size_t)p->batch * p->heads_q * (size_t)afp8::dq_units_per_head(p->seqlen) * 2048);
+  return round256((size_t)p->batch * p->heads_q * units_per_head(p) * 2048);
 }
 size_t ws_exp_bytes(const attn_fp8_problem* p) {
-  return round256((size_t)p->batch * p->heads_q * (size_t)afp8::dq_units_per_head(p->seqlen) * 2);
+  return round256((size_t)p->batch * p->heads_q * units_per_head(p) * 2);
 }
 size_t ws_delta_bytes(const attn_fp8_problem* p) {
   return round256((size_t)p->batch * p->heads_q * p->seqlen * 2 * sizeof(float));
@@ -165,7 +181,7 @@ size_t ws_tile_cs_bytes(const attn_fp8_problem* p) {
   return round256((size_t)p->batch * p->heads_q * ((p->seqlen + 63) / 64) * 2 * (p->dim_qk + p->dim_v));
 }
 size_t ws_tile_kcs_bytes(const attn_fp8_problem* p) {
-  return round256((size_t)p->batch * p->heads_kv * ((p->seqlen + 63) / 64) * 2 * p->dim_qk);
+  return round256((size_t)p->batch * p->heads_kv * ((kv_len(p) + 63) / 64) * 2 * p->dim_qk);
 }
 size_t ws_bwd_bytes(const attn_fp8_problem* p) {
   return ws_units_bytes(p) + ws_exp_bytes(p) + ws_delta_bytes(p) + ws_rows_bytes(p) + ws_tile_cs_bytes(p) +

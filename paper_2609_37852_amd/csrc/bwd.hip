@@ -2,8 +2,8 @@
 //
 // Key-major: a workgroup owns BKB = 32*NWK keys of one (batch, KV head); wave
 // w owns keys 32w..32w+31 of them.  The workgroup loops over the query heads
-// of the KV group and over 64-query tiles from the causal diagonal to the end
-// of the sequence.  dK and dV for its keys stay in MFMA accumulators (FP32)
+// of the KV group and over 64-query tiles from the causal diagonal (the first
+// tile, without the mask) to the end of the sequence.  dK and dV for its keys stay in MFMA accumulators (FP32)
 // across the whole loop, which is the GQA group sum.
 //
 // Query tiles reach LDS by direct global->LDS loads (no registers): while
@@ -13,8 +13,9 @@
 //
 // Per wave, tile and 32-query sub-block qs (near the diagonal a sub-block is
 // skipped when it lies wholly before the wave's keys or past the sequence,
-// and masked when it holds them; tiles wholly after the workgroup's keys take
-// a path without either):
+// and masked when it holds them; tiles wholly after the workgroup's keys, or
+// any tile inside both sequences without the mask, take a path without
+// either):
 //   S  = Q K^T, dP = dO V^T   MX MFMA (A = Q / dO row tiles in LDS, B = the
 //                             wave's K / V row codes in registers); lane l
 //                             owns key l % 32 and holds 16 queries.
@@ -99,9 +100,11 @@ struct BwdCfg {
   static constexpr int NCB = 2 * RSTAGE + 2 * CSTAGE + FIXED + (KV_LDS ? KV : 0) <= LIM ? 2 : 1;
 };
 
-// dQ operand units of one head before query block q (block q has q/2 + 1
-// units of 64 keys up to the diagonal): sum_{i<q} (floor(i/2) + 1).
-__host__ __device__ __forceinline__ int64_t tri_units(int64_t q) {
+// dQ operand units of one head before 32-query block q.  Causal: block q has
+// q/2 + 1 units of 64 keys up to the diagonal, sum_{i<q} (floor(i/2) + 1);
+// without the mask every block has nks = ceil(Nk / 64).
+__host__ __device__ __forceinline__ int64_t units_before(int64_t q, int64_t nks, bool causal) {
+  if (!causal) return q * nks;
   const int64_t m = q >> 1;
   return (q & 1) ? (m + 1) * (m + 1) : m * (m + 1);
 }
@@ -288,17 +291,18 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
   const int kbw = w % KBW;                      // this wave's 32-key block within the workgroup
   const int qs = w / KBW;                       // and its 32-query half of every tile
-  const int N = (int)a.N;
+  const int N = (int)a.N, Nk = (int)a.Nk;
+  const bool causal = a.causal != 0;
   // workgroup id -> key block (slowest, in the order of key_block_of) and
   // (batch, KV head) (fastest: the key blocks of one KV head get ids equal
   // mod 16, hence one XCD and its L2 when B * Hkv % 8 == 0)
   const int GI = (int)(a.B * a.Hkv);
-  const KeyBlock kbk = key_block_of((int)blockIdx.x / GI, (N + BKB - 1) / BKB, a.bwd_cohort);
+  const KeyBlock kbk = key_block_of((int)blockIdx.x / GI, (Nk + BKB - 1) / BKB, a.bwd_cohort);
   const int kb0 = kbk.kb * BKB;
   const bool up = kbk.up;
   const int kh = ((int)blockIdx.x % GI) % (int)a.Hkv, b = ((int)blockIdx.x % GI) / (int)a.Hkv;
   const int kw0 = kb0 + 32 * kbw;               // this wave's first key
-  const bool live = kw0 < N;
+  const bool live = kw0 < Nk;
   const int kj = kw0 + li;                      // this lane's key
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
   const size_t bhk = (size_t)b * a.Hkv + kh;
@@ -316,21 +320,21 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   __shared__ __attribute__((aligned(16))) uint8_t vL[KVL ? BKB * DV : 16];
   {
     const int row = live ? kj : 0;
-    const uint8_t* kr = a.k_code + (bhk * N + row) * DQK;
-    const uint8_t* vr = a.v_code + (bhk * N + row) * DV;
+    const uint8_t* kr = a.k_code + (bhk * Nk + row) * DQK;
+    const uint8_t* vr = a.v_code + (bhk * Nk + row) * DV;
 #pragma unroll
     for (int s = 0; s < KS; s++) {
       kf[s] = frag_rows_global(kr, s, hf);
       clear_channel(kf[s], s, hf, hot);
-      ksc[s] = a.k_scale[(bhk * N + row) * (DQK / 32) + 2 * s + hf];
+      ksc[s] = a.k_scale[(bhk * Nk + row) * (DQK / 32) + 2 * s + hf];
     }
 #pragma unroll
     for (int s = 0; s < VS; s++) {
       vf[s] = frag_rows_global(vr, s, hf);
-      vsc[s] = a.v_scale[(bhk * N + row) * (DV / 32) + 2 * s + hf];
+      vsc[s] = a.v_scale[(bhk * Nk + row) * (DV / 32) + 2 * s + hf];
     }
     if (hf == 0)
-      kb = hot >= 0 ? row_value<DQK>(a.k_code + bhk * N * DQK, a.k_scale + bhk * N * (DQK / 32), row, hot) : 0.f;
+      kb = hot >= 0 ? row_value<DQK>(a.k_code + bhk * Nk * DQK, a.k_scale + bhk * Nk * (DQK / 32), row, hot) : 0.f;
     if constexpr (KVL) {
       // the first wave of each key block stores the K fragments, the second
       // the V fragments, where frag_rows_swz reads them (visible after the
@@ -362,10 +366,11 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
 #pragma unroll
     for (int r = 0; r < 16; r++) acc[i][r] = 0.f;
 
-  const int nqt = (N + BQ - 1) / BQ, qt0 = kb0 / BQ, nq = nqt - qt0;
+  const int nqt = (N + BQ - 1) / BQ, qt0 = causal ? kb0 / BQ : 0, nq = nqt - qt0;
   const int total = G * nq;
   const size_t bh0 = (size_t)b * Hq + (size_t)kh * G;   // first query head of the group
-  const int64_t units_per_head = tri_units(N / 32);
+  const int nks = (Nk + 63) / 64;               // 64-key steps of the dQ units
+  const int64_t units_per_head = units_before(N / 32, nks, causal);
   auto q0_of = [&](TilePos p) __attribute__((always_inline)) { return (up ? qt0 + p.r : nqt - 1 - p.r) * BQ; };
   BwdLoads<DQK, DV> ld;
   ld.init(loader_index<DQK, DV>() >= 0 ? loader_index<DQK, DV>() : 0, lane, N);
@@ -408,7 +413,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
       for (int e4 = 0; e4 < 4; e4++) {
         const int r = 4 * g + e4;
         float p = bwd_prob(s[r], c);
-        if (EDGE && qb == kw0) p = (li > 8 * g + 4 * hf + e4) ? 0.f : p;   // diagonal block: key > query
+        if (EDGE && causal && qb == kw0) p = (li > 8 * g + 4 * hf + e4) ? 0.f : p;   // diagonal block: key > query
         s[r] = p;
         if constexpr (STATS) pdp[r] = fabsf(p * dp[r]);
         dp[r] = __builtin_fmaf(p, dp[r], p * ndv[e4]);
@@ -463,8 +468,8 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
       __attribute__((always_inline)) {
     const int i0 = q0_of(p);
     const int qb = i0 + 32 * qs;
-    const bool full = i0 >= kb0 + BKB && i0 + BQ <= N;
-    const bool skip = !full && (!live || qb < kw0 || qb >= N);
+    const bool full = (causal ? i0 >= kb0 + BKB : kb0 + BKB <= Nk) && i0 + BQ <= N;
+    const bool skip = !full && (!live || (causal && qb < kw0) || qb >= N);
     const int h = kh * G + p.hi;
     if (full) probs(std::false_type{}, qb, skip, h, R);
     else probs(std::true_type{}, qb, skip, h, R);
@@ -479,8 +484,8 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   auto front_skip = [&](TilePos p) __attribute__((always_inline)) {
     const int i0 = q0_of(p);
     const int qb = i0 + 32 * qs;
-    const bool full = i0 >= kb0 + BKB && i0 + BQ <= N;
-    return !full && (!live || qb < kw0 || qb >= N);
+    const bool full = (causal ? i0 >= kb0 + BKB : kb0 + BKB <= Nk) && i0 + BQ <= N;
+    return !full && (!live || (causal && qb < kw0) || qb >= N);
   };
 
   // The MFMAs of one pipeline step, as one straight sequence: S and dP of the
@@ -593,7 +598,8 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
 
   // dQ operand units of the tile at p (its dS' codes and exponents in ds /
   // es): unit (query half uq, key step ks) holds 32 queries x 64 keys; units
-  // wholly in the future of their queries do not exist
+  // wholly in the future of their queries (causal) or past the last key do
+  // not exist
   auto ds_store = [&](TilePos p, const uint8_t* ds, const uint8_t* es) __attribute__((always_inline)) {
     constexpr int KSN = BKB / 64;
     const int h = kh * G + p.hi;
@@ -601,7 +607,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
     if (w >= 2 * KSN) return;
     const int uq = w / KSN, ks = w % KSN;
     const int qb = i0 + 32 * uq;
-    if (qb >= N || kb0 + 64 * ks > qb + 31) return;
+    if (qb >= N || kb0 + 64 * ks >= Nk || (causal && kb0 + 64 * ks > qb + 31)) return;
     uint32_t ex2 = *reinterpret_cast<const uint16_t*>(es + uq * KBW + 2 * ks);
     asm volatile("" : "+v"(ex2));
     const int i16 = lane & 15;
@@ -616,7 +622,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
       af[2 * part] = tv[0];
       af[2 * part + 1] = tv[1];
     }
-    const int64_t unit = ((int64_t)b * Hq + h) * units_per_head + tri_units(qb / 32) + (kb0 + 64 * ks) / 64;
+    const int64_t unit = ((int64_t)b * Hq + h) * units_per_head + units_before(qb / 32, nks, causal) + (kb0 + 64 * ks) / 64;
     // streamed past the caches: the units are read once, by dq_kernel, and
     // must not evict the query tiles the workgroups share
     // (a unit is two 1 KB halves, operand bytes 0..15 then 16..31 of every
@@ -721,16 +727,19 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
 //   tile_cs [B, Hq, ceil(N/64)] x 2 (Dqk + Dv) B: for each 64-query tile, the
 //           col-copy scales of Q then dO for the tile's two 32-query groups
 //           ([channel][group]), the second clamped to the first past the end;
-//   tile_kcs [B, Hkv, ceil(N/64)] x 2 Dqk B: the same for K (dq_kernel).
+//   tile_kcs [B, Hkv, ceil(Nk/64)] x 2 Dqk B: the same for K per 64-key step
+//           (dq_kernel).
+// Workgroup x covers queries and keys 64 x .. 64 x + 63 (either may lie past
+// its sequence).
 template <int DQK, int DV>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
   __shared__ int hot_slot;
-  const int N = (int)a.N;
+  const int N = (int)a.N, Nk = (int)a.Nk;
   const int h = blockIdx.y, b = blockIdx.z, kh = h / (int)a.G;
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
   const size_t bh = (size_t)b * a.Hq + h;
   const int i0 = blockIdx.x * 64;
-  if (threadIdx.x < 64) {
+  if (i0 < N && threadIdx.x < 64) {
     uint8_t* blk = reinterpret_cast<uint8_t*>(a.rows) + (bh * ((N + 63) / 64) + blockIdx.x) * 1024;
     float2 pr = make_float2(0.f, 0.f);
     float nd = 0.f;
@@ -744,20 +753,23 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
     reinterpret_cast<float2*>(blk)[threadIdx.x] = pr;
     reinterpret_cast<float*>(blk + 512)[threadIdx.x] = nd;
   }
-  const int g0 = i0 / 32, g1 = (i0 + 32 < N ? i0 + 32 : i0) / 32;
-  uint8_t* dst = a.tile_cs + (bh * ((N + 63) / 64) + blockIdx.x) * (2 * (DQK + DV));
-  for (int u = threadIdx.x; u < DQK + DV; u += 256) {
-    const uint8_t* src = u < DQK ? a.qc_scale + (bh * DQK + u) * (N / 32)
-                                 : a.doc_scale + (bh * DV + (u - DQK)) * (N / 32);
-    dst[2 * u] = src[g0];
-    dst[2 * u + 1] = src[g1];
+  if (i0 < N) {
+    const int g0 = i0 / 32, g1 = (i0 + 32 < N ? i0 + 32 : i0) / 32;
+    uint8_t* dst = a.tile_cs + (bh * ((N + 63) / 64) + blockIdx.x) * (2 * (DQK + DV));
+    for (int u = threadIdx.x; u < DQK + DV; u += 256) {
+      const uint8_t* src = u < DQK ? a.qc_scale + (bh * DQK + u) * (N / 32)
+                                   : a.doc_scale + (bh * DV + (u - DQK)) * (N / 32);
+      dst[2 * u] = src[g0];
+      dst[2 * u + 1] = src[g1];
+    }
   }
-  // the K col scales of the same 64 keys, once per KV head (for dq_kernel)
-  if (h < a.Hkv) {
+  // the K col scales of keys i0 .., once per KV head (for dq_kernel)
+  if (h < a.Hkv && i0 < Nk) {
+    const int g0 = i0 / 32, g1 = (i0 + 32 < Nk ? i0 + 32 : i0) / 32;
     const size_t bk = (size_t)b * a.Hkv + h;
-    uint8_t* dk = a.tile_kcs + (bk * ((N + 63) / 64) + blockIdx.x) * (2 * DQK);
+    uint8_t* dk = a.tile_kcs + (bk * ((Nk + 63) / 64) + blockIdx.x) * (2 * DQK);
     for (int u = threadIdx.x; u < DQK; u += 256) {
-      const uint8_t* src = a.kc_scale + (bk * DQK + u) * (N / 32);
+      const uint8_t* src = a.kc_scale + (bk * DQK + u) * (Nk / 32);
       dk[2 * u] = src[g0];
       dk[2 * u + 1] = src[g1];
     }
@@ -767,7 +779,8 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
 // dQ = tau dS' K_col, query-major: a workgroup of 4 waves owns 128 queries
 // of one (batch, query head), wave w one 32-query block and all Dqk channels
 // (small workgroups: several per CU keep more unit loads in flight).
-// Per 64-key step up to the diagonal: the A operand is the stored unit (32
+// Per 64-key step up to the diagonal (over all keys without the mask): the A
+// operand is the stored unit (32
 // bytes per lane in operand order, as two 1 KB halves, prefetched into
 // registers one step ahead); the K col tile of the step [Dqk][64] and its
 // scales reach LDS by direct loads, double-buffered and shared by the 4
@@ -780,26 +793,28 @@ __global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t kA[KT + KSB];
   __shared__ __attribute__((aligned(16))) uint8_t kB[KT + KSB];
   const int lane = threadIdx.x & 63, w = wave_id(), hf = lane >> 5, li = lane & 31;
-  const int N = (int)a.N, nqb = N / 32;
+  const int N = (int)a.N, Nk = (int)a.Nk, nqb = N / 32;
+  const bool causal = a.causal != 0;
+  const int nks = (Nk + 63) / 64;                    // 64-key steps over the keys
   const int ntile = (nqb + NW - 1) / NW;
   const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);
   const int tile = ntile - 1 - wc.r;                 // longest rows first
   const int h = wc.h, b = wc.b, kh = h / (int)a.G;
   const int qb = NW * tile + w;                      // this wave's 32-query block
   const int qlast = NW * tile + NW - 1 < nqb - 1 ? NW * tile + NW - 1 : nqb - 1;
-  const int nk = qb < nqb ? qb / 2 + 1 : 0;          // this wave's 64-key steps
-  const int nkw = qlast / 2 + 1;                     // the workgroup's
+  const int nk = qb < nqb ? (causal ? qb / 2 + 1 : nks) : 0;   // this wave's 64-key steps
+  const int nkw = causal ? qlast / 2 + 1 : nks;                 // the workgroup's
   const int64_t bh = (int64_t)b * a.Hq + h;
-  const int64_t unit0 = bh * tri_units(nqb) + tri_units(qb < nqb ? qb : 0);
+  const int64_t unit0 = bh * units_before(nqb, nks, causal) + units_before(qb < nqb ? qb : 0, nks, causal);
   const uint8_t* units = a.ds_units + unit0 * 2048 + 16 * lane;
   const uint8_t* ex = a.ds_exp + unit0 * 2;
   const int64_t bk = (int64_t)b * a.Hkv + kh;
-  const uint8_t* kc = a.kc_code + bk * DQK * N;
-  const uint8_t* tk = a.tile_kcs + bk * ((N + 63) / 64) * KSB;
+  const uint8_t* kc = a.kc_code + bk * DQK * Nk;
+  const uint8_t* tk = a.tile_kcs + bk * nks * KSB;
 
-  const Buf tkb = make_buf(tk, (uint32_t)((N + 63) / 64) * KSB);
+  const Buf tkb = make_buf(tk, (uint32_t)nks * KSB);
   auto issue = [&](lds8* dst, int ks) __attribute__((always_inline)) {
-    dma_cols<DQK, NW>(dst, kc, 64 * ks, N, w, lane);
+    dma_cols<DQK, NW>(dst, kc, 64 * ks, Nk, w, lane);
     constexpr int NI = (KSB + 255) / 256;
     for (int k = 0; k < NI; k++) {
       if ((NW - 1 - k) != w) continue;
@@ -872,12 +887,12 @@ hipError_t launch_dq(const AttnArgs& a, int dqk, hipStream_t s) {
   return hipGetLastError();
 }
 
-int64_t dq_units_per_head(int64_t N) { return tri_units(N / 32); }
+int64_t dq_units_per_head(int64_t nq, int64_t nk, bool causal) { return units_before(nq / 32, (nk + 63) / 64, causal); }
 
 template <int DQK, int DV>
 static hipError_t bwd_dispatch(const AttnArgs& a0, hipStream_t s) {
   using C = BwdCfg<DQK, DV>;
-  const int64_t nkb = (a0.N + C::BKB - 1) / C::BKB;
+  const int64_t nkb = (a0.Nk + C::BKB - 1) / C::BKB;
   const dim3 grid((unsigned)(nkb * a0.Hkv * a0.B));
   // workgroups of one KV head that run at once: one per compute unit (the
   // kernel's LDS allows one), the units shared by the B Hkv heads
@@ -899,7 +914,8 @@ static hipError_t bwd_dispatch(const AttnArgs& a0, hipStream_t s) {
 }
 
 hipError_t launch_bwd_prep(const AttnArgs& a, int dqk, int dv, hipStream_t s) {
-  const dim3 grid((unsigned)((a.N + 63) / 64), (unsigned)a.Hq, (unsigned)a.B);
+  const int64_t L = a.N > a.Nk ? a.N : a.Nk;
+  const dim3 grid((unsigned)((L + 63) / 64), (unsigned)a.Hq, (unsigned)a.B);
   if (dqk == 64 && dv == 64) hipLaunchKernelGGL((bwd_prep_kernel<64, 64>), grid, dim3(256), 0, s, a);
   else if (dqk == 128 && dv == 128) hipLaunchKernelGGL((bwd_prep_kernel<128, 128>), grid, dim3(256), 0, s, a);
   else if (dqk == 256 && dv == 256) hipLaunchKernelGGL((bwd_prep_kernel<256, 256>), grid, dim3(256), 0, s, a);

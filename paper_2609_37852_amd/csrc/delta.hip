@@ -19,7 +19,8 @@
 // (same MX MFMA products and k order, the same rank-2 update, bwd_prob()),
 // so the backward's dS = P (dP - delta) sums to zero over every row up to
 // FP32 rounding of its own terms.  Only the 32-key group holding the
-// diagonal is masked; groups in a wave's future are skipped.
+// diagonal is masked; groups in a wave's future (causal) or past the last key
+// are skipped.
 #include <type_traits>
 
 #include "common.hpp"
@@ -53,7 +54,8 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
-  const int N = (int)a.N;
+  const int N = (int)a.N, Nk = (int)a.Nk;
+  const bool causal = a.causal != 0;
   const int nqb = (N + BQ - 1) / BQ;
   const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);
   const int qb = nqb - 1 - wc.r;              // longest causal rows first
@@ -61,6 +63,8 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   const int q0 = qb * BQ + 32 * w;
   const bool live = q0 < N;
   const int qi = q0 + li;
+  // groups visible to the wave's queries start before klim (a multiple of 32)
+  const int klim = causal ? q0 + 32 : Nk;
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
 
   const size_t bhq = (size_t)b * a.Hq + h, bhk = (size_t)b * a.Hkv + kh;
@@ -87,12 +91,13 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   }
   double num = 0.0, den = 0.0;
 
-  const uint8_t* kcode = a.k_code + bhk * N * DQK;
-  const uint8_t* kscale = a.k_scale + bhk * N * (DQK / 32);
-  const uint8_t* vcode = a.v_code + bhk * N * DV;
-  const uint8_t* vscale = a.v_scale + bhk * N * (DV / 32);
-  const int qend = (qb + 1) * BQ < N ? (qb + 1) * BQ : N;
-  const int ntiles = (qend + BK - 1) / BK;
+  const uint8_t* kcode = a.k_code + bhk * Nk * DQK;
+  const uint8_t* kscale = a.k_scale + bhk * Nk * (DQK / 32);
+  const uint8_t* vcode = a.v_code + bhk * Nk * DV;
+  const uint8_t* vscale = a.v_scale + bhk * Nk * (DV / 32);
+  // key tiles up to the block's last query, or over all keys
+  const int kend = causal ? ((qb + 1) * BQ < N ? (qb + 1) * BQ : N) : Nk;
+  const int ntiles = (kend + BK - 1) / BK;
 
   // loads of tile j0 (raw isolated-channel bytes in registers, decoded when
   // they are stored to LDS)
@@ -102,12 +107,12 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   kload.init(w, lane);
   vload.init(w, lane);
   auto issue = [&](lds8* st, int j0) __attribute__((always_inline)) {
-    kload.issue(st + C::K_OFF, kcode, j0, N, w, lane);
-    vload.issue(st + C::V_OFF, vcode, j0, N, w, lane);
-    dma_row_scales<DQK, NW, BK>(st + C::KS_OFF, kscale, j0, N, w, lane, 0);
-    dma_row_scales<DV, NW, BK>(st + C::VS_OFF, vscale, j0, N, w, lane, 1);
+    kload.issue(st + C::K_OFF, kcode, j0, Nk, w, lane);
+    vload.issue(st + C::V_OFF, vcode, j0, Nk, w, lane);
+    dma_row_scales<DQK, NW, BK>(st + C::KS_OFF, kscale, j0, Nk, w, lane, 0);
+    dma_row_scales<DV, NW, BK>(st + C::VS_OFF, vscale, j0, Nk, w, lane, 1);
     if (hot >= 0 && threadIdx.x < BK) {
-      const int r = j0 + (int)threadIdx.x < N ? j0 + (int)threadIdx.x : N - 1;
+      const int r = j0 + (int)threadIdx.x < Nk ? j0 + (int)threadIdx.x : Nk - 1;
       khc = kcode[(int64_t)r * DQK + hot];
       khs = kscale[(int64_t)r * (DQK / 32) + hot / 32];
     }
@@ -163,11 +168,11 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   };
 
   auto tile = [&](const uint8_t* st, int j0) __attribute__((always_inline)) {
-    if (!live || j0 > q0) return;
+    if (!live || j0 >= klim) return;
     v16f s0, dp0, s1, dp1;
-    if (j0 + BK <= q0) {
-      // wholly before the wave's queries: every group, no mask; the MFMAs of
-      // group g + 1 are issued before the vector work of group g
+    if (causal ? j0 + BK <= q0 : j0 + BK <= Nk) {
+      // every key visible to every query of the wave: every group, no mask;
+      // the MFMAs of group g + 1 are issued before the vector work of group g
       group_mfma(st, 0, s0, dp0);
 #pragma unroll
       for (int g = 0; g < BK / 32; g += 2) {
@@ -181,9 +186,9 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
 #pragma unroll
     for (int g = 0; g < BK / 32; g++) {
       const int g0 = j0 + 32 * g;              // first key of the group
-      if (g0 > q0) break;                      // this and later groups are in the wave's future
+      if (g0 >= klim) break;                   // this and later groups are invisible to the wave
       group_mfma(st, g, s0, dp0);
-      if (g0 == q0) group_sums(s0, dp0, std::true_type{});
+      if (causal && g0 == q0) group_sums(s0, dp0, std::true_type{});
       else group_sums(s0, dp0, std::false_type{});
     }
   };

@@ -5,8 +5,8 @@
 // [Dv][BK], their scales) reach
 // LDS by direct loads, double-buffered: the next tile streams in while the
 // current one is computed, one barrier per tile.  Tiles run from key 0 up to
-// the causal diagonal, so the workgroups of one KV head that run together
-// read the same tiles.
+// the causal diagonal (to the last key without the mask), so the workgroups
+// of one KV head that run together read the same tiles.
 //
 // Per wave and tile (aligned 32-key groups, taken in 64-key halves):
 //   S^T = K Q^T       MX MFMA, A = K row tile (LDS), B = Q row codes (regs);
@@ -27,7 +27,7 @@
 //                     from registers, put in natural key order by one
 //                     v_permlane32_swap per dword pair.
 // Only the group holding the diagonal needs a mask; groups wholly in a wave's
-// future skip their MFMA and exponentials.
+// future (causal) or past the last key skip their MFMA and exponentials.
 // Epilogue: O = O_acc / l (bf16 or fp32), LSE = (M + log2 l) ln 2.
 #include <type_traits>
 
@@ -75,7 +75,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
-  const int N = (int)a.N;
+  const int N = (int)a.N, Nk = (int)a.Nk;
+  const bool causal = a.causal != 0;
   const int nqb = (N + BQ - 1) / BQ;
   const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);
   const int qb = nqb - 1 - wc.r;              // longest causal rows first
@@ -83,13 +84,16 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   const int q0 = qb * BQ + 32 * w;
   const bool live = q0 < N;
   const int qi = q0 + li;
+  // keys j0 .. visible to the wave's queries start groups before klim (a
+  // multiple of 32): the diagonal group's end when causal, else Nk
+  const int klim = causal ? q0 + 32 : Nk;
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
 
   const size_t bhq = (size_t)b * a.Hq + h, bhk = (size_t)b * a.Hkv + kh;
-  const uint8_t* kcode = a.k_code + bhk * N * DQK;
-  const uint8_t* kscale = a.k_scale + bhk * N * (DQK / 32);
-  const uint8_t* vcode = a.vc_code + bhk * DV * N;
-  const uint8_t* vscale = a.vc_scale + bhk * DV * (N / 32);
+  const uint8_t* kcode = a.k_code + bhk * Nk * DQK;
+  const uint8_t* kscale = a.k_scale + bhk * Nk * (DQK / 32);
+  const uint8_t* vcode = a.vc_code + bhk * DV * Nk;
+  const uint8_t* vscale = a.vc_scale + bhk * DV * (Nk / 32);
 
   v8i qf[KS];
   int qsc[KS];
@@ -113,7 +117,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   float M = -__builtin_inff();
   float lsum = 0.f;
   const float c = a.c;
-  const int ntiles = (qb + 1) * (BQ / BK);     // key tiles up to the block's diagonal
+  // key tiles up to the block's diagonal, or over all keys
+  const int ntiles = causal ? (qb + 1) * (BQ / BK) : (Nk + BK - 1) / BK;
 
   // Loads of tile j0: codes and K scales straight to LDS; the V col scales
   // (4 strided bytes per channel) and the isolated-channel bytes of each key
@@ -123,20 +128,20 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   RowLoads<DQK, NW, BK> kload;
   ColLoads<DV, NW, BK> vload;
   kload.init(w, lane);
-  vload.init(w, lane, N);
+  vload.init(w, lane, Nk);
   auto issue = [&](lds8* st, int j0) __attribute__((always_inline)) {
-    kload.issue(st + C::K_OFF, kcode, j0, N, w, lane);
-    vload.issue(st + C::V_OFF, vcode, j0, N, w, lane);
-    dma_row_scales<DQK, NW, BK>(st + C::KS_OFF, kscale, j0, N, w, lane, 0);
+    kload.issue(st + C::K_OFF, kcode, j0, Nk, w, lane);
+    vload.issue(st + C::V_OFF, vcode, j0, Nk, w, lane);
+    dma_row_scales<DQK, NW, BK>(st + C::KS_OFF, kscale, j0, Nk, w, lane, 0);
     if (threadIdx.x < DV) {
 #pragma unroll
       for (int g = 0; g < BK / 32; g++) {
-        const int grp = (j0 + 32 * g < N ? j0 + 32 * g : N - 32) / 32;
-        vsr[g] = vscale[threadIdx.x * (N / 32) + grp];
+        const int grp = (j0 + 32 * g < Nk ? j0 + 32 * g : Nk - 32) / 32;
+        vsr[g] = vscale[threadIdx.x * (Nk / 32) + grp];
       }
     }
     if (hot >= 0 && threadIdx.x < BK) {
-      const int r = j0 + (int)threadIdx.x < N ? j0 + (int)threadIdx.x : N - 1;
+      const int r = j0 + (int)threadIdx.x < Nk ? j0 + (int)threadIdx.x : Nk - 1;
       khc = kcode[(int64_t)r * DQK + hot];
       khs = kscale[(int64_t)r * (DQK / 32) + hot / 32];
     }
@@ -154,9 +159,9 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
       reinterpret_cast<float*>(st + C::KH_OFF)[threadIdx.x] = hot >= 0 ? scaled_value(khc, khs) : 0.f;
   };
 
-  // FULL: the tile lies wholly before the wave's queries (no mask, no skipped
-  // group, no branch between groups, so one half's MFMAs can overlap the
-  // other's vector work)
+  // FULL: every key of the tile is visible to every query of the wave (no
+  // mask, no skipped group, no branch between groups, so one half's MFMAs
+  // can overlap the other's vector work)
   auto tile_body = [&](const uint8_t* st, int j0, auto full_tag) __attribute__((always_inline)) {
     constexpr bool FULL = decltype(full_tag)::value;
     const uint8_t* K = st + C::K_OFF;
@@ -166,14 +171,14 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
     const float* Kh = reinterpret_cast<const float*>(st + C::KH_OFF);
 #pragma unroll
     for (int hk = 0; hk < BK / 64; hk++) {
-      if (!FULL && j0 + 64 * hk > q0) break;   // both groups of this half are in the wave's future
+      if (!FULL && j0 + 64 * hk >= klim) break;   // both groups of this half are invisible
       v16f s[2];
       float gm[2];
 #pragma unroll
       for (int g2 = 0; g2 < 2; g2++) {
         const int kb = 2 * hk + g2;
         const int g0 = j0 + 32 * kb;           // first key of the group
-        if (!FULL && g0 > q0) {                // whole group in this wave's future
+        if (!FULL && g0 >= klim) {             // whole group invisible to this wave
           gm[g2] = -__builtin_inff();
           continue;
         }
@@ -188,7 +193,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
         if (hot >= 0) s[g2] = rank2_update(hf ? 0.f : Kh[32 * kb + li], qv, s[g2]);
         // lane holds keys g0 + 8 (r/4) + 4 hf + r % 4 of query qi
         float m = -__builtin_inff();
-        if (!FULL && g0 == q0) {               // the diagonal group: keys after the query are masked
+        if (!FULL && causal && g0 == q0) {     // the diagonal group: keys after the query are masked
 #pragma unroll
           for (int r = 0; r < 16; r++) {
             s[g2][r] = (8 * (r >> 2) + 4 * hf + (r & 3)) > li ? -__builtin_inff() : s[g2][r];
@@ -221,7 +226,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
       int eg[2];
 #pragma unroll
       for (int g2 = 0; g2 < 2; g2++) {
-        if (!FULL && j0 + 32 * (2 * hk + g2) > q0) {
+        if (!FULL && j0 + 32 * (2 * hk + g2) >= klim) {
           codes[g2] = v4i{0, 0, 0, 0};
           eg[g2] = -126;
           continue;
@@ -254,8 +259,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
     }
   };
   auto tile = [&](const uint8_t* st, int j0) __attribute__((always_inline)) {
-    if (!live || j0 > q0) return;
-    if (j0 + BK <= q0) tile_body(st, j0, std::true_type{});
+    if (!live || j0 >= klim) return;
+    if (causal ? j0 + BK <= q0 : j0 + BK <= Nk) tile_body(st, j0, std::true_type{});
     else tile_body(st, j0, std::false_type{});
   };
 

@@ -43,17 +43,21 @@ struct StaleArgs {
 };
 
 // Shared by the forward, the matched-correction pass and the backward.
+// Query-side arrays have the query length N, key-side arrays (K, V, dK, dV,
+// the K col scales per 64-key step) the key length Nk (equal when causal).
 struct AttnArgs {
   int64_t B, N, Hq, Hkv, G;  // G = Hq / Hkv
+  int64_t Nk;                // key / value length
+  int causal;                // 1: key j visible to query i iff j <= i; 0: every key
   float c;                   // tau * log2(e), applied to the score accumulator
   float tau;
   const uint8_t *q_code, *q_scale;     // row copy of Q      [B,Hq,N,Dqk], [B,Hq,N,Dqk/32]
-  const uint8_t *k_code, *k_scale;     // row copy of K      [B,Hkv,N,Dqk]
-  const uint8_t *v_code, *v_scale;     // row copy of V      [B,Hkv,N,Dv]
+  const uint8_t *k_code, *k_scale;     // row copy of K      [B,Hkv,Nk,Dqk]
+  const uint8_t *v_code, *v_scale;     // row copy of V      [B,Hkv,Nk,Dv]
   const uint8_t *do_code, *do_scale;   // row copy of dO     [B,Hq,N,Dv]
   const uint8_t *qc_code, *qc_scale;   // col copy of Q      [B,Hq,Dqk,N], [B,Hq,Dqk,N/32]
-  const uint8_t *kc_code, *kc_scale;   // col copy of K      [B,Hkv,Dqk,N]
-  const uint8_t *vc_code, *vc_scale;   // col copy of V      [B,Hkv,Dv,N]
+  const uint8_t *kc_code, *kc_scale;   // col copy of K      [B,Hkv,Dqk,Nk]
+  const uint8_t *vc_code, *vc_scale;   // col copy of V      [B,Hkv,Dv,Nk]
   const uint8_t *doc_code, *doc_scale; // col copy of dO     [B,Hq,Dv,N]
   const float* q_amax;                 // nullable [B,Hq,Dqk] per-channel max |q|
   const float* k_amax;                 // nullable [B,Hkv,Dqk] per-channel max |k|
@@ -63,9 +67,9 @@ struct AttnArgs {
   float* delta_out;
   float* rows;                         // [B,Hq,ceil(N/64)] x 1 KB backward per-query values (workspace)
   uint8_t* tile_cs;                    // [B,Hq,ceil(N/64),2(Dqk+Dv)] backward per-tile col scales (workspace)
-  uint8_t* tile_kcs;                   // [B,Hkv,ceil(N/64),2 Dqk] K col scales per 64-key step (workspace)
+  uint8_t* tile_kcs;                   // [B,Hkv,ceil(Nk/64),2 Dqk] K col scales per 64-key step (workspace)
   void* o;  int64_t os[3]; int o_bf16;
-  uint8_t* ds_units;                   // dQ operand units (workspace): 2048 B per (head, query block, 64 keys)
+  uint8_t* ds_units;                   // dQ operand units (workspace): 2048 B per (head, 32 queries, 64 keys)
   uint8_t* ds_exp;                     // their block exponents, 2 B per unit
   void* dq; int64_t dqs[3];
   void* dk; int64_t dks[3];
@@ -84,6 +88,8 @@ hipError_t launch_delta_matching(const AttnArgs& a, int dqk, int dv, hipStream_t
 hipError_t launch_bwd_prep(const AttnArgs& a, int dqk, int dv, hipStream_t s);
 hipError_t launch_bwd(const AttnArgs& a, int dqk, int dv, hipStream_t s);
 hipError_t launch_dq(const AttnArgs& a, int dqk, hipStream_t s);
-int64_t dq_units_per_head(int64_t N);   // stored dQ operand units of one head
+// stored dQ operand units of one head: one per (32-query block, 64-key
+// step) that holds a visible key
+int64_t dq_units_per_head(int64_t nq, int64_t nk, bool causal);
 
 }  // namespace afp8

@@ -32,6 +32,12 @@ class Workload:
     dtype: str          # "f32" or "bf16": storage dtype of Q, K, V, dO
     transform: str      # "none", "outlier", "outlier3", "qknorm", "rope", "temperature"
     tau: float          # softmax scale
+    causal: bool = True
+    Nk: int = 0         # key / value length (0: N); causal problems have Nk = N
+
+    @property
+    def nk(self) -> int:
+        return self.Nk if self.Nk else self.N
 
     @property
     def causal_pairs(self) -> int:
@@ -39,8 +45,10 @@ class Workload:
 
     def credited_flops(self):
         """Paper's accounting (App. C.2) generalized to dqk != dv:
-        fwd B*Hq*N^2*(dqk+dv), bwd B*Hq*N^2*(3*dqk+2*dv)."""
-        n2 = self.B * self.Hq * self.N * self.N
+        fwd B*Hq*N^2*(dqk+dv), bwd B*Hq*N^2*(3*dqk+2*dv) for the causal
+        problem (half of the full N x N products); without the mask the full
+        N x Nk products count, twice as many per query-key pair."""
+        n2 = self.B * self.Hq * self.N * self.N if self.causal else 2 * self.B * self.Hq * self.N * self.nk
         return n2 * (self.Dqk + self.Dv), n2 * (3 * self.Dqk + 2 * self.Dv)
 
 
@@ -79,12 +87,12 @@ def bf16_bits(x: np.ndarray) -> np.ndarray:
 
 
 def generate(w: Workload, seed: int = 0):
-    """Returns dict q [B,N,Hq,Dqk], k [B,N,Hkv,Dqk], v [B,N,Hkv,Dv],
+    """Returns dict q [B,N,Hq,Dqk], k [B,Nk,Hkv,Dqk], v [B,Nk,Hkv,Dv],
     do [B,N,Hq,Dv] (float32 arrays of dtype-exact values)."""
-    B, N = w.B, w.N
+    B, N, Nk = w.B, w.N, w.nk
     q = _rng(seed, "q").standard_normal((B, N, w.Hq, w.Dqk), dtype=np.float32)
-    k = _rng(seed, "k").standard_normal((B, N, w.Hkv, w.Dqk), dtype=np.float32)
-    v = _rng(seed, "v").standard_normal((B, N, w.Hkv, w.Dv), dtype=np.float32)
+    k = _rng(seed, "k").standard_normal((B, Nk, w.Hkv, w.Dqk), dtype=np.float32)
+    v = _rng(seed, "v").standard_normal((B, Nk, w.Hkv, w.Dv), dtype=np.float32)
     do = _rng(seed, "do").standard_normal((B, N, w.Hq, w.Dv), dtype=np.float32)
     aux = _rng(seed, "aux")
     if w.transform in ("outlier", "outlier3"):
@@ -107,14 +115,13 @@ def generate(w: Workload, seed: int = 0):
         # (NeoX half-split, base 10000, position = token index); the key's rotary
         # part is one vector per (batch, token) shared by every head.
         nope = w.Dqk - 64
-        k_rope = aux.standard_normal((B, N, 1, 64), dtype=np.float32)
+        k_rope = aux.standard_normal((B, Nk, 1, 64), dtype=np.float32)
         k[..., nope:] = k_rope
-        pos = np.arange(N, dtype=np.float64)[:, None]
         inv = 10000.0 ** (-np.arange(0, 32, dtype=np.float64) * 2.0 / 64.0)
-        ang = pos * inv[None, :]
-        cos = np.cos(ang).astype(np.float32)[None, :, None, :]
-        sin = np.sin(ang).astype(np.float32)[None, :, None, :]
         for t in (q, k):
+            ang = np.arange(t.shape[1], dtype=np.float64)[:, None] * inv[None, :]
+            cos = np.cos(ang).astype(np.float32)[None, :, None, :]
+            sin = np.sin(ang).astype(np.float32)[None, :, None, :]
             x1 = t[..., nope:nope + 32].copy()
             x2 = t[..., nope + 32:].copy()
             t[..., nope:nope + 32] = x1 * cos - x2 * sin

@@ -38,7 +38,8 @@ def np64(t: torch.Tensor) -> np.ndarray:
 
 
 def problem(w: synth.Workload) -> pk.Problem:
-    return pk.Problem(w.B, w.N, w.Hq, w.Hkv, w.Dqk, w.Dv, float(np.float32(w.tau)))
+    return pk.Problem(w.B, w.N, w.Hq, w.Hkv, w.Dqk, w.Dv, float(np.float32(w.tau)), causal=int(w.causal),
+                      seqlen_kv=w.Nk)
 
 
 def bwd_plain_and_stats(p, mode, mq, mk, mv, mdo, lse, do=None, o=None, delta_in=None, grad_dtype=torch.float32):
@@ -88,7 +89,8 @@ def run_gpu(w, d, mode=pk.DELTA_MATCHING, grad_dtype=torch.float32, o_dtype=torc
 
 def run_oracle(w, d, mode=orc.DELTA_MATCHING, o_round=orc.ROUND_BF16, **kw):
     out, quant = orc.attention_from_inputs(d["q"], d["k"], d["v"], d["do"], float(np.float32(w.tau)),
-                                           delta_mode=mode, o_round=o_round, want_rowstats=True, **kw)
+                                           delta_mode=mode, o_round=o_round, want_rowstats=True,
+                                           causal=w.causal, **kw)
     out["quant"] = quant
     return out
 

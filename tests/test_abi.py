@@ -38,7 +38,11 @@ def _fake_mx(addr=4096):
 
 @pytest.mark.parametrize("kw,code", [
     (dict(dim_qk=96, dim_v=96), -2), (dict(dim_qk=128, dim_v=64), -2), (dict(seqlen=100), -2),
-    (dict(heads_q=3, heads_kv=2), -2), (dict(causal=0), -2), (dict(softmax_scale=float("nan")), -1),
+    (dict(heads_q=3, heads_kv=2), -2), (dict(causal=2), -1), (dict(softmax_scale=float("nan")), -1),
+    # the causal mask needs equal lengths; key lengths in blocks of 32; no keys without queries
+    (dict(seqlen_kv=256), -2), (dict(causal=0, seqlen_kv=100), -2), (dict(causal=0, seqlen_kv=-32), -1),
+    (dict(causal=0, seqlen=0, seqlen_kv=64), -2), (dict(causal=0, seqlen_kv=(1 << 30) + 32), -2),
+    (dict(causal=0, batch=512, heads_q=64, heads_kv=64, seqlen=32, seqlen_kv=1 << 15), -2),
     (dict(seqlen=-32), -1), (dict(heads_kv=0), -1),
     # one launch dimension holds fewer than 2^32 work-items: B Hq N < 2^31, B Hkv N < 2^30
     (dict(batch=1024, heads_q=64, heads_kv=64, seqlen=1 << 15), -2),
@@ -152,3 +156,28 @@ def test_producer_rejects_bad_arguments():
                                         None) == -1
     assert L.attn_fp8_quantize_producer(*args, 1.0, 1, ctypes.c_void_p(4096), None, ctypes.byref(m), 3, None,
                                         None) == -1
+
+
+def test_workspace_size_without_mask():
+    """Stored dQ operand units: causal problems keep the ones up to the
+    diagonal, sum over 32-query blocks q of floor(q/2) + 1; without the mask
+    every block has ceil(Nk / 64).  The K col scales per 64-key step follow
+    the key length."""
+    L = pk.lib()
+    r256 = lambda x: (x + 255) // 256 * 256
+
+    def ws(**kw):
+        p = _prob(**kw).c()
+        out = ctypes.c_size_t(0)
+        assert L.attn_fp8_bwd_workspace_size(ctypes.byref(p), ctypes.byref(out)) == 0, pk.last_error()
+        return out.value
+
+    def expect(B, N, Nk, Hq, Hkv, D, units):
+        nt = (N + 63) // 64
+        return (r256(B * Hq * units * 2048) + r256(B * Hq * units * 2) + r256(B * Hq * N * 8) +
+                r256(B * Hq * nt * 1024) + r256(B * Hq * nt * 4 * D) + r256(B * Hkv * ((Nk + 63) // 64) * 2 * D))
+    causal_units = sum(q // 2 + 1 for q in range(128 // 32))
+    assert ws() == expect(1, 128, 128, 2, 2, 128, causal_units)
+    assert ws(causal=0) == expect(1, 128, 128, 2, 2, 128, 4 * 2)
+    assert ws(causal=0, seqlen_kv=320) == expect(1, 128, 320, 2, 2, 128, 4 * 5)
+    assert ws(causal=0, seqlen=352, seqlen_kv=96) == expect(1, 352, 96, 2, 2, 128, 11 * 2)
