@@ -266,7 +266,8 @@ __device__ __forceinline__ TilePos next_pos(TilePos p, int G) {
   return p.hi + 1 < G ? TilePos{p.hi + 1, p.r} : TilePos{0, p.r + 1};
 }
 
-template <int DQK, int DV, bool STATS>
+// CAUSAL: the mask (key length = query length) or every key of Nk
+template <int DQK, int DV, bool STATS, bool CAUSAL>
 __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) {
   using C = BwdCfg<DQK, DV>;
   constexpr int KBW = C::KBW, BKB = C::BKB, BQ = C::BQ, NCB = C::NCB;
@@ -291,8 +292,8 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
   const int kbw = w % KBW;                      // this wave's 32-key block within the workgroup
   const int qs = w / KBW;                       // and its 32-query half of every tile
-  const int N = (int)a.N, Nk = (int)a.Nk;
-  const bool causal = a.causal != 0;
+  constexpr bool causal = CAUSAL;
+  const int N = (int)a.N, Nk = CAUSAL ? N : (int)a.Nk;
   // workgroup id -> key block (slowest, in the order of key_block_of) and
   // (batch, KV head) (fastest: the key blocks of one KV head get ids equal
   // mod 16, hence one XCD and its L2 when B * Hkv % 8 == 0)
@@ -607,7 +608,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
     if (w >= 2 * KSN) return;
     const int uq = w / KSN, ks = w % KSN;
     const int qb = i0 + 32 * uq;
-    if (qb >= N || kb0 + 64 * ks >= Nk || (causal && kb0 + 64 * ks > qb + 31)) return;
+    if (qb >= N || (CAUSAL ? kb0 + 64 * ks > qb + 31 : kb0 + 64 * ks >= Nk)) return;
     uint32_t ex2 = *reinterpret_cast<const uint16_t*>(es + uq * KBW + 2 * ks);
     asm volatile("" : "+v"(ex2));
     const int i16 = lane & 15;
@@ -908,8 +909,13 @@ static hipError_t bwd_dispatch(const AttnArgs& a0, hipStream_t s) {
   AttnArgs a = a0;
   const int64_t per_head = cus / (a.B * a.Hkv);
   a.bwd_cohort = (int)(per_head > 1 ? per_head : 1);
-  if (a.rowstats) hipLaunchKernelGGL((bwd_kernel<DQK, DV, true>), grid, dim3(C::NT), 0, s, a);
-  else hipLaunchKernelGGL((bwd_kernel<DQK, DV, false>), grid, dim3(C::NT), 0, s, a);
+  if (a.causal) {
+    if (a.rowstats) hipLaunchKernelGGL((bwd_kernel<DQK, DV, true, true>), grid, dim3(C::NT), 0, s, a);
+    else hipLaunchKernelGGL((bwd_kernel<DQK, DV, false, true>), grid, dim3(C::NT), 0, s, a);
+  } else {
+    if (a.rowstats) hipLaunchKernelGGL((bwd_kernel<DQK, DV, true, false>), grid, dim3(C::NT), 0, s, a);
+    else hipLaunchKernelGGL((bwd_kernel<DQK, DV, false, false>), grid, dim3(C::NT), 0, s, a);
+  }
   return hipGetLastError();
 }
 

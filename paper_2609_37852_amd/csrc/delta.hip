@@ -44,7 +44,8 @@ struct DeltaCfg {
   static constexpr int WGS = 2 * STAGE <= 80 * 1024 ? 2 : 1;
 };
 
-template <int DQK, int DV>
+// CAUSAL: the mask (key length = query length) or every key of Nk
+template <int DQK, int DV, bool CAUSAL>
 __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_kernel(AttnArgs a) {
   using C = DeltaCfg<DQK, DV>;
   constexpr int NW = C::NW, BQ = C::BQ, BK = C::BK;
@@ -54,8 +55,8 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
-  const int N = (int)a.N, Nk = (int)a.Nk;
-  const bool causal = a.causal != 0;
+  constexpr bool causal = CAUSAL;
+  const int N = (int)a.N, Nk = CAUSAL ? N : (int)a.Nk;
   const int nqb = (N + BQ - 1) / BQ;
   const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);
   const int qb = nqb - 1 - wc.r;              // longest causal rows first
@@ -219,7 +220,8 @@ static hipError_t delta_dispatch(const AttnArgs& a, hipStream_t s) {
   using C = DeltaCfg<DQK, DV>;
   const int64_t nqb = (a.N + C::BQ - 1) / C::BQ;
   const dim3 grid((unsigned)(nqb * a.Hq * a.B));
-  hipLaunchKernelGGL((delta_matching_kernel<DQK, DV>), grid, dim3(C::NT), 0, s, a);
+  if (a.causal) hipLaunchKernelGGL((delta_matching_kernel<DQK, DV, true>), grid, dim3(C::NT), 0, s, a);
+  else hipLaunchKernelGGL((delta_matching_kernel<DQK, DV, false>), grid, dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }
 

@@ -65,7 +65,9 @@ struct FwdCfg {
   static_assert(BQ % BK == 0, "a query block's diagonal starts a key tile");
 };
 
-template <int DQK, int DV>
+// CAUSAL: the mask (key length = query length) or every key of Nk; a
+// template parameter, so the causal kernel carries no key-length arithmetic
+template <int DQK, int DV, bool CAUSAL>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   using C = FwdCfg<DQK, DV>;
   constexpr int NW = C::NW, BQ = C::BQ, BK = C::BK;
@@ -75,8 +77,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   __shared__ int hot_slot;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
-  const int N = (int)a.N, Nk = (int)a.Nk;
-  const bool causal = a.causal != 0;
+  constexpr bool causal = CAUSAL;
+  const int N = (int)a.N, Nk = CAUSAL ? N : (int)a.Nk;
   const int nqb = (N + BQ - 1) / BQ;
   const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);
   const int qb = nqb - 1 - wc.r;              // longest causal rows first
@@ -260,8 +262,14 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   };
   auto tile = [&](const uint8_t* st, int j0) __attribute__((always_inline)) {
     if (!live || j0 >= klim) return;
-    if (causal ? j0 + BK <= q0 : j0 + BK <= Nk) tile_body(st, j0, std::true_type{});
-    else tile_body(st, j0, std::false_type{});
+    if constexpr (CAUSAL) {
+      if (j0 + BK <= q0) tile_body(st, j0, std::true_type{});
+      else tile_body(st, j0, std::false_type{});
+    } else {
+      // one body (its group tests pass on every tile but the last): the
+      // second body of the masked kernel does not fit the registers here
+      tile_body(st, j0, std::false_type{});
+    }
   };
 
   issue((lds8*)stA, 0);
@@ -314,7 +322,8 @@ static hipError_t fwd_dispatch(const AttnArgs& a, hipStream_t s) {
   using C = FwdCfg<DQK, DV>;
   const int64_t nqb = (a.N + C::BQ - 1) / C::BQ;
   const dim3 grid((unsigned)(nqb * a.Hq * a.B));
-  hipLaunchKernelGGL((fwd_kernel<DQK, DV>), grid, dim3(C::NT), 0, s, a);
+  if (a.causal) hipLaunchKernelGGL((fwd_kernel<DQK, DV, true>), grid, dim3(C::NT), 0, s, a);
+  else hipLaunchKernelGGL((fwd_kernel<DQK, DV, false>), grid, dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }
 
