@@ -17,9 +17,9 @@ the quantizer and the saved-output corrections, the main backward kernel's
 roofline, the paper's own timing protocol (App. C.2: clock warm-up, five
 interleaved rounds of the median of 20 timings after 5 warm-up calls, mean
 and standard error, pre-quantized inputs) for the matched and the stale
-backward, a whole step with the stale correction, the same on the d = 256
-workload, and the oracle's CPU rate.  `--gpus N` with N > 1 exits: this
-benchmark measures a single GPU.
+backward, a whole step with the stale correction, the same workload without
+the causal mask, the d = 256 workload, and the oracle's CPU rate.
+`--gpus N` with N > 1 exits: this benchmark measures a single GPU.
 """
 from __future__ import annotations
 
@@ -69,7 +69,7 @@ def read_traffic(path):
     return int(fields["bytes_per_launch"])
 
 
-def write_traffic_summary(fetch_csv, write_csv, out):
+def write_traffic_summary(fetch_csv, write_csv, out, calib_mib):
     """Calibrated HBM bytes per launch of bwd_kernel<128,128> from two
     rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE in KiB per dispatch) of
     `bench.py --copy-calibration MIB`, whose negate kernel reads and writes
@@ -82,7 +82,7 @@ def write_traffic_summary(fetch_csv, write_csv, out):
             if r["Counter_Name"] != counter:
                 continue
             name = r["Kernel_Name"]
-            if "bwd_kernel<128, 128, false>" in name:
+            if "bwd_kernel<128, 128, false, true>" in name:
                 vals["bwd"].append(float(r["Counter_Value"]))
             elif "neg" in name:
                 vals["copy"].append(float(r["Counter_Value"]))
@@ -90,10 +90,7 @@ def write_traffic_summary(fetch_csv, write_csv, out):
             raise RuntimeError(f"{path}: no {counter} rows for the backward or the calibration kernel")
         return float(np.mean(vals["bwd"])), float(np.mean(vals["copy"]))
 
-    calib = None
-    for line in open(os.path.join(os.path.dirname(fetch_csv), "..", "bench_traffic.log")):
-        if line.startswith("{"):
-            calib = json.loads(line)["copy_calibration_bytes"]
+    calib = calib_mib << 20
     fb, fc = per_kernel(fetch_csv, "FETCH_SIZE")
     wb, wc = per_kernel(write_csv, "WRITE_SIZE")
     f_scale, w_scale = calib / (fc * 1024), calib / (wc * 1024)
@@ -104,10 +101,9 @@ def write_traffic_summary(fetch_csv, write_csv, out):
 Commands (MI355X, ROCm 7.2, repository root; `cd /tmp && export TMPDIR=/tmp` first):
 
 ```
-python -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration 1024 > gpurun_out/bench_traffic.log
-rocprofv3 --kernel-include-regex "bwd_kernel|neg" --pmc FETCH_SIZE -d gpurun_out/tr_fetch -o run --output-format csv -- python -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration 1024
-rocprofv3 --kernel-include-regex "bwd_kernel|neg" --pmc WRITE_SIZE -d gpurun_out/tr_write -o run --output-format csv -- python -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration 1024
-python bench.py --traffic-summary gpurun_out/tr_fetch/run_counter_collection.csv gpurun_out/tr_write/run_counter_collection.csv
+rocprofv3 --kernel-include-regex "bwd_kernel|neg" --pmc FETCH_SIZE -d gpurun_out/tr_fetch -o run --output-format csv -- python -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-protocol --copy-calibration {calib_mib}
+rocprofv3 --kernel-include-regex "bwd_kernel|neg" --pmc WRITE_SIZE -d gpurun_out/tr_write -o run --output-format csv -- python -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-protocol --copy-calibration {calib_mib}
+python bench.py --traffic-summary gpurun_out/tr_fetch/run_counter_collection.csv gpurun_out/tr_write/run_counter_collection.csv --copy-calibration {calib_mib}
 ```
 
 The calibration kernel is a float32 negate over {calib} bytes (it reads and writes
@@ -181,14 +177,15 @@ class Runner:
         tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
         self.q, self.k, self.v, self.do = (torch.from_numpy(d[n]).to(tdt).to(dev) for n in ("q", "k", "v", "do"))
         del d
-        self.p = pk.Problem(w.B, w.N, w.Hq, w.Hkv, w.Dqk, w.Dv, float(np.float32(w.tau)))
+        self.p = pk.Problem(w.B, w.N, w.Hq, w.Hkv, w.Dqk, w.Dv, float(np.float32(w.tau)), causal=int(w.causal),
+                            seqlen_kv=w.Nk)
         self.mq, self.mk, self.mv, self.mdo = (pk.MX.empty(*t.shape, dev) for t in (self.q, self.k, self.v, self.do))
         self.o = torch.empty((w.B, w.N, w.Hq, w.Dv), dtype=torch.bfloat16, device=dev)
         self.lse = torch.empty((w.B, w.Hq, w.N), dtype=torch.float32, device=dev)
         self.delta = torch.empty((w.B, w.Hq, w.N, 2), dtype=torch.float32, device=dev)
         self.grads = (torch.empty((w.B, w.N, w.Hq, w.Dqk), dtype=torch.bfloat16, device=dev),
-                      torch.empty((w.B, w.N, w.Hkv, w.Dqk), dtype=torch.bfloat16, device=dev),
-                      torch.empty((w.B, w.N, w.Hkv, w.Dv), dtype=torch.bfloat16, device=dev))
+                      torch.empty((w.B, w.nk, w.Hkv, w.Dqk), dtype=torch.bfloat16, device=dev),
+                      torch.empty((w.B, w.nk, w.Hkv, w.Dv), dtype=torch.bfloat16, device=dev))
         self.ws = torch.empty(pk.attn_fp8_bwd_workspace_size(self.p), dtype=torch.uint8, device=dev)
         self.L = pk.lib()
         self.stream = torch.cuda.current_stream(dev).cuda_stream
@@ -349,7 +346,7 @@ def main():
                          "FETCH_SIZE / WRITE_SIZE calibrate the HBM counters)")
     args = ap.parse_args()
     if args.traffic_summary:
-        write_traffic_summary(*args.traffic_summary, TRAFFIC_SUMMARY)
+        write_traffic_summary(*args.traffic_summary, TRAFFIC_SUMMARY, args.copy_calibration or 1024)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the hot path runs on a "
@@ -449,9 +446,21 @@ def main():
         line["paper_protocol"] = run.protocol(args.clock_warmup)
         line["stale_step"] = run.full_step(pk.DELTA_STALE_ROWSUM)
         if args.workload == "gqa_d128_8k":
-            # the paper's other throughput shape: d = 256 (QK-norm workload), matched and stale
+            # the same workload without the causal mask (every query sees all
+            # 8192 keys; credited FLOPs count the full N x N products)
             del run
             torch.cuda.empty_cache()
+            wn = synth.with_shape(w, causal=False)
+            rn = Runner(wn, ev)
+            for _ in range(3):
+                rn.step()
+            torch.cuda.synchronize()
+            line["noncausal"] = {"workload": wn.name + " without the mask",
+                                 "matched_step": rn.full_step(pk.DELTA_MATCHING),
+                                 "paper_protocol": rn.protocol(0.0, rounds=3)}
+            del rn
+            torch.cuda.empty_cache()
+            # the paper's other throughput shape: d = 256 (QK-norm workload), matched and stale
             w3 = synth.WORKLOADS["gqa_d256_8k_qknorm"]
             r3 = Runner(w3, ev)
             for _ in range(3):
