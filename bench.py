@@ -17,8 +17,8 @@ the quantizer and the saved-output corrections, the main backward kernel's
 roofline, the paper's own timing protocol (App. C.2: clock warm-up, five
 interleaved rounds of the median of 20 timings after 5 warm-up calls, mean
 and standard error, pre-quantized inputs) for the matched and the stale
-backward, a whole step with the stale correction, the same workload without
-the causal mask, the d = 256 workload, and the oracle's CPU rate.
+backward, a whole step with the stale correction, the cost of the
+compensated matched correction, the same workload without the causal mask, the d = 256 workload, and the oracle's CPU rate.
 `--gpus N` with N > 1 exits: this benchmark measures a single GPU.
 """
 from __future__ import annotations
@@ -42,7 +42,7 @@ PEAK_HBM_GBS = 8000.0
 # WRITE_SIZE, calibrated with a plain copy kernel), valid only for the kernel
 # sources it was taken on.
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "bwd_kernel_gqa_d128_8k_traffic.md")
-BWD_SOURCES = ("bwd.hip", "dma.hpp", "common.hpp", "tiles.hpp", "kernels.hpp")
+BWD_SOURCES = ("bwd_main.hpp", "bwd_main_causal.hip", "dma.hpp", "common.hpp", "tiles.hpp", "kernels.hpp")
 
 
 def bwd_sources_sha256():
@@ -232,6 +232,18 @@ class Runner:
             self.step(m, mode=mode)
         self.torch.cuda.synchronize()
         return float(np.mean([self.ev.ms(m[2], m[3]) for m in ms_]))
+
+    def breakdown(self, mode, n=10):
+        """Mean times of the correction pass, the main backward kernel and
+        the whole step over n steps in the given mode (after 3 warm-ups)."""
+        for _ in range(3):
+            self.step(mode=mode)
+        ms_ = [self.ev.create(7) for _ in range(n)]
+        for m in ms_:
+            self.step(m, mode=mode)
+        self.torch.cuda.synchronize()
+        avg = lambda a, b: float(np.mean([self.ev.ms(m[a], m[b]) for m in ms_]))
+        return {"delta_ms": round(avg(2, 3), 4), "bwd_main_ms": round(avg(4, 5), 4), "step_ms": round(avg(0, 6), 4)}
 
     def timed(self, fn, warm=5, reps=20):
         """Median of `reps` event timings of fn() after `warm` calls."""
@@ -445,6 +457,10 @@ def main():
     if not args.no_protocol:
         line["paper_protocol"] = run.protocol(args.clock_warmup)
         line["stale_step"] = run.full_step(pk.DELTA_STALE_ROWSUM)
+        # the opt-in compensated matched correction against the plain one
+        cm, pm = run.breakdown(pk.DELTA_MATCHING_COMPENSATED), run.breakdown(pk.DELTA_MATCHING)
+        line["compensated"] = {"matching": pm, "compensated": cm,
+                               "step_over_matching": round(cm["step_ms"] / pm["step_ms"] - 1, 4)}
         if args.workload == "gqa_d128_8k":
             # the same workload without the causal mask (every query sees all
             # 8192 keys; credited FLOPs count the full N x N products)

@@ -198,7 +198,7 @@ int check_delta_inputs(const attn_fp8_problem* p, int mode, const attn_fp8_mx* q
                        int dout_dtype, const int64_t* dout_strides, const void* o, int o_dtype,
                        const int64_t* o_strides) {
   int rc;
-  if (mode == ATTN_FP8_DELTA_MATCHING) {
+  if (mode == ATTN_FP8_DELTA_MATCHING || mode == ATTN_FP8_DELTA_MATCHING_COMPENSATED) {
     if ((rc = check_mx("q", q, true, false)) || (rc = check_mx("k", k, true, false)) ||
         (rc = check_mx("v", v, true, false)) || (rc = check_mx("dout", dout, true, false)) ||
         (rc = check_ptr("lse", lse)))
@@ -224,8 +224,9 @@ int launch_delta(const attn_fp8_problem* p, int mode, const attn_fp8_mx* q, cons
                  const attn_fp8_mx* v, const attn_fp8_mx* dout, const float* lse, const void* dout_raw,
                  int dout_dtype, const int64_t* dout_strides, const void* o, int o_dtype,
                  const int64_t* o_strides, float* delta, hipStream_t stream) {
-  if (mode == ATTN_FP8_DELTA_MATCHING) {
+  if (mode == ATTN_FP8_DELTA_MATCHING || mode == ATTN_FP8_DELTA_MATCHING_COMPENSATED) {
     afp8::AttnArgs a = base_args(p);
+    a.comp = mode == ATTN_FP8_DELTA_MATCHING_COMPENSATED;
     set_row(q, a.q_code, a.q_scale);
     set_row(k, a.k_code, a.k_scale);
     set_row(v, a.v_code, a.v_scale);
@@ -373,8 +374,7 @@ int attn_fp8_delta(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx*
                    const int64_t o_strides[3], float* delta, hipStream_t stream) {
   int rc;
   if ((rc = check_problem(p))) return rc;
-  if (delta_mode != ATTN_FP8_DELTA_MATCHING && delta_mode != ATTN_FP8_DELTA_STALE_ROWSUM &&
-      delta_mode != ATTN_FP8_DELTA_CONSISTENT_DO)
+  if (delta_mode < ATTN_FP8_DELTA_MATCHING || delta_mode > ATTN_FP8_DELTA_MATCHING_COMPENSATED)
     return fail(ATTN_FP8_EINVAL, "unknown delta_mode %d", delta_mode);
   if (empty(p)) return ok();
   if ((rc = check_delta_inputs(p, delta_mode, q, k, v, dout, lse, dout_raw, dout_dtype, dout_strides, o, o_dtype,
@@ -404,6 +404,8 @@ int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q
                  hipStream_t stream) {
   int rc;
   if ((rc = check_problem(p))) return rc;
+  if (delta_mode < ATTN_FP8_DELTA_MATCHING || delta_mode > ATTN_FP8_DELTA_MATCHING_COMPENSATED)
+    return fail(ATTN_FP8_EINVAL, "unknown delta_mode %d", delta_mode);
   const int gs = dtype_size(grad_dtype);
   if (!gs) return fail(ATTN_FP8_EINVAL, "grad_dtype %d", grad_dtype);
   if (empty(p)) return ok();
@@ -462,6 +464,7 @@ int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q
     a.dqs[i] = dq_strides[i];
   }
   a.grad_bf16 = grad_dtype == ATTN_FP8_DTYPE_BF16;
+  a.comp = delta_mode == ATTN_FP8_DELTA_MATCHING_COMPENSATED;
   a.rowstats = rowstats;
   a.rows = rows;
   a.tile_cs = tile_cs;

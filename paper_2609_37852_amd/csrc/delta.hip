@@ -7,7 +7,9 @@
 // FP64, and delta is stored as an FP32 pair (hi, lo) with hi + lo the FP64
 // quotient to about 2^-48.  Dividing by sum P makes the pair the exact
 // centring constant of the P the backward recomputes, even where the stored
-// LSE leaves sum P a few ulp away from 1.
+// LSE leaves sum P a few ulp away from 1.  Compensated variant (COMP): every
+// product P dP is formed exactly in FP64 and all sums run in FP64, so delta
+// carries no FP32 rounding of the terms it cancels.
 //
 // Workgroup: NW waves x 32 queries of one (batch, query head); 128-key tiles
 // of K and V (row copies) reach LDS by direct loads, double-buffered, so the
@@ -44,8 +46,9 @@ struct DeltaCfg {
   static constexpr int WGS = 2 * STAGE <= 80 * 1024 ? 2 : 1;
 };
 
-// CAUSAL: the mask (key length = query length) or every key of Nk
-template <int DQK, int DV, bool CAUSAL>
+// CAUSAL: the mask (key length = query length) or every key of Nk; COMP:
+// FP64 products and sums
+template <int DQK, int DV, bool CAUSAL, bool COMP>
 __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_kernel(AttnArgs a) {
   using C = DeltaCfg<DQK, DV>;
   constexpr int NW = C::NW, BQ = C::BQ, BK = C::BK;
@@ -151,6 +154,23 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   // 32 g + 8 (r/4) + 4 hf + r % 4 of the tile, query qi.
   auto group_sums = [&](const v16f& s, const v16f& dp, auto diag_tag) __attribute__((always_inline)) {
     constexpr bool DIAG = decltype(diag_tag)::value;
+    if constexpr (COMP) {
+      double qn = 0.0, qd = 0.0;
+#pragma unroll
+      for (int q4 = 0; q4 < 4; q4++) {
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+          const int r = 4 * q4 + e;
+          float p = bwd_prob(s[r], a.c);
+          if (DIAG) p = (8 * q4 + 4 * hf + e) > li ? 0.f : p;
+          qn = __builtin_fma((double)p, (double)dp[r], qn);   // the product is exact in FP64
+          qd += (double)p;
+        }
+      }
+      num += qn + __shfl_xor(qn, 32);
+      den += qd + __shfl_xor(qd, 32);
+      return;
+    }
     float pn = 0.f, pd = 0.f;
 #pragma unroll
     for (int q4 = 0; q4 < 4; q4++) {
@@ -220,8 +240,13 @@ static hipError_t delta_dispatch(const AttnArgs& a, hipStream_t s) {
   using C = DeltaCfg<DQK, DV>;
   const int64_t nqb = (a.N + C::BQ - 1) / C::BQ;
   const dim3 grid((unsigned)(nqb * a.Hq * a.B));
-  if (a.causal) hipLaunchKernelGGL((delta_matching_kernel<DQK, DV, true>), grid, dim3(C::NT), 0, s, a);
-  else hipLaunchKernelGGL((delta_matching_kernel<DQK, DV, false>), grid, dim3(C::NT), 0, s, a);
+  if (a.causal) {
+    if (a.comp) hipLaunchKernelGGL((delta_matching_kernel<DQK, DV, true, true>), grid, dim3(C::NT), 0, s, a);
+    else hipLaunchKernelGGL((delta_matching_kernel<DQK, DV, true, false>), grid, dim3(C::NT), 0, s, a);
+  } else {
+    if (a.comp) hipLaunchKernelGGL((delta_matching_kernel<DQK, DV, false, true>), grid, dim3(C::NT), 0, s, a);
+    else hipLaunchKernelGGL((delta_matching_kernel<DQK, DV, false, false>), grid, dim3(C::NT), 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -181,3 +181,22 @@ def test_workspace_size_without_mask():
     assert ws(causal=0) == expect(1, 128, 128, 2, 2, 128, 4 * 2)
     assert ws(causal=0, seqlen_kv=320) == expect(1, 128, 320, 2, 2, 128, 4 * 5)
     assert ws(causal=0, seqlen=352, seqlen_kv=96) == expect(1, 352, 96, 2, 2, 128, 11 * 2)
+
+
+def test_unknown_delta_mode_rejected():
+    """Modes 0..3 (matched, stale, consistent dO, compensated matched); others
+    are rejected by the correction and by the backward, even with delta_in."""
+    L = pk.lib()
+    p = _prob().c()
+    m = _fake_mx()
+    st = bd._I64x3(128 * 2 * 128, 2 * 128, 128)
+    vp = ctypes.c_void_p(4096)
+    for mode in (-1, 4):
+        rc = L.attn_fp8_delta(ctypes.byref(p), mode, ctypes.byref(m), ctypes.byref(m), ctypes.byref(m),
+                              ctypes.byref(m), vp, vp, 1, st, vp, 1, st, vp, None)
+        assert rc == -1 and "delta_mode" in pk.last_error()
+        rc = L.attn_fp8_bwd(ctypes.byref(p), mode, ctypes.byref(m), ctypes.byref(m), ctypes.byref(m),
+                            ctypes.byref(m), vp, vp, 1, st, vp, 1, st, vp, vp, vp, vp, 1, st, st, st,
+                            ctypes.c_void_p(1 << 20), 1 << 30, None, None, None)
+        assert rc == -1 and "delta_mode" in pk.last_error()
+    assert pk.DELTA_MATCHING_COMPENSATED == 3
