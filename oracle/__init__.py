@@ -24,7 +24,7 @@ _dp = ctypes.POINTER(ctypes.c_double)
 _u8p = ctypes.POINTER(ctypes.c_uint8)
 _i32p = ctypes.POINTER(ctypes.c_int32)
 
-EXACT_PFWD, EXACT_PBWD, EXACT_DS = 1, 2, 4
+EXACT_PFWD, EXACT_PBWD, EXACT_DS, MX_PBWD = 1, 2, 4, 8
 EXACT_ALL = EXACT_PFWD | EXACT_PBWD | EXACT_DS
 DELTA_MATCHING, DELTA_STALE_ROWSUM, DELTA_CONSISTENT_DO = 0, 1, 2
 ROUND_NONE, ROUND_F32, ROUND_BF16 = 0, 1, 2
@@ -63,7 +63,7 @@ def lib():
         L.orc_dequantize.argtypes = [_u8p] * 4 + [ctypes.c_int64] * 4 + [_dp, _dp]
         L.orc_producer.argtypes = [_dp] + [ctypes.c_int64] * 4 + [ctypes.c_double, ctypes.c_int, _dp, _dp]
         L.orc_attention.restype = ctypes.c_int
-        L.orc_attention.argtypes = ([ctypes.POINTER(_Problem)] + [ctypes.c_int] * 4 + [_dp] * 22
+        L.orc_attention.argtypes = ([ctypes.POINTER(_Problem)] + [ctypes.c_int] * 4 + [_dp] * 23
                                     + [ctypes.c_int64, ctypes.c_int])
         _LIB = L
     return _LIB
@@ -187,11 +187,13 @@ def attention(B, N, Hq, Hkv, Dqk, Dv, tau, ops, dO_raw=None, *, flags=0, delta_m
     out["phat"] = np.zeros((B, Hq, N, Nk)) if want_phat else None
     out["dsraw"] = np.zeros((B, Hq, N, Nk)) if want_ds else None
     out["dshat"] = np.zeros((B, Hq, N, Nk)) if want_ds else None
+    out["pbhat"] = np.zeros((B, Hq, N, Nk)) if want_ds else None
     rc = L.orc_attention(ctypes.byref(pr), flags, delta_mode, o_round, grad_round,
                          *[_ptr(arrs[k]) for k in names], _ptr(dO_raw), _ptr(delta_in), _ptr(lse_in),
                          _ptr(out["O"]), _ptr(out["O_unrounded"]), _ptr(out["LSE"]), _ptr(out["delta"]),
                          _ptr(out["dQ"]), _ptr(out["dK"]), _ptr(out["dV"]), _ptr(out["rowstats"]),
-                         _ptr(out["phat"]), _ptr(out["dsraw"]), _ptr(out["dshat"]), int(row_lo), int(nthreads))
+                         _ptr(out["phat"]), _ptr(out["dsraw"]), _ptr(out["dshat"]), _ptr(out["pbhat"]), int(row_lo),
+                         int(nthreads))
     if rc != 0:
         raise ValueError(f"orc_attention failed ({rc})")
     return out

@@ -38,6 +38,9 @@
  *   R11 consistent-dO correction: the stale correction with the raw dO
  *      replaced by its dequantized row copy (the operand of dP), the stored
  *      O unchanged: sum_c dO^_ic O_ic.
+ *   R15 (a variant, not the paper's kernel; ORC_MX_PBWD): the backward
+ *      probability operand cast like dS' (R7), one power-of-two scale per
+ *      aligned 32x32 block from its largest P, instead of the fixed 2^-8.
  *   R10 causal mask is top-left aligned (key j visible to query i iff j <= i,
  *      equal query and key lengths); without the mask (causal == 0) every
  *      query sees all Nk keys and the key length may differ from the query
@@ -295,13 +298,14 @@ typedef struct {
 
 /* One aligned 32x32 tile of the backward (query rows i0.., keys j0..):
  * P and dS = P (dP - delta) before any cast (zero for masked j > i when
- * causal), the
- * backward probability operand P' = C8(256 P) 2^-8 (R6) and the dS operand
- * dS' cast with one power-of-two scale for the whole tile (R7). */
+ * causal), the backward probability operand P' = C8(256 P) 2^-8 (R6; with
+ * ORC_MX_PBWD, R15: C8(P 2^-e) 2^e with e from the tile's largest P by R2's
+ * rule) and the dS operand dS' cast with one power-of-two scale for the whole
+ * tile (R7). */
 static void tile(const tile_ctx* c, int64_t b, int64_t h, int64_t i0, int64_t nr, int64_t j0,
                  int64_t nc, double P[32][32], double dS[32][32], double Pb[32][32], double dSh[32][32]) {
   const int64_t kh = h / c->G;
-  double amax = 0.0;
+  double amax = 0.0, pmax = 0.0;
   for (int64_t r = 0; r < 32; r++)
     for (int64_t t = 0; t < 32; t++) {
       const int64_t i = i0 + r, j = j0 + t;
@@ -314,12 +318,14 @@ static void tile(const tile_ctx* c, int64_t b, int64_t h, int64_t i0, int64_t nr
       P[r][t] = pij;
       dS[r][t] = pij * (dpij - c->delta[(b * c->Hq + h) * c->N + i]);
       if (fabs(dS[r][t]) > amax) amax = fabs(dS[r][t]);
+      if (pij > pmax) pmax = pij;
     }
   const int e = orc_pow2_exponent(amax);
+  const int ep = (c->flags & ORC_MX_PBWD) ? orc_pow2_exponent(pmax) : -8;
   for (int64_t r = 0; r < 32; r++)
     for (int64_t t = 0; t < 32; t++) {
       Pb[r][t] = (c->flags & ORC_EXACT_PBWD) ? P[r][t]
-                                             : ldexp(orc_e4m3_value(orc_e4m3_round(256.0 * P[r][t])), -8);
+                                             : ldexp(orc_e4m3_value(orc_e4m3_round(ldexp(P[r][t], -ep))), ep);
       dSh[r][t] = (c->flags & ORC_EXACT_DS) ? dS[r][t]
                                             : ldexp(orc_e4m3_value(orc_e4m3_round(ldexp(dS[r][t], -e))), e);
     }
@@ -332,8 +338,8 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
                   const double* dO_raw, const double* delta_in, const double* lse_in,
                   double* O, double* O_unrounded, double* LSE, double* delta,
                   double* dQ, double* dK, double* dV,
-                  double* rowstats, double* phat, double* dsraw, double* dshat, int64_t row_lo,
-                  int nthreads) {
+                  double* rowstats, double* phat, double* dsraw, double* dshat, double* pbhat,
+                  int64_t row_lo, int nthreads) {
   const int64_t B = p->B, N = p->N, Nk = p->Nk, Hq = p->Hq, Hkv = p->Hkv, Dqk = p->Dqk, Dv = p->Dv;
   const int causal = p->causal;
   const double tau = p->tau;
@@ -354,6 +360,7 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
   if (phat) memset(phat, 0, sizeof(double) * (size_t)(B * Hq * N * Nk));
   if (dshat) memset(dshat, 0, sizeof(double) * (size_t)(B * Hq * N * Nk));
   if (dsraw) memset(dsraw, 0, sizeof(double) * (size_t)(B * Hq * N * Nk));
+  if (pbhat) memset(pbhat, 0, sizeof(double) * (size_t)(B * Hq * N * Nk));
 
   /* ---- forward (Sec. 2.3; App. B.6.2 with reading R5) ---- */
 #pragma omp parallel
@@ -489,6 +496,7 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
               spc[r] += Pb[r][t];
               if (dsraw) dsraw[((b * Hq + h) * N + i) * Nk + j] = dS[r][t];
               if (dshat) dshat[((b * Hq + h) * N + i) * Nk + j] = g;
+              if (pbhat) pbhat[((b * Hq + h) * N + i) * Nk + j] = Pb[r][t];
               const double* kc = Kc + ((b * Hkv + kh) * Nk + j) * Dqk;
               for (int64_t c = 0; c < Dqk; c++) dq[r][c] += g * kc[c];
             }

@@ -64,7 +64,10 @@ typedef struct {
 
 enum { ORC_EXACT_PFWD = 1,    /* forward probabilities are not cast to FP8 */
        ORC_EXACT_PBWD = 2,    /* backward (dV) probabilities are not cast */
-       ORC_EXACT_DS   = 4 };  /* dS is not cast */
+       ORC_EXACT_DS   = 4,    /* dS is not cast */
+       ORC_MX_PBWD    = 8 };  /* backward probabilities cast with one power-of-two
+                                 scale per aligned 32x32 block (a variant, R15)
+                                 instead of the fixed 2^-8 */
 enum { ORC_DELTA_MATCHING = 0, ORC_DELTA_STALE_ROWSUM = 1, ORC_DELTA_CONSISTENT_DO = 2 };
 enum { ORC_ROUND_NONE = 0, ORC_ROUND_F32 = 1, ORC_ROUND_BF16 = 2 };
 
@@ -95,9 +98,10 @@ enum { ORC_ST_SUM_DS = 0,      /* sum_j dS_ij (pre-cast)            */
  * j >= row_lo (dK, dV): by causality those depend on no other rows or keys'
  * outputs, so they come out exactly as in the whole problem; the rest of
  * the outputs are left untouched.
- * phat / dsraw / dshat (nullable, [B,Hq,N,Nk]) receive the normalized forward
- * probabilities actually used for O, dS before and after the FP8 cast
- * (tiny problems only).
+ * phat / dsraw / dshat / pbhat (nullable, [B,Hq,N,Nk]) receive the
+ * normalized forward probabilities actually used for O, dS before and after
+ * the FP8 cast, and the backward probability operand P' of dV (tiny problems
+ * only).
  * Returns 0, or -1 on invalid geometry. */
 int orc_attention(const orc_problem* p, int flags, int delta_mode,
                   int o_round, int grad_round,
@@ -106,8 +110,8 @@ int orc_attention(const orc_problem* p, int flags, int delta_mode,
                   const double* dO_raw, const double* delta_in, const double* lse_in,
                   double* O, double* O_unrounded, double* LSE, double* delta,
                   double* dQ, double* dK, double* dV,
-                  double* rowstats, double* phat, double* dsraw, double* dshat, int64_t row_lo,
-                  int nthreads);
+                  double* rowstats, double* phat, double* dsraw, double* dshat, double* pbhat,
+                  int64_t row_lo, int nthreads);
 
 #ifdef __cplusplus
 }
