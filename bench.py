@@ -42,7 +42,7 @@ PEAK_HBM_GBS = 8000.0
 # WRITE_SIZE, calibrated with a plain copy kernel), valid only for the kernel
 # sources it was taken on.
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "bwd_kernel_gqa_d128_8k_traffic.md")
-BWD_SOURCES = ("bwd_main.hpp", "bwd_main_causal.hip", "dma.hpp", "common.hpp", "tiles.hpp", "kernels.hpp")
+BWD_SOURCES = ("bwd_main.hpp", "bwd_main_causal_v0.hip", "dma.hpp", "common.hpp", "tiles.hpp", "kernels.hpp")
 
 
 def bwd_sources_sha256():
@@ -82,7 +82,7 @@ def write_traffic_summary(fetch_csv, write_csv, out, calib_mib):
             if r["Counter_Name"] != counter:
                 continue
             name = r["Kernel_Name"]
-            if "bwd_kernel<128, 128, false, true>" in name:
+            if "bwd_kernel<128, 128, false, true, 0>" in name:
                 vals["bwd"].append(float(r["Counter_Value"]))
             elif "neg" in name:
                 vals["copy"].append(float(r["Counter_Value"]))

@@ -97,6 +97,17 @@ typedef enum {
 
 enum { ATTN_FP8_QUANT_ROW = 1, ATTN_FP8_QUANT_COL = 2, ATTN_FP8_QUANT_BOTH = 3 };
 
+/* Numerics options of a problem (attn_fp8_problem.flags). */
+enum {
+  /* Backward probability operand of dV cast with one power-of-two scale per
+   * aligned 32x32 (query x key) block, chosen from the block's largest P as
+   * for dS', instead of the fixed scale 2^-8 of App. B.6.3.  A variant, not
+   * the paper's kernel: the fixed scale keeps probabilities below 2^-14 in
+   * E4M3's subnormal range (one or two significant bits, zero below 2^-17),
+   * the block scale keeps three mantissa bits at any magnitude. */
+  ATTN_FP8_FLAG_PBWD_BLOCK_SCALED = 1
+};
+
 /* Problem geometry, read-only.  softmax_scale (tau, e.g. 1/sqrt(dim_qk))
  * multiplies the FP32 score accumulator S = Q K^T. */
 typedef struct {
@@ -104,6 +115,7 @@ typedef struct {
   int32_t causal;          /* 1: top-left causal mask (seqlen_kv == seqlen); 0: no mask */
   float softmax_scale;
   int64_t seqlen_kv;       /* key / value length; 0 stands for seqlen */
+  int32_t flags;           /* ATTN_FP8_FLAG_* (0: the paper's numerics) */
 } attn_fp8_problem;
 
 /* One MX-quantized operand X of shape [B, N, H, D]; device memory, caller-owned.

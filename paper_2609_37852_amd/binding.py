@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libattn_fp8.so")
 
 DTYPE_F32, DTYPE_BF16 = 0, 1
 DELTA_MATCHING, DELTA_STALE_ROWSUM, DELTA_CONSISTENT_DO, DELTA_MATCHING_COMPENSATED = 0, 1, 2, 3
+FLAG_PBWD_BLOCK_SCALED = 1
 QUANT_ROW, QUANT_COL, QUANT_BOTH = 1, 2, 3
 # fields of the backward's per-row statistics [B, Hq, N, ROWSTATS] (FP64)
 RS_SUM_DS, RS_SUMABS_DS, RS_SUM_DSCAST, RS_MAXABS_DS, RS_SUMABS_DSCAST, RS_MAX_PDP, RS_SUM_PCAST = range(7)
@@ -37,7 +38,8 @@ class AttnFp8Error(RuntimeError):
 class _Problem(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int64), ("seqlen", ctypes.c_int64), ("heads_q", ctypes.c_int64),
                 ("heads_kv", ctypes.c_int64), ("dim_qk", ctypes.c_int64), ("dim_v", ctypes.c_int64),
-                ("causal", ctypes.c_int32), ("softmax_scale", ctypes.c_float), ("seqlen_kv", ctypes.c_int64)]
+                ("causal", ctypes.c_int32), ("softmax_scale", ctypes.c_float), ("seqlen_kv", ctypes.c_int64),
+                ("flags", ctypes.c_int32)]
 
 
 class _MX(ctypes.Structure):
@@ -120,6 +122,7 @@ class Problem:
     softmax_scale: float
     causal: int = 1
     seqlen_kv: int = 0          # key / value length; 0 stands for seqlen
+    flags: int = 0              # FLAG_* numerics options
 
     @property
     def nk(self) -> int:
@@ -127,7 +130,7 @@ class Problem:
 
     def c(self):
         return _Problem(self.batch, self.seqlen, self.heads_q, self.heads_kv, self.dim_qk, self.dim_v,
-                        self.causal, self.softmax_scale, self.seqlen_kv)
+                        self.causal, self.softmax_scale, self.seqlen_kv, self.flags)
 
 
 @dataclass

@@ -94,6 +94,7 @@ int check_problem(const attn_fp8_problem* p) {
     return fail(ATTN_FP8_EUNSUPPORTED, "head dims (%lld, %lld) not instantiated", (long long)p->dim_qk,
                 (long long)p->dim_v);
   if (p->causal != 0 && p->causal != 1) return fail(ATTN_FP8_EINVAL, "causal must be 0 or 1");
+  if (p->flags & ~ATTN_FP8_FLAG_PBWD_BLOCK_SCALED) return fail(ATTN_FP8_EINVAL, "unknown flags 0x%x", p->flags);
   if (p->seqlen_kv < 0) return fail(ATTN_FP8_EINVAL, "negative seqlen_kv");
   const int64_t nk = kv_len(p);
   if (p->causal && nk != p->seqlen)
@@ -138,6 +139,7 @@ afp8::AttnArgs base_args(const attn_fp8_problem* p) {
   a.G = p->heads_q / p->heads_kv;
   a.Nk = kv_len(p);
   a.causal = p->causal;
+  a.pmx = (p->flags & ATTN_FP8_FLAG_PBWD_BLOCK_SCALED) != 0;
   a.tau = p->softmax_scale;
   a.c = (float)((double)p->softmax_scale * 1.4426950408889634);
   return a;

@@ -198,9 +198,16 @@ static hipError_t bwd_dispatch(const AttnArgs& a0, hipStream_t s) {
   AttnArgs a = a0;
   const int64_t per_head = cus / (a.B * a.Hkv);
   a.bwd_cohort = (int)(per_head > 1 ? per_head : 1);
-  if (a.causal) return a.comp ? launch_bwd_main<true, true>(a, DQK, DV, grid, s)
-                              : launch_bwd_main<true, false>(a, DQK, DV, grid, s);
-  return a.comp ? launch_bwd_main<false, true>(a, DQK, DV, grid, s) : launch_bwd_main<false, false>(a, DQK, DV, grid, s);
+  switch ((a.causal ? 4 : 0) | (a.pmx ? 2 : 0) | (a.comp ? 1 : 0)) {
+    case 0: return launch_bwd_main<false, 0>(a, DQK, DV, grid, s);
+    case 1: return launch_bwd_main<false, 1>(a, DQK, DV, grid, s);
+    case 2: return launch_bwd_main<false, 2>(a, DQK, DV, grid, s);
+    case 3: return launch_bwd_main<false, 3>(a, DQK, DV, grid, s);
+    case 4: return launch_bwd_main<true, 0>(a, DQK, DV, grid, s);
+    case 5: return launch_bwd_main<true, 1>(a, DQK, DV, grid, s);
+    case 6: return launch_bwd_main<true, 2>(a, DQK, DV, grid, s);
+    default: return launch_bwd_main<true, 3>(a, DQK, DV, grid, s);
+  }
 }
 
 hipError_t launch_bwd_prep(const AttnArgs& a, int dqk, int dv, hipStream_t s) {

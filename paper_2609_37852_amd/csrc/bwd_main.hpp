@@ -30,8 +30,9 @@
 //        formation): the rounding error of fl(P (-delta_hi)), recovered
 //        exactly by an fma, and P (-delta_lo) are added back, so the error of
 //        dS scales with dS itself rather than with P |dP|.
-//   P' = C8(256 P) with scale 2^-8;  dS' = C8(dS / 2^e) with one exponent e
-//        per aligned 32x32 block (the wave's 32 keys x 32 queries).
+//   P' = C8(256 P) with scale 2^-8 (PMX: C8(P / 2^ep), one exponent ep per
+//        aligned 32x32 block from its largest P);  dS' = C8(dS / 2^e) with one
+//        exponent e per aligned 32x32 block (the wave's 32 keys x 32 queries).
 //   dV += P'^T dO_col,  dK += dS'^T Q_col   (A = the codes after one
 //                             v_permlane32_swap per dword pair puts each
 //                             lane's 16 queries in natural order).
@@ -271,9 +272,10 @@ __device__ __forceinline__ TilePos next_pos(TilePos p, int G) {
   return p.hi + 1 < G ? TilePos{p.hi + 1, p.r} : TilePos{0, p.r + 1};
 }
 
-// CAUSAL: the mask (key length = query length) or every key of Nk; COMP:
-// compensated dS formation
-template <int DQK, int DV, bool STATS, bool CAUSAL, bool COMP>
+// CAUSAL: the mask (key length = query length) or every key of Nk; VAR:
+// numerics variant, bit 0 compensated dS formation (COMP), bit 1 block-scaled
+// backward probability operand (PMX)
+template <int DQK, int DV, bool STATS, bool CAUSAL, int VAR>
 __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) {
   using C = BwdCfg<DQK, DV>;
   constexpr int KBW = C::KBW, BKB = C::BKB, BQ = C::BQ, NCB = C::NCB;
@@ -287,8 +289,11 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   __shared__ __attribute__((aligned(16))) uint8_t cB[NCB == 2 ? C::CSTAGE : 16];
   __shared__ __attribute__((aligned(16))) uint8_t dsA[BKB * C::DST];
   __shared__ __attribute__((aligned(16))) uint8_t dsB[BKB * C::DST];
-  __shared__ __attribute__((aligned(16))) uint8_t esA[KBW * 2];
-  __shared__ __attribute__((aligned(16))) uint8_t esB[KBW * 2];
+  constexpr bool COMP = (VAR & 1) != 0, PMX = (VAR & 2) != 0;
+  // block exponents + 127 of the two query halves: dS' at [half][kbw], P'
+  // (PMX) at 2 KBW + [half][kbw]
+  __shared__ __attribute__((aligned(16))) uint8_t esA[KBW * 4];
+  __shared__ __attribute__((aligned(16))) uint8_t esB[KBW * 4];
   // code exchange within a key block, 16 bytes per lane in natural query
   // order: [0] dS' of the first half (for dK), [1] P' of the second (for dV)
   __shared__ __attribute__((aligned(16))) uint4 xA[2][KBW * 64];
@@ -395,6 +400,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   v16f s, dp;
   v4i pn = v4i{0, 0, 0, 0}, dn = v4i{0, 0, 0, 0};   // this half's P' / dS' codes, natural query order
   int e = -127;                                      // and the dS' block exponent
+  int ep = -8;                                       // and the P' block exponent (PMX)
   v4i mine = v4i{0, 0, 0, 0};                        // this wave's operand codes for dV (P') or dK (dS')
 
   // P, dS and their codes from the shifted s, dp; EDGE tiles may skip the
@@ -403,6 +409,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
     constexpr bool EDGE = decltype(edge_tag)::value;
     v4i pc, dc;
     e = -127;
+    ep = -8;
     if (EDGE && skip) {
       pn = v4i{0, 0, 0, 0};
       dn = v4i{0, 0, 0, 0};
@@ -410,6 +417,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
     }
     // lane holds queries qb + 8 g + 4 hf + e4 (accumulator r = 4 g + e4)
     float amax = 0.f;
+    [[maybe_unused]] float pmax = 0.f;
     float pdp[16];   // |P dP| (row statistics only)
 #pragma unroll
     for (int g = 0; g < 4; g++) {
@@ -430,6 +438,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
         float p = bwd_prob(s[r], c);
         if (EDGE && causal && qb == kw0) p = (li > 8 * g + 4 * hf + e4) ? 0.f : p;   // diagonal block: key > query
         s[r] = p;
+        if constexpr (PMX) pmax = fmaxf(pmax, p);
         if constexpr (STATS) pdp[r] = fabsf(p * dp[r]);
         if constexpr (COMP) {
           const float pd = p * ndv[e4];                        // fl(P (-delta_hi))
@@ -442,9 +451,15 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
         amax = fmaxf(amax, fabsf(dp[r]));
       }
     }
+    float scp = 0.00390625f;   // the P' scale: 2^-8, or the block's (PMX)
+    if constexpr (PMX) {
+      ep = pow2_exponent(wave_max_nonneg(pmax));
+      ep = ep < -126 ? -126 : ep;
+      scp = exp2i(ep);
+    }
 #pragma unroll
     for (int k = 0; k < 4; k++)
-      pc[k] = (int)cvt4_div(s[4 * k], s[4 * k + 1], s[4 * k + 2], s[4 * k + 3], 0.00390625f);
+      pc[k] = (int)cvt4_div(s[4 * k], s[4 * k + 1], s[4 * k + 2], s[4 * k + 3], scp);
     e = pow2_exponent(wave_max_nonneg(amax));
     e = e < -126 ? -126 : e;
     const float sc = exp2i(e);
@@ -457,7 +472,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
 #pragma unroll
       for (int r = 0; r < 16; r++) {
         const float cast = fp8_value((uint32_t)dc[r >> 2], r & 3) * sc;
-        const float pcast = fp8_value((uint32_t)pc[r >> 2], r & 3) * 0.00390625f;
+        const float pcast = fp8_value((uint32_t)pc[r >> 2], r & 3) * scp;
         const double s0 = half_sum_d((double)dp[r]);
         const double s1 = half_sum_d((double)fabsf(dp[r]));
         const double s2 = half_sum_d((double)cast);
@@ -498,7 +513,10 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
     // dS' codes for the dQ units and the exchange with the other half
     *reinterpret_cast<uint4*>(ds + (32 * kbw + li) * C::DST + 32 * qs + 16 * hf) =
         make_uint4((uint32_t)dn[0], (uint32_t)dn[1], (uint32_t)dn[2], (uint32_t)dn[3]);
-    if (lane == 0) es[qs * KBW + kbw] = (uint8_t)(e + 127);
+    if (lane == 0) {
+      es[qs * KBW + kbw] = (uint8_t)(e + 127);
+      if constexpr (PMX) es[2 * KBW + qs * KBW + kbw] = (uint8_t)(ep + 127);
+    }
     const v4i xv = qs == 0 ? dn : pn;
     x[qs][kbw * 64 + lane] = make_uint4((uint32_t)xv[0], (uint32_t)xv[1], (uint32_t)xv[2], (uint32_t)xv[3]);
     mine = qs == 0 ? pn : dn;
@@ -537,7 +555,10 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
     const int qrow = 32 * qs + li;
     const uint4 o = x[1 - qs][kbw * 64 + lane];
     const v8i A = v8i{mine[0], mine[1], mine[2], mine[3], (int)o.x, (int)o.y, (int)o.z, (int)o.w};
-    const int ascale = qs == 0 ? 127 - 8 : (hf ? (int)es[kbw] : e + 127);
+    // A scale of the lane half: own block (hf = 0) or the other half's
+    int ascale;
+    if constexpr (PMX) ascale = hf ? (int)es[(qs == 0 ? 3 * KBW : 0) + kbw] : (qs == 0 ? ep : e) + 127;
+    else ascale = qs == 0 ? 127 - 8 : (hf ? (int)es[kbw] : e + 127);
     const uint8_t* Bt = Cc + (qs ? C::QC_OFF : C::OC_OFF);
     const uint8_t* Bs = Cc + (qs ? C::QCS_OFF : C::OCS_OFF);
     const int nb = qs ? CK : CV;
@@ -741,17 +762,17 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   }
 }
 
-// Launch of the main backward kernel for one (mask, compensation) variant;
-// each variant is instantiated in a translation unit of its own (they
-// compile in parallel), the row statistics and the head dims at run time.
-template <bool CAUSAL, bool COMP>
+// Launch of the main backward kernel for one (mask, numerics) variant; each
+// variant is instantiated in a translation unit of its own (they compile in
+// parallel), the row statistics and the head dims at run time.
+template <bool CAUSAL, int VAR>
 hipError_t launch_bwd_main(const AttnArgs& a, int dqk, int dv, dim3 grid, hipStream_t s) {
 #define AFP8_BWD_GO(Q, V)                                                                                   \
   if (dqk == Q && dv == V) {                                                                                \
     if (a.rowstats)                                                                                         \
-      hipLaunchKernelGGL((bwd_kernel<Q, V, true, CAUSAL, COMP>), grid, dim3(BwdCfg<Q, V>::NT), 0, s, a);    \
+      hipLaunchKernelGGL((bwd_kernel<Q, V, true, CAUSAL, VAR>), grid, dim3(BwdCfg<Q, V>::NT), 0, s, a);     \
     else                                                                                                    \
-      hipLaunchKernelGGL((bwd_kernel<Q, V, false, CAUSAL, COMP>), grid, dim3(BwdCfg<Q, V>::NT), 0, s, a);   \
+      hipLaunchKernelGGL((bwd_kernel<Q, V, false, CAUSAL, VAR>), grid, dim3(BwdCfg<Q, V>::NT), 0, s, a);    \
     return hipGetLastError();                                                                               \
   }
   AFP8_BWD_GO(64, 64)
@@ -762,9 +783,15 @@ hipError_t launch_bwd_main(const AttnArgs& a, int dqk, int dv, dim3 grid, hipStr
   return hipErrorInvalidValue;
 }
 
-extern template hipError_t launch_bwd_main<true, false>(const AttnArgs&, int, int, dim3, hipStream_t);
-extern template hipError_t launch_bwd_main<true, true>(const AttnArgs&, int, int, dim3, hipStream_t);
-extern template hipError_t launch_bwd_main<false, false>(const AttnArgs&, int, int, dim3, hipStream_t);
-extern template hipError_t launch_bwd_main<false, true>(const AttnArgs&, int, int, dim3, hipStream_t);
+#define AFP8_BWD_EXTERN(C, V) extern template hipError_t launch_bwd_main<C, V>(const AttnArgs&, int, int, dim3, hipStream_t);
+AFP8_BWD_EXTERN(true, 0)
+AFP8_BWD_EXTERN(true, 1)
+AFP8_BWD_EXTERN(true, 2)
+AFP8_BWD_EXTERN(true, 3)
+AFP8_BWD_EXTERN(false, 0)
+AFP8_BWD_EXTERN(false, 1)
+AFP8_BWD_EXTERN(false, 2)
+AFP8_BWD_EXTERN(false, 3)
+#undef AFP8_BWD_EXTERN
 
 }  // namespace afp8

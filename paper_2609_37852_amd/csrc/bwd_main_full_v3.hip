@@ -1,0 +1,8 @@
+// Main backward kernel, without the mask, compensated dS formation and block-
+// scaled backward probability operand: every head-dim pair, with and without
+// row statistics.
+#include "bwd_main.hpp"
+
+namespace afp8 {
+template hipError_t launch_bwd_main<false, 3>(const AttnArgs&, int, int, dim3, hipStream_t);
+}  // namespace afp8

@@ -51,6 +51,7 @@ struct AttnArgs {
   int causal;                // 1: key j visible to query i iff j <= i; 0: every key
   int comp;                  // compensated correction: FP64 products in the correction pass,
                              // compensated dS formation in the backward
+  int pmx;                   // block-scaled backward probability operand (one scale per 32x32 block)
   float c;                   // tau * log2(e), applied to the score accumulator
   float tau;
   const uint8_t *q_code, *q_scale;     // row copy of Q      [B,Hq,N,Dqk], [B,Hq,N,Dqk/32]

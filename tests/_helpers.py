@@ -60,16 +60,17 @@ def bwd_plain_and_stats(p, mode, mq, mk, mv, mdo, lse, do=None, o=None, delta_in
 
 
 def run_gpu(w, d, mode=pk.DELTA_MATCHING, grad_dtype=torch.float32, o_dtype=torch.bfloat16, rowstats=True,
-            delta_in=None, isolate=True, lse_shift=0.0):
+            delta_in=None, isolate=True, lse_shift=0.0, flags=0):
     """Quantize, forward, correction and backward on the GPU.  The gradients
     are those of the plain backward kernel; with rowstats the instrumented
     kernel runs as well (bitwise-equal gradients are asserted) and supplies
     the row statistics.  isolate=False drops the per-channel maxima (no
     isolated score channel); lse_shift is added to the LSE the correction
-    and the backward read."""
+    and the backward read; flags are the problem's numerics options."""
     q, k, v, do = (to_dev(d[n], w.dtype) for n in ("q", "k", "v", "do"))
     mq, mk, mv, mdo = (pk.attn_fp8_quantize(t, amax=isolate) for t in (q, k, v, do))
     p = problem(w)
+    p.flags = flags
     o, lse = pk.attn_fp8_fwd(p, mq, mk, mv, o_dtype=o_dtype)
     lse_b = lse + lse_shift if lse_shift else lse
     delta = pk.attn_fp8_delta(p, mode, mq, mk, mv, mdo, lse_b, do, o)
