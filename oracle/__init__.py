@@ -62,6 +62,8 @@ def lib():
         L.orc_quantize.argtypes = [_dp] + [ctypes.c_int64] * 4 + [_u8p] * 4
         L.orc_dequantize.argtypes = [_u8p] * 4 + [ctypes.c_int64] * 4 + [_dp, _dp]
         L.orc_producer.argtypes = [_dp] + [ctypes.c_int64] * 4 + [ctypes.c_double, ctypes.c_int, _dp, _dp]
+        L.orc_producer_rope.argtypes = ([_dp] + [ctypes.c_int64] * 4 + [_dp, ctypes.c_int64, ctypes.c_int64,
+                                        ctypes.c_double, ctypes.c_int, _dp, _dp])
         L.orc_attention.restype = ctypes.c_int
         L.orc_attention.argtypes = ([ctypes.POINTER(_Problem)] + [ctypes.c_int] * 4 + [_dp] * 23
                                     + [ctypes.c_int64, ctypes.c_int])
@@ -135,6 +137,23 @@ def producer(x, prescale=1.0, center=False):
     y = np.empty_like(x)
     mean = np.empty((B, H, D))
     lib().orc_producer(_ptr(x), B, N, H, D, float(np.float32(prescale)), int(bool(center)), _ptr(y), _ptr(mean))
+    return y, mean
+
+
+def producer_rope(x, rope, lo, R, prescale=1.0, center=False):
+    """Producer with the fused rotary embedding (App. B.6.1, reading R16):
+    rope [N, R/2, 2] (cosine, sine per token and pair, FP32 values); channels
+    lo .. lo + R - 1 rotated in pairs (lo + c, lo + c + R/2) and rounded to
+    BF16, then producer().  Returns (y, mean)."""
+    x = _f64(x)
+    B, N, H, D = x.shape
+    assert N % 32 == 0 and R % 2 == 0 and 0 <= lo and lo + R <= D
+    rope = _f64(rope)
+    assert rope.shape == (N, R // 2, 2)
+    y = np.empty_like(x)
+    mean = np.empty((B, H, D))
+    lib().orc_producer_rope(_ptr(x), B, N, H, D, _ptr(rope), int(lo), int(R), float(np.float32(prescale)),
+                            int(bool(center)), _ptr(y), _ptr(mean))
     return y, mean
 
 

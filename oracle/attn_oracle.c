@@ -41,6 +41,10 @@
  *   R15 (a variant, not the paper's kernel; ORC_MX_PBWD): the backward
  *      probability operand cast like dS' (R7), one power-of-two scale per
  *      aligned 32x32 block from its largest P, instead of the fixed 2^-8.
+ *   R16 fused rotary producer: rotated channels in half-split pairs
+ *      (lo + c, lo + c + R/2) with the caller's FP32 cosine/sine table,
+ *      each product and sum rounded to FP32, then to BF16, before the
+ *      prescale (orc_producer_rope).
  *   R10 causal mask is top-left aligned (key j visible to query i iff j <= i,
  *      equal query and key lengths); without the mask (causal == 0) every
  *      query sees all Nk keys and the key length may differ from the query
@@ -220,6 +224,33 @@ void orc_producer(const double* x, int64_t B, int64_t N, int64_t H, int64_t D, d
           y[o] = fl32(fl32(x[o] * prescale) - m);
         }
       }
+}
+
+/* Reading R16 (the rotation's arithmetic; the paper fixes only that the
+ * rotated channels are rounded to BF16 before the prescale): products and
+ * the sum of each rotated channel rounded to FP32, pairs (lo + c,
+ * lo + c + R/2), the caller's cosine/sine table per token. */
+void orc_producer_rope(const double* x, int64_t B, int64_t N, int64_t H, int64_t D, const double* rope,
+                       int64_t lo, int64_t R, double prescale, int center, double* y, double* mean) {
+  const int64_t n_el = B * N * H * D, h2 = R / 2;
+  double* r = (double*)malloc(sizeof(double) * (size_t)(n_el > 0 ? n_el : 1));
+  memcpy(r, x, sizeof(double) * (size_t)n_el);
+  if (rope && R > 0) {
+    for (int64_t b = 0; b < B; b++)
+      for (int64_t n = 0; n < N; n++)
+        for (int64_t h = 0; h < H; h++) {
+          const double* src = x + ((b * N + n) * H + h) * D;
+          double* dst = r + ((b * N + n) * H + h) * D;
+          for (int64_t c = 0; c < h2; c++) {
+            const double cs = rope[(n * h2 + c) * 2], sn = rope[(n * h2 + c) * 2 + 1];
+            const double a = src[lo + c], p = src[lo + c + h2];
+            dst[lo + c] = orc_bf16_round(fl32(fl32(a * cs) - fl32(p * sn)));
+            dst[lo + c + h2] = orc_bf16_round(fl32(fl32(p * cs) + fl32(a * sn)));
+          }
+        }
+  }
+  orc_producer(r, B, N, H, D, prescale, center, y, mean);
+  free(r);
 }
 
 void orc_dequantize(const uint8_t* code_row, const uint8_t* scale_row,

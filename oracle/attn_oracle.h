@@ -49,6 +49,18 @@ int64_t orc_quantize(const double* x, int64_t B, int64_t N, int64_t H, int64_t D
 void orc_producer(const double* x, int64_t B, int64_t N, int64_t H, int64_t D, double prescale, int center,
                   double* y, double* mean);
 
+/* Input producer with the fused rotary embedding (App. B.6.1, reading R16):
+ * channels lo .. lo + R - 1 of every (token n, head) are rotated in pairs
+ * (lo + c, lo + c + R/2), c < R/2, by the angle whose cosine and sine are
+ * rope[(n * R/2 + c) * 2 + {0, 1}] (FP32 values):
+ *   y_c      = fl32(fl32(x_c cos) - fl32(x_{c+R/2} sin))
+ *   y_{c+R/2} = fl32(fl32(x_{c+R/2} cos) + fl32(x_c sin)),
+ * each rounded to BF16 (RNE); other channels pass unchanged.  Then the
+ * producer above (prescale, mean) runs on the result.  R = 0 (or rope NULL):
+ * no rotation. */
+void orc_producer_rope(const double* x, int64_t B, int64_t N, int64_t H, int64_t D, const double* rope,
+                       int64_t lo, int64_t R, double prescale, int center, double* y, double* mean);
+
 /* Decode both copies into [B,H,N,D] doubles (either output may be NULL). */
 void orc_dequantize(const uint8_t* code_row, const uint8_t* scale_row,
                     const uint8_t* code_col, const uint8_t* scale_col,

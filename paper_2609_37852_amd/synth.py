@@ -135,3 +135,14 @@ def generate(w: Workload, seed: int = 0):
     if w.dtype == "bf16":
         q, k, v, do = (round_bf16(t) for t in (q, k, v, do))
     return dict(q=q, k=k, v=v, do=do)
+
+
+def rope_table(N: int, R: int, base: float, pos0: int = 0) -> np.ndarray:
+    """Cosine and sine of the rotary angles, [N, R/2, 2] float32: token n at
+    position pos0 + n, pair c at frequency base^(-2c/R) (angles in float64,
+    each value rounded once to float32).  An input of the producer, like the
+    tensors above."""
+    pos = np.arange(pos0, pos0 + N, dtype=np.float64)[:, None]
+    inv = base ** (-np.arange(R // 2, dtype=np.float64) * 2.0 / R)
+    ang = pos * inv[None, :]
+    return np.stack([np.cos(ang), np.sin(ang)], axis=-1).astype(np.float32)
