@@ -158,7 +158,13 @@ int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t 
 
 /* Input producer + quantizer (App. B.6.1, Operands, Scaling, and
  * Accumulation): the quantizer above applied to the transformed values
- *   x' = fl32(x * prescale)                     (e.g. the query times tau,
+ *   r  = x, with channels rope_lo .. rope_lo + rope_dim - 1 rotated (the
+ *        fused rotary embedding) when rope_dim > 0: pairs (c, c + rope_dim/2)
+ *        of that range, first r_c = x_c cos - x_{c+h} sin, second
+ *        r_{c+h} = x_{c+h} cos + x_c sin with h = rope_dim/2 and (cos, sin) =
+ *        rope_cs[n][c - rope_lo] of token n; each product and sum rounded to
+ *        FP32, the rotated channels then rounded to BF16 (RNE)
+ *   x' = fl32(r * prescale)                     (e.g. the query times tau,
  *                                                 with softmax_scale 1 later)
  *   y  = fl32(x' - mean[b, h, c])   if center   (e.g. the key minus its mean
  *                                                 over sequence positions,
@@ -168,16 +174,23 @@ int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t 
  * ascending), divided by N in FP64 and rounded to FP32, so it does not depend
  * on scheduling.  The backward takes the resulting codes as given: gradients
  * are those of the transformed operands (straight-through, App. B.6.3; the
- * key gradient is not re-centered).
+ * key gradient is not re-centered and refers to the rotated key).
  *   prescale      finite, nonzero (1 for none)
  *   center        0 or 1
  *   channel_mean  device float [B, H, D], written when center (else unused)
  *   partials      device double [B, H, D, N/32] workspace, when center
+ *   rope_cs       device float [N, rope_dim/2, 2] (cos, sin of token n's
+ *                 angle for each pair; the caller's table, so positions and
+ *                 frequencies are the caller's), 16-byte aligned; read when
+ *                 rope_dim > 0
+ *   rope_lo, rope_dim  multiples of 32 with rope_lo + rope_dim <= D
+ *                 (EUNSUPPORTED otherwise); rope_dim 0 for no rotation
  * Other arguments, checks and outputs as attn_fp8_quantize (channel_amax,
  * when requested, is of the transformed values). */
 int attn_fp8_quantize_producer(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H,
                                int64_t D, const int64_t strides[3], float prescale, int center,
-                               float* channel_mean, double* partials, const attn_fp8_mx* out,
+                               float* channel_mean, double* partials, const float* rope_cs,
+                               int64_t rope_lo, int64_t rope_dim, const attn_fp8_mx* out,
                                int which, uint32_t* nonfinite_count, hipStream_t stream);
 
 /* Forward (Sec. 2.3; App. B.6.2): S = tau * Q K^T, online softmax with

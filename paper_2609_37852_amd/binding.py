@@ -63,7 +63,7 @@ def lib():
         P = ctypes.POINTER
         L.attn_fp8_quantize.argtypes = [vp, i32, i64, i64, i64, i64, P(ctypes.c_int64), P(_MX), i32, vp, vp]
         L.attn_fp8_quantize_producer.argtypes = [vp, i32, i64, i64, i64, i64, P(ctypes.c_int64), ctypes.c_float, i32,
-                                                 vp, vp, P(_MX), i32, vp, vp]
+                                                 vp, vp, vp, i64, i64, P(_MX), i32, vp, vp]
         L.attn_fp8_fwd.argtypes = [P(_Problem), P(_MX), P(_MX), P(_MX), vp, i32, P(ctypes.c_int64), vp, vp]
         L.attn_fp8_delta.argtypes = [P(_Problem), i32, P(_MX), P(_MX), P(_MX), P(_MX), vp, vp, i32,
                                      P(ctypes.c_int64), vp, i32, P(ctypes.c_int64), vp, vp]
@@ -173,10 +173,18 @@ def attn_fp8_quantize(x: torch.Tensor, which: int = QUANT_BOTH, nonfinite: torch
 
 
 def attn_fp8_quantize_producer(x: torch.Tensor, prescale: float = 1.0, center: bool = False,
-                               which: int = QUANT_BOTH, nonfinite: torch.Tensor | None = None, amax: bool = True):
+                               which: int = QUANT_BOTH, nonfinite: torch.Tensor | None = None, amax: bool = True,
+                               rope: torch.Tensor | None = None, rope_lo: int = 0):
     """The input producer (App. B.6.1) then the quantizer: x [B, N, H, D] ->
-    (MX copies of fl32(fl32(x prescale) - mean), mean [B, H, D] or None)."""
+    (MX copies of fl32(fl32(r prescale) - mean), mean [B, H, D] or None), r =
+    x with channels rope_lo .. rope_lo + R - 1 rotated by the table rope
+    [N, R/2, 2] (float32 cos, sin on the device) and rounded to bf16."""
     B, N, H, D = x.shape
+    rope_dim = 0
+    if rope is not None:
+        assert rope.dtype == torch.float32 and rope.dim() == 3 and rope.shape[0] == N and rope.shape[2] == 2
+        rope = rope.contiguous()
+        rope_dim = 2 * rope.shape[1]
     out = MX.empty(B, N, H, D, x.device, which, amax=amax)
     mean = torch.empty((B, H, D), dtype=torch.float32, device=x.device) if center else None
     parts = torch.empty((B, H, D, max(N // 32, 1)), dtype=torch.float64, device=x.device) if center else None
@@ -184,7 +192,8 @@ def attn_fp8_quantize_producer(x: torch.Tensor, prescale: float = 1.0, center: b
     _check("attn_fp8_quantize_producer",
            lib().attn_fp8_quantize_producer(_ptr(x), _dtype_code(x.dtype), B, N, H, D, _strides_bnh(x),
                                             float(prescale), int(bool(center)), _ptr(mean), _ptr(parts),
-                                            ctypes.byref(m), which, _ptr(nonfinite), _stream(x.device)))
+                                            _ptr(rope), int(rope_lo), int(rope_dim), ctypes.byref(m), which,
+                                            _ptr(nonfinite), _stream(x.device)))
     return out, mean
 
 

@@ -280,8 +280,8 @@ int scratch_address(void** out) {
 }
 
 int quantize_impl(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, int64_t D, const int64_t strides[3],
-                  float prescale, float* mean, double* partials, const attn_fp8_mx* out, int which,
-                  uint32_t* nonfinite_count, hipStream_t stream) {
+                  float prescale, float* mean, double* partials, const float* rope, int64_t rope_lo, int64_t rope_dim,
+                  const attn_fp8_mx* out, int which, uint32_t* nonfinite_count, hipStream_t stream) {
   int rc;
   const int es = dtype_size(x_dtype);
   if (!es) return fail(ATTN_FP8_EINVAL, "x_dtype %d is not F32 or BF16", x_dtype);
@@ -316,6 +316,9 @@ int quantize_impl(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, i
   a.prescale = prescale;
   a.mean = mean;
   a.partials = partials;
+  a.rope = rope_dim > 0 ? rope : nullptr;
+  a.rope_lo = (int)rope_lo;
+  a.rope_dim = (int)rope_dim;
   if ((rc = hip_status(afp8::launch_quantize(a, (int)D, x_dtype == ATTN_FP8_DTYPE_BF16, stream), "quantize")))
     return rc;
   return ok();
@@ -330,21 +333,29 @@ const char* attn_fp8_last_error(void) { return g_error.c_str(); }
 int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, int64_t D,
                       const int64_t strides[3], const attn_fp8_mx* out, int which, uint32_t* nonfinite_count,
                       hipStream_t stream) {
-  return quantize_impl(x, x_dtype, B, N, H, D, strides, 1.0f, nullptr, nullptr, out, which, nonfinite_count, stream);
+  return quantize_impl(x, x_dtype, B, N, H, D, strides, 1.0f, nullptr, nullptr, nullptr, 0, 0, out, which,
+                       nonfinite_count, stream);
 }
 
 int attn_fp8_quantize_producer(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, int64_t D,
                                const int64_t strides[3], float prescale, int center, float* channel_mean,
-                               double* partials, const attn_fp8_mx* out, int which, uint32_t* nonfinite_count,
-                               hipStream_t stream) {
+                               double* partials, const float* rope_cs, int64_t rope_lo, int64_t rope_dim,
+                               const attn_fp8_mx* out, int which, uint32_t* nonfinite_count, hipStream_t stream) {
   int rc;
   if (!(std::isfinite(prescale) && prescale != 0.f))
     return fail(ATTN_FP8_EINVAL, "prescale must be finite and nonzero");
   if (center) {
     if ((rc = check_ptr("channel_mean", channel_mean)) || (rc = check_ptr("partials", partials))) return rc;
   }
+  if (rope_dim < 0 || rope_lo < 0) return fail(ATTN_FP8_EINVAL, "negative rope_lo / rope_dim");
+  if (rope_dim > 0) {
+    if (rope_dim % 32 != 0 || rope_lo % 32 != 0 || rope_lo + rope_dim > D)
+      return fail(ATTN_FP8_EUNSUPPORTED, "rotary channels [%lld, %lld) are not 32-aligned inside D = %lld",
+                  (long long)rope_lo, (long long)(rope_lo + rope_dim), (long long)D);
+    if ((rc = check_ptr("rope_cs", rope_cs))) return rc;
+  }
   return quantize_impl(x, x_dtype, B, N, H, D, strides, prescale, center ? channel_mean : nullptr,
-                       center ? partials : nullptr, out, which, nonfinite_count, stream);
+                       center ? partials : nullptr, rope_cs, rope_lo, rope_dim, out, which, nonfinite_count, stream);
 }
 
 int attn_fp8_fwd(const attn_fp8_problem* p, const attn_fp8_mx* q, const attn_fp8_mx* k, const attn_fp8_mx* v,

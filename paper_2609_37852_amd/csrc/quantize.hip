@@ -93,6 +93,19 @@ __device__ __forceinline__ float sub_rn(float x, float y) {
 #pragma clang fp contract(off)
   return x - y;
 }
+__device__ __forceinline__ float add_rn(float x, float y) {
+#pragma clang fp contract(off)
+  return x + y;
+}
+
+// One rotated channel of the fused rotary embedding: the first of a pair
+// gives x cos - p sin, the second x cos + p sin (x this channel's value, p
+// the pair partner's), every product and the sum rounded to FP32, the result
+// rounded to BF16.
+__device__ __forceinline__ float rope_rotate(float x, float p, float2 cs, bool first) {
+  const float a = mul_rn(x, cs.x), b = mul_rn(p, cs.y);
+  return bf16_to_f32(f32_to_bf16(first ? sub_rn(a, b) : add_rn(a, b)));
+}
 
 // One workgroup = 32 NB tokens (NB 32-token blocks; the last ones may lie
 // past the end of the sequence) x D channels of one (batch, head), 2*D threads.
@@ -130,6 +143,28 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
     if (bad) atomicAdd(a.nonfinite, bad);
   }
   if constexpr (PROD) {
+    if (a.rope) {
+      // fused rotary embedding: the pair partner's value comes through the
+      // tile (a token's chunks may lie in two waves)
+#pragma unroll
+      for (int u = 0; u < NB; u++)
+#pragma unroll
+        for (int k = 0; k < 16; k++) tile[32 * u + tok][ch + k] = v[u][k];
+      __syncthreads();
+      const int h2 = a.rope_dim >> 1, rel = ch - a.rope_lo;
+      if (rel >= 0 && rel < a.rope_dim) {
+        const bool first = rel < h2;
+        const int pch = first ? ch + h2 : ch - h2, c0 = first ? rel : rel - h2;
+#pragma unroll
+        for (int u = 0; u < NB; u++) {
+          if (u >= nb) break;
+          const float2* cs = reinterpret_cast<const float2*>(a.rope) + (n0 + 32 * u + tok) * h2 + c0;
+#pragma unroll
+          for (int k = 0; k < 16; k++) v[u][k] = rope_rotate(v[u][k], tile[32 * u + tok][pch + k], cs[k], first);
+        }
+      }
+      __syncthreads();   // the tile is written again below
+    }
     float mu[16];
 #pragma unroll
     for (int k = 0; k < 16; k++) mu[k] = a.mean ? a.mean[bh * D + ch + k] : 0.f;
@@ -199,17 +234,28 @@ hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 // divided by N in FP64 and rounded once to FP32.  The fixed order makes the
 // mean independent of scheduling.
 template <typename T>
+__device__ __forceinline__ float to_f32(T x) {
+  if constexpr (sizeof(T) == 2) return bf16_to_f32(x);
+  else return (float)x;
+}
+
+template <typename T>
 __global__ __launch_bounds__(256) void producer_partials_kernel(QuantArgs a, int D) {
   const int c = threadIdx.x;
   if (c >= D) return;
   const int64_t t = blockIdx.x, h = blockIdx.y, b = blockIdx.z, nblk = a.N / 32;
   const T* src = reinterpret_cast<const T*>(a.x) + b * a.sb + h * a.sh + c;
+  // rotary channel: its pair partner and table column (the same rotation as
+  // the quantizer's)
+  const int h2 = a.rope_dim >> 1, rel = c - a.rope_lo;
+  const bool rot = a.rope && rel >= 0 && rel < a.rope_dim, first = rel < h2;
+  const int poff = first ? h2 : -h2, c0 = first ? rel : rel - h2;
   double part = 0.0;
 #pragma unroll 8
   for (int k = 0; k < 32; k++) {
-    const T x = src[(32 * t + k) * a.sn];
-    float f;
-    if constexpr (sizeof(T) == 2) f = bf16_to_f32(x); else f = (float)x;
+    const int64_t n = 32 * t + k;
+    float f = to_f32(src[n * a.sn]);
+    if (rot) f = rope_rotate(f, to_f32(src[n * a.sn + poff]), reinterpret_cast<const float2*>(a.rope)[n * h2 + c0], first);
     part += (double)mul_rn(f, a.prescale);
   }
   a.partials[((b * a.H + h) * D + c) * nblk + t] = part;
@@ -232,7 +278,7 @@ hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_
     const hipError_t e = launch_fill_zero(a.chan_amax, a.B * a.H * D, s);
     if (e != hipSuccess) return e;
   }
-  const bool prod = a.prescale != 1.0f || a.mean;
+  const bool prod = a.prescale != 1.0f || a.mean || a.rope;
   if (a.mean) {
     const dim3 g1((unsigned)(a.N / 32), (unsigned)a.H, (unsigned)a.B), g2((unsigned)a.H, (unsigned)a.B);
     if (dtype_bf16) hipLaunchKernelGGL(producer_partials_kernel<uint16_t>, g1, dim3(256), 0, s, a, D);

@@ -149,12 +149,21 @@ def test_producer_rejects_bad_arguments():
     m = _fake_mx()
     st = bd._I64x3(64 * 64, 64, 64)
     args = (ctypes.c_void_p(4096), 1, 1, 64, 1, 64, st)
-    assert L.attn_fp8_quantize_producer(*args, float("nan"), 0, None, None, ctypes.byref(m), 3, None, None) == -1
-    assert L.attn_fp8_quantize_producer(*args, 0.0, 0, None, None, ctypes.byref(m), 3, None, None) == -1
+    nr = (None, 0, 0)   # no rotary table
+    assert L.attn_fp8_quantize_producer(*args, float("nan"), 0, None, None, *nr, ctypes.byref(m), 3, None, None) == -1
+    assert L.attn_fp8_quantize_producer(*args, 0.0, 0, None, None, *nr, ctypes.byref(m), 3, None, None) == -1
     # centering needs the mean output and the partial-sum workspace
-    assert L.attn_fp8_quantize_producer(*args, 1.0, 1, None, ctypes.c_void_p(4096), ctypes.byref(m), 3, None,
+    assert L.attn_fp8_quantize_producer(*args, 1.0, 1, None, ctypes.c_void_p(4096), *nr, ctypes.byref(m), 3, None,
                                         None) == -1
-    assert L.attn_fp8_quantize_producer(*args, 1.0, 1, ctypes.c_void_p(4096), None, ctypes.byref(m), 3, None,
+    assert L.attn_fp8_quantize_producer(*args, 1.0, 1, ctypes.c_void_p(4096), None, *nr, ctypes.byref(m), 3, None,
+                                        None) == -1
+    # rotary channels: 32-aligned, inside D, with a table
+    vp = ctypes.c_void_p(4096)
+    # (only rejected calls: the pointers here are placeholders)
+    for lo, R, code in ((0, 48, -2), (16, 32, -2), (32, 64, -2), (-32, 32, -1)):
+        rc = L.attn_fp8_quantize_producer(*args, 1.0, 0, None, None, vp, lo, R, ctypes.byref(m), 3, None, None)
+        assert rc == code, (lo, R, rc, pk.last_error())
+    assert L.attn_fp8_quantize_producer(*args, 1.0, 0, None, None, None, 0, 32, ctypes.byref(m), 3, None,
                                         None) == -1
 
 

@@ -1,7 +1,7 @@
-"""The input producer (App. B.6.1; reading R13) on the GPU: FP32 query
-prescale and per-(channel, KV head) key centering before quantization.
-Codes, scales and the key mean are bit-exact with the oracle's producer and
-quantizer; the whole path on the transformed operands (queries prescaled by
+"""The input producer (App. B.6.1; readings R13, R16) on the GPU: the fused
+rotary embedding (rotated channels rounded to BF16), FP32 query prescale and
+per-(channel, KV head) key centering before quantization.  Codes, scales and
+the key mean are bit-exact with the oracle's producer and quantizer; the whole path on the transformed operands (queries prescaled by
 tau, softmax scale 1, keys centred; straight-through key gradient) agrees
 with the oracle within the parity bounds and keeps the invariant."""
 import math
@@ -79,3 +79,60 @@ def test_producer_path_matches_oracle():
         assert errs[n] <= REL_TOL, (n, errs[n])
     check_blocks(blk)
     assert errs["LSE"] < 1e-3 and rep["violations"] == 0
+
+
+@pytest.mark.parametrize("D,lo,R", [(128, 0, 32), (192, 128, 64), (64, 0, 64), (256, 64, 128)])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("prescale,center", [(1 / math.sqrt(128), False), (1.0, True)])
+def test_rope_producer_codes_bit_exact(D, lo, R, dtype, prescale, center):
+    """The fused rotary producer (reading R16): codes, scales, channel maxima
+    and the key mean bit-exact with the oracle's rotary producer and
+    quantizer, on a strided input."""
+    B, N, H = 2, 96, 3
+    x = _keys(B, N, H, D, seed=D + R, dtype=dtype)
+    tab = synth.rope_table(N, R, 1e4, pos0=7)
+    wide = np.zeros((B, N, 2 * H, D), np.float32)
+    wide[:, :, ::2] = x
+    t = torch.from_numpy(wide).cuda()
+    t = (t.to(torch.bfloat16) if dtype == "bf16" else t)[:, :, ::2]
+    g, mean = pk.attn_fp8_quantize_producer(t, prescale, center, rope=torch.from_numpy(tab).cuda(), rope_lo=lo)
+    torch.cuda.synchronize()
+    y, m = orc.producer_rope(x, tab, lo, R, prescale, center)
+    ref = orc.quantize(y)
+    for f in ("code_row", "scale_row", "code_col", "scale_col"):
+        assert np.array_equal(getattr(g, f).cpu().numpy(), ref[f]), f
+    if center:
+        assert np.array_equal(mean.cpu().numpy().astype(np.float64), m)
+    assert np.array_equal(g.channel_amax.cpu().numpy(), np.abs(y).max(axis=1).astype(np.float32))
+
+
+def test_rope_producer_path_matches_oracle():
+    """MLA-shaped heads (dqk 192, dv 128) with the rotary part on channels
+    128..191 applied by the fused producer: queries rotated and prescaled by
+    tau (softmax scale 1), keys rotated and centred; the whole path against
+    the oracle run on the oracle producer's operands."""
+    w = synth.with_shape(synth.WORKLOADS["mla_d192_4k"], B=1, N=256, Hq=2, Hkv=2, transform="none")
+    d = synth.generate(w, seed=8)
+    tau = float(np.float32(w.tau))
+    tab = synth.rope_table(w.N, 64, 1e4)
+    qt, kt, vt, dot = (torch.from_numpy(a).to(torch.bfloat16).cuda() for a in (d["q"], d["k"], d["v"], d["do"]))
+    tt = torch.from_numpy(tab).cuda()
+    mq, _ = pk.attn_fp8_quantize_producer(qt, tau, False, rope=tt, rope_lo=128)
+    mk, _ = pk.attn_fp8_quantize_producer(kt, 1.0, True, rope=tt, rope_lo=128)
+    mv, mdo = pk.attn_fp8_quantize(vt), pk.attn_fp8_quantize(dot)
+    p = pk.Problem(w.B, w.N, w.Hq, w.Hkv, w.Dqk, w.Dv, 1.0)
+    o, lse = pk.attn_fp8_fwd(p, mq, mk, mv)
+    dq, dk, dv, rs = bwd_plain_and_stats(p, pk.DELTA_MATCHING, mq, mk, mv, mdo, lse)
+    torch.cuda.synchronize()
+    qy, _ = orc.producer_rope(d["q"], tab, 128, 64, tau, False)
+    ky, _ = orc.producer_rope(d["k"], tab, 128, 64, 1.0, True)
+    ref, _ = orc.attention_from_inputs(qy, ky, d["v"], d["do"], 1.0, want_rowstats=True)
+    g = dict(O=np64(o), dQ=np64(dq), dK=np64(dk), dV=np64(dv))
+    errs = {n: rel_err(g[n], ref[n]) for n in g}
+    blk = {n: block_errors(g[n], ref[n]) for n in g}
+    rep = invariant_report(rs.cpu().numpy())
+    say("  errors", {n: f"{e:.2e}" for n, e in errs.items()}, "invariant", rep)
+    for n in ("O", "dQ", "dK", "dV"):
+        assert errs[n] <= REL_TOL, (n, errs[n])
+    check_blocks(blk)
+    assert rep["violations"] == 0
