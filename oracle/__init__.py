@@ -64,6 +64,8 @@ def lib():
         L.orc_producer.argtypes = [_dp] + [ctypes.c_int64] * 4 + [ctypes.c_double, ctypes.c_int, _dp, _dp]
         L.orc_producer_rope.argtypes = ([_dp] + [ctypes.c_int64] * 4 + [_dp, ctypes.c_int64, ctypes.c_int64,
                                         ctypes.c_double, ctypes.c_int, _dp, _dp])
+        L.orc_producer_ext.argtypes = ([_dp] + [ctypes.c_int64] * 4 + [_dp, ctypes.c_double, _dp, ctypes.c_int64,
+                                       ctypes.c_int64, ctypes.c_double, ctypes.c_int, _dp, _dp])
         L.orc_attention.restype = ctypes.c_int
         L.orc_attention.argtypes = ([ctypes.POINTER(_Problem)] + [ctypes.c_int] * 4 + [_dp] * 23
                                     + [ctypes.c_int64, ctypes.c_int])
@@ -137,6 +139,27 @@ def producer(x, prescale=1.0, center=False):
     y = np.empty_like(x)
     mean = np.empty((B, H, D))
     lib().orc_producer(_ptr(x), B, N, H, D, float(np.float32(prescale)), int(bool(center)), _ptr(y), _ptr(mean))
+    return y, mean
+
+
+def producer_ext(x, gain=None, eps=1e-6, rope=None, lo=0, R=0, prescale=1.0, center=False):
+    """The full producer (readings R17, R16, R13): QK normalization with
+    gain [D] (FP32 values) and eps (taken as its FP32 value), the rotary
+    embedding with rope [N, R/2, 2], prescale, centring.  Returns (y, mean)."""
+    x = _f64(x)
+    B, N, H, D = x.shape
+    assert N % 32 == 0
+    if gain is not None:
+        gain = _f64(gain)
+        assert gain.shape == (D,)
+    if rope is not None:
+        rope = _f64(rope)
+        assert rope.shape == (N, R // 2, 2) and lo + R <= D
+    y = np.empty_like(x)
+    mean = np.empty((B, H, D))
+    lib().orc_producer_ext(_ptr(x), B, N, H, D, _ptr(gain), float(np.float32(eps)), _ptr(rope), int(lo),
+                           int(R if rope is not None else 0), float(np.float32(prescale)), int(bool(center)),
+                           _ptr(y), _ptr(mean))
     return y, mean
 
 

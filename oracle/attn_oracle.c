@@ -45,6 +45,9 @@
  *      (lo + c, lo + c + R/2) with the caller's FP32 cosine/sine table,
  *      each product and sum rounded to FP32, then to BF16, before the
  *      prescale (orc_producer_rope).
+ *   R17 QK normalization in the producer: the row statistic in FP64,
+ *      rounded once to FP32; x r and the gain product in FP32; BF16 result
+ *      (orc_producer_ext).
  *   R10 causal mask is top-left aligned (key j visible to query i iff j <= i,
  *      equal query and key lengths); without the mask (causal == 0) every
  *      query sees all Nk keys and the key length may differ from the query
@@ -230,6 +233,30 @@ void orc_producer(const double* x, int64_t B, int64_t N, int64_t H, int64_t D, d
  * rotated channels are rounded to BF16 before the prescale): products and
  * the sum of each rotated channel rounded to FP32, pairs (lo + c,
  * lo + c + R/2), the caller's cosine/sine table per token. */
+/* Reading R17 (the QK normalization's arithmetic; App. B.4 gives the key
+ * RMSNorm, App. B.2 its eps and FP32 computation): the row statistic in
+ * FP64 (squares summed over channels ascending, divided by D, eps added, the
+ * reciprocal square root), rounded once to FP32; then two FP32 products and
+ * the rounding to BF16 of the normalized activation. */
+void orc_producer_ext(const double* x, int64_t B, int64_t N, int64_t H, int64_t D, const double* gain, double eps,
+                      const double* rope, int64_t lo, int64_t R, double prescale, int center, double* y,
+                      double* mean) {
+  const int64_t n_el = B * N * H * D;
+  double* t = (double*)malloc(sizeof(double) * (size_t)(n_el > 0 ? n_el : 1));
+  memcpy(t, x, sizeof(double) * (size_t)n_el);
+  if (gain) {
+    for (int64_t row = 0; row < B * N * H; row++) {
+      double* v = t + row * D;
+      double ss = 0.0;
+      for (int64_t c = 0; c < D; c++) ss += v[c] * v[c];
+      const double r = fl32(1.0 / sqrt(ss / (double)D + eps));
+      for (int64_t c = 0; c < D; c++) v[c] = orc_bf16_round(fl32(fl32(v[c] * r) * gain[c]));
+    }
+  }
+  orc_producer_rope(t, B, N, H, D, rope, lo, R, prescale, center, y, mean);
+  free(t);
+}
+
 void orc_producer_rope(const double* x, int64_t B, int64_t N, int64_t H, int64_t D, const double* rope,
                        int64_t lo, int64_t R, double prescale, int center, double* y, double* mean) {
   const int64_t n_el = B * N * H * D, h2 = R / 2;

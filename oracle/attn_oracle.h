@@ -61,6 +61,15 @@ void orc_producer(const double* x, int64_t B, int64_t N, int64_t H, int64_t D, d
 void orc_producer_rope(const double* x, int64_t B, int64_t N, int64_t H, int64_t D, const double* rope,
                        int64_t lo, int64_t R, double prescale, int center, double* y, double* mean);
 
+/* The producer with the QK normalization in front (reading R17): when gain
+ * (FP32 values, [D], shared by the heads) is given, every (token, head) row
+ * becomes bf16(fl32(fl32(x_c r) g_c)) with r = fl32(1 / sqrt(ss / D + eps))
+ * in FP64, ss the FP64 sum of x_c^2 over c ascending (the key RMSNorm of
+ * App. B.4; eps 1e-6 in App. B.2); then orc_producer_rope. */
+void orc_producer_ext(const double* x, int64_t B, int64_t N, int64_t H, int64_t D, const double* gain, double eps,
+                      const double* rope, int64_t lo, int64_t R, double prescale, int center, double* y,
+                      double* mean);
+
 /* Decode both copies into [B,H,N,D] doubles (either output may be NULL). */
 void orc_dequantize(const uint8_t* code_row, const uint8_t* scale_row,
                     const uint8_t* code_col, const uint8_t* scale_col,
