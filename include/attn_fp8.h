@@ -156,12 +156,18 @@ int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t 
                       const int64_t strides[3], const attn_fp8_mx* out, int which,
                       uint32_t* nonfinite_count, hipStream_t stream);
 
-/* Input producer + quantizer (App. B.6.1, Operands, Scaling, and
- * Accumulation): the quantizer above applied to the transformed values
- *   r  = x, with channels rope_lo .. rope_lo + rope_dim - 1 rotated (the
+/* Options of the input producer (App. B.6.1, Operands, Scaling, and
+ * Accumulation; App. B.4 and B.2 for the QK normalization).  Applied in this
+ * order to every (token n, head h) row x of D channels:
+ *   u  = x, or with rms_gain: the QK normalization (RMSNorm)
+ *        r_nh = fl32(1 / sqrt(sum_c x_c^2 / D + rms_eps)), the sum of the
+ *        squares taken in FP64 over c ascending and divided, offset (by the
+ *        FP32 eps) and inverted in FP64, each step rounded to nearest, then
+ *        u_c = bf16(fl32(fl32(x_c r_nh) g_c)), g = rms_gain
+ *   r  = u, with channels rope_lo .. rope_lo + rope_dim - 1 rotated (the
  *        fused rotary embedding) when rope_dim > 0: pairs (c, c + rope_dim/2)
- *        of that range, first r_c = x_c cos - x_{c+h} sin, second
- *        r_{c+h} = x_{c+h} cos + x_c sin with h = rope_dim/2 and (cos, sin) =
+ *        of that range, first r_c = u_c cos - u_{c+h} sin, second
+ *        r_{c+h} = u_{c+h} cos + u_c sin with h = rope_dim/2 and (cos, sin) =
  *        rope_cs[n][c - rope_lo] of token n; each product and sum rounded to
  *        FP32, the rotated channels then rounded to BF16 (RNE)
  *   x' = fl32(r * prescale)                     (e.g. the query times tau,
@@ -172,25 +178,53 @@ int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t 
  * each rounded once to FP32 (no fused multiply-add).  The mean is the FP64
  * sum of FP64 sums over aligned 32-token blocks (tokens ascending, blocks
  * ascending), divided by N in FP64 and rounded to FP32, so it does not depend
- * on scheduling.  The backward takes the resulting codes as given: gradients
- * are those of the transformed operands (straight-through, App. B.6.3; the
- * key gradient is not re-centered and refers to the rotated key).
+ * on scheduling.
  *   prescale      finite, nonzero (1 for none)
  *   center        0 or 1
  *   channel_mean  device float [B, H, D], written when center (else unused)
- *   partials      device double [B, H, D, N/32] workspace, when center
+ *   rms_gain      nullable device float [D], 16-byte aligned: the norm's
+ *                 per-channel gain; NULL for no normalization
+ *   rms_eps       finite, >= 0 (read with rms_gain)
  *   rope_cs       device float [N, rope_dim/2, 2] (cos, sin of token n's
  *                 angle for each pair; the caller's table, so positions and
  *                 frequencies are the caller's), 16-byte aligned; read when
  *                 rope_dim > 0
  *   rope_lo, rope_dim  multiples of 32 with rope_lo + rope_dim <= D
- *                 (EUNSUPPORTED otherwise); rope_dim 0 for no rotation
+ *                 (EUNSUPPORTED otherwise); rope_dim 0 for no rotation */
+typedef struct attn_fp8_producer {
+  float prescale;
+  int32_t center;
+  float* channel_mean;
+  const float* rms_gain;
+  float rms_eps;
+  const float* rope_cs;
+  int64_t rope_lo;
+  int64_t rope_dim;
+} attn_fp8_producer;
+
+/* Workspace bytes attn_fp8_quantize_producer needs with these options: the
+ * key-mean partial sums (FP64 [B, H, D, N/32]) when center, then the norm's
+ * row scales (FP32 [B, N, H]) when rms_gain, each rounded up to 256 bytes;
+ * 0 when neither.  Checks the options and sizes as the producer does.
+ * Returns 0 / negative status. */
+int attn_fp8_producer_workspace_size(int64_t B, int64_t N, int64_t H, int64_t D,
+                                     const attn_fp8_producer* opt, size_t* bytes);
+
+/* Input producer + quantizer: the quantizer above applied to the values y
+ * that the options (attn_fp8_producer) define.  The backward takes the
+ * resulting codes as given: gradients are those of the transformed operands
+ * (straight-through, App. B.6.3; the key gradient is not re-centered and
+ * refers to the normalized, rotated key).
+ *   opt        the options (not NULL)
+ *   workspace  device, at least attn_fp8_producer_workspace_size() bytes,
+ *              256-byte aligned (may be NULL when that size is 0); its
+ *              contents on entry do not matter and on return are unspecified
  * Other arguments, checks and outputs as attn_fp8_quantize (channel_amax,
- * when requested, is of the transformed values). */
+ * when requested, is of the transformed values).  The input is read once
+ * more for the norm's row scales and once more for the key mean. */
 int attn_fp8_quantize_producer(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H,
-                               int64_t D, const int64_t strides[3], float prescale, int center,
-                               float* channel_mean, double* partials, const float* rope_cs,
-                               int64_t rope_lo, int64_t rope_dim, const attn_fp8_mx* out,
+                               int64_t D, const int64_t strides[3], const attn_fp8_producer* opt,
+                               void* workspace, size_t workspace_bytes, const attn_fp8_mx* out,
                                int which, uint32_t* nonfinite_count, hipStream_t stream);
 
 /* Forward (Sec. 2.3; App. B.6.2): S = tau * Q K^T, online softmax with

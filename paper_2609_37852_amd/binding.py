@@ -25,7 +25,8 @@ RS_SUM_DS, RS_SUMABS_DS, RS_SUM_DSCAST, RS_MAXABS_DS, RS_SUMABS_DSCAST, RS_MAX_P
 ROWSTATS = 7
 STATUS = {0: "OK", -1: "EINVAL", -2: "EUNSUPPORTED", -3: "EALIGN", -4: "EWORKSPACE", -5: "EHIP"}
 EXPORTS = ("attn_fp8_quantize", "attn_fp8_fwd", "attn_fp8_delta", "attn_fp8_bwd_workspace_size",
-           "attn_fp8_bwd", "attn_fp8_bwd_noalloc", "attn_fp8_quantize_producer", "attn_fp8_last_error")
+           "attn_fp8_bwd", "attn_fp8_bwd_noalloc", "attn_fp8_quantize_producer",
+           "attn_fp8_producer_workspace_size", "attn_fp8_last_error")
 NOALLOC_SCRATCH_BYTES = 64 << 20   # ATTN_FP8_NOALLOC_SCRATCH_BYTES
 
 
@@ -40,6 +41,12 @@ class _Problem(ctypes.Structure):
                 ("heads_kv", ctypes.c_int64), ("dim_qk", ctypes.c_int64), ("dim_v", ctypes.c_int64),
                 ("causal", ctypes.c_int32), ("softmax_scale", ctypes.c_float), ("seqlen_kv", ctypes.c_int64),
                 ("flags", ctypes.c_int32)]
+
+
+class _Producer(ctypes.Structure):
+    _fields_ = [("prescale", ctypes.c_float), ("center", ctypes.c_int32), ("channel_mean", ctypes.c_void_p),
+                ("rms_gain", ctypes.c_void_p), ("rms_eps", ctypes.c_float), ("rope_cs", ctypes.c_void_p),
+                ("rope_lo", ctypes.c_int64), ("rope_dim", ctypes.c_int64)]
 
 
 class _MX(ctypes.Structure):
@@ -62,8 +69,9 @@ def lib():
         vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
         P = ctypes.POINTER
         L.attn_fp8_quantize.argtypes = [vp, i32, i64, i64, i64, i64, P(ctypes.c_int64), P(_MX), i32, vp, vp]
-        L.attn_fp8_quantize_producer.argtypes = [vp, i32, i64, i64, i64, i64, P(ctypes.c_int64), ctypes.c_float, i32,
-                                                 vp, vp, vp, i64, i64, P(_MX), i32, vp, vp]
+        L.attn_fp8_quantize_producer.argtypes = [vp, i32, i64, i64, i64, i64, P(ctypes.c_int64), P(_Producer), vp, sz,
+                                                 P(_MX), i32, vp, vp]
+        L.attn_fp8_producer_workspace_size.argtypes = [i64, i64, i64, i64, P(_Producer), P(sz)]
         L.attn_fp8_fwd.argtypes = [P(_Problem), P(_MX), P(_MX), P(_MX), vp, i32, P(ctypes.c_int64), vp, vp]
         L.attn_fp8_delta.argtypes = [P(_Problem), i32, P(_MX), P(_MX), P(_MX), P(_MX), vp, vp, i32,
                                      P(ctypes.c_int64), vp, i32, P(ctypes.c_int64), vp, vp]
@@ -174,25 +182,35 @@ def attn_fp8_quantize(x: torch.Tensor, which: int = QUANT_BOTH, nonfinite: torch
 
 def attn_fp8_quantize_producer(x: torch.Tensor, prescale: float = 1.0, center: bool = False,
                                which: int = QUANT_BOTH, nonfinite: torch.Tensor | None = None, amax: bool = True,
-                               rope: torch.Tensor | None = None, rope_lo: int = 0):
+                               rope: torch.Tensor | None = None, rope_lo: int = 0,
+                               rms_gain: torch.Tensor | None = None, rms_eps: float = 1e-6):
     """The input producer (App. B.6.1) then the quantizer: x [B, N, H, D] ->
-    (MX copies of fl32(fl32(r prescale) - mean), mean [B, H, D] or None), r =
-    x with channels rope_lo .. rope_lo + R - 1 rotated by the table rope
-    [N, R/2, 2] (float32 cos, sin on the device) and rounded to bf16."""
+    (MX copies of fl32(fl32(r prescale) - mean), mean [B, H, D] or None).  r
+    is x, RMS-normalized with the gain rms_gain [D] (float32 on the device)
+    when given, with channels rope_lo .. rope_lo + R - 1 then rotated by the
+    table rope [N, R/2, 2] (float32 cos, sin on the device); normalized and
+    rotated values are rounded to bf16."""
     B, N, H, D = x.shape
     rope_dim = 0
     if rope is not None:
         assert rope.dtype == torch.float32 and rope.dim() == 3 and rope.shape[0] == N and rope.shape[2] == 2
         rope = rope.contiguous()
         rope_dim = 2 * rope.shape[1]
+    if rms_gain is not None:
+        assert rms_gain.dtype == torch.float32 and rms_gain.shape == (D,)
+        rms_gain = rms_gain.contiguous()
     out = MX.empty(B, N, H, D, x.device, which, amax=amax)
     mean = torch.empty((B, H, D), dtype=torch.float32, device=x.device) if center else None
-    parts = torch.empty((B, H, D, max(N // 32, 1)), dtype=torch.float64, device=x.device) if center else None
+    opt = _Producer(float(prescale), int(bool(center)), _ptr(mean).value, _ptr(rms_gain).value, float(rms_eps),
+                    _ptr(rope).value, int(rope_lo), int(rope_dim))
+    need = ctypes.c_size_t(0)
+    _check("attn_fp8_producer_workspace_size",
+           lib().attn_fp8_producer_workspace_size(B, N, H, D, ctypes.byref(opt), ctypes.byref(need)))
+    ws = torch.empty(need.value, dtype=torch.uint8, device=x.device) if need.value else None
     m = out.c()
     _check("attn_fp8_quantize_producer",
            lib().attn_fp8_quantize_producer(_ptr(x), _dtype_code(x.dtype), B, N, H, D, _strides_bnh(x),
-                                            float(prescale), int(bool(center)), _ptr(mean), _ptr(parts),
-                                            _ptr(rope), int(rope_lo), int(rope_dim), ctypes.byref(m), which,
+                                            ctypes.byref(opt), _ptr(ws), need.value, ctypes.byref(m), which,
                                             _ptr(nonfinite), _stream(x.device)))
     return out, mean
 

@@ -279,9 +279,42 @@ int scratch_address(void** out) {
   return ATTN_FP8_OK;
 }
 
+// Producer workspace: the key-mean partial sums (FP64 [B, H, D, N/32]) when
+// centering, then the QK-normalization row scales (FP32 [B, N, H]) when a
+// gain is given, each 256-byte aligned.
+size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
+size_t ws_partials_bytes(int64_t B, int64_t N, int64_t H, int64_t D, const attn_fp8_producer* o) {
+  return o->center ? align256(size_t(B * H * D * (N / 32)) * sizeof(double)) : 0;
+}
+size_t ws_rscale_bytes(int64_t B, int64_t N, int64_t H, const attn_fp8_producer* o) {
+  return o->rms_gain ? align256(size_t(B * N * H) * sizeof(float)) : 0;
+}
+
+int check_producer(int64_t D, const attn_fp8_producer* o) {
+  int rc;
+  if (!o) return fail(ATTN_FP8_EINVAL, "producer options are NULL");
+  if (!(std::isfinite(o->prescale) && o->prescale != 0.f))
+    return fail(ATTN_FP8_EINVAL, "prescale must be finite and nonzero");
+  if (o->center != 0 && o->center != 1) return fail(ATTN_FP8_EINVAL, "center = %d", (int)o->center);
+  if (o->center && (rc = check_ptr("channel_mean", o->channel_mean))) return rc;
+  if (o->rms_gain) {
+    if (!(std::isfinite(o->rms_eps) && o->rms_eps >= 0.0)) return fail(ATTN_FP8_EINVAL, "rms_eps must be finite, >= 0");
+    if (reinterpret_cast<uintptr_t>(o->rms_gain) & 15u) return fail(ATTN_FP8_EALIGN, "rms_gain is not 16-byte aligned");
+  }
+  if (o->rope_dim < 0 || o->rope_lo < 0) return fail(ATTN_FP8_EINVAL, "negative rope_lo / rope_dim");
+  if (o->rope_dim > 0) {
+    if (o->rope_dim % 32 != 0 || o->rope_lo % 32 != 0 || o->rope_lo + o->rope_dim > D)
+      return fail(ATTN_FP8_EUNSUPPORTED, "rotary channels [%lld, %lld) are not 32-aligned inside D = %lld",
+                  (long long)o->rope_lo, (long long)(o->rope_lo + o->rope_dim), (long long)D);
+    if ((rc = check_ptr("rope_cs", o->rope_cs))) return rc;
+  }
+  return ATTN_FP8_OK;
+}
+
+// opt NULL: the plain quantizer
 int quantize_impl(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, int64_t D, const int64_t strides[3],
-                  float prescale, float* mean, double* partials, const float* rope, int64_t rope_lo, int64_t rope_dim,
-                  const attn_fp8_mx* out, int which, uint32_t* nonfinite_count, hipStream_t stream) {
+                  const attn_fp8_producer* opt, void* workspace, size_t workspace_bytes, const attn_fp8_mx* out,
+                  int which, uint32_t* nonfinite_count, hipStream_t stream) {
   int rc;
   const int es = dtype_size(x_dtype);
   if (!es) return fail(ATTN_FP8_EINVAL, "x_dtype %d is not F32 or BF16", x_dtype);
@@ -290,6 +323,7 @@ int quantize_impl(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, i
   if (N % 32 != 0) return fail(ATTN_FP8_EUNSUPPORTED, "N = %lld is not a multiple of 32", (long long)N);
   if (which < 1 || which > 3) return fail(ATTN_FP8_EINVAL, "which = %d", which);
   if (B > 65535 || H > 65535 || N > (int64_t(1) << 30)) return fail(ATTN_FP8_EUNSUPPORTED, "grid limits");
+  if (opt && (rc = check_producer(D, opt))) return rc;
   if (B == 0 || N == 0 || H == 0) return ok();  // empty: nothing is read or written
   if ((rc = check_ptr("x", x)) || (rc = check_strides("x", strides, es)) ||
       (rc = check_mx("out", out, which & 1, which & 2)))
@@ -313,12 +347,32 @@ int quantize_impl(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, i
   a.which = which;
   a.nonfinite = nonfinite_count;
   a.chan_amax = out->channel_amax;
-  a.prescale = prescale;
-  a.mean = mean;
-  a.partials = partials;
-  a.rope = rope_dim > 0 ? rope : nullptr;
-  a.rope_lo = (int)rope_lo;
-  a.rope_dim = (int)rope_dim;
+  a.prescale = 1.0f;
+  if (opt) {
+    const size_t np = ws_partials_bytes(B, N, H, D, opt), need = np + ws_rscale_bytes(B, N, H, opt);
+    if (need) {
+      if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
+        return fail(ATTN_FP8_EWORKSPACE, "workspace is NULL or not 256-byte aligned");
+      if (workspace_bytes < need)
+        return fail(ATTN_FP8_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
+    }
+    uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+    a.prescale = opt->prescale;
+    if (opt->center) {
+      a.mean = opt->channel_mean;
+      a.partials = reinterpret_cast<double*>(ws);
+    }
+    if (opt->rms_gain) {
+      a.gain = opt->rms_gain;
+      a.eps = (double)opt->rms_eps;
+      a.rscale = reinterpret_cast<float*>(ws + np);
+    }
+    if (opt->rope_dim > 0) {
+      a.rope = opt->rope_cs;
+      a.rope_lo = (int)opt->rope_lo;
+      a.rope_dim = (int)opt->rope_dim;
+    }
+  }
   if ((rc = hip_status(afp8::launch_quantize(a, (int)D, x_dtype == ATTN_FP8_DTYPE_BF16, stream), "quantize")))
     return rc;
   return ok();
@@ -333,29 +387,29 @@ const char* attn_fp8_last_error(void) { return g_error.c_str(); }
 int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, int64_t D,
                       const int64_t strides[3], const attn_fp8_mx* out, int which, uint32_t* nonfinite_count,
                       hipStream_t stream) {
-  return quantize_impl(x, x_dtype, B, N, H, D, strides, 1.0f, nullptr, nullptr, nullptr, 0, 0, out, which,
-                       nonfinite_count, stream);
+  return quantize_impl(x, x_dtype, B, N, H, D, strides, nullptr, nullptr, 0, out, which, nonfinite_count, stream);
+}
+
+int attn_fp8_producer_workspace_size(int64_t B, int64_t N, int64_t H, int64_t D, const attn_fp8_producer* opt,
+                                     size_t* bytes) {
+  int rc;
+  if (!bytes) return fail(ATTN_FP8_EINVAL, "bytes is NULL");
+  if (B < 0 || N < 0 || H < 0) return fail(ATTN_FP8_EINVAL, "negative size");
+  if (!head_dim_ok(D)) return fail(ATTN_FP8_EUNSUPPORTED, "D = %lld not in {64,128,192,256}", (long long)D);
+  if (N % 32 != 0) return fail(ATTN_FP8_EUNSUPPORTED, "N = %lld is not a multiple of 32", (long long)N);
+  if (B > 65535 || H > 65535 || N > (int64_t(1) << 30)) return fail(ATTN_FP8_EUNSUPPORTED, "grid limits");
+  if ((rc = check_producer(D, opt))) return rc;
+  *bytes = ws_partials_bytes(B, N, H, D, opt) + ws_rscale_bytes(B, N, H, opt);
+  return ok();
 }
 
 int attn_fp8_quantize_producer(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, int64_t D,
-                               const int64_t strides[3], float prescale, int center, float* channel_mean,
-                               double* partials, const float* rope_cs, int64_t rope_lo, int64_t rope_dim,
-                               const attn_fp8_mx* out, int which, uint32_t* nonfinite_count, hipStream_t stream) {
-  int rc;
-  if (!(std::isfinite(prescale) && prescale != 0.f))
-    return fail(ATTN_FP8_EINVAL, "prescale must be finite and nonzero");
-  if (center) {
-    if ((rc = check_ptr("channel_mean", channel_mean)) || (rc = check_ptr("partials", partials))) return rc;
-  }
-  if (rope_dim < 0 || rope_lo < 0) return fail(ATTN_FP8_EINVAL, "negative rope_lo / rope_dim");
-  if (rope_dim > 0) {
-    if (rope_dim % 32 != 0 || rope_lo % 32 != 0 || rope_lo + rope_dim > D)
-      return fail(ATTN_FP8_EUNSUPPORTED, "rotary channels [%lld, %lld) are not 32-aligned inside D = %lld",
-                  (long long)rope_lo, (long long)(rope_lo + rope_dim), (long long)D);
-    if ((rc = check_ptr("rope_cs", rope_cs))) return rc;
-  }
-  return quantize_impl(x, x_dtype, B, N, H, D, strides, prescale, center ? channel_mean : nullptr,
-                       center ? partials : nullptr, rope_cs, rope_lo, rope_dim, out, which, nonfinite_count, stream);
+                               const int64_t strides[3], const attn_fp8_producer* opt, void* workspace,
+                               size_t workspace_bytes, const attn_fp8_mx* out, int which, uint32_t* nonfinite_count,
+                               hipStream_t stream) {
+  if (!opt) return fail(ATTN_FP8_EINVAL, "producer options are NULL");
+  return quantize_impl(x, x_dtype, B, N, H, D, strides, opt, workspace, workspace_bytes, out, which,
+                       nonfinite_count, stream);
 }
 
 int attn_fp8_fwd(const attn_fp8_problem* p, const attn_fp8_mx* q, const attn_fp8_mx* k, const attn_fp8_mx* v,

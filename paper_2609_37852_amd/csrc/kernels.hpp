@@ -33,6 +33,12 @@ struct QuantArgs {
   // by rope[n][c][{cos, sin}] ([N, rope_dim/2, 2] FP32) and rounded to BF16
   const float* rope;
   int rope_lo, rope_dim;
+  // QK normalization before the rotary embedding (nullable gain [D]): each
+  // (token, head) row times rscale[b, n, h] (FP32, from FP64 statistics,
+  // written by producer_rscale_kernel), times the gain, rounded to BF16
+  const float* gain;
+  double eps;
+  float* rscale;             // workspace [B, N, H], with gain
 };
 
 struct StaleArgs {

@@ -107,6 +107,12 @@ __device__ __forceinline__ float rope_rotate(float x, float p, float2 cs, bool f
   return bf16_to_f32(f32_to_bf16(first ? sub_rn(a, b) : add_rn(a, b)));
 }
 
+// One channel of the QK normalization: x times the row's reciprocal RMS,
+// times the channel gain, each product rounded to FP32, rounded to BF16.
+__device__ __forceinline__ float qk_norm(float x, float r, float g) {
+  return bf16_to_f32(f32_to_bf16(mul_rn(mul_rn(x, r), g)));
+}
+
 // One workgroup = 32 NB tokens (NB 32-token blocks; the last ones may lie
 // past the end of the sequence) x D channels of one (batch, head), 2*D threads.
 // PROD: the input producer's transform is applied to every value first
@@ -143,6 +149,15 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
     if (bad) atomicAdd(a.nonfinite, bad);
   }
   if constexpr (PROD) {
+    if (a.gain) {
+#pragma unroll
+      for (int u = 0; u < NB; u++) {
+        if (u >= nb) break;
+        const float r = a.rscale[((b * a.N) + n0 + 32 * u + tok) * a.H + h];
+#pragma unroll
+        for (int k = 0; k < 16; k++) v[u][k] = qk_norm(v[u][k], r, a.gain[ch + k]);
+      }
+    }
     if (a.rope) {
       // fused rotary embedding: the pair partner's value comes through the
       // tile (a token's chunks may lie in two waves)
@@ -255,10 +270,37 @@ __global__ __launch_bounds__(256) void producer_partials_kernel(QuantArgs a, int
   for (int k = 0; k < 32; k++) {
     const int64_t n = 32 * t + k;
     float f = to_f32(src[n * a.sn]);
-    if (rot) f = rope_rotate(f, to_f32(src[n * a.sn + poff]), reinterpret_cast<const float2*>(a.rope)[n * h2 + c0], first);
+    float p = rot ? to_f32(src[n * a.sn + poff]) : 0.f;
+    if (a.gain) {
+      const float r = a.rscale[(b * a.N + n) * a.H + h];
+      f = qk_norm(f, r, a.gain[c]);
+      if (rot) p = qk_norm(p, r, a.gain[c + poff]);
+    }
+    if (rot) f = rope_rotate(f, p, reinterpret_cast<const float2*>(a.rope)[n * h2 + c0], first);
     part += (double)mul_rn(f, a.prescale);
   }
   a.partials[((b * a.H + h) * D + c) * nblk + t] = part;
+}
+
+// Reciprocal RMS of every (token, head) row for the QK normalization: the
+// squares summed in FP64 over the channels in ascending order, divided by D,
+// eps added, 1 / sqrt in FP64 (each rounded to nearest), rounded once to
+// FP32.  One thread per row; the grid strides over the rows.
+template <typename T>
+__global__ __launch_bounds__(256) void producer_rscale_kernel(QuantArgs a, int D) {
+  const int64_t rows = a.B * a.N * a.H;
+  for (int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x; row < rows; row += (int64_t)gridDim.x * 256) {
+    const int64_t h = row % a.H, n = (row / a.H) % a.N, b = row / (a.H * a.N);
+    const T* src = reinterpret_cast<const T*>(a.x) + b * a.sb + n * a.sn + h * a.sh;
+    double ss = 0.0;
+    for (int c = 0; c < D; c += 16) {
+      float v[16];
+      load16<T>(src + c, v);
+#pragma unroll
+      for (int k = 0; k < 16; k++) ss += (double)v[k] * (double)v[k];   // exact products
+    }
+    a.rscale[row] = (float)(1.0 / __builtin_sqrt(ss / (double)D + a.eps));
+  }
 }
 
 __global__ __launch_bounds__(256) void producer_mean_kernel(QuantArgs a, int D) {
@@ -278,7 +320,13 @@ hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_
     const hipError_t e = launch_fill_zero(a.chan_amax, a.B * a.H * D, s);
     if (e != hipSuccess) return e;
   }
-  const bool prod = a.prescale != 1.0f || a.mean || a.rope;
+  const bool prod = a.prescale != 1.0f || a.mean || a.rope || a.gain;
+  if (a.gain) {
+    const int64_t nblk = (a.B * a.N * a.H + 255) / 256;
+    const dim3 g0((unsigned)(nblk < 65536 ? nblk : 65536));
+    if (dtype_bf16) hipLaunchKernelGGL(producer_rscale_kernel<uint16_t>, g0, dim3(256), 0, s, a, D);
+    else hipLaunchKernelGGL(producer_rscale_kernel<float>, g0, dim3(256), 0, s, a, D);
+  }
   if (a.mean) {
     const dim3 g1((unsigned)(a.N / 32), (unsigned)a.H, (unsigned)a.B), g2((unsigned)a.H, (unsigned)a.B);
     if (dtype_bf16) hipLaunchKernelGGL(producer_partials_kernel<uint16_t>, g1, dim3(256), 0, s, a, D);

@@ -144,27 +144,68 @@ def test_noalloc_rejects_oversized_problem_on_the_host():
     assert rc == -2 and "scratch" in pk.last_error()
 
 
+def _opt(**kw):
+    d = dict(prescale=1.0, center=0, channel_mean=None, rms_gain=None, rms_eps=1e-6, rope_cs=None, rope_lo=0,
+             rope_dim=0)
+    d.update(kw)
+    return bd._Producer(**d)
+
+
 def test_producer_rejects_bad_arguments():
     L = pk.lib()
     m = _fake_mx()
     st = bd._I64x3(64 * 64, 64, 64)
     args = (ctypes.c_void_p(4096), 1, 1, 64, 1, 64, st)
-    nr = (None, 0, 0)   # no rotary table
-    assert L.attn_fp8_quantize_producer(*args, float("nan"), 0, None, None, *nr, ctypes.byref(m), 3, None, None) == -1
-    assert L.attn_fp8_quantize_producer(*args, 0.0, 0, None, None, *nr, ctypes.byref(m), 3, None, None) == -1
-    # centering needs the mean output and the partial-sum workspace
-    assert L.attn_fp8_quantize_producer(*args, 1.0, 1, None, ctypes.c_void_p(4096), *nr, ctypes.byref(m), 3, None,
-                                        None) == -1
-    assert L.attn_fp8_quantize_producer(*args, 1.0, 1, ctypes.c_void_p(4096), None, *nr, ctypes.byref(m), 3, None,
-                                        None) == -1
-    # rotary channels: 32-aligned, inside D, with a table
-    vp = ctypes.c_void_p(4096)
+    vp = ctypes.c_void_p(4096).value
+    ws = (ctypes.c_void_p(4096), 1 << 20)
+
+    def call(opt, w=ws):
+        return L.attn_fp8_quantize_producer(*args, ctypes.byref(opt) if opt is not None else None, *w,
+                                            ctypes.byref(m), 3, None, None)
     # (only rejected calls: the pointers here are placeholders)
+    assert call(None) == -1
+    assert call(_opt(prescale=float("nan"))) == -1
+    assert call(_opt(prescale=0.0)) == -1
+    assert call(_opt(center=2, channel_mean=vp)) == -1
+    # centering needs the mean output, and a workspace for its partial sums
+    assert call(_opt(center=1)) == -1
+    assert call(_opt(center=1, channel_mean=vp), (None, 0)) == -4
+    assert call(_opt(center=1, channel_mean=vp), (ctypes.c_void_p(4096), 255)) == -4
+    assert call(_opt(center=1, channel_mean=vp), (ctypes.c_void_p(4096 + 16), 1 << 20)) == -4
+    # the norm: finite non-negative eps, aligned gain, a workspace for the row scales
+    assert call(_opt(rms_gain=vp, rms_eps=-1.0)) == -1
+    assert call(_opt(rms_gain=vp, rms_eps=float("inf"))) == -1
+    assert call(_opt(rms_gain=4100)) == -3
+    assert call(_opt(rms_gain=vp), (None, 0)) == -4
+    # rotary channels: 32-aligned, inside D, with a table
     for lo, R, code in ((0, 48, -2), (16, 32, -2), (32, 64, -2), (-32, 32, -1)):
-        rc = L.attn_fp8_quantize_producer(*args, 1.0, 0, None, None, vp, lo, R, ctypes.byref(m), 3, None, None)
+        rc = call(_opt(rope_cs=vp, rope_lo=lo, rope_dim=R))
         assert rc == code, (lo, R, rc, pk.last_error())
-    assert L.attn_fp8_quantize_producer(*args, 1.0, 0, None, None, None, 0, 32, ctypes.byref(m), 3, None,
-                                        None) == -1
+    assert call(_opt(rope_dim=32)) == -1
+
+
+def test_producer_workspace_size():
+    """Partial sums FP64 [B, H, D, N/32] when centering, then the norm's row
+    scales FP32 [B, N, H], each rounded up to 256 bytes; nothing otherwise."""
+    L = pk.lib()
+    vp = ctypes.c_void_p(4096).value
+    n = ctypes.c_size_t(7)
+
+    def size(B, N, H, D, opt):
+        rc = L.attn_fp8_producer_workspace_size(B, N, H, D, ctypes.byref(opt), ctypes.byref(n))
+        return rc, n.value
+    r256 = lambda b: (b + 255) // 256 * 256
+    assert size(2, 96, 3, 128, _opt()) == (0, 0)
+    assert size(2, 96, 3, 128, _opt(prescale=0.3, rope_cs=vp, rope_dim=64)) == (0, 0)
+    assert size(2, 96, 3, 128, _opt(center=1, channel_mean=vp)) == (0, r256(2 * 3 * 128 * 3 * 8))
+    assert size(2, 96, 3, 128, _opt(rms_gain=vp)) == (0, r256(2 * 96 * 3 * 4))
+    assert size(4, 8192, 4, 128, _opt(center=1, channel_mean=vp, rms_gain=vp)) == \
+        (0, 4 * 4 * 128 * 256 * 8 + r256(4 * 8192 * 4 * 4))
+    assert size(1, 100, 1, 128, _opt())[0] == -2
+    assert size(1, 96, 1, 96, _opt())[0] == -2
+    assert size(1, 96, 1, 128, _opt(prescale=0.0))[0] == -1
+    assert L.attn_fp8_producer_workspace_size(1, 96, 1, 128, None, ctypes.byref(n)) == -1
+    assert L.attn_fp8_producer_workspace_size(1, 96, 1, 128, ctypes.byref(_opt()), None) == -1
 
 
 def test_workspace_size_without_mask():
