@@ -109,13 +109,33 @@ enum {
 };
 
 /* Problem geometry, read-only.  softmax_scale (tau, e.g. 1/sqrt(dim_qk))
- * multiplies the FP32 score accumulator S = Q K^T. */
+ * multiplies the FP32 score accumulator S = Q K^T.
+ *
+ * Sequences of their own lengths (a padded batch): with seqlens_q (and,
+ * without the mask, seqlens_kv) every batch entry b is its own attention
+ * problem over its first Lq_b = seqlens_q[b] queries and Lk_b =
+ * seqlens_kv[b] keys (Lk_b = Lq_b under the mask); seqlen and seqlen_kv stay
+ * the lengths of every array's layout.  Both are nullable device int32 [B]
+ * arrays, 4-byte aligned, read by the kernels (the host never reads them).
+ * Each length must lie in [0, seqlen] / [0, seqlen_kv] and be a multiple of
+ * 32; a length outside that is clamped into it and rounded down to a
+ * multiple of 32, so no access ever leaves the arrays (the results are then
+ * those of the rounded length).  Positions at or past a sequence's length
+ * are padding: the attention kernels never read them and leave their rows
+ * of O, LSE, delta and dQ (queries) and dK, dV (keys) unwritten.  A sequence
+ * with keys and no queries gets zero dK, dV; one with queries and no keys
+ * counts as empty.  The channel maxima of Q and K (channel_amax) come from
+ * the quantizer over the whole layout, padding included: keep the padding
+ * finite (e.g. zero) for them to describe the sequences. */
 typedef struct {
   int64_t batch, seqlen, heads_q, heads_kv, dim_qk, dim_v;
   int32_t causal;          /* 1: top-left causal mask (seqlen_kv == seqlen); 0: no mask */
   float softmax_scale;
   int64_t seqlen_kv;       /* key / value length; 0 stands for seqlen */
   int32_t flags;           /* ATTN_FP8_FLAG_* (0: the paper's numerics) */
+  const int32_t* seqlens_q;   /* nullable device [B]: query length of each sequence */
+  const int32_t* seqlens_kv;  /* nullable device [B]: key length of each sequence (NULL
+                                 under the mask, where it equals the query length) */
 } attn_fp8_problem;
 
 /* One MX-quantized operand X of shape [B, N, H, D]; device memory, caller-owned.

@@ -40,7 +40,7 @@ class _Problem(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int64), ("seqlen", ctypes.c_int64), ("heads_q", ctypes.c_int64),
                 ("heads_kv", ctypes.c_int64), ("dim_qk", ctypes.c_int64), ("dim_v", ctypes.c_int64),
                 ("causal", ctypes.c_int32), ("softmax_scale", ctypes.c_float), ("seqlen_kv", ctypes.c_int64),
-                ("flags", ctypes.c_int32)]
+                ("flags", ctypes.c_int32), ("seqlens_q", ctypes.c_void_p), ("seqlens_kv", ctypes.c_void_p)]
 
 
 class _Producer(ctypes.Structure):
@@ -131,14 +131,22 @@ class Problem:
     causal: int = 1
     seqlen_kv: int = 0          # key / value length; 0 stands for seqlen
     flags: int = 0              # FLAG_* numerics options
+    # per-sequence lengths of a padded batch: device int32 [batch] tensors
+    # (seqlens_kv without the mask only), or None for the full lengths
+    seqlens_q: torch.Tensor | None = None
+    seqlens_kv: torch.Tensor | None = None
 
     @property
     def nk(self) -> int:
         return self.seqlen_kv if self.seqlen_kv else self.seqlen
 
     def c(self):
+        for t in (self.seqlens_q, self.seqlens_kv):
+            assert t is None or (t.dtype == torch.int32 and t.is_contiguous() and t.numel() == self.batch), \
+                "seqlens: contiguous int32 [batch] tensors"
         return _Problem(self.batch, self.seqlen, self.heads_q, self.heads_kv, self.dim_qk, self.dim_v,
-                        self.causal, self.softmax_scale, self.seqlen_kv, self.flags)
+                        self.causal, self.softmax_scale, self.seqlen_kv, self.flags,
+                        _ptr(self.seqlens_q).value, _ptr(self.seqlens_kv).value)
 
 
 @dataclass

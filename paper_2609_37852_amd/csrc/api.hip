@@ -96,6 +96,10 @@ int check_problem(const attn_fp8_problem* p) {
   if (p->causal != 0 && p->causal != 1) return fail(ATTN_FP8_EINVAL, "causal must be 0 or 1");
   if (p->flags & ~ATTN_FP8_FLAG_PBWD_BLOCK_SCALED) return fail(ATTN_FP8_EINVAL, "unknown flags 0x%x", p->flags);
   if (p->seqlen_kv < 0) return fail(ATTN_FP8_EINVAL, "negative seqlen_kv");
+  if (p->causal && p->seqlens_kv)
+    return fail(ATTN_FP8_EINVAL, "seqlens_kv with the causal mask (the key length is the query length)");
+  if ((reinterpret_cast<uintptr_t>(p->seqlens_q) | reinterpret_cast<uintptr_t>(p->seqlens_kv)) & 3u)
+    return fail(ATTN_FP8_EALIGN, "seqlens_q / seqlens_kv not 4-byte aligned");
   const int64_t nk = kv_len(p);
   if (p->causal && nk != p->seqlen)
     return fail(ATTN_FP8_EUNSUPPORTED, "causal attention needs seqlen_kv == seqlen (%lld != %lld)", (long long)nk,
@@ -140,6 +144,8 @@ afp8::AttnArgs base_args(const attn_fp8_problem* p) {
   a.Nk = kv_len(p);
   a.causal = p->causal;
   a.pmx = (p->flags & ATTN_FP8_FLAG_PBWD_BLOCK_SCALED) != 0;
+  a.lens_q = p->seqlens_q;
+  a.lens_k = p->causal ? nullptr : p->seqlens_kv;
   a.tau = p->softmax_scale;
   a.c = (float)((double)p->softmax_scale * 1.4426950408889634);
   return a;
@@ -246,6 +252,9 @@ int launch_delta(const attn_fp8_problem* p, int mode, const attn_fp8_mx* q, cons
   s.N = p->seqlen;
   s.Hq = p->heads_q;
   s.Dv = (int)p->dim_v;
+  s.lens_q = p->seqlens_q;
+  s.lens_k = p->causal ? nullptr : p->seqlens_kv;
+  s.Nk = kv_len(p);
   if (mode == ATTN_FP8_DELTA_CONSISTENT_DO) {
     s.do_code = dout->code_row;
     s.do_scale = dout->scale_row;

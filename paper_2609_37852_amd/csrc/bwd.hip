@@ -18,12 +18,14 @@ namespace afp8 {
 //   tile_kcs [B, Hkv, ceil(Nk/64)] x 2 Dqk B: the same for K per 64-key step
 //           (dq_kernel).
 // Workgroup x covers queries and keys 64 x .. 64 x + 63 (either may lie past
-// its sequence).
+// its sequence; "the end" is the sequence's own length, the layouts have N
+// and Nk rows).
 template <int DQK, int DV>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
   __shared__ int hot_slot;
   const int N = (int)a.N, Nk = (int)a.Nk;
   const int h = blockIdx.y, b = blockIdx.z, kh = h / (int)a.G;
+  const SeqLens L = a.causal ? seq_lens<true>(a, b, N, Nk) : seq_lens<false>(a, b, N, Nk);
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
   const size_t bh = (size_t)b * a.Hq + h;
   const int i0 = blockIdx.x * 64;
@@ -31,7 +33,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
     uint8_t* blk = reinterpret_cast<uint8_t*>(a.rows) + (bh * ((N + 63) / 64) + blockIdx.x) * 1024;
     float2 pr = make_float2(0.f, 0.f);
     float nd = 0.f, ndl = 0.f;
-    if (i0 + (int)threadIdx.x < N) {
+    if (i0 + (int)threadIdx.x < L.q) {
       const size_t row = bh * N + i0 + threadIdx.x;
       const float2 d = *reinterpret_cast<const float2*>(a.delta + row * 2);
       const float qh = hot >= 0 ? row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot) : 0.f;
@@ -43,8 +45,8 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
     reinterpret_cast<float*>(blk + 512)[threadIdx.x] = nd;
     reinterpret_cast<float*>(blk + 768)[threadIdx.x] = ndl;
   }
-  if (i0 < N) {
-    const int g0 = i0 / 32, g1 = (i0 + 32 < N ? i0 + 32 : i0) / 32;
+  if (i0 < L.q) {
+    const int g0 = i0 / 32, g1 = (i0 + 32 < L.q ? i0 + 32 : i0) / 32;
     uint8_t* dst = a.tile_cs + (bh * ((N + 63) / 64) + blockIdx.x) * (2 * (DQK + DV));
     for (int u = threadIdx.x; u < DQK + DV; u += 256) {
       const uint8_t* src = u < DQK ? a.qc_scale + (bh * DQK + u) * (N / 32)
@@ -54,8 +56,8 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
     }
   }
   // the K col scales of keys i0 .., once per KV head (for dq_kernel)
-  if (h < a.Hkv && i0 < Nk) {
-    const int g0 = i0 / 32, g1 = (i0 + 32 < Nk ? i0 + 32 : i0) / 32;
+  if (h < a.Hkv && i0 < L.k) {
+    const int g0 = i0 / 32, g1 = (i0 + 32 < L.k ? i0 + 32 : i0) / 32;
     const size_t bk = (size_t)b * a.Hkv + h;
     uint8_t* dk = a.tile_kcs + (bk * ((Nk + 63) / 64) + blockIdx.x) * (2 * DQK);
     for (int u = threadIdx.x; u < DQK; u += 256) {
@@ -75,7 +77,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
 // registers one step ahead); the K col tile of the step [Dqk][64] and its
 // scales reach LDS by direct loads, double-buffered and shared by the 4
 // waves.  Keys past the sequence meet zero dS' codes (their K loads are
-// clamped into the array).
+// clamped to the sequence's last keys).
 template <int DQK>
 __global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
   constexpr int CQ = DQK / 32, NW = 4;
@@ -85,17 +87,21 @@ __global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
   const int lane = threadIdx.x & 63, w = wave_id(), hf = lane >> 5, li = lane & 31;
   const int N = (int)a.N, Nk = (int)a.Nk, nqb = N / 32;
   const bool causal = a.causal != 0;
-  const int nks = (Nk + 63) / 64;                    // 64-key steps over the keys
+  const int nks = (Nk + 63) / 64;                    // 64-key steps over the keys (unit layout)
   const int ntile = (nqb + NW - 1) / NW;
   const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);
   const int tile = ntile - 1 - wc.r;                 // longest rows first
   const int h = wc.h, b = wc.b, kh = h / (int)a.G;
+  // the sequence's own lengths bound the work
+  const SeqLens L = causal ? seq_lens<true>(a, b, N, Nk) : seq_lens<false>(a, b, N, Nk);
+  const int nqs = L.q / 32, nkss = (L.k + 63) / 64;
+  if (NW * tile >= nqs) return;                      // the whole tile is past the sequence
   const int qb = NW * tile + w;                      // this wave's 32-query block
-  const int qlast = NW * tile + NW - 1 < nqb - 1 ? NW * tile + NW - 1 : nqb - 1;
-  const int nk = qb < nqb ? (causal ? qb / 2 + 1 : nks) : 0;   // this wave's 64-key steps
-  const int nkw = causal ? qlast / 2 + 1 : nks;                 // the workgroup's
+  const int qlast = NW * tile + NW - 1 < nqs - 1 ? NW * tile + NW - 1 : nqs - 1;
+  const int nk = qb < nqs ? (causal ? qb / 2 + 1 : nkss) : 0;   // this wave's 64-key steps
+  const int nkw = causal ? qlast / 2 + 1 : nkss;                 // the workgroup's
   const int64_t bh = (int64_t)b * a.Hq + h;
-  const int64_t unit0 = bh * units_before(nqb, nks, causal) + units_before(qb < nqb ? qb : 0, nks, causal);
+  const int64_t unit0 = bh * units_before(nqb, nks, causal) + units_before(qb < nqs ? qb : 0, nks, causal);
   const uint8_t* units = a.ds_units + unit0 * 2048 + 16 * lane;
   const uint8_t* ex = a.ds_exp + unit0 * 2;
   const int64_t bk = (int64_t)b * a.Hkv + kh;
@@ -104,7 +110,7 @@ __global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
 
   const Buf tkb = make_buf(tk, (uint32_t)nks * KSB);
   auto issue = [&](lds8* dst, int ks) __attribute__((always_inline)) {
-    dma_cols<DQK, NW>(dst, kc, 64 * ks, Nk, w, lane);
+    dma_cols<DQK, NW>(dst, kc, 64 * ks, Nk, L.k, w, lane);
     constexpr int NI = (KSB + 255) / 256;
     for (int k = 0; k < NI; k++) {
       if ((NW - 1 - k) != w) continue;
@@ -134,21 +140,21 @@ __global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
     }
   };
   Aop a0, a1;
-  if (qb < nqb) load_a(a0, 0);
+  if (qb < nqs) load_a(a0, 0);
   issue((lds8*)kA, 0);
   lds_barrier();
   for (int ks = 0; ks < nkw; ks += 2) {
     if (ks + 1 < nkw) issue((lds8*)kB, ks + 1);
-    if (qb < nqb) load_a(a1, ks + 1);
+    if (qb < nqs) load_a(a1, ks + 1);
     if (ks < nk) compute(kA, a0);
     lds_barrier();
     if (ks + 1 >= nkw) break;
     if (ks + 2 < nkw) issue((lds8*)kA, ks + 2);
-    if (qb < nqb) load_a(a0, ks + 2);
+    if (qb < nqs) load_a(a0, ks + 2);
     if (ks + 1 < nk) compute(kB, a1);
     lds_barrier();
   }
-  if (qb >= nqb) return;
+  if (qb >= nqs) return;
   // lane holds channel 32 i + li, queries 32 qb + 8 (r/4) + 4 hf + r % 4
 #pragma unroll
   for (int r = 0; r < 16; r++) {

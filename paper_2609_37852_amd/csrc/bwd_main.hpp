@@ -175,19 +175,21 @@ __device__ __forceinline__ int loader_index() {
 }
 
 // Direct-to-LDS loads of the row part of one query tile (head hi of the
-// group, queries i0..): codes, row scales and the per-query records.
+// group, queries i0..): codes, row scales and the per-query records.  N is
+// the layouts' query length, lim the sequence's (queries at or past it are
+// clamped to its last ones).
 template <int DQK, int DV>
 __device__ __forceinline__ void stage_rows(lds8* st, const BwdLoads<DQK, DV>& L, const BwdGroup& g, int G, int hi,
-                                           int i0, int N) {
+                                           int i0, int N, int lim) {
   using C = BwdCfg<DQK, DV>;
   constexpr int NWK = C::NLD;
   const int lane = threadIdx.x & 63, w = loader_index<DQK, DV>();
   if (w < 0) return;
   const BwdStrides<DQK, DV> S{N};
-  L.q.issue_s(st + C::Q_OFF, make_buf(g.qrow, G * S.q()), hi * S.q(), i0, N, w, lane);
-  L.o.issue_s(st + C::O_OFF, make_buf(g.orow, G * S.o()), hi * S.o(), i0, N, w, lane);
-  dma_row_scales_s<DQK, NWK>(st + C::QS_OFF, make_buf(g.qsc, G * S.qs()), hi * S.qs(), i0, N, w, lane, 0);
-  dma_row_scales_s<DV, NWK>(st + C::OS_OFF, make_buf(g.osc, G * S.os()), hi * S.os(), i0, N, w, lane, 1);
+  L.q.issue_s(st + C::Q_OFF, make_buf(g.qrow, G * S.q()), hi * S.q(), i0, lim, w, lane);
+  L.o.issue_s(st + C::O_OFF, make_buf(g.orow, G * S.o()), hi * S.o(), i0, lim, w, lane);
+  dma_row_scales_s<DQK, NWK>(st + C::QS_OFF, make_buf(g.qsc, G * S.qs()), hi * S.qs(), i0, lim, w, lane, 0);
+  dma_row_scales_s<DV, NWK>(st + C::OS_OFF, make_buf(g.osc, G * S.os()), hi * S.os(), i0, lim, w, lane, 1);
   if (w == (3 % NWK)) {
     dma16s(make_buf(g.rows, G * S.rows()), (uint32_t)lane * 16, hi * S.rows() + (uint32_t)(i0 / 64) * 1024,
            st + C::ROW_OFF);
@@ -197,14 +199,14 @@ __device__ __forceinline__ void stage_rows(lds8* st, const BwdLoads<DQK, DV>& L,
 // ... and of its col part: codes and the col scales packed by bwd_prep.
 template <int DQK, int DV>
 __device__ __forceinline__ void stage_cols(lds8* st, const BwdLoads<DQK, DV>& L, const BwdGroup& g, int G, int hi,
-                                           int i0, int N) {
+                                           int i0, int N, int lim) {
   using C = BwdCfg<DQK, DV>;
   constexpr int NWK = C::NLD;
   const int lane = threadIdx.x & 63, w = loader_index<DQK, DV>();
   if (w < 0) return;
   const BwdStrides<DQK, DV> S{N};
-  L.qc.issue_s(st + C::QC_OFF, make_buf(g.qcol, G * S.q()), hi * S.q(), i0, N, w, lane);
-  L.oc.issue_s(st + C::OC_OFF, make_buf(g.ocol, G * S.o()), hi * S.o(), i0, N, w, lane);
+  L.qc.issue_s(st + C::QC_OFF, make_buf(g.qcol, G * S.q()), hi * S.q(), i0, N, lim, w, lane);
+  L.oc.issue_s(st + C::OC_OFF, make_buf(g.ocol, G * S.o()), hi * S.o(), i0, N, lim, w, lane);
   constexpr int NCI = (C::CS_BYTES + 255) / 256;
   for (int k = 0; k < NCI; k++) {
     if ((2 + k) % NWK != w) continue;   // loaders 2, 3, ...: 0 and 1 take the row scales
@@ -313,8 +315,11 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   const int kb0 = kbk.kb * BKB;
   const bool up = kbk.up;
   const int kh = ((int)blockIdx.x % GI) % (int)a.Hkv, b = ((int)blockIdx.x % GI) / (int)a.Hkv;
+  // the sequence's own lengths bound the work; N and Nk remain the strides
+  const SeqLens L = seq_lens<CAUSAL>(a, b, N, Nk);
+  if (kb0 >= L.k) return;                       // the whole key block is past the sequence
   const int kw0 = kb0 + 32 * kbw;               // this wave's first key
-  const bool live = kw0 < Nk;
+  const bool live = kw0 < L.k;
   const int kj = kw0 + li;                      // this lane's key
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
   const size_t bhk = (size_t)b * a.Hkv + kh;
@@ -378,8 +383,8 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
 #pragma unroll
     for (int r = 0; r < 16; r++) acc[i][r] = 0.f;
 
-  const int nqt = (N + BQ - 1) / BQ, qt0 = causal ? kb0 / BQ : 0, nq = nqt - qt0;
-  const int total = G * nq;
+  const int nqt = (L.q + BQ - 1) / BQ, qt0 = causal ? kb0 / BQ : 0, nq = nqt - qt0;
+  const int total = G * nq;                     // 0 only for a sequence without queries
   const size_t bh0 = (size_t)b * Hq + (size_t)kh * G;   // first query head of the group
   const int nks = (Nk + 63) / 64;               // 64-key steps of the dQ units
   const int64_t units_per_head = units_before(N / 32, nks, causal);
@@ -505,8 +510,8 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
       __attribute__((always_inline)) {
     const int i0 = q0_of(p);
     const int qb = i0 + 32 * qs;
-    const bool full = (causal ? i0 >= kb0 + BKB : kb0 + BKB <= Nk) && i0 + BQ <= N;
-    const bool skip = !full && (!live || (causal && qb < kw0) || qb >= N);
+    const bool full = (causal ? i0 >= kb0 + BKB : kb0 + BKB <= L.k) && i0 + BQ <= L.q;
+    const bool skip = !full && (!live || (causal && qb < kw0) || qb >= L.q);
     const int h = kh * G + p.hi;
     if (full) probs(std::false_type{}, qb, skip, h, R);
     else probs(std::true_type{}, qb, skip, h, R);
@@ -524,8 +529,8 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   auto front_skip = [&](TilePos p) __attribute__((always_inline)) {
     const int i0 = q0_of(p);
     const int qb = i0 + 32 * qs;
-    const bool full = (causal ? i0 >= kb0 + BKB : kb0 + BKB <= Nk) && i0 + BQ <= N;
-    return !full && (!live || (causal && qb < kw0) || qb >= N);
+    const bool full = (causal ? i0 >= kb0 + BKB : kb0 + BKB <= L.k) && i0 + BQ <= L.q;
+    return !full && (!live || (causal && qb < kw0) || qb >= L.q);
   };
 
   // The MFMAs of one pipeline step, as one straight sequence: S and dP of the
@@ -650,7 +655,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
     if (w >= 2 * KSN) return;
     const int uq = w / KSN, ks = w % KSN;
     const int qb = i0 + 32 * uq;
-    if (qb >= N || (CAUSAL ? kb0 + 64 * ks > qb + 31 : kb0 + 64 * ks >= Nk)) return;
+    if (qb >= L.q || (CAUSAL ? kb0 + 64 * ks > qb + 31 : kb0 + 64 * ks >= L.k)) return;
     uint32_t ex2 = *reinterpret_cast<const uint16_t*>(es + uq * KBW + 2 * ks);
     asm volatile("" : "+v"(ex2));
     const int i16 = lane & 15;
@@ -691,28 +696,31 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
     ds_store(p, ds, es);
     const float rec = row_rec(R1);
     if constexpr (NCB == 2) {
-      if (more) stage_cols<DQK, DV>(Cl, ld, grp, G, p1.hi, q0_of(p1), N);
+      if (more) stage_cols<DQK, DV>(Cl, ld, grp, G, p1.hi, q0_of(p1), N, L.q);
     }
-    if (i + 2 < total) stage_rows<DQK, DV>(Rl, ld, grp, G, p2.hi, q0_of(p2), N);
+    if (i + 2 < total) stage_rows<DQK, DV>(Rl, ld, grp, G, p2.hi, q0_of(p2), N, L.q);
     const bool skip1 = !more || front_skip(p1);
     mfmas(R1, skip1, rec, Cc, es, x, std::true_type{});
     __builtin_amdgcn_sched_barrier(0);   // every MFMA issues before the VALU work below
     if constexpr (NCB == 1) {
       lds_sync();                          // every wave has read the col operands of tile i
-      if (more) stage_cols<DQK, DV>(Cl, ld, grp, G, p1.hi, q0_of(p1), N);
+      if (more) stage_cols<DQK, DV>(Cl, ld, grp, G, p1.hi, q0_of(p1), N, L.q);
     }
     if (more) front_vals(p1, R1, ds1, es1, x1);
   };
 
   // prologue: rows of tiles 0 and 1, cols of tile 0; S, dP, P, dS of tile 0
+  // (none without queries: the key gradients are then zero)
   const TilePos p0 = TilePos{0, 0};
-  stage_rows<DQK, DV>((lds8*)rA, ld, grp, G, p0.hi, q0_of(p0), N);
-  stage_cols<DQK, DV>((lds8*)cA, ld, grp, G, p0.hi, q0_of(p0), N);
-  TilePos pa = next_pos(p0, G);
-  if (total > 1) stage_rows<DQK, DV>((lds8*)rB, ld, grp, G, pa.hi, q0_of(pa), N);
-  lds_barrier();
-  mfmas(rA, front_skip(p0), row_rec(rA), cA, esA, xA, std::false_type{});
-  front_vals(p0, rA, dsA, esA, xA);
+  if (total > 0) {
+    stage_rows<DQK, DV>((lds8*)rA, ld, grp, G, p0.hi, q0_of(p0), N, L.q);
+    stage_cols<DQK, DV>((lds8*)cA, ld, grp, G, p0.hi, q0_of(p0), N, L.q);
+    TilePos pa = next_pos(p0, G);
+    if (total > 1) stage_rows<DQK, DV>((lds8*)rB, ld, grp, G, pa.hi, q0_of(pa), N, L.q);
+    lds_barrier();
+    mfmas(rA, front_skip(p0), row_rec(rA), cA, esA, xA, std::false_type{});
+    front_vals(p0, rA, dsA, esA, xA);
+  }
 
   TilePos p = p0;
   for (int i = 0; i < total; i += 2) {

@@ -64,11 +64,14 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);
   const int qb = nqb - 1 - wc.r;              // longest causal rows first
   const int h = wc.h, b = wc.b, kh = h / (int)a.G;
+  // the sequence's own lengths bound the work; N and Nk remain the strides
+  const SeqLens L = seq_lens<CAUSAL>(a, b, N, Nk);
+  if (qb * BQ >= L.q) return;                 // the whole block is past the sequence
   const int q0 = qb * BQ + 32 * w;
-  const bool live = q0 < N;
+  const bool live = q0 < L.q;
   const int qi = q0 + li;
   // groups visible to the wave's queries start before klim (a multiple of 32)
-  const int klim = causal ? q0 + 32 : Nk;
+  const int klim = causal ? q0 + 32 : L.k;
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
 
   const size_t bhq = (size_t)b * a.Hq + h, bhk = (size_t)b * a.Hkv + kh;
@@ -100,7 +103,7 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   const uint8_t* vcode = a.v_code + bhk * Nk * DV;
   const uint8_t* vscale = a.v_scale + bhk * Nk * (DV / 32);
   // key tiles up to the block's last query, or over all keys
-  const int kend = causal ? ((qb + 1) * BQ < N ? (qb + 1) * BQ : N) : Nk;
+  const int kend = causal ? ((qb + 1) * BQ < L.q ? (qb + 1) * BQ : L.q) : L.k;
   const int ntiles = (kend + BK - 1) / BK;
 
   // loads of tile j0 (raw isolated-channel bytes in registers, decoded when
@@ -111,12 +114,13 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   kload.init(w, lane);
   vload.init(w, lane);
   auto issue = [&](lds8* st, int j0) __attribute__((always_inline)) {
-    kload.issue(st + C::K_OFF, kcode, j0, Nk, w, lane);
-    vload.issue(st + C::V_OFF, vcode, j0, Nk, w, lane);
-    dma_row_scales<DQK, NW, BK>(st + C::KS_OFF, kscale, j0, Nk, w, lane, 0);
-    dma_row_scales<DV, NW, BK>(st + C::VS_OFF, vscale, j0, Nk, w, lane, 1);
+    // keys past the sequence are clamped to its last ones (never the padding)
+    kload.issue(st + C::K_OFF, kcode, j0, L.k, w, lane);
+    vload.issue(st + C::V_OFF, vcode, j0, L.k, w, lane);
+    dma_row_scales<DQK, NW, BK>(st + C::KS_OFF, kscale, j0, L.k, w, lane, 0);
+    dma_row_scales<DV, NW, BK>(st + C::VS_OFF, vscale, j0, L.k, w, lane, 1);
     if (hot >= 0 && threadIdx.x < BK) {
-      const int r = j0 + (int)threadIdx.x < Nk ? j0 + (int)threadIdx.x : Nk - 1;
+      const int r = j0 + (int)threadIdx.x < L.k ? j0 + (int)threadIdx.x : L.k - 1;
       khc = kcode[(int64_t)r * DQK + hot];
       khs = kscale[(int64_t)r * (DQK / 32) + hot / 32];
     }
@@ -191,7 +195,7 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   auto tile = [&](const uint8_t* st, int j0) __attribute__((always_inline)) {
     if (!live || j0 >= klim) return;
     v16f s0, dp0, s1, dp1;
-    if (causal ? j0 + BK <= q0 : j0 + BK <= Nk) {
+    if (causal ? j0 + BK <= q0 : j0 + BK <= L.k) {
       // every key visible to every query of the wave: every group, no mask;
       // the MFMAs of group g + 1 are issued before the vector work of group g
       group_mfma(st, 0, s0, dp0);

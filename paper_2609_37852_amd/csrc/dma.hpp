@@ -90,16 +90,17 @@ __device__ __forceinline__ void dma_rows(lds8* lds, const uint8_t* code, int i0,
     dma16(b, (uint32_t)(row * D + 16 * (p ^ swz_row<D>(r))), lds + 1024 * k);
   }
 }
-// Col-copy code tile: channels [0, D), queries [i0, i0 + 64) (clamped) -> [D][64].
+// Col-copy code tile: channels [0, D), queries [i0, i0 + 64) of a [D][N]
+// matrix, clamped to the first lim (<= N, >= 16) -> [D][64].
 template <int D, int NWK>
-__device__ __forceinline__ void dma_cols(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) {
+__device__ __forceinline__ void dma_cols(lds8* lds, const uint8_t* code, int i0, int N, int lim, int w, int lane) {
   constexpr int NI = D * 64 / 1024;
   const Buf b = make_buf(code, (uint32_t)D * N);
   for (int k = w; k < NI; k += NWK) {
     const int off = 1024 * k + 16 * lane;
     const int c = off / 64, p = (off % 64) / 16;
     const int q = p ^ swz_col(c);
-    const int col = i0 + 16 * q < N - 16 ? i0 + 16 * q : N - 16;
+    const int col = i0 + 16 * q < lim - 16 ? i0 + 16 * q : lim - 16;
     dma16(b, (uint32_t)(c * N + col), lds + 1024 * k);
   }
 }
@@ -228,7 +229,8 @@ struct RowLoads {
 // Col tile: channels [0, D), sequence positions [i0, i0 + COLS) of a [D][N]
 // code matrix -> LDS [D][COLS] (COLS = 64: the col-tile swizzle; 128: the
 // 128-byte row swizzle; both repeat with the channel step of one wave's
-// instructions).
+// instructions).  Positions at or past lim (<= N, >= 16) are clamped to the
+// last 16 before it.
 template <int D, int NWK, int COLS = 64>
 struct ColLoads {
   static_assert(COLS == 64 || COLS == 128, "col tile width");
@@ -244,9 +246,10 @@ struct ColLoads {
     off = (uint32_t)(c * N + 16 * q);
     cstride = CSTEP * N;
   }
-  __device__ __forceinline__ void issue(lds8* lds, const uint8_t* code, int i0, int N, int w, int lane) const {
+  __device__ __forceinline__ void issue(lds8* lds, const uint8_t* code, int i0, int N, int lim, int w,
+                                        int lane) const {
     const Buf b = make_buf(code, (uint32_t)D * N);
-    if (i0 + COLS > N) {
+    if (i0 + COLS > lim) {
       // ragged tile: clamp every 16-byte piece into its row
 #pragma unroll
       for (int j = 0; j < NS; j++) {
@@ -255,7 +258,7 @@ struct ColLoads {
         const int o = 1024 * k + 16 * lane;
         const int c = o / COLS, p = (o % COLS) / 16;
         const int q = COLS == 64 ? (p ^ swz_col(c)) : (p ^ swz_row<128>(c));
-        const int col = i0 + 16 * q < N - 16 ? i0 + 16 * q : N - 16;
+        const int col = i0 + 16 * q < lim - 16 ? i0 + 16 * q : lim - 16;
         dma16(b, (uint32_t)(c * N + col), lds + 1024 * k);
       }
       return;
@@ -268,9 +271,9 @@ struct ColLoads {
     }
   }
   // The same for a matrix at byte offset `head` inside buffer b.
-  __device__ __forceinline__ void issue_s(lds8* lds, const Buf& b, uint32_t head, int i0, int N, int w,
+  __device__ __forceinline__ void issue_s(lds8* lds, const Buf& b, uint32_t head, int i0, int N, int lim, int w,
                                           int lane) const {
-    if (i0 + COLS > N) {
+    if (i0 + COLS > lim) {
 #pragma unroll
       for (int j = 0; j < NS; j++) {
         const int k = w + NWK * j;
@@ -278,7 +281,7 @@ struct ColLoads {
         const int o = 1024 * k + 16 * lane;
         const int c = o / COLS, p = (o % COLS) / 16;
         const int q = COLS == 64 ? (p ^ swz_col(c)) : (p ^ swz_row<128>(c));
-        const int col = i0 + 16 * q < N - 16 ? i0 + 16 * q : N - 16;
+        const int col = i0 + 16 * q < lim - 16 ? i0 + 16 * q : lim - 16;
         dma16s(b, (uint32_t)(c * N + col), head, lds + 1024 * k);
       }
       return;

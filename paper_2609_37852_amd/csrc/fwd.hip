@@ -83,12 +83,15 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);
   const int qb = nqb - 1 - wc.r;              // longest causal rows first
   const int h = wc.h, b = wc.b, kh = h / (int)a.G;
+  // the sequence's own lengths bound the work; N and Nk remain the strides
+  const SeqLens L = seq_lens<CAUSAL>(a, b, N, Nk);
+  if (qb * BQ >= L.q) return;                 // the whole block is past the sequence
   const int q0 = qb * BQ + 32 * w;
-  const bool live = q0 < N;
+  const bool live = q0 < L.q;
   const int qi = q0 + li;
   // keys j0 .. visible to the wave's queries start groups before klim (a
-  // multiple of 32): the diagonal group's end when causal, else Nk
-  const int klim = causal ? q0 + 32 : Nk;
+  // multiple of 32): the diagonal group's end when causal, else the key length
+  const int klim = causal ? q0 + 32 : L.k;
   const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
 
   const size_t bhq = (size_t)b * a.Hq + h, bhk = (size_t)b * a.Hkv + kh;
@@ -120,7 +123,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   float lsum = 0.f;
   const float c = a.c;
   // key tiles up to the block's diagonal, or over all keys
-  const int ntiles = causal ? (qb + 1) * (BQ / BK) : (Nk + BK - 1) / BK;
+  const int ktiles = (L.k + BK - 1) / BK;
+  const int ntiles = causal && (qb + 1) * (BQ / BK) < ktiles ? (qb + 1) * (BQ / BK) : ktiles;
 
   // Loads of tile j0: codes and K scales straight to LDS; the V col scales
   // (4 strided bytes per channel) and the isolated-channel bytes of each key
@@ -132,18 +136,19 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   kload.init(w, lane);
   vload.init(w, lane, Nk);
   auto issue = [&](lds8* st, int j0) __attribute__((always_inline)) {
-    kload.issue(st + C::K_OFF, kcode, j0, Nk, w, lane);
-    vload.issue(st + C::V_OFF, vcode, j0, Nk, w, lane);
-    dma_row_scales<DQK, NW, BK>(st + C::KS_OFF, kscale, j0, Nk, w, lane, 0);
+    // keys past the sequence are clamped to its last ones (never the padding)
+    kload.issue(st + C::K_OFF, kcode, j0, L.k, w, lane);
+    vload.issue(st + C::V_OFF, vcode, j0, Nk, L.k, w, lane);
+    dma_row_scales<DQK, NW, BK>(st + C::KS_OFF, kscale, j0, L.k, w, lane, 0);
     if (threadIdx.x < DV) {
 #pragma unroll
       for (int g = 0; g < BK / 32; g++) {
-        const int grp = (j0 + 32 * g < Nk ? j0 + 32 * g : Nk - 32) / 32;
+        const int grp = (j0 + 32 * g < L.k ? j0 + 32 * g : L.k - 32) / 32;
         vsr[g] = vscale[threadIdx.x * (Nk / 32) + grp];
       }
     }
     if (hot >= 0 && threadIdx.x < BK) {
-      const int r = j0 + (int)threadIdx.x < Nk ? j0 + (int)threadIdx.x : Nk - 1;
+      const int r = j0 + (int)threadIdx.x < L.k ? j0 + (int)threadIdx.x : L.k - 1;
       khc = kcode[(int64_t)r * DQK + hot];
       khs = kscale[(int64_t)r * (DQK / 32) + hot / 32];
     }

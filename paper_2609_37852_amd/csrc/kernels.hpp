@@ -51,6 +51,11 @@ struct StaleArgs {
   float* delta;              // [B, Hq, N, 2]
   int64_t B, N, Hq;
   int Dv;
+  // nullable [B]: query and key length of each sequence (rows past the
+  // query length, and every row of a sequence without keys, are skipped)
+  const int32_t* lens_q;
+  const int32_t* lens_k;
+  int64_t Nk;
 };
 
 // Shared by the forward, the matched-correction pass and the backward.
@@ -91,7 +96,36 @@ struct AttnArgs {
   int grad_bf16;
   int bwd_cohort;                      // backward: workgroups of one KV head that run at once (set at launch)
   double* rowstats;                    // nullable [B,Hq,N,kRowStats]
+  // Padded batch of sequences of their own lengths (nullable [B] each):
+  // sequence b has lens_q[b] queries and lens_k[b] keys, at the first
+  // positions of the N / Nk of the layouts above; NULL: N and Nk
+  const int32_t* lens_q;
+  const int32_t* lens_k;
 };
+
+// Query and key length of sequence b as the kernels use them: the given
+// length clamped into [0, N] / [0, Nk] and rounded down to a multiple of 32
+// (so no access leaves the arrays), the key length equal to the query length
+// under the mask, and no queries where there are no keys.
+struct SeqLens {
+  int q, k;
+};
+template <bool CAUSAL>
+__device__ __forceinline__ SeqLens seq_lens(const AttnArgs& a, int b, int N, int Nk) {
+  int q = N, k = Nk;
+  if (a.lens_q) {
+    const int v = a.lens_q[b];
+    q = (v < 0 ? 0 : v > N ? N : v) & ~31;
+  }
+  if (CAUSAL) {
+    k = q;
+  } else if (a.lens_k) {
+    const int v = a.lens_k[b];
+    k = (v < 0 ? 0 : v > Nk ? Nk : v) & ~31;
+  }
+  if (k == 0) q = 0;
+  return SeqLens{q, k};
+}
 
 hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_t s);
 hipError_t launch_stale_rowsum(const StaleArgs& a, int dout_bf16, int o_bf16, hipStream_t s);

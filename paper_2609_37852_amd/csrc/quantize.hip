@@ -385,6 +385,22 @@ __device__ __forceinline__ void load8<float>(const float* p, float (&v)[8]) {
   v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 
+// Whether (b, n, h) row `row` lies inside its sequence (per-sequence lengths
+// clamped and rounded down to a multiple of 32, a sequence without keys
+// empty, as the attention kernels take them); rows past it are neither read
+// nor written.
+__device__ __forceinline__ bool row_in_sequence(const StaleArgs& a, int64_t row) {
+  if (!a.lens_q && !a.lens_k) return true;
+  const int64_t n = (row / a.Hq) % a.N, b = row / (a.Hq * a.N);
+  if (a.lens_k) {
+    const int64_t k = a.lens_k[b];
+    if (((k < 0 ? 0 : k > a.Nk ? a.Nk : k) & ~int64_t(31)) == 0) return false;
+  }
+  if (!a.lens_q) return true;
+  const int64_t v = a.lens_q[b];
+  return n < ((v < 0 ? 0 : v > a.N ? a.N : v) & ~int64_t(31));
+}
+
 template <int DV, typename TD, typename TO, bool QDO>
 __global__ __launch_bounds__(256) void stale_rowsum_kernel(StaleArgs a) {
   constexpr int LPR = DV / 8;            // lanes per row
@@ -400,7 +416,7 @@ __global__ __launch_bounds__(256) void stale_rowsum_kernel(StaleArgs a) {
       const int64_t row = base + u * RPW + t / LPR;   // (b, n, h) position
       rr[u] = row;
       acc[u] = 0.f;
-      if (row >= nrows) continue;
+      if (row >= nrows || !row_in_sequence(a, row)) continue;
       const int64_t h = row % a.Hq, n = (row / a.Hq) % a.N, b = row / (a.Hq * a.N);
       float dv[8], ov[8];
       if constexpr (QDO) {
@@ -421,7 +437,7 @@ __global__ __launch_bounds__(256) void stale_rowsum_kernel(StaleArgs a) {
 #pragma unroll
       for (int m = LPR / 2; m >= 1; m >>= 1) acc[u] += __shfl_xor(acc[u], m);
       const int64_t row = rr[u];
-      if (sub == 0 && row < nrows) {
+      if (sub == 0 && row < nrows && row_in_sequence(a, row)) {
         const int64_t h = row % a.Hq, n = (row / a.Hq) % a.N, b = row / (a.Hq * a.N);
         *reinterpret_cast<float2*>(a.delta + ((b * a.Hq + h) * a.N + n) * 2) = make_float2(acc[u], 0.f);
       }

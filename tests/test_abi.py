@@ -250,3 +250,31 @@ def test_unknown_delta_mode_rejected():
                             ctypes.c_void_p(1 << 20), 1 << 30, None, None, None)
         assert rc == -1 and "delta_mode" in pk.last_error()
     assert pk.DELTA_MATCHING_COMPENSATED == 3
+
+
+def test_seqlens_checks():
+    """Per-sequence lengths: no key lengths under the mask (the key length is
+    the query length there), 4-byte aligned arrays."""
+    L = pk.lib()
+    m = _fake_mx()
+    st = bd._I64x3(128 * 2 * 128, 2 * 128, 128)
+
+    def fwd(**kw):
+        p = _prob(**{k: v for k, v in kw.items() if not k.startswith("seqlens")}).c()
+        p.seqlens_q = kw.get("seqlens_q")
+        p.seqlens_kv = kw.get("seqlens_kv")
+        return L.attn_fp8_fwd(ctypes.byref(p), ctypes.byref(m), ctypes.byref(m), ctypes.byref(m),
+                              ctypes.c_void_p(4096), 1, st, ctypes.c_void_p(4096), None)
+    assert fwd(seqlens_kv=4096) == -1
+    assert fwd(seqlens_q=4096, seqlens_kv=4096) == -1
+    assert fwd(seqlens_q=4098) == -3
+    assert fwd(causal=0, seqlens_kv=4094) == -3
+    n = ctypes.c_size_t(0)
+    p = _prob(causal=0).c()
+    p.seqlens_q = 4096
+    p.seqlens_kv = 8192
+    # the workspace follows the layouts, not the lengths
+    assert L.attn_fp8_bwd_workspace_size(ctypes.byref(p), ctypes.byref(n)) == 0
+    ref = ctypes.c_size_t(0)
+    assert L.attn_fp8_bwd_workspace_size(ctypes.byref(_prob(causal=0).c()), ctypes.byref(ref)) == 0
+    assert n.value == ref.value > 0
