@@ -242,10 +242,16 @@ def attention(B, N, Hq, Hkv, Dqk, Dv, tau, ops, dO_raw=None, *, flags=0, delta_m
 
 
 def attention_from_inputs(q, k, v, do, tau, *, flags=0, delta_mode=DELTA_MATCHING, o_round=ROUND_BF16,
-                          grad_round=ROUND_NONE, exact_inputs=False, **kw):
+                          grad_round=ROUND_NONE, exact_inputs=False, protected_dp=False, **kw):
     """Convenience: raw inputs q,do [B,N,Hq,D], k,v [B,Nk,Hkv,D] (exact
     values) -> quantize each (or, with exact_inputs, use the raw values for
-    both copies) -> attention().  Returns (outputs, quantized dict)."""
+    both copies) -> attention().  Returns (outputs, quantized dict).
+
+    protected_dp: the protected-dP variant (App. B.6.3, correction variants;
+    App. C.4.2): dP = dO V^T from dO and V rounded to BF16 instead of their
+    FP8 row copies (products exact, sums in FP64 here); the row copies of dO
+    and V are the operands of dP only, so every other product keeps its FP8
+    operands.  The paper pairs it with the stale correction."""
     q, k, v, do = (_f64(t) for t in (q, k, v, do))
     B, N, Hq, Dqk = q.shape
     Nk, Hkv, Dv = k.shape[1], k.shape[2], v.shape[3]
@@ -260,6 +266,9 @@ def attention_from_inputs(q, k, v, do, tau, *, flags=0, delta_mode=DELTA_MATCHIN
             qd = quantize(t)
             quant[name] = qd
             ops[name + "r"], ops[name + "c"] = dequantize(qd, Bt, Nt, Ht, Dt)
+    if protected_dp:
+        ops["dOr"] = np.ascontiguousarray(bf16_round(do).transpose(0, 2, 1, 3))
+        ops["Vr"] = np.ascontiguousarray(bf16_round(v).transpose(0, 2, 1, 3))
     out = attention(B, N, Hq, Hkv, Dqk, Dv, tau, ops, do, flags=flags, delta_mode=delta_mode,
                     o_round=o_round, grad_round=grad_round, Nk=Nk, **kw)
     return out, quant
