@@ -18,7 +18,8 @@ roofline, the paper's own timing protocol (App. C.2: clock warm-up, five
 interleaved rounds of the median of 20 timings after 5 warm-up calls, mean
 and standard error, pre-quantized inputs) for the matched and the stale
 backward, a whole step with the stale correction, the cost of the
-compensated matched correction, the same workload without the causal mask, the d = 256 workload, and the oracle's CPU rate.
+compensated matched correction, the protected-dP variant, the same workload without the causal mask,
+the d = 256 workload, and the oracle's CPU rate.
 `--gpus N` with N > 1 exits: this benchmark measures a single GPU.
 """
 from __future__ import annotations
@@ -305,6 +306,35 @@ class Runner:
         return out
 
 
+def protected_dp_line(run):
+    """The protected-dP variant (dP from BF16 operands, App. C.4.2) against
+    the FP8-dP backward, both with the stale correction: forward +
+    correction + backward, each the median of 20 timings after 5 warm-ups,
+    pre-quantized inputs."""
+    import dataclasses
+    import torch
+    pk = run.pk
+    pp = dataclasses.replace(run.p, flags=pk.FLAG_PROTECTED_DP)
+    wsp = torch.empty(pk.attn_fp8_bwd_workspace_size(pp), dtype=torch.uint8, device="cuda:0")
+    stale = pk.DELTA_STALE_ROWSUM
+
+    def protected():
+        run.fwd()
+        run.correction(stale)
+        pk.attn_fp8_bwd_protected_dp(pp, run.mq, run.mk, run.mdo, run.lse, run.do, run.v, run.o,
+                                     delta_in=run.delta, workspace=wsp, out=run.grads)
+    run.quantize()
+    t_fwd = run.timed(run.fwd)
+    t_prot = run.timed(protected)
+    t_stale = run.timed(lambda: (run.fwd(), run.correction(stale), run.bwd(stale)))
+    f, b = run.w.credited_flops()
+    del wsp
+    return {"fwd_bwd_ms": round(t_prot, 4), "bwd_ms": round(t_prot - t_fwd, 4),
+            "bwd_tflops": round(b / ((t_prot - t_fwd) * 1e-3) / 1e12, 2),
+            "fwd_bwd_stale_fp8dp_ms": round(t_stale, 4),
+            "bwd_over_fp8dp_bwd": round((t_prot - t_fwd) / (t_stale - t_fwd) - 1, 4)}
+
+
 def cpu_baseline(w, d, threads, kv_heads=2):
     """The oracle (FP64 C, OpenMP) timed on the host cores on the first
     `kv_heads` KV groups of batch 0 at the full sequence length."""
@@ -461,6 +491,7 @@ def main():
         cm, pm = run.breakdown(pk.DELTA_MATCHING_COMPENSATED), run.breakdown(pk.DELTA_MATCHING)
         line["compensated"] = {"matching": pm, "compensated": cm,
                                "step_over_matching": round(cm["step_ms"] / pm["step_ms"] - 1, 4)}
+        line["protected_dp"] = protected_dp_line(run)
         if args.workload == "gqa_d128_8k":
             # the same workload without the causal mask (every query sees all
             # 8192 keys; credited FLOPs count the full N x N products)

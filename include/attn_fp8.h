@@ -105,7 +105,15 @@ enum {
    * the paper's kernel: the fixed scale keeps probabilities below 2^-14 in
    * E4M3's subnormal range (one or two significant bits, zero below 2^-17),
    * the block scale keeps three mantissa bits at any magnitude. */
-  ATTN_FP8_FLAG_PBWD_BLOCK_SCALED = 1
+  ATTN_FP8_FLAG_PBWD_BLOCK_SCALED = 1,
+  /* The protected-dP variant (App. B.6.3, correction variants; App. C.4.2):
+   * the backward computes dP = dO V^T from BF16 operands with FP32
+   * accumulation and keeps every other product in FP8, with the stale
+   * correction.  Its backward is attn_fp8_bwd_protected_dp (attn_fp8_bwd and
+   * attn_fp8_bwd_noalloc refuse the flag, attn_fp8_delta refuses the matched
+   * modes); attn_fp8_bwd_workspace_size counts its BF16 copies.  Not with
+   * ATTN_FP8_FLAG_PBWD_BLOCK_SCALED, nor at head dims (256, 256). */
+  ATTN_FP8_FLAG_PROTECTED_DP = 2
 };
 
 /* Problem geometry, read-only.  softmax_scale (tau, e.g. 1/sqrt(dim_qk))
@@ -316,6 +324,33 @@ int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q
                  int grad_dtype, const int64_t dq_strides[3], const int64_t dk_strides[3],
                  const int64_t dv_strides[3], void* workspace, size_t workspace_bytes,
                  double* rowstats, const hipEvent_t* main_events, hipStream_t stream);
+
+/* Protected-dP backward (App. B.6.3, correction variants; App. C.4.2, the
+ * SageBwd-style precision split): attn_fp8_bwd's passes with dP = dO V^T
+ * formed from BF16 operands (dout_raw and v_raw rounded to BF16, nearest
+ * even, products exact, FP32 MFMA accumulation) instead of the FP8 row
+ * copies, and the stale correction delta_i = sum_c dO_ic O_ic (or delta_in).
+ * S, P', dS', dV, dK and dQ keep their FP8 operands and casts.
+ *   p        flags must hold ATTN_FP8_FLAG_PROTECTED_DP (so that
+ *            attn_fp8_bwd_workspace_size counts the BF16 copies of dO and V
+ *            the call packs into the workspace); head dims (64, 64),
+ *            (128, 128) or (192, 128)
+ *   q, k     row and col copies;  dout  col copy (the operand of dV)
+ *   dout_raw device [B, N, Hq, Dv] of dout_dtype with dout_strides: the
+ *            operand of dP and of the stale correction
+ *   v_raw    device [B, Nk, Hkv, Dv] of v_dtype with v_strides, 16-byte
+ *            aligned rows: the operand of dP
+ *   o        the stored output (stale correction; unused with delta_in)
+ * Other arguments, outputs and errors as attn_fp8_bwd. */
+int attn_fp8_bwd_protected_dp(const attn_fp8_problem* p, const attn_fp8_mx* q,
+                              const attn_fp8_mx* k, const attn_fp8_mx* dout, const float* lse,
+                              const void* dout_raw, int dout_dtype, const int64_t dout_strides[3],
+                              const void* v_raw, int v_dtype, const int64_t v_strides[3],
+                              const void* o, int o_dtype, const int64_t o_strides[3],
+                              const float* delta_in, void* dq, void* dk, void* dv, int grad_dtype,
+                              const int64_t dq_strides[3], const int64_t dk_strides[3],
+                              const int64_t dv_strides[3], void* workspace, size_t workspace_bytes,
+                              double* rowstats, hipStream_t stream);
 
 /* Backward without any device allocation, for callers that cannot allocate
  * (code under HIP graph capture, tight serving loops, harnesses that forbid

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libattn_fp8.so")
 
 DTYPE_F32, DTYPE_BF16 = 0, 1
 DELTA_MATCHING, DELTA_STALE_ROWSUM, DELTA_CONSISTENT_DO, DELTA_MATCHING_COMPENSATED = 0, 1, 2, 3
-FLAG_PBWD_BLOCK_SCALED = 1
+FLAG_PBWD_BLOCK_SCALED, FLAG_PROTECTED_DP = 1, 2
 QUANT_ROW, QUANT_COL, QUANT_BOTH = 1, 2, 3
 # fields of the backward's per-row statistics [B, Hq, N, ROWSTATS] (FP64)
 RS_SUM_DS, RS_SUMABS_DS, RS_SUM_DSCAST, RS_MAXABS_DS, RS_SUMABS_DSCAST, RS_MAX_PDP, RS_SUM_PCAST = range(7)
@@ -26,7 +26,7 @@ ROWSTATS = 7
 STATUS = {0: "OK", -1: "EINVAL", -2: "EUNSUPPORTED", -3: "EALIGN", -4: "EWORKSPACE", -5: "EHIP"}
 EXPORTS = ("attn_fp8_quantize", "attn_fp8_fwd", "attn_fp8_delta", "attn_fp8_bwd_workspace_size",
            "attn_fp8_bwd", "attn_fp8_bwd_noalloc", "attn_fp8_quantize_producer",
-           "attn_fp8_producer_workspace_size", "attn_fp8_last_error")
+           "attn_fp8_producer_workspace_size", "attn_fp8_bwd_protected_dp", "attn_fp8_last_error")
 NOALLOC_SCRATCH_BYTES = 64 << 20   # ATTN_FP8_NOALLOC_SCRATCH_BYTES
 
 
@@ -82,6 +82,10 @@ def lib():
         L.attn_fp8_bwd_noalloc.argtypes = [P(_Problem), i32, P(_MX), P(_MX), P(_MX), P(_MX), vp, vp, i32,
                                            P(ctypes.c_int64), vp, i32, P(ctypes.c_int64), vp, vp, vp, vp, i32,
                                            P(ctypes.c_int64), P(ctypes.c_int64), P(ctypes.c_int64), vp, vp, vp]
+        L.attn_fp8_bwd_protected_dp.argtypes = [P(_Problem), P(_MX), P(_MX), P(_MX), vp, vp, i32, P(ctypes.c_int64),
+                                                vp, i32, P(ctypes.c_int64), vp, i32, P(ctypes.c_int64), vp, vp, vp,
+                                                vp, i32, P(ctypes.c_int64), P(ctypes.c_int64), P(ctypes.c_int64), vp,
+                                                sz, vp, vp]
         L.attn_fp8_last_error.restype = ctypes.c_char_p
         for name in EXPORTS[:-1]:
             getattr(L, name).restype = ctypes.c_int
@@ -292,6 +296,34 @@ def attn_fp8_bwd(p: Problem, mode: int, q: MX, k: MX, v: MX, dout: MX, lse, dout
         _dtype_code(dq.dtype), _strides_bnh(dq), _strides_bnh(dk), _strides_bnh(dv), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _ptr(rs),
         (ctypes.c_void_p * 2)(*main_events) if main_events is not None else None, _stream(dev)))
+    return dq, dk, dv, rs
+
+
+def attn_fp8_bwd_protected_dp(p: Problem, q: MX, k: MX, dout: MX, lse, dout_raw, v_raw, o=None, delta_in=None,
+                              grad_dtype=torch.bfloat16, rowstats: bool = False, workspace=None, out=None):
+    """The protected-dP backward (dP from the BF16 dout_raw and v_raw, the
+    stale correction from dout_raw and o, or delta_in); p.flags must hold
+    FLAG_PROTECTED_DP.  Returns (dq, dk, dv, rowstats or None)."""
+    dev = q.code_row.device
+    if out is None:
+        dq = torch.empty((p.batch, p.seqlen, p.heads_q, p.dim_qk), dtype=grad_dtype, device=dev)
+        dk = torch.empty((p.batch, p.nk, p.heads_kv, p.dim_qk), dtype=grad_dtype, device=dev)
+        dv = torch.empty((p.batch, p.nk, p.heads_kv, p.dim_v), dtype=grad_dtype, device=dev)
+    else:
+        dq, dk, dv = out
+    ws_bytes = attn_fp8_bwd_workspace_size(p)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    rs = torch.zeros((p.batch, p.heads_q, p.seqlen, ROWSTATS), dtype=torch.float64, device=dev) if rowstats else None
+    pc = p.c()
+    mxs = [m.c() for m in (q, k, dout)]
+    os_ = _strides_bnh(o) if o is not None else None
+    _check("attn_fp8_bwd_protected_dp", lib().attn_fp8_bwd_protected_dp(
+        ctypes.byref(pc), *[ctypes.byref(m) for m in mxs], _ptr(lse), _ptr(dout_raw), _dtype_code(dout_raw.dtype),
+        _strides_bnh(dout_raw), _ptr(v_raw), _dtype_code(v_raw.dtype), _strides_bnh(v_raw), _ptr(o),
+        _dtype_code(o.dtype) if o is not None else 0, os_, _ptr(delta_in), _ptr(dq), _ptr(dk), _ptr(dv),
+        _dtype_code(dq.dtype), _strides_bnh(dq), _strides_bnh(dk), _strides_bnh(dv), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(rs), _stream(dev)))
     return dq, dk, dv, rs
 
 

@@ -94,7 +94,14 @@ int check_problem(const attn_fp8_problem* p) {
     return fail(ATTN_FP8_EUNSUPPORTED, "head dims (%lld, %lld) not instantiated", (long long)p->dim_qk,
                 (long long)p->dim_v);
   if (p->causal != 0 && p->causal != 1) return fail(ATTN_FP8_EINVAL, "causal must be 0 or 1");
-  if (p->flags & ~ATTN_FP8_FLAG_PBWD_BLOCK_SCALED) return fail(ATTN_FP8_EINVAL, "unknown flags 0x%x", p->flags);
+  if (p->flags & ~(ATTN_FP8_FLAG_PBWD_BLOCK_SCALED | ATTN_FP8_FLAG_PROTECTED_DP))
+    return fail(ATTN_FP8_EINVAL, "unknown flags 0x%x", p->flags);
+  if (p->flags & ATTN_FP8_FLAG_PROTECTED_DP) {
+    if (p->flags & ATTN_FP8_FLAG_PBWD_BLOCK_SCALED)
+      return fail(ATTN_FP8_EUNSUPPORTED, "protected dP with the block-scaled backward probability operand");
+    if (p->dim_qk == 256 && p->dim_v == 256)
+      return fail(ATTN_FP8_EUNSUPPORTED, "protected dP at head dims (256, 256) (its BF16 tiles exceed the LDS)");
+  }
   if (p->seqlen_kv < 0) return fail(ATTN_FP8_EINVAL, "negative seqlen_kv");
   if (p->causal && p->seqlens_kv)
     return fail(ATTN_FP8_EINVAL, "seqlens_kv with the causal mask (the key length is the query length)");
@@ -127,6 +134,9 @@ int check_problem(const attn_fp8_problem* p) {
     if (L * D >= (int64_t(1) << 32))
       return fail(ATTN_FP8_EUNSUPPORTED, "problem exceeds the 32-bit buffer offsets (max(G N, Nk) D = %lld)",
                   (long long)(L * D));
+    // protected dP: the group's BF16 dO rows take 2 bytes per element
+    if ((p->flags & ATTN_FP8_FLAG_PROTECTED_DP) && G * p->seqlen * p->dim_v * 2 >= (int64_t(1) << 32))
+      return fail(ATTN_FP8_EUNSUPPORTED, "protected dP: the BF16 dO of one group exceeds 32-bit buffer offsets");
   }
   return ATTN_FP8_OK;
 }
@@ -191,9 +201,18 @@ size_t ws_tile_cs_bytes(const attn_fp8_problem* p) {
 size_t ws_tile_kcs_bytes(const attn_fp8_problem* p) {
   return round256((size_t)p->batch * p->heads_kv * ((kv_len(p) + 63) / 64) * 2 * p->dim_qk);
 }
+// protected dP: BF16 copies of dO [B, Hq, N, Dv] and V [B, Hkv, Nk, Dv]
+size_t ws_do_bf16_bytes(const attn_fp8_problem* p) {
+  return (p->flags & ATTN_FP8_FLAG_PROTECTED_DP) ? round256((size_t)p->batch * p->heads_q * p->seqlen * p->dim_v * 2)
+                                                 : 0;
+}
+size_t ws_v_bf16_bytes(const attn_fp8_problem* p) {
+  return (p->flags & ATTN_FP8_FLAG_PROTECTED_DP) ? round256((size_t)p->batch * p->heads_kv * kv_len(p) * p->dim_v * 2)
+                                                 : 0;
+}
 size_t ws_bwd_bytes(const attn_fp8_problem* p) {
   return ws_units_bytes(p) + ws_exp_bytes(p) + ws_delta_bytes(p) + ws_rows_bytes(p) + ws_tile_cs_bytes(p) +
-         ws_tile_kcs_bytes(p);
+         ws_tile_kcs_bytes(p) + ws_do_bf16_bytes(p) + ws_v_bf16_bytes(p);
 }
 
 int hip_status(hipError_t e, const char* what) {
@@ -207,6 +226,8 @@ int check_delta_inputs(const attn_fp8_problem* p, int mode, const attn_fp8_mx* q
                        const int64_t* o_strides) {
   int rc;
   if (mode == ATTN_FP8_DELTA_MATCHING || mode == ATTN_FP8_DELTA_MATCHING_COMPENSATED) {
+    if (p->flags & ATTN_FP8_FLAG_PROTECTED_DP)
+      return fail(ATTN_FP8_EUNSUPPORTED, "the matched correction of the protected-dP variant (its dP is BF16)");
     if ((rc = check_mx("q", q, true, false)) || (rc = check_mx("k", k, true, false)) ||
         (rc = check_mx("v", v, true, false)) || (rc = check_mx("dout", dout, true, false)) ||
         (rc = check_ptr("lse", lse)))
@@ -471,14 +492,18 @@ int attn_fp8_bwd_workspace_size(const attn_fp8_problem* p, size_t* bytes) {
   return ok();
 }
 
-int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q, const attn_fp8_mx* k,
-                 const attn_fp8_mx* v, const attn_fp8_mx* dout, const float* lse, const void* dout_raw,
-                 int dout_dtype, const int64_t dout_strides[3], const void* o, int o_dtype,
-                 const int64_t o_strides[3], const float* delta_in, void* dq, void* dk, void* dv, int grad_dtype,
-                 const int64_t dq_strides[3], const int64_t dk_strides[3], const int64_t dv_strides[3],
-                 void* workspace, size_t workspace_bytes, double* rowstats, const hipEvent_t* main_events,
-                 hipStream_t stream) {
+// The backward, FP8 dP (v_raw NULL) or protected dP (dP = dO V^T from BF16
+// copies of dout_raw and v_raw packed into the workspace).
+static int bwd_impl(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q, const attn_fp8_mx* k,
+                    const attn_fp8_mx* v, const attn_fp8_mx* dout, const float* lse, const void* dout_raw,
+                    int dout_dtype, const int64_t dout_strides[3], const void* v_raw, int v_dtype,
+                    const int64_t v_strides[3], const void* o, int o_dtype, const int64_t o_strides[3],
+                    const float* delta_in, void* dq, void* dk, void* dv, int grad_dtype,
+                    const int64_t dq_strides[3], const int64_t dk_strides[3], const int64_t dv_strides[3],
+                    void* workspace, size_t workspace_bytes, double* rowstats, const hipEvent_t* main_events,
+                    hipStream_t stream) {
   int rc;
+  const bool pdp = v_raw != nullptr;
   if ((rc = check_problem(p))) return rc;
   if (delta_mode < ATTN_FP8_DELTA_MATCHING || delta_mode > ATTN_FP8_DELTA_MATCHING_COMPENSATED)
     return fail(ATTN_FP8_EINVAL, "unknown delta_mode %d", delta_mode);
@@ -486,11 +511,17 @@ int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q
   if (!gs) return fail(ATTN_FP8_EINVAL, "grad_dtype %d", grad_dtype);
   if (empty(p)) return ok();
   if ((rc = check_mx("q", q, true, true)) || (rc = check_mx("k", k, true, true)) ||
-      (rc = check_mx("v", v, true, false)) || (rc = check_mx("dout", dout, true, true)) ||
+      (!pdp && (rc = check_mx("v", v, true, false))) || (rc = check_mx("dout", dout, !pdp, true)) ||
       (rc = check_ptr("lse", lse)) || (rc = check_ptr("dq", dq)) || (rc = check_ptr("dk", dk)) ||
       (rc = check_ptr("dv", dv)) || (rc = check_strides("dq", dq_strides, gs)) ||
       (rc = check_strides("dk", dk_strides, gs)) || (rc = check_strides("dv", dv_strides, gs)))
     return rc;
+  if (pdp) {
+    if (!dtype_size(dout_dtype) || !dtype_size(v_dtype)) return fail(ATTN_FP8_EINVAL, "bad dout_raw / v_raw dtype");
+    if ((rc = check_ptr("dout_raw", dout_raw)) || (rc = check_strides("dout_raw", dout_strides, dtype_size(dout_dtype))) ||
+        (rc = check_strides("v_raw", v_strides, dtype_size(v_dtype))))
+      return rc;
+  }
   if (delta_in) {
     if ((rc = check_ptr("delta_in", delta_in))) return rc;
   } else if ((rc = check_delta_inputs(p, delta_mode, q, k, v, dout, lse, dout_raw, dout_dtype, dout_strides, o,
@@ -511,6 +542,8 @@ int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q
   float* rows = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(delta) + ws_delta_bytes(p));
   uint8_t* tile_cs = reinterpret_cast<uint8_t*>(rows) + ws_rows_bytes(p);
   uint8_t* tile_kcs = tile_cs + ws_tile_cs_bytes(p);
+  uint16_t* do_bf16 = reinterpret_cast<uint16_t*>(tile_kcs + ws_tile_kcs_bytes(p));
+  uint16_t* v_bf16 = reinterpret_cast<uint16_t*>(reinterpret_cast<uint8_t*>(do_bf16) + ws_do_bf16_bytes(p));
   if (delta_in) {
     delta = const_cast<float*>(delta_in);
   } else if ((rc = launch_delta(p, delta_mode, q, k, v, dout, lse, dout_raw, dout_dtype, dout_strides, o, o_dtype,
@@ -521,8 +554,10 @@ int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q
   afp8::AttnArgs a = base_args(p);
   set_row(q, a.q_code, a.q_scale);
   set_row(k, a.k_code, a.k_scale);
-  set_row(v, a.v_code, a.v_scale);
-  set_row(dout, a.do_code, a.do_scale);
+  if (!pdp) {
+    set_row(v, a.v_code, a.v_scale);
+    set_row(dout, a.do_code, a.do_scale);
+  }
   set_col(q, a.qc_code, a.qc_scale);
   set_col(k, a.kc_code, a.kc_scale);
   set_col(dout, a.doc_code, a.doc_scale);
@@ -545,6 +580,20 @@ int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q
   a.rows = rows;
   a.tile_cs = tile_cs;
   a.tile_kcs = tile_kcs;
+  if (pdp) {
+    a.pdp = 1;
+    a.comp = 0;
+    a.do_bf16 = do_bf16;
+    a.v_bf16 = v_bf16;
+    if ((rc = hip_status(afp8::launch_pack_bf16(dout_raw, dout_dtype == ATTN_FP8_DTYPE_BF16, dout_strides, p->batch,
+                                                p->seqlen, p->heads_q, (int)p->dim_v, a.lens_q, do_bf16, stream),
+                         "pack dO")) ||
+        (rc = hip_status(afp8::launch_pack_bf16(v_raw, v_dtype == ATTN_FP8_DTYPE_BF16, v_strides, p->batch, kv_len(p),
+                                                p->heads_kv, (int)p->dim_v, p->causal ? a.lens_q : a.lens_k, v_bf16,
+                                                stream),
+                         "pack V")))
+      return rc;
+  }
   if ((rc = hip_status(afp8::launch_bwd_prep(a, (int)p->dim_qk, (int)p->dim_v, stream), "bwd_prep"))) return rc;
   if (main_events && (rc = hip_status(hipEventRecord(main_events[0], stream), "event record"))) return rc;
   if ((rc = hip_status(afp8::launch_bwd(a, (int)p->dim_qk, (int)p->dim_v, stream), "bwd"))) return rc;
@@ -552,6 +601,39 @@ int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q
 
   if ((rc = hip_status(afp8::launch_dq(a, (int)p->dim_qk, stream), "dq"))) return rc;
   return ok();
+}
+
+int attn_fp8_bwd(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q, const attn_fp8_mx* k,
+                 const attn_fp8_mx* v, const attn_fp8_mx* dout, const float* lse, const void* dout_raw,
+                 int dout_dtype, const int64_t dout_strides[3], const void* o, int o_dtype,
+                 const int64_t o_strides[3], const float* delta_in, void* dq, void* dk, void* dv, int grad_dtype,
+                 const int64_t dq_strides[3], const int64_t dk_strides[3], const int64_t dv_strides[3],
+                 void* workspace, size_t workspace_bytes, double* rowstats, const hipEvent_t* main_events,
+                 hipStream_t stream) {
+  if (p && (p->flags & ATTN_FP8_FLAG_PROTECTED_DP))
+    return fail(ATTN_FP8_EINVAL, "a protected-dP problem takes attn_fp8_bwd_protected_dp (it reads the raw V)");
+  return bwd_impl(p, delta_mode, q, k, v, dout, lse, dout_raw, dout_dtype, dout_strides, nullptr, 0, nullptr, o,
+                  o_dtype, o_strides, delta_in, dq, dk, dv, grad_dtype, dq_strides, dk_strides, dv_strides, workspace,
+                  workspace_bytes, rowstats, main_events, stream);
+}
+
+int attn_fp8_bwd_protected_dp(const attn_fp8_problem* p, const attn_fp8_mx* q, const attn_fp8_mx* k,
+                              const attn_fp8_mx* dout, const float* lse, const void* dout_raw, int dout_dtype,
+                              const int64_t dout_strides[3], const void* v_raw, int v_dtype,
+                              const int64_t v_strides[3], const void* o, int o_dtype, const int64_t o_strides[3],
+                              const float* delta_in, void* dq, void* dk, void* dv, int grad_dtype,
+                              const int64_t dq_strides[3], const int64_t dk_strides[3],
+                              const int64_t dv_strides[3], void* workspace, size_t workspace_bytes,
+                              double* rowstats, hipStream_t stream) {
+  int rc;
+  if ((rc = check_problem(p))) return rc;
+  if (!(p->flags & ATTN_FP8_FLAG_PROTECTED_DP))
+    return fail(ATTN_FP8_EINVAL, "attn_fp8_bwd_protected_dp needs ATTN_FP8_FLAG_PROTECTED_DP in the problem's flags");
+  if (empty(p)) return ok();
+  if ((rc = check_ptr("v_raw", v_raw))) return rc;
+  return bwd_impl(p, ATTN_FP8_DELTA_STALE_ROWSUM, q, k, nullptr, dout, lse, dout_raw, dout_dtype, dout_strides, v_raw,
+                  v_dtype, v_strides, o, o_dtype, o_strides, delta_in, dq, dk, dv, grad_dtype, dq_strides, dk_strides,
+                  dv_strides, workspace, workspace_bytes, rowstats, nullptr, stream);
 }
 
 int attn_fp8_bwd_noalloc(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx* q, const attn_fp8_mx* k,
@@ -563,6 +645,8 @@ int attn_fp8_bwd_noalloc(const attn_fp8_problem* p, int delta_mode, const attn_f
                          hipStream_t stream) {
   int rc;
   if ((rc = check_problem(p))) return rc;
+  if (p->flags & ATTN_FP8_FLAG_PROTECTED_DP)
+    return fail(ATTN_FP8_EINVAL, "attn_fp8_bwd_noalloc runs the FP8-dP backward (no protected dP)");
   if (empty(p)) return ok();
   const size_t need = ws_bwd_bytes(p);
   if (need > kNoAllocScratchBytes)

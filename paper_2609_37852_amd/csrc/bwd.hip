@@ -171,6 +171,53 @@ __global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
   }
 }
 
+// BF16 copies of dO and V for the protected-dP backward: x [B, N, H, D] of
+// FP32 or BF16 with element strides {sb, sn, sh} -> out [B, H, N, D] BF16
+// (round to nearest even), head-major like the FP8 row copies.  A thread
+// converts 8 channels (one 16-byte store); rows past a sequence's length
+// (lens, clamped and rounded down as in seq_lens) are not read.
+template <typename T>
+__global__ __launch_bounds__(256) void pack_bf16_kernel(const T* x, int64_t sb, int64_t sn, int64_t sh, int64_t B,
+                                                        int64_t N, int64_t H, int D, const int32_t* lens,
+                                                        uint16_t* out) {
+  const int64_t c8n = D / 8, total = B * N * H * c8n;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t c8 = i % c8n, r = i / c8n, h = r % H, n = (r / H) % N, b = r / (H * N);
+    if (lens) {
+      const int64_t v = lens[b];
+      if (n >= ((v < 0 ? 0 : v > N ? N : v) & ~int64_t(31))) continue;
+    }
+    const T* src = x + b * sb + n * sn + h * sh + 8 * c8;
+    uint32_t w[4];
+    if constexpr (sizeof(T) == 2) {
+      const uint4 u = *reinterpret_cast<const uint4*>(src);
+      w[0] = u.x; w[1] = u.y; w[2] = u.z; w[3] = u.w;
+    } else {
+      const float4 f0 = reinterpret_cast<const float4*>(src)[0], f1 = reinterpret_cast<const float4*>(src)[1];
+      const float f[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+#pragma unroll
+      for (int k = 0; k < 4; k++)
+        w[k] = (uint32_t)f32_to_bf16(f[2 * k]) | ((uint32_t)f32_to_bf16(f[2 * k + 1]) << 16);
+    }
+    *reinterpret_cast<uint4*>(out + ((b * H + h) * N + n) * D + 8 * c8) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+hipError_t launch_pack_bf16(const void* x, int bf16, const int64_t st[3], int64_t B, int64_t N, int64_t H, int D,
+                            const int32_t* lens, uint16_t* out, hipStream_t s) {
+  const int64_t total = B * N * H * (D / 8);
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  if (blocks == 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL(pack_bf16_kernel<uint16_t>, dim3((unsigned)blocks), dim3(256), 0, s,
+                       reinterpret_cast<const uint16_t*>(x), st[0], st[1], st[2], B, N, H, D, lens, out);
+  else
+    hipLaunchKernelGGL(pack_bf16_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, s,
+                       reinterpret_cast<const float*>(x), st[0], st[1], st[2], B, N, H, D, lens, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_dq(const AttnArgs& a, int dqk, hipStream_t s) {
   const dim3 grid((unsigned)((a.N / 32 + 3) / 4 * a.Hq * a.B));
   switch (dqk) {
@@ -204,6 +251,7 @@ static hipError_t bwd_dispatch(const AttnArgs& a0, hipStream_t s) {
   AttnArgs a = a0;
   const int64_t per_head = cus / (a.B * a.Hkv);
   a.bwd_cohort = (int)(per_head > 1 ? per_head : 1);
+  if (a.pdp) return a.causal ? launch_bwd_main<true, 4>(a, DQK, DV, grid, s) : launch_bwd_main<false, 4>(a, DQK, DV, grid, s);
   switch ((a.causal ? 4 : 0) | (a.pmx ? 2 : 0) | (a.comp ? 1 : 0)) {
     case 0: return launch_bwd_main<false, 0>(a, DQK, DV, grid, s);
     case 1: return launch_bwd_main<false, 1>(a, DQK, DV, grid, s);

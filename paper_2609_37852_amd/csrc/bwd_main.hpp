@@ -61,7 +61,10 @@
 
 namespace afp8 {
 
-template <int DQK, int DV>
+// PDP: the protected-dP variant, dP = dO V^T from BF16 operands (the dO row
+// part of a query tile holds BF16 values, the workgroup's V rows sit in LDS
+// as BF16); every other product keeps its FP8 operands.
+template <int DQK, int DV, bool PDP = false>
 struct BwdCfg {
   // 8 waves: 4 blocks of 32 keys x 2 query halves.  The two waves of a key
   // block (w and w + KBW) each compute S, dP, P and dS for one 32-query half
@@ -80,11 +83,12 @@ struct BwdCfg {
   static constexpr int DST = BQ + 16;   // row stride of the dS' tile [key][query]
   static constexpr int al16(int x) { return (x + 15) & ~15; }
   // row part of a query tile (operands of S and dP, the per-query records)
+  static constexpr int OB = PDP ? 2 : 1;                            // bytes per dO row element
   static constexpr int Q_OFF = 0;                                   // Q row codes [BQ][DQK], swizzled
-  static constexpr int O_OFF = Q_OFF + BQ * DQK;                    // dO row codes [BQ][DV], swizzled
-  static constexpr int QS_OFF = O_OFF + BQ * DV;                    // Q row scales [BQ][DQK/32]
-  static constexpr int OS_OFF = al16(QS_OFF + BQ * DQK / 32);       // dO row scales [BQ][DV/32]
-  static constexpr int ROW_OFF = al16(OS_OFF + BQ * DV / 32);       // the tile's 1 KB block of per-query values
+  static constexpr int O_OFF = Q_OFF + BQ * DQK;                    // dO row codes [BQ][DV] (PDP: BF16), swizzled
+  static constexpr int QS_OFF = O_OFF + BQ * DV * OB;               // Q row scales [BQ][DQK/32]
+  static constexpr int OS_OFF = al16(QS_OFF + BQ * DQK / 32);       // dO row scales [BQ][DV/32] (not with PDP)
+  static constexpr int ROW_OFF = al16(OS_OFF + (PDP ? 0 : BQ * DV / 32));   // the tile's 1 KB block of per-query values
   static constexpr int RSTAGE = ROW_OFF + BQ * 16;
   // col part (operands of dV and dK)
   static constexpr int QC_OFF = 0;                                  // Q col codes [DQK][BQ], swizzled
@@ -97,13 +101,16 @@ struct BwdCfg {
   static constexpr int FIXED = 2 * (BKB * DST + KBW * 2 + 2 * KBW * 64 * 16);
   // the workgroup's K and V row codes [BKB][DQK + DV] (swizzled), read as
   // MFMA operands from LDS at wide heads; up to d = 128 each lane keeps its
-  // key's fragments in registers (no LDS traffic for them)
-  static constexpr int KV = BKB * (DQK + DV);
+  // key's fragments in registers (no LDS traffic for them).  PDP: the V rows
+  // are BF16 [BKB][DV] in LDS at every head dim, the K codes as above.
+  static constexpr int KV = BKB * (DQK + (PDP ? 0 : DV));
+  static constexpr int VB = PDP ? BKB * DV * 2 : 0;
   static constexpr int LIM = 156 * 1024;
   // row parts are double-buffered; col parts too and K / V are kept in LDS
   // where the LDS allows, preferring K / V in LDS over a second col buffer
-  static constexpr bool KV_LDS = DQK + DV > 256 && 2 * RSTAGE + CSTAGE + FIXED + KV <= LIM;
-  static constexpr int NCB = 2 * RSTAGE + 2 * CSTAGE + FIXED + (KV_LDS ? KV : 0) <= LIM ? 2 : 1;
+  static constexpr bool KV_LDS = DQK + DV > 256 && 2 * RSTAGE + CSTAGE + FIXED + KV + VB <= LIM;
+  static constexpr int NCB = 2 * RSTAGE + 2 * CSTAGE + FIXED + (KV_LDS ? KV : 0) + VB <= LIM ? 2 : 1;
+  static_assert(2 * RSTAGE + NCB * CSTAGE + FIXED + (KV_LDS ? KV : 0) + VB <= LIM, "LDS of the backward");
 };
 
 // dQ operand units of one head before 32-query block q.  Causal: block q has
@@ -123,27 +130,28 @@ struct BwdGroup {
   const uint8_t *qrow, *qsc, *orow, *osc, *qcol, *ocol, *tcs, *rows;
 };
 
-template <int DQK, int DV>
+template <int DQK, int DV, bool PDP = false>
 struct BwdStrides {   // bytes from one query head to the next
   int N;
   __device__ __forceinline__ uint32_t q() const { return (uint32_t)N * DQK; }
   __device__ __forceinline__ uint32_t qs() const { return (uint32_t)N * (DQK / 32); }
-  __device__ __forceinline__ uint32_t o() const { return (uint32_t)N * DV; }
+  __device__ __forceinline__ uint32_t o() const { return (uint32_t)N * DV * (PDP ? 2 : 1); }   // row part of dO
+  __device__ __forceinline__ uint32_t oc() const { return (uint32_t)N * DV; }                  // col codes of dO
   __device__ __forceinline__ uint32_t os() const { return (uint32_t)N * (DV / 32); }
   __device__ __forceinline__ uint32_t tcs() const { return (uint32_t)((N + 63) / 64) * (2 * (DQK + DV)); }
   __device__ __forceinline__ uint32_t rows() const { return (uint32_t)((N + 63) / 64) * 1024; }
 };
 
-template <int DQK, int DV>
+template <int DQK, int DV, bool PDP>
 __device__ __forceinline__ BwdGroup bwd_group(const AttnArgs& a, size_t bh0, int N) {
-  const BwdStrides<DQK, DV> S{N};
+  const BwdStrides<DQK, DV, PDP> S{N};
   BwdGroup g;
   g.qrow = a.q_code + bh0 * S.q();
   g.qsc = a.q_scale + bh0 * S.qs();
-  g.orow = a.do_code + bh0 * S.o();
-  g.osc = a.do_scale + bh0 * S.os();
+  g.orow = PDP ? reinterpret_cast<const uint8_t*>(a.do_bf16) + bh0 * S.o() : a.do_code + bh0 * S.o();
+  g.osc = PDP ? nullptr : a.do_scale + bh0 * S.os();
   g.qcol = a.qc_code + bh0 * S.q();
-  g.ocol = a.doc_code + bh0 * S.o();
+  g.ocol = a.doc_code + bh0 * S.oc();
   g.tcs = a.tile_cs + bh0 * S.tcs();
   g.rows = reinterpret_cast<const uint8_t*>(a.rows) + bh0 * S.rows();
   return g;
@@ -151,11 +159,11 @@ __device__ __forceinline__ BwdGroup bwd_group(const AttnArgs& a, size_t bh0, int
 
 // Load plans of one loading wave (index w among the NLD) for the code tiles
 // of a query tile.
-template <int DQK, int DV>
+template <int DQK, int DV, bool PDP>
 struct BwdLoads {
   static constexpr int NL = BwdCfg<DQK, DV>::NLD;
   RowLoads<DQK, NL, 64> q;
-  RowLoads<DV, NL, 64> o;
+  RowLoads<DV * (PDP ? 2 : 1), NL, 64> o;   // PDP: BF16 rows of 2 DV bytes
   ColLoads<DQK, NL> qc;
   ColLoads<DV, NL> oc;
   __device__ __forceinline__ void init(int w, int lane, int N) {
@@ -178,18 +186,19 @@ __device__ __forceinline__ int loader_index() {
 // group, queries i0..): codes, row scales and the per-query records.  N is
 // the layouts' query length, lim the sequence's (queries at or past it are
 // clamped to its last ones).
-template <int DQK, int DV>
-__device__ __forceinline__ void stage_rows(lds8* st, const BwdLoads<DQK, DV>& L, const BwdGroup& g, int G, int hi,
-                                           int i0, int N, int lim) {
-  using C = BwdCfg<DQK, DV>;
+template <int DQK, int DV, bool PDP>
+__device__ __forceinline__ void stage_rows(lds8* st, const BwdLoads<DQK, DV, PDP>& L, const BwdGroup& g, int G,
+                                           int hi, int i0, int N, int lim) {
+  using C = BwdCfg<DQK, DV, PDP>;
   constexpr int NWK = C::NLD;
   const int lane = threadIdx.x & 63, w = loader_index<DQK, DV>();
   if (w < 0) return;
-  const BwdStrides<DQK, DV> S{N};
+  const BwdStrides<DQK, DV, PDP> S{N};
   L.q.issue_s(st + C::Q_OFF, make_buf(g.qrow, G * S.q()), hi * S.q(), i0, lim, w, lane);
   L.o.issue_s(st + C::O_OFF, make_buf(g.orow, G * S.o()), hi * S.o(), i0, lim, w, lane);
   dma_row_scales_s<DQK, NWK>(st + C::QS_OFF, make_buf(g.qsc, G * S.qs()), hi * S.qs(), i0, lim, w, lane, 0);
-  dma_row_scales_s<DV, NWK>(st + C::OS_OFF, make_buf(g.osc, G * S.os()), hi * S.os(), i0, lim, w, lane, 1);
+  if constexpr (!PDP)
+    dma_row_scales_s<DV, NWK>(st + C::OS_OFF, make_buf(g.osc, G * S.os()), hi * S.os(), i0, lim, w, lane, 1);
   if (w == (3 % NWK)) {
     dma16s(make_buf(g.rows, G * S.rows()), (uint32_t)lane * 16, hi * S.rows() + (uint32_t)(i0 / 64) * 1024,
            st + C::ROW_OFF);
@@ -197,16 +206,16 @@ __device__ __forceinline__ void stage_rows(lds8* st, const BwdLoads<DQK, DV>& L,
 }
 
 // ... and of its col part: codes and the col scales packed by bwd_prep.
-template <int DQK, int DV>
-__device__ __forceinline__ void stage_cols(lds8* st, const BwdLoads<DQK, DV>& L, const BwdGroup& g, int G, int hi,
-                                           int i0, int N, int lim) {
-  using C = BwdCfg<DQK, DV>;
+template <int DQK, int DV, bool PDP>
+__device__ __forceinline__ void stage_cols(lds8* st, const BwdLoads<DQK, DV, PDP>& L, const BwdGroup& g, int G,
+                                           int hi, int i0, int N, int lim) {
+  using C = BwdCfg<DQK, DV, PDP>;
   constexpr int NWK = C::NLD;
   const int lane = threadIdx.x & 63, w = loader_index<DQK, DV>();
   if (w < 0) return;
-  const BwdStrides<DQK, DV> S{N};
+  const BwdStrides<DQK, DV, PDP> S{N};
   L.qc.issue_s(st + C::QC_OFF, make_buf(g.qcol, G * S.q()), hi * S.q(), i0, N, lim, w, lane);
-  L.oc.issue_s(st + C::OC_OFF, make_buf(g.ocol, G * S.o()), hi * S.o(), i0, N, lim, w, lane);
+  L.oc.issue_s(st + C::OC_OFF, make_buf(g.ocol, G * S.oc()), hi * S.oc(), i0, N, lim, w, lane);
   constexpr int NCI = (C::CS_BYTES + 255) / 256;
   for (int k = 0; k < NCI; k++) {
     if ((2 + k) % NWK != w) continue;   // loaders 2, 3, ...: 0 and 1 take the row scales
@@ -276,10 +285,11 @@ __device__ __forceinline__ TilePos next_pos(TilePos p, int G) {
 
 // CAUSAL: the mask (key length = query length) or every key of Nk; VAR:
 // numerics variant, bit 0 compensated dS formation (COMP), bit 1 block-scaled
-// backward probability operand (PMX)
+// backward probability operand (PMX), bit 2 dP from BF16 operands (PDP)
 template <int DQK, int DV, bool STATS, bool CAUSAL, int VAR>
 __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) {
-  using C = BwdCfg<DQK, DV>;
+  constexpr bool PDP = (VAR & 4) != 0;
+  using C = BwdCfg<DQK, DV, PDP>;
   constexpr int KBW = C::KBW, BKB = C::BKB, BQ = C::BQ, NCB = C::NCB;
   constexpr int KS = DQK / 64, VS = DV / 64, CK = DQK / 32, CV = DV / 32;
   constexpr int CMAX = CK > CV ? CK : CV;
@@ -334,7 +344,10 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   float kb = 1.0f;
   constexpr bool KVL = C::KV_LDS;
   __shared__ __attribute__((aligned(16))) uint8_t kL[KVL ? BKB * DQK : 16];
-  __shared__ __attribute__((aligned(16))) uint8_t vL[KVL ? BKB * DV : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t vL[KVL && !PDP ? BKB * DV : 16];
+  // PDP: the keys' BF16 V rows [BKB][2 DV bytes], 16-byte chunks swizzled as
+  // in a row tile
+  __shared__ __attribute__((aligned(16))) uint8_t vB[PDP ? C::VB : 16];
   {
     const int row = live ? kj : 0;
     const uint8_t* kr = a.k_code + (bhk * Nk + row) * DQK;
@@ -345,10 +358,22 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
       clear_channel(kf[s], s, hf, hot);
       ksc[s] = a.k_scale[(bhk * Nk + row) * (DQK / 32) + 2 * s + hf];
     }
+    if constexpr (!PDP) {
 #pragma unroll
-    for (int s = 0; s < VS; s++) {
-      vf[s] = frag_rows_global(vr, s, hf);
-      vsc[s] = a.v_scale[(bhk * Nk + row) * (DV / 32) + 2 * s + hf];
+      for (int s = 0; s < VS; s++) {
+        vf[s] = frag_rows_global(vr, s, hf);
+        vsc[s] = a.v_scale[(bhk * Nk + row) * (DV / 32) + 2 * s + hf];
+      }
+    } else {
+      // the second wave of each key block stores its keys' BF16 V rows, the
+      // two lane halves alternate chunks (visible after the prologue's barrier)
+      if (qs == 1) {
+        const uint4* src = reinterpret_cast<const uint4*>(a.v_bf16 + (bhk * Nk + row) * DV);
+        const int kr2 = 32 * kbw + li;
+#pragma unroll
+        for (int ch = hf; ch < DV / 8; ch += 2)
+          *reinterpret_cast<uint4*>(vB + kr2 * (2 * DV) + 16 * (ch ^ swz_row<2 * DV>(kr2))) = src[ch];
+      }
     }
     if (hf == 0)
       kb = hot >= 0 ? row_value<DQK>(a.k_code + bhk * Nk * DQK, a.k_scale + bhk * Nk * (DQK / 32), row, hot) : 0.f;
@@ -360,7 +385,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
       if (qs == 0) {
 #pragma unroll
         for (int t = 0; t < KS; t++) kv_store<DQK>(kL, kr2, t, hf, kf[t]);
-      } else {
+      } else if constexpr (!PDP) {
 #pragma unroll
         for (int t = 0; t < VS; t++) kv_store<DV>(vL, kr2, t, hf, vf[t]);
       }
@@ -389,12 +414,12 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   const int nks = (Nk + 63) / 64;               // 64-key steps of the dQ units
   const int64_t units_per_head = units_before(N / 32, nks, causal);
   auto q0_of = [&](TilePos p) __attribute__((always_inline)) { return (up ? qt0 + p.r : nqt - 1 - p.r) * BQ; };
-  BwdLoads<DQK, DV> ld;
+  BwdLoads<DQK, DV, PDP> ld;
   ld.init(loader_index<DQK, DV>() >= 0 ? loader_index<DQK, DV>() : 0, lane, N);
   auto row_rec = [&](const uint8_t* R) __attribute__((always_inline)) {
     return *reinterpret_cast<const float*>(R + C::ROW_OFF + (32 * qs + li) * 8 + 4 * hf);
   };
-  const BwdGroup grp = bwd_group<DQK, DV>(a, bh0, N);
+  const BwdGroup grp = bwd_group<DQK, DV, PDP>(a, bh0, N);
 
   // Pipeline, per tile i (each step a function of the buffers it touches):
   //   barrier (codes of tile i exchanged, loads of rows i+1 and cols i landed)
@@ -568,9 +593,11 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
     const uint8_t* Bs = Cc + (qs ? C::QCS_OFF : C::OCS_OFF);
     const int nb = qs ? CK : CV;
     const int clo = hf + 2 * qs, chi = hf + 2 - 2 * qs, sbk = hf ^ qs;
-    // S and dP operations interleaved while both last (independent chains)
-    constexpr int NSD = KS + VS, NI2 = KS < VS ? KS : VS;
-    auto sd_is_s = [](int m) { return m < 2 * NI2 ? (m & 1) == 0 : KS > VS; };
+    // S and dP operations interleaved while both last (independent chains);
+    // PDP: dP in DV / 16 BF16 MFMAs of 16 channels each
+    constexpr int VSD = PDP ? DV / 16 : VS;
+    constexpr int NSD = KS + VSD, NI2 = KS < VSD ? KS : VSD;
+    auto sd_is_s = [](int m) { return m < 2 * NI2 ? (m & 1) == 0 : KS > VSD; };
     auto sd_t = [](int m) { return m < 2 * NI2 ? m >> 1 : m - NI2; };
     auto load = [&](int m) __attribute__((always_inline)) {
       Opnd r;
@@ -581,6 +608,16 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
           r.b = kfrag(t);
           r.sa = Qs[qrow * (DQK / 32) + 2 * t + hf];
           r.sb = ksc[t];
+        } else if constexpr (PDP) {
+          // BF16 fragments of channels 16 t + 8 hf .. + 7 of the query's dO
+          // row and the key's V row (both operands pair the same channels)
+          const int kr2 = 32 * kbw + li;
+          const v4i av = *reinterpret_cast<const v4i*>(O + qrow * (2 * DV) + 16 * ((2 * t + hf) ^ swz_row<2 * DV>(qrow)));
+          const v4i bv = *reinterpret_cast<const v4i*>(vB + kr2 * (2 * DV) + 16 * ((2 * t + hf) ^ swz_row<2 * DV>(kr2)));
+          r.a = v8i{av[0], av[1], av[2], av[3], 0, 0, 0, 0};
+          r.b = v8i{bv[0], bv[1], bv[2], bv[3], 0, 0, 0, 0};
+          r.sa = 0;
+          r.sb = 0;
         } else {
           r.a = frag_rows_swz<DV>(O, qrow, t, hf);
           r.b = vfrag(t);
@@ -599,6 +636,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
     auto exec = [&](int m, const Opnd& r) __attribute__((always_inline)) {
       if (m < NSD) {
         if (sd_is_s(m)) s = mfma_mx(r.a, r.b, s, r.sa, r.sb);
+        else if constexpr (PDP) dp = mfma_bf16(r.a, r.b, dp);
         else dp = mfma_mx(r.a, r.b, dp, r.sa, r.sb);
       } else {
         const int i = m - NSD;
@@ -696,15 +734,15 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
     ds_store(p, ds, es);
     const float rec = row_rec(R1);
     if constexpr (NCB == 2) {
-      if (more) stage_cols<DQK, DV>(Cl, ld, grp, G, p1.hi, q0_of(p1), N, L.q);
+      if (more) stage_cols<DQK, DV, PDP>(Cl, ld, grp, G, p1.hi, q0_of(p1), N, L.q);
     }
-    if (i + 2 < total) stage_rows<DQK, DV>(Rl, ld, grp, G, p2.hi, q0_of(p2), N, L.q);
+    if (i + 2 < total) stage_rows<DQK, DV, PDP>(Rl, ld, grp, G, p2.hi, q0_of(p2), N, L.q);
     const bool skip1 = !more || front_skip(p1);
     mfmas(R1, skip1, rec, Cc, es, x, std::true_type{});
     __builtin_amdgcn_sched_barrier(0);   // every MFMA issues before the VALU work below
     if constexpr (NCB == 1) {
       lds_sync();                          // every wave has read the col operands of tile i
-      if (more) stage_cols<DQK, DV>(Cl, ld, grp, G, p1.hi, q0_of(p1), N, L.q);
+      if (more) stage_cols<DQK, DV, PDP>(Cl, ld, grp, G, p1.hi, q0_of(p1), N, L.q);
     }
     if (more) front_vals(p1, R1, ds1, es1, x1);
   };
@@ -713,10 +751,10 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   // (none without queries: the key gradients are then zero)
   const TilePos p0 = TilePos{0, 0};
   if (total > 0) {
-    stage_rows<DQK, DV>((lds8*)rA, ld, grp, G, p0.hi, q0_of(p0), N, L.q);
-    stage_cols<DQK, DV>((lds8*)cA, ld, grp, G, p0.hi, q0_of(p0), N, L.q);
+    stage_rows<DQK, DV, PDP>((lds8*)rA, ld, grp, G, p0.hi, q0_of(p0), N, L.q);
+    stage_cols<DQK, DV, PDP>((lds8*)cA, ld, grp, G, p0.hi, q0_of(p0), N, L.q);
     TilePos pa = next_pos(p0, G);
-    if (total > 1) stage_rows<DQK, DV>((lds8*)rB, ld, grp, G, pa.hi, q0_of(pa), N, L.q);
+    if (total > 1) stage_rows<DQK, DV, PDP>((lds8*)rB, ld, grp, G, pa.hi, q0_of(pa), N, L.q);
     lds_barrier();
     mfmas(rA, front_skip(p0), row_rec(rA), cA, esA, xA, std::false_type{});
     front_vals(p0, rA, dsA, esA, xA);
@@ -785,7 +823,10 @@ hipError_t launch_bwd_main(const AttnArgs& a, int dqk, int dv, dim3 grid, hipStr
   }
   AFP8_BWD_GO(64, 64)
   AFP8_BWD_GO(128, 128)
-  AFP8_BWD_GO(256, 256)
+  // the protected-dP variant's BF16 dO and V tiles do not fit the LDS at d = 256
+  if constexpr ((VAR & 4) == 0) {
+    AFP8_BWD_GO(256, 256)
+  }
   AFP8_BWD_GO(192, 128)
 #undef AFP8_BWD_GO
   return hipErrorInvalidValue;
@@ -796,10 +837,12 @@ AFP8_BWD_EXTERN(true, 0)
 AFP8_BWD_EXTERN(true, 1)
 AFP8_BWD_EXTERN(true, 2)
 AFP8_BWD_EXTERN(true, 3)
+AFP8_BWD_EXTERN(true, 4)
 AFP8_BWD_EXTERN(false, 0)
 AFP8_BWD_EXTERN(false, 1)
 AFP8_BWD_EXTERN(false, 2)
 AFP8_BWD_EXTERN(false, 3)
+AFP8_BWD_EXTERN(false, 4)
 #undef AFP8_BWD_EXTERN
 
 }  // namespace afp8

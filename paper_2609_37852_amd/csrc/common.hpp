@@ -33,6 +33,17 @@ __device__ __forceinline__ v16f mfma_mx(const v8i& a, const v8i& b, const v16f& 
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, scale_a, 0, scale_b);
 }
 
+// BF16 32x32x16 MFMA with FP32 accumulation: lane l gives 8 BF16 values of
+// row (A) / column (B) l % 32 in the low four dwords of a / b, lane half hf
+// the k values 8 hf .. 8 hf + 7 (the same mapping for both operands, so
+// loading both with the same channels pairs them); C as above.
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ v16f mfma_bf16(const v8i& a, const v8i& b, const v16f& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, __builtin_shufflevector(a, a, 0, 1, 2, 3)),
+                                                 __builtin_bit_cast(v8bf, __builtin_shufflevector(b, b, 0, 1, 2, 3)),
+                                                 c, 0, 0, 0);
+}
+
 // Smallest integer e with amax <= 448 * 2^e (448 = 1.75 * 2^8), clamped to the
 // E8M0 range [-127, 127]; zero and FP32-subnormal amax give -127.  Pure
 // integer arithmetic on the FP32 bit pattern.

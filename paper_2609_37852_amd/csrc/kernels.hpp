@@ -68,6 +68,7 @@ struct AttnArgs {
   int comp;                  // compensated correction: FP64 products in the correction pass,
                              // compensated dS formation in the backward
   int pmx;                   // block-scaled backward probability operand (one scale per 32x32 block)
+  int pdp;                   // protected dP: dP = dO V^T from the BF16 copies below
   float c;                   // tau * log2(e), applied to the score accumulator
   float tau;
   const uint8_t *q_code, *q_scale;     // row copy of Q      [B,Hq,N,Dqk], [B,Hq,N,Dqk/32]
@@ -78,6 +79,8 @@ struct AttnArgs {
   const uint8_t *kc_code, *kc_scale;   // col copy of K      [B,Hkv,Dqk,Nk]
   const uint8_t *vc_code, *vc_scale;   // col copy of V      [B,Hkv,Dv,Nk]
   const uint8_t *doc_code, *doc_scale; // col copy of dO     [B,Hq,Dv,N]
+  const uint16_t* do_bf16;             // protected dP: dO   [B,Hq,N,Dv] BF16 (workspace)
+  const uint16_t* v_bf16;              //               V    [B,Hkv,Nk,Dv] BF16 (workspace)
   const float* q_amax;                 // nullable [B,Hq,Dqk] per-channel max |q|
   const float* k_amax;                 // nullable [B,Hkv,Dqk] per-channel max |k|
   const float* lse;                    // [B,Hq,N]
@@ -136,6 +139,8 @@ hipError_t launch_delta_matching(const AttnArgs& a, int dqk, int dv, hipStream_t
 hipError_t launch_bwd_prep(const AttnArgs& a, int dqk, int dv, hipStream_t s);
 hipError_t launch_bwd(const AttnArgs& a, int dqk, int dv, hipStream_t s);
 hipError_t launch_dq(const AttnArgs& a, int dqk, hipStream_t s);
+hipError_t launch_pack_bf16(const void* x, int bf16, const int64_t st[3], int64_t B, int64_t N, int64_t H, int D,
+                            const int32_t* lens, uint16_t* out, hipStream_t s);
 // stored dQ operand units of one head: one per (32-query block, 64-key
 // step) that holds a visible key
 int64_t dq_units_per_head(int64_t nq, int64_t nk, bool causal);
