@@ -79,7 +79,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
 // waves.  Keys past the sequence meet zero dS' codes (their K loads are
 // clamped to the sequence's last keys).
 template <int DQK>
-__global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256, DQK <= 128 ? 4 : 1) void dq_kernel(AttnArgs a) {
   constexpr int CQ = DQK / 32, NW = 4;
   constexpr int KT = DQK * 64, KSB = 2 * DQK;       // K tile and scale bytes per step
   __shared__ __attribute__((aligned(16))) uint8_t kA[KT + KSB];
@@ -121,8 +121,11 @@ __global__ __launch_bounds__(256) void dq_kernel(AttnArgs a) {
   struct Aop { uint4 lo, hi; uint32_t e; };
   auto load_a = [&](Aop& op, int ks) __attribute__((always_inline)) {
     ks = ks < nk ? ks : (nk > 0 ? nk - 1 : 0);     // past the wave's last step: reload it (unused)
-    op.lo = *reinterpret_cast<const uint4*>(units + ks * 2048);
-    op.hi = *reinterpret_cast<const uint4*>(units + ks * 2048 + 1024);
+    // read once: streamed past the caches, which keep the K tiles
+    const v4i lo = __builtin_nontemporal_load(reinterpret_cast<const v4i*>(units + ks * 2048));
+    const v4i hi = __builtin_nontemporal_load(reinterpret_cast<const v4i*>(units + ks * 2048 + 1024));
+    op.lo = make_uint4((uint32_t)lo[0], (uint32_t)lo[1], (uint32_t)lo[2], (uint32_t)lo[3]);
+    op.hi = make_uint4((uint32_t)hi[0], (uint32_t)hi[1], (uint32_t)hi[2], (uint32_t)hi[3]);
     op.e = ex[2 * ks + hf];
   };
   v16f acc[CQ];
