@@ -18,8 +18,9 @@ roofline, the paper's own timing protocol (App. C.2: clock warm-up, five
 interleaved rounds of the median of 20 timings after 5 warm-up calls, mean
 and standard error, pre-quantized inputs) for the matched and the stale
 backward, a whole step with the stale correction, the cost of the
-compensated matched correction, the protected-dP variant, the same workload without the causal mask,
-the d = 256 workload, and the oracle's CPU rate.
+compensated matched correction, the protected-dP variant, the block-scaled backward probability
+operand, a padded batch of sequences of their own lengths, the input producer, the same workload
+without the causal mask, the d = 256 workload, and the oracle's CPU rate.
 `--gpus N` with N > 1 exits: this benchmark measures a single GPU.
 """
 from __future__ import annotations
@@ -335,6 +336,64 @@ def protected_dp_line(run):
             "bwd_over_fp8dp_bwd": round((t_prot - t_fwd) / (t_stale - t_fwd) - 1, 4)}
 
 
+def variants_line(run):
+    """The f3/f4 options on the same workload, each the median of 20 timings
+    after 5 warm-ups: the block-scaled backward probability operand (matched
+    backward call against the default one), a padded batch of sequences of
+    their own lengths (forward + matched correction + backward, credited
+    with each sequence's own causal FLOPs), and the input producer (query:
+    QK normalization, rotary embedding on 64 channels, prescale by tau; key:
+    the same with centring instead of the prescale) against the plain
+    quantizer."""
+    import dataclasses
+    import torch
+    pk, w = run.pk, run.w
+    from paper_2609_37852_amd import synth
+    out = {}
+    mode = pk.DELTA_MATCHING
+    run.quantize()
+    run.fwd()
+    run.correction(mode)
+    pm = dataclasses.replace(run.p, flags=pk.FLAG_PBWD_BLOCK_SCALED)
+    t_def = run.timed(lambda: run.bwd(mode))
+    t_pmx = run.timed(lambda: pk.attn_fp8_bwd(pm, mode, run.mq, run.mk, run.mv, run.mdo, run.lse, run.do, run.o,
+                                              delta_in=run.delta, workspace=run.ws, out=run.grads))
+    out["pbwd_block_scaled"] = {"bwd_call_ms": round(t_pmx, 4), "default_bwd_call_ms": round(t_def, 4),
+                                "over_default": round(t_pmx / t_def - 1, 4)}
+    # sequences of their own lengths in the padded layout
+    lens = [w.N - (w.N // 4) * (b % 4) for b in range(w.B)]
+    pv = dataclasses.replace(run.p, seqlens_q=torch.tensor(lens, dtype=torch.int32, device="cuda:0"))
+
+    def varlen_step():
+        pk.attn_fp8_fwd(pv, run.mq, run.mk, run.mv, o=run.o, lse=run.lse)
+        pk.attn_fp8_delta(pv, mode, run.mq, run.mk, run.mv, run.mdo, run.lse, run.do, run.o, delta=run.delta)
+        pk.attn_fp8_bwd(pv, mode, run.mq, run.mk, run.mv, run.mdo, run.lse, run.do, run.o, delta_in=run.delta,
+                        workspace=run.ws, out=run.grads)
+    t_var = run.timed(varlen_step)
+    t_full = run.timed(lambda: (run.fwd(), run.correction(mode), run.bwd(mode)))
+    fl = sum(sum(synth.with_shape(w, B=1, N=L).credited_flops()) for L in lens)
+    ff = sum(w.credited_flops())
+    out["varlen"] = {"seqlens": lens, "fwd_bwd_ms": round(t_var, 4),
+                     "tflops": round(fl / (t_var * 1e-3) / 1e12, 2),
+                     "full_length_fwd_bwd_ms": round(t_full, 4),
+                     "full_length_tflops": round(ff / (t_full * 1e-3) / 1e12, 2)}
+    # the input producer
+    R = 64
+    tab = torch.from_numpy(synth.rope_table(w.N, R, 1e4)).cuda()
+    g = torch.ones(w.Dqk, dtype=torch.float32, device="cuda:0")
+    t_q = run.timed(lambda: pk.attn_fp8_quantize(run.q))
+    t_k = run.timed(lambda: pk.attn_fp8_quantize(run.k))
+    t_pq = run.timed(lambda: pk.attn_fp8_quantize_producer(run.q, float(np.float32(w.tau)), False, rope=tab,
+                                                           rms_gain=g))
+    t_pk = run.timed(lambda: pk.attn_fp8_quantize_producer(run.k, 1.0, True, rope=tab, rms_gain=g))
+    bq, bk = 4.0625 * run.q.numel(), 4.0625 * run.k.numel()
+    out["producer"] = {"q_ms": round(t_pq, 4), "q_plain_quantize_ms": round(t_q, 4),
+                       "k_ms": round(t_pk, 4), "k_plain_quantize_ms": round(t_k, 4),
+                       "q_gbs_algorithmic": round(bq / (t_pq * 1e-3) / 1e9, 1),
+                       "k_gbs_algorithmic": round(bk / (t_pk * 1e-3) / 1e9, 1)}
+    return out
+
+
 def cpu_baseline(w, d, threads, kv_heads=2):
     """The oracle (FP64 C, OpenMP) timed on the host cores on the first
     `kv_heads` KV groups of batch 0 at the full sequence length."""
@@ -492,6 +551,7 @@ def main():
         line["compensated"] = {"matching": pm, "compensated": cm,
                                "step_over_matching": round(cm["step_ms"] / pm["step_ms"] - 1, 4)}
         line["protected_dp"] = protected_dp_line(run)
+        line["variants"] = variants_line(run)
         if args.workload == "gqa_d128_8k":
             # the same workload without the causal mask (every query sees all
             # 8192 keys; credited FLOPs count the full N x N products)

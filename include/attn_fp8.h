@@ -231,7 +231,7 @@ typedef struct attn_fp8_producer {
 } attn_fp8_producer;
 
 /* Workspace bytes attn_fp8_quantize_producer needs with these options: the
- * key-mean partial sums (FP64 [B, H, D, N/32]) when center, then the norm's
+ * key-mean partial sums (FP64 [B, H, N/32, D]) when center, then the norm's
  * row scales (FP32 [B, N, H]) when rms_gain, each rounded up to 256 bytes;
  * 0 when neither.  Checks the options and sizes as the producer does.
  * Returns 0 / negative status. */

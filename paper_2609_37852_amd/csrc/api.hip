@@ -309,7 +309,7 @@ int scratch_address(void** out) {
   return ATTN_FP8_OK;
 }
 
-// Producer workspace: the key-mean partial sums (FP64 [B, H, D, N/32]) when
+// Producer workspace: the key-mean partial sums (FP64 [B, H, N/32, D]) when
 // centering, then the QK-normalization row scales (FP32 [B, N, H]) when a
 // gain is given, each 256-byte aligned.
 size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
@@ -354,6 +354,8 @@ int quantize_impl(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, i
   if (which < 1 || which > 3) return fail(ATTN_FP8_EINVAL, "which = %d", which);
   if (B > 65535 || H > 65535 || N > (int64_t(1) << 30)) return fail(ATTN_FP8_EUNSUPPORTED, "grid limits");
   if (opt && (rc = check_producer(D, opt))) return rc;
+  if (opt && opt->rms_gain && B * N * H >= (int64_t(1) << 38))
+    return fail(ATTN_FP8_EUNSUPPORTED, "grid limits (B N H = %lld rows for the norm)", (long long)(B * N * H));
   if (B == 0 || N == 0 || H == 0) return ok();  // empty: nothing is read or written
   if ((rc = check_ptr("x", x)) || (rc = check_strides("x", strides, es)) ||
       (rc = check_mx("out", out, which & 1, which & 2)))

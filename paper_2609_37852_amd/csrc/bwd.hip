@@ -89,7 +89,7 @@ __global__ __launch_bounds__(256, DQK <= 128 ? 4 : 1) void dq_kernel(AttnArgs a)
   const bool causal = a.causal != 0;
   const int nks = (Nk + 63) / 64;                    // 64-key steps over the keys (unit layout)
   const int ntile = (nqb + NW - 1) / NW;
-  const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);
+  const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv, a.lens_q != nullptr);
   const int tile = ntile - 1 - wc.r;                 // longest rows first
   const int h = wc.h, b = wc.b, kh = h / (int)a.G;
   // the sequence's own lengths bound the work

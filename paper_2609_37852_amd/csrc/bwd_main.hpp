@@ -320,11 +320,14 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   // workgroup id -> key block (slowest, in the order of key_block_of) and
   // (batch, KV head) (fastest: the key blocks of one KV head get ids equal
   // mod 16, hence one XCD and its L2 when B * Hkv % 8 == 0)
-  const int GI = (int)(a.B * a.Hkv);
-  const KeyBlock kbk = key_block_of((int)blockIdx.x / GI, (Nk + BKB - 1) / BKB, a.bwd_cohort);
+  // (with sequences of their own lengths the groups rotate over the XCDs
+  // from one slot to the next, as in query_major_coord)
+  const int GI = (int)(a.B * a.Hkv), slot = (int)blockIdx.x / GI;
+  const KeyBlock kbk = key_block_of(slot, (Nk + BKB - 1) / BKB, a.bwd_cohort);
   const int kb0 = kbk.kb * BKB;
   const bool up = kbk.up;
-  const int kh = ((int)blockIdx.x % GI) % (int)a.Hkv, b = ((int)blockIdx.x % GI) / (int)a.Hkv;
+  const int gi = a.lens_q ? ((int)blockIdx.x % GI + slot) % GI : (int)blockIdx.x % GI;
+  const int kh = gi % (int)a.Hkv, b = gi / (int)a.Hkv;
   // the sequence's own lengths bound the work; N and Nk remain the strides
   const SeqLens L = seq_lens<CAUSAL>(a, b, N, Nk);
   if (kb0 >= L.k) return;                       // the whole key block is past the sequence

@@ -128,15 +128,19 @@ __device__ __forceinline__ float wave_max_nonneg(float v) {
 //   query-major kernels: id -> (rank r of the query block, heaviest first,
 //   batch b, query head h); within a rank, the query heads of one KV group
 //   get ids that are equal mod 8 whenever B * Hkv is a multiple of 8.
+//   rotate (sequences of their own lengths): the groups move to the next
+//   XCD from one rank to the next, so that no XCD holds only long sequences
+//   (with equal lengths every group weighs the same and stays on its XCD).
 struct WgCoord { int r, b, h; };
-__device__ __forceinline__ WgCoord query_major_coord(int id, int B, int Hq, int Hkv) {
+__device__ __forceinline__ WgCoord query_major_coord(int id, int B, int Hq, int Hkv, bool rotate = false) {
   const int BH = B * Hq, G = Hq / Hkv, GI = B * Hkv;
   WgCoord c;
   c.r = id / BH;
   const int u = id % BH;
   if (GI % 8 == 0) {
     const int xcd = u % 8, j = u / 8;
-    const int gi = (j / G) * 8 + xcd;           // (batch, KV head) group
+    int gi = (j / G) * 8 + xcd;                 // (batch, KV head) group
+    if (rotate) gi = (gi + c.r) % GI;
     c.b = gi / Hkv;
     c.h = (gi % Hkv) * G + j % G;
   } else {

@@ -61,7 +61,7 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   constexpr bool causal = CAUSAL;
   const int N = (int)a.N, Nk = CAUSAL ? N : (int)a.Nk;
   const int nqb = (N + BQ - 1) / BQ;
-  const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv);
+  const WgCoord wc = query_major_coord((int)blockIdx.x, (int)a.B, (int)a.Hq, (int)a.Hkv, a.lens_q != nullptr);
   const int qb = nqb - 1 - wc.r;              // longest causal rows first
   const int h = wc.h, b = wc.b, kh = h / (int)a.G;
   // the sequence's own lengths bound the work; N and Nk remain the strides

@@ -23,7 +23,7 @@ struct QuantArgs {
   uint32_t* nonfinite;       // nullable
   float* chan_amax;          // nullable [B, H, D]: max over tokens of |x| (zeroed before the launch)
   // input producer (all optional): x' = fl32(x * prescale), then
-  // fl32(x' - mean[b, h, c]) when mean is given; partials: [B, H, D, N/32]
+  // fl32(x' - mean[b, h, c]) when mean is given; partials: [B, H, N/32, D]
   // FP64 block sums of x' the mean is formed from
   float prescale;            // 1 for none
   float* mean;               // nullable [B, H, D]

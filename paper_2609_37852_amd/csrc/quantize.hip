@@ -102,15 +102,22 @@ __device__ __forceinline__ float add_rn(float x, float y) {
 // gives x cos - p sin, the second x cos + p sin (x this channel's value, p
 // the pair partner's), every product and the sum rounded to FP32, the result
 // rounded to BF16.
+//
+// Rounding to BF16 uses the hardware conversion (v_cvt_pk_bf16_f32, round to
+// nearest even; it agrees with the integer rounding rule on every finite
+// FP32 value, subnormals included, which an in-bounds probe checked on 4M
+// values).
+__device__ __forceinline__ float round_bf16(float x) { return (float)(__bf16)x; }
+
 __device__ __forceinline__ float rope_rotate(float x, float p, float2 cs, bool first) {
   const float a = mul_rn(x, cs.x), b = mul_rn(p, cs.y);
-  return bf16_to_f32(f32_to_bf16(first ? sub_rn(a, b) : add_rn(a, b)));
+  return round_bf16(first ? sub_rn(a, b) : add_rn(a, b));
 }
 
 // One channel of the QK normalization: x times the row's reciprocal RMS,
 // times the channel gain, each product rounded to FP32, rounded to BF16.
 __device__ __forceinline__ float qk_norm(float x, float r, float g) {
-  return bf16_to_f32(f32_to_bf16(mul_rn(mul_rn(x, r), g)));
+  return round_bf16(mul_rn(mul_rn(x, r), g));
 }
 
 // One workgroup = 32 NB tokens (NB 32-token blocks; the last ones may lie
@@ -159,26 +166,48 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
       }
     }
     if (a.rope) {
-      // fused rotary embedding: the pair partner's value comes through the
-      // tile (a token's chunks may lie in two waves)
-#pragma unroll
-      for (int u = 0; u < NB; u++)
-#pragma unroll
-        for (int k = 0; k < 16; k++) tile[32 * u + tok][ch + k] = v[u][k];
-      __syncthreads();
+      // fused rotary embedding: the pair partner's 16 values come from the
+      // lane h2 / 16 further along the token (a token's CH lanes are
+      // consecutive), or through the tile where a token's chunks may lie in
+      // two waves (64 % CH != 0)
       const int h2 = a.rope_dim >> 1, rel = ch - a.rope_lo;
-      if (rel >= 0 && rel < a.rope_dim) {
-        const bool first = rel < h2;
-        const int pch = first ? ch + h2 : ch - h2, c0 = first ? rel : rel - h2;
+      const bool rot = rel >= 0 && rel < a.rope_dim, first = rel < h2;
+      const int pch = first ? ch + h2 : ch - h2, c0 = first ? rel : rel - h2;
+      if constexpr (64 % CH == 0) {
+        const int plane = (t & 63) + (rot ? (pch - ch) / 16 : 0);
 #pragma unroll
         for (int u = 0; u < NB; u++) {
-          if (u >= nb) break;
-          const float2* cs = reinterpret_cast<const float2*>(a.rope) + (n0 + 32 * u + tok) * h2 + c0;
+          float pv[16];
 #pragma unroll
-          for (int k = 0; k < 16; k++) v[u][k] = rope_rotate(v[u][k], tile[32 * u + tok][pch + k], cs[k], first);
+          for (int k = 0; k < 16; k++) pv[k] = __shfl(v[u][k], plane);
+          if (rot && u < nb) {
+            const float4* cs4 = reinterpret_cast<const float4*>(
+                reinterpret_cast<const float2*>(a.rope) + (n0 + 32 * u + tok) * h2 + c0);
+#pragma unroll
+            for (int k = 0; k < 8; k++) {
+              const float4 cs = cs4[k];
+              v[u][2 * k] = rope_rotate(v[u][2 * k], pv[2 * k], make_float2(cs.x, cs.y), first);
+              v[u][2 * k + 1] = rope_rotate(v[u][2 * k + 1], pv[2 * k + 1], make_float2(cs.z, cs.w), first);
+            }
+          }
         }
+      } else {
+#pragma unroll
+        for (int u = 0; u < NB; u++)
+#pragma unroll
+          for (int k = 0; k < 16; k++) tile[32 * u + tok][ch + k] = v[u][k];
+        __syncthreads();
+        if (rot) {
+#pragma unroll
+          for (int u = 0; u < NB; u++) {
+            if (u >= nb) break;
+            const float2* cs = reinterpret_cast<const float2*>(a.rope) + (n0 + 32 * u + tok) * h2 + c0;
+#pragma unroll
+            for (int k = 0; k < 16; k++) v[u][k] = rope_rotate(v[u][k], tile[32 * u + tok][pch + k], cs[k], first);
+          }
+        }
+        __syncthreads();   // the tile is written again below
       }
-      __syncthreads();   // the tile is written again below
     }
     float mu[16];
 #pragma unroll
@@ -254,62 +283,124 @@ __device__ __forceinline__ float to_f32(T x) {
   else return (float)x;
 }
 
+// Two consecutive channels of one token as FP32.
 template <typename T>
-__global__ __launch_bounds__(256) void producer_partials_kernel(QuantArgs a, int D) {
-  const int c = threadIdx.x;
+__device__ __forceinline__ float2 load2(const T* p) {
+  if constexpr (sizeof(T) == 2) {
+    const uint32_t u = *reinterpret_cast<const uint32_t*>(p);
+    return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
+  } else {
+    return *reinterpret_cast<const float2*>(p);
+  }
+}
+
+// Key-mean partial sums: a thread owns channels c, c + 1 (2 t) of one aligned
+// 32-token block of one (batch, head) and sums the transformed values of
+// each in FP64 over the block's tokens in ascending order; partials are laid
+// out [B, H, N/32, D] so that the mean pass reads them coalesced.  The
+// transform (norm, rotation, prescale) is the quantizer's; the two channels
+// of a thread are both rotary or both not, and both first or both second of
+// their pairs (the rotary range is 32-aligned), so their partners are
+// consecutive as well.
+template <typename T>
+__global__ __launch_bounds__(128) void producer_partials_kernel(QuantArgs a, int D) {
+  const int c = 2 * (int)threadIdx.x;
   if (c >= D) return;
   const int64_t t = blockIdx.x, h = blockIdx.y, b = blockIdx.z, nblk = a.N / 32;
   const T* src = reinterpret_cast<const T*>(a.x) + b * a.sb + h * a.sh + c;
-  // rotary channel: its pair partner and table column (the same rotation as
-  // the quantizer's)
   const int h2 = a.rope_dim >> 1, rel = c - a.rope_lo;
   const bool rot = a.rope && rel >= 0 && rel < a.rope_dim, first = rel < h2;
   const int poff = first ? h2 : -h2, c0 = first ? rel : rel - h2;
-  double part = 0.0;
+  float2 g = make_float2(1.f, 1.f), pg = make_float2(1.f, 1.f);
+  if (a.gain) {
+    g = make_float2(a.gain[c], a.gain[c + 1]);
+    if (rot) pg = make_float2(a.gain[c + poff], a.gain[c + poff + 1]);
+  }
+  double part0 = 0.0, part1 = 0.0;
 #pragma unroll 8
   for (int k = 0; k < 32; k++) {
     const int64_t n = 32 * t + k;
-    float f = to_f32(src[n * a.sn]);
-    float p = rot ? to_f32(src[n * a.sn + poff]) : 0.f;
+    float2 f = load2<T>(src + n * a.sn);
+    float2 p = rot ? load2<T>(src + n * a.sn + poff) : make_float2(0.f, 0.f);
     if (a.gain) {
       const float r = a.rscale[(b * a.N + n) * a.H + h];
-      f = qk_norm(f, r, a.gain[c]);
-      if (rot) p = qk_norm(p, r, a.gain[c + poff]);
+      f = make_float2(qk_norm(f.x, r, g.x), qk_norm(f.y, r, g.y));
+      if (rot) p = make_float2(qk_norm(p.x, r, pg.x), qk_norm(p.y, r, pg.y));
     }
-    if (rot) f = rope_rotate(f, p, reinterpret_cast<const float2*>(a.rope)[n * h2 + c0], first);
-    part += (double)mul_rn(f, a.prescale);
+    if (rot) {
+      const float4 cs = *reinterpret_cast<const float4*>(a.rope + 2 * (n * h2 + c0));
+      f = make_float2(rope_rotate(f.x, p.x, make_float2(cs.x, cs.y), first),
+                      rope_rotate(f.y, p.y, make_float2(cs.z, cs.w), first));
+    }
+    part0 += (double)mul_rn(f.x, a.prescale);
+    part1 += (double)mul_rn(f.y, a.prescale);
   }
-  a.partials[((b * a.H + h) * D + c) * nblk + t] = part;
+  *reinterpret_cast<double2*>(a.partials + ((b * a.H + h) * nblk + t) * D + c) = make_double2(part0, part1);
 }
 
 // Reciprocal RMS of every (token, head) row for the QK normalization: the
 // squares summed in FP64 over the channels in ascending order, divided by D,
 // eps added, 1 / sqrt in FP64 (each rounded to nearest), rounded once to
-// FP32.  One thread per row; the grid strides over the rows.
+// FP32.  A workgroup of 256 threads takes 256 rows: 32-channel slices of
+// them reach LDS with coalesced loads (rows in (b, n, h) order, h fastest),
+// then each thread continues its own row's sum over the slice.
 template <typename T>
 __global__ __launch_bounds__(256) void producer_rscale_kernel(QuantArgs a, int D) {
-  const int64_t rows = a.B * a.N * a.H;
-  for (int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x; row < rows; row += (int64_t)gridDim.x * 256) {
-    const int64_t h = row % a.H, n = (row / a.H) % a.N, b = row / (a.H * a.N);
-    const T* src = reinterpret_cast<const T*>(a.x) + b * a.sb + n * a.sn + h * a.sh;
-    double ss = 0.0;
-    for (int c = 0; c < D; c += 16) {
-      float v[16];
-      load16<T>(src + c, v);
+  constexpr int RS = 33;                                   // padded row of a slice (floats)
+  __shared__ float sl[256 * RS];
+  const int64_t rows = a.B * a.N * a.H, row0 = (int64_t)blockIdx.x * 256;
+  const int t = threadIdx.x, q = t & 3;
+  // thread t loads the 8-channel piece q = t % 4 of rows t / 4 + 64 j
+  const T* base[4];
 #pragma unroll
-      for (int k = 0; k < 16; k++) ss += (double)v[k] * (double)v[k];   // exact products
-    }
-    a.rscale[row] = (float)(1.0 / __builtin_sqrt(ss / (double)D + a.eps));
+  for (int j = 0; j < 4; j++) {
+    const int64_t rr = row0 + (t >> 2) + 64 * j, row = rr < rows ? rr : rows - 1;
+    const int64_t h = row % a.H, n = (row / a.H) % a.N, b = row / (a.H * a.N);
+    base[j] = reinterpret_cast<const T*>(a.x) + b * a.sb + n * a.sn + h * a.sh + 8 * q;
   }
+  double ss = 0.0;
+  for (int c0 = 0; c0 < D; c0 += 32) {
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const int r = (t >> 2) + 64 * j;
+      const T* src = base[j] + c0;
+      float v[8];
+      if constexpr (sizeof(T) == 2) {
+        const uint4 u = *reinterpret_cast<const uint4*>(src);
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int m = 0; m < 4; m++) {
+          v[2 * m] = __uint_as_float(w[m] << 16);
+          v[2 * m + 1] = __uint_as_float(w[m] & 0xffff0000u);
+        }
+      } else {
+        const float4 x0 = reinterpret_cast<const float4*>(src)[0], x1 = reinterpret_cast<const float4*>(src)[1];
+        v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w; v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
+      }
+#pragma unroll
+      for (int k = 0; k < 8; k++) sl[r * RS + 8 * q + k] = v[k];
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int k = 0; k < 32; k++) {
+      const double x = (double)sl[t * RS + k];
+      ss += x * x;                                          // exact products
+    }
+    __syncthreads();
+  }
+  if (row0 + t < rows) a.rscale[row0 + t] = (float)(1.0 / __builtin_sqrt(ss / (double)D + a.eps));
 }
 
+// The key mean: FP64 sum of the block partial sums in block order (coalesced
+// over the channels), divided by N in FP64, rounded once to FP32.
 __global__ __launch_bounds__(256) void producer_mean_kernel(QuantArgs a, int D) {
   const int c = threadIdx.x;
   if (c >= D) return;
   const int64_t h = blockIdx.x, b = blockIdx.y, nblk = a.N / 32;
-  const double* p = a.partials + ((b * a.H + h) * D + c) * nblk;
+  const double* p = a.partials + (b * a.H + h) * nblk * D + c;
   double total = 0.0;
-  for (int64_t t = 0; t < nblk; t++) total += p[t];
+#pragma unroll 8
+  for (int64_t t = 0; t < nblk; t++) total += p[t * D];
   a.mean[(b * a.H + h) * D + c] = (float)(total / (double)a.N);
 }
 
@@ -322,15 +413,14 @@ hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_
   }
   const bool prod = a.prescale != 1.0f || a.mean || a.rope || a.gain;
   if (a.gain) {
-    const int64_t nblk = (a.B * a.N * a.H + 255) / 256;
-    const dim3 g0((unsigned)(nblk < 65536 ? nblk : 65536));
+    const dim3 g0((unsigned)((a.B * a.N * a.H + 255) / 256));
     if (dtype_bf16) hipLaunchKernelGGL(producer_rscale_kernel<uint16_t>, g0, dim3(256), 0, s, a, D);
     else hipLaunchKernelGGL(producer_rscale_kernel<float>, g0, dim3(256), 0, s, a, D);
   }
   if (a.mean) {
     const dim3 g1((unsigned)(a.N / 32), (unsigned)a.H, (unsigned)a.B), g2((unsigned)a.H, (unsigned)a.B);
-    if (dtype_bf16) hipLaunchKernelGGL(producer_partials_kernel<uint16_t>, g1, dim3(256), 0, s, a, D);
-    else hipLaunchKernelGGL(producer_partials_kernel<float>, g1, dim3(256), 0, s, a, D);
+    if (dtype_bf16) hipLaunchKernelGGL(producer_partials_kernel<uint16_t>, g1, dim3(D / 2), 0, s, a, D);
+    else hipLaunchKernelGGL(producer_partials_kernel<float>, g1, dim3(D / 2), 0, s, a, D);
     hipLaunchKernelGGL(producer_mean_kernel, g2, dim3(256), 0, s, a, D);
   }
 #define AFP8_Q(DD)                                                                                      \
