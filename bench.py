@@ -98,14 +98,16 @@ def write_traffic_summary(fetch_csv, write_csv, out, calib_mib):
     f_scale, w_scale = calib / (fc * 1024), calib / (wc * 1024)
     fetch, write = fb * 1024 * f_scale, wb * 1024 * w_scale
     total = int(round(fetch + write))
+    # the profiler's output directories are those of the CSVs given here
+    fdir_f, fdir_w = os.path.relpath(os.path.dirname(fetch_csv), ROOT), os.path.relpath(os.path.dirname(write_csv), ROOT)
     text = f"""# HBM traffic: bwd_kernel<128,128> on gqa_d128_8k (B=4, N=8192, Hq=16, Hkv=4, d=128, causal)
 
 Commands (MI355X, ROCm 7.2, repository root; `cd /tmp && export TMPDIR=/tmp` first):
 
 ```
-rocprofv3 --kernel-include-regex "bwd_kernel|neg" --pmc FETCH_SIZE -d gpurun_out/tr_fetch -o run --output-format csv -- python -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-protocol --copy-calibration {calib_mib}
-rocprofv3 --kernel-include-regex "bwd_kernel|neg" --pmc WRITE_SIZE -d gpurun_out/tr_write -o run --output-format csv -- python -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-protocol --copy-calibration {calib_mib}
-python bench.py --traffic-summary gpurun_out/tr_fetch/run_counter_collection.csv gpurun_out/tr_write/run_counter_collection.csv --copy-calibration {calib_mib}
+rocprofv3 --kernel-include-regex "bwd_kernel|neg" --pmc FETCH_SIZE -d {fdir_f} -o run --output-format csv -- python -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-protocol --copy-calibration {calib_mib}
+rocprofv3 --kernel-include-regex "bwd_kernel|neg" --pmc WRITE_SIZE -d {fdir_w} -o run --output-format csv -- python -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-protocol --copy-calibration {calib_mib}
+python bench.py --traffic-summary {os.path.relpath(fetch_csv, ROOT)} {os.path.relpath(write_csv, ROOT)} --copy-calibration {calib_mib}
 ```
 
 The calibration kernel is a float32 negate over {calib} bytes (it reads and writes
@@ -451,7 +453,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the hot path runs on a "
-              f"single MI355X; see the sharding notes in DESIGN.md)", file=sys.stderr)
+              f"single MI355X; the problem shards by (batch, KV head) without communication)", file=sys.stderr)
         sys.exit(2)
 
     import torch
