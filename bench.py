@@ -341,7 +341,8 @@ def protected_dp_line(run):
 def variants_line(run):
     """The f3/f4 options on the same workload, each the median of 20 timings
     after 5 warm-ups: the block-scaled backward probability operand (matched
-    backward call against the default one), a padded batch of sequences of
+    backward call against the default one), three isolated score channels
+    (forward + matched correction + backward), a padded batch of sequences of
     their own lengths (forward + matched correction + backward, credited
     with each sequence's own causal FLOPs), and the input producer (query:
     QK normalization, rotary embedding on 64 channels, prescale by tau; key:
@@ -362,6 +363,18 @@ def variants_line(run):
                                               delta_in=run.delta, workspace=run.ws, out=run.grads))
     out["pbwd_block_scaled"] = {"bwd_call_ms": round(t_pmx, 4), "default_bwd_call_ms": round(t_def, 4),
                                 "over_default": round(t_pmx / t_def - 1, 4)}
+    # three isolated score channels (forward + matched correction + backward)
+    pi = dataclasses.replace(run.p, flags=pk.FLAG_ISOLATE3)
+
+    def iso3_step():
+        pk.attn_fp8_fwd(pi, run.mq, run.mk, run.mv, o=run.o, lse=run.lse)
+        pk.attn_fp8_delta(pi, mode, run.mq, run.mk, run.mv, run.mdo, run.lse, run.do, run.o, delta=run.delta)
+        pk.attn_fp8_bwd(pi, mode, run.mq, run.mk, run.mv, run.mdo, run.lse, run.do, run.o, delta_in=run.delta,
+                        workspace=run.ws, out=run.grads)
+    t_iso = run.timed(iso3_step)
+    t_one = run.timed(lambda: (run.fwd(), run.correction(mode), run.bwd(mode)))
+    out["isolate3"] = {"fwd_bwd_ms": round(t_iso, 4), "one_channel_fwd_bwd_ms": round(t_one, 4),
+                       "over_one_channel": round(t_iso / t_one - 1, 4)}
     # sequences of their own lengths in the padded layout
     lens = [w.N - (w.N // 4) * (b % 4) for b in range(w.B)]
     pv = dataclasses.replace(run.p, seqlens_q=torch.tensor(lens, dtype=torch.int32, device="cuda:0"))

@@ -113,7 +113,16 @@ enum {
    * attn_fp8_bwd_noalloc refuse the flag, attn_fp8_delta refuses the matched
    * modes); attn_fp8_bwd_workspace_size counts its BF16 copies.  Not with
    * ATTN_FP8_FLAG_PBWD_BLOCK_SCALED, nor at head dims (256, 256). */
-  ATTN_FP8_FLAG_PROTECTED_DP = 2
+  ATTN_FP8_FLAG_PROTECTED_DP = 2,
+  /* Three isolated score channels instead of one (see the score-precision
+   * note at attn_fp8_mx): the channels with the three largest
+   * max_h amax_q[b,h,c] * amax_k[b,kv,c] are taken out of the FP8 MFMA and
+   * their exact products added in FP32, for inputs with several outlier
+   * channels.  An opt-in instantiation of the forward, the matched
+   * correction and the backward (one more rank-2 FP32 MFMA per 32 x 32
+   * score block); not with ATTN_FP8_FLAG_PBWD_BLOCK_SCALED,
+   * ATTN_FP8_FLAG_PROTECTED_DP or the compensated correction. */
+  ATTN_FP8_FLAG_ISOLATE3 = 4
 };
 
 /* Problem geometry, read-only.  softmax_scale (tau, e.g. 1/sqrt(dim_qk))
@@ -160,8 +169,9 @@ typedef struct {
  * channel (a large q_c k_c) rounds away the other products of its group.
  * When both q and k carry channel_amax, the channel c* maximizing
  * max_h amax_q[b,h,c] * amax_k[b,kv,c] (per batch and KV head; lowest index
- * on ties) is taken out of the MFMA (its codes are zeroed in both operands)
- * and its exact product q^_c* k^_c* is added to the FP32 score. */
+ * on ties) is taken out of the MFMA (its codes are zeroed in one operand)
+ * and its exact product q^_c* k^_c* is added to the FP32 score; with
+ * ATTN_FP8_FLAG_ISOLATE3 the three channels with the largest products. */
 typedef struct {
   uint8_t* code_row;
   uint8_t* scale_row;

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libattn_fp8.so")
 
 DTYPE_F32, DTYPE_BF16 = 0, 1
 DELTA_MATCHING, DELTA_STALE_ROWSUM, DELTA_CONSISTENT_DO, DELTA_MATCHING_COMPENSATED = 0, 1, 2, 3
-FLAG_PBWD_BLOCK_SCALED, FLAG_PROTECTED_DP = 1, 2
+FLAG_PBWD_BLOCK_SCALED, FLAG_PROTECTED_DP, FLAG_ISOLATE3 = 1, 2, 4
 QUANT_ROW, QUANT_COL, QUANT_BOTH = 1, 2, 3
 # fields of the backward's per-row statistics [B, Hq, N, ROWSTATS] (FP64)
 RS_SUM_DS, RS_SUMABS_DS, RS_SUM_DSCAST, RS_MAXABS_DS, RS_SUMABS_DSCAST, RS_MAX_PDP, RS_SUM_PCAST = range(7)

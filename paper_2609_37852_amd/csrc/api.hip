@@ -94,8 +94,11 @@ int check_problem(const attn_fp8_problem* p) {
     return fail(ATTN_FP8_EUNSUPPORTED, "head dims (%lld, %lld) not instantiated", (long long)p->dim_qk,
                 (long long)p->dim_v);
   if (p->causal != 0 && p->causal != 1) return fail(ATTN_FP8_EINVAL, "causal must be 0 or 1");
-  if (p->flags & ~(ATTN_FP8_FLAG_PBWD_BLOCK_SCALED | ATTN_FP8_FLAG_PROTECTED_DP))
+  if (p->flags & ~(ATTN_FP8_FLAG_PBWD_BLOCK_SCALED | ATTN_FP8_FLAG_PROTECTED_DP | ATTN_FP8_FLAG_ISOLATE3))
     return fail(ATTN_FP8_EINVAL, "unknown flags 0x%x", p->flags);
+  if ((p->flags & ATTN_FP8_FLAG_ISOLATE3) &&
+      (p->flags & (ATTN_FP8_FLAG_PBWD_BLOCK_SCALED | ATTN_FP8_FLAG_PROTECTED_DP)))
+    return fail(ATTN_FP8_EUNSUPPORTED, "three isolated channels with another numerics variant");
   if (p->flags & ATTN_FP8_FLAG_PROTECTED_DP) {
     if (p->flags & ATTN_FP8_FLAG_PBWD_BLOCK_SCALED)
       return fail(ATTN_FP8_EUNSUPPORTED, "protected dP with the block-scaled backward probability operand");
@@ -154,6 +157,7 @@ afp8::AttnArgs base_args(const attn_fp8_problem* p) {
   a.Nk = kv_len(p);
   a.causal = p->causal;
   a.pmx = (p->flags & ATTN_FP8_FLAG_PBWD_BLOCK_SCALED) != 0;
+  a.iso3 = (p->flags & ATTN_FP8_FLAG_ISOLATE3) != 0;
   a.lens_q = p->seqlens_q;
   a.lens_k = p->causal ? nullptr : p->seqlens_kv;
   a.tau = p->softmax_scale;
@@ -228,6 +232,8 @@ int check_delta_inputs(const attn_fp8_problem* p, int mode, const attn_fp8_mx* q
   if (mode == ATTN_FP8_DELTA_MATCHING || mode == ATTN_FP8_DELTA_MATCHING_COMPENSATED) {
     if (p->flags & ATTN_FP8_FLAG_PROTECTED_DP)
       return fail(ATTN_FP8_EUNSUPPORTED, "the matched correction of the protected-dP variant (its dP is BF16)");
+    if ((p->flags & ATTN_FP8_FLAG_ISOLATE3) && mode == ATTN_FP8_DELTA_MATCHING_COMPENSATED)
+      return fail(ATTN_FP8_EUNSUPPORTED, "the compensated correction with three isolated channels");
     if ((rc = check_mx("q", q, true, false)) || (rc = check_mx("k", k, true, false)) ||
         (rc = check_mx("v", v, true, false)) || (rc = check_mx("dout", dout, true, false)) ||
         (rc = check_ptr("lse", lse)))
@@ -509,6 +515,8 @@ static int bwd_impl(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx
   if ((rc = check_problem(p))) return rc;
   if (delta_mode < ATTN_FP8_DELTA_MATCHING || delta_mode > ATTN_FP8_DELTA_MATCHING_COMPENSATED)
     return fail(ATTN_FP8_EINVAL, "unknown delta_mode %d", delta_mode);
+  if ((p->flags & ATTN_FP8_FLAG_ISOLATE3) && delta_mode == ATTN_FP8_DELTA_MATCHING_COMPENSATED)
+    return fail(ATTN_FP8_EUNSUPPORTED, "the compensated correction with three isolated channels");
   const int gs = dtype_size(grad_dtype);
   if (!gs) return fail(ATTN_FP8_EINVAL, "grad_dtype %d", grad_dtype);
   if (empty(p)) return ok();

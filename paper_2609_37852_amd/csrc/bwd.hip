@@ -255,6 +255,7 @@ static hipError_t bwd_dispatch(const AttnArgs& a0, hipStream_t s) {
   const int64_t per_head = cus / (a.B * a.Hkv);
   a.bwd_cohort = (int)(per_head > 1 ? per_head : 1);
   if (a.pdp) return a.causal ? launch_bwd_main<true, 4>(a, DQK, DV, grid, s) : launch_bwd_main<false, 4>(a, DQK, DV, grid, s);
+  if (a.iso3) return a.causal ? launch_bwd_main<true, 8>(a, DQK, DV, grid, s) : launch_bwd_main<false, 8>(a, DQK, DV, grid, s);
   switch ((a.causal ? 4 : 0) | (a.pmx ? 2 : 0) | (a.comp ? 1 : 0)) {
     case 0: return launch_bwd_main<false, 0>(a, DQK, DV, grid, s);
     case 1: return launch_bwd_main<false, 1>(a, DQK, DV, grid, s);

@@ -285,10 +285,14 @@ __device__ __forceinline__ TilePos next_pos(TilePos p, int G) {
 
 // CAUSAL: the mask (key length = query length) or every key of Nk; VAR:
 // numerics variant, bit 0 compensated dS formation (COMP), bit 1 block-scaled
-// backward probability operand (PMX), bit 2 dP from BF16 operands (PDP)
+// backward probability operand (PMX), bit 2 dP from BF16 operands (PDP),
+// bit 3 three isolated score channels (ISO3: channels 1 and 2 take a second
+// rank-2 FP32 MFMA after the one that adds channel 0 and the shift, as in the
+// correction pass, so both form S identically)
 template <int DQK, int DV, bool STATS, bool CAUSAL, int VAR>
 __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) {
-  constexpr bool PDP = (VAR & 4) != 0;
+  constexpr bool PDP = (VAR & 4) != 0, ISO3 = (VAR & 8) != 0;
+  constexpr int NH = ISO3 ? 3 : 1;
   using C = BwdCfg<DQK, DV, PDP>;
   constexpr int KBW = C::KBW, BKB = C::BKB, BQ = C::BQ, NCB = C::NCB;
   constexpr int KS = DQK / 64, VS = DV / 64, CK = DQK / 32, CV = DV / 32;
@@ -310,7 +314,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   // order: [0] dS' of the first half (for dK), [1] P' of the second (for dV)
   __shared__ __attribute__((aligned(16))) uint4 xA[2][KBW * 64];
   __shared__ __attribute__((aligned(16))) uint4 xB[2][KBW * 64];
-  __shared__ int hot_slot;
+  __shared__ int hot_slot[NH];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
   const int kbw = w % KBW;                      // this wave's 32-key block within the workgroup
@@ -334,7 +338,10 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   const int kw0 = kb0 + 32 * kbw;               // this wave's first key
   const bool live = kw0 < L.k;
   const int kj = kw0 + li;                      // this lane's key
-  const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
+  int hots[NH];
+  if constexpr (NH == 1) hots[0] = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, hot_slot);
+  else select_hot_channels<DQK, NH>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, hot_slot, hots);
+  const int hot = hots[0];
   const size_t bhk = (size_t)b * a.Hkv + kh;
   const int Hq = (int)a.Hq, G = (int)a.G;
   const float c = a.c;
@@ -345,6 +352,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   v8i kf[KS], vf[VS];
   int ksc[KS], vsc[VS];
   float kb = 1.0f;
+  float kb12 = 0.f;   // ISO3: the key's channel 1 (lanes < 32) and 2 (lanes >= 32) values
   constexpr bool KVL = C::KV_LDS;
   __shared__ __attribute__((aligned(16))) uint8_t kL[KVL ? BKB * DQK : 16];
   __shared__ __attribute__((aligned(16))) uint8_t vL[KVL && !PDP ? BKB * DV : 16];
@@ -358,7 +366,8 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
 #pragma unroll
     for (int s = 0; s < KS; s++) {
       kf[s] = frag_rows_global(kr, s, hf);
-      clear_channel(kf[s], s, hf, hot);
+#pragma unroll
+      for (int i = 0; i < NH; i++) clear_channel(kf[s], s, hf, hots[i]);
       ksc[s] = a.k_scale[(bhk * Nk + row) * (DQK / 32) + 2 * s + hf];
     }
     if constexpr (!PDP) {
@@ -380,6 +389,10 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
     }
     if (hf == 0)
       kb = hot >= 0 ? row_value<DQK>(a.k_code + bhk * Nk * DQK, a.k_scale + bhk * Nk * (DQK / 32), row, hot) : 0.f;
+    if constexpr (ISO3) {
+      if (hot >= 0)
+        kb12 = row_value<DQK>(a.k_code + bhk * Nk * DQK, a.k_scale + bhk * Nk * (DQK / 32), row, hf ? hots[2] : hots[1]);
+    }
     if constexpr (KVL) {
       // the first wave of each key block stores the K fragments, the second
       // the V fragments, where frag_rows_swz reads them (visible after the
@@ -581,6 +594,16 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
   };
   auto mfmas = [&](const uint8_t* R, bool skip, float rec, const uint8_t* Cc, const uint8_t* es,
                    uint4 (*x)[KBW * 64], auto back_tag) __attribute__((always_inline)) {
+    // ISO3: the lane's query's channel 1 (lanes < 32) or 2 value, decoded
+    // from the staged Q row tile
+    [[maybe_unused]] float rec12 = 0.f;
+    if constexpr (ISO3) {
+      if (hot >= 0) {
+        const int row = 32 * qs + li, c = hf ? hots[2] : hots[1];
+        const uint32_t code = R[C::Q_OFF + row * DQK + 16 * ((c >> 4) ^ swz_row<DQK>(row)) + (c & 15)];
+        rec12 = scaled_value(code, R[C::QS_OFF + row * (DQK / 32) + c / 32]);
+      }
+    }
     const uint8_t* Q = R + C::Q_OFF;
     const uint8_t* Qs = R + C::QS_OFF;
     const uint8_t* O = R + C::O_OFF;
@@ -669,6 +692,7 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
         if (act) exec(m, cur);
         if (M0 == 0 && m == R2) {
           s = rank2_update(rec, kb, s);
+          if constexpr (ISO3) s = rank2_update(rec12, kb12, s);
         }
         __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);   // the reads of the next MFMA
         __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);    // then this step's MFMAs
@@ -841,11 +865,13 @@ AFP8_BWD_EXTERN(true, 1)
 AFP8_BWD_EXTERN(true, 2)
 AFP8_BWD_EXTERN(true, 3)
 AFP8_BWD_EXTERN(true, 4)
+AFP8_BWD_EXTERN(true, 8)
 AFP8_BWD_EXTERN(false, 0)
 AFP8_BWD_EXTERN(false, 1)
 AFP8_BWD_EXTERN(false, 2)
 AFP8_BWD_EXTERN(false, 3)
 AFP8_BWD_EXTERN(false, 4)
+AFP8_BWD_EXTERN(false, 8)
 #undef AFP8_BWD_EXTERN
 
 }  // namespace afp8

@@ -1,0 +1,7 @@
+// Main backward kernel, causal, three isolated score channels: every
+// head-dim pair, with and without row statistics.
+#include "bwd_main.hpp"
+
+namespace afp8 {
+template hipError_t launch_bwd_main<true, 8>(const AttnArgs&, int, int, dim3, hipStream_t);
+}  // namespace afp8

@@ -32,7 +32,7 @@
 
 namespace afp8 {
 
-template <int DQK, int DV>
+template <int DQK, int DV, int NH = 1>
 struct DeltaCfg {
   static constexpr int NW = 4, NT = 64 * NW, BQ = 32 * NW, BK = 128;
   static constexpr int al16(int x) { return (x + 15) & ~15; }
@@ -40,22 +40,23 @@ struct DeltaCfg {
   static constexpr int V_OFF = K_OFF + BK * DQK;                // V row codes [BK][DV], swizzled
   static constexpr int KS_OFF = V_OFF + BK * DV;                // K row scales [BK][DQK/32]
   static constexpr int VS_OFF = al16(KS_OFF + BK * DQK / 32);   // V row scales [BK][DV/32]
-  static constexpr int KH_OFF = al16(VS_OFF + BK * DV / 32);    // isolated-channel key values [BK] FP32
-  static constexpr int STAGE = KH_OFF + BK * 4;
+  static constexpr int KH_OFF = al16(VS_OFF + BK * DV / 32);    // isolated-channel key values [NH][BK] FP32
+  static constexpr int STAGE = KH_OFF + BK * 4 * NH;
   // two workgroups per CU where both stage buffers fit 80 KB
   static constexpr int WGS = 2 * STAGE <= 80 * 1024 ? 2 : 1;
 };
 
 // CAUSAL: the mask (key length = query length) or every key of Nk; COMP:
-// FP64 products and sums
-template <int DQK, int DV, bool CAUSAL, bool COMP>
-__global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_kernel(AttnArgs a) {
-  using C = DeltaCfg<DQK, DV>;
+// FP64 products and sums; NH: isolated score channels (with 3, channels 1
+// and 2 take a second rank-2 FP32 MFMA, the first shares one with the shift)
+template <int DQK, int DV, bool CAUSAL, bool COMP, int NH = 1>
+__global__ __launch_bounds__(256, (DeltaCfg<DQK, DV, NH>::WGS)) void delta_matching_kernel(AttnArgs a) {
+  using C = DeltaCfg<DQK, DV, NH>;
   constexpr int NW = C::NW, BQ = C::BQ, BK = C::BK;
   constexpr int KS = DQK / 64, VS = DV / 64;
   __shared__ __attribute__((aligned(16))) uint8_t stA[C::STAGE];
   __shared__ __attribute__((aligned(16))) uint8_t stB[C::STAGE];
-  __shared__ int hot_slot;
+  __shared__ int hot_slot[NH];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
   constexpr bool causal = CAUSAL;
@@ -72,7 +73,10 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   const int qi = q0 + li;
   // groups visible to the wave's queries start before klim (a multiple of 32)
   const int klim = causal ? q0 + 32 : L.k;
-  const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
+  int hots[NH];
+  if constexpr (NH == 1) hots[0] = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, hot_slot);
+  else select_hot_channels<DQK, NH>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, hot_slot, hots);
+  const int hot = hots[0];
 
   const size_t bhq = (size_t)b * a.Hq + h, bhk = (size_t)b * a.Hkv + kh;
   v8i qf[KS], df[VS];
@@ -80,12 +84,14 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
   // B operand of the score's rank-2 update: isolated-channel value (lanes
   // < 32), -LSE / tau (lanes >= 32) of the lane's query
   float qv = 0.f;
+  float qv12 = 0.f;   // NH = 3: channel 1 (lanes < 32) and 2 (lanes >= 32) of the lane's query
   {
     const size_t row = bhq * N + (live ? qi : 0);
 #pragma unroll
     for (int s = 0; s < KS; s++) {
       qf[s] = frag_rows_global(a.q_code + row * DQK, s, hf);
-      clear_channel(qf[s], s, hf, hot);
+#pragma unroll
+      for (int i = 0; i < NH; i++) clear_channel(qf[s], s, hf, hots[i]);
       qsc[s] = a.q_scale[row * (DQK / 32) + 2 * s + hf];
     }
 #pragma unroll
@@ -95,6 +101,9 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
     }
     const float qhot = hot >= 0 ? row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot) : 0.f;
     qv = hf ? neg_lse_over_tau(a.lse[row], a.tau) : qhot;
+    if constexpr (NH == 3) {
+      if (hot >= 0) qv12 = row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hf ? hots[2] : hots[1]);
+    }
   }
   double num = 0.0, den = 0.0;
 
@@ -108,7 +117,7 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
 
   // loads of tile j0 (raw isolated-channel bytes in registers, decoded when
   // they are stored to LDS)
-  uint32_t khc = 0, khs = 0;
+  uint32_t khc[NH] = {}, khs[NH] = {};
   RowLoads<DQK, NW, BK> kload;
   RowLoads<DV, NW, BK> vload;
   kload.init(w, lane);
@@ -121,14 +130,20 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
     dma_row_scales<DV, NW, BK>(st + C::VS_OFF, vscale, j0, L.k, w, lane, 1);
     if (hot >= 0 && threadIdx.x < BK) {
       const int r = j0 + (int)threadIdx.x < L.k ? j0 + (int)threadIdx.x : L.k - 1;
-      khc = kcode[(int64_t)r * DQK + hot];
-      khs = kscale[(int64_t)r * (DQK / 32) + hot / 32];
+#pragma unroll
+      for (int i = 0; i < NH; i++) {
+        khc[i] = kcode[(int64_t)r * DQK + hots[i]];
+        khs[i] = kscale[(int64_t)r * (DQK / 32) + hots[i] / 32];
+      }
     }
     __builtin_amdgcn_sched_barrier(0);   // keep every load ahead of the tile's compute
   };
   auto finish = [&](uint8_t* st) __attribute__((always_inline)) {
-    if (threadIdx.x < BK)
-      reinterpret_cast<float*>(st + C::KH_OFF)[threadIdx.x] = hot >= 0 ? scaled_value(khc, khs) : 0.f;
+    if (threadIdx.x < BK) {
+#pragma unroll
+      for (int i = 0; i < NH; i++)
+        reinterpret_cast<float*>(st + C::KH_OFF)[i * BK + threadIdx.x] = hot >= 0 ? scaled_value(khc[i], khs[i]) : 0.f;
+    }
   };
 
   // Scores (with the rank-2 update) and dP of one 32-key group (keys
@@ -152,6 +167,7 @@ __global__ __launch_bounds__(256, (DeltaCfg<DQK, DV>::WGS)) void delta_matching_
     // S + k_c* q_c* - LSE / tau: A = isolated-channel key value (lanes
     // < 32) or 1 (lanes >= 32), B = qv
     s = rank2_update(hf ? 1.0f : Kh[32 * g + li], qv, s);
+    if constexpr (NH == 3) s = rank2_update(Kh[(hf ? 2 * BK : BK) + 32 * g + li], qv12, s);
   };
   // P, then the group's sums of P dP and P; DIAG: the group holding the
   // wave's diagonal (keys after the query masked).  The lane holds keys
@@ -244,7 +260,10 @@ static hipError_t delta_dispatch(const AttnArgs& a, hipStream_t s) {
   using C = DeltaCfg<DQK, DV>;
   const int64_t nqb = (a.N + C::BQ - 1) / C::BQ;
   const dim3 grid((unsigned)(nqb * a.Hq * a.B));
-  if (a.causal) {
+  if (a.iso3) {
+    if (a.causal) hipLaunchKernelGGL((delta_matching_kernel<DQK, DV, true, false, 3>), grid, dim3(C::NT), 0, s, a);
+    else hipLaunchKernelGGL((delta_matching_kernel<DQK, DV, false, false, 3>), grid, dim3(C::NT), 0, s, a);
+  } else if (a.causal) {
     if (a.comp) hipLaunchKernelGGL((delta_matching_kernel<DQK, DV, true, true>), grid, dim3(C::NT), 0, s, a);
     else hipLaunchKernelGGL((delta_matching_kernel<DQK, DV, true, false>), grid, dim3(C::NT), 0, s, a);
   } else {

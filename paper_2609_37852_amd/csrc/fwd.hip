@@ -46,11 +46,14 @@ constexpr float kLog2_448 = 8.807354922057604f;
 // same whenever the rescales happen.
 constexpr float kLazyRescale = 16.0f;
 
-template <int DQK, int DV>
+// NH: isolated score channels (1, or 3 with ATTN_FP8_FLAG_ISOLATE3)
+template <int DQK, int DV, int NH = 1>
 struct FwdCfg {
   static constexpr int NW = 4, NT = 64 * NW, BQ = 32 * NW;
   static constexpr int al16(int x) { return (x + 15) & ~15; }
-  static constexpr int stage_bytes(int bk) { return al16(al16(bk * (DQK + DV) + bk * DQK / 32) + DV * 4) + bk * 4; }
+  static constexpr int stage_bytes(int bk) {
+    return al16(al16(bk * (DQK + DV) + bk * DQK / 32) + DV * 4) + bk * 4 * NH;
+  }
   // 128-key tiles where two double-buffered workgroups fit a CU's LDS,
   // else 64-key tiles (wide heads)
   static constexpr int BK = 2 * stage_bytes(128) <= 80 * 1024 ? 128 : 64;
@@ -58,23 +61,25 @@ struct FwdCfg {
   static constexpr int V_OFF = K_OFF + BK * DQK;                // V col codes [DV][BK], swizzled
   static constexpr int KS_OFF = V_OFF + DV * BK;                // K row scales [BK][DQK/32]
   static constexpr int VS_OFF = al16(KS_OFF + BK * DQK / 32);   // V col scales [DV][4] (BK/32 used)
-  static constexpr int KH_OFF = al16(VS_OFF + DV * 4);          // isolated-channel key values [BK] FP32
-  static constexpr int STAGE = KH_OFF + BK * 4;
+  static constexpr int KH_OFF = al16(VS_OFF + DV * 4);          // isolated-channel key values [NH][BK] FP32
+  static constexpr int STAGE = KH_OFF + BK * 4 * NH;
   static_assert(STAGE == stage_bytes(BK), "stage layout");
   static_assert(DV <= NT, "one V scale word per thread");
   static_assert(BQ % BK == 0, "a query block's diagonal starts a key tile");
 };
 
 // CAUSAL: the mask (key length = query length) or every key of Nk; a
-// template parameter, so the causal kernel carries no key-length arithmetic
-template <int DQK, int DV, bool CAUSAL>
+// template parameter, so the causal kernel carries no key-length arithmetic.
+// NH: isolated score channels; with 3, the first two share one rank-2 FP32
+// MFMA (its two k slots) and the third takes a second one.
+template <int DQK, int DV, bool CAUSAL, int NH = 1>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
-  using C = FwdCfg<DQK, DV>;
+  using C = FwdCfg<DQK, DV, NH>;
   constexpr int NW = C::NW, BQ = C::BQ, BK = C::BK;
   constexpr int KS = DQK / 64, CB = DV / 32;
   __shared__ __attribute__((aligned(16))) uint8_t stA[C::STAGE];
   __shared__ __attribute__((aligned(16))) uint8_t stB[C::STAGE];
-  __shared__ int hot_slot;
+  __shared__ int hot_slot[NH];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, li = lane & 31;
   constexpr bool causal = CAUSAL;
@@ -92,7 +97,10 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   // keys j0 .. visible to the wave's queries start groups before klim (a
   // multiple of 32): the diagonal group's end when causal, else the key length
   const int klim = causal ? q0 + 32 : L.k;
-  const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
+  int hots[NH];
+  if constexpr (NH == 1) hots[0] = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, hot_slot);
+  else select_hot_channels<DQK, NH>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, hot_slot, hots);
+  const int hot = hots[0];
 
   const size_t bhq = (size_t)b * a.Hq + h, bhk = (size_t)b * a.Hkv + kh;
   const uint8_t* kcode = a.k_code + bhk * Nk * DQK;
@@ -103,15 +111,22 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   v8i qf[KS];
   int qsc[KS];
   float qv = 0.f;     // B operand of the isolated channel's rank-1 update (lanes < 32)
+  float qv2 = 0.f;    // NH = 3: qv holds channel 0 (lanes < 32) and 1 (lanes >= 32), qv2 channel 2
   {
     const size_t row = bhq * N + (live ? qi : 0);
 #pragma unroll
     for (int s = 0; s < KS; s++) {
       qf[s] = frag_rows_global(a.q_code + row * DQK, s, hf);
       qsc[s] = a.q_scale[row * (DQK / 32) + 2 * s + hf];
-      clear_channel(qf[s], s, hf, hot);
+#pragma unroll
+      for (int i = 0; i < NH; i++) clear_channel(qf[s], s, hf, hots[i]);
     }
-    if (hot >= 0 && hf == 0) qv = row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot);
+    if constexpr (NH == 1) {
+      if (hot >= 0 && hf == 0) qv = row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot);
+    } else if (hot >= 0) {
+      qv = row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hf ? hots[1] : hots[0]);
+      if (hf == 0) qv2 = row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hots[2]);
+    }
   }
 
   v16f oacc[CB];
@@ -130,7 +145,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
   // (4 strided bytes per channel) and the isolated-channel bytes of each key
   // through registers, written by finish().
   uint32_t vsr[BK / 32] = {};
-  uint32_t khc = 0, khs = 0;
+  uint32_t khc[NH] = {}, khs[NH] = {};
   RowLoads<DQK, NW, BK> kload;
   ColLoads<DV, NW, BK> vload;
   kload.init(w, lane);
@@ -149,8 +164,11 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
     }
     if (hot >= 0 && threadIdx.x < BK) {
       const int r = j0 + (int)threadIdx.x < L.k ? j0 + (int)threadIdx.x : L.k - 1;
-      khc = kcode[(int64_t)r * DQK + hot];
-      khs = kscale[(int64_t)r * (DQK / 32) + hot / 32];
+#pragma unroll
+      for (int i = 0; i < NH; i++) {
+        khc[i] = kcode[(int64_t)r * DQK + hots[i]];
+        khs[i] = kscale[(int64_t)r * (DQK / 32) + hots[i] / 32];
+      }
     }
     __builtin_amdgcn_sched_barrier(0);   // keep every load ahead of the tile's compute
   };
@@ -162,8 +180,11 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
       else
         *reinterpret_cast<uint16_t*>(st + C::VS_OFF + 4 * threadIdx.x) = (uint16_t)(vsr[0] | (vsr[1] << 8));
     }
-    if (threadIdx.x < BK)
-      reinterpret_cast<float*>(st + C::KH_OFF)[threadIdx.x] = hot >= 0 ? scaled_value(khc, khs) : 0.f;
+    if (threadIdx.x < BK) {
+#pragma unroll
+      for (int i = 0; i < NH; i++)
+        reinterpret_cast<float*>(st + C::KH_OFF)[i * BK + threadIdx.x] = hot >= 0 ? scaled_value(khc[i], khs[i]) : 0.f;
+    }
   };
 
   // FULL: every key of the tile is visible to every query of the wave (no
@@ -197,7 +218,12 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
                           Ks[(32 * kb + li) * (DQK / 32) + 2 * t + hf], qsc[t]);
         // + k_c* q_c*: rank-1 update, A = isolated-channel key value
         // (lanes < 32), B = qv; lanes >= 32 contribute 0 * 0
-        if (hot >= 0) s[g2] = rank2_update(hf ? 0.f : Kh[32 * kb + li], qv, s[g2]);
+        if constexpr (NH == 1) {
+          if (hot >= 0) s[g2] = rank2_update(hf ? 0.f : Kh[32 * kb + li], qv, s[g2]);
+        } else if (hot >= 0) {
+          s[g2] = rank2_update(Kh[(hf ? BK : 0) + 32 * kb + li], qv, s[g2]);
+          s[g2] = rank2_update(hf ? 0.f : Kh[2 * BK + 32 * kb + li], qv2, s[g2]);
+        }
         // lane holds keys g0 + 8 (r/4) + 4 hf + r % 4 of query qi
         float m = -__builtin_inff();
         if (!FULL && causal && g0 == q0) {     // the diagonal group: keys after the query are masked
@@ -327,8 +353,13 @@ static hipError_t fwd_dispatch(const AttnArgs& a, hipStream_t s) {
   using C = FwdCfg<DQK, DV>;
   const int64_t nqb = (a.N + C::BQ - 1) / C::BQ;
   const dim3 grid((unsigned)(nqb * a.Hq * a.B));
-  if (a.causal) hipLaunchKernelGGL((fwd_kernel<DQK, DV, true>), grid, dim3(C::NT), 0, s, a);
-  else hipLaunchKernelGGL((fwd_kernel<DQK, DV, false>), grid, dim3(C::NT), 0, s, a);
+  if (a.iso3) {
+    if (a.causal) hipLaunchKernelGGL((fwd_kernel<DQK, DV, true, 3>), grid, dim3(C::NT), 0, s, a);
+    else hipLaunchKernelGGL((fwd_kernel<DQK, DV, false, 3>), grid, dim3(C::NT), 0, s, a);
+  } else {
+    if (a.causal) hipLaunchKernelGGL((fwd_kernel<DQK, DV, true>), grid, dim3(C::NT), 0, s, a);
+    else hipLaunchKernelGGL((fwd_kernel<DQK, DV, false>), grid, dim3(C::NT), 0, s, a);
+  }
   return hipGetLastError();
 }
 

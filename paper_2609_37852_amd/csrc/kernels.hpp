@@ -69,6 +69,7 @@ struct AttnArgs {
                              // compensated dS formation in the backward
   int pmx;                   // block-scaled backward probability operand (one scale per 32x32 block)
   int pdp;                   // protected dP: dP = dO V^T from the BF16 copies below
+  int iso3;                  // three isolated score channels instead of one
   float c;                   // tau * log2(e), applied to the score accumulator
   float tau;
   const uint8_t *q_code, *q_scale;     // row copy of Q      [B,Hq,N,Dqk], [B,Hq,N,Dqk/32]

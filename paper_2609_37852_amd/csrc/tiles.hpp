@@ -165,6 +165,56 @@ __device__ __forceinline__ int select_hot_channel(const float* q_amax, const flo
   return *slot;
 }
 
+// The NH isolated score channels of KV head kh (ATTN_FP8_FLAG_ISOLATE3):
+// the channels with the NH largest max_{h in group} q_amax[b,h,c] *
+// k_amax[b,kh,c], in decreasing order (lowest index first on ties), chosen
+// one at a time by select_hot_channel's rule over the channels not yet
+// taken; all -1 without the per-channel maxima.  Computed by wave 0; every
+// thread of the block gets the same values (contains a barrier).
+template <int D, int NH>
+__device__ __forceinline__ void select_hot_channels(const float* q_amax, const float* k_amax, int64_t b,
+                                                    int64_t kh, int64_t Hq, int64_t Hkv, int64_t G, int* slots,
+                                                    int (&hot)[NH]) {
+  if (!q_amax || !k_amax) {
+#pragma unroll
+    for (int i = 0; i < NH; i++) hot[i] = -1;
+    return;
+  }
+  if (threadIdx.x < 64) {
+    constexpr int PER = D / 64;       // channels per lane: threadIdx.x + 64 u
+    float sc[PER];
+#pragma unroll
+    for (int u = 0; u < PER; u++) {
+      const int c = threadIdx.x + 64 * u;
+      float qm = 0.f;
+      for (int64_t g = 0; g < G; g++) qm = fmaxf(qm, q_amax[(b * Hq + kh * G + g) * D + c]);
+      sc[u] = qm * k_amax[(b * Hkv + kh) * D + c];
+    }
+#pragma unroll
+    for (int i = 0; i < NH; i++) {
+      float best = -1.f;
+      int bi = D;
+#pragma unroll
+      for (int u = 0; u < PER; u++)
+        if (sc[u] > best) { best = sc[u]; bi = threadIdx.x + 64 * u; }
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) {
+        const float ob = __shfl_xor(best, m);
+        const int oi = __shfl_xor(bi, m);
+        if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
+      }
+      // the chosen channel is out of the next rounds
+#pragma unroll
+      for (int u = 0; u < PER; u++)
+        if (threadIdx.x + 64 * u == bi) sc[u] = -2.f;
+      if (threadIdx.x == 0) slots[i] = bi < D ? bi : -1;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < NH; i++) hot[i] = slots[i];
+}
+
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 // The four code dwords a lane holds for one 32-wide block of an MFMA result

@@ -278,3 +278,30 @@ def test_seqlens_checks():
     ref = ctypes.c_size_t(0)
     assert L.attn_fp8_bwd_workspace_size(ctypes.byref(_prob(causal=0).c()), ctypes.byref(ref)) == 0
     assert n.value == ref.value > 0
+
+
+def test_isolate3_combinations():
+    """Three isolated channels combine with none of the other numerics
+    variants, nor with the compensated correction."""
+    L = pk.lib()
+    m = _fake_mx()
+    st = bd._I64x3(128 * 2 * 128, 2 * 128, 128)
+
+    def fwd(flags):
+        p = _prob(flags=flags).c()
+        return L.attn_fp8_fwd(ctypes.byref(p), ctypes.byref(m), ctypes.byref(m), ctypes.byref(m),
+                              ctypes.c_void_p(4096), 1, st, ctypes.c_void_p(4096), None)
+    assert fwd(pk.FLAG_ISOLATE3 | pk.FLAG_PBWD_BLOCK_SCALED) == -2
+    assert fwd(pk.FLAG_ISOLATE3 | pk.FLAG_PROTECTED_DP) == -2
+    assert fwd(8) == -1
+    p = _prob(flags=pk.FLAG_ISOLATE3).c()
+    # (every call here fails a later check too, so none could launch: no LSE
+    # for the correction, a one-byte workspace for the backward)
+    rc = L.attn_fp8_delta(ctypes.byref(p), pk.DELTA_MATCHING_COMPENSATED, *[ctypes.byref(m)] * 4,
+                          None, None, 1, None, None, 1, None, ctypes.c_void_p(4096), None)
+    assert rc == -2 and "isolated" in pk.last_error()
+    rc = L.attn_fp8_bwd(ctypes.byref(p), pk.DELTA_MATCHING_COMPENSATED, *[ctypes.byref(m)] * 4,
+                        ctypes.c_void_p(4096), None, 1, None, None, 1, None, ctypes.c_void_p(4096),
+                        *[ctypes.c_void_p(4096)] * 3, 1, st, st, st, ctypes.c_void_p(4096), 1, None, None,
+                        None)
+    assert rc == -2 and "isolated" in pk.last_error()

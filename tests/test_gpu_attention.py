@@ -132,10 +132,14 @@ def test_injected_lse_reaches_the_probability_clamp():
 def test_three_outlier_channels():
     """Robustness of the isolated score channel: three x20 channels in Q and K
     (the kernels take one channel out of the MFMA; the other two stay in its
-    grouped accumulation)."""
+    grouped accumulation).  ATTN_FP8_FLAG_ISOLATE3 (next test) covers it."""
+    _three_outliers(0)
+
+
+def _three_outliers(flags):
     w = _workload("gqa_d128_8k", dict(B=1, N=320, Hq=4, Hkv=1, transform="outlier3"))
     d = synth.generate(w, seed=1)
-    g = run_gpu(w, d)
+    g = run_gpu(w, d, flags=flags)
     o = run_oracle(w, d)
     errs, blk = _compare(g, o)
     errs["LSE"] = float(np.max(np.abs(g["LSE"] - o["LSE"])))
@@ -147,6 +151,34 @@ def test_three_outlier_channels():
         assert errs[k] <= REL_TOL, (k, errs[k])
     check_blocks(blk)
     assert rep["violations"] == 0
+
+
+def test_three_outlier_channels_isolated():
+    """The same three x20 channels with ATTN_FP8_FLAG_ISOLATE3: all three are
+    taken out of the MFMA and their products added exactly."""
+    _three_outliers(pk.FLAG_ISOLATE3)
+
+
+@pytest.mark.parametrize("name,kw", [("gqa_d128_8k", dict(B=1, N=256, Hq=4, Hkv=2)),
+                                     ("gqa_d256_8k_qknorm", dict(B=1, N=160, Hq=2, Hkv=1)),
+                                     ("mla_d192_4k", dict(B=1, N=128, Hq=2, Hkv=2, causal=False, Nk=192)),
+                                     ("tiny_mha_128", dict(B=2, N=96))])
+def test_isolate3_parity(name, kw):
+    """Three isolated channels on the other recipes and head dims (one or no
+    outlier channel): parity and the invariant as in the default mode."""
+    w = _workload(name, kw)
+    d = synth.generate(w, seed=2)
+    g = run_gpu(w, d, flags=pk.FLAG_ISOLATE3)
+    o = run_oracle(w, d)
+    errs, blk = _compare(g, o)
+    errs["LSE"] = float(np.max(np.abs(g["LSE"] - o["LSE"])))
+    say("  errors", {k: f"{v:.2e}" for k, v in errs.items()})
+    rep = invariant_report(g["rowstats"], min_row=1 if w.causal else 0)
+    say("  invariant", rep)
+    for k in ("O", "dQ", "dK", "dV"):
+        assert errs[k] <= REL_TOL, (k, errs[k])
+    check_blocks(blk)
+    assert errs["LSE"] < 1e-3 and rep["violations"] == 0
 
 
 def test_key_block_order_with_partial_cohort():
