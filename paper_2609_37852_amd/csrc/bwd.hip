@@ -71,19 +71,23 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
 // dQ = tau dS' K_col, query-major: a workgroup of 4 waves owns 128 queries
 // of one (batch, query head), wave w one 32-query block and all Dqk channels
 // (small workgroups: several per CU keep more unit loads in flight).
-// Per 64-key step up to the diagonal (over all keys without the mask): the A
-// operand is the stored unit (32
-// bytes per lane in operand order, as two 1 KB halves, prefetched into
-// registers one step ahead); the K col tile of the step [Dqk][64] and its
-// scales reach LDS by direct loads, double-buffered and shared by the 4
-// waves.  Keys past the sequence meet zero dS' codes (their K loads are
-// clamped to the sequence's last keys).
+// The keys are taken SB 64-key steps at a time between two barriers: per
+// 64-key step up to the diagonal (over all keys without the mask) the A
+// operand is the stored unit (32 bytes per lane in operand order, as two
+// 1 KB halves, loaded into registers during the previous interval); the K col
+// tile of the step [Dqk][64] and its scales reach LDS by direct loads,
+// double-buffered and shared by the 4 waves.  Every barrier waits for all
+// loads in flight, so the loads of a wave between two barriers are what
+// hides the memory latency: SB steps of them per interval.  Keys past the
+// sequence meet zero dS' codes (their K loads are clamped to the sequence's
+// last keys).
 template <int DQK>
 __global__ __launch_bounds__(256, DQK <= 128 ? 4 : 1) void dq_kernel(AttnArgs a) {
-  constexpr int CQ = DQK / 32, NW = 4;
+  constexpr int CQ = DQK / 32, NW = 4, SB = 2;
   constexpr int KT = DQK * 64, KSB = 2 * DQK;       // K tile and scale bytes per step
-  __shared__ __attribute__((aligned(16))) uint8_t kA[KT + KSB];
-  __shared__ __attribute__((aligned(16))) uint8_t kB[KT + KSB];
+  constexpr int KST = KT + KSB;
+  __shared__ __attribute__((aligned(16))) uint8_t kA[SB * KST];
+  __shared__ __attribute__((aligned(16))) uint8_t kB[SB * KST];
   const int lane = threadIdx.x & 63, w = wave_id(), hf = lane >> 5, li = lane & 31;
   const int N = (int)a.N, Nk = (int)a.Nk, nqb = N / 32;
   const bool causal = a.causal != 0;
@@ -109,52 +113,71 @@ __global__ __launch_bounds__(256, DQK <= 128 ? 4 : 1) void dq_kernel(AttnArgs a)
   const uint8_t* tk = a.tile_kcs + bk * nks * KSB;
 
   const Buf tkb = make_buf(tk, (uint32_t)nks * KSB);
-  auto issue = [&](lds8* dst, int ks) __attribute__((always_inline)) {
-    dma_cols<DQK, NW>(dst, kc, 64 * ks, Nk, L.k, w, lane);
-    constexpr int NI = (KSB + 255) / 256;
-    for (int k = 0; k < NI; k++) {
-      if ((NW - 1 - k) != w) continue;
-      const int off = 256 * k + 4 * lane;
-      if (off < KSB) dma4(tkb, (uint32_t)(ks * KSB + off), dst + KT + 256 * k);
+  // K col tiles and scales of steps ks0 .. ks0 + SB - 1 (those before nkw)
+  auto issue = [&](lds8* dst, int ks0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < SB; s++) {
+      const int ks = ks0 + s;
+      if (ks >= nkw) break;
+      dma_cols<DQK, NW>(dst + s * KST, kc, 64 * ks, Nk, L.k, w, lane);
+      constexpr int NI = (KSB + 255) / 256;
+      for (int k = 0; k < NI; k++) {
+        if ((NW - 1 - k) != w) continue;
+        const int off = 256 * k + 4 * lane;
+        if (off < KSB) dma4(tkb, (uint32_t)(ks * KSB + off), dst + s * KST + KT + 256 * k);
+      }
     }
   };
   struct Aop { uint4 lo, hi; uint32_t e; };
-  auto load_a = [&](Aop& op, int ks) __attribute__((always_inline)) {
-    ks = ks < nk ? ks : (nk > 0 ? nk - 1 : 0);     // past the wave's last step: reload it (unused)
-    // read once: streamed past the caches, which keep the K tiles
-    const v4i lo = __builtin_nontemporal_load(reinterpret_cast<const v4i*>(units + ks * 2048));
-    const v4i hi = __builtin_nontemporal_load(reinterpret_cast<const v4i*>(units + ks * 2048 + 1024));
-    op.lo = make_uint4((uint32_t)lo[0], (uint32_t)lo[1], (uint32_t)lo[2], (uint32_t)lo[3]);
-    op.hi = make_uint4((uint32_t)hi[0], (uint32_t)hi[1], (uint32_t)hi[2], (uint32_t)hi[3]);
-    op.e = ex[2 * ks + hf];
+  // the wave's units of steps ks0 .. ks0 + SB - 1 (those before nk)
+  auto load_a = [&](Aop (&op)[SB], int ks0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < SB; s++) {
+      const int ks = ks0 + s;
+      if (ks >= nk) break;
+      // read once: streamed past the caches, which keep the K tiles
+      const v4i lo = __builtin_nontemporal_load(reinterpret_cast<const v4i*>(units + ks * 2048));
+      const v4i hi = __builtin_nontemporal_load(reinterpret_cast<const v4i*>(units + ks * 2048 + 1024));
+      op[s].lo = make_uint4((uint32_t)lo[0], (uint32_t)lo[1], (uint32_t)lo[2], (uint32_t)lo[3]);
+      op[s].hi = make_uint4((uint32_t)hi[0], (uint32_t)hi[1], (uint32_t)hi[2], (uint32_t)hi[3]);
+      op[s].e = ex[2 * ks + hf];
+    }
   };
   v16f acc[CQ];
 #pragma unroll
   for (int i = 0; i < CQ; i++)
 #pragma unroll
     for (int r = 0; r < 16; r++) acc[i][r] = 0.f;
-  auto compute = [&](const uint8_t* kt, const Aop& op) __attribute__((always_inline)) {
-    const v8i af = v8i{(int)op.lo.x, (int)op.lo.y, (int)op.lo.z, (int)op.lo.w,
-                       (int)op.hi.x, (int)op.hi.y, (int)op.hi.z, (int)op.hi.w};
+  auto compute = [&](const uint8_t* kt0, const Aop (&op)[SB], int ks0) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < CQ; i++) {
-      const int ch = 32 * i + li;
-      acc[i] = mfma_mx(af, frag_cols_swz(kt, ch, hf), acc[i], (int)op.e, kt[KT + 2 * ch + hf]);
+    for (int s = 0; s < SB; s++) {
+      if (ks0 + s >= nk) break;
+      const uint8_t* kt = kt0 + s * KST;
+      const v8i af = v8i{(int)op[s].lo.x, (int)op[s].lo.y, (int)op[s].lo.z, (int)op[s].lo.w,
+                         (int)op[s].hi.x, (int)op[s].hi.y, (int)op[s].hi.z, (int)op[s].hi.w};
+#pragma unroll
+      for (int i = 0; i < CQ; i++) {
+        const int ch = 32 * i + li;
+        acc[i] = mfma_mx(af, frag_cols_swz(kt, ch, hf), acc[i], (int)op[s].e, kt[KT + 2 * ch + hf]);
+      }
     }
   };
-  Aop a0, a1;
-  if (qb < nqs) load_a(a0, 0);
+  // one register set: the units of the next interval are loaded after the
+  // MFMAs that read the current ones (the loads are in flight across the
+  // barrier wait, which the short MFMA work barely shortens)
+  Aop op[SB];
+  load_a(op, 0);
   issue((lds8*)kA, 0);
   lds_barrier();
-  for (int ks = 0; ks < nkw; ks += 2) {
-    if (ks + 1 < nkw) issue((lds8*)kB, ks + 1);
-    if (qb < nqs) load_a(a1, ks + 1);
-    if (ks < nk) compute(kA, a0);
+  for (int ks = 0; ks < nkw; ks += 2 * SB) {
+    if (ks + SB < nkw) issue((lds8*)kB, ks + SB);
+    compute(kA, op, ks);
+    load_a(op, ks + SB);
     lds_barrier();
-    if (ks + 1 >= nkw) break;
-    if (ks + 2 < nkw) issue((lds8*)kA, ks + 2);
-    if (qb < nqs) load_a(a0, ks + 2);
-    if (ks + 1 < nk) compute(kB, a1);
+    if (ks + SB >= nkw) break;
+    if (ks + 2 * SB < nkw) issue((lds8*)kA, ks + 2 * SB);
+    compute(kB, op, ks + SB);
+    load_a(op, ks + 2 * SB);
     lds_barrier();
   }
   if (qb >= nqs) return;
