@@ -1,8 +1,8 @@
 // Forward pass (Sec. 2.3; App. B.6.2 with power-of-two probability scales).
 //
 // Workgroup: NW waves, 32 queries each, one (batch, query head).  Key tiles of
-// BK = 128 keys (64 for wide heads; K row codes [BK][Dqk], V col codes
-// [Dv][BK], their scales) reach
+// BK = 128 keys (64 for wide heads without the mask; K row codes [BK][Dqk], V
+// col codes [Dv][BK], their scales) reach
 // LDS by direct loads, double-buffered: the next tile streams in while the
 // current one is computed, one barrier per tile.  Tiles run from key 0 up to
 // the causal diagonal (to the last key without the mask), so the workgroups
@@ -47,16 +47,24 @@ constexpr float kLog2_448 = 8.807354922057604f;
 constexpr float kLazyRescale = 16.0f;
 
 // NH: isolated score channels (1, or 3 with ATTN_FP8_FLAG_ISOLATE3)
-template <int DQK, int DV, int NH = 1>
+template <int DQK, int DV, int NH = 1, bool CAUSAL = true>
 struct FwdCfg {
   static constexpr int NW = 4, NT = 64 * NW, BQ = 32 * NW;
   static constexpr int al16(int x) { return (x + 15) & ~15; }
   static constexpr int stage_bytes(int bk) {
     return al16(al16(bk * (DQK + DV) + bk * DQK / 32) + DV * 4) + bk * 4 * NH;
   }
-  // 128-key tiles where two double-buffered workgroups fit a CU's LDS,
-  // else 64-key tiles (wide heads)
-  static constexpr int BK = 2 * stage_bytes(128) <= 80 * 1024 ? 128 : 64;
+  // Workgroups per CU.  At dv = 256 each wave holds 128 VGPRs of O
+  // accumulators: with two workgroups (two waves a SIMD, 256 VGPRs each) the
+  // causal kernel spilled inside its tile loop, and every spill reload waited
+  // for the tile loads in flight, so it runs one workgroup per CU (no spills,
+  // 128-key tiles: 0.53 against 0.61 ms on B = 2, N = 8192, 8 / 2 heads).
+  // Without the mask it spills less and two workgroups stay faster (0.82
+  // against 0.97 ms).
+  static constexpr int WGS = CAUSAL && DV > 128 ? 1 : 2;
+  // 128-key tiles where the double-buffered workgroups fit a CU's LDS (two
+  // in 80 KB each, or one), else 64-key tiles (wide heads)
+  static constexpr int BK = WGS == 1 || 2 * stage_bytes(128) <= 80 * 1024 ? 128 : 64;
   static constexpr int K_OFF = 0;                               // K row codes [BK][DQK], swizzled
   static constexpr int V_OFF = K_OFF + BK * DQK;                // V col codes [DV][BK], swizzled
   static constexpr int KS_OFF = V_OFF + DV * BK;                // K row scales [BK][DQK/32]
@@ -66,6 +74,7 @@ struct FwdCfg {
   static_assert(STAGE == stage_bytes(BK), "stage layout");
   static_assert(DV <= NT, "one V scale word per thread");
   static_assert(BQ % BK == 0, "a query block's diagonal starts a key tile");
+  static_assert(WGS * 2 * STAGE <= 160 * 1024, "LDS of the forward");
 };
 
 // CAUSAL: the mask (key length = query length) or every key of Nk; a
@@ -73,8 +82,8 @@ struct FwdCfg {
 // NH: isolated score channels; with 3, the first two share one rank-2 FP32
 // MFMA (its two k slots) and the third takes a second one.
 template <int DQK, int DV, bool CAUSAL, int NH = 1>
-__global__ __launch_bounds__(256, 2) void fwd_kernel(AttnArgs a) {
-  using C = FwdCfg<DQK, DV, NH>;
+__global__ __launch_bounds__(256, (FwdCfg<DQK, DV, NH, CAUSAL>::WGS)) void fwd_kernel(AttnArgs a) {
+  using C = FwdCfg<DQK, DV, NH, CAUSAL>;
   constexpr int NW = C::NW, BQ = C::BQ, BK = C::BK;
   constexpr int KS = DQK / 64, CB = DV / 32;
   __shared__ __attribute__((aligned(16))) uint8_t stA[C::STAGE];
