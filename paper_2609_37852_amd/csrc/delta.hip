@@ -12,15 +12,15 @@
 // carries no FP32 rounding of the terms it cancels.
 //
 // Workgroup: NW waves x 32 queries of one (batch, query head); 128-key tiles
-// of K and V (row copies) reach LDS by direct loads, double-buffered, so the
-// next tile streams in while the current one is computed.  S^T and dP^T put
-// one query in each lane (row reductions in-lane plus one exchange with lane
-// l ^ 32).  The isolated score channel (if any) is zeroed in the Q operand;
-// its product and the shift -LSE / tau are added to the scores by one FP32
-// rank-2 MFMA.  P and dP use exactly the operations of the backward kernel
-// (same MX MFMA products and k order, the same rank-2 update, bwd_prob()),
-// so the backward's dS = P (dP - delta) sums to zero over every row up to
-// FP32 rounding of its own terms.  Only the 32-key group holding the
+// (64 at wide heads) of K and V (row copies) reach LDS by direct loads,
+// double-buffered, so the next tile streams in while the current one is
+// computed.  S^T and dP^T put one query in each lane (row reductions in-lane
+// plus one exchange with lane l ^ 32).  The isolated score channel (if any)
+// is zeroed in the Q operand; its product and the shift -LSE / tau are added
+// to the scores by one FP32 rank-2 MFMA.  P and dP use exactly the
+// operations of the backward kernel (same MX MFMA products and k order, the
+// same rank-2 update, bwd_prob()), so the backward's dS = P (dP - delta) sums
+// to zero over every row up to FP32 rounding of its own terms.  Only the 32-key group holding the
 // diagonal is masked; groups in a wave's future (causal) or past the last key
 // are skipped.
 #include <type_traits>
@@ -32,9 +32,15 @@
 
 namespace afp8 {
 
-template <int DQK, int DV, int NH = 1>
+template <int DQK, int DV, int NH = 1, bool CAUSAL = true>
 struct DeltaCfg {
-  static constexpr int NW = 4, NT = 64 * NW, BQ = 32 * NW, BK = 128;
+  // Wide heads (dqk + dv > 256) take 64-key tiles, so that two
+  // double-buffered workgroups fit a CU (with 128-key tiles one did, a single
+  // wave per SIMD, 15 % slower on the d = 256 and 192 / 128 problems); dv =
+  // 256 without the mask keeps 128-key tiles and one workgroup, since two do
+  // not fit its registers (they spilled, 3x slower).
+  static constexpr bool WIDE = DQK + DV > 256;
+  static constexpr int NW = 4, NT = 64 * NW, BQ = 32 * NW, BK = WIDE && (CAUSAL || DV <= 128) ? 64 : 128;
   static constexpr int al16(int x) { return (x + 15) & ~15; }
   static constexpr int K_OFF = 0;                               // K row codes [BK][DQK], swizzled
   static constexpr int V_OFF = K_OFF + BK * DQK;                // V row codes [BK][DV], swizzled
@@ -50,8 +56,8 @@ struct DeltaCfg {
 // FP64 products and sums; NH: isolated score channels (with 3, channels 1
 // and 2 take a second rank-2 FP32 MFMA, the first shares one with the shift)
 template <int DQK, int DV, bool CAUSAL, bool COMP, int NH = 1>
-__global__ __launch_bounds__(256, (DeltaCfg<DQK, DV, NH>::WGS)) void delta_matching_kernel(AttnArgs a) {
-  using C = DeltaCfg<DQK, DV, NH>;
+__global__ __launch_bounds__(256, (DeltaCfg<DQK, DV, NH, CAUSAL>::WGS)) void delta_matching_kernel(AttnArgs a) {
+  using C = DeltaCfg<DQK, DV, NH, CAUSAL>;
   constexpr int NW = C::NW, BQ = C::BQ, BK = C::BK;
   constexpr int KS = DQK / 64, VS = DV / 64;
   __shared__ __attribute__((aligned(16))) uint8_t stA[C::STAGE];
