@@ -17,53 +17,133 @@ namespace afp8 {
 //           ([channel][group]), the second clamped to the first past the end;
 //   tile_kcs [B, Hkv, ceil(Nk/64)] x 2 Dqk B: the same for K per 64-key step
 //           (dq_kernel).
-// Workgroup x covers queries and keys 64 x .. 64 x + 63 (either may lie past
-// its sequence; "the end" is the sequence's own length, the layouts have N
-// and Nk rows).
+// Workgroup x covers the PT = 4 tiles of queries and keys 64 PT x ..
+// 64 PT x + 64 PT - 1 (any may lie past its sequence; "the end" is the
+// sequence's own length, the layouts have N and Nk rows): one isolated-channel
+// choice per workgroup, and every load of a part issued before its stores.
+constexpr int kPrepTiles = 4;
 template <int DQK, int DV>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
+  constexpr int PT = kPrepTiles;
+  static_assert(PT * 64 == 256, "one query per thread");
   __shared__ int hot_slot;
   const int N = (int)a.N, Nk = (int)a.Nk;
   const int h = blockIdx.y, b = blockIdx.z, kh = h / (int)a.G;
   const SeqLens L = a.causal ? seq_lens<true>(a, b, N, Nk) : seq_lens<false>(a, b, N, Nk);
-  const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
   const size_t bh = (size_t)b * a.Hq + h;
-  const int i0 = blockIdx.x * 64;
-  if (i0 < N && threadIdx.x < 64) {
-    uint8_t* blk = reinterpret_cast<uint8_t*>(a.rows) + (bh * ((N + 63) / 64) + blockIdx.x) * 1024;
-    float2 pr = make_float2(0.f, 0.f);
-    float nd = 0.f, ndl = 0.f;
-    if (i0 + (int)threadIdx.x < L.q) {
-      const size_t row = bh * N + i0 + threadIdx.x;
-      const float2 d = *reinterpret_cast<const float2*>(a.delta + row * 2);
-      const float qh = hot >= 0 ? row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot) : 0.f;
-      pr = make_float2(qh, neg_lse_over_tau(a.lse[row], a.tau));
-      nd = -d.x;
-      ndl = -d.y;
-    }
-    reinterpret_cast<float2*>(blk)[threadIdx.x] = pr;
-    reinterpret_cast<float*>(blk + 512)[threadIdx.x] = nd;
-    reinterpret_cast<float*>(blk + 768)[threadIdx.x] = ndl;
+  const int x0 = blockIdx.x * PT, t = threadIdx.x;
+  const int nq = (N + 63) / 64, nk = (Nk + 63) / 64;
+  // every load that does not depend on the isolated channel is issued before
+  // its choice (which ends in a barrier)
+  // records: thread t holds query t % 64 of tile x0 + t / 64
+  const int xr = x0 + t / 64, r = t % 64, i = 64 * xr + r;
+  const bool rec = xr < nq, inseq = rec && i < L.q;
+  const size_t row = bh * N + (inseq ? i : 0);
+  float2 d = make_float2(0.f, 0.f);
+  float lse = 0.f;
+  if (inseq) {
+    d = *reinterpret_cast<const float2*>(a.delta + row * 2);
+    lse = a.lse[row];
   }
-  if (i0 < L.q) {
-    const int g0 = i0 / 32, g1 = (i0 + 32 < L.q ? i0 + 32 : i0) / 32;
-    uint8_t* dst = a.tile_cs + (bh * ((N + 63) / 64) + blockIdx.x) * (2 * (DQK + DV));
-    for (int u = threadIdx.x; u < DQK + DV; u += 256) {
-      const uint8_t* src = u < DQK ? a.qc_scale + (bh * DQK + u) * (N / 32)
-                                   : a.doc_scale + (bh * DV + (u - DQK)) * (N / 32);
-      dst[2 * u] = src[g0];
-      dst[2 * u + 1] = src[g1];
+  // col scales of Q and dO for the tiles' two 32-query groups: where all PT
+  // tiles lie inside the sequence, one 8-byte load per channel (its 2 PT
+  // consecutive groups), else one byte at a time
+  constexpr int NU = (DQK + DV + 255) / 256;
+  uint8_t v[NU][PT][2];
+  const bool whole = 64 * (x0 + PT) <= L.q && (N / 32) % (2 * PT) == 0;
+#pragma unroll
+  for (int k = 0; k < NU; k++) {
+    const int u = t + 256 * k;
+    if (u >= DQK + DV) continue;
+    const uint8_t* src = u < DQK ? a.qc_scale + (bh * DQK + u) * (N / 32)
+                                 : a.doc_scale + (bh * DV + (u - DQK)) * (N / 32);
+    if (whole) {
+      const uint2 w = *reinterpret_cast<const uint2*>(src + 2 * x0);
+#pragma unroll
+      for (int j = 0; j < PT; j++) {
+        const uint32_t q = j < 2 ? w.x : w.y;
+        v[k][j][0] = (uint8_t)(q >> (16 * (j & 1)));
+        v[k][j][1] = (uint8_t)(q >> (16 * (j & 1) + 8));
+      }
+      continue;
+    }
+#pragma unroll
+    for (int j = 0; j < PT; j++) {
+      const int i0 = 64 * (x0 + j);
+      if (i0 < L.q) {
+        const int g0 = i0 / 32, g1 = (i0 + 32 < L.q ? i0 + 32 : i0) / 32;
+        v[k][j][0] = src[g0];
+        v[k][j][1] = src[g1];
+      }
     }
   }
-  // the K col scales of keys i0 .., once per KV head (for dq_kernel)
-  if (h < a.Hkv && i0 < L.k) {
-    const int g0 = i0 / 32, g1 = (i0 + 32 < L.k ? i0 + 32 : i0) / 32;
-    const size_t bk = (size_t)b * a.Hkv + h;
-    uint8_t* dk = a.tile_kcs + (bk * ((Nk + 63) / 64) + blockIdx.x) * (2 * DQK);
-    for (int u = threadIdx.x; u < DQK; u += 256) {
+  // the K col scales of keys 64 (x0 + j) .., once per KV head (for dq_kernel)
+  constexpr int NK = (DQK + 255) / 256;
+  uint8_t kv[NK][PT][2];
+  const size_t bk = (size_t)b * a.Hkv + (h < a.Hkv ? h : 0);
+  if (h < a.Hkv) {
+    const bool kwhole = 64 * (x0 + PT) <= L.k && (Nk / 32) % (2 * PT) == 0;
+#pragma unroll
+    for (int k = 0; k < NK; k++) {
+      const int u = t + 256 * k;
+      if (u >= DQK) continue;
       const uint8_t* src = a.kc_scale + (bk * DQK + u) * (Nk / 32);
-      dk[2 * u] = src[g0];
-      dk[2 * u + 1] = src[g1];
+      if (kwhole) {
+        const uint2 w = *reinterpret_cast<const uint2*>(src + 2 * x0);
+#pragma unroll
+        for (int j = 0; j < PT; j++) {
+          const uint32_t q = j < 2 ? w.x : w.y;
+          kv[k][j][0] = (uint8_t)(q >> (16 * (j & 1)));
+          kv[k][j][1] = (uint8_t)(q >> (16 * (j & 1) + 8));
+        }
+        continue;
+      }
+#pragma unroll
+      for (int j = 0; j < PT; j++) {
+        const int i0 = 64 * (x0 + j);
+        if (i0 < L.k) {
+          const int g0 = i0 / 32, g1 = (i0 + 32 < L.k ? i0 + 32 : i0) / 32;
+          kv[k][j][0] = src[g0];
+          kv[k][j][1] = src[g1];
+        }
+      }
+    }
+  }
+
+  const int hot = select_hot_channel<DQK>(a.q_amax, a.k_amax, b, kh, a.Hq, a.Hkv, a.G, &hot_slot);
+  if (rec) {
+    uint8_t* blk = reinterpret_cast<uint8_t*>(a.rows) + (bh * nq + xr) * 1024;
+    float2 pr = make_float2(0.f, 0.f);
+    if (inseq) {
+      const float qh = hot >= 0 ? row_value<DQK>(a.q_code, a.q_scale, (int64_t)row, hot) : 0.f;
+      pr = make_float2(qh, neg_lse_over_tau(lse, a.tau));
+    }
+    reinterpret_cast<float2*>(blk)[r] = pr;
+    reinterpret_cast<float*>(blk + 512)[r] = inseq ? -d.x : 0.f;
+    reinterpret_cast<float*>(blk + 768)[r] = inseq ? -d.y : 0.f;
+  }
+#pragma unroll
+  for (int k = 0; k < NU; k++) {
+    const int u = t + 256 * k;
+#pragma unroll
+    for (int j = 0; j < PT; j++) {
+      if (u < DQK + DV && 64 * (x0 + j) < L.q) {
+        uint8_t* dst = a.tile_cs + (bh * nq + x0 + j) * (2 * (DQK + DV));
+        *reinterpret_cast<uint16_t*>(dst + 2 * u) = (uint16_t)(v[k][j][0] | (v[k][j][1] << 8));
+      }
+    }
+  }
+  if (h < a.Hkv) {
+#pragma unroll
+    for (int k = 0; k < NK; k++) {
+      const int u = t + 256 * k;
+#pragma unroll
+      for (int j = 0; j < PT; j++) {
+        if (u < DQK && 64 * (x0 + j) < L.k) {
+          uint8_t* dk = a.tile_kcs + (bk * nk + x0 + j) * (2 * DQK);
+          *reinterpret_cast<uint16_t*>(dk + 2 * u) = (uint16_t)(kv[k][j][0] | (kv[k][j][1] << 8));
+        }
+      }
     }
   }
 }
@@ -293,7 +373,7 @@ static hipError_t bwd_dispatch(const AttnArgs& a0, hipStream_t s) {
 
 hipError_t launch_bwd_prep(const AttnArgs& a, int dqk, int dv, hipStream_t s) {
   const int64_t L = a.N > a.Nk ? a.N : a.Nk;
-  const dim3 grid((unsigned)((L + 63) / 64), (unsigned)a.Hq, (unsigned)a.B);
+  const dim3 grid((unsigned)(((L + 63) / 64 + kPrepTiles - 1) / kPrepTiles), (unsigned)a.Hq, (unsigned)a.B);
   if (dqk == 64 && dv == 64) hipLaunchKernelGGL((bwd_prep_kernel<64, 64>), grid, dim3(256), 0, s, a);
   else if (dqk == 128 && dv == 128) hipLaunchKernelGGL((bwd_prep_kernel<128, 128>), grid, dim3(256), 0, s, a);
   else if (dqk == 256 && dv == 256) hipLaunchKernelGGL((bwd_prep_kernel<256, 256>), grid, dim3(256), 0, s, a);
