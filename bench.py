@@ -457,6 +457,10 @@ def main():
                     help="summary with the measured HBM bytes of the bwd kernel (used while its sources match)")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the traffic summary from two rocprofv3 --pmc counter CSVs and exit")
+    ap.add_argument("--more-configs", action="store_true",
+                    help="also time the MLA d = 192/128 4K and the 64K long-context workloads (whole step, "
+                         "matched and stale, and the matched per-kernel split; their inputs take about a "
+                         "minute to generate on the host)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the timed steps, copy MIB MiB device-to-device once (a plain copy kernel whose "
                          "FETCH_SIZE / WRITE_SIZE calibrate the HBM counters)")
@@ -592,6 +596,24 @@ def main():
                                  "stale_step": r3.full_step(pk.DELTA_STALE_ROWSUM),
                                  "paper_protocol": r3.protocol(0.0)}
             run = r3
+    if args.more_configs:
+        # the other throughput shapes of the workload table, measured as C2 is
+        del run
+        torch.cuda.empty_cache()
+        more = {}
+        for name in ("mla_d192_4k", "gqa_d128_64k_nope"):
+            wm = synth.WORKLOADS[name]
+            rm = Runner(wm, ev)
+            for _ in range(3):
+                rm.step()
+            torch.cuda.synchronize()
+            more[name] = {"matched_step": rm.full_step(pk.DELTA_MATCHING),
+                          "stale_step": rm.full_step(pk.DELTA_STALE_ROWSUM),
+                          "matched_split": rm.breakdown(pk.DELTA_MATCHING, n=5)}
+            del rm
+            torch.cuda.empty_cache()
+        line["more_configs"] = more
+        run = None
     if args.copy_calibration > 0:
         # a plain streaming kernel of known size: n bytes read, n written
         n = args.copy_calibration << 20
