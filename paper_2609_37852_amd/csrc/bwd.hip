@@ -19,8 +19,9 @@ namespace afp8 {
 //           (dq_kernel).
 // Workgroup x covers the PT = 4 tiles of queries and keys 64 PT x ..
 // 64 PT x + 64 PT - 1 (any may lie past its sequence; "the end" is the
-// sequence's own length, the layouts have N and Nk rows): one isolated-channel
-// choice per workgroup, and every load of a part issued before its stores.
+// sequence's own length, the layouts have N and Nk rows), with one
+// isolated-channel choice per workgroup, made once every load that does not
+// depend on it is in flight.
 constexpr int kPrepTiles = 4;
 template <int DQK, int DV>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(AttnArgs a) {
