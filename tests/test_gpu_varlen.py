@@ -53,7 +53,7 @@ def _full(shape, dtype):
     return torch.full(shape, SENTINEL, dtype=dtype, device="cuda")
 
 
-def _run(w, d, lq, lk, mode=pk.DELTA_MATCHING, delta_in=None):
+def _run(w, d, lq, lk, mode=pk.DELTA_MATCHING, delta_in=None, flags=0):
     """The path on the padded batch; outputs pre-filled with SENTINEL."""
     B, N, Nk = w.B, w.N, w.nk
     q, do = (to_dev(_padded(d[n], lq), w.dtype) for n in ("q", "do"))
@@ -61,7 +61,7 @@ def _run(w, d, lq, lk, mode=pk.DELTA_MATCHING, delta_in=None):
     mq, mk, mv, mdo = (pk.attn_fp8_quantize(t) for t in (q, k, v, do))
     p = pk.Problem(B, N, w.Hq, w.Hkv, w.Dqk, w.Dv, float(np.float32(w.tau)), causal=int(w.causal), seqlen_kv=w.Nk,
                    seqlens_q=torch.tensor(lq, dtype=torch.int32, device="cuda"),
-                   seqlens_kv=None if w.causal else torch.tensor(lk, dtype=torch.int32, device="cuda"))
+                   seqlens_kv=None if w.causal else torch.tensor(lk, dtype=torch.int32, device="cuda"), flags=flags)
     o, lse = pk.attn_fp8_fwd(p, mq, mk, mv, o=_full((B, N, w.Hq, w.Dv), torch.bfloat16),
                              lse=_full((B, w.Hq, N), torch.float32))
     delta = pk.attn_fp8_delta(p, mode, mq, mk, mv, mdo, lse, do, o, delta=_full((B, w.Hq, N, 2), torch.float32))
@@ -79,13 +79,14 @@ def _run(w, d, lq, lk, mode=pk.DELTA_MATCHING, delta_in=None):
     return dict(O=f(o), LSE=f(lse), delta=f(delta), dQ=f(dq), dK=f(dk), dV=f(dv), rowstats=rs.cpu().numpy())
 
 
-def _alone(w, d, b, nq, nk):
+def _alone(w, d, b, nq, nk, flags=0):
     """The same kernels on sequence b alone (B = 1, its own lengths)."""
     w1 = synth.with_shape(w, B=1, N=nq, Nk=0 if w.causal else nk)
     q, do = (to_dev(d[n][b:b + 1, :nq], w.dtype) for n in ("q", "do"))
     k, v = (to_dev(d[n][b:b + 1, :nk], w.dtype) for n in ("k", "v"))
     mq, mk, mv, mdo = (pk.attn_fp8_quantize(t) for t in (q, k, v, do))
-    p = pk.Problem(1, nq, w.Hq, w.Hkv, w.Dqk, w.Dv, float(np.float32(w.tau)), causal=int(w.causal), seqlen_kv=w1.Nk)
+    p = pk.Problem(1, nq, w.Hq, w.Hkv, w.Dqk, w.Dv, float(np.float32(w.tau)), causal=int(w.causal), seqlen_kv=w1.Nk,
+                   flags=flags)
     o, lse = pk.attn_fp8_fwd(p, mq, mk, mv)
     delta = pk.attn_fp8_delta(p, pk.DELTA_MATCHING, mq, mk, mv, mdo, lse, do, o)
     dq, _, _, _ = pk.attn_fp8_bwd(p, pk.DELTA_MATCHING, mq, mk, mv, mdo, lse, do, o, grad_dtype=torch.float32)
@@ -96,10 +97,24 @@ def _alone(w, d, b, nq, nk):
 
 @pytest.mark.parametrize("name,kw,lq,lk", CASES, ids=_ids())
 def test_varlen_parity(name, kw, lq, lk):
+    _check(name, kw, lq, lk, 0)
+
+
+def test_varlen_isolate3():
+    """Three isolated score channels (ATTN_FP8_FLAG_ISOLATE3) on a padded
+    batch: the channels are chosen per (sequence, KV head) from maxima that
+    the NaN padding does not reach, so every sequence meets the same checks
+    as in the default mode, against the oracle and against the sequence run
+    alone with the same flag."""
+    name, kw, lq, lk = CASES[0]
+    _check(name, kw, lq, lk, pk.FLAG_ISOLATE3)
+
+
+def _check(name, kw, lq, lk, flags):
     w = synth.with_shape(synth.WORKLOADS[name], **kw)
-    say(f"varlen parity {w} lens_q={lq} lens_kv={lk}")
+    say(f"varlen parity {w} lens_q={lq} lens_kv={lk} flags={flags}")
     d = synth.generate(w, seed=11)
-    g = _run(w, d, lq, lk)
+    g = _run(w, d, lq, lk, flags=flags)
     for b, (nq, nk) in enumerate(_eff(lq, lk, w.causal)):
         # padding rows untouched
         assert np.all(g["O"][b, nq:] == SENTINEL) and np.all(g["LSE"][b, :, nq:] == SENTINEL), b
@@ -127,7 +142,7 @@ def test_varlen_parity(name, kw, lq, lk):
         assert errs["LSE"] < 1e-3 and errs["delta"] < 1e-3, (b, errs)
         assert rep["violations"] == 0, (b, rep)
         # the query-major results equal those of the sequence run alone
-        a = _alone(w, d, b, nq, nk)
+        a = _alone(w, d, b, nq, nk, flags)
         assert np.array_equal(g["O"][b:b + 1, :nq], a["O"]), b
         assert np.array_equal(g["LSE"][b:b + 1, :, :nq], a["LSE"]), b
         assert np.array_equal(g["delta"][b:b + 1, :, :nq], a["delta"]), b
