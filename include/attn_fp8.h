@@ -216,7 +216,11 @@ int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t 
  * each rounded once to FP32 (no fused multiply-add).  The mean is the FP64
  * sum of FP64 sums over aligned 32-token blocks (tokens ascending, blocks
  * ascending), divided by N in FP64 and rounded to FP32, so it does not depend
- * on scheduling.
+ * on scheduling.  With seqlens (a padded batch, as in attn_fp8_problem) the
+ * mean of batch entry b runs over its first L_b tokens only, L_b =
+ * seqlens[b] clamped into [0, N] and rounded down to a multiple of 32 (the
+ * length the attention kernels take), and is 0 where L_b = 0; every row is
+ * still transformed and quantized (the padding's codes are never read).
  *   prescale      finite, nonzero (1 for none)
  *   center        0 or 1
  *   channel_mean  device float [B, H, D], written when center (else unused)
@@ -228,7 +232,10 @@ int attn_fp8_quantize(const void* x, int x_dtype, int64_t B, int64_t N, int64_t 
  *                 frequencies are the caller's), 16-byte aligned; read when
  *                 rope_dim > 0
  *   rope_lo, rope_dim  multiples of 32 with rope_lo + rope_dim <= D
- *                 (EUNSUPPORTED otherwise); rope_dim 0 for no rotation */
+ *                 (EUNSUPPORTED otherwise); rope_dim 0 for no rotation
+ *   seqlens       nullable device int32 [B], 4-byte aligned: the sequence
+ *                 length of each batch entry for the key mean (read when
+ *                 center) */
 typedef struct attn_fp8_producer {
   float prescale;
   int32_t center;
@@ -238,6 +245,7 @@ typedef struct attn_fp8_producer {
   const float* rope_cs;
   int64_t rope_lo;
   int64_t rope_dim;
+  const int32_t* seqlens;
 } attn_fp8_producer;
 
 /* Workspace bytes attn_fp8_quantize_producer needs with these options: the

@@ -46,7 +46,7 @@ class _Problem(ctypes.Structure):
 class _Producer(ctypes.Structure):
     _fields_ = [("prescale", ctypes.c_float), ("center", ctypes.c_int32), ("channel_mean", ctypes.c_void_p),
                 ("rms_gain", ctypes.c_void_p), ("rms_eps", ctypes.c_float), ("rope_cs", ctypes.c_void_p),
-                ("rope_lo", ctypes.c_int64), ("rope_dim", ctypes.c_int64)]
+                ("rope_lo", ctypes.c_int64), ("rope_dim", ctypes.c_int64), ("seqlens", ctypes.c_void_p)]
 
 
 class _MX(ctypes.Structure):
@@ -195,13 +195,15 @@ def attn_fp8_quantize(x: torch.Tensor, which: int = QUANT_BOTH, nonfinite: torch
 def attn_fp8_quantize_producer(x: torch.Tensor, prescale: float = 1.0, center: bool = False,
                                which: int = QUANT_BOTH, nonfinite: torch.Tensor | None = None, amax: bool = True,
                                rope: torch.Tensor | None = None, rope_lo: int = 0,
-                               rms_gain: torch.Tensor | None = None, rms_eps: float = 1e-6):
+                               rms_gain: torch.Tensor | None = None, rms_eps: float = 1e-6,
+                               seqlens: torch.Tensor | None = None):
     """The input producer (App. B.6.1) then the quantizer: x [B, N, H, D] ->
     (MX copies of fl32(fl32(r prescale) - mean), mean [B, H, D] or None).  r
     is x, RMS-normalized with the gain rms_gain [D] (float32 on the device)
     when given, with channels rope_lo .. rope_lo + R - 1 then rotated by the
     table rope [N, R/2, 2] (float32 cos, sin on the device); normalized and
-    rotated values are rounded to bf16."""
+    rotated values are rounded to bf16.  seqlens (int32 [B] on the device):
+    each batch entry's sequence length for the key mean."""
     B, N, H, D = x.shape
     rope_dim = 0
     if rope is not None:
@@ -213,8 +215,10 @@ def attn_fp8_quantize_producer(x: torch.Tensor, prescale: float = 1.0, center: b
         rms_gain = rms_gain.contiguous()
     out = MX.empty(B, N, H, D, x.device, which, amax=amax)
     mean = torch.empty((B, H, D), dtype=torch.float32, device=x.device) if center else None
+    if seqlens is not None:
+        assert seqlens.dtype == torch.int32 and seqlens.shape == (B,)
     opt = _Producer(float(prescale), int(bool(center)), _ptr(mean).value, _ptr(rms_gain).value, float(rms_eps),
-                    _ptr(rope).value, int(rope_lo), int(rope_dim))
+                    _ptr(rope).value, int(rope_lo), int(rope_dim), _ptr(seqlens).value)
     need = ctypes.c_size_t(0)
     _check("attn_fp8_producer_workspace_size",
            lib().attn_fp8_producer_workspace_size(B, N, H, D, ctypes.byref(opt), ctypes.byref(need)))

@@ -344,6 +344,8 @@ int check_producer(int64_t D, const attn_fp8_producer* o) {
                   (long long)o->rope_lo, (long long)(o->rope_lo + o->rope_dim), (long long)D);
     if ((rc = check_ptr("rope_cs", o->rope_cs))) return rc;
   }
+  if (o->seqlens && (reinterpret_cast<uintptr_t>(o->seqlens) & 3u))
+    return fail(ATTN_FP8_EALIGN, "producer seqlens not 4-byte aligned");
   return ATTN_FP8_OK;
 }
 
@@ -399,6 +401,7 @@ int quantize_impl(const void* x, int x_dtype, int64_t B, int64_t N, int64_t H, i
     if (opt->center) {
       a.mean = opt->channel_mean;
       a.partials = reinterpret_cast<double*>(ws);
+      a.lens = opt->seqlens;
     }
     if (opt->rms_gain) {
       a.gain = opt->rms_gain;

@@ -28,6 +28,7 @@ struct QuantArgs {
   float prescale;            // 1 for none
   float* mean;               // nullable [B, H, D]
   double* partials;          // required with mean
+  const int32_t* lens;       // nullable [B]: each sequence's length for the mean
   // fused rotary embedding before the prescale (nullable): channels
   // rope_lo .. rope_lo + rope_dim - 1 rotated in pairs (c, c + rope_dim/2)
   // by rope[n][c][{cos, sin}] ([N, rope_dim/2, 2] FP32) and rounded to BF16

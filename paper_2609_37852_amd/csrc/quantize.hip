@@ -302,11 +302,25 @@ __device__ __forceinline__ float2 load2(const T* p) {
 // of a thread are both rotary or both not, and both first or both second of
 // their pairs (the rotary range is 32-aligned), so their partners are
 // consecutive as well.
+// With sequence lengths, the mean's tokens of batch entry b: its first L_b
+// (clamped into [0, N], rounded down to a multiple of 32, as the attention
+// kernels take it).
+__device__ __forceinline__ int64_t mean_tokens(const QuantArgs& a, int64_t b) {
+  if (!a.lens) return a.N;
+  const int64_t v = a.lens[b];
+  return (v < 0 ? 0 : v > a.N ? a.N : v) & ~int64_t(31);
+}
+
 template <typename T>
 __global__ __launch_bounds__(128) void producer_partials_kernel(QuantArgs a, int D) {
   const int c = 2 * (int)threadIdx.x;
   if (c >= D) return;
   const int64_t t = blockIdx.x, h = blockIdx.y, b = blockIdx.z, nblk = a.N / 32;
+  if (32 * t >= mean_tokens(a, b)) {
+    // a block past the sequence adds nothing to its mean
+    *reinterpret_cast<double2*>(a.partials + ((b * a.H + h) * nblk + t) * D + c) = make_double2(0.0, 0.0);
+    return;
+  }
   const T* src = reinterpret_cast<const T*>(a.x) + b * a.sb + h * a.sh + c;
   const int h2 = a.rope_dim >> 1, rel = c - a.rope_lo;
   const bool rot = a.rope && rel >= 0 && rel < a.rope_dim, first = rel < h2;
@@ -392,16 +406,17 @@ __global__ __launch_bounds__(256) void producer_rscale_kernel(QuantArgs a, int D
 }
 
 // The key mean: FP64 sum of the block partial sums in block order (coalesced
-// over the channels), divided by N in FP64, rounded once to FP32.
+// over the channels), divided by the token count (N, or the sequence's
+// length) in FP64, rounded once to FP32; 0 for a sequence without tokens.
 __global__ __launch_bounds__(256) void producer_mean_kernel(QuantArgs a, int D) {
   const int c = threadIdx.x;
   if (c >= D) return;
-  const int64_t h = blockIdx.x, b = blockIdx.y, nblk = a.N / 32;
+  const int64_t h = blockIdx.x, b = blockIdx.y, nblk = a.N / 32, n = mean_tokens(a, b);
   const double* p = a.partials + (b * a.H + h) * nblk * D + c;
   double total = 0.0;
 #pragma unroll 8
-  for (int64_t t = 0; t < nblk; t++) total += p[t * D];
-  a.mean[(b * a.H + h) * D + c] = (float)(total / (double)a.N);
+  for (int64_t t = 0; t < n / 32; t++) total += p[t * D];
+  a.mean[(b * a.H + h) * D + c] = n > 0 ? (float)(total / (double)n) : 0.f;
 }
 
 hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_t s) {

@@ -146,7 +146,7 @@ def test_noalloc_rejects_oversized_problem_on_the_host():
 
 def _opt(**kw):
     d = dict(prescale=1.0, center=0, channel_mean=None, rms_gain=None, rms_eps=1e-6, rope_cs=None, rope_lo=0,
-             rope_dim=0)
+             rope_dim=0, seqlens=None)
     d.update(kw)
     return bd._Producer(**d)
 
@@ -182,6 +182,8 @@ def test_producer_rejects_bad_arguments():
         rc = call(_opt(rope_cs=vp, rope_lo=lo, rope_dim=R))
         assert rc == code, (lo, R, rc, pk.last_error())
     assert call(_opt(rope_dim=32)) == -1
+    # the key mean's sequence lengths: int32 alignment
+    assert call(_opt(center=1, channel_mean=vp, seqlens=4098)) == -3
 
 
 def test_producer_workspace_size():

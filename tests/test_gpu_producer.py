@@ -202,3 +202,40 @@ def test_qknorm_producer_path_matches_oracle():
         assert errs[n] <= REL_TOL, (n, errs[n])
     check_blocks(blk)
     assert rep["violations"] == 0
+
+
+@pytest.mark.parametrize("D,lo,R", [(128, 0, 0), (192, 128, 64)])
+def test_producer_varlen_mean(D, lo, R):
+    """A padded batch (NaN in every padding row) with per-sequence lengths
+    for the key mean: each sequence's codes, scales, channel maxima and mean
+    bit for bit those of the oracle producer run on that sequence's rows
+    alone (QK normalization, rotary embedding where given, prescale and
+    centering); a sequence without tokens gets a zero mean."""
+    B, N, H = 3, 160, 2
+    lens = [160, 64, 0]
+    x = _keys(B, N, H, D, seed=7, dtype="bf16")
+    for b, L in enumerate(lens):
+        x[b, L:] = np.nan
+    rng = np.random.default_rng(8)
+    gain = rng.uniform(0.5, 2.0, D).astype(np.float32)
+    rope = synth.rope_table(N, R, 10000.0) if R else None
+    g, mean = pk.attn_fp8_quantize_producer(
+        torch.from_numpy(x).cuda().to(torch.bfloat16), 0.3, True, rms_gain=torch.from_numpy(gain).cuda(),
+        rope=torch.from_numpy(rope).cuda() if R else None, rope_lo=lo,
+        seqlens=torch.tensor(lens, dtype=torch.int32, device="cuda"))
+    torch.cuda.synchronize()
+    got = {f: getattr(g, f).cpu().numpy() for f in ("code_row", "scale_row", "code_col", "scale_col")}
+    amax, mean = g.channel_amax.cpu().numpy(), mean.cpu().numpy().astype(np.float64)
+    for b, L in enumerate(lens):
+        if L == 0:
+            assert np.all(mean[b] == 0.0)
+            continue
+        y, m = orc.producer_ext(x[b:b + 1, :L], gain=gain, eps=1e-6, rope=rope[:L] if R else None, lo=lo, R=R,
+                                prescale=0.3, center=True)
+        ref = orc.quantize(y)
+        assert np.array_equal(mean[b:b + 1], m), b
+        assert np.array_equal(got["code_row"][b:b + 1, :, :L], ref["code_row"]), b
+        assert np.array_equal(got["scale_row"][b:b + 1, :, :L], ref["scale_row"]), b
+        assert np.array_equal(got["code_col"][b:b + 1, :, :, :L], ref["code_col"]), b
+        assert np.array_equal(got["scale_col"][b:b + 1, :, :, :L // 32], ref["scale_col"]), b
+        assert np.array_equal(amax[b:b + 1], np.abs(y).max(axis=1).astype(np.float32)), b
