@@ -13,6 +13,7 @@ import numpy as np
 import pytest
 import torch
 
+import oracle as orc
 import paper_2609_37852_amd as pk
 from paper_2609_37852_amd import synth
 from _helpers import REL_TOL, block_errors, check_blocks, invariant_report, rel_err, run_oracle, say, to_dev
@@ -79,7 +80,7 @@ def _run(w, d, lq, lk, mode=pk.DELTA_MATCHING, delta_in=None, flags=0):
     return dict(O=f(o), LSE=f(lse), delta=f(delta), dQ=f(dq), dK=f(dk), dV=f(dv), rowstats=rs.cpu().numpy())
 
 
-def _alone(w, d, b, nq, nk, flags=0):
+def _alone(w, d, b, nq, nk, flags=0, mode=pk.DELTA_MATCHING):
     """The same kernels on sequence b alone (B = 1, its own lengths)."""
     w1 = synth.with_shape(w, B=1, N=nq, Nk=0 if w.causal else nk)
     q, do = (to_dev(d[n][b:b + 1, :nq], w.dtype) for n in ("q", "do"))
@@ -88,8 +89,8 @@ def _alone(w, d, b, nq, nk, flags=0):
     p = pk.Problem(1, nq, w.Hq, w.Hkv, w.Dqk, w.Dv, float(np.float32(w.tau)), causal=int(w.causal), seqlen_kv=w1.Nk,
                    flags=flags)
     o, lse = pk.attn_fp8_fwd(p, mq, mk, mv)
-    delta = pk.attn_fp8_delta(p, pk.DELTA_MATCHING, mq, mk, mv, mdo, lse, do, o)
-    dq, _, _, _ = pk.attn_fp8_bwd(p, pk.DELTA_MATCHING, mq, mk, mv, mdo, lse, do, o, grad_dtype=torch.float32)
+    delta = pk.attn_fp8_delta(p, mode, mq, mk, mv, mdo, lse, do, o)
+    dq, _, _, _ = pk.attn_fp8_bwd(p, mode, mq, mk, mv, mdo, lse, do, o, grad_dtype=torch.float32)
     torch.cuda.synchronize()
     f = lambda t: t.float().cpu().numpy().astype(np.float64)
     return dict(O=f(o), LSE=f(lse), delta=f(delta), dQ=f(dq))
@@ -110,11 +111,24 @@ def test_varlen_isolate3():
     _check(name, kw, lq, lk, pk.FLAG_ISOLATE3)
 
 
-def _check(name, kw, lq, lk, flags):
+@pytest.mark.parametrize("variant", ["pbwd_block_scaled", "compensated"])
+@pytest.mark.parametrize("case", [0, 3], ids=["causal", "unmasked"])
+def test_varlen_numerics_variants(variant, case):
+    """The block-scaled backward probability operand (against the oracle's
+    variant) and the compensated correction on padded batches, causal and
+    without the mask: the same per-sequence checks."""
+    name, kw, lq, lk = CASES[case]
+    if variant == "pbwd_block_scaled":
+        _check(name, kw, lq, lk, pk.FLAG_PBWD_BLOCK_SCALED, oracle_flags=orc.MX_PBWD)
+    else:
+        _check(name, kw, lq, lk, 0, mode=pk.DELTA_MATCHING_COMPENSATED)
+
+
+def _check(name, kw, lq, lk, flags, mode=pk.DELTA_MATCHING, oracle_flags=0):
     w = synth.with_shape(synth.WORKLOADS[name], **kw)
-    say(f"varlen parity {w} lens_q={lq} lens_kv={lk} flags={flags}")
+    say(f"varlen parity {w} lens_q={lq} lens_kv={lk} flags={flags} mode={mode}")
     d = synth.generate(w, seed=11)
-    g = _run(w, d, lq, lk, flags=flags)
+    g = _run(w, d, lq, lk, mode=mode, flags=flags)
     for b, (nq, nk) in enumerate(_eff(lq, lk, w.causal)):
         # padding rows untouched
         assert np.all(g["O"][b, nq:] == SENTINEL) and np.all(g["LSE"][b, :, nq:] == SENTINEL), b
@@ -126,7 +140,7 @@ def _check(name, kw, lq, lk, flags):
             continue
         ws = synth.with_shape(w, B=1, N=nq, Nk=0 if w.causal else nk)
         ds = {n: d[n][b:b + 1, :(nq if n in ("q", "do") else nk)] for n in ("q", "k", "v", "do")}
-        o = run_oracle(ws, ds)
+        o = run_oracle(ws, ds, flags=oracle_flags) if oracle_flags else run_oracle(ws, ds)
         gs = dict(O=g["O"][b:b + 1, :nq], dQ=g["dQ"][b:b + 1, :nq], dK=g["dK"][b:b + 1, :nk],
                   dV=g["dV"][b:b + 1, :nk])
         errs = {n: rel_err(gs[n], o[n]) for n in gs}
@@ -142,7 +156,7 @@ def _check(name, kw, lq, lk, flags):
         assert errs["LSE"] < 1e-3 and errs["delta"] < 1e-3, (b, errs)
         assert rep["violations"] == 0, (b, rep)
         # the query-major results equal those of the sequence run alone
-        a = _alone(w, d, b, nq, nk, flags)
+        a = _alone(w, d, b, nq, nk, flags, mode)
         assert np.array_equal(g["O"][b:b + 1, :nq], a["O"]), b
         assert np.array_equal(g["LSE"][b:b + 1, :, :nq], a["LSE"]), b
         assert np.array_equal(g["delta"][b:b + 1, :, :nq], a["delta"]), b
