@@ -519,6 +519,15 @@ def main():
     rows = w.B * w.N * w.Hq
     stale_bytes = 4.0 * rows * w.Dv + 8.0 * rows    # bf16 dO and O in, (hi, lo) out
     consistent_bytes = (1 + 1 / 32 + 2) * rows * w.Dv + 8.0 * rows
+    # the matched correction reads the Q and dO row copies, the K and V row
+    # copies (codes and scales) and the LSE, and writes (hi, lo) per row
+    kv_rows = w.B * w.nk * w.Hkv
+    delta_bytes = (rows * (1 + 1 / 32) * (w.Dqk + w.Dv) + kv_rows * (1 + 1 / 32) * (w.Dqk + w.Dv)
+                   + 4.0 * rows + 8.0 * rows)
+    # after the main kernel: the dQ pass reads the one-byte dS' units (one per
+    # causal score) and the K col copy, and writes dQ (bf16); the preparation
+    # kernel's few MB are in the same interval
+    dq_bytes = rows * w.N / 2 + kv_rows * (1 + 1 / 32) * w.Dqk + 2.0 * rows * w.Dqk
 
     line = {
         "metric": "FP8 attention fwd+bwd TFLOP/s and % of FP8 MFMA peak (causal GQA d128, 8K)",
@@ -554,7 +563,18 @@ def main():
         "hbm_gbs": {"quantize": round(quant_bytes / (t_quant * 1e-3) / 1e9, 1),
                     "delta_stale_rowsum": round(stale_bytes / (t_delta_stale * 1e-3) / 1e9, 1),
                     "delta_consistent_do": round(consistent_bytes / (t_delta_consistent * 1e-3) / 1e9, 1),
+                    # compute-bound (its GEMMs and exponentials), listed for completeness
+                    "delta_matching": round(delta_bytes / (t_delta * 1e-3) / 1e9, 1),
+                    "dq_pass_and_prep": round(dq_bytes / ((t_bwd_call - t_bwd_main) * 1e-3) / 1e9, 1),
                     "peak": PEAK_HBM_GBS},
+        # the other attention kernels against the same FP8 MFMA peak: the
+        # forward's credited FLOPs and the correction pass's S and dP
+        # (uncredited), each over its own time
+        "mfma_other": {"fwd_kernel": {"achieved": round(fwd_f / (t_fwd * 1e-3) / 1e12, 2),
+                                      "frac": round(fwd_f / (t_fwd * 1e-3) / 1e12 / PEAK_FP8_TFLOPS, 4)},
+                       "delta_matching_kernel": {"achieved": round(fwd_f / (t_delta * 1e-3) / 1e12, 2),
+                                                 "frac": round(fwd_f / (t_delta * 1e-3) / 1e12 / PEAK_FP8_TFLOPS,
+                                                               4)}},
         "roofline": {"kernel": "bwd_kernel<128,128>", "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP8_TFLOPS, 4),
                      "traffic": traffic, "flops_per_launch": main_f, "ms_per_launch": round(t_bwd_main, 4)},
