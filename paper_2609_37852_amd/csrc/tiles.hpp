@@ -206,7 +206,7 @@ __device__ __forceinline__ void select_hot_channels(const float* q_amax, const f
       // the chosen channel is out of the next rounds
 #pragma unroll
       for (int u = 0; u < PER; u++)
-        if (threadIdx.x + 64 * u == bi) sc[u] = -2.f;
+        if ((int)threadIdx.x + 64 * u == bi) sc[u] = -2.f;
       if (threadIdx.x == 0) slots[i] = bi < D ? bi : -1;
     }
   }
