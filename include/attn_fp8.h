@@ -153,7 +153,29 @@ typedef struct {
   const int32_t* seqlens_q;   /* nullable device [B]: query length of each sequence */
   const int32_t* seqlens_kv;  /* nullable device [B]: key length of each sequence (NULL
                                  under the mask, where it equals the query length) */
+  void* cast_dump;            /* nullable device buffer, test instrumentation read by
+                                 the instrumented backward only (rowstats given): see
+                                 ATTN_FP8_CAST_DUMP_BYTES */
 } attn_fp8_problem;
+
+/* Cast dump of the instrumented backward (App. B.6.3's in-kernel casts, for
+ * checking them code by code against a reference codec): with
+ * problem.cast_dump and rowstats, attn_fp8_bwd also writes, for every
+ * (query, key) pair of every 32 x 32 block it computes (blocks it skips are
+ * left as they were), with S = B Hq N Nk:
+ *   float   P[S]        the backward probability, pre-cast (0 where masked)
+ *   float   dS[S]       the score gradient, pre-cast
+ *   uint8_t Pc[S]       the code of P' (scale 2^-8, or the block's with
+ *                       ATTN_FP8_FLAG_PBWD_BLOCK_SCALED)
+ *   uint8_t dSc[S]      the code of dS' in its 32 x 32 block
+ *   uint8_t eS[B Hq (N/32) (Nk/32)]  dS' block exponents + 127
+ *   uint8_t eP[B Hq (N/32) (Nk/32)]  P' block exponents + 127 (with the flag)
+ * each array [b, h, query, key] / [b, h, query block, key block], one after
+ * the other in this order, the buffer 16-byte aligned (EALIGN otherwise).
+ * For small problems only (about 10 bytes per pair); EINVAL without
+ * rowstats. */
+#define ATTN_FP8_CAST_DUMP_BYTES(B, Hq, N, Nk) \
+  (10 * (size_t)(B) * (Hq) * (N) * (Nk) + 2 * (size_t)(B) * (Hq) * ((N) / 32) * ((Nk) / 32))
 
 /* One MX-quantized operand X of shape [B, N, H, D]; device memory, caller-owned.
  *   code_row  [B, H, N, D]     E4M3FN codes, 1x32 blocks along D

@@ -40,7 +40,8 @@ class _Problem(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int64), ("seqlen", ctypes.c_int64), ("heads_q", ctypes.c_int64),
                 ("heads_kv", ctypes.c_int64), ("dim_qk", ctypes.c_int64), ("dim_v", ctypes.c_int64),
                 ("causal", ctypes.c_int32), ("softmax_scale", ctypes.c_float), ("seqlen_kv", ctypes.c_int64),
-                ("flags", ctypes.c_int32), ("seqlens_q", ctypes.c_void_p), ("seqlens_kv", ctypes.c_void_p)]
+                ("flags", ctypes.c_int32), ("seqlens_q", ctypes.c_void_p), ("seqlens_kv", ctypes.c_void_p),
+                ("cast_dump", ctypes.c_void_p)]
 
 
 class _Producer(ctypes.Structure):
@@ -139,6 +140,9 @@ class Problem:
     # (seqlens_kv without the mask only), or None for the full lengths
     seqlens_q: torch.Tensor | None = None
     seqlens_kv: torch.Tensor | None = None
+    # instrumented backward only: a device uint8 tensor of cast_dump_bytes()
+    # that receives the pre-cast P, dS and their codes (or None)
+    cast_dump: torch.Tensor | None = None
 
     @property
     def nk(self) -> int:
@@ -150,7 +154,22 @@ class Problem:
                 "seqlens: contiguous int32 [batch] tensors"
         return _Problem(self.batch, self.seqlen, self.heads_q, self.heads_kv, self.dim_qk, self.dim_v,
                         self.causal, self.softmax_scale, self.seqlen_kv, self.flags,
-                        _ptr(self.seqlens_q).value, _ptr(self.seqlens_kv).value)
+                        _ptr(self.seqlens_q).value, _ptr(self.seqlens_kv).value, _ptr(self.cast_dump).value)
+
+    def cast_dump_bytes(self) -> int:
+        s = self.batch * self.heads_q * self.seqlen * self.nk
+        return 10 * s + 2 * self.batch * self.heads_q * (self.seqlen // 32) * (self.nk // 32)
+
+    def cast_dump_views(self):
+        """(P, dS, Pc, dSc, eS, eP) views of cast_dump, each [B, Hq, N, Nk] or
+        [B, Hq, N/32, Nk/32]."""
+        B, H, N, Nk = self.batch, self.heads_q, self.seqlen, self.nk
+        s, nb = B * H * N * Nk, B * H * (N // 32) * (Nk // 32)
+        d = self.cast_dump
+        return (d[:4 * s].view(torch.float32).view(B, H, N, Nk), d[4 * s:8 * s].view(torch.float32).view(B, H, N, Nk),
+                d[8 * s:9 * s].view(B, H, N, Nk), d[9 * s:10 * s].view(B, H, N, Nk),
+                d[10 * s:10 * s + nb].view(B, H, N // 32, Nk // 32),
+                d[10 * s + nb:10 * s + 2 * nb].view(B, H, N // 32, Nk // 32))
 
 
 @dataclass

@@ -160,6 +160,7 @@ afp8::AttnArgs base_args(const attn_fp8_problem* p) {
   a.iso3 = (p->flags & ATTN_FP8_FLAG_ISOLATE3) != 0;
   a.lens_q = p->seqlens_q;
   a.lens_k = p->causal ? nullptr : p->seqlens_kv;
+  a.cast_dump = p->cast_dump;
   a.tau = p->softmax_scale;
   a.c = (float)((double)p->softmax_scale * 1.4426950408889634);
   return a;
@@ -542,6 +543,8 @@ static int bwd_impl(const attn_fp8_problem* p, int delta_mode, const attn_fp8_mx
     return rc;
   }
   if (rowstats && !aligned16(rowstats)) return fail(ATTN_FP8_EALIGN, "rowstats is not 16-byte aligned");
+  if (p->cast_dump && !rowstats) return fail(ATTN_FP8_EINVAL, "cast_dump without rowstats");
+  if (p->cast_dump && !aligned16(p->cast_dump)) return fail(ATTN_FP8_EALIGN, "cast_dump is not 16-byte aligned");
   const size_t need = ws_bwd_bytes(p);
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u))
     return fail(ATTN_FP8_EWORKSPACE, "workspace is NULL or not 256-byte aligned");

@@ -541,6 +541,31 @@ __global__ __launch_bounds__((BwdCfg<DQK, DV>::NT)) void bwd_kernel(AttnArgs a) 
         }
       }
     }
+    if constexpr (STATS) {
+      // the cast dump: pre-cast P and dS of the lane's 16 pairs, their codes,
+      // and the block exponents
+      if (a.cast_dump) {
+        const size_t S = (size_t)a.B * Hq * N * Nk, bhq = (size_t)b * Hq + h;
+        float* Pd = reinterpret_cast<float*>(a.cast_dump);
+        float* Dd = Pd + S;
+        uint8_t* Pcd = reinterpret_cast<uint8_t*>(Dd + S);
+        uint8_t* Dcd = Pcd + S;
+        uint8_t* Ed = Dcd + S;
+#pragma unroll
+        for (int r = 0; r < 16; r++) {
+          const size_t idx = (bhq * N + qb + 8 * (r >> 2) + 4 * hf + (r & 3)) * Nk + kj;
+          Pd[idx] = s[r];
+          Dd[idx] = dp[r];
+          Pcd[idx] = (uint8_t)((uint32_t)pc[r >> 2] >> (8 * (r & 3)));
+          Dcd[idx] = (uint8_t)((uint32_t)dc[r >> 2] >> (8 * (r & 3)));
+        }
+        if (lane == 0) {
+          const size_t bi = (bhq * (N / 32) + qb / 32) * (Nk / 32) + kw0 / 32;
+          Ed[bi] = (uint8_t)(e + 127);
+          if constexpr (PMX) Ed[(size_t)a.B * Hq * (N / 32) * (Nk / 32) + bi] = (uint8_t)(ep + 127);
+        }
+      }
+    }
     // natural query order: lane hf holds queries 16 hf .. 16 hf + 15 of the half
     pn = to_natural4(pc);
     dn = to_natural4(dc);

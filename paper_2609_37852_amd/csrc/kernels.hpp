@@ -101,6 +101,7 @@ struct AttnArgs {
   int grad_bf16;
   int bwd_cohort;                      // backward: workgroups of one KV head that run at once (set at launch)
   double* rowstats;                    // nullable [B,Hq,N,kRowStats]
+  void* cast_dump;                     // nullable, with rowstats: pre-cast P, dS and their codes
   // Padded batch of sequences of their own lengths (nullable [B] each):
   // sequence b has lens_q[b] queries and lens_k[b] keys, at the first
   // positions of the N / Nk of the layouts above; NULL: N and Nk
