@@ -146,6 +146,34 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
       for (int k = 0; k < 16; k++) v[u][k] = 0.f;
     }
   }
+  // the producer's other inputs, loaded together with the tokens: row
+  // scales, gains, rotary table entries and the channel means (gain, table
+  // and mean are 16-byte aligned, ch a multiple of 16)
+  [[maybe_unused]] float rsc[NB], gn[16], mu[16];
+  [[maybe_unused]] float4 cs[NB][8];
+  [[maybe_unused]] const int h2 = a.rope_dim >> 1, rel = ch - a.rope_lo;
+  [[maybe_unused]] const bool rot = a.rope && rel >= 0 && rel < a.rope_dim, first = rel < h2;
+  [[maybe_unused]] const int pch = first ? ch + h2 : ch - h2, c0 = first ? rel : rel - h2;
+  if constexpr (PROD) {
+#pragma unroll
+    for (int u = 0; u < NB; u++) rsc[u] = a.gain && u < nb ? a.rscale[((b * a.N) + n0 + 32 * u + tok) * a.H + h] : 1.f;
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+      const float4 g4 = a.gain ? reinterpret_cast<const float4*>(a.gain + ch)[k] : make_float4(1.f, 1.f, 1.f, 1.f);
+      const float4 m4 = a.mean ? reinterpret_cast<const float4*>(a.mean + bh * D + ch)[k] : make_float4(0.f, 0.f, 0.f, 0.f);
+      gn[4 * k] = g4.x; gn[4 * k + 1] = g4.y; gn[4 * k + 2] = g4.z; gn[4 * k + 3] = g4.w;
+      mu[4 * k] = m4.x; mu[4 * k + 1] = m4.y; mu[4 * k + 2] = m4.z; mu[4 * k + 3] = m4.w;
+    }
+#pragma unroll
+    for (int u = 0; u < NB; u++) {
+      if (rot && u < nb) {
+        const float4* cs4 = reinterpret_cast<const float4*>(
+            reinterpret_cast<const float2*>(a.rope) + (n0 + 32 * u + tok) * h2 + c0);
+#pragma unroll
+        for (int k = 0; k < 8; k++) cs[u][k] = cs4[k];
+      }
+    }
+  }
 
   if (a.nonfinite) {
     uint32_t bad = 0;
@@ -160,9 +188,8 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
 #pragma unroll
       for (int u = 0; u < NB; u++) {
         if (u >= nb) break;
-        const float r = a.rscale[((b * a.N) + n0 + 32 * u + tok) * a.H + h];
 #pragma unroll
-        for (int k = 0; k < 16; k++) v[u][k] = qk_norm(v[u][k], r, a.gain[ch + k]);
+        for (int k = 0; k < 16; k++) v[u][k] = qk_norm(v[u][k], rsc[u], gn[k]);
       }
     }
     if (a.rope) {
@@ -170,9 +197,6 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
       // lane h2 / 16 further along the token (a token's CH lanes are
       // consecutive), or through the tile where a token's chunks may lie in
       // two waves (64 % CH != 0)
-      const int h2 = a.rope_dim >> 1, rel = ch - a.rope_lo;
-      const bool rot = rel >= 0 && rel < a.rope_dim, first = rel < h2;
-      const int pch = first ? ch + h2 : ch - h2, c0 = first ? rel : rel - h2;
       if constexpr (64 % CH == 0) {
         const int plane = (t & 63) + (rot ? (pch - ch) / 16 : 0);
 #pragma unroll
@@ -181,13 +205,10 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
 #pragma unroll
           for (int k = 0; k < 16; k++) pv[k] = __shfl(v[u][k], plane);
           if (rot && u < nb) {
-            const float4* cs4 = reinterpret_cast<const float4*>(
-                reinterpret_cast<const float2*>(a.rope) + (n0 + 32 * u + tok) * h2 + c0);
 #pragma unroll
             for (int k = 0; k < 8; k++) {
-              const float4 cs = cs4[k];
-              v[u][2 * k] = rope_rotate(v[u][2 * k], pv[2 * k], make_float2(cs.x, cs.y), first);
-              v[u][2 * k + 1] = rope_rotate(v[u][2 * k + 1], pv[2 * k + 1], make_float2(cs.z, cs.w), first);
+              v[u][2 * k] = rope_rotate(v[u][2 * k], pv[2 * k], make_float2(cs[u][k].x, cs[u][k].y), first);
+              v[u][2 * k + 1] = rope_rotate(v[u][2 * k + 1], pv[2 * k + 1], make_float2(cs[u][k].z, cs[u][k].w), first);
             }
           }
         }
@@ -201,17 +222,17 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
 #pragma unroll
           for (int u = 0; u < NB; u++) {
             if (u >= nb) break;
-            const float2* cs = reinterpret_cast<const float2*>(a.rope) + (n0 + 32 * u + tok) * h2 + c0;
 #pragma unroll
-            for (int k = 0; k < 16; k++) v[u][k] = rope_rotate(v[u][k], tile[32 * u + tok][pch + k], cs[k], first);
+            for (int k = 0; k < 8; k++) {
+              v[u][2 * k] = rope_rotate(v[u][2 * k], tile[32 * u + tok][pch + 2 * k], make_float2(cs[u][k].x, cs[u][k].y), first);
+              v[u][2 * k + 1] = rope_rotate(v[u][2 * k + 1], tile[32 * u + tok][pch + 2 * k + 1],
+                                            make_float2(cs[u][k].z, cs[u][k].w), first);
+            }
           }
         }
         __syncthreads();   // the tile is written again below
       }
     }
-    float mu[16];
-#pragma unroll
-    for (int k = 0; k < 16; k++) mu[k] = a.mean ? a.mean[bh * D + ch + k] : 0.f;
 #pragma unroll
     for (int u = 0; u < NB; u++)
 #pragma unroll
@@ -273,38 +294,42 @@ __global__ __launch_bounds__(2 * D) void quantize_kernel(QuantArgs a) {
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 
 // Key mean of the input producer (reading R13): FP64 sums of the prescaled
-// values over aligned 32-token blocks, tokens ascending (one thread per
-// channel: grid (N/32, H, B)), then the block sums ascending (grid (H, B)),
-// divided by N in FP64 and rounded once to FP32.  The fixed order makes the
-// mean independent of scheduling.
+// values over aligned 32-token blocks, tokens ascending (one thread per 8
+// channels and block), then the block sums ascending (one thread per
+// channel: grid (H, B)), divided by N in FP64 and rounded once to FP32.  The
+// fixed order makes the mean independent of scheduling.
+// Eight consecutive channels of one token as FP32, from their raw bytes
+// (one 16-byte word for BF16, two for FP32).
 template <typename T>
-__device__ __forceinline__ float to_f32(T x) {
-  if constexpr (sizeof(T) == 2) return bf16_to_f32(x);
-  else return (float)x;
-}
-
-// Two consecutive channels of one token as FP32.
-template <typename T>
-__device__ __forceinline__ float2 load2(const T* p) {
+__device__ __forceinline__ void unpack8(const uint4 (&u)[sizeof(T) / 2], float (&v)[8]) {
   if constexpr (sizeof(T) == 2) {
-    const uint32_t u = *reinterpret_cast<const uint32_t*>(p);
-    return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
+    const uint32_t w[4] = {u[0].x, u[0].y, u[0].z, u[0].w};
+#pragma unroll
+    for (int m = 0; m < 4; m++) {
+      v[2 * m] = __uint_as_float(w[m] << 16);
+      v[2 * m + 1] = __uint_as_float(w[m] & 0xffff0000u);
+    }
   } else {
-    return *reinterpret_cast<const float2*>(p);
+    const uint32_t w[8] = {u[0].x, u[0].y, u[0].z, u[0].w, u[1].x, u[1].y, u[1].z, u[1].w};
+#pragma unroll
+    for (int m = 0; m < 8; m++) v[m] = __uint_as_float(w[m]);
   }
 }
 
-// Key-mean partial sums: a thread owns channels c, c + 1 (2 t) of one aligned
+// Key-mean partial sums: a thread owns channels c .. c + 7 of one aligned
 // 32-token block of one (batch, head) and sums the transformed values of
-// each in FP64 over the block's tokens in ascending order; partials are laid
-// out [B, H, N/32, D] so that the mean pass reads them coalesced.  The
-// transform (norm, rotation, prescale) is the quantizer's; the two channels
-// of a thread are both rotary or both not, and both first or both second of
-// their pairs (the rotary range is 32-aligned), so their partners are
-// consecutive as well.
+// each in FP64 over the block's tokens in ascending order; a workgroup of
+// D / 2 threads takes kPartialBlocks blocks (D / 8 threads each).  Partials
+// are laid out [B, H, N/32, D] so that the mean pass reads them coalesced.
+// The transform (norm, rotation, prescale) is the quantizer's; the eight
+// channels of a thread are all rotary or all not, and all first or all
+// second of their pairs (the rotary range and its halves are multiples of
+// 16 channels), so their partners are consecutive as well.
 // With sequence lengths, the mean's tokens of batch entry b: its first L_b
 // (clamped into [0, N], rounded down to a multiple of 32, as the attention
 // kernels take it).
+constexpr int kPartialBlocks = 4;
+
 __device__ __forceinline__ int64_t mean_tokens(const QuantArgs& a, int64_t b) {
   if (!a.lens) return a.N;
   const int64_t v = a.lens[b];
@@ -313,43 +338,76 @@ __device__ __forceinline__ int64_t mean_tokens(const QuantArgs& a, int64_t b) {
 
 template <typename T>
 __global__ __launch_bounds__(128) void producer_partials_kernel(QuantArgs a, int D) {
-  const int c = 2 * (int)threadIdx.x;
-  if (c >= D) return;
-  const int64_t t = blockIdx.x, h = blockIdx.y, b = blockIdx.z, nblk = a.N / 32;
+  const int cpr = D / 8, c = 8 * ((int)threadIdx.x % cpr);
+  const int64_t nblk = a.N / 32, t = (int64_t)blockIdx.x * kPartialBlocks + threadIdx.x / cpr;
+  const int64_t h = blockIdx.y, b = blockIdx.z;
+  if (t >= nblk) return;
+  double2* out = reinterpret_cast<double2*>(a.partials + ((b * a.H + h) * nblk + t) * D + c);
   if (32 * t >= mean_tokens(a, b)) {
     // a block past the sequence adds nothing to its mean
-    *reinterpret_cast<double2*>(a.partials + ((b * a.H + h) * nblk + t) * D + c) = make_double2(0.0, 0.0);
+#pragma unroll
+    for (int m = 0; m < 4; m++) out[m] = make_double2(0.0, 0.0);
     return;
   }
   const T* src = reinterpret_cast<const T*>(a.x) + b * a.sb + h * a.sh + c;
   const int h2 = a.rope_dim >> 1, rel = c - a.rope_lo;
   const bool rot = a.rope && rel >= 0 && rel < a.rope_dim, first = rel < h2;
   const int poff = first ? h2 : -h2, c0 = first ? rel : rel - h2;
-  float2 g = make_float2(1.f, 1.f), pg = make_float2(1.f, 1.f);
-  if (a.gain) {
-    g = make_float2(a.gain[c], a.gain[c + 1]);
-    if (rot) pg = make_float2(a.gain[c + poff], a.gain[c + poff + 1]);
+  float g[8], pg[8];
+#pragma unroll
+  for (int m = 0; m < 8; m++) {
+    g[m] = a.gain ? a.gain[c + m] : 1.f;
+    pg[m] = a.gain && rot ? a.gain[c + poff + m] : 1.f;
   }
-  double part0 = 0.0, part1 = 0.0;
-#pragma unroll 8
-  for (int k = 0; k < 32; k++) {
-    const int64_t n = 32 * t + k;
-    float2 f = load2<T>(src + n * a.sn);
-    float2 p = rot ? load2<T>(src + n * a.sn + poff) : make_float2(0.f, 0.f);
-    if (a.gain) {
-      const float r = a.rscale[(b * a.N + n) * a.H + h];
-      f = make_float2(qk_norm(f.x, r, g.x), qk_norm(f.y, r, g.y));
-      if (rot) p = make_float2(qk_norm(p.x, r, pg.x), qk_norm(p.y, r, pg.y));
+  double part[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+  // KC tokens' loads issued ahead of their arithmetic (c is a multiple of 8
+  // and every stride a multiple of 16 bytes, so the words are aligned)
+  constexpr int KC = 8, W = sizeof(T) / 2;
+  for (int k0 = 0; k0 < 32; k0 += KC) {
+    uint4 xr[KC][W], pr[KC][W];
+    float4 cs[KC][4];
+    float rs[KC];
+#pragma unroll
+    for (int k = 0; k < KC; k++) {
+      const int64_t n = 32 * t + k0 + k;
+      const uint4* x4 = reinterpret_cast<const uint4*>(src + n * a.sn);
+#pragma unroll
+      for (int m = 0; m < W; m++) xr[k][m] = x4[m];
+      if (rot) {
+        const uint4* p4 = reinterpret_cast<const uint4*>(src + n * a.sn + poff);
+        const float4* c4 = reinterpret_cast<const float4*>(a.rope + 2 * (n * h2 + c0));
+#pragma unroll
+        for (int m = 0; m < W; m++) pr[k][m] = p4[m];
+#pragma unroll
+        for (int m = 0; m < 4; m++) cs[k][m] = c4[m];
+      }
+      rs[k] = a.gain ? a.rscale[(b * a.N + n) * a.H + h] : 1.f;
     }
-    if (rot) {
-      const float4 cs = *reinterpret_cast<const float4*>(a.rope + 2 * (n * h2 + c0));
-      f = make_float2(rope_rotate(f.x, p.x, make_float2(cs.x, cs.y), first),
-                      rope_rotate(f.y, p.y, make_float2(cs.z, cs.w), first));
+#pragma unroll
+    for (int k = 0; k < KC; k++) {
+      float f[8], p[8];
+      unpack8<T>(xr[k], f);
+      if (rot) unpack8<T>(pr[k], p);
+      if (a.gain) {
+#pragma unroll
+        for (int m = 0; m < 8; m++) {
+          f[m] = qk_norm(f[m], rs[k], g[m]);
+          if (rot) p[m] = qk_norm(p[m], rs[k], pg[m]);
+        }
+      }
+      if (rot) {
+#pragma unroll
+        for (int m = 0; m < 4; m++) {
+          f[2 * m] = rope_rotate(f[2 * m], p[2 * m], make_float2(cs[k][m].x, cs[k][m].y), first);
+          f[2 * m + 1] = rope_rotate(f[2 * m + 1], p[2 * m + 1], make_float2(cs[k][m].z, cs[k][m].w), first);
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < 8; m++) part[m] += (double)mul_rn(f[m], a.prescale);
     }
-    part0 += (double)mul_rn(f.x, a.prescale);
-    part1 += (double)mul_rn(f.y, a.prescale);
   }
-  *reinterpret_cast<double2*>(a.partials + ((b * a.H + h) * nblk + t) * D + c) = make_double2(part0, part1);
+#pragma unroll
+  for (int m = 0; m < 4; m++) out[m] = make_double2(part[2 * m], part[2 * m + 1]);
 }
 
 // Reciprocal RMS of every (token, head) row for the QK normalization: the
@@ -413,9 +471,18 @@ __global__ __launch_bounds__(256) void producer_mean_kernel(QuantArgs a, int D) 
   if (c >= D) return;
   const int64_t h = blockIdx.x, b = blockIdx.y, nblk = a.N / 32, n = mean_tokens(a, b);
   const double* p = a.partials + (b * a.H + h) * nblk * D + c;
+  // 64 block sums loaded at a time, then added in order
   double total = 0.0;
-#pragma unroll 8
-  for (int64_t t = 0; t < n / 32; t++) total += p[t * D];
+  const int64_t nb = n / 32;
+  int64_t t0 = 0;
+  for (; t0 + 64 <= nb; t0 += 64) {
+    double v[64];
+#pragma unroll
+    for (int k = 0; k < 64; k++) v[k] = p[(t0 + k) * D];
+#pragma unroll
+    for (int k = 0; k < 64; k++) total += v[k];
+  }
+  for (; t0 < nb; t0++) total += p[t0 * D];
   a.mean[(b * a.H + h) * D + c] = n > 0 ? (float)(total / (double)n) : 0.f;
 }
 
@@ -433,7 +500,8 @@ hipError_t launch_quantize(const QuantArgs& a, int D, int dtype_bf16, hipStream_
     else hipLaunchKernelGGL(producer_rscale_kernel<float>, g0, dim3(256), 0, s, a, D);
   }
   if (a.mean) {
-    const dim3 g1((unsigned)(a.N / 32), (unsigned)a.H, (unsigned)a.B), g2((unsigned)a.H, (unsigned)a.B);
+    const dim3 g1((unsigned)((a.N / 32 + kPartialBlocks - 1) / kPartialBlocks), (unsigned)a.H, (unsigned)a.B),
+        g2((unsigned)a.H, (unsigned)a.B);
     if (dtype_bf16) hipLaunchKernelGGL(producer_partials_kernel<uint16_t>, g1, dim3(D / 2), 0, s, a, D);
     else hipLaunchKernelGGL(producer_partials_kernel<float>, g1, dim3(D / 2), 0, s, a, D);
     hipLaunchKernelGGL(producer_mean_kernel, g2, dim3(256), 0, s, a, D);
