@@ -183,7 +183,9 @@ class Runner:
         del d
         self.p = pk.Problem(w.B, w.N, w.Hq, w.Hkv, w.Dqk, w.Dv, float(np.float32(w.tau)), causal=int(w.causal),
                             seqlen_kv=w.Nk)
-        self.mq, self.mk, self.mv, self.mdo = (pk.MX.empty(*t.shape, dev) for t in (self.q, self.k, self.v, self.do))
+        # channel maxima only where a kernel reads them: Q and K (the isolated score channel)
+        self.mq, self.mk, self.mv, self.mdo = (pk.MX.empty(*t.shape, dev, amax=a) for t, a in
+                                               ((self.q, True), (self.k, True), (self.v, False), (self.do, False)))
         self.o = torch.empty((w.B, w.N, w.Hq, w.Dv), dtype=torch.bfloat16, device=dev)
         self.lse = torch.empty((w.B, w.Hq, w.N), dtype=torch.float32, device=dev)
         self.delta = torch.empty((w.B, w.Hq, w.N, 2), dtype=torch.float32, device=dev)
