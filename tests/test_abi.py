@@ -93,6 +93,14 @@ def test_null_alignment_and_workspace_errors():
                                                            None] + [ctypes.c_void_p(4096)] * 3 + [1, st, st, st]
     assert L.attn_fp8_bwd(*args, ctypes.c_void_p(4096), ctypes.c_size_t(n.value - 1), None, None, None) == -4
     assert L.attn_fp8_bwd(*args, ctypes.c_void_p(4096 + 16), ctypes.c_size_t(n.value), None, None, None) == -4
+    # the cast dump needs the row statistics and 16-byte alignment
+    p.cast_dump = 4096
+    assert L.attn_fp8_bwd(*args, ctypes.c_void_p(4096), ctypes.c_size_t(n.value), None, None, None) == -1
+    assert "rowstats" in pk.last_error()
+    p.cast_dump = 4096 + 4
+    assert L.attn_fp8_bwd(*args, ctypes.c_void_p(4096), ctypes.c_size_t(n.value), ctypes.c_void_p(4096),
+                          None, None) == -3
+    p.cast_dump = None
 
 
 def test_quantize_rejects_bad_args():
