@@ -53,6 +53,10 @@ CASES = [
     ("causal_pmx", synth.with_shape(synth.WORKLOADS["gqa_d128_8k"], B=1, N=192, Hq=2, Hkv=1),
      pk.FLAG_PBWD_BLOCK_SCALED),
     ("unmasked", synth.with_shape(synth.WORKLOADS["tiny_mha_128"], B=2, N=96, Nk=160, causal=False), 0),
+    # wide heads: two key blocks per workgroup
+    ("d192", synth.with_shape(synth.WORKLOADS["mla_d192_4k"], B=1, N=160, Hq=2, Hkv=2), 0),
+    ("d256_unmasked", synth.with_shape(synth.WORKLOADS["gqa_d256_8k_qknorm"], B=1, N=96, Nk=128, Hq=2, Hkv=1,
+                                       causal=False), 0),
 ]
 
 
