@@ -57,6 +57,11 @@ CASES = [
     ("d192", synth.with_shape(synth.WORKLOADS["mla_d192_4k"], B=1, N=160, Hq=2, Hkv=2), 0),
     ("d256_unmasked", synth.with_shape(synth.WORKLOADS["gqa_d256_8k_qknorm"], B=1, N=96, Nk=128, Hq=2, Hkv=1,
                                        causal=False), 0),
+    # the other backward instantiations: three isolated score channels, and
+    # the protected dP (dP from BF16 operands, the stale correction)
+    ("causal_iso3", synth.with_shape(synth.WORKLOADS["gqa_d128_8k"], B=1, N=128, Hq=2, Hkv=1), pk.FLAG_ISOLATE3),
+    ("causal_pdp", synth.with_shape(synth.WORKLOADS["gqa_d128_8k"], B=1, N=128, Hq=2, Hkv=1),
+     pk.FLAG_PROTECTED_DP),
 ]
 
 
@@ -71,8 +76,12 @@ def test_cast_dump(name, w, flags):
     o, lse = pk.attn_fp8_fwd(p, mq, mk, mv)
     p.cast_dump = torch.full((p.cast_dump_bytes(),), SENTINEL, dtype=torch.uint8, device="cuda")
     say(f"{name}: {w} flags {flags}, dump {p.cast_dump_bytes()} bytes")
-    _, _, _, rs = pk.attn_fp8_bwd(p, pk.DELTA_MATCHING, mq, mk, mv, mdo, lse, do, o, grad_dtype=torch.float32,
-                                  rowstats=True)
+    if flags & pk.FLAG_PROTECTED_DP:
+        _, _, _, rs = pk.attn_fp8_bwd_protected_dp(p, mq, mk, mdo, lse, do, v, o, grad_dtype=torch.float32,
+                                                   rowstats=True)
+    else:
+        _, _, _, rs = pk.attn_fp8_bwd(p, pk.DELTA_MATCHING, mq, mk, mv, mdo, lse, do, o, grad_dtype=torch.float32,
+                                      rowstats=True)
     torch.cuda.synchronize()
     P, dS, Pc, dSc, eS, eP = (t.cpu().numpy() for t in p.cast_dump_views())
     rs, lse = rs.cpu().numpy(), lse.cpu().numpy().astype(np.float64)
